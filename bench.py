@@ -1,0 +1,150 @@
+#!/usr/bin/env python3
+"""Benchmark of the MTI k-means hot path on one MI355X.
+
+A step is one Lloyd iteration with MTI pruning: centroid table and drift,
+bound update and Clause-1 test, fused distance + argmin of the survivors,
+per-cluster reduction into new centroids and the convergence counters.  The
+timed region enqueues K consecutive iterations of a run started from the
+workload's seeded initial centroids (inputs already resident in HBM) and is
+bracketed by device synchronisation; the reported value is iterations per
+second.  Per-kernel device times come from HIP events recorded by the
+library on its stream around every launch.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+DEFAULT_WORKLOAD = "aniso-8M-d16-k10"
+METRIC = "k-means iters/sec + effective dist evals/sec; % HBM peak (low d) / % MFMA (big k·d)"
+
+
+def log(msg: str) -> None:
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(X, C0, w, budget_s: float = 15.0) -> dict:
+    """Time the CPU oracle (plain float64 Lloyd's, as it stands) on this host."""
+    import oracle
+    t0 = time.perf_counter()
+    oracle.lloyd(X, C0, 1, 0.0)
+    t1 = time.perf_counter() - t0
+    iters = int(max(1, min(w.max_iters, budget_s // max(t1, 1e-3))))
+    t0 = time.perf_counter()
+    r = oracle.lloyd(X, C0, iters, 0.0)
+    el = time.perf_counter() - t0
+    ips = r["iters"] / el
+    return {
+        "value": ips, "unit": "iters/s", "cores": oracle.get_threads(), "kind": "oracle",
+        "sample": "all %d rows of %s, first %d iterations from the seeded centroids (tol ignored); "
+                  "%.3g effective dist evals/s" % (w.n, w.name, r["iters"], ips * w.n * w.k),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed iterations (default: workload max_iters)")
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures the one-GPU hot path only; --gpus %d is not supported "
+              "(this build runs on a single GPU)" % args.gpus, file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_1902_09527_amd as km
+
+    w = synth.WORKLOADS[args.workload]
+    K = args.steps or w.max_iters
+    log("workload %s: n=%d d=%d k=%d; generating" % (w.name, w.n, w.d, w.k))
+    X, C0, _ = synth.make(w.name)
+    dev = torch.device("cuda:0")
+    Xg = torch.from_numpy(X).to(dev)
+    Cg = torch.from_numpy(C0).to(dev)
+    torch.cuda.synchronize()
+
+    # Warmup: W iterations on a throwaway context (kernel load, caches, clocks).
+    if args.warmup > 0:
+        with km.KMeansMTI(Xg, Cg) as ctx:
+            for _ in range(args.warmup):
+                ctx.iterate()
+            torch.cuda.synchronize()
+    log("warmup done (%d iterations)" % args.warmup)
+
+    # Timed region: K iterations from C0.
+    ctx = km.KMeansMTI(Xg, Cg, timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        ctx.iterate()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    tm = ctx.timing()
+    hist = ctx.history()
+    st = ctx.stats()
+    ctx.close()
+    log("timed %d iterations in %.3f ms" % (K, elapsed * 1e3))
+
+    # The job as the workload defines it (tol stop), for the iteration count.
+    a, c, job = km.run(Xg, Cg, w.max_iters, w.tol)
+    torch.cuda.synchronize()
+
+    n, d, k = w.n, w.d, w.k
+    ips = K / elapsed
+    computed = int(hist["computed"].sum())
+    lloyd = n * k * K
+    assign_avg_s = tm["assign_ms"] / max(1, tm["iters"]) / 1e3
+    bytes_per_launch = n * (4 * d + 12)       # X row + assignment read + bound read/write
+    achieved = bytes_per_launch / assign_avg_s / 1e9
+    result = {
+        "metric": METRIC,
+        "value": ips,
+        "unit": "iters/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "n": n, "d": d, "k": k, "max_iters": w.max_iters, "tol": w.tol,
+                   "timed": "first %d iterations from the seeded centroids" % K},
+        "eff_dist_evals_per_s": lloyd / elapsed,
+        "computed_dist_evals_per_s": computed / elapsed,
+        "pruned_frac": 1.0 - computed / lloyd,
+        "clause1_frac": float(hist["clause1"].sum()) / (n * K),
+        "kernel_ms_per_iter": {key[:-3]: tm[key] / max(1, tm["iters"])
+                               for key in ("assign_ms", "reduce_ms", "update_ms", "table_ms")},
+        "job": {"iterations": job["iterations"], "converged": bool(job["converged"]),
+                "device_ms": job["device_ms"],
+                "iters_per_s": job["iterations"] / (job["device_ms"] / 1e3) if job["device_ms"] else None},
+        "roofline": {"kernel": "k_assign", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "bytes_per_launch": bytes_per_launch},
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        result["cpu_baseline"] = cpu_baseline(X, C0, w)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

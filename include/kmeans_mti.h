@@ -1,0 +1,167 @@
+/*
+ * kmeans_mti.h -- C ABI of the MI355X (gfx950) k-means hot path:
+ * Lloyd's k-means with Minimal Triangle Inequality (MTI) pruning.
+ *
+ * Method (Mhembere et al., "clusterNOR: A NUMA-Optimized Clustering
+ * Framework", arXiv 1902.09527):
+ *   - one iteration is the merged assignment + update step of ||Lloyd's
+ *     (section III-B): every point is assigned to its nearest centroid under
+ *     the Euclidean distance of Table I, then each centroid becomes the mean
+ *     of its members (section IV-A);
+ *   - MTI pruning (section III-C) keeps one upper bound u per point and the
+ *     centroid-to-centroid distances; a point whose bound is within half the
+ *     distance from its centroid to the nearest other centroid keeps its
+ *     assignment with no distance work (Clause 1), and single point-centroid
+ *     distances are skipped by the same test per centroid before and after
+ *     the bound is tightened (Clauses 2 and 3); after each update the bound
+ *     grows by the drift f(c) = d(c^t, c^{t-1}) of its centroid (Table I).
+ * MTI is exact: the results are those of unpruned Lloyd's.
+ *
+ * Results.  Assignment ties: the previous assignment wins an exact tie,
+ * otherwise the lowest centroid index.  A cluster with no member keeps its
+ * centroid.  Per-cluster sums are exact integer sums of the inputs in a fixed
+ * binary point (scale 2^S with S chosen at init so that no sum can
+ * overflow), so results do not depend on thread scheduling: two runs on the
+ * same inputs are bitwise identical.  Distances run in float32; a point
+ * whose best and second-best float32 distances are within the float32 error
+ * bound is decided again in float64 against float64 master centroids.
+ *
+ * Memory.  X, C0, assign_out and C_out are DEVICE pointers (HIP device
+ * memory of the current device).  X is n rows of d contiguous float32
+ * (row-major, row stride d); C0 / C_out are k rows of d float32; assign_out
+ * is n int32.  The library borrows X for the lifetime of a context (it is
+ * read every iteration and must not change) and never frees caller memory.
+ * A context owns all its scratch (bounds, assignments, float64 centroids,
+ * per-block partial sums, counters).
+ *
+ * Streams.  All device work is ordered on the hip_stream given at init
+ * (NULL = the null stream).  Calls marked "synchronizes" wait for that
+ * stream.  A context is not thread-safe: use one context per host thread.
+ *
+ * Errors.  Every int-returning entry point returns KM_OK or a negative
+ * KM_ERR_* code and never throws.  On KM_ERR_HIP the HIP runtime's message
+ * is available from kmeans_mti_last_hip_error() (per host thread).  After a
+ * failed init *out is NULL.  A context whose device work failed returns
+ * KM_ERR_STATE from later calls except kmeans_mti_destroy.
+ */
+#ifndef KMEANS_MTI_H
+#define KMEANS_MTI_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct km_ctx km_ctx;
+
+enum {
+    KM_OK = 0,
+    KM_ERR_INVALID_ARG = -1,   /* null pointer, bad size, k > n, tol < 0 or NaN, n*d overflow */
+    KM_ERR_OOM = -2,           /* a device or host allocation failed */
+    KM_ERR_HIP = -3,           /* a HIP runtime call failed; see kmeans_mti_last_hip_error() */
+    KM_ERR_UNSUPPORTED = -4,   /* no kernel path handles this shape */
+    KM_ERR_STATE = -5,         /* context is unusable (earlier device failure) */
+    KM_ERR_NONFINITE = -6      /* KM_FLAG_VALIDATE: X or C0 holds a NaN or an infinity */
+};
+
+enum {
+    KM_FLAG_NO_PRUNE = 1u,     /* compute all k distances every iteration (plain Lloyd's) */
+    KM_FLAG_STATS = 2u,        /* also accumulate the inertia sum_i ||x_i - c_{a_i}||^2 */
+    KM_FLAG_VALIDATE = 4u,     /* reject non-finite X or C0 at init with KM_ERR_NONFINITE */
+    KM_FLAG_TIMING = 8u        /* record HIP events around every kernel (kmeans_mti_get_timing) */
+};
+
+/* Totals over the iterations run so far (kmeans_mti_get_stats, kmeans_mti_run). */
+typedef struct {
+    int32_t iterations;        /* assignment steps executed */
+    int32_t converged;         /* run only: 1 if it stopped on the tol test before max_iters */
+    int64_t changed_last;      /* points whose assignment changed in the last step */
+    int64_t dist_computed;     /* float32 point-centroid distances evaluated, tightenings included */
+    int64_t dist_lloyd;        /* n * k * iterations: what unpruned Lloyd's evaluates */
+    int64_t clause1_skips;     /* point-iterations skipped whole by Clause 1 */
+    int64_t rechecks;          /* points decided again in float64 (near ties) */
+    double inertia_last;       /* last step's inertia (float32 distances summed exactly); NaN without KM_FLAG_STATS */
+    double device_ms;          /* run only: device time of the iteration loop (HIP events); else 0 */
+} km_stats;
+
+/*
+ * Create a context for one k-means problem and compute the centroid table of
+ * C0.  X: device, n x d float32, borrowed until kmeans_mti_destroy.  C0:
+ * device, k x d float32, copied (may be freed after the call).  Requires
+ * n >= 1, 1 <= d, 1 <= k <= n.  hip_stream: a hipStream_t or NULL.  flags:
+ * KM_FLAG_*.  Synchronizes.  On success *out owns the context.
+ */
+int kmeans_mti_init(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t k,
+                    const float* C0, void* hip_stream, uint32_t flags);
+
+/*
+ * Enqueue one iteration: the assignment step with MTI pruning, then the
+ * update of the centroids, their drift and their distance table (one
+ * ||Lloyd's iteration, section III-B).  Asynchronous unless changed_out is
+ * non-NULL, in which case it synchronizes and stores the number of points
+ * whose assignment changed in this step (n in the first step).
+ */
+int kmeans_mti_iterate(km_ctx* ctx, int64_t* changed_out);
+
+/*
+ * Copy the current state into caller device buffers (either may be NULL):
+ * assign_out (n int32) = assignment of the last step, C_out (k x d float32)
+ * = centroids after the last update (C0 before the first iteration).
+ * Stream-ordered, asynchronous.  KM_ERR_STATE before the first iteration
+ * when assign_out is non-NULL.
+ */
+int kmeans_mti_get(km_ctx* ctx, int32_t* assign_out, float* C_out);
+
+/* Copy the float64 master centroids (k x d) into a HOST buffer.  Synchronizes. */
+int kmeans_mti_get_centroids64(km_ctx* ctx, double* C_out);
+
+/* Totals over the iterations run so far.  Synchronizes. */
+int kmeans_mti_get_stats(km_ctx* ctx, km_stats* stats);
+
+/*
+ * Per-iteration history into HOST arrays of length cap (any may be NULL):
+ * changed, distances computed, Clause-1 skips, float64 rechecks, inertia
+ * (NaN without KM_FLAG_STATS).  Returns the number of iterations written
+ * (min(iterations, cap, 4096): the context keeps the last 4096), or a
+ * negative KM_ERR_*.  Synchronizes.
+ */
+int kmeans_mti_get_history(km_ctx* ctx, int64_t* changed, int64_t* computed, int64_t* clause1,
+                           int64_t* rechecks, double* inertia, int32_t cap);
+
+/*
+ * Device time per kernel over the iterations enqueued so far, measured with
+ * HIP events recorded on the context's stream around every launch (needs
+ * KM_FLAG_TIMING at init).  ms (HOST, 4 doubles) receives the total
+ * milliseconds of the assignment, reduction, update and centroid-table
+ * kernels; *iters (nullable) the number of iterations timed.  Synchronizes.
+ * KM_ERR_STATE without KM_FLAG_TIMING.
+ */
+int kmeans_mti_get_timing(km_ctx* ctx, double* ms, int64_t* iters);
+
+/*
+ * Whole run (the paper's base::run): iterate from C0 until fewer than
+ * tol * n points change assignment in a step (checked after that step's
+ * update; tol = 0 runs all steps) or max_iters steps ran.  Outputs as in
+ * kmeans_mti_get.  All iterations are enqueued without host round trips;
+ * steps after convergence return at once.  Synchronizes once at the end.
+ * stats: HOST pointer, may be NULL.
+ */
+int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float* C0,
+                   int32_t max_iters, double tol, int32_t* assign_out, float* C_out,
+                   void* hip_stream, uint32_t flags, km_stats* stats);
+
+/* Release a context and its device scratch.  NULL-safe.  Synchronizes. */
+void kmeans_mti_destroy(km_ctx* ctx);
+
+/* Static text for a KM_* status code. */
+const char* kmeans_mti_strerror(int status);
+
+/* Text of the last HIP error seen on this host thread ("" if none). */
+const char* kmeans_mti_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KMEANS_MTI_H */

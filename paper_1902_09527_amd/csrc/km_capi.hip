@@ -1,0 +1,531 @@
+// C-ABI host side of the MTI k-means hot path: argument checks, scratch
+// ownership, launch configuration, the run loop and error reporting.  The
+// declarations and their contracts are in include/kmeans_mti.h.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <climits>
+#include <new>
+
+#include "kmeans_mti.h"
+#include "km_internal.h"
+
+namespace {
+
+thread_local char g_last_hip[256] = "";
+
+int hip_fail(hipError_t e, const char* what) {
+    snprintf(g_last_hip, sizeof g_last_hip, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+    return e == hipErrorOutOfMemory ? KM_ERR_OOM : KM_ERR_HIP;
+}
+
+#define KM_HIP(call)                                  \
+    do {                                              \
+        hipError_t e_ = (call);                       \
+        if (e_ != hipSuccess) return hip_fail(e_, #call); \
+    } while (0)
+
+int ceil_log2_u64(uint64_t v) {
+    int c = 0;
+    while (c < 64 && (1ull << c) < v) ++c;
+    return c;
+}
+
+// Checks that [p, p + bytes) lies inside one device allocation of the
+// current device, so that a host pointer or a short buffer is refused here
+// instead of faulting in a kernel.
+int check_device_range(const void* p, size_t bytes, int device, const char* what) {
+    hipPointerAttribute_t attr;
+    hipError_t e = hipPointerGetAttributes(&attr, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        snprintf(g_last_hip, sizeof g_last_hip, "%s is not a HIP device pointer", what);
+        return KM_ERR_INVALID_ARG;
+    }
+    if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged) {
+        snprintf(g_last_hip, sizeof g_last_hip, "%s is not device memory", what);
+        return KM_ERR_INVALID_ARG;
+    }
+    if (attr.device != device) {
+        snprintf(g_last_hip, sizeof g_last_hip, "%s is on device %d, current device is %d", what,
+                 attr.device, device);
+        return KM_ERR_INVALID_ARG;
+    }
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    e = hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return KM_OK;   // range unknown (e.g. managed memory): trust the caller
+    }
+    const uintptr_t lo = (uintptr_t)base, hi = lo + size, q = (uintptr_t)p;
+    if (q < lo || q + bytes > hi) {
+        snprintf(g_last_hip, sizeof g_last_hip, "%s: buffer too small (%zu bytes needed)", what,
+                 bytes);
+        return KM_ERR_INVALID_ARG;
+    }
+    return KM_OK;
+}
+
+}  // namespace
+
+struct km_ctx {
+    int64_t n = 0;
+    int32_t d = 0, k = 0;
+    uint32_t flags = 0;
+    hipStream_t stream = nullptr;
+    int device = 0;
+    int tp = 0, lds = 0;
+    int variant = 0;   // assignment-kernel specialisation
+    km::Dev dv{};
+    void* bufs[16] = {};
+    int nbufs = 0;
+    bool broken = false;
+    bool stepped = false;
+
+    // KM_FLAG_TIMING: events around the four launches of each iteration,
+    // harvested into per-kernel totals when the pool fills or on request.
+    static constexpr int kEvIters = 256;
+    bool timing = false;
+    hipEvent_t ev[kEvIters][5] = {};
+    int ev_used = 0;
+    double t_ms[4] = {0, 0, 0, 0};
+    int64_t t_iters = 0;
+
+    template <class T>
+    int alloc(T** p, size_t count) {
+        void* q = nullptr;
+        hipError_t e = hipMalloc(&q, count * sizeof(T) > 0 ? count * sizeof(T) : 16);
+        if (e != hipSuccess) return hip_fail(e, "hipMalloc");
+        bufs[nbufs++] = q;
+        *p = static_cast<T*>(q);
+        return KM_OK;
+    }
+    ~km_ctx() {
+        (void)hipStreamSynchronize(stream);
+        for (int i = 0; i < nbufs; ++i) (void)hipFree(bufs[i]);
+        for (auto& row : ev)
+            for (auto& e : row)
+                if (e) (void)hipEventDestroy(e);
+    }
+};
+
+namespace {
+
+int fail_ctx(km_ctx* c, int rc) {
+    if (c) c->broken = true;
+    return rc;
+}
+
+// Accumulate the elapsed times of the recorded iterations and free the pool.
+int harvest_timing(km_ctx* c) {
+    if (!c->timing || c->ev_used == 0) return KM_OK;
+    hipError_t e = hipEventSynchronize(c->ev[c->ev_used - 1][4]);
+    if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventSynchronize"));
+    for (int i = 0; i < c->ev_used; ++i)
+        for (int s = 0; s < 4; ++s) {
+            float ms = 0.f;
+            e = hipEventElapsedTime(&ms, c->ev[i][s], c->ev[i][s + 1]);
+            if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventElapsedTime"));
+            c->t_ms[s] += ms;
+        }
+    c->t_iters += c->ev_used;
+    c->ev_used = 0;
+    return KM_OK;
+}
+
+int enqueue_iteration(km_ctx* c) {
+    hipError_t e;
+    hipEvent_t* ev = nullptr;
+    if (c->timing) {
+        if (c->ev_used == km_ctx::kEvIters) {
+            int rc = harvest_timing(c);
+            if (rc != KM_OK) return rc;
+        }
+        ev = c->ev[c->ev_used++];
+    }
+    auto mark = [&](int i) -> hipError_t { return ev ? hipEventRecord(ev[i], c->stream) : hipSuccess; };
+    if ((e = mark(0)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
+    if ((e = km::launch_assign(c->dv, c->variant, c->tp, c->lds, c->stream)) != hipSuccess)
+        return fail_ctx(c, hip_fail(e, "assign kernel"));
+    if ((e = mark(1)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
+    if ((e = km::launch_reduce(c->dv, c->stream)) != hipSuccess)
+        return fail_ctx(c, hip_fail(e, "reduce kernel"));
+    if ((e = mark(2)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
+    if ((e = km::launch_update(c->dv, c->stream)) != hipSuccess)
+        return fail_ctx(c, hip_fail(e, "update kernel"));
+    if ((e = mark(3)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
+    if ((e = km::launch_centroid_table(c->dv, 0, c->stream)) != hipSuccess)
+        return fail_ctx(c, hip_fail(e, "centroid table kernel"));
+    if ((e = mark(4)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
+    c->stepped = true;
+    return KM_OK;
+}
+
+int read_state(km_ctx* c, km::IterState* out) {
+    hipError_t e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "hipStreamSynchronize"));
+    e = hipMemcpy(out, c->dv.st, sizeof(km::IterState), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "hipMemcpy state"));
+    return KM_OK;
+}
+
+int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const float* C0) {
+    KM_HIP(hipGetDevice(&c->device));
+    int rc;
+    if ((rc = check_device_range(X, (size_t)n * (size_t)d * sizeof(float), c->device, "X")) != KM_OK)
+        return rc;
+    if ((rc = check_device_range(C0, (size_t)k * (size_t)d * sizeof(float), c->device, "C0")) != KM_OK)
+        return rc;
+
+    int cus = 0, max_lds = 0;
+    KM_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, c->device));
+    KM_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device));
+
+    // Tile size: the largest of 256/128/64 points whose LDS image fits.
+    c->tp = 0;
+    for (int tp = 256; tp >= 64; tp /= 2) {
+        int bytes = km::assign_lds(d, k, tp).bytes;
+        if (bytes <= max_lds) {
+            c->tp = tp;
+            c->lds = bytes;
+            break;
+        }
+    }
+    if (c->tp == 0) {
+        snprintf(g_last_hip, sizeof g_last_hip,
+                 "k*d = %lld too large for the LDS-resident centroid path (%d bytes of LDS)",
+                 (long long)k * d, max_lds);
+        return KM_ERR_UNSUPPORTED;
+    }
+    c->variant = km::assign_variant(d);
+    if (reinterpret_cast<uintptr_t>(X) % 16 != 0) c->variant = 0;
+    const void* sym = km::assign_kernel_symbol(c->variant);
+    KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds));
+    int per_cu = 0;
+    KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, c->tp, c->lds));
+    if (per_cu < 1) return KM_ERR_UNSUPPORTED;
+    const int64_t ntiles = (n + c->tp - 1) / c->tp;
+    int64_t G = (int64_t)per_cu * cus;
+    if (G > ntiles) G = ntiles;
+
+    km::Dev& v = c->dv;
+    v.X = X;
+    v.n = n;
+    v.d = d;
+    v.k = k;
+    v.G = (int32_t)G;
+    v.L = km::row_len(d, k);
+    v.flags = c->flags;
+    v.gamma = (float)((d + 4) * 0x1p-23);
+    if ((rc = c->alloc(&v.a, (size_t)n)) || (rc = c->alloc(&v.u, (size_t)n)) ||
+        (rc = c->alloc(&v.C64, (size_t)k * d)) || (rc = c->alloc(&v.C32, (size_t)k * d)) ||
+        (rc = c->alloc(&v.ec, (size_t)k)) || (rc = c->alloc(&v.h, (size_t)k * k)) ||
+        (rc = c->alloc(&v.s, (size_t)k)) || (rc = c->alloc(&v.f, (size_t)k)) ||
+        (rc = c->alloc(&v.part, (size_t)G * v.L)) || (rc = c->alloc(&v.total, (size_t)v.L)) ||
+        (rc = c->alloc(&v.st, 1)) || (rc = c->alloc(&v.rec, (size_t)km::kHistCap)))
+        return rc;
+    uint32_t* scratch = nullptr;
+    if ((rc = c->alloc(&scratch, 4))) return rc;
+
+    // Largest magnitude of X and C0 (and non-finite detection) -> fixed-point scales.
+    KM_HIP(hipMemsetAsync(scratch, 0, 4 * sizeof(uint32_t), c->stream));
+    KM_HIP(km::launch_absmax(X, n * d, scratch, reinterpret_cast<int32_t*>(scratch + 1), c->stream));
+    KM_HIP(km::launch_absmax(C0, (int64_t)k * d, scratch + 2, reinterpret_cast<int32_t*>(scratch + 3),
+                             c->stream));
+    uint32_t host[4];
+    KM_HIP(hipMemcpyAsync(host, scratch, sizeof host, hipMemcpyDeviceToHost, c->stream));
+    KM_HIP(hipStreamSynchronize(c->stream));
+    if ((c->flags & KM_FLAG_VALIDATE) && (host[1] || host[3])) return KM_ERR_NONFINITE;
+    float xmax, cmax;
+    memcpy(&xmax, &host[0], 4);
+    memcpy(&cmax, &host[2], 4);
+    int ex = 0, ec0 = 0;
+    if (xmax > 0) frexp((double)xmax, &ex);   // xmax <= 2^ex
+    // Coordinate sums: |x * 2^S| <= 2^50 per point and n * 2^(ex+S) <= 2^61 overall.
+    const int lgn = ceil_log2_u64((uint64_t)n);
+    int S = 61 - lgn - ex;
+    if (S > 50 - ex) S = 50 - ex;
+    v.qscale = ldexp(1.0, S);
+    v.qinv = ldexp(1.0, -S);
+    // Inertia: every squared distance is <= d * (2 * max|coordinate|)^2.
+    const double amax = xmax > cmax ? (double)xmax : (double)cmax;
+    const double dmax = (double)d * 4.0 * amax * amax;
+    int eD = 0;
+    if (dmax > 0) frexp(dmax, &eD);
+    (void)ec0;
+    int SI = 61 - lgn - eD;
+    if (SI > 50 - eD) SI = 50 - eD;
+    v.iscale = ldexp(1.0, SI);
+    v.iinv = ldexp(1.0, -SI);
+
+    if (c->flags & KM_FLAG_TIMING) {
+        c->timing = true;
+        for (auto& row : c->ev)
+            for (auto& e : row) KM_HIP(hipEventCreate(&e));
+    }
+
+    km::IterState st0{};
+    st0.max_iters = INT_MAX;
+    st0.tol_n = -1.0;
+    KM_HIP(hipMemcpyAsync(v.st, &st0, sizeof st0, hipMemcpyHostToDevice, c->stream));
+    KM_HIP(hipMemsetAsync(v.total, 0, sizeof(uint64_t) * (size_t)v.L, c->stream));
+    KM_HIP(hipMemsetAsync(v.rec, 0, sizeof(km::IterRec) * km::kHistCap, c->stream));
+    KM_HIP(km::launch_set_centroids(C0, v.C64, v.C32, v.ec, (int64_t)k * d, k, c->stream));
+    KM_HIP(km::launch_centroid_table(v, 1, c->stream));
+    KM_HIP(hipStreamSynchronize(c->stream));
+    return KM_OK;
+}
+
+int check_shape(const float* X, int64_t n, int32_t d, int32_t k, const float* C0) {
+    if (!X || !C0 || n < 1 || d < 1 || k < 1 || k > n) return KM_ERR_INVALID_ARG;
+    if (n > INT64_MAX / 4 / d) return KM_ERR_INVALID_ARG;                     // n*d*4 overflow
+    if ((int64_t)k * d + k + km::kNumStat > INT_MAX / 8) return KM_ERR_INVALID_ARG;
+    return KM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kmeans_mti_init(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t k, const float* C0,
+                    void* hip_stream, uint32_t flags) {
+    if (!out) return KM_ERR_INVALID_ARG;
+    *out = nullptr;
+    int rc = check_shape(X, n, d, k, C0);
+    if (rc != KM_OK) return rc;
+    if (flags & ~(uint32_t)(KM_FLAG_NO_PRUNE | KM_FLAG_STATS | KM_FLAG_VALIDATE | KM_FLAG_TIMING))
+        return KM_ERR_INVALID_ARG;
+    km_ctx* c = new (std::nothrow) km_ctx;
+    if (!c) return KM_ERR_OOM;
+    c->n = n;
+    c->d = d;
+    c->k = k;
+    c->flags = flags;
+    c->stream = static_cast<hipStream_t>(hip_stream);
+    rc = init_impl(c, X, n, d, k, C0);
+    if (rc != KM_OK) {
+        delete c;
+        return rc;
+    }
+    *out = c;
+    return KM_OK;
+}
+
+int kmeans_mti_iterate(km_ctx* ctx, int64_t* changed_out) {
+    if (!ctx) return KM_ERR_INVALID_ARG;
+    if (ctx->broken) return KM_ERR_STATE;
+    int rc = enqueue_iteration(ctx);
+    if (rc != KM_OK) return rc;
+    if (changed_out) {
+        km::IterState st;
+        if ((rc = read_state(ctx, &st)) != KM_OK) return rc;
+        *changed_out = st.changed_last;
+    }
+    return KM_OK;
+}
+
+int kmeans_mti_get(km_ctx* ctx, int32_t* assign_out, float* C_out) {
+    if (!ctx) return KM_ERR_INVALID_ARG;
+    if (ctx->broken) return KM_ERR_STATE;
+    if (assign_out && !ctx->stepped) return KM_ERR_STATE;
+    int rc;
+    if (assign_out &&
+        (rc = check_device_range(assign_out, (size_t)ctx->n * 4, ctx->device, "assign_out")) != KM_OK)
+        return rc;
+    if (C_out && (rc = check_device_range(C_out, (size_t)ctx->k * ctx->d * 4, ctx->device, "C_out")) !=
+                     KM_OK)
+        return rc;
+    hipError_t e;
+    if (assign_out &&
+        (e = hipMemcpyAsync(assign_out, ctx->dv.a, (size_t)ctx->n * sizeof(int32_t),
+                            hipMemcpyDeviceToDevice, ctx->stream)) != hipSuccess)
+        return fail_ctx(ctx, hip_fail(e, "hipMemcpyAsync assign"));
+    if (C_out &&
+        (e = hipMemcpyAsync(C_out, ctx->dv.C32, (size_t)ctx->k * ctx->d * sizeof(float),
+                            hipMemcpyDeviceToDevice, ctx->stream)) != hipSuccess)
+        return fail_ctx(ctx, hip_fail(e, "hipMemcpyAsync centroids"));
+    return KM_OK;
+}
+
+int kmeans_mti_get_centroids64(km_ctx* ctx, double* C_out) {
+    if (!ctx || !C_out) return KM_ERR_INVALID_ARG;
+    if (ctx->broken) return KM_ERR_STATE;
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess) return fail_ctx(ctx, hip_fail(e, "hipStreamSynchronize"));
+    e = hipMemcpy(C_out, ctx->dv.C64, (size_t)ctx->k * ctx->d * sizeof(double), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail_ctx(ctx, hip_fail(e, "hipMemcpy centroids"));
+    return KM_OK;
+}
+
+static void fill_stats(const km_ctx* c, const km::IterState& st, km_stats* s) {
+    s->iterations = st.t;
+    s->converged = st.converged;
+    s->changed_last = st.changed_last;
+    s->dist_computed = st.tot_computed;
+    s->dist_lloyd = c->n * (int64_t)c->k * st.t;
+    s->clause1_skips = st.tot_clause1;
+    s->rechecks = st.tot_rechecks;
+    s->inertia_last = (c->flags & KM_FLAG_STATS) && st.t > 0 ? st.inertia_last : NAN;
+    s->device_ms = 0.0;
+}
+
+int kmeans_mti_get_stats(km_ctx* ctx, km_stats* stats) {
+    if (!ctx || !stats) return KM_ERR_INVALID_ARG;
+    if (ctx->broken) return KM_ERR_STATE;
+    km::IterState st;
+    int rc = read_state(ctx, &st);
+    if (rc != KM_OK) return rc;
+    fill_stats(ctx, st, stats);
+    return KM_OK;
+}
+
+int kmeans_mti_get_history(km_ctx* ctx, int64_t* changed, int64_t* computed, int64_t* clause1,
+                           int64_t* rechecks, double* inertia, int32_t cap) {
+    if (!ctx || cap < 0) return KM_ERR_INVALID_ARG;
+    if (ctx->broken) return KM_ERR_STATE;
+    km::IterState st;
+    int rc = read_state(ctx, &st);
+    if (rc != KM_OK) return rc;
+    int m = st.t < cap ? st.t : cap;
+    if (m > km::kHistCap) m = km::kHistCap;
+    if (m == 0) return 0;
+    km::IterRec* rec = new (std::nothrow) km::IterRec[km::kHistCap];
+    if (!rec) return KM_ERR_OOM;
+    hipError_t e = hipMemcpy(rec, ctx->dv.rec, sizeof(km::IterRec) * km::kHistCap, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) {
+        delete[] rec;
+        return fail_ctx(ctx, hip_fail(e, "hipMemcpy history"));
+    }
+    for (int i = 0; i < m; ++i) {
+        const km::IterRec& r = rec[(st.t - m + i) % km::kHistCap];
+        if (changed) changed[i] = r.changed;
+        if (computed) computed[i] = r.computed;
+        if (clause1) clause1[i] = r.clause1;
+        if (rechecks) rechecks[i] = r.rechecks;
+        if (inertia) inertia[i] = (ctx->flags & KM_FLAG_STATS) ? r.inertia : NAN;
+    }
+    delete[] rec;
+    return m;
+}
+
+int kmeans_mti_get_timing(km_ctx* ctx, double* ms, int64_t* iters) {
+    if (!ctx || !ms) return KM_ERR_INVALID_ARG;
+    if (ctx->broken) return KM_ERR_STATE;
+    if (!ctx->timing) return KM_ERR_STATE;
+    int rc = harvest_timing(ctx);
+    if (rc != KM_OK) return rc;
+    for (int s = 0; s < 4; ++s) ms[s] = ctx->t_ms[s];
+    if (iters) *iters = ctx->t_iters;
+    return KM_OK;
+}
+
+int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float* C0, int32_t max_iters,
+                   double tol, int32_t* assign_out, float* C_out, void* hip_stream, uint32_t flags,
+                   km_stats* stats) {
+    if (max_iters < 1 || !(tol >= 0.0) || !assign_out || !C_out) return KM_ERR_INVALID_ARG;
+    int rc = check_shape(X, n, d, k, C0);
+    if (rc != KM_OK) return rc;
+    int dev = 0;
+    hipError_t e0 = hipGetDevice(&dev);
+    if (e0 != hipSuccess) return hip_fail(e0, "hipGetDevice");
+    if ((rc = check_device_range(assign_out, (size_t)n * 4, dev, "assign_out")) != KM_OK) return rc;
+    if ((rc = check_device_range(C_out, (size_t)k * d * 4, dev, "C_out")) != KM_OK) return rc;
+    km_ctx* c = nullptr;
+    if ((rc = kmeans_mti_init(&c, X, n, d, k, C0, hip_stream, flags)) != KM_OK) return rc;
+
+    hipEvent_t ev0 = nullptr, ev1 = nullptr, evc[2] = {nullptr, nullptr};
+    int32_t* pinned = nullptr;
+    float ms = 0.f;
+    auto cleanup = [&]() {
+        if (ev0) (void)hipEventDestroy(ev0);
+        if (ev1) (void)hipEventDestroy(ev1);
+        for (auto& e : evc)
+            if (e) (void)hipEventDestroy(e);
+        if (pinned) (void)hipHostFree(pinned);
+        kmeans_mti_destroy(c);
+    };
+#define RUN_HIP(call)                                   \
+    do {                                                \
+        hipError_t e_ = (call);                         \
+        if (e_ != hipSuccess) {                         \
+            int r_ = hip_fail(e_, #call);               \
+            cleanup();                                  \
+            return r_;                                  \
+        }                                               \
+    } while (0)
+
+    km::IterState st0{};
+    st0.max_iters = max_iters;
+    st0.tol_n = tol * (double)n;
+    RUN_HIP(hipMemcpyAsync(c->dv.st, &st0, sizeof st0, hipMemcpyHostToDevice, c->stream));
+    RUN_HIP(hipEventCreate(&ev0));
+    RUN_HIP(hipEventCreate(&ev1));
+    RUN_HIP(hipEventCreateWithFlags(&evc[0], hipEventDisableTiming));
+    RUN_HIP(hipEventCreateWithFlags(&evc[1], hipEventDisableTiming));
+    RUN_HIP(hipHostMalloc(reinterpret_cast<void**>(&pinned), 2 * sizeof(int32_t), hipHostMallocDefault));
+    pinned[0] = pinned[1] = 0;
+
+    // Enqueue chunks of iterations; the device stop flag makes surplus
+    // launches return at once.  The host polls the flag one chunk behind,
+    // so at most two chunks are enqueued past convergence.
+    const int chunk = 4;
+    RUN_HIP(hipEventRecord(ev0, c->stream));
+    int enq = 0, ci = 0;
+    while (enq < max_iters) {
+        const int m = max_iters - enq < chunk ? max_iters - enq : chunk;
+        for (int i = 0; i < m; ++i) {
+            if ((rc = enqueue_iteration(c)) != KM_OK) {
+                cleanup();
+                return rc;
+            }
+        }
+        enq += m;
+        RUN_HIP(hipMemcpyAsync(&pinned[ci & 1], &c->dv.st->done, sizeof(int32_t), hipMemcpyDeviceToHost,
+                               c->stream));
+        RUN_HIP(hipEventRecord(evc[ci & 1], c->stream));
+        if (ci >= 1) {
+            RUN_HIP(hipEventSynchronize(evc[(ci - 1) & 1]));
+            if (pinned[(ci - 1) & 1]) break;
+        }
+        ++ci;
+    }
+    RUN_HIP(hipEventRecord(ev1, c->stream));
+    if ((rc = kmeans_mti_get(c, assign_out, C_out)) != KM_OK) {
+        cleanup();
+        return rc;
+    }
+    km::IterState st;
+    if ((rc = read_state(c, &st)) != KM_OK) {
+        cleanup();
+        return rc;
+    }
+    RUN_HIP(hipEventElapsedTime(&ms, ev0, ev1));
+    if (stats) {
+        fill_stats(c, st, stats);
+        stats->device_ms = ms;
+    }
+    cleanup();
+    return KM_OK;
+#undef RUN_HIP
+}
+
+void kmeans_mti_destroy(km_ctx* ctx) { delete ctx; }
+
+const char* kmeans_mti_strerror(int status) {
+    switch (status) {
+        case KM_OK: return "ok";
+        case KM_ERR_INVALID_ARG: return "invalid argument";
+        case KM_ERR_OOM: return "out of memory";
+        case KM_ERR_HIP: return "HIP runtime error";
+        case KM_ERR_UNSUPPORTED: return "unsupported shape";
+        case KM_ERR_STATE: return "context unusable";
+        case KM_ERR_NONFINITE: return "non-finite input";
+        default: return "unknown status";
+    }
+}
+
+const char* kmeans_mti_last_hip_error(void) { return g_last_hip; }
+
+}  // extern "C"

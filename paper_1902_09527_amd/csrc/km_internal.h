@@ -1,0 +1,124 @@
+// Internal declarations shared by the kernels (km_kernels.hip) and the C-ABI
+// host code (km_capi.hip).  Not installed; the public interface is
+// include/kmeans_mti.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace km {
+
+// Float64 rounding constant 1.5 * 2^52: for |v| < 2^51, fma(x, scale, kMagic)
+// rounds x*scale to the nearest integer q and stores it in the low mantissa
+// bits, so bits(result) = kMagicBits + q.  This gives an exact integer image
+// of each input in two instructions, and sums of images are exact.
+constexpr double kMagic = 6755399441055744.0;
+constexpr uint64_t kMagicBits = 0x4338000000000000ull;
+
+constexpr int kHistCap = 4096;   // per-iteration records kept (ring)
+constexpr int kNumStat = 5;      // per-block counters appended to each partial row
+
+// Partial-row layout (uint64 words): [0, k*d) coordinate sums (cluster-major),
+// [k*d, k*d + k) member counts, then the counters below.
+enum StatCol { kStChanged = 0, kStComputed = 1, kStClause1 = 2, kStRecheck = 3, kStInertia = 4 };
+
+struct IterRec {
+    int64_t changed, computed, clause1, rechecks;
+    double inertia;   // NaN unless inertia is collected
+};
+
+// Device-resident loop state.  Written only by the kernels named per field.
+struct IterState {
+    int32_t t;            // steps completed (update kernel)
+    int32_t done;         // stop test met (update kernel); read by the next step
+    int32_t active;       // 1 if the current step runs (assignment kernel)
+    int32_t converged;    // stopped on the tol test (update kernel)
+    int32_t max_iters;    // stop after this many steps (host, at init)
+    int32_t pad_;
+    double tol_n;         // stop when changed < tol_n; negative: never (host)
+    int64_t changed_last; // update kernel
+    int64_t tot_computed, tot_clause1, tot_rechecks;   // update kernel
+    double inertia_last;  // update kernel
+    float ec_max;         // max_j ||c32_j - c64_j|| (centroid-table kernel)
+    float pad2_;
+};
+
+// Everything the kernels need, passed by value.
+struct Dev {
+    const float* X;
+    int64_t n;
+    int32_t d, k;
+    int32_t* a;           // n assignments
+    float* u;             // n upper bounds
+    double* C64;          // k*d master centroids
+    float* C32;           // k*d float32 copy used for distances
+    float* ec;            // k: ||c32_j - c64_j|| rounded up
+    float* h;             // k*k: half centroid distances rounded down
+    float* s;             // k: min_{j != i} h[i][j] rounded down (+inf if k == 1)
+    float* f;             // k: drift ||c_j^t - c_j^{t-1}|| rounded up
+    uint64_t* part;       // G x L per-block partial rows
+    uint64_t* total;      // L reduced row (zero between iterations)
+    IterState* st;
+    IterRec* rec;
+    int32_t G;            // assignment blocks = partial rows
+    int32_t L;            // partial row length
+    double qscale, qinv;  // 2^S, 2^-S: fixed-point scale of coordinate sums
+    double iscale, iinv;  // fixed-point scale of the inertia sum
+    float gamma;          // relative error bound of a float32 squared distance, d-dependent
+    uint32_t flags;
+};
+
+inline int row_len(int d, int k) { return k * d + k + kNumStat; }
+
+// Padded LDS row stride of the X tile: 16-byte aligned rows, offset by 4
+// floats so that 16-byte row reads of consecutive lanes spread over banks.
+__host__ __device__ inline int xs_stride(int d) { return ((d + 3) / 4) * 4 + 4; }
+
+// Dynamic LDS layout of the assignment kernel for tile size tp.
+struct AssignLds {
+    int off_acc, off_cnt, off_c, off_f, off_s, off_ec, off_x, off_sa, off_su, off_sd, off_sq,
+        off_misc, bytes;
+};
+
+__host__ __device__ inline AssignLds assign_lds(int d, int k, int tp) {
+    AssignLds L;
+    int o = 0;
+    auto take = [&](int bytes, int align) {
+        o = (o + align - 1) / align * align;
+        int r = o;
+        o += bytes;
+        return r;
+    };
+    L.off_acc = take(8 * k * d, 16);
+    L.off_cnt = take(4 * k, 16);
+    L.off_c = take(4 * k * d, 16);
+    L.off_f = take(4 * k, 16);
+    L.off_s = take(4 * k, 16);
+    L.off_ec = take(4 * k, 16);
+    L.off_x = take(4 * tp * xs_stride(d), 16);
+    L.off_sa = take(4 * tp, 16);
+    L.off_su = take(4 * tp, 16);
+    L.off_sd = take(4 * tp, 16);
+    L.off_sq = take(4 * tp, 16);
+    L.off_misc = take(64, 16);   // queue length (int) at 0, kNumStat uint64 counters at 16
+    L.bytes = (o + 15) / 16 * 16;
+    return L;
+}
+
+// Kernel launchers (km_kernels.hip).  Each returns the launch status.
+hipError_t launch_absmax(const float* X, int64_t count, uint32_t* absmax_bits, int32_t* nonfinite,
+                         hipStream_t s);
+hipError_t launch_set_centroids(const float* C0, double* C64, float* C32, float* ec, int64_t kd,
+                                int32_t k, hipStream_t s);
+hipError_t launch_assign(const Dev& dv, int variant, int tp, int lds_bytes, hipStream_t s);
+hipError_t launch_reduce(const Dev& dv, hipStream_t s);
+hipError_t launch_update(const Dev& dv, hipStream_t s);
+hipError_t launch_centroid_table(const Dev& dv, int force, hipStream_t s);
+
+// Compile-time dimension specialisation for d (0 = generic); the
+// specialisations read X with 16-byte loads and need a 16-byte aligned X.
+int assign_variant(int d);
+// Kernel symbol of an assignment-kernel variant (for occupancy queries).
+const void* assign_kernel_symbol(int variant);
+
+}  // namespace km

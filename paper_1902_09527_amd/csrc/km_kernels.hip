@@ -1,0 +1,586 @@
+// HIP kernels of the MTI k-means hot path for gfx950 (MI355X).
+//
+// One iteration (one merged ||Lloyd's MM step, paper section III-B) is four
+// stream-ordered launches, none of which needs the host:
+//   k_assign          Clause-1 test on the drift-updated bound, fused float32
+//                     distance + argmin for the surviving points with the
+//                     per-centroid Clause 2/3 skips, and the per-block
+//                     fixed-point partial sums/counts of ALL points
+//                     (section III-C; section V "per-thread local centroids");
+//   k_reduce          sums the per-block partial rows (integer, exact);
+//   k_update          new centroids (member means, empty clusters kept),
+//                     drift f(c) (Table I), loop counters and the stop test;
+//   k_centroid_table  half centroid-to-centroid distances h and
+//                     s(c) = min_{c' != c} h(c, c') for the next step.
+// Every kernel first reads the device loop state and returns at once when
+// the run has stopped, so a whole run can be enqueued up front.
+#include <float.h>
+#include <math.h>
+
+#include "kmeans_mti.h"
+#include "km_internal.h"
+
+namespace km {
+
+namespace {
+
+constexpr float kUp = 1.0f + 0x1p-22f;   // covers one float32 rounding, upward
+
+// Largest float <= v and smallest float >= v.
+__device__ inline float f32_down(double v) {
+    float r = (float)v;
+    if ((double)r > v) r = nextafterf(r, -INFINITY);
+    return r;
+}
+__device__ inline float f32_up(double v) {
+    float r = (float)v;
+    if ((double)r < v) r = nextafterf(r, INFINITY);
+    return r;
+}
+
+// Upper bound on the exact distance to the float64 centroid from a float32
+// squared distance D (relative error <= gamma) and the centroid's float32
+// rounding error ec.
+__device__ inline float upper_bound(float D, float ec, float gamma) {
+    return (sqrtf(D) * (1.0f + gamma) + ec) * kUp;
+}
+
+// Exact integer image of v * scale (|v * scale| < 2^51), offset by kMagicBits.
+__device__ inline uint64_t fixed_bits(double v, double scale) {
+    return (uint64_t)__double_as_longlong(fma(v, scale, kMagic));
+}
+
+template <int D>
+struct Row {
+    float v[D > 0 ? D : 1];
+};
+
+// Squared float32 distance of a register row to an LDS centroid row.
+template <int D>
+__device__ inline float sqd_reg(const Row<D>& x, const float* c) {
+    float acc = 0.f;
+#pragma unroll
+    for (int m = 0; m < D; m += 4) {
+        const float4 cv = *reinterpret_cast<const float4*>(c + m);
+        float t0 = x.v[m] - cv.x, t1 = x.v[m + 1] - cv.y, t2 = x.v[m + 2] - cv.z, t3 = x.v[m + 3] - cv.w;
+        acc = fmaf(t0, t0, acc);
+        acc = fmaf(t1, t1, acc);
+        acc = fmaf(t2, t2, acc);
+        acc = fmaf(t3, t3, acc);
+    }
+    return acc;
+}
+
+// Generic-d form: both rows in LDS.
+__device__ inline float sqd_lds(const float* x, const float* c, int d) {
+    float acc = 0.f;
+    for (int m = 0; m < d; ++m) {
+        float t = x[m] - c[m];
+        acc = fmaf(t, t, acc);
+    }
+    return acc;
+}
+
+// Squared float64 distance (direct-difference form) of an LDS float row to a
+// float64 centroid row in global memory.
+__device__ inline double sqd64(const float* x, const double* c, int d) {
+    double acc = 0.0;
+    for (int m = 0; m < d; ++m) {
+        double t = (double)x[m] - c[m];
+        acc = fma(t, t, acc);
+    }
+    return acc;
+}
+
+__device__ inline uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Init helpers
+
+__global__ void k_absmax(const float* __restrict__ X, int64_t count, uint32_t* absmax_bits,
+                         int32_t* nonfinite) {
+    uint32_t m = 0;
+    int bad = 0;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) {
+        const uint32_t b = __float_as_uint(X[i]) & 0x7fffffffu;
+        if (b >= 0x7f800000u) bad = 1;
+        else m = b > m ? b : m;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t o = __shfl_xor(m, off);
+        m = o > m ? o : m;
+    }
+    const bool any_bad = __any(bad);
+    if ((threadIdx.x & 63) == 0) {
+        atomicMax(absmax_bits, m);
+        if (any_bad) atomicOr(nonfinite, 1);
+    }
+}
+
+__global__ void k_set_centroids(const float* __restrict__ C0, double* C64, float* C32, float* ec,
+                                int64_t kd, int32_t k) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < kd) {
+        const float v = C0[i];
+        C64[i] = (double)v;
+        C32[i] = v;
+    }
+    if (i < k) ec[i] = 0.f;
+}
+
+// ---------------------------------------------------------------------------
+// Centroid table: h[i][j] = d(c_i, c_j) / 2 rounded down, s[i] = min_{j != i}
+// h[i][j] (paper section III-C, with the factor 1/2 of Elkan's lemma), and
+// ec_max for the recheck band.  One block per row i.
+
+__global__ __launch_bounds__(256) void k_centroid_table(Dev P, int force) {
+    if (!force && !P.st->active) return;
+    const int i = blockIdx.x, k = P.k, d = P.d;
+    const double* ci = P.C64 + (int64_t)i * d;
+    float mn = INFINITY;
+    for (int j = threadIdx.x; j < k; j += blockDim.x) {
+        float hv = 0.f;
+        if (j != i) {
+            const double* cj = P.C64 + (int64_t)j * d;
+            double acc = 0.0;
+            for (int m = 0; m < d; ++m) {
+                double t = ci[m] - cj[m];
+                acc = fma(t, t, acc);
+            }
+            // float64 rounding of the sum and the square root stays far below 2^-40
+            hv = f32_down(0.5 * sqrt(acc) * (1.0 - 0x1p-40));
+            mn = fminf(mn, hv);
+        }
+        P.h[(int64_t)i * k + j] = hv;
+    }
+    __shared__ float red[256];
+    __shared__ float redm[256];
+    red[threadIdx.x] = mn;
+    float em = 0.f;
+    if (i == 0)
+        for (int j = threadIdx.x; j < k; j += blockDim.x) em = fmaxf(em, P.ec[j]);
+    redm[threadIdx.x] = em;
+    __syncthreads();
+    for (int w = blockDim.x / 2; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) {
+            red[threadIdx.x] = fminf(red[threadIdx.x], red[threadIdx.x + w]);
+            redm[threadIdx.x] = fmaxf(redm[threadIdx.x], redm[threadIdx.x + w]);
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        P.s[i] = red[0];
+        if (i == 0) P.st->ec_max = redm[0];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Assignment + partial sums.  Block = tp threads = one tile of tp points;
+// blocks stride over tiles.  D > 0: the row lives in registers (D % 4 == 0);
+// D == 0: any d, rows read from LDS.
+
+template <int D>
+__global__ __launch_bounds__(256) void k_assign(Dev P) {
+    IterState* st = P.st;
+    if (st->done) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
+        return;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 1;
+
+    const int d = D > 0 ? D : P.d;
+    const int k = P.k;
+    const int tp = blockDim.x;
+    const int tid = threadIdx.x;
+    const bool first = st->t == 0;
+    const bool prune = !(P.flags & KM_FLAG_NO_PRUNE);
+    const bool want_inertia = (P.flags & KM_FLAG_STATS) != 0;
+    const float ecmax = st->ec_max;
+    const float gamma = P.gamma;
+    const int xs = xs_stride(d);
+
+    const AssignLds lay = assign_lds(d, k, tp);
+    extern __shared__ __align__(16) unsigned char smem[];
+    uint64_t* acc = reinterpret_cast<uint64_t*>(smem + lay.off_acc);
+    uint32_t* cnt = reinterpret_cast<uint32_t*>(smem + lay.off_cnt);
+    float* Cs = reinterpret_cast<float*>(smem + lay.off_c);
+    float* fs = reinterpret_cast<float*>(smem + lay.off_f);
+    float* ss = reinterpret_cast<float*>(smem + lay.off_s);
+    float* ecs = reinterpret_cast<float*>(smem + lay.off_ec);
+    float* Xs = reinterpret_cast<float*>(smem + lay.off_x);
+    int* sa = reinterpret_cast<int*>(smem + lay.off_sa);
+    float* su = reinterpret_cast<float*>(smem + lay.off_su);
+    float* sD = reinterpret_cast<float*>(smem + lay.off_sd);
+    int* sq = reinterpret_cast<int*>(smem + lay.off_sq);
+    int* qlen = reinterpret_cast<int*>(smem + lay.off_misc);
+    uint64_t* bst = reinterpret_cast<uint64_t*>(smem + lay.off_misc + 16);
+
+    for (int i = tid; i < k * d; i += tp) {
+        Cs[i] = P.C32[i];
+        acc[i] = 0;
+    }
+    for (int i = tid; i < k; i += tp) {
+        cnt[i] = 0;
+        fs[i] = P.f[i];
+        ss[i] = P.s[i];
+        ecs[i] = P.ec[i];
+    }
+    if (tid < kNumStat) bst[tid] = 0;
+
+    uint64_t my_changed = 0, my_comp = 0, my_c1 = 0, my_rc = 0, my_iq = 0;
+    const int64_t ntiles = (P.n + tp - 1) / tp;
+
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t base = tile * tp;
+        const int rows = (int)((P.n - base) < tp ? (P.n - base) : tp);
+        __syncthreads();   // the previous tile is fully consumed
+        if (tid == 0) *qlen = 0;
+
+        // Stage the tile: coalesced 16-byte loads of the contiguous rows.
+        const float* src = P.X + base * d;
+        if constexpr (D > 0) {
+            constexpr int cpr = D / 4;
+            const float4* s4 = reinterpret_cast<const float4*>(src);
+            const int nch = rows * cpr;
+            for (int c = tid; c < nch; c += tp) {
+                const int r = c / cpr, q = c - r * cpr;
+                *reinterpret_cast<float4*>(Xs + r * xs + 4 * q) = s4[c];
+            }
+        } else {
+            const int ne = rows * d;
+            for (int e = tid; e < ne; e += tp) {
+                const int r = e / d;
+                Xs[r * xs + (e - r * d)] = src[e];
+            }
+        }
+
+        // Bound update and Clause 1.
+        const bool valid = tid < rows;
+        const int64_t p = base + tid;
+        int a_old = -1;
+        bool surv = false;
+        if (valid) {
+            float u_cur = 0.f;
+            if (first) {
+                surv = true;
+            } else {
+                a_old = P.a[p];
+                u_cur = (P.u[p] + fs[a_old]) * kUp;
+                if (!prune || u_cur > ss[a_old]) surv = true;
+                else my_c1 += 1;
+            }
+            sa[tid] = a_old;
+            su[tid] = u_cur;
+        }
+        __syncthreads();
+        if (surv) sq[atomicAdd(qlen, 1)] = tid;
+        __syncthreads();
+
+        // Survivors, compacted: fused distance + argmin with Clauses 2/3.
+        const int nq = *qlen;
+        for (int qi = tid; qi < nq; qi += tp) {
+            const int r = sq[qi];
+            const float* xr = Xs + r * xs;
+            Row<D> x;
+            if constexpr (D > 0) {
+#pragma unroll
+                for (int m = 0; m < D; m += 4) {
+                    const float4 v = *reinterpret_cast<const float4*>(xr + m);
+                    x.v[m] = v.x;
+                    x.v[m + 1] = v.y;
+                    x.v[m + 2] = v.z;
+                    x.v[m + 3] = v.w;
+                }
+            }
+            auto dist = [&](int j) -> float {
+                if constexpr (D > 0) return sqd_reg<D>(x, Cs + j * D);
+                else return sqd_lds(xr, Cs + j * d, d);
+            };
+            const int inc = sa[r];
+            int b = -1;
+            float Db = INFINITY, D2 = INFINITY, ub = 0.f;
+            uint64_t nc = 0;
+            if (inc >= 0) {   // tighten: exact distance to the incumbent (U(u))
+                Db = dist(inc);
+                b = inc;
+                nc += 1;
+                ub = upper_bound(Db, ecs[inc], gamma);
+            }
+            // Tightened bound within s(a): every other centroid is skipped.
+            const bool skip_all = prune && inc >= 0 && ub <= ss[inc];
+            if (!skip_all) {
+                for (int j = 0; j < k; ++j) {
+                    if (j == inc) continue;
+                    if (prune && b >= 0 && ub <= P.h[(int64_t)b * k + j]) continue;   // Clause 2/3
+                    const float Dj = dist(j);
+                    nc += 1;
+                    if (Dj < Db) {
+                        D2 = Db;
+                        Db = Dj;
+                        b = j;
+                        ub = upper_bound(Db, ecs[j], gamma);
+                    } else if (Dj < D2) {
+                        D2 = Dj;
+                    }
+                }
+            }
+            // Near tie within the float32 error bound: decide in float64
+            // against the master centroids with the oracle's tie rule.
+            if (D2 != INFINITY) {
+                const float band = 2.f * gamma * (Db + D2) +
+                                   4.f * (sqrtf(Db) + sqrtf(D2)) * ecmax + 8.f * ecmax * ecmax;
+                if (D2 - Db <= band) {
+                    int bb = -1;
+                    double Dbb = INFINITY;
+                    if (inc >= 0) {
+                        Dbb = sqd64(xr, P.C64 + (int64_t)inc * d, d);
+                        bb = inc;
+                    }
+                    for (int j = 0; j < k; ++j) {
+                        if (j == inc) continue;
+                        const double Dj = sqd64(xr, P.C64 + (int64_t)j * d, d);
+                        if (Dj < Dbb) {
+                            Dbb = Dj;
+                            bb = j;
+                        }
+                    }
+                    b = bb;
+                    Db = (float)Dbb;
+                    ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
+                    my_rc += 1;
+                }
+            }
+            if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
+            sa[r] = b;
+            su[r] = ub;
+            sD[r] = Db;
+            my_comp += nc;
+        }
+        __syncthreads();
+
+        // Write back the point state; count members.
+        if (valid) {
+            const int a_new = sa[tid];
+            if (a_new != a_old) {
+                P.a[p] = a_new;
+                my_changed += 1;
+            }
+            P.u[p] = su[tid];
+            if (want_inertia) {
+                float Dv;
+                if (surv) {
+                    Dv = sD[tid];
+                } else if constexpr (D > 0) {
+                    Row<D> x;
+#pragma unroll
+                    for (int m = 0; m < D; ++m) x.v[m] = Xs[tid * xs + m];
+                    Dv = sqd_reg<D>(x, Cs + a_new * D);
+                } else {
+                    Dv = sqd_lds(Xs + tid * xs, Cs + a_new * d, d);
+                }
+                my_iq += fixed_bits((double)Dv, P.iscale) - kMagicBits;
+            }
+            atomicAdd(&cnt[a_new], 1u);
+        }
+
+        // Per-cluster coordinate sums of every point of the tile (pruned or
+        // not), as exact fixed-point integers in LDS.
+        const int ne = rows * d;
+        for (int e = tid; e < ne; e += tp) {
+            const int r = e / d, m = e - r * d;
+            const uint64_t bits = fixed_bits((double)Xs[r * xs + m], P.qscale);
+            atomicAdd(reinterpret_cast<unsigned long long*>(&acc[sa[r] * d + m]),
+                      (unsigned long long)bits);
+        }
+    }
+    __syncthreads();
+
+    // Block counters, then the block's partial row.
+    my_changed = wave_sum_u64(my_changed);
+    my_comp = wave_sum_u64(my_comp);
+    my_c1 = wave_sum_u64(my_c1);
+    my_rc = wave_sum_u64(my_rc);
+    my_iq = wave_sum_u64(my_iq);
+    if ((tid & 63) == 0) {
+        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStChanged]), my_changed);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStComputed]), my_comp);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStClause1]), my_c1);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStRecheck]), my_rc);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStInertia]), my_iq);
+    }
+    __syncthreads();
+    uint64_t* row = P.part + (int64_t)blockIdx.x * P.L;
+    for (int i = tid; i < k * d; i += tp) row[i] = acc[i];
+    for (int i = tid; i < k; i += tp) row[k * d + i] = cnt[i];
+    if (tid < kNumStat) row[k * d + k + tid] = bst[tid];
+}
+
+// ---------------------------------------------------------------------------
+// Second pass: total[col] = sum over blocks of part[g][col].  Integer, so the
+// order of the additions does not matter.  Grid: (ceil(L/64), slices).
+
+constexpr int kReduceRows = 64;   // partial rows per slice
+
+__global__ __launch_bounds__(256) void k_reduce(Dev P) {
+    if (!P.st->active) return;
+    const int col = blockIdx.x * 64 + (threadIdx.x & 63);
+    const int sub = threadIdx.x >> 6;
+    const int g0 = blockIdx.y * kReduceRows;
+    const int g1 = min(P.G, g0 + kReduceRows);
+    uint64_t v = 0;
+    if (col < P.L)
+        for (int g = g0 + sub; g < g1; g += 4) v += P.part[(int64_t)g * P.L + col];
+    __shared__ uint64_t red[256];
+    red[threadIdx.x] = v;
+    __syncthreads();
+    if (sub == 0 && col < P.L) {
+        v = red[threadIdx.x] + red[threadIdx.x + 64] + red[threadIdx.x + 128] + red[threadIdx.x + 192];
+        atomicAdd(reinterpret_cast<unsigned long long*>(&P.total[col]), (unsigned long long)v);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Update: one wave per cluster j.  c_j = sum / count (an empty cluster keeps
+// c_j), drift f_j = ||c_j^{t+1} - c_j^t|| rounded up, float32 copy and its
+// rounding error.  Block 0 also closes the iteration: counters, history
+// record, step count and the stop test.  Leaves total[] zero.
+
+__global__ __launch_bounds__(64) void k_update(Dev P) {
+    IterState* st = P.st;
+    if (!st->active) return;
+    const int j = blockIdx.x, d = P.d, k = P.k;
+    const uint64_t count = P.total[(int64_t)k * d + j];
+    double dr = 0.0, de = 0.0;
+    for (int m = threadIdx.x; m < d; m += 64) {
+        const int64_t o = (int64_t)j * d + m;
+        const uint64_t raw = P.total[o];
+        P.total[o] = 0;
+        const double cold = P.C64[o];
+        double cnew = cold;
+        if (count > 0) {
+            const int64_t q = (int64_t)(raw - count * kMagicBits);
+            cnew = ((double)q * P.qinv) / (double)count;
+        }
+        const double df = cnew - cold;
+        dr = fma(df, df, dr);
+        const float c32 = (float)cnew;
+        const double e = (double)c32 - cnew;
+        de = fma(e, e, de);
+        P.C64[o] = cnew;
+        P.C32[o] = c32;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        dr += __shfl_xor(dr, off);
+        de += __shfl_xor(de, off);
+    }
+    if (threadIdx.x == 0) {
+        P.f[j] = f32_up(sqrt(dr) * (1.0 + 0x1p-40));
+        P.ec[j] = f32_up(sqrt(de) * (1.0 + 0x1p-40));
+        P.total[(int64_t)k * d + j] = 0;
+    }
+    if (j == 0 && threadIdx.x == 0) {
+        uint64_t* sc = P.total + (int64_t)k * d + k;
+        const int64_t changed = (int64_t)sc[kStChanged];
+        const int64_t computed = (int64_t)sc[kStComputed];
+        const int64_t c1 = (int64_t)sc[kStClause1];
+        const int64_t rc = (int64_t)sc[kStRecheck];
+        const int64_t iq = (int64_t)sc[kStInertia];
+        for (int c = 0; c < kNumStat; ++c) sc[c] = 0;
+        const double inertia = (P.flags & KM_FLAG_STATS) ? (double)iq * P.iinv : NAN;
+        const int t = st->t;
+        IterRec& r = P.rec[t % kHistCap];
+        r.changed = changed;
+        r.computed = computed;
+        r.clause1 = c1;
+        r.rechecks = rc;
+        r.inertia = inertia;
+        st->changed_last = changed;
+        st->tot_computed += computed;
+        st->tot_clause1 += c1;
+        st->tot_rechecks += rc;
+        st->inertia_last = inertia;
+        st->t = t + 1;
+        const bool tol_hit = (double)changed < st->tol_n;
+        if (tol_hit || t + 1 >= st->max_iters) {
+            st->done = 1;
+            st->converged = tol_hit ? 1 : 0;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers
+
+int assign_variant(int d) {
+    if (d == 16) return 16;
+    if (d == 32) return 32;
+    return 0;
+}
+
+const void* assign_kernel_symbol(int variant) {
+    switch (variant) {
+        case 16: return reinterpret_cast<const void*>(&k_assign<16>);
+        case 32: return reinterpret_cast<const void*>(&k_assign<32>);
+        default: return reinterpret_cast<const void*>(&k_assign<0>);
+    }
+}
+
+hipError_t launch_absmax(const float* X, int64_t count, uint32_t* absmax_bits, int32_t* nonfinite,
+                         hipStream_t s) {
+    int64_t blocks = (count + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(k_absmax, dim3((unsigned)blocks), dim3(256), 0, s, X, count, absmax_bits,
+                       nonfinite);
+    return hipGetLastError();
+}
+
+hipError_t launch_set_centroids(const float* C0, double* C64, float* C32, float* ec, int64_t kd,
+                                int32_t k, hipStream_t s) {
+    int64_t m = kd > k ? kd : k;
+    hipLaunchKernelGGL(k_set_centroids, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, s, C0, C64,
+                       C32, ec, kd, k);
+    return hipGetLastError();
+}
+
+hipError_t launch_assign(const Dev& dv, int variant, int tp, int lds_bytes, hipStream_t s) {
+    switch (variant) {
+        case 16:
+            hipLaunchKernelGGL(k_assign<16>, dim3(dv.G), dim3(tp), lds_bytes, s, dv);
+            break;
+        case 32:
+            hipLaunchKernelGGL(k_assign<32>, dim3(dv.G), dim3(tp), lds_bytes, s, dv);
+            break;
+        default:
+            hipLaunchKernelGGL(k_assign<0>, dim3(dv.G), dim3(tp), lds_bytes, s, dv);
+            break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce(const Dev& dv, hipStream_t s) {
+    dim3 grid((unsigned)((dv.L + 63) / 64), (unsigned)((dv.G + kReduceRows - 1) / kReduceRows));
+    hipLaunchKernelGGL(k_reduce, grid, dim3(256), 0, s, dv);
+    return hipGetLastError();
+}
+
+hipError_t launch_update(const Dev& dv, hipStream_t s) {
+    hipLaunchKernelGGL(k_update, dim3(dv.k), dim3(64), 0, s, dv);
+    return hipGetLastError();
+}
+
+hipError_t launch_centroid_table(const Dev& dv, int force, hipStream_t s) {
+    hipLaunchKernelGGL(k_centroid_table, dim3(dv.k), dim3(256), 0, s, dv, force);
+    return hipGetLastError();
+}
+
+}  // namespace km

@@ -1,0 +1,210 @@
+"""GPU path vs the CPU oracle, through the C ABI (via the ctypes binding).
+
+Small seeded cases span several tiles with a ragged tail and cover the
+specialised (d = 16, 32) and generic kernels; the edge cases are k = 1,
+k = n, d = 1, exact ties, an empty cluster, duplicates and the tol stop.
+"""
+import ctypes as C
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from parity import check_assign, check_centroids
+
+import paper_1902_09527_amd as km
+from paper_1902_09527_amd import _native as N
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _gpu(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(DEV)
+
+
+def _run_both(X, C0, iters, tol=0.0, prune=True, stats=False):
+    ref = oracle.lloyd(X, C0, iters, tol)
+    a, c, st = km.run(_gpu(X), _gpu(C0), iters, tol, prune=prune, stats=stats)
+    torch.cuda.synchronize()
+    return ref, a.cpu().numpy(), c.cpu().numpy(), st
+
+
+CASES = [
+    # seed, n, d, k, spread, sigma, iters, tol
+    (1, 1000, 16, 8, 10.0, 1.0, 20, 0.0),
+    (2, 3 * 256 + 37, 32, 20, 5.0, 2.0, 25, 0.0),
+    (3, 5000, 3, 7, 4.0, 1.5, 30, 0.0),
+    (4, 2000, 1, 5, 3.0, 1.0, 20, 0.0),
+    (5, 4000, 16, 1, 3.0, 1.0, 5, 0.0),
+    (6, 3000, 5, 50, 3.0, 1.0, 40, 0.001),
+    (7, 4096 + 1, 64, 30, 5.0, 2.0, 15, 0.0),
+    (8, 20000, 32, 100, 20.0, 1.5, 30, 0.0),
+    (9, 9000, 16, 10, 3.0, 2.0, 50, 0.001),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "s%d-n%d-d%d-k%d" % c[:4])
+def test_run_matches_oracle(case):
+    seed, n, d, k, spread, sigma, iters, tol = case
+    print("case", case, flush=True)
+    X, C0 = synth.blobs(n, d, k, seed=seed, spread=spread, sigma=sigma)
+    ref, a, c, st = _run_both(X, C0, iters, tol, stats=True)
+    assert st["iterations"] == ref["iters"]
+    check_assign(a, ref["assign"], ref["best"], ref["second"], "final assignment")
+    check_centroids(c, ref["C"], X, "final centroids")
+    assert st["dist_computed"] <= st["dist_lloyd"]
+    assert st["inertia_last"] == pytest.approx(ref["inertia"][-1], rel=1e-5)
+
+
+@pytest.mark.parametrize("case", CASES[:4] + CASES[6:7], ids=lambda c: "s%d-n%d-d%d-k%d" % c[:4])
+def test_prune_and_no_prune_are_bitwise_identical(case):
+    seed, n, d, k, spread, sigma, iters, tol = case
+    X, C0 = synth.blobs(n, d, k, seed=seed, spread=spread, sigma=sigma)
+    Xg, Cg = _gpu(X), _gpu(C0)
+    a1, c1, s1 = km.run(Xg, Cg, iters, tol, prune=True)
+    a2, c2, s2 = km.run(Xg, Cg, iters, tol, prune=False)
+    assert torch.equal(a1, a2) and torch.equal(c1, c2)
+    assert s1["iterations"] == s2["iterations"]
+    assert s2["dist_computed"] >= s2["dist_lloyd"]          # unpruned: all n*k each step
+    assert s1["dist_computed"] <= s2["dist_computed"]
+
+
+def test_trajectory_every_step_matches_oracle():
+    X, C0 = synth.blobs(6000, 16, 12, seed=21, spread=4.0, sigma=1.5)
+    T = 15
+    ref = oracle.lloyd(X, C0, T, history=True)
+    with km.KMeansMTI(_gpu(X), _gpu(C0), stats=True) as ctx:
+        for t in range(T):
+            C_before = ctx.centroids64()
+            np.testing.assert_allclose(C_before, ref["C_hist"][t], rtol=1e-12, atol=1e-12)
+            ch = ctx.iterate(sync=True)
+            a, c = ctx.get()
+            prev = None if t == 0 else ref["assign_hist"][t - 1]
+            _, b, s, _ = oracle.assign(X, ref["C_hist"][t], prev=prev)
+            info = check_assign(a.cpu().numpy(), ref["assign_hist"][t], b, s, "step %d" % t)
+            if info["mismatch"] == 0:
+                assert ch == ref["changed"][t]
+            check_centroids(c.cpu().numpy(), ref["C_hist"][t + 1], X, "step %d" % t)
+        hist = ctx.history()
+        assert len(hist["changed"]) == T
+        np.testing.assert_array_equal(hist["changed"], ref["changed"])
+        np.testing.assert_allclose(hist["inertia"], ref["inertia"], rtol=1e-5)
+        assert hist["computed"][0] <= 6000 * 12
+
+
+def test_determinism_bitwise():
+    X, C0 = synth.blobs(30000, 32, 40, seed=31, spread=3.0, sigma=2.0)
+    outs = []
+    for _ in range(2):
+        with km.KMeansMTI(_gpu(X), _gpu(C0)) as ctx:
+            for _ in range(12):
+                ctx.iterate()
+            a, c = ctx.get()
+            outs.append((a.cpu().numpy(), c.cpu().numpy(), ctx.centroids64()))
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+    np.testing.assert_array_equal(outs[0][2], outs[1][2])
+
+
+def test_k1_every_point_clause1_after_first_step():
+    X, C0 = synth.blobs(5000, 16, 1, seed=41)
+    with km.KMeansMTI(_gpu(X), _gpu(C0)) as ctx:
+        for _ in range(4):
+            ctx.iterate()
+        h = ctx.history()
+        C64 = ctx.centroids64()
+    assert h["clause1"].tolist() == [0, 5000, 5000, 5000]
+    assert h["computed"].tolist() == [5000, 0, 0, 0]
+    np.testing.assert_allclose(C64[0], X.astype(np.float64).mean(0), rtol=1e-12, atol=1e-12)
+
+
+def test_k_equals_n():
+    X, _ = synth.blobs(300, 16, 300, seed=51)
+    ref, a, c, st = _run_both(X, X, 3)
+    assert a.tolist() == list(range(300))
+    np.testing.assert_array_equal(c, X)
+
+
+@pytest.mark.parametrize("case", json.load(open(os.path.join(GOLDEN, "ties_1d.json")))["cases"],
+                         ids=lambda c: c["name"])
+def test_golden_ties_and_empty_cluster(case):
+    X = np.array(case["X"], np.float32)
+    C0 = np.array(case["C0"], np.float32)
+    with km.KMeansMTI(_gpu(X), _gpu(C0)) as ctx:
+        for t in range(case["max_iters"]):
+            ctx.iterate()
+            a, _ = ctx.get(centroids=False)
+            assert a.cpu().tolist() == case["assign_hist"][t]
+        _, c = ctx.get(assign=False)
+    np.testing.assert_array_equal(c.cpu().numpy(), np.array(case["C"], np.float32))
+
+
+def test_golden_worked_example():
+    g = json.load(open(os.path.join(GOLDEN, "worked_2d.json")))
+    X = np.array(g["X"], np.float32)
+    C0 = np.array(g["C0"], np.float32)
+    with km.KMeansMTI(_gpu(X), _gpu(C0), stats=True) as ctx:
+        for st in g["steps"]:
+            assert ctx.iterate(sync=True) == st["changed"]
+            a, _ = ctx.get(centroids=False)
+            assert a.cpu().tolist() == st["assign"]
+            np.testing.assert_allclose(ctx.centroids64(), np.array(st["C_after"]), rtol=1e-15)
+        h = ctx.history()
+    np.testing.assert_allclose(h["inertia"], [s["inertia"] for s in g["steps"]], rtol=1e-6)
+    for run in g["runs"]:
+        _, _, s = km.run(_gpu(X), _gpu(C0), run["max_iters"], run["tol"])
+        assert s["iterations"] == run["iters"]
+
+
+def test_duplicates_and_single_point():
+    X, C0 = synth.blobs(700, 16, 6, seed=61)
+    X = np.concatenate([X, X[:300]])
+    ref, a, c, st = _run_both(X, C0, 15)
+    check_assign(a, ref["assign"], ref["best"], ref["second"])
+    assert (a[700:] == a[:300]).all()
+    check_centroids(c, ref["C"], X)
+    X1 = np.array([[1.5, -2.0, 3.0]], np.float32)
+    a, c, st = km.run(_gpu(X1), _gpu(X1), 3)
+    assert a.cpu().tolist() == [0] and st["iterations"] == 3
+    np.testing.assert_array_equal(c.cpu().numpy(), X1)
+
+
+def test_unaligned_x_uses_generic_kernel():
+    X, C0 = synth.blobs(2000, 16, 9, seed=71)
+    big = torch.zeros(2000 * 16 + 1, dtype=torch.float32, device=DEV)
+    big[1:] = _gpu(X).reshape(-1)
+    Xu = big[1:].view(2000, 16)          # 4-byte aligned, not 16-byte aligned
+    assert Xu.data_ptr() % 16 != 0 and Xu.is_contiguous()
+    a, c, st = km.run(Xu, _gpu(C0), 20)
+    ref = oracle.lloyd(X, C0, 20)
+    check_assign(a.cpu().numpy(), ref["assign"], ref["best"], ref["second"])
+    check_centroids(c.cpu().numpy(), ref["C"], X)
+
+
+def test_errors_on_device():
+    lib = N.load()
+    X, C0 = synth.blobs(100, 4, 3, seed=81)
+    ctx = C.c_void_p()
+    # a host pointer is refused, not dereferenced
+    st = lib.kmeans_mti_init(C.byref(ctx), X.ctypes.data_as(C.c_void_p), 100, 4, 3,
+                             C0.ctypes.data_as(C.c_void_p), None, 0)
+    assert st == N.KM_ERR_INVALID_ARG and not ctx.value
+    Xn = X.copy()
+    Xn[17, 2] = np.nan
+    with pytest.raises(N.KMError) as e:
+        km.KMeansMTI(_gpu(Xn), _gpu(C0), validate=True)
+    assert e.value.status == N.KM_ERR_NONFINITE
+    Xi = X.copy()
+    Xi[3, 0] = np.inf
+    with pytest.raises(N.KMError):
+        km.run(_gpu(Xi), _gpu(C0), 3, validate=True)
+    with km.KMeansMTI(_gpu(X), _gpu(C0)) as c:
+        with pytest.raises(N.KMError) as e:
+            c.get(assign=True, centroids=False)     # no step yet
+        assert e.value.status == N.KM_ERR_STATE
