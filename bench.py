@@ -57,6 +57,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile", action="store_true",
+                    help="run only the timed region (no warmup context, no job run, no CPU leg), "
+                         "so a profiler's per-kernel averages cover exactly the timed launches")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures the one-GPU hot path only; --gpus %d is not supported "
@@ -79,6 +82,9 @@ def main() -> int:
     torch.cuda.synchronize()
 
     # Warmup: W iterations on a throwaway context (kernel load, caches, clocks).
+    if args.profile:
+        args.warmup = 0
+        args.no_cpu_baseline = True
     if args.warmup > 0:
         with km.KMeansMTI(Xg, Cg) as ctx:
             for _ in range(args.warmup):
@@ -101,8 +107,10 @@ def main() -> int:
     log("timed %d iterations in %.3f ms" % (K, elapsed * 1e3))
 
     # The job as the workload defines it (tol stop), for the iteration count.
-    a, c, job = km.run(Xg, Cg, w.max_iters, w.tol)
-    torch.cuda.synchronize()
+    job = {"iterations": 0, "converged": 0, "device_ms": 0.0}
+    if not args.profile:
+        _, _, job = km.run(Xg, Cg, w.max_iters, w.tol)
+        torch.cuda.synchronize()
 
     n, d, k = w.n, w.d, w.k
     ips = K / elapsed

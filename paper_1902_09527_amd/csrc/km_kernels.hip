@@ -26,6 +26,8 @@ namespace {
 
 constexpr float kUp = 1.0f + 0x1p-22f;   // covers one float32 rounding, upward
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));   // native 16-byte vector
+
 // Largest float <= v and smallest float >= v.
 __device__ inline float f32_down(double v) {
     float r = (float)v;
@@ -238,29 +240,58 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
     uint64_t my_changed = 0, my_comp = 0, my_c1 = 0, my_rc = 0, my_iq = 0;
     const int64_t ntiles = (P.n + tp - 1) / tp;
 
+    // Register prefetch of the next tile: its X rows (coalesced 16-byte
+    // chunks, specialised d only) and this thread's point state, issued
+    // before the current tile is processed so global loads overlap compute.
+    constexpr int kChunks = D > 0 ? D / 4 : 1;   // 16-byte chunks per thread per tile
+    f32x4 xbuf[kChunks];
+    int abuf = -1;
+    float ubuf = 0.f;
+    auto prefetch = [&](int64_t tl) {
+        const int64_t b = tl * tp;
+        const int r = (int)((P.n - b) < tp ? (P.n - b) : tp);
+        if constexpr (D > 0) {
+            const f32x4* s4 = reinterpret_cast<const f32x4*>(P.X + b * D);
+#pragma unroll
+            for (int i = 0; i < kChunks; ++i) {
+                const int c = tid + i * tp;
+                if (c < r * kChunks) xbuf[i] = __builtin_nontemporal_load(s4 + c);
+            }
+        }
+        if (!first && tid < r) {
+            abuf = P.a[b + tid];
+            ubuf = P.u[b + tid];
+        }
+    };
+    if ((int64_t)blockIdx.x < ntiles) prefetch(blockIdx.x);
+
     for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         const int64_t base = tile * tp;
         const int rows = (int)((P.n - base) < tp ? (P.n - base) : tp);
         __syncthreads();   // the previous tile is fully consumed
         if (tid == 0) *qlen = 0;
 
-        // Stage the tile: coalesced 16-byte loads of the contiguous rows.
-        const float* src = P.X + base * d;
+        // Stage the tile in LDS.
         if constexpr (D > 0) {
-            constexpr int cpr = D / 4;
-            const float4* s4 = reinterpret_cast<const float4*>(src);
-            const int nch = rows * cpr;
-            for (int c = tid; c < nch; c += tp) {
-                const int r = c / cpr, q = c - r * cpr;
-                *reinterpret_cast<float4*>(Xs + r * xs + 4 * q) = s4[c];
+#pragma unroll
+            for (int i = 0; i < kChunks; ++i) {
+                const int c = tid + i * tp;
+                if (c < rows * kChunks) {
+                    const int r = c / kChunks, q = c - r * kChunks;
+                    *reinterpret_cast<f32x4*>(Xs + r * xs + 4 * q) = xbuf[i];
+                }
             }
         } else {
+            const float* src = P.X + base * d;
             const int ne = rows * d;
             for (int e = tid; e < ne; e += tp) {
                 const int r = e / d;
                 Xs[r * xs + (e - r * d)] = src[e];
             }
         }
+        const int a_pre = abuf;
+        const float u_pre = ubuf;
+        if (tile + gridDim.x < ntiles) prefetch(tile + gridDim.x);
 
         // Bound update and Clause 1.
         const bool valid = tid < rows;
@@ -272,8 +303,8 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
             if (first) {
                 surv = true;
             } else {
-                a_old = P.a[p];
-                u_cur = (P.u[p] + fs[a_old]) * kUp;
+                a_old = a_pre;
+                u_cur = (u_pre + fs[a_old]) * kUp;
                 if (!prune || u_cur > ss[a_old]) surv = true;
                 else my_c1 += 1;
             }
