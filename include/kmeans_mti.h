@@ -69,7 +69,9 @@ enum {
     KM_FLAG_NO_PRUNE = 1u,     /* compute all k distances every iteration (plain Lloyd's) */
     KM_FLAG_STATS = 2u,        /* also accumulate the inertia sum_i ||x_i - c_{a_i}||^2 */
     KM_FLAG_VALIDATE = 4u,     /* reject non-finite X or C0 at init with KM_ERR_NONFINITE */
-    KM_FLAG_TIMING = 8u        /* record HIP events around every kernel (kmeans_mti_get_timing) */
+    KM_FLAG_TIMING = 8u,       /* record HIP events around every kernel (kmeans_mti_get_timing) */
+    KM_FLAG_VECTOR_ONLY = 16u  /* use the per-point vector distance loop even where the
+                                  matrix-core (MFMA) survivor path applies; same results */
 };
 
 /* Totals over the iterations run so far (kmeans_mti_get_stats, kmeans_mti_run). */

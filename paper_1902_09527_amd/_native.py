@@ -22,6 +22,7 @@ KM_FLAG_NO_PRUNE = 1
 KM_FLAG_STATS = 2
 KM_FLAG_VALIDATE = 4
 KM_FLAG_TIMING = 8
+KM_FLAG_VECTOR_ONLY = 16
 
 #: Every symbol include/kmeans_mti.h declares.
 EXPORTS = (

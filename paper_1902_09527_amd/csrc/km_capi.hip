@@ -199,8 +199,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
                  (long long)k * d, max_lds);
         return KM_ERR_UNSUPPORTED;
     }
-    c->variant = km::assign_variant(d);
-    if (reinterpret_cast<uintptr_t>(X) % 16 != 0) c->variant = 0;
+    c->variant = km::assign_variant(d, k, reinterpret_cast<uintptr_t>(X) % 16 == 0,
+                                    (c->flags & KM_FLAG_VECTOR_ONLY) != 0);
     const void* sym = km::assign_kernel_symbol(c->variant);
     KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds));
     int per_cu = 0;
@@ -223,6 +223,7 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         (rc = c->alloc(&v.C64, (size_t)k * d)) || (rc = c->alloc(&v.C32, (size_t)k * d)) ||
         (rc = c->alloc(&v.ec, (size_t)k)) || (rc = c->alloc(&v.h, (size_t)k * k)) ||
         (rc = c->alloc(&v.s, (size_t)k)) || (rc = c->alloc(&v.f, (size_t)k)) ||
+        (rc = c->alloc(&v.cn2, (size_t)k)) ||
         (rc = c->alloc(&v.part, (size_t)G * v.L)) || (rc = c->alloc(&v.total, (size_t)v.L)) ||
         (rc = c->alloc(&v.st, 1)) || (rc = c->alloc(&v.rec, (size_t)km::kHistCap)))
         return rc;
@@ -295,7 +296,8 @@ int kmeans_mti_init(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t 
     *out = nullptr;
     int rc = check_shape(X, n, d, k, C0);
     if (rc != KM_OK) return rc;
-    if (flags & ~(uint32_t)(KM_FLAG_NO_PRUNE | KM_FLAG_STATS | KM_FLAG_VALIDATE | KM_FLAG_TIMING))
+    if (flags & ~(uint32_t)(KM_FLAG_NO_PRUNE | KM_FLAG_STATS | KM_FLAG_VALIDATE | KM_FLAG_TIMING |
+                            KM_FLAG_VECTOR_ONLY))
         return KM_ERR_INVALID_ARG;
     km_ctx* c = new (std::nothrow) km_ctx;
     if (!c) return KM_ERR_OOM;

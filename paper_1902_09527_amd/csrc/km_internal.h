@@ -56,6 +56,7 @@ struct Dev {
     float* h;             // k*k: half centroid distances rounded down
     float* s;             // k: min_{j != i} h[i][j] rounded down (+inf if k == 1)
     float* f;             // k: drift ||c_j^t - c_j^{t-1}|| rounded up
+    float* cn2;           // k: ||c32_j||^2 (matrix-core path)
     uint64_t* part;       // G x L per-block partial rows
     uint64_t* total;      // L reduced row (zero between iterations)
     IterState* st;
@@ -76,9 +77,12 @@ __host__ __device__ inline int xs_stride(int d) { return ((d + 3) / 4) * 4 + 4; 
 
 // Dynamic LDS layout of the assignment kernel for tile size tp.
 struct AssignLds {
-    int off_acc, off_cnt, off_c, off_f, off_s, off_ec, off_x, off_sa, off_su, off_sd, off_sq,
-        off_misc, bytes;
+    int off_acc, off_cnt, off_c, off_f, off_s, off_ec, off_cn, off_x, off_sa, off_su, off_sd,
+        off_sq, off_misc, bytes;
 };
+
+// Centroid count rounded up to the 32-row blocks of the matrix-core path.
+__host__ __device__ inline int k_pad32(int k) { return (k + 31) / 32 * 32; }
 
 __host__ __device__ inline AssignLds assign_lds(int d, int k, int tp) {
     AssignLds L;
@@ -95,6 +99,7 @@ __host__ __device__ inline AssignLds assign_lds(int d, int k, int tp) {
     L.off_f = take(4 * k, 16);
     L.off_s = take(4 * k, 16);
     L.off_ec = take(4 * k, 16);
+    L.off_cn = take(4 * k_pad32(k), 16);
     L.off_x = take(4 * tp * xs_stride(d), 16);
     L.off_sa = take(4 * tp, 16);
     L.off_su = take(4 * tp, 16);
@@ -115,9 +120,12 @@ hipError_t launch_reduce(const Dev& dv, hipStream_t s);
 hipError_t launch_update(const Dev& dv, hipStream_t s);
 hipError_t launch_centroid_table(const Dev& dv, int force, hipStream_t s);
 
-// Compile-time dimension specialisation for d (0 = generic); the
-// specialisations read X with 16-byte loads and need a 16-byte aligned X.
-int assign_variant(int d);
+// Assignment-kernel variant for (d, k): 16 * D + KB, where D is the
+// compile-time dimension (16, 32; 0 = generic, any d) and KB the number of
+// 32-centroid blocks of the matrix-core survivor path (0 = vector path).
+// The specialised dimensions read X with 16-byte loads and need a 16-byte
+// aligned X; vector_only selects KB = 0.
+int assign_variant(int d, int k, bool aligned, bool vector_only);
 // Kernel symbol of an assignment-kernel variant (for occupancy queries).
 const void* assign_kernel_symbol(int variant);
 

@@ -15,6 +15,7 @@
 // Every kernel first reads the device loop state and returns at once when
 // the run has stopped, so a whole run can be enqueued up front.
 #include <float.h>
+#include <limits.h>
 #include <math.h>
 
 #include "kmeans_mti.h"
@@ -26,7 +27,8 @@ namespace {
 
 constexpr float kUp = 1.0f + 0x1p-22f;   // covers one float32 rounding, upward
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));   // native 16-byte vector
+typedef float f32x4 __attribute__((ext_vector_type(4)));    // native 16-byte vector
+typedef float f32x16 __attribute__((ext_vector_type(16)));  // 32x32 MFMA accumulator slice
 
 // Largest float <= v and smallest float >= v.
 __device__ inline float f32_down(double v) {
@@ -65,6 +67,23 @@ __device__ inline float sqd_reg(const Row<D>& x, const float* c) {
     for (int m = 0; m < D; m += 4) {
         const float4 cv = *reinterpret_cast<const float4*>(c + m);
         float t0 = x.v[m] - cv.x, t1 = x.v[m + 1] - cv.y, t2 = x.v[m + 2] - cv.z, t3 = x.v[m + 3] - cv.w;
+        acc = fmaf(t0, t0, acc);
+        acc = fmaf(t1, t1, acc);
+        acc = fmaf(t2, t2, acc);
+        acc = fmaf(t3, t3, acc);
+    }
+    return acc;
+}
+
+// Both rows in LDS, compile-time D (16-byte aligned rows).
+template <int D>
+__device__ inline float sqd_lds_fixed(const float* x, const float* c) {
+    float acc = 0.f;
+#pragma unroll
+    for (int m = 0; m < D; m += 4) {
+        const float4 xv = *reinterpret_cast<const float4*>(x + m);
+        const float4 cv = *reinterpret_cast<const float4*>(c + m);
+        float t0 = xv.x - cv.x, t1 = xv.y - cv.y, t2 = xv.z - cv.z, t3 = xv.w - cv.w;
         acc = fmaf(t0, t0, acc);
         acc = fmaf(t1, t1, acc);
         acc = fmaf(t2, t2, acc);
@@ -163,6 +182,12 @@ __global__ __launch_bounds__(256) void k_centroid_table(Dev P, int force) {
         }
         P.h[(int64_t)i * k + j] = hv;
     }
+    if (threadIdx.x == 0) {   // ||c32_i||^2 for the expansion form of the matrix-core path
+        const float* c = P.C32 + (int64_t)i * d;
+        double n2 = 0.0;
+        for (int m = 0; m < d; ++m) n2 = fma((double)c[m], (double)c[m], n2);
+        P.cn2[i] = (float)n2;
+    }
     __shared__ float red[256];
     __shared__ float redm[256];
     red[threadIdx.x] = mn;
@@ -187,9 +212,15 @@ __global__ __launch_bounds__(256) void k_centroid_table(Dev P, int force) {
 // ---------------------------------------------------------------------------
 // Assignment + partial sums.  Block = tp threads = one tile of tp points;
 // blocks stride over tiles.  D > 0: the row lives in registers (D % 4 == 0);
-// D == 0: any d, rows read from LDS.
+// D == 0: any d, rows read from LDS.  KB == 0: the survivors run the
+// per-point MTI scan on the vector units.  KB > 0 (D = 16 or 32, k <= 32*KB):
+// the survivors' distances to all centroids come from float32 MFMA tiles
+// (X . C^T in the expanded form |x|^2 + |c|^2 - 2 x.c), and every centroid
+// within the expanded form's error bound of the best is re-evaluated in the
+// direct form before the decision, so the result is the same as the vector
+// path's.
 
-template <int D>
+template <int D, int KB>
 __global__ __launch_bounds__(256) void k_assign(Dev P) {
     IterState* st = P.st;
     if (st->done) {
@@ -224,6 +255,7 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
     int* sq = reinterpret_cast<int*>(smem + lay.off_sq);
     int* qlen = reinterpret_cast<int*>(smem + lay.off_misc);
     uint64_t* bst = reinterpret_cast<uint64_t*>(smem + lay.off_misc + 16);
+    float* cn2s = reinterpret_cast<float*>(smem + lay.off_cn);
 
     for (int i = tid; i < k * d; i += tp) {
         Cs[i] = P.C32[i];
@@ -236,6 +268,35 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
         ecs[i] = P.ec[i];
     }
     if (tid < kNumStat) bst[tid] = 0;
+
+    // Matrix-core path: this lane's A operands (centroid rows) for the whole
+    // kernel.  Lane l feeds row (32*cb + l%32) and dimension half l/32; the
+    // MFMA k-step s pairs dimension s with dimension D/2 + s.
+    constexpr int kCb = KB > 0 ? KB : 1;
+    constexpr int kHalf = D > 0 ? D / 2 : 1;
+    float creg[kCb][kHalf];
+    float cnmax = 0.f;
+    if constexpr (KB > 0) {
+        static_assert(D == 16 || D == 32, "matrix-core path needs d = 16 or 32");
+        const int lane = tid & 63, half = lane >> 5;
+#pragma unroll
+        for (int cb = 0; cb < KB; ++cb) {
+            const int j = cb * 32 + (lane & 31);
+#pragma unroll
+            for (int q = 0; q < kHalf; ++q)
+                creg[cb][q] = j < k ? P.C32[(int64_t)j * D + half * kHalf + q] : 0.f;
+        }
+        for (int i = tid; i < KB * 32; i += tp) cn2s[i] = i < k ? P.cn2[i] : INFINITY;
+        __syncthreads();
+        float m2 = 0.f;
+        for (int i = lane; i < k; i += 64) m2 = fmaxf(m2, cn2s[i]);
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) m2 = fmaxf(m2, __shfl_xor(m2, off));
+        cnmax = sqrtf(m2) * kUp;
+    }
+    // Error bound factor of an expanded-form float32 squared distance,
+    // relative to (|x| + |c|)^2.
+    const float gexp = (float)(D + 8) * 0x1p-24f;
 
     uint64_t my_changed = 0, my_comp = 0, my_c1 = 0, my_rc = 0, my_iq = 0;
     const int64_t ntiles = (P.n + tp - 1) / tp;
@@ -315,85 +376,206 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
         if (surv) sq[atomicAdd(qlen, 1)] = tid;
         __syncthreads();
 
-        // Survivors, compacted: fused distance + argmin with Clauses 2/3.
+        // Survivors, compacted into sq[0, nq).
         const int nq = *qlen;
-        for (int qi = tid; qi < nq; qi += tp) {
-            const int r = sq[qi];
-            const float* xr = Xs + r * xs;
-            Row<D> x;
-            if constexpr (D > 0) {
+        if constexpr (KB > 0) {
+            // Matrix cores: one wave per block of 32 survivors.  Lanes l and
+            // l + 32 serve survivor l % 32 and hold 16 of its centroid
+            // distances per 32-centroid block.
+            const int lane = tid & 63, col = lane & 31, half = lane >> 5;
+            const int nwaves = tp >> 6;
+            for (int blk = tid >> 6; blk * 32 < nq; blk += nwaves) {
+                const int qi = blk * 32 + col;
+                const bool live = qi < nq;
+                const int r = sq[live ? qi : blk * 32];
+                const float* xr = Xs + r * xs;
+                float xh[kHalf];
 #pragma unroll
-                for (int m = 0; m < D; m += 4) {
-                    const float4 v = *reinterpret_cast<const float4*>(xr + m);
-                    x.v[m] = v.x;
-                    x.v[m + 1] = v.y;
-                    x.v[m + 2] = v.z;
-                    x.v[m + 3] = v.w;
+                for (int q = 0; q < kHalf; q += 4) {
+                    const f32x4 v = *reinterpret_cast<const f32x4*>(xr + half * kHalf + q);
+                    xh[q] = v.x;
+                    xh[q + 1] = v.y;
+                    xh[q + 2] = v.z;
+                    xh[q + 3] = v.w;
                 }
-            }
-            auto dist = [&](int j) -> float {
-                if constexpr (D > 0) return sqd_reg<D>(x, Cs + j * D);
-                else return sqd_lds(xr, Cs + j * d, d);
-            };
-            const int inc = sa[r];
-            int b = -1;
-            float Db = INFINITY, D2 = INFINITY, ub = 0.f;
-            uint64_t nc = 0;
-            if (inc >= 0) {   // tighten: exact distance to the incumbent (U(u))
-                Db = dist(inc);
-                b = inc;
-                nc += 1;
-                ub = upper_bound(Db, ecs[inc], gamma);
-            }
-            // Tightened bound within s(a): every other centroid is skipped.
-            const bool skip_all = prune && inc >= 0 && ub <= ss[inc];
-            if (!skip_all) {
-                for (int j = 0; j < k; ++j) {
-                    if (j == inc) continue;
-                    if (prune && b >= 0 && ub <= P.h[(int64_t)b * k + j]) continue;   // Clause 2/3
-                    const float Dj = dist(j);
-                    nc += 1;
-                    if (Dj < Db) {
-                        D2 = Db;
-                        Db = Dj;
-                        b = j;
-                        ub = upper_bound(Db, ecs[j], gamma);
-                    } else if (Dj < D2) {
-                        D2 = Dj;
+                float x2 = 0.f;
+#pragma unroll
+                for (int q = 0; q < kHalf; ++q) x2 = fmaf(xh[q], xh[q], x2);
+                x2 += __shfl_xor(x2, 32);
+                f32x16 dot[kCb];
+#pragma unroll
+                for (int cb = 0; cb < KB; ++cb)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) dot[cb][e] = 0.f;
+#pragma unroll
+                for (int q = 0; q < kHalf; ++q)
+#pragma unroll
+                    for (int cb = 0; cb < KB; ++cb)
+                        dot[cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(creg[cb][q], xh[q], dot[cb], 0, 0, 0);
+                // Register e of block cb holds centroid 32*cb + 8*(e/4) + 4*half + e%4.
+                auto cent = [&](int cb, int e) { return cb * 32 + 8 * (e >> 2) + 4 * half + (e & 3); };
+                float e1 = INFINITY;
+#pragma unroll
+                for (int cb = 0; cb < KB; ++cb)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+                        e1 = fminf(e1, x2 + cn2s[cent(cb, e)] - 2.f * dot[cb][e]);
+                e1 = fminf(e1, __shfl_xor(e1, 32));
+                // Every centroid whose expanded-form value is within twice the
+                // error bound of the smallest one is a candidate; the others
+                // are certified farther than the true nearest centroid.
+                const float R = sqrtf(fmaxf(x2, 0.f)) * kUp + cnmax;
+                const float thr = e1 + 2.f * (gexp * R * R + 4.f * R * ecmax + 2.f * ecmax * ecmax);
+                // Candidate bitmask (bit 16*cb + e), then direct-form distances
+                // of the candidates from the LDS rows.
+                uint64_t cmask = 0;
+#pragma unroll
+                for (int cb = 0; cb < KB; ++cb)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+                        if (x2 + cn2s[cent(cb, e)] - 2.f * dot[cb][e] <= thr) cmask |= 1ull << (16 * cb + e);
+                const int inc = live ? sa[r] : -1;
+                float d1 = INFINITY, d2 = INFINITY;
+                int rk1 = INT_MAX, j1 = 0, ncand = 0;
+                while (cmask) {
+                    const int bit = __builtin_ctzll(cmask);
+                    cmask &= cmask - 1;
+                    const int j = cent(bit >> 4, bit & 15);
+                    const float Dd = sqd_lds_fixed<D>(xr, Cs + j * D);
+                    const int rk = j == inc ? -1 : j;   // incumbent wins a tie, then lowest index
+                    ncand += 1;
+                    if (Dd < d1 || (Dd == d1 && rk < rk1)) {
+                        d2 = d1;
+                        d1 = Dd;
+                        rk1 = rk;
+                        j1 = j;
+                    } else if (Dd < d2) {
+                        d2 = Dd;
                     }
                 }
-            }
-            // Near tie within the float32 error bound: decide in float64
-            // against the master centroids with the oracle's tie rule.
-            if (D2 != INFINITY) {
-                const float band = 2.f * gamma * (Db + D2) +
-                                   4.f * (sqrtf(Db) + sqrtf(D2)) * ecmax + 8.f * ecmax * ecmax;
-                if (D2 - Db <= band) {
-                    int bb = -1;
-                    double Dbb = INFINITY;
-                    if (inc >= 0) {
-                        Dbb = sqd64(xr, P.C64 + (int64_t)inc * d, d);
-                        bb = inc;
-                    }
-                    for (int j = 0; j < k; ++j) {
-                        if (j == inc) continue;
-                        const double Dj = sqd64(xr, P.C64 + (int64_t)j * d, d);
-                        if (Dj < Dbb) {
-                            Dbb = Dj;
-                            bb = j;
+                const float od1 = __shfl_xor(d1, 32), od2 = __shfl_xor(d2, 32);
+                const int ork = __shfl_xor(rk1, 32), oj = __shfl_xor(j1, 32);
+                ncand += __shfl_xor(ncand, 32);
+                if (od1 < d1 || (od1 == d1 && ork < rk1)) {
+                    d2 = fminf(d1, fminf(d2, od2));
+                    d1 = od1;
+                    j1 = oj;
+                } else {
+                    d2 = fminf(d2, fminf(od1, od2));
+                }
+                if (live && half == 0) {
+                    int b = j1;
+                    float Db = d1;
+                    float ub = upper_bound(Db, ecs[b], gamma);
+                    if (d2 != INFINITY) {
+                        const float band = 2.f * gamma * (d1 + d2) +
+                                           4.f * (sqrtf(d1) + sqrtf(d2)) * ecmax + 8.f * ecmax * ecmax;
+                        if (d2 - d1 <= band) {
+                            int bb = -1;
+                            double Dbb = INFINITY;
+                            if (inc >= 0) {
+                                Dbb = sqd64(xr, P.C64 + (int64_t)inc * d, d);
+                                bb = inc;
+                            }
+                            for (int j = 0; j < k; ++j) {
+                                if (j == inc) continue;
+                                const double Dj = sqd64(xr, P.C64 + (int64_t)j * d, d);
+                                if (Dj < Dbb) {
+                                    Dbb = Dj;
+                                    bb = j;
+                                }
+                            }
+                            b = bb < 0 ? 0 : bb;
+                            Db = (float)Dbb;
+                            ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
+                            my_rc += 1;
                         }
                     }
-                    b = bb;
-                    Db = (float)Dbb;
-                    ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
-                    my_rc += 1;
+                    sa[r] = b;
+                    su[r] = ub;
+                    sD[r] = Db;
+                    my_comp += (uint64_t)k;   // the dense pairs; refinements re-evaluate some
                 }
             }
-            if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
-            sa[r] = b;
-            su[r] = ub;
-            sD[r] = Db;
-            my_comp += nc;
+        } else {
+            for (int qi = tid; qi < nq; qi += tp) {
+                const int r = sq[qi];
+                const float* xr = Xs + r * xs;
+                Row<D> x;
+                if constexpr (D > 0) {
+    #pragma unroll
+                    for (int m = 0; m < D; m += 4) {
+                        const float4 v = *reinterpret_cast<const float4*>(xr + m);
+                        x.v[m] = v.x;
+                        x.v[m + 1] = v.y;
+                        x.v[m + 2] = v.z;
+                        x.v[m + 3] = v.w;
+                    }
+                }
+                auto dist = [&](int j) -> float {
+                    if constexpr (D > 0) return sqd_reg<D>(x, Cs + j * D);
+                    else return sqd_lds(xr, Cs + j * d, d);
+                };
+                const int inc = sa[r];
+                int b = -1;
+                float Db = INFINITY, D2 = INFINITY, ub = 0.f;
+                uint64_t nc = 0;
+                if (inc >= 0) {   // tighten: exact distance to the incumbent (U(u))
+                    Db = dist(inc);
+                    b = inc;
+                    nc += 1;
+                    ub = upper_bound(Db, ecs[inc], gamma);
+                }
+                // Tightened bound within s(a): every other centroid is skipped.
+                const bool skip_all = prune && inc >= 0 && ub <= ss[inc];
+                if (!skip_all) {
+                    for (int j = 0; j < k; ++j) {
+                        if (j == inc) continue;
+                        if (prune && b >= 0 && ub <= P.h[(int64_t)b * k + j]) continue;   // Clause 2/3
+                        const float Dj = dist(j);
+                        nc += 1;
+                        if (Dj < Db) {
+                            D2 = Db;
+                            Db = Dj;
+                            b = j;
+                            ub = upper_bound(Db, ecs[j], gamma);
+                        } else if (Dj < D2) {
+                            D2 = Dj;
+                        }
+                    }
+                }
+                // Near tie within the float32 error bound: decide in float64
+                // against the master centroids with the oracle's tie rule.
+                if (D2 != INFINITY) {
+                    const float band = 2.f * gamma * (Db + D2) +
+                                       4.f * (sqrtf(Db) + sqrtf(D2)) * ecmax + 8.f * ecmax * ecmax;
+                    if (D2 - Db <= band) {
+                        int bb = -1;
+                        double Dbb = INFINITY;
+                        if (inc >= 0) {
+                            Dbb = sqd64(xr, P.C64 + (int64_t)inc * d, d);
+                            bb = inc;
+                        }
+                        for (int j = 0; j < k; ++j) {
+                            if (j == inc) continue;
+                            const double Dj = sqd64(xr, P.C64 + (int64_t)j * d, d);
+                            if (Dj < Dbb) {
+                                Dbb = Dj;
+                                bb = j;
+                            }
+                        }
+                        b = bb;
+                        Db = (float)Dbb;
+                        ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
+                        my_rc += 1;
+                    }
+                }
+                if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
+                sa[r] = b;
+                su[r] = ub;
+                sD[r] = Db;
+                my_comp += nc;
+            }
         }
         __syncthreads();
 
@@ -551,17 +733,22 @@ __global__ __launch_bounds__(64) void k_update(Dev P) {
 // ---------------------------------------------------------------------------
 // Launchers
 
-int assign_variant(int d) {
-    if (d == 16) return 16;
-    if (d == 32) return 32;
-    return 0;
+int assign_variant(int d, int k, bool aligned, bool vector_only) {
+    const int D = aligned && (d == 16 || d == 32) ? d : 0;
+    int KB = 0;
+    if (D > 0 && !vector_only && k > 16 && k <= 128) KB = k <= 32 ? 1 : (k <= 64 ? 2 : 4);
+    return 16 * D + KB;
 }
+
+#define KM_ASSIGN_VARIANTS(X) X(0, 0) X(16, 0) X(32, 0) X(16, 1) X(16, 2) X(16, 4) X(32, 1) X(32, 2) X(32, 4)
 
 const void* assign_kernel_symbol(int variant) {
     switch (variant) {
-        case 16: return reinterpret_cast<const void*>(&k_assign<16>);
-        case 32: return reinterpret_cast<const void*>(&k_assign<32>);
-        default: return reinterpret_cast<const void*>(&k_assign<0>);
+#define KM_SYM(D_, KB_) \
+    case 16 * D_ + KB_: return reinterpret_cast<const void*>(&k_assign<D_, KB_>);
+        KM_ASSIGN_VARIANTS(KM_SYM)
+#undef KM_SYM
+        default: return nullptr;
     }
 }
 
@@ -585,15 +772,13 @@ hipError_t launch_set_centroids(const float* C0, double* C64, float* C32, float*
 
 hipError_t launch_assign(const Dev& dv, int variant, int tp, int lds_bytes, hipStream_t s) {
     switch (variant) {
-        case 16:
-            hipLaunchKernelGGL(k_assign<16>, dim3(dv.G), dim3(tp), lds_bytes, s, dv);
-            break;
-        case 32:
-            hipLaunchKernelGGL(k_assign<32>, dim3(dv.G), dim3(tp), lds_bytes, s, dv);
-            break;
-        default:
-            hipLaunchKernelGGL(k_assign<0>, dim3(dv.G), dim3(tp), lds_bytes, s, dv);
-            break;
+#define KM_LAUNCH(D_, KB_)                                                              \
+    case 16 * D_ + KB_:                                                                 \
+        hipLaunchKernelGGL((k_assign<D_, KB_>), dim3(dv.G), dim3(tp), lds_bytes, s, dv); \
+        break;
+        KM_ASSIGN_VARIANTS(KM_LAUNCH)
+#undef KM_LAUNCH
+        default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }

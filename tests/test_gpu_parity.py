@@ -46,6 +46,12 @@ CASES = [
     (7, 4096 + 1, 64, 30, 5.0, 2.0, 15, 0.0),
     (8, 20000, 32, 100, 20.0, 1.5, 30, 0.0),
     (9, 9000, 16, 10, 3.0, 2.0, 50, 0.001),
+    # matrix-core survivor path (d = 16 or 32, 16 < k <= 128), incl. padded centroid blocks
+    (10, 5000, 16, 40, 4.0, 2.0, 25, 0.0),
+    (11, 3 * 256 + 77, 32, 17, 3.0, 2.0, 25, 0.0),
+    (12, 12000, 32, 64, 30.0, 3.0, 25, 0.0),
+    (13, 7000, 16, 100, 3.0, 1.5, 20, 0.0),
+    (14, 6000, 32, 128, 10.0, 2.0, 20, 0.001),
 ]
 
 
@@ -73,6 +79,17 @@ def test_prune_and_no_prune_are_bitwise_identical(case):
     assert s1["iterations"] == s2["iterations"]
     assert s2["dist_computed"] >= s2["dist_lloyd"]          # unpruned: all n*k each step
     assert s1["dist_computed"] <= s2["dist_computed"]
+
+
+@pytest.mark.parametrize("case", CASES[9:], ids=lambda c: "s%d-n%d-d%d-k%d" % c[:4])
+def test_matrix_core_and_vector_paths_are_bitwise_identical(case):
+    seed, n, d, k, spread, sigma, iters, tol = case
+    X, C0 = synth.blobs(n, d, k, seed=seed, spread=spread, sigma=sigma)
+    Xg, Cg = _gpu(X), _gpu(C0)
+    a1, c1, s1 = km.run(Xg, Cg, iters, tol)
+    a2, c2, s2 = km.run(Xg, Cg, iters, tol, vector_only=True)
+    assert torch.equal(a1, a2) and torch.equal(c1, c2)
+    assert s1["iterations"] == s2["iterations"]
 
 
 def test_trajectory_every_step_matches_oracle():
