@@ -70,8 +70,10 @@ enum {
     KM_FLAG_STATS = 2u,        /* also accumulate the inertia sum_i ||x_i - c_{a_i}||^2 */
     KM_FLAG_VALIDATE = 4u,     /* reject non-finite X or C0 at init with KM_ERR_NONFINITE */
     KM_FLAG_TIMING = 8u,       /* record HIP events around every kernel (kmeans_mti_get_timing) */
-    KM_FLAG_VECTOR_ONLY = 16u  /* use the per-point vector distance loop even where the
+    KM_FLAG_VECTOR_ONLY = 16u, /* use the per-point vector distance loop even where the
                                   matrix-core (MFMA) survivor path applies; same results */
+    KM_FLAG_LARGE_PATH = 32u   /* use the global-memory path (dense MFMA survivors, sums by
+                                  counting sort) even where the LDS path fits; same results */
 };
 
 /* Totals over the iterations run so far (kmeans_mti_get_stats, kmeans_mti_run). */

@@ -78,8 +78,12 @@ struct km_ctx {
     int device = 0;
     int tp = 0, lds = 0;
     int variant = 0;   // assignment-kernel specialisation
+    bool large = false;   // global-memory path (centroids / sums too large for LDS)
+    km::Large lg{};
+    int gb = 0;           // blocks of the large path's bound pass
     km::Dev dv{};
-    void* bufs[16] = {};
+    static constexpr int kMaxBufs = 32;
+    void* bufs[kMaxBufs] = {};
     int nbufs = 0;
     bool broken = false;
     bool stepped = false;
@@ -95,6 +99,10 @@ struct km_ctx {
 
     template <class T>
     int alloc(T** p, size_t count) {
+        if (nbufs >= kMaxBufs) {
+            snprintf(g_last_hip, sizeof g_last_hip, "internal: more than %d scratch buffers", kMaxBufs);
+            return KM_ERR_STATE;
+        }
         void* q = nullptr;
         hipError_t e = hipMalloc(&q, count * sizeof(T) > 0 ? count * sizeof(T) : 16);
         if (e != hipSuccess) return hip_fail(e, "hipMalloc");
@@ -147,17 +155,18 @@ int enqueue_iteration(km_ctx* c) {
     }
     auto mark = [&](int i) -> hipError_t { return ev ? hipEventRecord(ev[i], c->stream) : hipSuccess; };
     if ((e = mark(0)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
-    if ((e = km::launch_assign(c->dv, c->variant, c->tp, c->lds, c->stream)) != hipSuccess)
-        return fail_ctx(c, hip_fail(e, "assign kernel"));
+    e = c->large ? km::launch_large_assign(c->dv, c->lg, c->gb, c->stream)
+                 : km::launch_assign(c->dv, c->variant, c->tp, c->lds, c->stream);
+    if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "assign kernel"));
     if ((e = mark(1)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
-    if ((e = km::launch_reduce(c->dv, c->stream)) != hipSuccess)
-        return fail_ctx(c, hip_fail(e, "reduce kernel"));
+    e = c->large ? km::launch_large_reduce(c->dv, c->lg, c->stream) : km::launch_reduce(c->dv, c->stream);
+    if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "reduce kernel"));
     if ((e = mark(2)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
     if ((e = km::launch_update(c->dv, c->stream)) != hipSuccess)
         return fail_ctx(c, hip_fail(e, "update kernel"));
     if ((e = mark(3)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
-    if ((e = km::launch_centroid_table(c->dv, 0, c->stream)) != hipSuccess)
-        return fail_ctx(c, hip_fail(e, "centroid table kernel"));
+    e = c->large ? km::launch_large_table(c->dv, 0, c->stream) : km::launch_centroid_table(c->dv, 0, c->stream);
+    if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "centroid table kernel"));
     if ((e = mark(4)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
     c->stepped = true;
     return KM_OK;
@@ -173,58 +182,93 @@ int read_state(km_ctx* c, km::IterState* out) {
 
 int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const float* C0) {
     KM_HIP(hipGetDevice(&c->device));
-    int rc;
-    if ((rc = check_device_range(X, (size_t)n * (size_t)d * sizeof(float), c->device, "X")) != KM_OK)
-        return rc;
-    if ((rc = check_device_range(C0, (size_t)k * (size_t)d * sizeof(float), c->device, "C0")) != KM_OK)
-        return rc;
+    int rc0;
+    if ((rc0 = check_device_range(X, (size_t)n * (size_t)d * sizeof(float), c->device, "X")) != KM_OK)
+        return rc0;
+    if ((rc0 = check_device_range(C0, (size_t)k * (size_t)d * sizeof(float), c->device, "C0")) != KM_OK)
+        return rc0;
 
     int cus = 0, max_lds = 0;
     KM_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, c->device));
     KM_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device));
-
-    // Tile size: the largest of 256/128/64 points whose LDS image fits.
-    c->tp = 0;
-    for (int tp = 256; tp >= 64; tp /= 2) {
-        int bytes = km::assign_lds(d, k, tp).bytes;
-        if (bytes <= max_lds) {
-            c->tp = tp;
-            c->lds = bytes;
-            break;
-        }
-    }
-    if (c->tp == 0) {
-        snprintf(g_last_hip, sizeof g_last_hip,
-                 "k*d = %lld too large for the LDS-resident centroid path (%d bytes of LDS)",
-                 (long long)k * d, max_lds);
-        return KM_ERR_UNSUPPORTED;
-    }
-    c->variant = km::assign_variant(d, k, reinterpret_cast<uintptr_t>(X) % 16 == 0,
-                                    (c->flags & KM_FLAG_VECTOR_ONLY) != 0);
-    const void* sym = km::assign_kernel_symbol(c->variant);
-    KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds));
-    int per_cu = 0;
-    KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, c->tp, c->lds));
-    if (per_cu < 1) return KM_ERR_UNSUPPORTED;
-    const int64_t ntiles = (n + c->tp - 1) / c->tp;
-    int64_t G = (int64_t)per_cu * cus;
-    if (G > ntiles) G = ntiles;
 
     km::Dev& v = c->dv;
     v.X = X;
     v.n = n;
     v.d = d;
     v.k = k;
-    v.G = (int32_t)G;
     v.L = km::row_len(d, k);
     v.flags = c->flags;
     v.gamma = (float)((d + 4) * 0x1p-23);
+    int rc2;
+
+    // LDS path: the largest tile of 256/128/64 points whose LDS image
+    // (centroids, fixed-point sums, X tile) fits; else the global-memory path.
+    c->tp = 0;
+    if (!(c->flags & KM_FLAG_LARGE_PATH)) {
+        for (int tp = 256; tp >= 64; tp /= 2) {
+            int bytes = km::assign_lds(d, k, tp).bytes;
+            if (bytes <= max_lds) {
+                c->tp = tp;
+                c->lds = bytes;
+                break;
+            }
+        }
+    }
+    if (c->tp > 0) {
+        c->variant = km::assign_variant(d, k, reinterpret_cast<uintptr_t>(X) % 16 == 0,
+                                        (c->flags & KM_FLAG_VECTOR_ONLY) != 0);
+        const void* sym = km::assign_kernel_symbol(c->variant);
+        KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds));
+        int per_cu = 0;
+        KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, c->tp, c->lds));
+        if (per_cu < 1) return KM_ERR_UNSUPPORTED;
+        const int64_t ntiles = (n + c->tp - 1) / c->tp;
+        int64_t G = (int64_t)per_cu * cus;
+        if (G > ntiles) G = ntiles;
+        v.G = (int32_t)G;
+    } else {
+        c->large = true;
+        km::Large& L = c->lg;
+        L.dp = (d + 31) / 32 * 32;
+        const int mlds = km::large_mfma_lds(L.dp);
+        if (d > km::kLgMaxD || mlds > max_lds || 4 * k > max_lds || km::large_table_lds(d) > max_lds) {
+            snprintf(g_last_hip, sizeof g_last_hip,
+                     "k = %d, d = %d: no kernel path (d <= %d and k <= %d needed)", k, d, km::kLgMaxD,
+                     max_lds / 4);
+            return KM_ERR_UNSUPPORTED;
+        }
+        const void* sym = km::large_mfma_symbol();
+        KM_HIP(km::large_set_attributes(k, d, L.dp));
+        int per_cu = 0;
+        KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, 256, mlds));
+        if (per_cu < 1) return KM_ERR_UNSUPPORTED;
+        L.Gm = per_cu * cus;
+        int64_t gs = (n + 4095) / 4096;
+        if (gs > 2048) gs = 2048;
+        L.Gs = (int32_t)gs;
+        L.span = (n + gs - 1) / gs;
+        L.NCmax = (int32_t)(n / km::kLgChunkRows + k + 1);
+        int64_t gb = (n + 255) / 256;
+        if (gb > (int64_t)cus * 8) gb = (int64_t)cus * 8;
+        c->gb = (int)gb;
+        v.G = 1;
+        if ((rc2 = c->alloc(&L.surv, (size_t)n)) || (rc2 = c->alloc(&L.nsurv, 4)) ||
+            (rc2 = c->alloc(&L.cnt, (size_t)L.Gs * k)) || (rc2 = c->alloc(&L.off, (size_t)L.Gs * k)) ||
+            (rc2 = c->alloc(&L.base, (size_t)k + 1)) || (rc2 = c->alloc(&L.cbase, (size_t)k + 1)) ||
+            (rc2 = c->alloc(&L.perm, (size_t)n)) || (rc2 = c->alloc(&L.cpart, (size_t)L.NCmax * d)) ||
+            (rc2 = c->alloc(&L.ciq, (size_t)L.NCmax)))
+            return rc2;
+        KM_HIP(hipMemsetAsync(L.nsurv, 0, 4 * sizeof(uint32_t), c->stream));
+    }
+
+    int rc;
     if ((rc = c->alloc(&v.a, (size_t)n)) || (rc = c->alloc(&v.u, (size_t)n)) ||
         (rc = c->alloc(&v.C64, (size_t)k * d)) || (rc = c->alloc(&v.C32, (size_t)k * d)) ||
         (rc = c->alloc(&v.ec, (size_t)k)) || (rc = c->alloc(&v.h, (size_t)k * k)) ||
         (rc = c->alloc(&v.s, (size_t)k)) || (rc = c->alloc(&v.f, (size_t)k)) ||
         (rc = c->alloc(&v.cn2, (size_t)k)) ||
-        (rc = c->alloc(&v.part, (size_t)G * v.L)) || (rc = c->alloc(&v.total, (size_t)v.L)) ||
+        (rc = c->alloc(&v.part, (size_t)v.G * v.L)) || (rc = c->alloc(&v.total, (size_t)v.L)) ||
         (rc = c->alloc(&v.st, 1)) || (rc = c->alloc(&v.rec, (size_t)km::kHistCap)))
         return rc;
     uint32_t* scratch = nullptr;
@@ -274,7 +318,11 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     KM_HIP(hipMemsetAsync(v.total, 0, sizeof(uint64_t) * (size_t)v.L, c->stream));
     KM_HIP(hipMemsetAsync(v.rec, 0, sizeof(km::IterRec) * km::kHistCap, c->stream));
     KM_HIP(km::launch_set_centroids(C0, v.C64, v.C32, v.ec, (int64_t)k * d, k, c->stream));
-    KM_HIP(km::launch_centroid_table(v, 1, c->stream));
+    if (c->large) {
+        KM_HIP(km::launch_large_table(v, 1, c->stream));
+    } else {
+        KM_HIP(km::launch_centroid_table(v, 1, c->stream));
+    }
     KM_HIP(hipStreamSynchronize(c->stream));
     return KM_OK;
 }
@@ -297,7 +345,7 @@ int kmeans_mti_init(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t 
     int rc = check_shape(X, n, d, k, C0);
     if (rc != KM_OK) return rc;
     if (flags & ~(uint32_t)(KM_FLAG_NO_PRUNE | KM_FLAG_STATS | KM_FLAG_VALIDATE | KM_FLAG_TIMING |
-                            KM_FLAG_VECTOR_ONLY))
+                            KM_FLAG_VECTOR_ONLY | KM_FLAG_LARGE_PATH))
         return KM_ERR_INVALID_ARG;
     km_ctx* c = new (std::nothrow) km_ctx;
     if (!c) return KM_ERR_OOM;

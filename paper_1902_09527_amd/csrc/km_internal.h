@@ -71,6 +71,39 @@ struct Dev {
 
 inline int row_len(int d, int k) { return k * d + k + kNumStat; }
 
+// Global-memory path (centroids or per-cluster sums too large for LDS): dense
+// matrix-core distances for the Clause-1 survivors, then per-cluster sums
+// through a counting sort of the points by cluster.
+constexpr int kLgSurvTile = 64;    // survivors per workgroup tile
+constexpr int kLgCentTile = 128;   // centroids per workgroup tile (32 per wave)
+constexpr int kLgChunkRows = 256;  // rows per segment-sum chunk
+constexpr int kLgMaxD = 320;       // largest d of the global-memory path (LDS-resident survivor tile)
+
+struct Large {
+    int32_t* surv;        // n: survivor point indices of the current step
+    uint32_t* nsurv;      // survivor count (zeroed by the histogram pass for the next step)
+    uint32_t* cnt;        // Gs x k per-block cluster counts
+    uint32_t* off;        // Gs x k per-block write offsets
+    uint32_t* base;       // k + 1 cluster starts in perm
+    uint32_t* cbase;      // k + 1 first segment chunk of each cluster
+    int32_t* perm;        // n point indices grouped by cluster
+    uint64_t* cpart;      // NCmax x d chunk partial sums (fixed point)
+    uint64_t* ciq;        // NCmax chunk inertia partials (fixed point)
+    int32_t Gs;           // blocks of the histogram / scatter passes
+    int32_t NCmax;        // n / kLgChunkRows + k
+    int64_t span;         // points per histogram / scatter block (contiguous)
+    int32_t Gm;           // resident blocks of the matrix-core kernel
+    int32_t dp;           // d rounded up to 32
+};
+
+// LDS bytes of the global-memory matrix-core kernel.
+__host__ __device__ inline int large_mfma_lds(int dp) {
+    return 4 * dp * (kLgSurvTile + 1)              // survivor tile, dimension-major
+           + 2 * 4 * 32 * (kLgCentTile + 1)        // centroid chunk, double buffered
+           + 8 * kLgSurvTile * 4 * 2 * 4           // candidate lists for the merge
+           + 4 * kLgSurvTile + 64;
+}
+
 // Padded LDS row stride of the X tile: 16-byte aligned rows, offset by 4
 // floats so that 16-byte row reads of consecutive lanes spread over banks.
 __host__ __device__ inline int xs_stride(int d) { return ((d + 3) / 4) * 4 + 4; }
@@ -109,6 +142,15 @@ __host__ __device__ inline AssignLds assign_lds(int d, int k, int tp) {
     L.bytes = (o + 15) / 16 * 16;
     return L;
 }
+
+// Global-memory path launchers (km_large.hip).  gb: blocks of the bound pass.
+hipError_t launch_large_assign(const Dev& dv, const Large& lg, int gb, hipStream_t s);
+hipError_t launch_large_reduce(const Dev& dv, const Large& lg, hipStream_t s);
+hipError_t launch_large_table(const Dev& dv, int force, hipStream_t s);
+int large_table_lds(int d);
+const void* large_mfma_symbol();
+// Raises the dynamic-LDS limits of the global-memory path's kernels.
+hipError_t large_set_attributes(int k, int d, int dp);
 
 // Kernel launchers (km_kernels.hip).  Each returns the launch status.
 hipError_t launch_absmax(const float* X, int64_t count, uint32_t* absmax_bits, int32_t* nonfinite,

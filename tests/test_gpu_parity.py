@@ -52,6 +52,10 @@ CASES = [
     (12, 12000, 32, 64, 30.0, 3.0, 25, 0.0),
     (13, 7000, 16, 100, 3.0, 1.5, 20, 0.0),
     (14, 6000, 32, 128, 10.0, 2.0, 20, 0.001),
+    # global-memory path (centroids or sums too large for LDS)
+    (15, 5000, 64, 200, 6.0, 2.0, 15, 0.0),
+    (16, 4000 + 3, 256, 1000, 2.0, 1.0, 6, 0.0),
+    (17, 3000, 40, 600, 5.0, 1.5, 10, 0.001),
 ]
 
 
@@ -81,7 +85,23 @@ def test_prune_and_no_prune_are_bitwise_identical(case):
     assert s1["dist_computed"] <= s2["dist_computed"]
 
 
-@pytest.mark.parametrize("case", CASES[9:], ids=lambda c: "s%d-n%d-d%d-k%d" % c[:4])
+LARGE_FORCED = [CASES[i] for i in (0, 1, 2, 5, 8, 9, 11)]
+
+
+@pytest.mark.parametrize("case", LARGE_FORCED, ids=lambda c: "s%d-n%d-d%d-k%d" % c[:4])
+def test_global_memory_path_is_bitwise_identical_to_lds_path(case):
+    seed, n, d, k, spread, sigma, iters, tol = case
+    X, C0 = synth.blobs(n, d, k, seed=seed, spread=spread, sigma=sigma)
+    Xg, Cg = _gpu(X), _gpu(C0)
+    a1, c1, s1 = km.run(Xg, Cg, iters, tol, stats=True)
+    a2, c2, s2 = km.run(Xg, Cg, iters, tol, stats=True, large_path=True)
+    assert torch.equal(a1, a2) and torch.equal(c1, c2)
+    assert s1["iterations"] == s2["iterations"]
+    assert s1["clause1_skips"] == s2["clause1_skips"]
+    assert s2["inertia_last"] == pytest.approx(s1["inertia_last"], rel=1e-5)
+
+
+@pytest.mark.parametrize("case", CASES[9:14], ids=lambda c: "s%d-n%d-d%d-k%d" % c[:4])
 def test_matrix_core_and_vector_paths_are_bitwise_identical(case):
     seed, n, d, k, spread, sigma, iters, tol = case
     X, C0 = synth.blobs(n, d, k, seed=seed, spread=spread, sigma=sigma)

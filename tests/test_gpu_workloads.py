@@ -1,12 +1,12 @@
 """The five benchmark workloads on the GPU, checked against the CPU oracle.
 
 The three smaller workloads run whole on both sides (assignments except
-oracle near ties, centroids, iteration count).  The 100M-point workload is
-too large for a whole oracle run; there every checked step is compared at
-full size in the launch configuration the benchmark uses: the oracle's
-assignment step on a seeded sample of points, from the GPU's own float64
-centroids and previous assignment, and the oracle's update step over all
-points from the GPU's assignment.
+oracle near ties, centroids, iteration count).  The 100M-point and the
+2M x 256, k = 1000 workloads are too large for a whole oracle run; there
+every checked step is compared at full size in the launch configuration the
+benchmark uses: the oracle's assignment step on a seeded sample of points,
+from the GPU's own float64 centroids and previous assignment, and the
+oracle's update step over all points from the GPU's assignment.
 """
 import numpy as np
 import pytest
@@ -39,13 +39,13 @@ def test_workload_whole_run(name):
     _whole(name)
 
 
-def test_zipf_100m_steps_sampled():
-    name = "zipf-100M-d32-k64"
+@pytest.mark.parametrize("name,sample", [("zipf-100M-d32-k64", 1_000_000), ("blobs-2M-d256-k1000", 20_000)])
+def test_large_workload_steps_sampled(name, sample):
     X, C0, w = synth.make(name)
     print("generated", name, flush=True)
     n = w.n
     rng = np.random.default_rng(2024)
-    sample = np.sort(rng.choice(n, 1_000_000, replace=False))
+    sample = np.sort(rng.choice(n, sample, replace=False))
     Xs = np.ascontiguousarray(X[sample])
     check_at = {0, 1, w.max_iters - 1}
     with km.KMeansMTI(torch.from_numpy(X).cuda(), torch.from_numpy(C0).cuda()) as ctx:
@@ -62,6 +62,6 @@ def test_zipf_100m_steps_sampled():
                 info = check_assign(a[sample], ra, rb, rs, "step %d (sample)" % t)
                 C_ref, counts = oracle.update(X, a, C_before)
                 assert counts.sum() == n
-                err = check_centroids(ctx.centroids64(), C_ref, X[:1_000_000], "step %d" % t)
+                err = check_centroids(ctx.centroids64(), C_ref, X[:100_000], "step %d" % t)
                 print("step", t, info, "centroid rel err %.2e" % err, flush=True)
             prev = a if (t + 1 in check_at) else None
