@@ -60,7 +60,21 @@ def main() -> int:
     ap.add_argument("--profile", action="store_true",
                     help="run only the timed region (no warmup context, no job run, no CPU leg), "
                          "so a profiler's per-kernel averages cover exactly the timed launches")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run 5 plain device-to-device copies of 512 MiB (reference kernel "
+                         "for scaling hardware byte counters)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+        nbytes = 512 << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": nbytes, "copies": 5}), flush=True)
+        return 0
     if args.gpus != 1:
         print("bench.py measures the one-GPU hot path only; --gpus %d is not supported "
               "(this build runs on a single GPU)" % args.gpus, file=sys.stderr)

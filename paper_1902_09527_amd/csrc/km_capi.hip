@@ -206,18 +206,18 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     // (centroids, fixed-point sums, X tile) fits; else the global-memory path.
     c->tp = 0;
     if (!(c->flags & KM_FLAG_LARGE_PATH)) {
-        for (int tp = 256; tp >= 64; tp /= 2) {
-            int bytes = km::assign_lds(d, k, tp).bytes;
+        c->variant = km::assign_variant(d, k, reinterpret_cast<uintptr_t>(X) % 16 == 0,
+                                        (c->flags & KM_FLAG_VECTOR_ONLY) != 0);
+        const bool h_lds = c->variant % 16 == 0 && k <= km::kHLdsMaxK;
+        for (int tp = 256; c->tp == 0 && tp >= 64; tp /= 2) {
+            int bytes = km::assign_lds(d, k, tp, h_lds).bytes;
             if (bytes <= max_lds) {
                 c->tp = tp;
                 c->lds = bytes;
-                break;
             }
         }
     }
     if (c->tp > 0) {
-        c->variant = km::assign_variant(d, k, reinterpret_cast<uintptr_t>(X) % 16 == 0,
-                                        (c->flags & KM_FLAG_VECTOR_ONLY) != 0);
         const void* sym = km::assign_kernel_symbol(c->variant);
         KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds));
         int per_cu = 0;

@@ -110,14 +110,17 @@ __host__ __device__ inline int xs_stride(int d) { return ((d + 3) / 4) * 4 + 4; 
 
 // Dynamic LDS layout of the assignment kernel for tile size tp.
 struct AssignLds {
-    int off_acc, off_cnt, off_c, off_f, off_s, off_ec, off_cn, off_x, off_sa, off_su, off_sd,
+    int off_acc, off_cnt, off_c, off_f, off_s, off_ec, off_cn, off_h, off_x, off_sa, off_su, off_sd,
         off_sq, off_misc, bytes;
 };
+
+// The vector survivor scan keeps the half-distance table in LDS up to this k.
+constexpr int kHLdsMaxK = 64;
 
 // Centroid count rounded up to the 32-row blocks of the matrix-core path.
 __host__ __device__ inline int k_pad32(int k) { return (k + 31) / 32 * 32; }
 
-__host__ __device__ inline AssignLds assign_lds(int d, int k, int tp) {
+__host__ __device__ inline AssignLds assign_lds(int d, int k, int tp, bool h_lds) {
     AssignLds L;
     int o = 0;
     auto take = [&](int bytes, int align) {
@@ -133,12 +136,13 @@ __host__ __device__ inline AssignLds assign_lds(int d, int k, int tp) {
     L.off_s = take(4 * k, 16);
     L.off_ec = take(4 * k, 16);
     L.off_cn = take(4 * k_pad32(k), 16);
+    L.off_h = take(h_lds ? 4 * k * k : 0, 16);
     L.off_x = take(4 * tp * xs_stride(d), 16);
     L.off_sa = take(4 * tp, 16);
     L.off_su = take(4 * tp, 16);
     L.off_sd = take(4 * tp, 16);
     L.off_sq = take(4 * tp, 16);
-    L.off_misc = take(64, 16);   // queue length (int) at 0, kNumStat uint64 counters at 16
+    L.off_misc = take(64, 16);   // two survivor counters (int) at 0, kNumStat uint64 counters at 16
     L.bytes = (o + 15) / 16 * 16;
     return L;
 }

@@ -24,6 +24,11 @@
 
 namespace km {
 
+// Dynamic LDS of the assignment kernels.  Declared once at namespace scope so
+// that device functions index it directly and every access stays an LDS
+// (ds_*) instruction.
+extern __shared__ __align__(16) unsigned char km_smem[];
+
 namespace {
 
 template <int D>
@@ -176,6 +181,249 @@ __global__ __launch_bounds__(256) void k_centroid_table(Dev P, int force) {
 }
 
 // ---------------------------------------------------------------------------
+// Grouped survivor scan (d = 16 or 32, vector units): the survivors of a tile
+// are spread over the whole block, L lanes per point, each lane holding D/L of
+// the point's coordinates.  Partial distances are combined with xor
+// butterflies, which give bitwise equal totals in every lane of a group, so
+// all lanes of a group take the same pruning branches; the scan is the same
+// MTI scan (incumbent first, then ascending index, running best) as the
+// one-lane form.
+
+namespace {
+
+template <int L>
+__device__ inline float group_sum(float v) {
+#pragma unroll
+    for (int o = 1; o < L; o <<= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+struct ScanCtx {
+    const float* Cs;
+    int h_off;          // byte offset of the LDS copy of h (when it is in LDS)
+    const float* hg;    // h in global memory (when it is not)
+    const float* ss;
+    const float* ecs;
+    const double* C64;
+    const float* Xs;
+    int* sa;
+    float* su;
+    float* sD;
+    const int* sq;
+    int k;
+    bool prune;
+    float gamma, ecmax;
+};
+
+template <int D, int L, bool HL>
+__device__ inline void grouped_survivors(const ScanCtx& W, int ns, int tid, int tp, uint64_t& comp,
+                                         uint64_t& rechecks) {
+    const float* hl = reinterpret_cast<const float*>(km_smem + W.h_off);
+    auto hval = [&](int i) -> float {
+        if constexpr (HL) return hl[i];
+        else return W.hg[i];
+    };
+    constexpr int XS = ((D + 3) / 4) * 4 + 4;
+    constexpr int DL = D / L;   // coordinates per lane
+    const int per = tp / L;     // survivors per pass
+    const int g = tid / L, sub = tid % L;
+    const int k = W.k;
+    for (int p0 = 0; p0 < ns; p0 += per) {
+        const int slot = p0 + g;
+        const bool act = slot < ns;
+        const int r = W.sq[act ? slot : p0];
+        const float* xrow = W.Xs + r * XS;
+        float xp[DL];
+        if constexpr (DL % 4 == 0) {
+#pragma unroll
+            for (int q = 0; q < DL; q += 4) {
+                const f32x4 v = *reinterpret_cast<const f32x4*>(xrow + sub * DL + q);
+                xp[q] = v.x;
+                xp[q + 1] = v.y;
+                xp[q + 2] = v.z;
+                xp[q + 3] = v.w;
+            }
+        } else {
+#pragma unroll
+            for (int q = 0; q < DL; ++q) xp[q] = xrow[sub * DL + q];
+        }
+        auto dist = [&](int j) -> float {
+            const float* c = W.Cs + j * D + sub * DL;
+            float acc = 0.f;
+#pragma unroll
+            for (int q = 0; q < DL; ++q) {
+                const float t = xp[q] - c[q];
+                acc = fmaf(t, t, acc);
+            }
+            return group_sum<L>(acc);
+        };
+        const int inc = W.sa[r];
+        int b = -1;
+        float Db = INFINITY, D2 = INFINITY, ub = 0.f;
+        uint64_t nc = 0;
+        if (inc >= 0) {   // tighten: exact distance to the incumbent (U(u))
+            Db = dist(inc);
+            b = inc;
+            nc = 1;
+            ub = upper_bound(Db, W.ecs[inc], W.gamma);
+        }
+        const bool skip_all = W.prune && inc >= 0 && ub <= W.ss[inc];
+        if (!skip_all) {
+            for (int j = 0; j < k; ++j) {
+                if (j == inc) continue;
+                if (W.prune && b >= 0 && ub <= hval(b * k + j)) continue;   // Clause 2/3
+                const float Dj = dist(j);
+                nc += 1;
+                if (Dj < Db) {
+                    D2 = Db;
+                    Db = Dj;
+                    b = j;
+                    ub = upper_bound(Db, W.ecs[j], W.gamma);
+                } else if (Dj < D2) {
+                    D2 = Dj;
+                }
+            }
+        }
+        bool re = false;
+        if (D2 != INFINITY) {
+            const float band = 2.f * W.gamma * (Db + D2) + 4.f * (sqrtf(Db) + sqrtf(D2)) * W.ecmax +
+                               8.f * W.ecmax * W.ecmax;
+            re = D2 - Db <= band;
+        }
+        if (act && sub == 0) {
+            if (re) {   // float64 decision against the master centroids, oracle's tie rule
+                int bb = -1;
+                double Dbb = INFINITY;
+                if (inc >= 0) {
+                    Dbb = sqd64(xrow, W.C64 + (int64_t)inc * D, D);
+                    bb = inc;
+                }
+                for (int j = 0; j < k; ++j) {
+                    if (j == inc) continue;
+                    const double Dj = sqd64(xrow, W.C64 + (int64_t)j * D, D);
+                    if (Dj < Dbb) {
+                        Dbb = Dj;
+                        bb = j;
+                    }
+                }
+                b = bb;
+                Db = (float)Dbb;
+                ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
+                rechecks += 1;
+            }
+            if (b < 0) b = 0;   // only for non-finite rows
+            W.sa[r] = b;
+            W.su[r] = ub;
+            W.sD[r] = Db;
+            comp += nc;
+        }
+    }
+}
+
+// Survivor scan for k <= 16 (d = 16 or 32): a group of G >= k lanes per
+// survivor, lane j evaluates centroid j in the direct form unless Clause 2
+// skips it (loose bound u <= h(a, j)); the group then takes the minimum
+// with the oracle's tie rule and the second-best value with DPP row
+// reductions.  All k distances of a survivor are in flight at once instead
+// of one after another.
+
+// All-reduce within rows of G lanes (G = 4, 8 or 16) on DPP row operations.
+template <int G>
+__device__ inline uint32_t dpp_min_u32(uint32_t v) {
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0xB1, 0xF, 0xF, false));   // xor 1
+    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x4E, 0xF, 0xF, false));   // xor 2
+    if constexpr (G >= 8)
+        v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x141, 0xF, 0xF, false));   // half mirror
+    if constexpr (G >= 16)
+        v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x140, 0xF, 0xF, false));   // mirror
+    return v;
+}
+
+template <int D, int G>
+__device__ inline void klane_survivors(const ScanCtx& W, const float* hl, int ns, int tid, int tp,
+                                       uint64_t& comp, uint64_t& rechecks) {
+    constexpr int XS = ((D + 3) / 4) * 4 + 4;
+    const int per = tp / G;            // survivors per pass
+    const int g = tid / G, j = tid % G;
+    const int k = W.k;
+    const int lane = tid & 63;
+    for (int p0 = 0; p0 < ns; p0 += per) {
+        const int slot = p0 + g;
+        const bool act = slot < ns;
+        const int r = W.sq[act ? slot : p0];
+        const float* xrow = W.Xs + r * XS;
+        const int inc = W.sa[r];
+        const float u = W.su[r];
+        // Clause 2 with the loose bound: centroid j cannot beat the incumbent.
+        const bool want = act && j < k &&
+                          !(W.prune && inc >= 0 && j != inc && u <= hl[inc * k + j]);
+        float Dj = INFINITY;
+        if (want) {
+            const float* c = W.Cs + j * D;
+            float acc = 0.f;
+#pragma unroll
+            for (int m = 0; m < D; m += 4) {
+                const f32x4 xv = *reinterpret_cast<const f32x4*>(xrow + m);
+                const f32x4 cv = *reinterpret_cast<const f32x4*>(c + m);
+                float t0 = xv.x - cv.x, t1 = xv.y - cv.y, t2 = xv.z - cv.z, t3 = xv.w - cv.w;
+                acc = fmaf(t0, t0, acc);
+                acc = fmaf(t1, t1, acc);
+                acc = fmaf(t2, t2, acc);
+                acc = fmaf(t3, t3, acc);
+            }
+            Dj = acc;
+        }
+        // D >= 0, so float order equals the order of the bit patterns.
+        const uint32_t dbits = __float_as_uint(Dj);
+        const uint32_t m1 = dpp_min_u32<G>(dbits);
+        // Among the minimal lanes the incumbent wins, then the lowest index.
+        const uint32_t key = dbits == m1 && want ? (j == inc ? 0u : (uint32_t)j + 1u) : 0xFFFFFFFFu;
+        const uint32_t kmin = dpp_min_u32<G>(key);
+        const int b = kmin == 0u ? inc : (int)kmin - 1;
+        const uint32_t m2 = dpp_min_u32<G>(want && j != b ? dbits : 0x7F800000u);
+        const float Db = __uint_as_float(m1), D2 = __uint_as_float(m2);
+        const uint64_t wm = __ballot(want);
+        const int gbase = lane - j;
+        const uint64_t gm = G == 64 ? ~0ull : (((1ull << G) - 1ull) << gbase);
+        if (act && j == 0) {
+            int bb = b < 0 ? 0 : b;
+            float Dbb = Db;
+            float ub = upper_bound(Db, W.ecs[bb], W.gamma);
+            if (D2 != INFINITY) {
+                const float band = 2.f * W.gamma * (Db + D2) + 4.f * (sqrtf(Db) + sqrtf(D2)) * W.ecmax +
+                                   8.f * W.ecmax * W.ecmax;
+                if (D2 - Db <= band) {   // float64 decision, oracle's tie rule
+                    int b64 = -1;
+                    double D64 = INFINITY;
+                    if (inc >= 0) {
+                        D64 = sqd64(xrow, W.C64 + (int64_t)inc * D, D);
+                        b64 = inc;
+                    }
+                    for (int q = 0; q < k; ++q) {
+                        if (q == inc) continue;
+                        const double Dq = sqd64(xrow, W.C64 + (int64_t)q * D, D);
+                        if (Dq < D64) {
+                            D64 = Dq;
+                            b64 = q;
+                        }
+                    }
+                    bb = b64 < 0 ? 0 : b64;
+                    Dbb = (float)D64;
+                    ub = f32_up(sqrt(D64) * (1.0 + 0x1p-40));
+                    rechecks += 1;
+                }
+            }
+            W.sa[r] = bb;
+            W.su[r] = ub;
+            W.sD[r] = Dbb;
+            comp += (uint64_t)__popcll(wm & gm);
+        }
+    }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
 // Assignment + partial sums.  Block = tp threads = one tile of tp points;
 // blocks stride over tiles.  D > 0: the row lives in registers (D % 4 == 0);
 // D == 0: any d, rows read from LDS.  KB == 0: the survivors run the
@@ -206,8 +454,9 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
     const float gamma = P.gamma;
     const int xs = xs_stride(d);
 
-    const AssignLds lay = assign_lds(d, k, tp);
-    extern __shared__ __align__(16) unsigned char smem[];
+    const bool h_lds = KB == 0 && k <= kHLdsMaxK;
+    const AssignLds lay = assign_lds(d, k, tp, h_lds);
+    unsigned char* smem = km_smem;
     uint64_t* acc = reinterpret_cast<uint64_t*>(smem + lay.off_acc);
     uint32_t* cnt = reinterpret_cast<uint32_t*>(smem + lay.off_cnt);
     float* Cs = reinterpret_cast<float*>(smem + lay.off_c);
@@ -222,6 +471,10 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
     int* qlen = reinterpret_cast<int*>(smem + lay.off_misc);
     uint64_t* bst = reinterpret_cast<uint64_t*>(smem + lay.off_misc + 16);
     float* cn2s = reinterpret_cast<float*>(smem + lay.off_cn);
+    if (h_lds) {   // half-distance table: LDS copy for small k
+        float* hl = reinterpret_cast<float*>(smem + lay.off_h);
+        for (int i = tid; i < k * k; i += tp) hl[i] = P.h[i];
+    }
 
     for (int i = tid; i < k * d; i += tp) {
         Cs[i] = P.C32[i];
@@ -268,35 +521,57 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
     const int64_t ntiles = (P.n + tp - 1) / tp;
 
     // Register prefetch of the next tile: its X rows (coalesced 16-byte
-    // chunks, specialised d only) and this thread's point state, issued
-    // before the current tile is processed so global loads overlap compute.
+    // chunks, specialised d only) and this thread's point state.  The loads
+    // are branch-free (addresses clamped into the tile, so a short last tile
+    // reads valid memory and ignores the extra values) so that the compiler
+    // can keep them in flight across the whole tile body.
     constexpr int kChunks = D > 0 ? D / 4 : 1;   // 16-byte chunks per thread per tile
     f32x4 xbuf[kChunks];
-    int abuf = -1;
+    int abuf = 0;
     float ubuf = 0.f;
     auto prefetch = [&](int64_t tl) {
         const int64_t b = tl * tp;
         const int r = (int)((P.n - b) < tp ? (P.n - b) : tp);
         if constexpr (D > 0) {
             const f32x4* s4 = reinterpret_cast<const f32x4*>(P.X + b * D);
+            const int last = r * kChunks - 1;
 #pragma unroll
-            for (int i = 0; i < kChunks; ++i) {
-                const int c = tid + i * tp;
-                if (c < r * kChunks) xbuf[i] = __builtin_nontemporal_load(s4 + c);
-            }
+            for (int i = 0; i < kChunks; ++i) xbuf[i] = __builtin_nontemporal_load(s4 + min(tid + i * tp, last));
         }
-        if (!first && tid < r) {
-            abuf = P.a[b + tid];
-            ubuf = P.u[b + tid];
-        }
+        const int64_t q = b + min(tid, r - 1);
+        abuf = P.a[q];   // unset before the first step: read but not used then
+        ubuf = P.u[q];
     };
     if ((int64_t)blockIdx.x < ntiles) prefetch(blockIdx.x);
+    if (tid < 2) qlen[tid] = 0;   // visible behind the first tile's barrier
+    int it = 0;
 
-    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x, ++it) {
         const int64_t base = tile * tp;
         const int rows = (int)((P.n - base) < tp ? (P.n - base) : tp);
         __syncthreads();   // the previous tile is fully consumed
-        if (tid == 0) *qlen = 0;
+        // Two survivor counters alternate: this tile's was cleared during the
+        // previous one (behind the barrier above); clear the next tile's now.
+        if (tid == 0) qlen[(it + 1) & 1] = 0;
+        int* qn = qlen + (it & 1);
+
+        // Bound update and Clause 1 on the prefetched state (before the next
+        // prefetch reuses its registers).
+        const bool valid = tid < rows;
+        const int64_t p = base + tid;
+        int a_old = -1;
+        float u_cur = 0.f;
+        bool surv = false;
+        if (valid) {
+            if (first) {
+                surv = true;
+            } else {
+                a_old = abuf;
+                u_cur = (ubuf + fs[a_old]) * kUp;
+                if (!prune || u_cur > ss[a_old]) surv = true;
+                else my_c1 += 1;
+            }
+        }
 
         // Stage the tile in LDS.
         if constexpr (D > 0) {
@@ -316,34 +591,24 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
                 Xs[r * xs + (e - r * d)] = src[e];
             }
         }
-        const int a_pre = abuf;
-        const float u_pre = ubuf;
         if (tile + gridDim.x < ntiles) prefetch(tile + gridDim.x);
 
-        // Bound update and Clause 1.
-        const bool valid = tid < rows;
-        const int64_t p = base + tid;
-        int a_old = -1;
-        bool surv = false;
         if (valid) {
-            float u_cur = 0.f;
-            if (first) {
-                surv = true;
-            } else {
-                a_old = a_pre;
-                u_cur = (u_pre + fs[a_old]) * kUp;
-                if (!prune || u_cur > ss[a_old]) surv = true;
-                else my_c1 += 1;
-            }
             sa[tid] = a_old;
             su[tid] = u_cur;
         }
-        __syncthreads();
-        if (surv) sq[atomicAdd(qlen, 1)] = tid;
+        {   // compaction: one LDS atomic per wave, ranks from the ballot
+            const uint64_t bm = __ballot(surv);
+            const int lane = tid & 63;
+            int wbase = 0;
+            if (lane == 0 && bm) wbase = atomicAdd(qn, __popcll(bm));
+            wbase = __shfl(wbase, 0);
+            if (surv) sq[wbase + __popcll(bm & ((1ull << lane) - 1ull))] = tid;
+        }
         __syncthreads();
 
         // Survivors, compacted into sq[0, nq).
-        const int nq = *qlen;
+        const int nq = *qn;
         if constexpr (KB > 0) {
             // Matrix cores: one wave per block of 32 survivors.  Lanes l and
             // l + 32 serve survivor l % 32 and hold 16 of its centroid
@@ -463,6 +728,20 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
                     my_comp += (uint64_t)k;   // the dense pairs; refinements re-evaluate some
                 }
             }
+        } else if constexpr (D > 0) {
+            ScanCtx W{Cs, lay.off_h, P.h, ss, ecs, P.C64, Xs, sa, su, sD, sq, k, prune, gamma, ecmax};
+            const float* hl = reinterpret_cast<const float*>(km_smem + lay.off_h);
+            if (k <= 4) {
+                klane_survivors<D, 4>(W, hl, nq, tid, tp, my_comp, my_rc);
+            } else if (k <= 8) {
+                klane_survivors<D, 8>(W, hl, nq, tid, tp, my_comp, my_rc);
+            } else if (k <= 16) {
+                klane_survivors<D, 16>(W, hl, nq, tid, tp, my_comp, my_rc);
+            } else if (h_lds) {
+                grouped_survivors<D, 1, true>(W, nq, tid, tp, my_comp, my_rc);
+            } else {
+                grouped_survivors<D, 1, false>(W, nq, tid, tp, my_comp, my_rc);
+            }
         } else {
             for (int qi = tid; qi < nq; qi += tp) {
                 const int r = sq[qi];
@@ -497,7 +776,9 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
                 if (!skip_all) {
                     for (int j = 0; j < k; ++j) {
                         if (j == inc) continue;
-                        if (prune && b >= 0 && ub <= P.h[(int64_t)b * k + j]) continue;   // Clause 2/3
+                        const float hv = h_lds ? reinterpret_cast<const float*>(smem + lay.off_h)[b * k + j]
+                                           : P.h[(int64_t)b * k + j];
+                    if (prune && b >= 0 && ub <= hv) continue;   // Clause 2/3
                         const float Dj = dist(j);
                         nc += 1;
                         if (Dj < Db) {
@@ -571,13 +852,27 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
         }
 
         // Per-cluster coordinate sums of every point of the tile (pruned or
-        // not), as exact fixed-point integers in LDS.
-        const int ne = rows * d;
-        for (int e = tid; e < ne; e += tp) {
-            const int r = e / d, m = e - r * d;
-            const uint64_t bits = fixed_bits((double)Xs[r * xs + m], P.qscale);
-            atomicAdd(reinterpret_cast<unsigned long long*>(&acc[sa[r] * d + m]),
-                      (unsigned long long)bits);
+        // not), as exact fixed-point integers in LDS.  Thread t adds
+        // coordinate t % d of rows t / d, t / d + tp / d, ...
+        if constexpr (D > 0) {
+            if (tp % D == 0) {
+                const int m = tid % D, r0 = tid / D, rstep = tp / D;
+                const int nr = (rows - r0 + rstep - 1) / rstep;
+                for (int i = 0; i < nr; ++i) {
+                    const int r = r0 + i * rstep;
+                    const uint64_t bits = fixed_bits((double)Xs[r * xs + m], P.qscale);
+                    const uint32_t slot = (uint32_t)sa[r] * (uint32_t)D + (uint32_t)m;
+                    atomicAdd(reinterpret_cast<unsigned long long*>(&acc[slot]), (unsigned long long)bits);
+                }
+            }
+        } else {
+            const int ne = rows * d;
+            for (int e = tid; e < ne; e += tp) {
+                const int r = e / d, m = e - r * d;
+                const uint64_t bits = fixed_bits((double)Xs[r * xs + m], P.qscale);
+                atomicAdd(reinterpret_cast<unsigned long long*>(&acc[sa[r] * d + m]),
+                          (unsigned long long)bits);
+            }
         }
     }
     __syncthreads();
