@@ -72,8 +72,11 @@ enum {
     KM_FLAG_TIMING = 8u,       /* record HIP events around every kernel (kmeans_mti_get_timing) */
     KM_FLAG_VECTOR_ONLY = 16u, /* use the per-point vector distance loop even where the
                                   matrix-core (MFMA) survivor path applies; same results */
-    KM_FLAG_LARGE_PATH = 32u   /* use the global-memory path (dense MFMA survivors, sums by
+    KM_FLAG_LARGE_PATH = 32u,  /* use the global-memory path (dense MFMA survivors, sums by
                                   counting sort) even where the LDS path fits; same results */
+    KM_FLAG_GENERIC = 64u      /* use the general assignment kernel and separate reduction,
+                                  update and table launches even where the one-launch
+                                  streaming step (d = 16, k <= 16) applies; same results */
 };
 
 /* Totals over the iterations run so far (kmeans_mti_get_stats, kmeans_mti_run). */

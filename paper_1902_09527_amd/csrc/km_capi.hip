@@ -79,6 +79,8 @@ struct km_ctx {
     int tp = 0, lds = 0;
     int variant = 0;   // assignment-kernel specialisation
     bool large = false;   // global-memory path (centroids / sums too large for LDS)
+    bool small = false;   // one-launch streaming step (d = 16, k <= 16)
+    km::Fused fz{};
     km::Large lg{};
     int gb = 0;           // blocks of the large path's bound pass
     km::Dev dv{};
@@ -155,6 +157,18 @@ int enqueue_iteration(km_ctx* c) {
     }
     auto mark = [&](int i) -> hipError_t { return ev ? hipEventRecord(ev[i], c->stream) : hipSuccess; };
     if ((e = mark(0)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
+    if (c->small) {   // two launches: streaming step, then the finishing block (update slot)
+        if ((e = km::launch_small(c->dv, c->fz, c->lds, c->stream)) != hipSuccess)
+            return fail_ctx(c, hip_fail(e, "streaming step kernel"));
+        if ((e = mark(1)) != hipSuccess || (e = mark(2)) != hipSuccess)
+            return fail_ctx(c, hip_fail(e, "hipEventRecord"));
+        if ((e = km::launch_small_finish(c->dv, c->fz, c->stream)) != hipSuccess)
+            return fail_ctx(c, hip_fail(e, "streaming step finish kernel"));
+        if ((e = mark(3)) != hipSuccess || (e = mark(4)) != hipSuccess)
+            return fail_ctx(c, hip_fail(e, "hipEventRecord"));
+        c->stepped = true;
+        return KM_OK;
+    }
     e = c->large ? km::launch_large_assign(c->dv, c->lg, c->gb, c->stream)
                  : km::launch_assign(c->dv, c->variant, c->tp, c->lds, c->stream);
     if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "assign kernel"));
@@ -205,9 +219,23 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     // LDS path: the largest tile of 256/128/64 points whose LDS image
     // (centroids, fixed-point sums, X tile) fits; else the global-memory path.
     c->tp = 0;
-    if (!(c->flags & KM_FLAG_LARGE_PATH)) {
-        c->variant = km::assign_variant(d, k, reinterpret_cast<uintptr_t>(X) % 16 == 0,
-                                        (c->flags & KM_FLAG_VECTOR_ONLY) != 0);
+    const bool aligned = reinterpret_cast<uintptr_t>(X) % 16 == 0;
+    if (!(c->flags & (KM_FLAG_LARGE_PATH | KM_FLAG_GENERIC)) && km::small_applies(d, k, aligned)) {
+        c->small = true;
+        c->tp = km::kSmallTile;
+        c->lds = km::small_lds_bytes(k);
+        if (c->lds > max_lds || km::small_finish_lds_bytes(k) > max_lds) return KM_ERR_UNSUPPORTED;
+        const void* sym = km::small_kernel_symbol(k);
+        KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds));
+        int per_cu = 0;
+        KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, c->tp, c->lds));
+        if (per_cu < 1) return KM_ERR_UNSUPPORTED;
+        const int64_t ntiles = (n + c->tp - 1) / c->tp;
+        int64_t G = (int64_t)per_cu * cus;
+        if (G > ntiles) G = ntiles;
+        v.G = (int32_t)G;
+    } else if (!(c->flags & KM_FLAG_LARGE_PATH)) {
+        c->variant = km::assign_variant(d, k, aligned, (c->flags & KM_FLAG_VECTOR_ONLY) != 0);
         const bool h_lds = c->variant % 16 == 0 && k <= km::kHLdsMaxK;
         for (int tp = 256; c->tp == 0 && tp >= 64; tp /= 2) {
             int bytes = km::assign_lds(d, k, tp, h_lds).bytes;
@@ -217,7 +245,9 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             }
         }
     }
-    if (c->tp > 0) {
+    if (c->small) {
+        // configured above
+    } else if (c->tp > 0) {
         const void* sym = km::assign_kernel_symbol(c->variant);
         KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds));
         int per_cu = 0;
@@ -271,6 +301,10 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         (rc = c->alloc(&v.part, (size_t)v.G * v.L)) || (rc = c->alloc(&v.total, (size_t)v.L)) ||
         (rc = c->alloc(&v.st, 1)) || (rc = c->alloc(&v.rec, (size_t)km::kHistCap)))
         return rc;
+    if (c->small) {
+        if ((rc = c->alloc(&c->fz.rows, (size_t)km::kSmallRows * v.L))) return rc;
+        KM_HIP(hipMemsetAsync(c->fz.rows, 0, sizeof(uint64_t) * (size_t)km::kSmallRows * v.L, c->stream));
+    }
     uint32_t* scratch = nullptr;
     if ((rc = c->alloc(&scratch, 4))) return rc;
 
@@ -345,7 +379,7 @@ int kmeans_mti_init(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t 
     int rc = check_shape(X, n, d, k, C0);
     if (rc != KM_OK) return rc;
     if (flags & ~(uint32_t)(KM_FLAG_NO_PRUNE | KM_FLAG_STATS | KM_FLAG_VALIDATE | KM_FLAG_TIMING |
-                            KM_FLAG_VECTOR_ONLY | KM_FLAG_LARGE_PATH))
+                            KM_FLAG_VECTOR_ONLY | KM_FLAG_LARGE_PATH | KM_FLAG_GENERIC))
         return KM_ERR_INVALID_ARG;
     km_ctx* c = new (std::nothrow) km_ctx;
     if (!c) return KM_ERR_OOM;

@@ -147,6 +147,64 @@ __host__ __device__ inline AssignLds assign_lds(int d, int k, int tp, bool h_lds
     return L;
 }
 
+// Streaming path for small k and d = 16 (km_small.hip): the streaming kernel,
+// then one block that reduces, updates and rebuilds the centroid table.
+constexpr int kSmallTile = 256;   // points per tile = threads per block
+constexpr int kSmallMaxK = 16;
+constexpr int kSmallCopies = 4;   // copies of the LDS sums (spread rows over banks and addresses)
+
+// Accumulation rows of the streaming step: block b adds its partial row into
+// row b % kSmallRows with device atomics; the finishing block sums and clears
+// them.
+constexpr int kSmallRows = 16;
+struct Fused {
+    uint64_t* rows;       // kSmallRows x L, zero between steps
+};
+
+struct SmallLds {
+    int off_c, off_f, off_s, off_ec, off_h, off_acc, off_cnt, off_x, off_sq, off_sa, off_su, off_misc, bytes;
+    int csu, kp;          // row stride (uint64) of one copy of the sums; of one copy of the counts
+};
+
+__host__ __device__ inline SmallLds small_lds(int k) {
+    SmallLds L;
+    int o = 0;
+    auto take = [&](int bytes, int align) {
+        o = (o + align - 1) / align * align;
+        int r = o;
+        o += bytes;
+        return r;
+    };
+    L.csu = 16 * k + 1;   // odd: the copies start on different banks
+    L.kp = k + 1;
+    L.off_c = take(4 * k * 20, 16);
+    L.off_f = take(4 * k, 16);
+    L.off_s = take(4 * k, 16);
+    L.off_ec = take(4 * k, 16);
+    L.off_h = take(4 * k * k, 16);
+    L.off_acc = take(8 * kSmallCopies * L.csu, 16);
+    L.off_cnt = take(4 * kSmallCopies * L.kp, 16);
+    L.off_x = take(4 * kSmallTile * 20, 16);
+    L.off_sq = take(4 * kSmallTile, 16);
+    L.off_sa = take(4 * kSmallTile, 16);
+    L.off_su = take(4 * kSmallTile, 16);
+    L.off_misc = take(64, 16);
+    L.bytes = (o + 15) / 16 * 16;
+    return L;
+}
+
+// LDS bytes of the finishing block (totals, centroids, drift terms, table).
+__host__ __device__ inline int finish_lds(int d, int k) {
+    return 8 * row_len(d, k) + 3 * 8 * k * d + 4 * k * k + 4 * k;
+}
+
+bool small_applies(int d, int k, bool aligned);
+const void* small_kernel_symbol(int k);
+int small_lds_bytes(int k);
+int small_finish_lds_bytes(int k);
+hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, hipStream_t s);
+hipError_t launch_small_finish(const Dev& dv, const Fused& F, hipStream_t s);
+
 // Global-memory path launchers (km_large.hip).  gb: blocks of the bound pass.
 hipError_t launch_large_assign(const Dev& dv, const Large& lg, int gb, hipStream_t s);
 hipError_t launch_large_reduce(const Dev& dv, const Large& lg, hipStream_t s);

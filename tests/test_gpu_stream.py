@@ -1,0 +1,111 @@
+"""The one-launch streaming step (d = 16, k <= 16) against the oracle and
+against the general kernels (KM_FLAG_GENERIC), through the C ABI.
+
+Sizes span one partial tile, several tiles per block, and enough blocks for
+several completion groups (the group and final reductions of the last
+blocks); every case has a ragged last tile.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from parity import check_assign, check_centroids
+
+import paper_1902_09527_amd as km
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _gpu(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(DEV)
+
+
+CASES = [
+    # seed, n, k, spread, sigma, iters, tol
+    (101, 1, 1, 3.0, 1.0, 3, 0.0),
+    (102, 37, 5, 3.0, 1.0, 10, 0.0),
+    (103, 255, 16, 2.0, 1.0, 15, 0.0),
+    (104, 3 * 256 + 1, 2, 1.0, 1.0, 20, 0.0),
+    (105, 20000 + 13, 10, 3.0, 2.0, 30, 0.0),
+    (106, 50000 + 77, 16, 1.5, 1.5, 30, 0.001),
+    (107, 400000 + 5, 10, 4.0, 2.0, 12, 0.0),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "s%d-n%d-k%d" % c[:3])
+def test_stream_matches_oracle(case):
+    seed, n, k, spread, sigma, iters, tol = case
+    print("case", case, flush=True)
+    X, C0 = synth.blobs(n, 16, k, seed=seed, spread=spread, sigma=sigma)
+    ref = oracle.lloyd(X, C0, iters, tol)
+    a, c, st = km.run(_gpu(X), _gpu(C0), iters, tol, stats=True)
+    assert st["iterations"] == ref["iters"]
+    check_assign(a.cpu().numpy(), ref["assign"], ref["best"], ref["second"], "final assignment")
+    check_centroids(c.cpu().numpy(), ref["C"], X, "final centroids")
+    assert st["inertia_last"] == pytest.approx(ref["inertia"][-1], rel=1e-5)
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "s%d-n%d-k%d" % c[:3])
+@pytest.mark.parametrize("prune", [True, False], ids=["prune", "noprune"])
+def test_stream_is_bitwise_identical_to_generic_path(case, prune):
+    seed, n, k, spread, sigma, iters, tol = case
+    print("case", case, prune, flush=True)
+    X, C0 = synth.blobs(n, 16, k, seed=seed, spread=spread, sigma=sigma)
+    Xg, Cg = _gpu(X), _gpu(C0)
+    hists, outs = [], []
+    for generic in (False, True):
+        with km.KMeansMTI(Xg, Cg, prune=prune, stats=True, generic=generic) as ctx:
+            for _ in range(iters):
+                ctx.iterate()
+            a, c = ctx.get()
+            outs.append((a.cpu().numpy(), c.cpu().numpy(), ctx.centroids64()))
+            hists.append(ctx.history())
+    np.testing.assert_array_equal(outs[0][0], outs[1][0])
+    np.testing.assert_array_equal(outs[0][1], outs[1][1])
+    np.testing.assert_array_equal(outs[0][2], outs[1][2])
+    np.testing.assert_array_equal(hists[0]["changed"], hists[1]["changed"])
+    np.testing.assert_allclose(hists[0]["inertia"], hists[1]["inertia"], rtol=1e-12)
+    if not prune:
+        assert (hists[0]["computed"] == n * k).all()
+
+
+def test_stream_trajectory_and_history():
+    X, C0 = synth.blobs(60000 + 3, 16, 10, seed=111, spread=3.0, sigma=2.0)
+    T = 12
+    ref = oracle.lloyd(X, C0, T, history=True)
+    with km.KMeansMTI(_gpu(X), _gpu(C0), stats=True, timing=True) as ctx:
+        for t in range(T):
+            ch = ctx.iterate(sync=True)
+            a, c = ctx.get()
+            prev = None if t == 0 else ref["assign_hist"][t - 1]
+            _, b, s, _ = oracle.assign(X, ref["C_hist"][t], prev=prev)
+            info = check_assign(a.cpu().numpy(), ref["assign_hist"][t], b, s, "step %d" % t)
+            if info["mismatch"] == 0:
+                assert ch == ref["changed"][t]
+            check_centroids(c.cpu().numpy(), ref["C_hist"][t + 1], X, "step %d" % t)
+            np.testing.assert_allclose(ctx.centroids64(), ref["C_hist"][t + 1], rtol=1e-9, atol=1e-9)
+        h = ctx.history()
+        tm = ctx.timing()
+    np.testing.assert_array_equal(h["changed"], ref["changed"])
+    np.testing.assert_allclose(h["inertia"], ref["inertia"], rtol=1e-5)
+    assert (h["computed"] <= X.shape[0] * 10).all() and h["clause1"][0] == 0
+    assert tm["iters"] == T and tm["assign_ms"] > 0
+    # two launches per step (streaming kernel, finishing block in the update
+    # slot): the reduce and table intervals enclose no kernel
+    assert tm["update_ms"] > 0 and tm["reduce_ms"] + tm["table_ms"] < 0.02 * T
+
+
+def test_stream_repeated_runs_reuse_accumulation_rows():
+    # Many steps per context, two contexts: the accumulation rows must be
+    # back at zero after every step, or a later step would double count.
+    X, C0 = synth.blobs(300000 + 11, 16, 8, seed=121, spread=3.0, sigma=1.5)
+    ref = oracle.lloyd(X, C0, 40, 0.0)
+    Xg, Cg = _gpu(X), _gpu(C0)
+    for _ in range(2):
+        a, c, st = km.run(Xg, Cg, 40, 0.0)
+        assert st["iterations"] == ref["iters"]
+        check_assign(a.cpu().numpy(), ref["assign"], ref["best"], ref["second"], "final assignment")
+        check_centroids(c.cpu().numpy(), ref["C"], X, "final centroids")
