@@ -32,6 +32,49 @@ def log(msg: str) -> None:
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
+# Dominant (assignment-step) kernel of each library path.
+DOMINANT_KERNEL = {"stream-d16": "k_small", "lds-vector": "k_assign", "lds-mfma": "k_assign",
+                   "global-mfma": "k_mfma_large"}
+# Sources of each dominant kernel: the hardware byte counts of a committed
+# profile summary are used only while these files are unchanged.
+KERNEL_SOURCES = {
+    "k_small": ["km_small.hip", "km_device.h", "km_internal.h"],
+    "k_assign": ["km_kernels.hip", "km_device.h", "km_internal.h"],
+    "k_mfma_large": ["km_large.hip", "km_device.h", "km_internal.h"],
+}
+
+
+def kernel_source_hash(kernel: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES.get(kernel, []):
+        with open(os.path.join(ROOT, "paper_1902_09527_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the rocprofv3 FETCH_SIZE / WRITE_SIZE summary in
+    profiles/<kernel>_<workload>.txt, scaled by the plain-copy calibration
+    recorded there; None when there is no summary or the kernel changed."""
+    path = os.path.join(ROOT, "profiles", "%s_%s.txt" % (kernel, workload))
+    if not os.path.exists(path):
+        return None, "no profile summary"
+    vals = {}
+    for line in open(path):
+        if "=" in line and line.strip().startswith("pmc."):
+            key, val = line.split("=", 1)
+            vals[key.strip()] = val.strip()
+    try:
+        if vals["pmc.kernel_source_sha256"] != kernel_source_hash(kernel):
+            return None, "kernel changed since the counters were taken"
+        fetch = float(vals["pmc.FETCH_SIZE_KiB_per_dispatch"]) * float(vals["pmc.FETCH_SIZE_scale"])
+        write = float(vals["pmc.WRITE_SIZE_KiB_per_dispatch"]) * float(vals["pmc.WRITE_SIZE_scale"])
+    except (KeyError, ValueError):
+        return None, "incomplete profile summary"
+    return (fetch + write) * 1024.0, os.path.relpath(path, ROOT)
+
+
 def cpu_baseline(X, C0, w, budget_s: float = 15.0) -> dict:
     """Time the CPU oracle (plain float64 Lloyd's, as it stands) on this host."""
     import oracle
@@ -55,11 +98,13 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed iterations (default: workload max_iters)")
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(
+        ["blobs-10k-d16-k8", "blobs-1M-d32-k100", "aniso-8M-d16-k10", "blobs-2M-d256-k1000",
+         "zipf-100M-d32-k64"]))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile", action="store_true",
-                    help="run only the timed region (no warmup context, no job run, no CPU leg), "
-                         "so a profiler's per-kernel averages cover exactly the timed launches")
+                    help="run only the warmup and the timed region (no event pass, no job run, no "
+                         "CPU leg), so a profiler sees warmup + K launches of each kernel")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run 5 plain device-to-device copies of 512 MiB (reference kernel "
                          "for scaling hardware byte counters)")
@@ -97,7 +142,6 @@ def main() -> int:
 
     # Warmup: W iterations on a throwaway context (kernel load, caches, clocks).
     if args.profile:
-        args.warmup = 0
         args.no_cpu_baseline = True
     if args.warmup > 0:
         with km.KMeansMTI(Xg, Cg) as ctx:
@@ -106,19 +150,27 @@ def main() -> int:
             torch.cuda.synchronize()
     log("warmup done (%d iterations)" % args.warmup)
 
-    # Timed region: K iterations from C0.
-    ctx = km.KMeansMTI(Xg, Cg, timing=True)
+    # Timed region: K iterations from C0, nothing else on the stream.
+    ctx = km.KMeansMTI(Xg, Cg)
+    path = ctx.path()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(K):
         ctx.iterate()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    tm = ctx.timing()
     hist = ctx.history()
-    st = ctx.stats()
     ctx.close()
-    log("timed %d iterations in %.3f ms" % (K, elapsed * 1e3))
+    log("timed %d iterations in %.3f ms (path %s)" % (K, elapsed * 1e3, path))
+
+    # The same K iterations again with HIP events around every launch (on the
+    # library's stream) for the per-kernel device times.
+    tm = None
+    if not args.profile:
+        with km.KMeansMTI(Xg, Cg, timing=True) as tctx:
+            for _ in range(K):
+                tctx.iterate()
+            tm = tctx.timing()
 
     # The job as the workload defines it (tol stop), for the iteration count.
     job = {"iterations": 0, "converged": 0, "device_ms": 0.0}
@@ -129,10 +181,21 @@ def main() -> int:
     n, d, k = w.n, w.d, w.k
     ips = K / elapsed
     computed = int(hist["computed"].sum())
+    changed = int(hist["changed"].sum())
     lloyd = n * k * K
-    assign_avg_s = tm["assign_ms"] / max(1, tm["iters"]) / 1e3
-    bytes_per_launch = n * (4 * d + 12)       # X row + assignment read + bound read/write
-    achieved = bytes_per_launch / assign_avg_s / 1e9
+    kernel = DOMINANT_KERNEL.get(path, path)
+    # Algorithmic bytes of one launch of the dominant kernel: one read of X,
+    # the assignment read, the bound read and write, and the assignment
+    # writes of the points that changed (averaged over the timed steps).
+    bytes_per_launch = n * (4 * d + 12) + 4 * changed / K
+    roof = {"kernel": kernel, "bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": None, "traffic": None, "bytes_per_launch": bytes_per_launch}
+    if tm is not None:
+        assign_avg_s = tm["assign_ms"] / max(1, tm["iters"]) / 1e3
+        roof["achieved"] = bytes_per_launch / assign_avg_s / 1e9
+        roof["frac"] = roof["achieved"] / HBM_PEAK_GBS
+        roof["kernel_us"] = assign_avg_s * 1e6
+    roof["traffic"], roof["traffic_source"] = measured_traffic(kernel, w.name)
     result = {
         "metric": METRIC,
         "value": ips,
@@ -147,19 +210,17 @@ def main() -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "n": n, "d": d, "k": k, "max_iters": w.max_iters, "tol": w.tol,
-                   "timed": "first %d iterations from the seeded centroids" % K},
+                   "timed": "first %d iterations from the seeded centroids" % K, "path": path},
         "eff_dist_evals_per_s": lloyd / elapsed,
         "computed_dist_evals_per_s": computed / elapsed,
         "pruned_frac": 1.0 - computed / lloyd,
         "clause1_frac": float(hist["clause1"].sum()) / (n * K),
-        "kernel_ms_per_iter": {key[:-3]: tm[key] / max(1, tm["iters"])
-                               for key in ("assign_ms", "reduce_ms", "update_ms", "table_ms")},
+        "kernel_ms_per_iter": None if tm is None else
+            {key[:-3]: tm[key] / max(1, tm["iters"]) for key in ("assign_ms", "reduce_ms", "update_ms", "table_ms")},
         "job": {"iterations": job["iterations"], "converged": bool(job["converged"]),
                 "device_ms": job["device_ms"],
                 "iters_per_s": job["iterations"] / (job["device_ms"] / 1e3) if job["device_ms"] else None},
-        "roofline": {"kernel": "k_assign", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "bytes_per_launch": bytes_per_launch},
+        "roofline": roof,
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")

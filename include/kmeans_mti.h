@@ -158,6 +158,16 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
                    int32_t max_iters, double tol, int32_t* assign_out, float* C_out,
                    void* hip_stream, uint32_t flags, km_stats* stats);
 
+/*
+ * Name of the kernel path the context uses, a static string: "stream-d16"
+ * (d = 16, k <= 16: streaming kernel k_small + one-block finish
+ * k_small_finish), "lds-vector" / "lds-mfma" (centroids and sums in LDS:
+ * k_assign with vector or matrix-core survivors, then k_reduce, k_update,
+ * k_centroid_table), "global-mfma" (centroids or sums too large for LDS:
+ * dense MFMA survivors, sums by counting sort).  "" for a NULL context.
+ */
+const char* kmeans_mti_path(const km_ctx* ctx);
+
 /* Release a context and its device scratch.  NULL-safe.  Synchronizes. */
 void kmeans_mti_destroy(km_ctx* ctx);
 

@@ -30,7 +30,7 @@ KM_FLAG_GENERIC = 64
 EXPORTS = (
     "kmeans_mti_init", "kmeans_mti_iterate", "kmeans_mti_get", "kmeans_mti_get_centroids64",
     "kmeans_mti_get_stats", "kmeans_mti_get_history", "kmeans_mti_get_timing", "kmeans_mti_run",
-    "kmeans_mti_destroy",
+    "kmeans_mti_path", "kmeans_mti_destroy",
     "kmeans_mti_strerror", "kmeans_mti_last_hip_error",
 )
 
@@ -90,6 +90,8 @@ def load() -> C.CDLL:
     lib.kmeans_mti_get_timing.restype = C.c_int
     lib.kmeans_mti_run.argtypes = [P, i64, i32, i32, P, i32, f64, P, P, P, u32, C.POINTER(KmStats)]
     lib.kmeans_mti_run.restype = C.c_int
+    lib.kmeans_mti_path.argtypes = [P]
+    lib.kmeans_mti_path.restype = C.c_char_p
     lib.kmeans_mti_destroy.argtypes = [P]
     lib.kmeans_mti_destroy.restype = None
     lib.kmeans_mti_strerror.argtypes = [C.c_int]

@@ -595,6 +595,13 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
 #undef RUN_HIP
 }
 
+const char* kmeans_mti_path(const km_ctx* ctx) {
+    if (!ctx) return "";
+    if (ctx->small) return "stream-d16";
+    if (ctx->large) return "global-mfma";
+    return ctx->variant % 16 ? "lds-mfma" : "lds-vector";
+}
+
 void kmeans_mti_destroy(km_ctx* ctx) { delete ctx; }
 
 const char* kmeans_mti_strerror(int status) {

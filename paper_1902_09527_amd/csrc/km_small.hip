@@ -7,11 +7,14 @@
 //      Clause 1 (section III-C, Table I);
 //   2. adds every point to the fixed-point sums of its PREVIOUS cluster
 //      (no dependence on the distance work, so it overlaps the stream);
-//   3. compacts the Clause-1 survivors into a queue and gives each survivor a
-//      group of G >= k lanes, lane j evaluating centroid j unless Clause 2
-//      skips it (u <= h(a, c), Elkan's lemma); the group takes the minimum
-//      with the oracle's tie rule and the second-best value with DPP row
-//      reductions, and near ties are decided in float64;
+//   3. compacts the Clause-1 survivors into a queue; a tile with many
+//      survivors gives each one lane that scans the centroids in index order,
+//      skipping a centroid for the whole wave when Clause 2 (u <= h(a, c),
+//      Elkan's lemma) holds for every lane; a tile with few gives each
+//      survivor a group of G >= k lanes, lane j evaluating centroid j unless
+//      Clause 2 skips it, and the group takes the minimum with the oracle's
+//      tie rule and the second-best value with DPP row reductions; near ties
+//      are decided in float64;
 //   4. moves a point whose assignment changed from its old cluster's sums to
 //      the new one (exact integer subtraction and addition, one coordinate
 //      per lane of the group).
@@ -39,6 +42,7 @@ namespace {
 constexpr int kTp = kSmallTile;    // points per tile = threads per block
 constexpr int kCopies = kSmallCopies;
 constexpr int kFinishThreads = 256;   // threads of the finishing block
+constexpr int kLaneScanMin = 32;      // more survivors per tile: one lane per survivor
 
 template <int D>
 __device__ inline float sqd_row(const float (&x)[D], const float* c) {
@@ -270,9 +274,86 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
             my_iq += fixed_bits((double)sqd_row<D>(x, Cs + a_old * CR), P.iscale) - kMagicBits;
         }
 
-        // 3. Survivors: a group of G lanes each, lane j for centroid j.
+        // 3. Survivors.  Many (early steps): one lane each, scanning the
+        //    centroids in index order.  Few (later steps): a group of G
+        //    lanes each, lane j for centroid j.
         const int nq = *qn;
-        for (int p0 = 0; p0 < nq; p0 += PER) {
+        if (nq > kLaneScanMin) {
+            if (tid < nq) {
+                const int e = sq[tid];
+                const int r = e & 0xffff, inc = (e >> 16) - 1;
+                const float* xrow = Xs + r * XS;
+                const float u = su[r];
+                float x[D];
+#pragma unroll
+                for (int m = 0; m < D; m += 4) {
+                    const f32x4 v = *reinterpret_cast<const f32x4*>(xrow + m);
+                    x[m] = v.x;
+                    x[m + 1] = v.y;
+                    x[m + 2] = v.z;
+                    x[m + 3] = v.w;
+                }
+                // Best so far under the oracle's order: smaller distance, then
+                // the incumbent, then the lower index (key 0 = incumbent).
+                int b = -1;
+                uint32_t kb = 0xFFFFFFFFu;
+                float Db = INFINITY, D2 = INFINITY;
+                uint64_t nc = 0;
+                for (int jj = 0; jj < k; ++jj) {
+                    // Clause 2: c_jj cannot be strictly closer than the incumbent.
+                    const bool need = !(prune && inc >= 0 && jj != inc && u <= hs[max(inc, 0) * k + jj]);
+                    if (!__any(need)) continue;   // the whole wave skips c_jj
+                    const float Dj = sqd_row<D>(x, Cs + jj * CR);
+                    if (need) {
+                        nc += 1;
+                        const uint32_t key = jj == inc ? 0u : (uint32_t)jj + 1u;
+                        if (Dj < Db || (Dj == Db && key < kb)) {
+                            D2 = Db;
+                            Db = Dj;
+                            b = jj;
+                            kb = key;
+                        } else {
+                            D2 = fminf(D2, Dj);
+                        }
+                    }
+                }
+                if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
+                float ub = upper_bound(Db, ecs[b], gamma);
+                bool re = false;
+                if (D2 != INFINITY) {
+                    const float band = 2.f * gamma * (Db + D2) + 4.f * (sqrtf(Db) + sqrtf(D2)) * ecmax +
+                                       8.f * ecmax * ecmax;
+                    re = D2 - Db <= band;
+                }
+                if (re) {
+                    b = recheck64(xrow, P.C64, D, k, inc, Db, ub);
+                    my_rc += 1;
+                }
+                const int64_t pr = base + r;
+                P.u[pr] = ub;
+                my_comp += nc;
+                if (want_inertia) my_iq += fixed_bits((double)Db, P.iscale) - kMagicBits;
+                if (b != inc) {
+                    P.a[pr] = b;
+                    my_changed += 1;
+                }
+                if (first) {
+                    sa[r] = b;
+                } else if (b != inc) {   // 4. move the point's sums from inc to b
+                    const int cp = tid & (kCopies - 1);
+                    uint64_t* to = acc + cp * csu + b * D;
+                    uint64_t* from = acc + cp * csu + inc * D;
+#pragma unroll
+                    for (int m = 0; m < D; ++m) {
+                        const uint64_t v = fixed_bits((double)x[m], P.qscale);
+                        atomicAdd(reinterpret_cast<unsigned long long*>(to + m), (unsigned long long)v);
+                        atomicAdd(reinterpret_cast<unsigned long long*>(from + m), (unsigned long long)(0 - v));
+                    }
+                    atomicAdd(&cnt[cp * kp + b], 1u);
+                    atomicAdd(&cnt[cp * kp + inc], 0xFFFFFFFFu);
+                }
+            }
+        } else for (int p0 = 0; p0 < nq; p0 += PER) {
             const int slot = p0 + g;
             const bool act = slot < nq;
             const int e = sq[act ? slot : p0];
@@ -409,7 +490,6 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
 __global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F) {
     constexpr int nt = kFinishThreads;
     IterState* st = P.st;
-    if (!st->active) return;
     const int tid = threadIdx.x;
     const int k = P.k, d = P.d, L = P.L;
     uint64_t* tot = reinterpret_cast<uint64_t*>(km_smem);
@@ -425,6 +505,8 @@ __global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F)
         const int e = tid + q * nt;
         cold[q] = e < k * d ? P.C64[e] : 0.0;
     }
+    // (Issued before the state flag is known: the loads are in bounds either way.)
+    const bool active = st->active != 0;
     for (int col = tid; col < L; col += nt) {
         uint64_t t[kSmallRows];
 #pragma unroll
@@ -433,9 +515,12 @@ __global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F)
 #pragma unroll
         for (int r = 0; r < kSmallRows; ++r) v += t[r];
         tot[col] = v;
+        if (active) {
 #pragma unroll
-        for (int r = 0; r < kSmallRows; ++r) F.rows[(int64_t)r * L + col] = 0;
+            for (int r = 0; r < kSmallRows; ++r) F.rows[(int64_t)r * L + col] = 0;
+        }
     }
+    if (!active) return;
     __syncthreads();
     // New centroids: member means of the exact sums; empty clusters keep theirs.
 #pragma unroll

@@ -136,6 +136,10 @@ class KMeansMTI:
             N.check(m, "kmeans_mti_get_history")
         return {name: a[:m] for name, a in arrs.items()}
 
+    def path(self) -> str:
+        """Kernel path of this context (kmeans_mti_path)."""
+        return self._lib.kmeans_mti_path(self._live()).decode()
+
     def timing(self) -> Dict[str, float]:
         """Per-kernel device milliseconds (HIP events) over the iterations so far."""
         ms = (C.c_double * 4)()

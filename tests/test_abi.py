@@ -41,6 +41,10 @@ def test_status_texts():
     assert isinstance(lib.kmeans_mti_last_hip_error(), bytes)
 
 
+def test_path_of_null_context_is_empty():
+    assert N.load().kmeans_mti_path(None) == b""
+
+
 def test_struct_layout_matches_header():
     # int32 x2, int64 x5, double x2 with natural alignment
     assert C.sizeof(N.KmStats) == 4 * 2 + 8 * 5 + 8 * 2

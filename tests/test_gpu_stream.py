@@ -109,3 +109,13 @@ def test_stream_repeated_runs_reuse_accumulation_rows():
         assert st["iterations"] == ref["iters"]
         check_assign(a.cpu().numpy(), ref["assign"], ref["best"], ref["second"], "final assignment")
         check_centroids(c.cpu().numpy(), ref["C"], X, "final centroids")
+
+
+@pytest.mark.parametrize("d,k,flags,path", [
+    (16, 10, {}, "stream-d16"), (16, 16, {}, "stream-d16"), (16, 10, {"generic": True}, "lds-vector"),
+    (16, 17, {}, "lds-mfma"), (32, 10, {}, "lds-vector"), (16, 10, {"large_path": True}, "global-mfma"),
+])
+def test_path_selection(d, k, flags, path):
+    X, C0 = synth.blobs(1000, d, k, seed=131)
+    with km.KMeansMTI(_gpu(X), _gpu(C0), **flags) as ctx:
+        assert ctx.path() == path
