@@ -74,9 +74,14 @@ enum {
                                   matrix-core (MFMA) survivor path applies; same results */
     KM_FLAG_LARGE_PATH = 32u,  /* use the global-memory path (dense MFMA survivors, sums by
                                   counting sort) even where the LDS path fits; same results */
-    KM_FLAG_GENERIC = 64u      /* use the general assignment kernel and separate reduction,
-                                  update and table launches even where the one-launch
-                                  streaming step (d = 16, k <= 16) applies; same results */
+    KM_FLAG_GENERIC = 64u,     /* use the general assignment kernel and separate reduction,
+                                  update and table launches even where the streaming step
+                                  (d = 16, k <= 16) applies; same results */
+    KM_FLAG_FULL_SUMS = 128u   /* streaming step: recompute the per-cluster sums from every
+                                  point (one full read of X) in every step instead of moving
+                                  the sums of the points whose assignment changed (after the
+                                  first step only the Clause-1 survivors' rows are read);
+                                  same results.  Implied by KM_FLAG_STATS. */
 };
 
 /* Totals over the iterations run so far (kmeans_mti_get_stats, kmeans_mti_run). */
@@ -160,8 +165,10 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
 
 /*
  * Name of the kernel path the context uses, a static string: "stream-d16"
- * (d = 16, k <= 16: streaming kernel k_small + one-block finish
- * k_small_finish), "lds-vector" / "lds-mfma" (centroids and sums in LDS:
+ * (d = 16, k <= 16: streaming kernel k_small in the first step, incremental
+ * kernel k_inc after it, each followed by the one-block finish
+ * k_small_finish), "stream-d16-full" (the same with KM_FLAG_FULL_SUMS or
+ * KM_FLAG_STATS: k_small every step), "lds-vector" / "lds-mfma" (centroids and sums in LDS:
  * k_assign with vector or matrix-core survivors, then k_reduce, k_update,
  * k_centroid_table), "global-mfma" (centroids or sums too large for LDS:
  * dense MFMA survivors, sums by counting sort).  "" for a NULL context.

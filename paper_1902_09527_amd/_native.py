@@ -25,6 +25,7 @@ KM_FLAG_TIMING = 8
 KM_FLAG_VECTOR_ONLY = 16
 KM_FLAG_LARGE_PATH = 32
 KM_FLAG_GENERIC = 64
+KM_FLAG_FULL_SUMS = 128
 
 #: Every symbol include/kmeans_mti.h declares.
 EXPORTS = (

@@ -79,7 +79,10 @@ struct km_ctx {
     int tp = 0, lds = 0;
     int variant = 0;   // assignment-kernel specialisation
     bool large = false;   // global-memory path (centroids / sums too large for LDS)
-    bool small = false;   // one-launch streaming step (d = 16, k <= 16)
+    bool small = false;   // streaming step (d = 16, k <= 16)
+    bool inc = false;     // ... with incremental steps after the first
+    int gi = 0, lds_inc = 0;   // grid and LDS of the incremental kernel
+    int64_t enq = 0;      // steps enqueued so far
     km::Fused fz{};
     km::Large lg{};
     int gb = 0;           // blocks of the large path's bound pass
@@ -157,13 +160,16 @@ int enqueue_iteration(km_ctx* c) {
     }
     auto mark = [&](int i) -> hipError_t { return ev ? hipEventRecord(ev[i], c->stream) : hipSuccess; };
     if ((e = mark(0)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
-    if (c->small) {   // two launches: streaming step, then the finishing block (update slot)
-        if ((e = km::launch_small(c->dv, c->fz, c->lds, c->stream)) != hipSuccess)
-            return fail_ctx(c, hip_fail(e, "streaming step kernel"));
+    if (c->small) {   // two launches: streaming or incremental step, then the finishing block
+        const bool delta = c->inc && c->enq > 0;
+        e = delta ? km::launch_inc(c->dv, c->fz, c->gi, c->lds_inc, c->stream)
+                  : km::launch_small(c->dv, c->fz, c->lds, c->stream);
+        if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "streaming step kernel"));
         if ((e = mark(1)) != hipSuccess || (e = mark(2)) != hipSuccess)
             return fail_ctx(c, hip_fail(e, "hipEventRecord"));
-        if ((e = km::launch_small_finish(c->dv, c->fz, c->stream)) != hipSuccess)
+        if ((e = km::launch_small_finish(c->dv, c->fz, delta ? 1 : 0, c->stream)) != hipSuccess)
             return fail_ctx(c, hip_fail(e, "streaming step finish kernel"));
+        ++c->enq;
         if ((e = mark(3)) != hipSuccess || (e = mark(4)) != hipSuccess)
             return fail_ctx(c, hip_fail(e, "hipEventRecord"));
         c->stepped = true;
@@ -234,6 +240,19 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         int64_t G = (int64_t)per_cu * cus;
         if (G > ntiles) G = ntiles;
         v.G = (int32_t)G;
+        c->inc = !(c->flags & (KM_FLAG_FULL_SUMS | KM_FLAG_STATS));
+        if (c->inc) {
+            c->lds_inc = km::inc_lds_bytes(k);
+            if (c->lds_inc > max_lds) return KM_ERR_UNSUPPORTED;
+            const void* isym = km::inc_kernel_symbol(k);
+            KM_HIP(hipFuncSetAttribute(isym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds_inc));
+            int per_cu_i = 0;
+            KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_i, isym, c->tp, c->lds_inc));
+            if (per_cu_i < 1) return KM_ERR_UNSUPPORTED;
+            const int64_t nti = (n + km::kIncTile - 1) / km::kIncTile;
+            int64_t gi = (int64_t)per_cu_i * cus;
+            c->gi = (int)(gi > nti ? nti : gi);
+        }
     } else if (!(c->flags & KM_FLAG_LARGE_PATH)) {
         c->variant = km::assign_variant(d, k, aligned, (c->flags & KM_FLAG_VECTOR_ONLY) != 0);
         const bool h_lds = c->variant % 16 == 0 && k <= km::kHLdsMaxK;
@@ -302,7 +321,9 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         (rc = c->alloc(&v.st, 1)) || (rc = c->alloc(&v.rec, (size_t)km::kHistCap)))
         return rc;
     if (c->small) {
-        if ((rc = c->alloc(&c->fz.rows, (size_t)km::kSmallRows * v.L))) return rc;
+        if ((rc = c->alloc(&c->fz.rows, (size_t)km::kSmallRows * v.L)) ||
+            (rc = c->alloc(&c->fz.sum, (size_t)k * d + k)))
+            return rc;
         KM_HIP(hipMemsetAsync(c->fz.rows, 0, sizeof(uint64_t) * (size_t)km::kSmallRows * v.L, c->stream));
     }
     uint32_t* scratch = nullptr;
@@ -379,7 +400,8 @@ int kmeans_mti_init(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t 
     int rc = check_shape(X, n, d, k, C0);
     if (rc != KM_OK) return rc;
     if (flags & ~(uint32_t)(KM_FLAG_NO_PRUNE | KM_FLAG_STATS | KM_FLAG_VALIDATE | KM_FLAG_TIMING |
-                            KM_FLAG_VECTOR_ONLY | KM_FLAG_LARGE_PATH | KM_FLAG_GENERIC))
+                            KM_FLAG_VECTOR_ONLY | KM_FLAG_LARGE_PATH | KM_FLAG_GENERIC |
+                            KM_FLAG_FULL_SUMS))
         return KM_ERR_INVALID_ARG;
     km_ctx* c = new (std::nothrow) km_ctx;
     if (!c) return KM_ERR_OOM;
@@ -597,7 +619,7 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
 
 const char* kmeans_mti_path(const km_ctx* ctx) {
     if (!ctx) return "";
-    if (ctx->small) return "stream-d16";
+    if (ctx->small) return ctx->inc ? "stream-d16" : "stream-d16-full";
     if (ctx->large) return "global-mfma";
     return ctx->variant % 16 ? "lds-mfma" : "lds-vector";
 }

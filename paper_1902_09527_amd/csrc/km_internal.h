@@ -159,7 +159,12 @@ constexpr int kSmallCopies = 4;   // copies of the LDS sums (spread rows over ba
 constexpr int kSmallRows = 16;
 struct Fused {
     uint64_t* rows;       // kSmallRows x L, zero between steps
+    uint64_t* sum;        // k*d + k: exact sums and counts after the last update
 };
+
+// Incremental step (km_small.hip): tiles of kIncTile points, the bound and
+// assignment streamed, X rows gathered for the Clause-1 survivors only.
+constexpr int kIncTile = 1024;
 
 struct SmallLds {
     int off_c, off_f, off_s, off_ec, off_h, off_acc, off_cnt, off_x, off_sq, off_sa, off_su, off_misc, bytes;
@@ -193,6 +198,36 @@ __host__ __device__ inline SmallLds small_lds(int k) {
     return L;
 }
 
+// Dynamic LDS layout of the incremental kernel: the tables and sums as in
+// small_lds, a gathered-row buffer of kSmallTile rows, and the survivor queue
+// and bounds of a whole tile.
+__host__ __device__ inline SmallLds inc_lds(int k) {
+    SmallLds L;
+    int o = 0;
+    auto take = [&](int bytes, int align) {
+        o = (o + align - 1) / align * align;
+        int r = o;
+        o += bytes;
+        return r;
+    };
+    L.csu = 16 * k + 1;
+    L.kp = k + 1;
+    L.off_c = take(4 * k * 20, 16);
+    L.off_f = take(4 * k, 16);
+    L.off_s = take(4 * k, 16);
+    L.off_ec = take(4 * k, 16);
+    L.off_h = take(4 * k * k, 16);
+    L.off_acc = take(8 * kSmallCopies * L.csu, 16);
+    L.off_cnt = take(4 * kSmallCopies * L.kp, 16);
+    L.off_x = take(4 * kSmallTile * 20, 16);
+    L.off_sq = take(4 * kIncTile, 16);
+    L.off_sa = 0;   // unused
+    L.off_su = take(4 * kIncTile, 16);
+    L.off_misc = take(64, 16);
+    L.bytes = (o + 15) / 16 * 16;
+    return L;
+}
+
 // LDS bytes of the finishing block (totals, centroids, drift terms, table).
 __host__ __device__ inline int finish_lds(int d, int k) {
     return 8 * row_len(d, k) + 3 * 8 * k * d + 4 * k * k + 4 * k;
@@ -200,10 +235,15 @@ __host__ __device__ inline int finish_lds(int d, int k) {
 
 bool small_applies(int d, int k, bool aligned);
 const void* small_kernel_symbol(int k);
+const void* inc_kernel_symbol(int k);
 int small_lds_bytes(int k);
+int inc_lds_bytes(int k);
 int small_finish_lds_bytes(int k);
 hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, hipStream_t s);
-hipError_t launch_small_finish(const Dev& dv, const Fused& F, hipStream_t s);
+hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, hipStream_t s);
+// delta: the rows hold the moves of one incremental step (added to F.sum),
+// else the full sums of a streaming step (replace F.sum).
+hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, hipStream_t s);
 
 // Global-memory path launchers (km_large.hip).  gb: blocks of the bound pass.
 hipError_t launch_large_assign(const Dev& dv, const Large& lg, int gb, hipStream_t s);

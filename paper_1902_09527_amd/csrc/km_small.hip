@@ -108,6 +108,180 @@ __device__ inline uint32_t group_min_u32(uint32_t v) {
 }
 
 // ---------------------------------------------------------------------------
+// Survivor processing shared by the streaming and the incremental kernel.
+
+struct SurvCtx {
+    const float* Cs;       // LDS centroid rows (stride D + 4)
+    const float* ecs;      // LDS rounding errors of the float32 centroids
+    const float* hs;       // LDS half-distance table
+    uint64_t* acc;         // LDS sums, kCopies copies of stride csu
+    uint32_t* cnt;         // LDS counts, kCopies copies of stride kp
+    int csu, kp;
+    const double* C64;     // float64 master centroids (near-tie decisions)
+    int32_t* a;            // point assignments
+    float* u;              // point bounds
+    int k;
+    bool prune, first, want_inertia;
+    float gamma, ecmax;
+    double qscale, iscale;
+};
+
+// One survivor: its LDS row, incumbent (-1 in the first step), drift-updated
+// bound, global index and tile row.
+struct Surv {
+    const float* xrow;
+    int inc;
+    float u;
+    int64_t p;
+    int r;
+};
+
+// Moves point row x from cluster inc to b in the LDS sums (coordinates
+// m0, m0 + step, ...; counts when count is set).
+template <int D>
+__device__ inline void move_sums(const SurvCtx& S, int cp, const float* x, int inc, int b, int m0, int step,
+                                 bool count) {
+    uint64_t* to = S.acc + cp * S.csu + b * D;
+    uint64_t* from = S.acc + cp * S.csu + inc * D;
+    for (int m = m0; m < D; m += step) {
+        const uint64_t v = fixed_bits((double)x[m], S.qscale);
+        atomicAdd(reinterpret_cast<unsigned long long*>(to + m), (unsigned long long)v);
+        atomicAdd(reinterpret_cast<unsigned long long*>(from + m), (unsigned long long)(0 - v));
+    }
+    if (count) {
+        atomicAdd(&S.cnt[cp * S.kp + b], 1u);
+        atomicAdd(&S.cnt[cp * S.kp + inc], 0xFFFFFFFFu);
+    }
+}
+
+// Survivors 0 .. nq-1 (nq <= kTp) of a block.  Many: one lane each, scanning
+// the centroids in index order and skipping one for the whole wave when
+// Clause 2 holds for every lane.  Few: G lanes each, lane j for centroid j.
+// Writes the bound, the assignment if it changed, sa[r] = b in the first
+// step, and moves the sums of a changed point (not in the first step).
+template <int D, int G, class Entry>
+__device__ inline void process_survivors(const SurvCtx& S, int nq, Entry entry, int* sa, uint64_t& changed,
+                                         uint64_t& comp, uint64_t& rechecks, uint64_t& iq) {
+    constexpr int CR = D + 4;
+    constexpr int PER = kTp / G;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int k = S.k;
+    if (nq > kLaneScanMin) {
+        if (tid >= nq) return;
+        const Surv v = entry(tid);
+        const int inc = v.inc;
+        float x[D];
+#pragma unroll
+        for (int m = 0; m < D; m += 4) {
+            const f32x4 q = *reinterpret_cast<const f32x4*>(v.xrow + m);
+            x[m] = q.x;
+            x[m + 1] = q.y;
+            x[m + 2] = q.z;
+            x[m + 3] = q.w;
+        }
+        // Best so far under the oracle's order: smaller distance, then the
+        // incumbent, then the lower index (key 0 = incumbent).
+        int b = -1;
+        uint32_t kb = 0xFFFFFFFFu;
+        float Db = INFINITY, D2 = INFINITY;
+        uint64_t nc = 0;
+        for (int jj = 0; jj < k; ++jj) {
+            // Clause 2: c_jj cannot be strictly closer than the incumbent.
+            const bool need = !(S.prune && inc >= 0 && jj != inc && v.u <= S.hs[max(inc, 0) * k + jj]);
+            if (!__any(need)) continue;   // the whole wave skips c_jj
+            const float Dj = sqd_row<D>(x, S.Cs + jj * CR);
+            if (need) {
+                nc += 1;
+                const uint32_t key = jj == inc ? 0u : (uint32_t)jj + 1u;
+                if (Dj < Db || (Dj == Db && key < kb)) {
+                    D2 = Db;
+                    Db = Dj;
+                    b = jj;
+                    kb = key;
+                } else {
+                    D2 = fminf(D2, Dj);
+                }
+            }
+        }
+        if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
+        float ub = upper_bound(Db, S.ecs[b], S.gamma);
+        if (D2 != INFINITY) {
+            const float band = 2.f * S.gamma * (Db + D2) + 4.f * (sqrtf(Db) + sqrtf(D2)) * S.ecmax +
+                               8.f * S.ecmax * S.ecmax;
+            if (D2 - Db <= band) {   // near tie: float64 decision, the oracle's tie rule
+                b = recheck64(v.xrow, S.C64, D, k, inc, Db, ub);
+                rechecks += 1;
+            }
+        }
+        S.u[v.p] = ub;
+        comp += nc;
+        if (S.want_inertia) iq += fixed_bits((double)Db, S.iscale) - kMagicBits;
+        if (b != inc) {
+            S.a[v.p] = b;
+            changed += 1;
+        }
+        if (S.first) sa[v.r] = b;
+        else if (b != inc) move_sums<D>(S, tid & (kCopies - 1), x, inc, b, 0, 1, true);
+        return;
+    }
+    const int g = tid / G, j = tid % G;
+    const uint64_t gmask = ((1ull << G) - 1ull) << (lane - j);
+    for (int p0 = 0; p0 < nq; p0 += PER) {
+        const int slot = p0 + g;
+        const bool act = slot < nq;
+        const Surv v = entry(act ? slot : p0);
+        const int inc = v.inc;
+        // Clause 2: c_j cannot be strictly closer than the incumbent.
+        const bool want = act && j < k && !(S.prune && inc >= 0 && j != inc && v.u <= S.hs[max(inc, 0) * k + j]);
+        float Dj = INFINITY;
+        if (want) {
+            float x[D];
+#pragma unroll
+            for (int m = 0; m < D; m += 4) {
+                const f32x4 q = *reinterpret_cast<const f32x4*>(v.xrow + m);
+                x[m] = q.x;
+                x[m + 1] = q.y;
+                x[m + 2] = q.z;
+                x[m + 3] = q.w;
+            }
+            Dj = sqd_row<D>(x, S.Cs + j * CR);
+        }
+        // D >= 0, so float order is the order of the bit patterns.
+        const uint32_t dbits = __float_as_uint(Dj);
+        const uint32_t m1 = group_min_u32<G>(dbits);
+        // Among the minimal lanes the incumbent wins, then the lowest index.
+        const uint32_t key = dbits == m1 && want ? (j == inc ? 0u : (uint32_t)j + 1u) : 0xFFFFFFFFu;
+        const uint32_t kmin = group_min_u32<G>(key);
+        int b = kmin == 0u ? inc : (int)kmin - 1;
+        const uint32_t m2 = group_min_u32<G>(want && j != b ? dbits : 0x7F800000u);
+        float Db = __uint_as_float(m1);
+        const float D2 = __uint_as_float(m2);
+        const uint64_t wm = __ballot(want);
+        if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
+        float ub = upper_bound(Db, S.ecs[b], S.gamma);
+        bool re = false;
+        if (D2 != INFINITY) {
+            const float band = 2.f * S.gamma * (Db + D2) + 4.f * (sqrtf(Db) + sqrtf(D2)) * S.ecmax +
+                               8.f * S.ecmax * S.ecmax;
+            re = act && D2 - Db <= band;
+        }
+        if (re) b = recheck64(v.xrow, S.C64, D, k, inc, Db, ub);   // every lane of the group alike
+        if (act && j == 0) {
+            S.u[v.p] = ub;
+            if (b != inc) {
+                S.a[v.p] = b;
+                changed += 1;
+            }
+            if (S.first) sa[v.r] = b;
+            comp += (uint64_t)__popcll(wm & gmask);
+            if (re) rechecks += 1;
+            if (S.want_inertia) iq += fixed_bits((double)Db, S.iscale) - kMagicBits;
+        }
+        if (act && !S.first && b != inc) move_sums<D>(S, g & (kCopies - 1), v.xrow, inc, b, j, G, j == 0);
+    }
+}
+
+// ---------------------------------------------------------------------------
 // The streaming kernel.  Block = kTp threads; wave w of a tile owns points
 // 64w .. 64w+63.  X is prefetched per wave as D/4 coalesced 16-byte loads per
 // lane: load i of lane l holds the 4-float chunk q = (64i + l) % (D/4) of the
@@ -121,7 +295,6 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     constexpr int CH = QD;         // chunks per lane per tile (64 rows * QD / 64 lanes)
     constexpr int XS = D + 4;      // padded LDS row stride of the tile (floats)
     constexpr int CR = D + 4;      // padded LDS centroid row stride (floats)
-    constexpr int PER = kTp / G;   // survivors per pass of the block
 
     IterState* st = P.st;
     if (st->done) {
@@ -185,10 +358,6 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     };
     if ((int64_t)blockIdx.x < ntiles) prefetch(blockIdx.x);
     int it = 0;
-
-    // Survivor-group coordinates: group g of the block, lane j of the group.
-    const int g = tid / G, j = tid % G;
-    const uint64_t gmask = ((1ull << G) - 1ull) << (lane - j);
 
     for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x, ++it) {
         const int64_t base = tile * kTp;
@@ -274,155 +443,16 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
             my_iq += fixed_bits((double)sqd_row<D>(x, Cs + a_old * CR), P.iscale) - kMagicBits;
         }
 
-        // 3. Survivors.  Many (early steps): one lane each, scanning the
-        //    centroids in index order.  Few (later steps): a group of G
-        //    lanes each, lane j for centroid j.
+        // 3. Survivors; 4. moves of the changed points' sums.
         const int nq = *qn;
-        if (nq > kLaneScanMin) {
-            if (tid < nq) {
-                const int e = sq[tid];
-                const int r = e & 0xffff, inc = (e >> 16) - 1;
-                const float* xrow = Xs + r * XS;
-                const float u = su[r];
-                float x[D];
-#pragma unroll
-                for (int m = 0; m < D; m += 4) {
-                    const f32x4 v = *reinterpret_cast<const f32x4*>(xrow + m);
-                    x[m] = v.x;
-                    x[m + 1] = v.y;
-                    x[m + 2] = v.z;
-                    x[m + 3] = v.w;
-                }
-                // Best so far under the oracle's order: smaller distance, then
-                // the incumbent, then the lower index (key 0 = incumbent).
-                int b = -1;
-                uint32_t kb = 0xFFFFFFFFu;
-                float Db = INFINITY, D2 = INFINITY;
-                uint64_t nc = 0;
-                for (int jj = 0; jj < k; ++jj) {
-                    // Clause 2: c_jj cannot be strictly closer than the incumbent.
-                    const bool need = !(prune && inc >= 0 && jj != inc && u <= hs[max(inc, 0) * k + jj]);
-                    if (!__any(need)) continue;   // the whole wave skips c_jj
-                    const float Dj = sqd_row<D>(x, Cs + jj * CR);
-                    if (need) {
-                        nc += 1;
-                        const uint32_t key = jj == inc ? 0u : (uint32_t)jj + 1u;
-                        if (Dj < Db || (Dj == Db && key < kb)) {
-                            D2 = Db;
-                            Db = Dj;
-                            b = jj;
-                            kb = key;
-                        } else {
-                            D2 = fminf(D2, Dj);
-                        }
-                    }
-                }
-                if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
-                float ub = upper_bound(Db, ecs[b], gamma);
-                bool re = false;
-                if (D2 != INFINITY) {
-                    const float band = 2.f * gamma * (Db + D2) + 4.f * (sqrtf(Db) + sqrtf(D2)) * ecmax +
-                                       8.f * ecmax * ecmax;
-                    re = D2 - Db <= band;
-                }
-                if (re) {
-                    b = recheck64(xrow, P.C64, D, k, inc, Db, ub);
-                    my_rc += 1;
-                }
-                const int64_t pr = base + r;
-                P.u[pr] = ub;
-                my_comp += nc;
-                if (want_inertia) my_iq += fixed_bits((double)Db, P.iscale) - kMagicBits;
-                if (b != inc) {
-                    P.a[pr] = b;
-                    my_changed += 1;
-                }
-                if (first) {
-                    sa[r] = b;
-                } else if (b != inc) {   // 4. move the point's sums from inc to b
-                    const int cp = tid & (kCopies - 1);
-                    uint64_t* to = acc + cp * csu + b * D;
-                    uint64_t* from = acc + cp * csu + inc * D;
-#pragma unroll
-                    for (int m = 0; m < D; ++m) {
-                        const uint64_t v = fixed_bits((double)x[m], P.qscale);
-                        atomicAdd(reinterpret_cast<unsigned long long*>(to + m), (unsigned long long)v);
-                        atomicAdd(reinterpret_cast<unsigned long long*>(from + m), (unsigned long long)(0 - v));
-                    }
-                    atomicAdd(&cnt[cp * kp + b], 1u);
-                    atomicAdd(&cnt[cp * kp + inc], 0xFFFFFFFFu);
-                }
-            }
-        } else for (int p0 = 0; p0 < nq; p0 += PER) {
-            const int slot = p0 + g;
-            const bool act = slot < nq;
-            const int e = sq[act ? slot : p0];
-            const int r = e & 0xffff, inc = (e >> 16) - 1;
-            const float* xrow = Xs + r * XS;
-            const float u = su[r];
-            // Clause 2: c_j cannot be strictly closer than the incumbent.
-            const bool want = act && j < k && !(prune && inc >= 0 && j != inc && u <= hs[max(inc, 0) * k + j]);
-            float Dj = INFINITY;
-            if (want) {
-                float x[D];
-#pragma unroll
-                for (int m = 0; m < D; m += 4) {
-                    const f32x4 v = *reinterpret_cast<const f32x4*>(xrow + m);
-                    x[m] = v.x;
-                    x[m + 1] = v.y;
-                    x[m + 2] = v.z;
-                    x[m + 3] = v.w;
-                }
-                Dj = sqd_row<D>(x, Cs + j * CR);
-            }
-            // D >= 0, so float order is the order of the bit patterns.
-            const uint32_t dbits = __float_as_uint(Dj);
-            const uint32_t m1 = group_min_u32<G>(dbits);
-            // Among the minimal lanes the incumbent wins, then the lowest index.
-            const uint32_t key = dbits == m1 && want ? (j == inc ? 0u : (uint32_t)j + 1u) : 0xFFFFFFFFu;
-            const uint32_t kmin = group_min_u32<G>(key);
-            int b = kmin == 0u ? inc : (int)kmin - 1;
-            const uint32_t m2 = group_min_u32<G>(want && j != b ? dbits : 0x7F800000u);
-            float Db = __uint_as_float(m1);
-            const float D2 = __uint_as_float(m2);
-            const uint64_t wm = __ballot(want);
-            if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
-            float ub = upper_bound(Db, ecs[b], gamma);
-            bool re = false;
-            if (D2 != INFINITY) {
-                const float band = 2.f * gamma * (Db + D2) + 4.f * (sqrtf(Db) + sqrtf(D2)) * ecmax +
-                                   8.f * ecmax * ecmax;
-                re = act && D2 - Db <= band;
-            }
-            if (re) b = recheck64(xrow, P.C64, D, k, inc, Db, ub);   // every lane of the group alike
-            if (act && j == 0) {
-                const int64_t pr = base + r;
-                P.u[pr] = ub;
-                if (b != inc) {
-                    P.a[pr] = b;
-                    my_changed += 1;
-                }
-                if (first) sa[r] = b;
-                my_comp += (uint64_t)__popcll(wm & gmask);
-                if (re) my_rc += 1;
-                if (want_inertia) my_iq += fixed_bits((double)Db, P.iscale) - kMagicBits;
-            }
-            // 4. Move a changed point's sums from inc to b, coordinates j, j + G, ...
-            if (act && !first && b != inc) {
-                const int cp = g & (kCopies - 1);
-                uint64_t* to = acc + cp * csu + b * D;
-                uint64_t* from = acc + cp * csu + inc * D;
-#pragma unroll
-                for (int m = j; m < D; m += G) {
-                    const uint64_t v = fixed_bits((double)xrow[m], P.qscale);
-                    atomicAdd(reinterpret_cast<unsigned long long*>(to + m), (unsigned long long)v);
-                    atomicAdd(reinterpret_cast<unsigned long long*>(from + m), (unsigned long long)(0 - v));
-                }
-                if (j == 0) {
-                    atomicAdd(&cnt[cp * kp + b], 1u);
-                    atomicAdd(&cnt[cp * kp + inc], 0xFFFFFFFFu);
-                }
-            }
+        {
+            const SurvCtx S{Cs, ecs, hs, acc, cnt, csu, kp, P.C64, P.a, P.u, k, prune, first, want_inertia,
+                            gamma, ecmax, P.qscale, P.iscale};
+            process_survivors<D, G>(S, nq, [&](int i) {
+                const int e = sq[i];
+                const int r = e & 0xffff;
+                return Surv{Xs + r * XS, (e >> 16) - 1, su[r], base + r, r};
+            }, sa, my_changed, my_comp, my_rc, my_iq);
         }
         if (first) {   // first step: sums of the new assignment, from the staged rows
             __syncthreads();
@@ -484,10 +514,183 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
 }
 
 // ---------------------------------------------------------------------------
+// The incremental kernel (the paper's skipping of the data of points that
+// Clause 1 keeps, section III-C; ||Lloyd's per-thread sums, section V).
+// Steps after the first only.  Tile = kIncTile points, PT per thread.  A
+// Clause-1 point moves only its bound: its assignment and bound are streamed
+// and its X row is never read.  The survivors' rows are gathered into LDS,
+// kTp at a time, and scanned as in the streaming kernel; the block's row
+// then holds the moves of the points that changed, which the finishing
+// block adds to the exact sums of the previous step.
+
+template <int D, int G>
+__global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P, Fused F) {
+    static_assert(D == 16, "incremental kernel is specialised for d = 16");
+    constexpr int QD = D / 4;               // 16-byte chunks per row
+    constexpr int XS = D + 4;               // padded LDS row stride of the gathered rows
+    constexpr int CR = D + 4;               // padded LDS centroid row stride
+    constexpr int PT = kIncTile / kTp;      // points per thread per tile
+
+    IterState* st = P.st;
+    if (st->done || st->t == 0) {   // the first step always runs the streaming kernel
+        if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
+        return;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 1;
+
+    const int k = P.k;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const bool prune = !(P.flags & KM_FLAG_NO_PRUNE);
+    const float ecmax = st->ec_max;
+
+    const SmallLds lay = inc_lds(k);
+    float* Cs = reinterpret_cast<float*>(km_smem + lay.off_c);
+    float* fs = reinterpret_cast<float*>(km_smem + lay.off_f);
+    float* ss = reinterpret_cast<float*>(km_smem + lay.off_s);
+    float* ecs = reinterpret_cast<float*>(km_smem + lay.off_ec);
+    float* hs = reinterpret_cast<float*>(km_smem + lay.off_h);
+    uint64_t* acc = reinterpret_cast<uint64_t*>(km_smem + lay.off_acc);
+    uint32_t* cnt = reinterpret_cast<uint32_t*>(km_smem + lay.off_cnt);
+    float* Xs = reinterpret_cast<float*>(km_smem + lay.off_x);
+    int* sq = reinterpret_cast<int*>(km_smem + lay.off_sq);
+    float* su = reinterpret_cast<float*>(km_smem + lay.off_su);
+    int* qlen = reinterpret_cast<int*>(km_smem + lay.off_misc);
+    uint64_t* bst = reinterpret_cast<uint64_t*>(km_smem + lay.off_misc + 16);
+    const int csu = lay.csu, kp = lay.kp;
+
+    for (int i = tid; i < k * D; i += kTp) Cs[(i / D) * CR + i % D] = P.C32[i];
+    for (int i = tid; i < k; i += kTp) {
+        fs[i] = P.f[i];
+        ss[i] = P.s[i];
+        ecs[i] = P.ec[i];
+    }
+    for (int i = tid; i < k * k; i += kTp) hs[i] = P.h[i];
+    for (int i = tid; i < kCopies * csu; i += kTp) acc[i] = 0;
+    for (int i = tid; i < kCopies * kp; i += kTp) cnt[i] = 0;
+    if (tid < kNumStat) bst[tid] = 0;
+    if (tid < 2) qlen[tid] = 0;
+
+    uint64_t my_changed = 0, my_comp = 0, my_c1 = 0, my_rc = 0, my_iq = 0;
+    const int64_t n = P.n;
+    const int64_t ntiles = (n + kIncTile - 1) / kIncTile;
+    const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
+
+    int abuf[PT];
+    float ubuf[PT];
+    auto prefetch = [&](int64_t tl) {
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const int64_t q = min(tl * kIncTile + tid + kTp * i, n - 1);
+            abuf[i] = P.a[q];
+            ubuf[i] = P.u[q];
+        }
+    };
+    if ((int64_t)blockIdx.x < ntiles) prefetch(blockIdx.x);
+    int it = 0;
+    const SurvCtx S{Cs, ecs, hs, acc, cnt, csu, kp, P.C64, P.a, P.u, k, prune, false, false,
+                    P.gamma, ecmax, P.qscale, P.iscale};
+
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x, ++it) {
+        const int64_t base = tile * kIncTile;
+        const int rows = (int)min((int64_t)kIncTile, n - base);
+        __syncthreads();   // the previous tile's queue and rows are consumed
+        if (tid == 0) qlen[(it + 1) & 1] = 0;
+        int* qn = qlen + (it & 1);
+
+        // Bound update and Clause 1 for this thread's PT points.
+        int a_old[PT];
+        float u_cur[PT];
+        bool surv[PT];
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const bool valid = tid + kTp * i < rows;
+            a_old[i] = valid ? abuf[i] : 0;
+            u_cur[i] = (ubuf[i] + fs[a_old[i]]) * kUp;
+            surv[i] = valid && (!prune || u_cur[i] > ss[a_old[i]]);
+            if (valid && !surv[i]) {   // Clause 1: only the bound moves
+                P.u[base + tid + kTp * i] = u_cur[i];
+                my_c1 += 1;
+            }
+        }
+        if (tile + gridDim.x < ntiles) prefetch(tile + gridDim.x);
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {   // survivor queue: one LDS atomic per wave and i
+            const uint64_t bm = __ballot(surv[i]);
+            int wbase = 0;
+            if (lane == 0 && bm) wbase = atomicAdd(qn, __popcll(bm));
+            wbase = __shfl(wbase, 0);
+            if (surv[i]) {
+                const int slot = wbase + __popcll(bm & ((1ull << lane) - 1ull));
+                sq[slot] = (tid + kTp * i) | ((a_old[i] + 1) << 16);
+                su[slot] = u_cur[i];
+            }
+        }
+        __syncthreads();
+
+        const int nq = *qn;
+        for (int c0 = 0; c0 < nq; c0 += kTp) {
+            const int nc = min(kTp, nq - c0);
+            if (c0 > 0) __syncthreads();   // the previous chunk's rows are consumed
+            // Gather the chunk's rows: QD 16-byte loads per thread, all in flight.
+            f32x4 gbuf[QD];
+#pragma unroll
+            for (int i = 0; i < QD; ++i) {
+                const int idx = tid + kTp * i;
+                const int sl = idx < nc * QD ? idx / QD : 0;
+                const int li = sq[c0 + sl] & 0xffff;
+                gbuf[i] = __builtin_nontemporal_load(X4 + (base + li) * QD + idx % QD);
+            }
+#pragma unroll
+            for (int i = 0; i < QD; ++i) {
+                const int idx = tid + kTp * i;
+                if (idx < nc * QD) *reinterpret_cast<f32x4*>(Xs + (idx / QD) * XS + 4 * (idx % QD)) = gbuf[i];
+            }
+            __syncthreads();
+            process_survivors<D, G>(S, nc, [&](int i) {
+                const int e = sq[c0 + i];
+                const int li = e & 0xffff;
+                return Surv{Xs + i * XS, (e >> 16) - 1, su[c0 + i], base + li, li};
+            }, nullptr, my_changed, my_comp, my_rc, my_iq);
+        }
+    }
+    __syncthreads();
+
+    // Block counters, then the block's moves into accumulation row
+    // blockIdx % kSmallRows.
+    my_changed = wave_sum_u64(my_changed);
+    my_comp = wave_sum_u64(my_comp);
+    my_c1 = wave_sum_u64(my_c1);
+    my_rc = wave_sum_u64(my_rc);
+    if (lane == 0) {
+        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStChanged]), my_changed);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStComputed]), my_comp);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStClause1]), my_c1);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStRecheck]), my_rc);
+    }
+    __syncthreads();
+    unsigned long long* row =
+        reinterpret_cast<unsigned long long*>(F.rows + (int64_t)(blockIdx.x % kSmallRows) * P.L);
+    for (int i = tid; i < k * D; i += kTp) {
+        uint64_t v = 0;
+#pragma unroll
+        for (int c = 0; c < kCopies; ++c) v += acc[c * csu + i];
+        if (v) atomicAdd(row + i, (unsigned long long)v);
+    }
+    for (int i = tid; i < k; i += kTp) {
+        uint32_t v = 0;
+#pragma unroll
+        for (int c = 0; c < kCopies; ++c) v += cnt[c * kp + i];
+        if (v) atomicAdd(row + k * D + i, (unsigned long long)(int64_t)(int32_t)v);
+    }
+    if (tid < kNumStat && bst[tid]) atomicAdd(row + k * D + k + tid, (unsigned long long)bst[tid]);
+    (void)my_iq;
+}
+
+// ---------------------------------------------------------------------------
 // End of a step (one block): totals of the accumulation rows (which it
 // clears), new centroids, drift, stop test, centroid table for the next step.
 
-__global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F) {
+__global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F, int delta) {
     constexpr int nt = kFinishThreads;
     IterState* st = P.st;
     const int tid = threadIdx.x;
@@ -514,6 +717,10 @@ __global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F)
         uint64_t v = 0;
 #pragma unroll
         for (int r = 0; r < kSmallRows; ++r) v += t[r];
+        if (col < k * d + k) {   // sums and counts: after the moves, or the full sums
+            if (delta) v += F.sum[col];
+            if (active) F.sum[col] = v;
+        }
         tot[col] = v;
         if (active) {
 #pragma unroll
@@ -627,7 +834,17 @@ const void* small_kernel_symbol(int k) {
     }
 }
 
+const void* inc_kernel_symbol(int k) {
+    switch (small_group(k)) {
+        case 4: return reinterpret_cast<const void*>(&k_inc<16, 4>);
+        case 8: return reinterpret_cast<const void*>(&k_inc<16, 8>);
+        default: return reinterpret_cast<const void*>(&k_inc<16, 16>);
+    }
+}
+
 int small_lds_bytes(int k) { return small_lds(k).bytes; }
+
+int inc_lds_bytes(int k) { return inc_lds(k).bytes; }
 
 int small_finish_lds_bytes(int k) { return finish_lds(16, k); }
 
@@ -640,8 +857,17 @@ hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, hipStream_
     return hipGetLastError();
 }
 
-hipError_t launch_small_finish(const Dev& dv, const Fused& F, hipStream_t s) {
-    hipLaunchKernelGGL(k_small_finish, dim3(1), dim3(kFinishThreads), finish_lds(dv.d, dv.k), s, dv, F);
+hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, hipStream_t s) {
+    switch (small_group(dv.k)) {
+        case 4: hipLaunchKernelGGL((k_inc<16, 4>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
+        case 8: hipLaunchKernelGGL((k_inc<16, 8>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
+        default: hipLaunchKernelGGL((k_inc<16, 16>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, hipStream_t s) {
+    hipLaunchKernelGGL(k_small_finish, dim3(1), dim3(kFinishThreads), finish_lds(dv.d, dv.k), s, dv, F, delta);
     return hipGetLastError();
 }
 

@@ -32,8 +32,11 @@ def _check_matrix(t: torch.Tensor, name: str, cols: Optional[int] = None) -> Non
 
 
 def _flags(prune: bool, stats: bool, validate: bool, timing: bool = False,
-           vector_only: bool = False, large_path: bool = False, generic: bool = False) -> int:
+           vector_only: bool = False, large_path: bool = False, generic: bool = False,
+           full_sums: bool = False) -> int:
     f = N.KM_FLAG_TIMING if timing else 0
+    if full_sums:
+        f |= N.KM_FLAG_FULL_SUMS
     if generic:
         f |= N.KM_FLAG_GENERIC
     if vector_only:
@@ -63,7 +66,7 @@ class KMeansMTI:
 
     def __init__(self, X: torch.Tensor, C0: torch.Tensor, prune: bool = True, stats: bool = False,
                  validate: bool = False, timing: bool = False, vector_only: bool = False,
-                 large_path: bool = False, generic: bool = False,
+                 large_path: bool = False, generic: bool = False, full_sums: bool = False,
                  stream: Optional[torch.cuda.Stream] = None):
         _check_matrix(X, "X")
         _check_matrix(C0, "C0", X.shape[1])
@@ -81,7 +84,7 @@ class KMeansMTI:
                                            self.d, self.k, C.c_void_p(C0.data_ptr()),
                                            _stream_ptr(self.device, stream),
                                            _flags(prune, stats, validate, timing, vector_only,
-                                                  large_path, generic))
+                                                  large_path, generic, full_sums))
         N.check(st, "kmeans_mti_init")
 
     def _live(self) -> C.c_void_p:
@@ -170,7 +173,8 @@ class KMeansMTI:
 
 def run(X: torch.Tensor, C0: torch.Tensor, max_iters: int, tol: float = 0.0, prune: bool = True,
         stats: bool = False, validate: bool = False, vector_only: bool = False,
-        large_path: bool = False, generic: bool = False, stream: Optional[torch.cuda.Stream] = None
+        large_path: bool = False, generic: bool = False, full_sums: bool = False,
+        stream: Optional[torch.cuda.Stream] = None
         ) -> Tuple[torch.Tensor, torch.Tensor, Dict[str, float]]:
     """Whole k-means run (kmeans_mti_run): (assign int32 [n], C float32 [k, d], stats)."""
     _check_matrix(X, "X")
@@ -188,7 +192,7 @@ def run(X: torch.Tensor, C0: torch.Tensor, max_iters: int, tol: float = 0.0, pru
                                 int(max_iters), float(tol), C.c_void_p(a.data_ptr()),
                                 C.c_void_p(c.data_ptr()), _stream_ptr(X.device, stream),
                                 _flags(prune, stats, validate, False, vector_only, large_path,
-                                       generic),
+                                       generic, full_sums),
                                 C.byref(s))
     N.check(st, "kmeans_mti_run")
     return a, c, s.as_dict()

@@ -36,40 +36,68 @@ CASES = [
 
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "s%d-n%d-k%d" % c[:3])
-def test_stream_matches_oracle(case):
+@pytest.mark.parametrize("stats", [False, True], ids=["incremental", "full+inertia"])
+def test_stream_matches_oracle(case, stats):
     seed, n, k, spread, sigma, iters, tol = case
-    print("case", case, flush=True)
+    print("case", case, stats, flush=True)
     X, C0 = synth.blobs(n, 16, k, seed=seed, spread=spread, sigma=sigma)
     ref = oracle.lloyd(X, C0, iters, tol)
-    a, c, st = km.run(_gpu(X), _gpu(C0), iters, tol, stats=True)
+    a, c, st = km.run(_gpu(X), _gpu(C0), iters, tol, stats=stats)
     assert st["iterations"] == ref["iters"]
     check_assign(a.cpu().numpy(), ref["assign"], ref["best"], ref["second"], "final assignment")
     check_centroids(c.cpu().numpy(), ref["C"], X, "final centroids")
-    assert st["inertia_last"] == pytest.approx(ref["inertia"][-1], rel=1e-5)
+    if stats:
+        assert st["inertia_last"] == pytest.approx(ref["inertia"][-1], rel=1e-5)
 
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "s%d-n%d-k%d" % c[:3])
 @pytest.mark.parametrize("prune", [True, False], ids=["prune", "noprune"])
-def test_stream_is_bitwise_identical_to_generic_path(case, prune):
+def test_stream_paths_are_bitwise_identical_to_generic_path(case, prune):
+    # incremental sums (default), full sums every step, full sums with inertia,
+    # and the general kernels: same assignments, centroids and changed counts
     seed, n, k, spread, sigma, iters, tol = case
     print("case", case, prune, flush=True)
     X, C0 = synth.blobs(n, 16, k, seed=seed, spread=spread, sigma=sigma)
     Xg, Cg = _gpu(X), _gpu(C0)
-    hists, outs = [], []
-    for generic in (False, True):
-        with km.KMeansMTI(Xg, Cg, prune=prune, stats=True, generic=generic) as ctx:
+    modes = [dict(), dict(full_sums=True), dict(stats=True), dict(stats=True, generic=True)]
+    paths, hists, outs = [], [], []
+    for m in modes:
+        with km.KMeansMTI(Xg, Cg, prune=prune, **m) as ctx:
             for _ in range(iters):
                 ctx.iterate()
             a, c = ctx.get()
             outs.append((a.cpu().numpy(), c.cpu().numpy(), ctx.centroids64()))
             hists.append(ctx.history())
-    np.testing.assert_array_equal(outs[0][0], outs[1][0])
-    np.testing.assert_array_equal(outs[0][1], outs[1][1])
-    np.testing.assert_array_equal(outs[0][2], outs[1][2])
-    np.testing.assert_array_equal(hists[0]["changed"], hists[1]["changed"])
-    np.testing.assert_allclose(hists[0]["inertia"], hists[1]["inertia"], rtol=1e-12)
+            paths.append(ctx.path())
+    assert paths == ["stream-d16", "stream-d16-full", "stream-d16-full", "lds-vector"]
+    for o, h in zip(outs[1:], hists[1:]):
+        np.testing.assert_array_equal(outs[0][0], o[0])
+        np.testing.assert_array_equal(outs[0][1], o[1])
+        np.testing.assert_array_equal(outs[0][2], o[2])
+        np.testing.assert_array_equal(hists[0]["changed"], h["changed"])
+    np.testing.assert_allclose(hists[2]["inertia"], hists[3]["inertia"], rtol=1e-12)
     if not prune:
         assert (hists[0]["computed"] == n * k).all()
+
+
+def test_incremental_trajectory_every_step_matches_oracle():
+    X, C0 = synth.blobs(70000 + 9, 16, 12, seed=112, spread=3.0, sigma=1.5)
+    T = 15
+    ref = oracle.lloyd(X, C0, T, history=True)
+    with km.KMeansMTI(_gpu(X), _gpu(C0)) as ctx:
+        assert ctx.path() == "stream-d16"
+        for t in range(T):
+            ch = ctx.iterate(sync=True)
+            a, c = ctx.get()
+            prev = None if t == 0 else ref["assign_hist"][t - 1]
+            _, b, s, _ = oracle.assign(X, ref["C_hist"][t], prev=prev)
+            info = check_assign(a.cpu().numpy(), ref["assign_hist"][t], b, s, "step %d" % t)
+            if info["mismatch"] == 0:
+                assert ch == ref["changed"][t]
+            np.testing.assert_allclose(ctx.centroids64(), ref["C_hist"][t + 1], rtol=1e-9, atol=1e-9)
+        h = ctx.history()
+    np.testing.assert_array_equal(h["changed"], ref["changed"])
+    assert np.isnan(h["inertia"]).all()
 
 
 def test_stream_trajectory_and_history():
@@ -112,7 +140,8 @@ def test_stream_repeated_runs_reuse_accumulation_rows():
 
 
 @pytest.mark.parametrize("d,k,flags,path", [
-    (16, 10, {}, "stream-d16"), (16, 16, {}, "stream-d16"), (16, 10, {"generic": True}, "lds-vector"),
+    (16, 10, {}, "stream-d16"), (16, 16, {}, "stream-d16"), (16, 10, {"full_sums": True}, "stream-d16-full"),
+    (16, 10, {"stats": True}, "stream-d16-full"), (16, 10, {"generic": True}, "lds-vector"),
     (16, 17, {}, "lds-mfma"), (32, 10, {}, "lds-vector"), (16, 10, {"large_path": True}, "global-mfma"),
 ])
 def test_path_selection(d, k, flags, path):
