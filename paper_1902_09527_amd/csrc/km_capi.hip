@@ -226,7 +226,7 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     // (centroids, fixed-point sums, X tile) fits; else the global-memory path.
     c->tp = 0;
     const bool aligned = reinterpret_cast<uintptr_t>(X) % 16 == 0;
-    if (!(c->flags & (KM_FLAG_LARGE_PATH | KM_FLAG_GENERIC)) && km::small_applies(d, k, aligned)) {
+    if (!(c->flags & (KM_FLAG_LARGE_PATH | KM_FLAG_GENERIC)) && km::small_applies(n, d, k, aligned)) {
         c->small = true;
         c->tp = km::kSmallTile;
         c->lds = km::small_lds_bytes(k);
@@ -249,9 +249,13 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             int per_cu_i = 0;
             KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_i, isym, c->tp, c->lds_inc));
             if (per_cu_i < 1) return KM_ERR_UNSUPPORTED;
+            // Contiguous ranges of tpb tiles per block, no block without a tile.
             const int64_t nti = (n + km::kIncTile - 1) / km::kIncTile;
             int64_t gi = (int64_t)per_cu_i * cus;
-            c->gi = (int)(gi > nti ? nti : gi);
+            if (gi > nti) gi = nti;
+            const int64_t tpb = (nti + gi - 1) / gi;
+            c->gi = (int)((nti + tpb - 1) / tpb);
+            c->fz.span = tpb * km::kIncTile;
         }
     } else if (!(c->flags & KM_FLAG_LARGE_PATH)) {
         c->variant = km::assign_variant(d, k, aligned, (c->flags & KM_FLAG_VECTOR_ONLY) != 0);
@@ -324,6 +328,12 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         if ((rc = c->alloc(&c->fz.rows, (size_t)km::kSmallRows * v.L)) ||
             (rc = c->alloc(&c->fz.sum, (size_t)k * d + k)))
             return rc;
+        if (c->inc) {
+            const size_t cap = (size_t)c->gi * (size_t)c->fz.span;
+            if ((rc = c->alloc(&c->fz.lq, cap)) || (rc = c->alloc(&c->fz.la, cap)) ||
+                (rc = c->alloc(&c->fz.lu, cap)))
+                return rc;
+        }
         KM_HIP(hipMemsetAsync(c->fz.rows, 0, sizeof(uint64_t) * (size_t)km::kSmallRows * v.L, c->stream));
     }
     uint32_t* scratch = nullptr;

@@ -160,10 +160,16 @@ constexpr int kSmallRows = 16;
 struct Fused {
     uint64_t* rows;       // kSmallRows x L, zero between steps
     uint64_t* sum;        // k*d + k: exact sums and counts after the last update
+    int32_t* lq;          // survivor lists of the incremental step: point index,
+    int32_t* la;          //   incumbent,
+    float* lu;            //   drift-updated bound; block b owns entries [b * span, (b + 1) * span)
+    int64_t span;         // tiles per block * kIncTile
 };
 
-// Incremental step (km_small.hip): tiles of kIncTile points, the bound and
-// assignment streamed, X rows gathered for the Clause-1 survivors only.
+// Incremental step (km_small.hip): each block streams the bound and
+// assignment of a contiguous range of tiles of kIncTile points, lists its
+// Clause-1 survivors in global memory, then gathers their X rows and scans
+// them kSmallTile at a time.
 constexpr int kIncTile = 1024;
 
 struct SmallLds {
@@ -199,8 +205,8 @@ __host__ __device__ inline SmallLds small_lds(int k) {
 }
 
 // Dynamic LDS layout of the incremental kernel: the tables and sums as in
-// small_lds, a gathered-row buffer of kSmallTile rows, and the survivor queue
-// and bounds of a whole tile.
+// small_lds, and one chunk of kSmallTile survivors (rows, index, incumbent,
+// bound).
 __host__ __device__ inline SmallLds inc_lds(int k) {
     SmallLds L;
     int o = 0;
@@ -220,10 +226,10 @@ __host__ __device__ inline SmallLds inc_lds(int k) {
     L.off_acc = take(8 * kSmallCopies * L.csu, 16);
     L.off_cnt = take(4 * kSmallCopies * L.kp, 16);
     L.off_x = take(4 * kSmallTile * 20, 16);
-    L.off_sq = take(4 * kIncTile, 16);
-    L.off_sa = 0;   // unused
-    L.off_su = take(4 * kIncTile, 16);
-    L.off_misc = take(64, 16);
+    L.off_sq = take(4 * kSmallTile, 16);   // chunk: point index
+    L.off_sa = take(4 * kSmallTile, 16);   // chunk: incumbent
+    L.off_su = take(4 * kSmallTile, 16);   // chunk: drift-updated bound
+    L.off_misc = take(64, 16);             // list length (int) at 0, counters at 16
     L.bytes = (o + 15) / 16 * 16;
     return L;
 }
@@ -233,7 +239,7 @@ __host__ __device__ inline int finish_lds(int d, int k) {
     return 8 * row_len(d, k) + 3 * 8 * k * d + 4 * k * k + 4 * k;
 }
 
-bool small_applies(int d, int k, bool aligned);
+bool small_applies(int64_t n, int d, int k, bool aligned);
 const void* small_kernel_symbol(int k);
 const void* inc_kernel_symbol(int k);
 int small_lds_bytes(int k);

@@ -9,8 +9,8 @@
 //      (no dependence on the distance work, so it overlaps the stream);
 //   3. compacts the Clause-1 survivors into a queue; a tile with many
 //      survivors gives each one lane that scans the centroids in index order,
-//      skipping a centroid for the whole wave when Clause 2 (u <= h(a, c),
-//      Elkan's lemma) holds for every lane; a tile with few gives each
+//      ignoring a centroid that Clause 2 (u <= h(a, c), Elkan's lemma) rules
+//      out; a tile with few gives each
 //      survivor a group of G >= k lanes, lane j evaluating centroid j unless
 //      Clause 2 skips it, and the group takes the minimum with the oracle's
 //      tie rule and the second-best value with DPP row reductions; near ties
@@ -155,8 +155,8 @@ __device__ inline void move_sums(const SurvCtx& S, int cp, const float* x, int i
 }
 
 // Survivors 0 .. nq-1 (nq <= kTp) of a block.  Many: one lane each, scanning
-// the centroids in index order and skipping one for the whole wave when
-// Clause 2 holds for every lane.  Few: G lanes each, lane j for centroid j.
+// the centroids in index order (a centroid that Clause 2 rules out is
+// computed but ignored).  Few: G lanes each, lane j for centroid j.
 // Writes the bound, the assignment if it changed, sa[r] = b in the first
 // step, and moves the sums of a changed point (not in the first step).
 template <int D, int G, class Entry>
@@ -185,23 +185,22 @@ __device__ inline void process_survivors(const SurvCtx& S, int nq, Entry entry, 
         uint32_t kb = 0xFFFFFFFFu;
         float Db = INFINITY, D2 = INFINITY;
         uint64_t nc = 0;
+        // Branch-free body, unrolled by two, so that the distance chains of
+        // consecutive centroids overlap.
+        const float* hrow = S.hs + max(inc, 0) * k;
+#pragma unroll 2
         for (int jj = 0; jj < k; ++jj) {
             // Clause 2: c_jj cannot be strictly closer than the incumbent.
-            const bool need = !(S.prune && inc >= 0 && jj != inc && v.u <= S.hs[max(inc, 0) * k + jj]);
-            if (!__any(need)) continue;   // the whole wave skips c_jj
+            const bool need = !(S.prune && inc >= 0 && jj != inc && v.u <= hrow[jj]);
             const float Dj = sqd_row<D>(x, S.Cs + jj * CR);
-            if (need) {
-                nc += 1;
-                const uint32_t key = jj == inc ? 0u : (uint32_t)jj + 1u;
-                if (Dj < Db || (Dj == Db && key < kb)) {
-                    D2 = Db;
-                    Db = Dj;
-                    b = jj;
-                    kb = key;
-                } else {
-                    D2 = fminf(D2, Dj);
-                }
-            }
+            const uint32_t key = jj == inc ? 0u : (uint32_t)jj + 1u;
+            const bool better = need && (Dj < Db || (Dj == Db && key < kb));
+            const float D2n = better ? Db : (need ? fminf(D2, Dj) : D2);
+            D2 = D2n;
+            Db = better ? Dj : Db;
+            b = better ? jj : b;
+            kb = better ? key : kb;
+            nc += need ? 1 : 0;
         }
         if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
         float ub = upper_bound(Db, S.ecs[b], S.gamma);
@@ -516,12 +515,14 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
 // ---------------------------------------------------------------------------
 // The incremental kernel (the paper's skipping of the data of points that
 // Clause 1 keeps, section III-C; ||Lloyd's per-thread sums, section V).
-// Steps after the first only.  Tile = kIncTile points, PT per thread.  A
-// Clause-1 point moves only its bound: its assignment and bound are streamed
-// and its X row is never read.  The survivors' rows are gathered into LDS,
-// kTp at a time, and scanned as in the streaming kernel; the block's row
-// then holds the moves of the points that changed, which the finishing
-// block adds to the exact sums of the previous step.
+// Steps after the first only.  Block b owns a contiguous range of tiles of
+// kIncTile points (PT per thread).  Phase 1 streams their assignments and
+// bounds: a Clause-1 point moves only its bound and its X row is never read;
+// a survivor is appended to the block's list in global memory.  Phase 2
+// takes the list kTp survivors at a time: their rows and state are gathered
+// into LDS and they are scanned as in the streaming kernel.  The block's row
+// then holds the moves of the points that changed, which the finishing block
+// adds to the exact sums of the previous step.
 
 template <int D, int G>
 __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P, Fused F) {
@@ -552,9 +553,10 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     uint64_t* acc = reinterpret_cast<uint64_t*>(km_smem + lay.off_acc);
     uint32_t* cnt = reinterpret_cast<uint32_t*>(km_smem + lay.off_cnt);
     float* Xs = reinterpret_cast<float*>(km_smem + lay.off_x);
-    int* sq = reinterpret_cast<int*>(km_smem + lay.off_sq);
-    float* su = reinterpret_cast<float*>(km_smem + lay.off_su);
-    int* qlen = reinterpret_cast<int*>(km_smem + lay.off_misc);
+    int* cq = reinterpret_cast<int*>(km_smem + lay.off_sq);
+    int* ca = reinterpret_cast<int*>(km_smem + lay.off_sa);
+    float* cu = reinterpret_cast<float*>(km_smem + lay.off_su);
+    int* lenp = reinterpret_cast<int*>(km_smem + lay.off_misc);
     uint64_t* bst = reinterpret_cast<uint64_t*>(km_smem + lay.off_misc + 16);
     const int csu = lay.csu, kp = lay.kp;
 
@@ -568,92 +570,104 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     for (int i = tid; i < kCopies * csu; i += kTp) acc[i] = 0;
     for (int i = tid; i < kCopies * kp; i += kTp) cnt[i] = 0;
     if (tid < kNumStat) bst[tid] = 0;
-    if (tid < 2) qlen[tid] = 0;
+    if (tid == 0) *lenp = 0;
+    __syncthreads();
 
     uint64_t my_changed = 0, my_comp = 0, my_c1 = 0, my_rc = 0, my_iq = 0;
     const int64_t n = P.n;
     const int64_t ntiles = (n + kIncTile - 1) / kIncTile;
-    const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
+    const int64_t tpb = F.span / kIncTile;
+    const int64_t t_begin = (int64_t)blockIdx.x * tpb;
+    const int64_t t_end = min(ntiles, t_begin + tpb);
+    const int64_t lbase = (int64_t)blockIdx.x * F.span;   // this block's list
 
-    int abuf[PT];
-    float ubuf[PT];
-    auto prefetch = [&](int64_t tl) {
+    // Phase 1: stream the assignments and bounds, two tiles in flight.
+    int abA[PT], abB[PT];
+    float ubA[PT], ubB[PT];
+    auto prefetch = [&](int (&ab)[PT], float (&ub)[PT], int64_t tl) {
+        if (tl >= t_end) return;
 #pragma unroll
         for (int i = 0; i < PT; ++i) {
             const int64_t q = min(tl * kIncTile + tid + kTp * i, n - 1);
-            abuf[i] = P.a[q];
-            ubuf[i] = P.u[q];
+            ab[i] = P.a[q];
+            ub[i] = P.u[q];
         }
     };
-    if ((int64_t)blockIdx.x < ntiles) prefetch(blockIdx.x);
-    int it = 0;
-    const SurvCtx S{Cs, ecs, hs, acc, cnt, csu, kp, P.C64, P.a, P.u, k, prune, false, false,
-                    P.gamma, ecmax, P.qscale, P.iscale};
-
-    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x, ++it) {
+    prefetch(abA, ubA, t_begin);
+    prefetch(abB, ubB, t_begin + 1);
+    auto tile_body = [&](int (&ab)[PT], float (&ub)[PT], int64_t tile) {
         const int64_t base = tile * kIncTile;
         const int rows = (int)min((int64_t)kIncTile, n - base);
-        __syncthreads();   // the previous tile's queue and rows are consumed
-        if (tid == 0) qlen[(it + 1) & 1] = 0;
-        int* qn = qlen + (it & 1);
-
-        // Bound update and Clause 1 for this thread's PT points.
         int a_old[PT];
         float u_cur[PT];
         bool surv[PT];
 #pragma unroll
         for (int i = 0; i < PT; ++i) {
             const bool valid = tid + kTp * i < rows;
-            a_old[i] = valid ? abuf[i] : 0;
-            u_cur[i] = (ubuf[i] + fs[a_old[i]]) * kUp;
+            a_old[i] = valid ? ab[i] : 0;
+            u_cur[i] = (ub[i] + fs[a_old[i]]) * kUp;
             surv[i] = valid && (!prune || u_cur[i] > ss[a_old[i]]);
             if (valid && !surv[i]) {   // Clause 1: only the bound moves
                 P.u[base + tid + kTp * i] = u_cur[i];
                 my_c1 += 1;
             }
         }
-        if (tile + gridDim.x < ntiles) prefetch(tile + gridDim.x);
+        prefetch(ab, ub, tile + 2);
 #pragma unroll
-        for (int i = 0; i < PT; ++i) {   // survivor queue: one LDS atomic per wave and i
+        for (int i = 0; i < PT; ++i) {   // append to the list: one LDS atomic per wave and i
             const uint64_t bm = __ballot(surv[i]);
             int wbase = 0;
-            if (lane == 0 && bm) wbase = atomicAdd(qn, __popcll(bm));
+            if (lane == 0 && bm) wbase = atomicAdd(lenp, __popcll(bm));
             wbase = __shfl(wbase, 0);
             if (surv[i]) {
-                const int slot = wbase + __popcll(bm & ((1ull << lane) - 1ull));
-                sq[slot] = (tid + kTp * i) | ((a_old[i] + 1) << 16);
-                su[slot] = u_cur[i];
+                const int64_t e = lbase + wbase + __popcll(bm & ((1ull << lane) - 1ull));
+                F.lq[e] = (int)(base + tid + kTp * i);
+                F.la[e] = a_old[i];
+                F.lu[e] = u_cur[i];
             }
+        }
+    };
+    for (int64_t tile = t_begin; tile < t_end; tile += 2) {
+        tile_body(abA, ubA, tile);
+        if (tile + 1 < t_end) tile_body(abB, ubB, tile + 1);
+    }
+    __syncthreads();   // the list (global, this block's own writes) and its length are complete
+
+    // Phase 2: the survivors, kTp at a time.
+    const SurvCtx S{Cs, ecs, hs, acc, cnt, csu, kp, P.C64, P.a, P.u, k, prune, false, false,
+                    P.gamma, ecmax, P.qscale, P.iscale};
+    const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
+    const int len = *lenp;
+    for (int c0 = 0; c0 < len; c0 += kTp) {
+        const int nc = min(kTp, len - c0);
+        // Gather: the chunk's state, then its rows (QD 16-byte loads per thread).
+        int qi = 0;
+        if (tid < nc) {
+            qi = F.lq[lbase + c0 + tid];
+            cq[tid] = qi;
+            ca[tid] = F.la[lbase + c0 + tid];
+            cu[tid] = F.lu[lbase + c0 + tid];
         }
         __syncthreads();
-
-        const int nq = *qn;
-        for (int c0 = 0; c0 < nq; c0 += kTp) {
-            const int nc = min(kTp, nq - c0);
-            if (c0 > 0) __syncthreads();   // the previous chunk's rows are consumed
-            // Gather the chunk's rows: QD 16-byte loads per thread, all in flight.
-            f32x4 gbuf[QD];
+        f32x4 gbuf[QD];
 #pragma unroll
-            for (int i = 0; i < QD; ++i) {
-                const int idx = tid + kTp * i;
-                const int sl = idx < nc * QD ? idx / QD : 0;
-                const int li = sq[c0 + sl] & 0xffff;
-                gbuf[i] = __builtin_nontemporal_load(X4 + (base + li) * QD + idx % QD);
-            }
-#pragma unroll
-            for (int i = 0; i < QD; ++i) {
-                const int idx = tid + kTp * i;
-                if (idx < nc * QD) *reinterpret_cast<f32x4*>(Xs + (idx / QD) * XS + 4 * (idx % QD)) = gbuf[i];
-            }
-            __syncthreads();
-            process_survivors<D, G>(S, nc, [&](int i) {
-                const int e = sq[c0 + i];
-                const int li = e & 0xffff;
-                return Surv{Xs + i * XS, (e >> 16) - 1, su[c0 + i], base + li, li};
-            }, nullptr, my_changed, my_comp, my_rc, my_iq);
+        for (int i = 0; i < QD; ++i) {
+            const int idx = tid + kTp * i;
+            const int sl = idx < nc * QD ? idx / QD : 0;
+            gbuf[i] = __builtin_nontemporal_load(X4 + (int64_t)cq[sl] * QD + idx % QD);
         }
+#pragma unroll
+        for (int i = 0; i < QD; ++i) {
+            const int idx = tid + kTp * i;
+            if (idx < nc * QD) *reinterpret_cast<f32x4*>(Xs + (idx / QD) * XS + 4 * (idx % QD)) = gbuf[i];
+        }
+        __syncthreads();
+        process_survivors<D, G>(S, nc, [&](int i) {
+            return Surv{Xs + i * XS, ca[i], cu[i], (int64_t)cq[i], 0};
+        }, nullptr, my_changed, my_comp, my_rc, my_iq);
+        __syncthreads();   // rows and chunk state consumed
+        (void)qi;
     }
-    __syncthreads();
 
     // Block counters, then the block's moves into accumulation row
     // blockIdx % kSmallRows.
@@ -822,7 +836,9 @@ __global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F,
 // ---------------------------------------------------------------------------
 // Host-side launchers and configuration.
 
-bool small_applies(int d, int k, bool aligned) { return aligned && d == 16 && k <= kSmallMaxK; }
+bool small_applies(int64_t n, int d, int k, bool aligned) {
+    return aligned && d == 16 && k <= kSmallMaxK && n <= INT_MAX;   // int32 point indices in the ring
+}
 
 int small_group(int k) { return k <= 4 ? 4 : (k <= 8 ? 8 : 16); }
 
