@@ -33,12 +33,14 @@ def log(msg: str) -> None:
 
 
 # Dominant (assignment-step) kernel of each library path.
-DOMINANT_KERNEL = {"stream-d16": "k_small", "lds-vector": "k_assign", "lds-mfma": "k_assign",
+DOMINANT_KERNEL = {"stream-d16": "k_inc", "stream-d16-full": "k_small", "lds-vector": "k_assign",
+                   "lds-mfma": "k_assign",
                    "global-mfma": "k_mfma_large"}
 # Sources of each dominant kernel: the hardware byte counts of a committed
 # profile summary are used only while these files are unchanged.
 KERNEL_SOURCES = {
     "k_small": ["km_small.hip", "km_device.h", "km_internal.h"],
+    "k_inc": ["km_small.hip", "km_device.h", "km_internal.h"],
     "k_assign": ["km_kernels.hip", "km_device.h", "km_internal.h"],
     "k_mfma_large": ["km_large.hip", "km_device.h", "km_internal.h"],
 }
@@ -75,6 +77,16 @@ def measured_traffic(kernel: str, workload: str):
     return (fetch + write) * 1024.0, os.path.relpath(path, ROOT)
 
 
+def roofline_entry(kernel: str, workload: str, bytes_per_launch: float, launch_ms: float, what: str) -> dict:
+    """HBM roofline of one kernel: algorithmic bytes per launch over its mean
+    launch time (HIP events), against the 8 TB/s peak."""
+    achieved = bytes_per_launch / (launch_ms / 1e3) / 1e9
+    traffic, source = measured_traffic(kernel, workload)
+    return {"kernel": kernel, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "traffic_source": source,
+            "bytes_per_launch": bytes_per_launch, "bytes_def": what, "kernel_us": launch_ms * 1e3}
+
+
 def cpu_baseline(X, C0, w, budget_s: float = 15.0) -> dict:
     """Time the CPU oracle (plain float64 Lloyd's, as it stands) on this host."""
     import oracle
@@ -102,6 +114,8 @@ def main() -> int:
         ["blobs-10k-d16-k8", "blobs-1M-d32-k100", "aniso-8M-d16-k10", "blobs-2M-d256-k1000",
          "zipf-100M-d32-k64"]))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--full-sums", action="store_true",
+                    help="recompute the sums from every point each step (KM_FLAG_FULL_SUMS)")
     ap.add_argument("--profile", action="store_true",
                     help="run only the warmup and the timed region (no event pass, no job run, no "
                          "CPU leg), so a profiler sees warmup + K launches of each kernel")
@@ -143,15 +157,16 @@ def main() -> int:
     # Warmup: W iterations on a throwaway context (kernel load, caches, clocks).
     if args.profile:
         args.no_cpu_baseline = True
+    base_flags = {"full_sums": True} if args.full_sums else {}
     if args.warmup > 0:
-        with km.KMeansMTI(Xg, Cg) as ctx:
+        with km.KMeansMTI(Xg, Cg, **base_flags) as ctx:
             for _ in range(args.warmup):
                 ctx.iterate()
             torch.cuda.synchronize()
     log("warmup done (%d iterations)" % args.warmup)
 
     # Timed region: K iterations from C0, nothing else on the stream.
-    ctx = km.KMeansMTI(Xg, Cg)
+    ctx = km.KMeansMTI(Xg, Cg, **base_flags)
     path = ctx.path()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -164,38 +179,58 @@ def main() -> int:
     log("timed %d iterations in %.3f ms (path %s)" % (K, elapsed * 1e3, path))
 
     # The same K iterations again with HIP events around every launch (on the
-    # library's stream) for the per-kernel device times.
-    tm = None
-    if not args.profile:
-        with km.KMeansMTI(Xg, Cg, timing=True) as tctx:
-            for _ in range(K):
+    # library's stream) for the per-kernel device times; the first step is
+    # timed on its own, since it runs the full streaming kernel on every path.
+    def kernel_pass(**flags):
+        with km.KMeansMTI(Xg, Cg, timing=True, **flags) as tctx:
+            tctx.iterate()
+            t_first = tctx.timing()
+            for _ in range(K - 1):
                 tctx.iterate()
-            tm = tctx.timing()
+            t_all = tctx.timing()
+            h = tctx.history()
+        later = {key: t_all[key] - t_first[key] for key in t_all if key.endswith("_ms")}
+        return t_first, later, h
+
+    n, d, k = w.n, w.d, w.k
+    tm = first_t = later_t = None
+    rooflines = []
+    if not args.profile and K > 1:
+        first_t, later_t, h_ev = kernel_pass(**base_flags)
+        tm = {key: first_t[key] + later_t[key] for key in later_t}
+        tm["iters"] = K
+        kernel = DOMINANT_KERNEL.get(path, path)
+        surv = n * (K - 1) - int(h_ev["clause1"][1:].sum())
+        ch = int(h_ev["changed"][1:].sum())
+        if path == "stream-d16":
+            # Incremental steps: assignment and bound read, bound written, the
+            # survivors' rows read, the changed points' assignment written.
+            bytes_per_launch = (12 * n * (K - 1) + 4 * d * surv + 4 * ch) / (K - 1)
+            what = "steps 2..K: 12n + survivors*4d + changed*4"
+        else:
+            bytes_per_launch = n * (4 * d + 12) + 4 * ch / (K - 1)
+            what = "steps 2..K: n*(4d+12) + changed*4"
+        rooflines.append(roofline_entry(kernel, w.name, bytes_per_launch, later_t["assign_ms"] / (K - 1),
+                                        what))
+        if path == "stream-d16":   # the full-read streaming kernel on the same steps
+            _, later_f, h_f = kernel_pass(full_sums=True)
+            ch_f = int(h_f["changed"][1:].sum())
+            rooflines.append(roofline_entry("k_small", w.name, n * (4 * d + 12) + 4 * ch_f / (K - 1),
+                                            later_f["assign_ms"] / (K - 1),
+                                            "steps 2..K with KM_FLAG_FULL_SUMS: n*(4d+12) + changed*4"))
 
     # The job as the workload defines it (tol stop), for the iteration count.
     job = {"iterations": 0, "converged": 0, "device_ms": 0.0}
     if not args.profile:
-        _, _, job = km.run(Xg, Cg, w.max_iters, w.tol)
+        _, _, job = km.run(Xg, Cg, w.max_iters, w.tol, **base_flags)
         torch.cuda.synchronize()
 
-    n, d, k = w.n, w.d, w.k
     ips = K / elapsed
     computed = int(hist["computed"].sum())
-    changed = int(hist["changed"].sum())
     lloyd = n * k * K
-    kernel = DOMINANT_KERNEL.get(path, path)
-    # Algorithmic bytes of one launch of the dominant kernel: one read of X,
-    # the assignment read, the bound read and write, and the assignment
-    # writes of the points that changed (averaged over the timed steps).
-    bytes_per_launch = n * (4 * d + 12) + 4 * changed / K
-    roof = {"kernel": kernel, "bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": None, "traffic": None, "bytes_per_launch": bytes_per_launch}
-    if tm is not None:
-        assign_avg_s = tm["assign_ms"] / max(1, tm["iters"]) / 1e3
-        roof["achieved"] = bytes_per_launch / assign_avg_s / 1e9
-        roof["frac"] = roof["achieved"] / HBM_PEAK_GBS
-        roof["kernel_us"] = assign_avg_s * 1e6
-    roof["traffic"], roof["traffic_source"] = measured_traffic(kernel, w.name)
+    roof = rooflines[0] if rooflines else {"kernel": DOMINANT_KERNEL.get(path, path), "bound": "hbm",
+                                          "achieved": None, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                          "frac": None, "traffic": None}
     result = {
         "metric": METRIC,
         "value": ips,
@@ -217,10 +252,13 @@ def main() -> int:
         "clause1_frac": float(hist["clause1"].sum()) / (n * K),
         "kernel_ms_per_iter": None if tm is None else
             {key[:-3]: tm[key] / max(1, tm["iters"]) for key in ("assign_ms", "reduce_ms", "update_ms", "table_ms")},
+        "first_step_ms": None if first_t is None else
+            {key[:-3]: first_t[key] for key in ("assign_ms", "reduce_ms", "update_ms", "table_ms")},
         "job": {"iterations": job["iterations"], "converged": bool(job["converged"]),
                 "device_ms": job["device_ms"],
                 "iters_per_s": job["iterations"] / (job["device_ms"] / 1e3) if job["device_ms"] else None},
         "roofline": roof,
+        "rooflines_all": rooflines[1:],
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")

@@ -9,8 +9,8 @@
 //      (no dependence on the distance work, so it overlaps the stream);
 //   3. compacts the Clause-1 survivors into a queue; a tile with many
 //      survivors gives each one lane that scans the centroids in index order,
-//      ignoring a centroid that Clause 2 (u <= h(a, c), Elkan's lemma) rules
-//      out; a tile with few gives each
+//      skipping a centroid for the whole wave when Clause 2 (u <= h(a, c),
+//      Elkan's lemma) holds for every lane; a tile with few gives each
 //      survivor a group of G >= k lanes, lane j evaluating centroid j unless
 //      Clause 2 skips it, and the group takes the minimum with the oracle's
 //      tie rule and the second-best value with DPP row reductions; near ties
@@ -155,8 +155,8 @@ __device__ inline void move_sums(const SurvCtx& S, int cp, const float* x, int i
 }
 
 // Survivors 0 .. nq-1 (nq <= kTp) of a block.  Many: one lane each, scanning
-// the centroids in index order (a centroid that Clause 2 rules out is
-// computed but ignored).  Few: G lanes each, lane j for centroid j.
+// the centroids in index order and skipping one for the whole wave when
+// Clause 2 holds for every lane.  Few: G lanes each, lane j for centroid j.
 // Writes the bound, the assignment if it changed, sa[r] = b in the first
 // step, and moves the sums of a changed point (not in the first step).
 template <int D, int G, class Entry>
@@ -185,22 +185,23 @@ __device__ inline void process_survivors(const SurvCtx& S, int nq, Entry entry, 
         uint32_t kb = 0xFFFFFFFFu;
         float Db = INFINITY, D2 = INFINITY;
         uint64_t nc = 0;
-        // Branch-free body, unrolled by two, so that the distance chains of
-        // consecutive centroids overlap.
-        const float* hrow = S.hs + max(inc, 0) * k;
-#pragma unroll 2
         for (int jj = 0; jj < k; ++jj) {
             // Clause 2: c_jj cannot be strictly closer than the incumbent.
-            const bool need = !(S.prune && inc >= 0 && jj != inc && v.u <= hrow[jj]);
+            const bool need = !(S.prune && inc >= 0 && jj != inc && v.u <= S.hs[max(inc, 0) * k + jj]);
+            if (!__any(need)) continue;   // the whole wave skips c_jj
             const float Dj = sqd_row<D>(x, S.Cs + jj * CR);
-            const uint32_t key = jj == inc ? 0u : (uint32_t)jj + 1u;
-            const bool better = need && (Dj < Db || (Dj == Db && key < kb));
-            const float D2n = better ? Db : (need ? fminf(D2, Dj) : D2);
-            D2 = D2n;
-            Db = better ? Dj : Db;
-            b = better ? jj : b;
-            kb = better ? key : kb;
-            nc += need ? 1 : 0;
+            if (need) {
+                nc += 1;
+                const uint32_t key = jj == inc ? 0u : (uint32_t)jj + 1u;
+                if (Dj < Db || (Dj == Db && key < kb)) {
+                    D2 = Db;
+                    Db = Dj;
+                    b = jj;
+                    kb = key;
+                } else {
+                    D2 = fminf(D2, Dj);
+                }
+            }
         }
         if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
         float ub = upper_bound(Db, S.ecs[b], S.gamma);
