@@ -203,10 +203,13 @@ def main() -> int:
         surv = n * (K - 1) - int(h_ev["clause1"][1:].sum())
         ch = int(h_ev["changed"][1:].sum())
         if path == "stream-d16":
-            # Incremental steps: assignment and bound read, bound written, the
-            # survivors' rows read, the changed points' assignment written.
-            bytes_per_launch = (12 * n * (K - 1) + 4 * d * surv + 4 * ch) / (K - 1)
-            what = "steps 2..K: 12n + survivors*4d + changed*4"
+            # Incremental steps: every point's 4-byte state read; a survivor's
+            # row read and its state rewritten (Clause-1 points are not written).
+            bytes_per_launch = (4 * n * (K - 1) + (4 * d + 4) * surv) / (K - 1)
+            what = "steps 2..K: 4n (states) + survivors*(4d+4) (rows, new states)"
+        elif path == "stream-d16-full":
+            bytes_per_launch = (n * (4 * d + 4) * (K - 1) + 4 * surv) / (K - 1)
+            what = "steps 2..K: n*(4d+4) (rows, states) + survivors*4 (new states)"
         else:
             bytes_per_launch = n * (4 * d + 12) + 4 * ch / (K - 1)
             what = "steps 2..K: n*(4d+12) + changed*4"
@@ -214,10 +217,10 @@ def main() -> int:
                                         what))
         if path == "stream-d16":   # the full-read streaming kernel on the same steps
             _, later_f, h_f = kernel_pass(full_sums=True)
-            ch_f = int(h_f["changed"][1:].sum())
-            rooflines.append(roofline_entry("k_small", w.name, n * (4 * d + 12) + 4 * ch_f / (K - 1),
+            surv_f = n * (K - 1) - int(h_f["clause1"][1:].sum())
+            rooflines.append(roofline_entry("k_small", w.name, (n * (4 * d + 4) * (K - 1) + 4 * surv_f) / (K - 1),
                                             later_f["assign_ms"] / (K - 1),
-                                            "steps 2..K with KM_FLAG_FULL_SUMS: n*(4d+12) + changed*4"))
+                                            "steps 2..K with KM_FLAG_FULL_SUMS: n*(4d+4) + survivors*4"))
 
     # The job as the workload defines it (tol stop), for the iteration count.
     job = {"iterations": 0, "converged": 0, "device_ms": 0.0}

@@ -316,8 +316,9 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     }
 
     int rc;
-    if ((rc = c->alloc(&v.a, (size_t)n)) || (rc = c->alloc(&v.u, (size_t)n)) ||
-        (rc = c->alloc(&v.C64, (size_t)k * d)) || (rc = c->alloc(&v.C32, (size_t)k * d)) ||
+    if (!c->small && ((rc = c->alloc(&v.a, (size_t)n)) || (rc = c->alloc(&v.u, (size_t)n))))
+        return rc;
+    if ((rc = c->alloc(&v.C64, (size_t)k * d)) || (rc = c->alloc(&v.C32, (size_t)k * d)) ||
         (rc = c->alloc(&v.ec, (size_t)k)) || (rc = c->alloc(&v.h, (size_t)k * k)) ||
         (rc = c->alloc(&v.s, (size_t)k)) || (rc = c->alloc(&v.f, (size_t)k)) ||
         (rc = c->alloc(&v.cn2, (size_t)k)) ||
@@ -325,16 +326,19 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         (rc = c->alloc(&v.st, 1)) || (rc = c->alloc(&v.rec, (size_t)km::kHistCap)))
         return rc;
     if (c->small) {
+        // Point states padded to whole incremental tiles (the padding stays zero).
+        const size_t nw = (size_t)((n + km::kIncTile - 1) / km::kIncTile) * km::kIncTile;
         if ((rc = c->alloc(&c->fz.rows, (size_t)km::kSmallRows * v.L)) ||
-            (rc = c->alloc(&c->fz.sum, (size_t)k * d + k)))
+            (rc = c->alloc(&c->fz.sum, (size_t)k * d + k)) || (rc = c->alloc(&c->fz.w, nw)) ||
+            (rc = c->alloc(&c->fz.dhi, (size_t)k)) || (rc = c->alloc(&c->fz.dlo, (size_t)k)) ||
+            (rc = c->alloc(&c->fz.dup, (size_t)k)) || (rc = c->alloc(&c->fz.ddn, (size_t)k)))
             return rc;
-        if (c->inc) {
-            const size_t cap = (size_t)c->gi * (size_t)c->fz.span;
-            if ((rc = c->alloc(&c->fz.lq, cap)) || (rc = c->alloc(&c->fz.la, cap)) ||
-                (rc = c->alloc(&c->fz.lu, cap)))
-                return rc;
-        }
         KM_HIP(hipMemsetAsync(c->fz.rows, 0, sizeof(uint64_t) * (size_t)km::kSmallRows * v.L, c->stream));
+        KM_HIP(hipMemsetAsync(c->fz.w, 0, sizeof(uint32_t) * nw, c->stream));
+        KM_HIP(hipMemsetAsync(c->fz.dhi, 0, sizeof(double) * (size_t)k, c->stream));
+        KM_HIP(hipMemsetAsync(c->fz.dlo, 0, sizeof(double) * (size_t)k, c->stream));
+        KM_HIP(hipMemsetAsync(c->fz.dup, 0, sizeof(float) * (size_t)k, c->stream));
+        KM_HIP(hipMemsetAsync(c->fz.ddn, 0, sizeof(float) * (size_t)k, c->stream));
     }
     uint32_t* scratch = nullptr;
     if ((rc = c->alloc(&scratch, 4))) return rc;
@@ -454,7 +458,10 @@ int kmeans_mti_get(km_ctx* ctx, int32_t* assign_out, float* C_out) {
                      KM_OK)
         return rc;
     hipError_t e;
-    if (assign_out &&
+    if (assign_out && ctx->small &&
+        (e = km::launch_small_unpack(ctx->fz, ctx->n, assign_out, ctx->stream)) != hipSuccess)
+        return fail_ctx(ctx, hip_fail(e, "assignment unpack kernel"));
+    if (assign_out && !ctx->small &&
         (e = hipMemcpyAsync(assign_out, ctx->dv.a, (size_t)ctx->n * sizeof(int32_t),
                             hipMemcpyDeviceToDevice, ctx->stream)) != hipSuccess)
         return fail_ctx(ctx, hip_fail(e, "hipMemcpyAsync assign"));

@@ -147,37 +147,60 @@ __host__ __device__ inline AssignLds assign_lds(int d, int k, int tp, bool h_lds
     return L;
 }
 
-// Streaming path for small k and d = 16 (km_small.hip): the streaming kernel,
-// then one block that reduces, updates and rebuilds the centroid table.
-constexpr int kSmallTile = 256;   // points per tile = threads per block
-constexpr int kSmallMaxK = 16;
+// Streaming path for small k and d = 16 (km_small.hip): the streaming kernel
+// (every row of X read) or the incremental kernel (only the Clause-1
+// survivors' rows read), then one block that reduces, updates and rebuilds
+// the centroid table.
+constexpr int kSmallTile = 256;   // threads per block; points per tile of the streaming kernel
+constexpr int kSmallMaxK = 16;    // the cluster index fits in the 4 low bits of the point state
 constexpr int kSmallCopies = 4;   // copies of the LDS sums (spread rows over banks and addresses)
+constexpr int kSmallRowStride = 20;   // padded LDS row stride (floats) of centroid and queued rows
 
 // Accumulation rows of the streaming step: block b adds its partial row into
 // row b % kSmallRows with device atomics; the finishing block sums and clears
 // them.
 constexpr int kSmallRows = 16;
+
+// Incremental kernel: each block owns a contiguous range of tiles of
+// kIncTile points; wave w of a block takes points 256w .. 256w+255 of each
+// tile (four per lane, one 16-byte state load).
+constexpr int kIncTile = 1024;
+
+// Survivor queues in LDS.  A batch of kSmallTile survivors is scanned as soon
+// as that many are queued, so a queue holds at most kSmallTile - 1 plus one
+// tile's points.
+constexpr int kSmallQ = 2 * kSmallTile;          // streaming kernel: rows staged with the entries
+// Incremental kernel: one queue per wave (point index and cluster); a wave
+// scans a batch of 64 as soon as that many are queued, and one wave tile
+// adds at most 256.
+constexpr int kIncWaveQ = 64 + kIncTile / 4;
+constexpr int kIncQ = 4 * kIncWaveQ;
+
+// Point state of the streaming path: one 32-bit word per point.  Bits 3..0
+// hold the assigned cluster; the word with those bits cleared is a float32
+// value v such that v + (cumulative drift of that cluster) is an upper bound
+// on the point's distance to its centroid.  The drift of every later update
+// is then added by the reader, so a point whose bound needs no tightening is
+// never written.
 struct Fused {
     uint64_t* rows;       // kSmallRows x L, zero between steps
     uint64_t* sum;        // k*d + k: exact sums and counts after the last update
-    int32_t* lq;          // survivor lists of the incremental step: point index,
-    int32_t* la;          //   incumbent,
-    float* lu;            //   drift-updated bound; block b owns entries [b * span, (b + 1) * span)
-    int64_t span;         // tiles per block * kIncTile
+    uint32_t* w;          // point states, n rounded up to kIncTile (padding zero)
+    double* dhi;          // k: cumulative drift sum_t f_j^t, rounded up (float64)
+    double* dlo;          // k: the same rounded down
+    float* dup;           // k: dhi rounded up to float32
+    float* ddn;           // k: dlo rounded down to float32
+    int64_t span;         // points per block of the incremental kernel (multiple of kIncTile)
 };
-
-// Incremental step (km_small.hip): each block streams the bound and
-// assignment of a contiguous range of tiles of kIncTile points, lists its
-// Clause-1 survivors in global memory, then gathers their X rows and scans
-// them kSmallTile at a time.
-constexpr int kIncTile = 1024;
 
 struct SmallLds {
-    int off_c, off_f, off_s, off_ec, off_h, off_acc, off_cnt, off_x, off_sq, off_sa, off_su, off_misc, bytes;
-    int csu, kp;          // row stride (uint64) of one copy of the sums; of one copy of the counts
+    int off_c, off_h, off_s, off_ec, off_du, off_dd, off_acc, off_cnt, off_qr, off_qp, off_qa, off_misc, bytes;
+    int csu, kp;          // stride (uint64) of one copy of the sums; of one copy of the counts
 };
 
-__host__ __device__ inline SmallLds small_lds(int k) {
+// Dynamic LDS layout of the streaming (staged = true: queued rows kept in
+// LDS) and incremental (staged = false: one batch of gathered rows) kernels.
+__host__ __device__ inline SmallLds small_lds(int k, bool staged) {
     SmallLds L;
     int o = 0;
     auto take = [&](int bytes, int align) {
@@ -186,50 +209,22 @@ __host__ __device__ inline SmallLds small_lds(int k) {
         o += bytes;
         return r;
     };
+    const int q = staged ? kSmallQ : kIncQ;
     L.csu = 16 * k + 1;   // odd: the copies start on different banks
     L.kp = k + 1;
-    L.off_c = take(4 * k * 20, 16);
-    L.off_f = take(4 * k, 16);
+    L.off_c = take(4 * k * kSmallRowStride, 16);
+    L.off_h = take(4 * k * kSmallMaxK, 16);   // rows padded to kSmallMaxK (16-byte row loads)
     L.off_s = take(4 * k, 16);
     L.off_ec = take(4 * k, 16);
-    L.off_h = take(4 * k * k, 16);
+    L.off_du = take(4 * k, 16);
+    L.off_dd = take(4 * k, 16);
     L.off_acc = take(8 * kSmallCopies * L.csu, 16);
     L.off_cnt = take(4 * kSmallCopies * L.kp, 16);
-    L.off_x = take(4 * kSmallTile * 20, 16);
-    L.off_sq = take(4 * kSmallTile, 16);
-    L.off_sa = take(4 * kSmallTile, 16);
-    L.off_su = take(4 * kSmallTile, 16);
-    L.off_misc = take(64, 16);
-    L.bytes = (o + 15) / 16 * 16;
-    return L;
-}
-
-// Dynamic LDS layout of the incremental kernel: the tables and sums as in
-// small_lds, and one chunk of kSmallTile survivors (rows, index, incumbent,
-// bound).
-__host__ __device__ inline SmallLds inc_lds(int k) {
-    SmallLds L;
-    int o = 0;
-    auto take = [&](int bytes, int align) {
-        o = (o + align - 1) / align * align;
-        int r = o;
-        o += bytes;
-        return r;
-    };
-    L.csu = 16 * k + 1;
-    L.kp = k + 1;
-    L.off_c = take(4 * k * 20, 16);
-    L.off_f = take(4 * k, 16);
-    L.off_s = take(4 * k, 16);
-    L.off_ec = take(4 * k, 16);
-    L.off_h = take(4 * k * k, 16);
-    L.off_acc = take(8 * kSmallCopies * L.csu, 16);
-    L.off_cnt = take(4 * kSmallCopies * L.kp, 16);
-    L.off_x = take(4 * kSmallTile * 20, 16);
-    L.off_sq = take(4 * kSmallTile, 16);   // chunk: point index
-    L.off_sa = take(4 * kSmallTile, 16);   // chunk: incumbent
-    L.off_su = take(4 * kSmallTile, 16);   // chunk: drift-updated bound
-    L.off_misc = take(64, 16);             // list length (int) at 0, counters at 16
+    // Queued rows (streaming kernel) or one gathered batch (incremental kernel).
+    L.off_qr = take(4 * (staged ? kSmallQ : kSmallTile) * kSmallRowStride, 16);
+    L.off_qp = take(4 * q, 16);
+    L.off_qa = take(4 * q, 16);
+    L.off_misc = take(64, 16);   // three queue counters (int) at 0, kNumStat uint64 counters at 16
     L.bytes = (o + 15) / 16 * 16;
     return L;
 }
@@ -247,6 +242,8 @@ int inc_lds_bytes(int k);
 int small_finish_lds_bytes(int k);
 hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, hipStream_t s);
 hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, hipStream_t s);
+// assign_out[i] = cluster of point i from the point states.
+hipError_t launch_small_unpack(const Fused& F, int64_t n, int32_t* assign_out, hipStream_t s);
 // delta: the rows hold the moves of one incremental step (added to F.sum),
 // else the full sums of a streaming step (replace F.sum).
 hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, hipStream_t s);

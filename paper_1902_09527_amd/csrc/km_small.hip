@@ -1,30 +1,44 @@
 // Streaming MTI iteration for small k (k <= 16) and d = 16: two launches per
 // merged ||Lloyd's step (paper section III-B).
 //
-// k_small streams X once in 256-point tiles (persistent blocks, one tile
-// prefetched into registers), and per tile
-//   1. updates every point's bound with the drift of its cluster and applies
-//      Clause 1 (section III-C, Table I);
-//   2. adds every point to the fixed-point sums of its PREVIOUS cluster
-//      (no dependence on the distance work, so it overlaps the stream);
-//   3. compacts the Clause-1 survivors into a queue; a tile with many
-//      survivors gives each one lane that scans the centroids in index order,
-//      skipping a centroid for the whole wave when Clause 2 (u <= h(a, c),
-//      Elkan's lemma) holds for every lane; a tile with few gives each
-//      survivor a group of G >= k lanes, lane j evaluating centroid j unless
-//      Clause 2 skips it, and the group takes the minimum with the oracle's
-//      tie rule and the second-best value with DPP row reductions; near ties
-//      are decided in float64;
-//   4. moves a point whose assignment changed from its old cluster's sums to
-//      the new one (exact integer subtraction and addition, one coordinate
-//      per lane of the group).
+// Point state.  Every point keeps one 32-bit word: its cluster in the low 4
+// bits and, in the rest, a float32 value v such that v plus the cumulative
+// drift D_a = sum over updates of f(c_a) (Table I) is an upper bound on the
+// point's distance to its centroid.  This is the bound of section III-C,
+// u^t = u^{t0} + f^{t0+1} + ... + f^t, kept as v = u^{t0} - D_a^{t0} so that a
+// point whose bound is not tightened is never rewritten; the reader adds
+// D_a^t.  v is rounded up and D is held rounded up (when read) and down (when
+// subtracted), so the bound stays valid for the float64 master centroids.
+//
+// k_small streams every row of X (persistent blocks, 256-point tiles, two
+// tiles in flight per block).  Per tile it
+//   1. applies Clause 1 to each point's drift-updated bound: u <= s(c_a) with
+//      s(c) half the distance to the nearest other centroid (Elkan's lemma);
+//   2. adds every row, from registers, to the fixed-point sums of its
+//      PREVIOUS cluster (all points contribute, the sums are Lloyd's);
+//   3. queues the Clause-1 survivors, rows included, in LDS.
+// Whenever 256 survivors are queued, each lane scans one of them: the
+// distance to its incumbent (the tightening of the bound), then the other
+// centroids in index order, skipping c_j when the tightened bound is at most
+// half the distance from the incumbent to c_j (Clause 3), with the oracle's
+// tie rule and a float64 decision of near ties.  A point whose
+// cluster changed moves its row from the old cluster's sums to the new one's
+// (exact integer subtraction and addition).  In the first step there is no
+// bound: every point is scanned and adds itself to its new cluster.
+//
+// k_inc (steps after the first, the paper's skipping of the data of points
+// Clause 1 keeps, section III-C) reads only the point states, one 16-byte
+// load of four states per thread; the survivors are queued by index and
+// their rows gathered from X when a batch is scanned.  Its sums hold only the
+// moves, which the finishing block adds to the exact sums of the previous
+// step.
+//
 // The block's sums are integers, so their order does not matter; each block
 // adds its row into one of kSmallRows accumulation rows with device atomics.
-// k_small_finish (one block) then adds those rows, forms the new centroids
-// (member means; an empty cluster keeps its centroid), the drift f(c), the
-// stop test and the centroid table h, s(c) for the next step (sections III-C
-// and IV-A), and clears the rows.  No block waits for another and no fence
-// is needed inside a kernel: the launch boundary orders the two.
+// k_small_finish (one block) adds those rows, forms the new centroids (member
+// means; an empty cluster keeps its centroid), the drift, the cumulative
+// drift, the stop test and the centroid table h, s(c) for the next step
+// (sections III-C and IV-A), and clears the rows.
 #include <float.h>
 #include <limits.h>
 #include <math.h>
@@ -39,16 +53,42 @@ extern __shared__ __align__(16) unsigned char km_smem[];
 
 namespace {
 
-constexpr int kTp = kSmallTile;    // points per tile = threads per block
+constexpr int kTp = kSmallTile;       // threads per block
 constexpr int kCopies = kSmallCopies;
 constexpr int kFinishThreads = 256;   // threads of the finishing block
-constexpr int kLaneScanMin = 32;      // more survivors per tile: one lane per survivor
+constexpr int kD = 16;                // dimension of this path
+constexpr int kQD = kD / 4;           // 16-byte chunks per row
+constexpr int kCR = kSmallRowStride;  // padded LDS row stride (floats)
 
-template <int D>
-__device__ inline float sqd_row(const float (&x)[D], const float* c) {
+// Point state word: v rounded up to a multiple of 16 units in the last place
+// (for v >= 0 the bit pattern grows, for v < 0 the magnitude shrinks), with
+// the cluster in the cleared bits.
+__device__ __forceinline__ uint32_t pack_state(float v, int a) {
+    uint32_t b = __float_as_uint(v);
+    if (!(b >> 31)) b += 15u;
+    return (b & ~15u) | (uint32_t)a;
+}
+__device__ __forceinline__ int state_cluster(uint32_t w) { return (int)(w & 15u); }
+__device__ __forceinline__ float state_value(uint32_t w) { return __uint_as_float(w & ~15u); }
+
+// State of a point now assigned to b with distance bound ub: v = ub - D_b,
+// with D_b rounded down and the subtraction rounded up.
+__device__ __forceinline__ uint32_t settle_state(float ub, float ddn_b, int b) {
+    const float r = ub - ddn_b;
+    return pack_state(r + fabsf(r) * 0x1p-22f, b);
+}
+
+// Drift-updated bound of a state word (cumulative drift rounded up).
+__device__ __forceinline__ float state_bound(uint32_t w, const float* dup) {
+    return (state_value(w) + dup[state_cluster(w)]) * kUp;
+}
+
+// Squared float32 distance, coordinates in order (the same rounding as the
+// other kernels of the library).
+__device__ __forceinline__ float sqd_row(const float (&x)[kD], const float* c) {
     float acc = 0.f;
 #pragma unroll
-    for (int m = 0; m < D; m += 4) {
+    for (int m = 0; m < kD; m += 4) {
         const f32x4 cv = *reinterpret_cast<const f32x4*>(c + m);
         const float t0 = x[m] - cv.x, t1 = x[m + 1] - cv.y, t2 = x[m + 2] - cv.z, t3 = x[m + 3] - cv.w;
         acc = fmaf(t0, t0, acc);
@@ -59,22 +99,33 @@ __device__ inline float sqd_row(const float (&x)[D], const float* c) {
     return acc;
 }
 
+// Continues the squared-distance sum over one 4-coordinate chunk.
+__device__ __forceinline__ float sqd_chunk(const f32x4 x, const float* c, float acc) {
+    const f32x4 cv = *reinterpret_cast<const f32x4*>(c);
+    const float t0 = x.x - cv.x, t1 = x.y - cv.y, t2 = x.z - cv.z, t3 = x.w - cv.w;
+    acc = fmaf(t0, t0, acc);
+    acc = fmaf(t1, t1, acc);
+    acc = fmaf(t2, t2, acc);
+    return fmaf(t3, t3, acc);
+}
+
 // Float64 decision of a near tie against the master centroids, with the
 // oracle's rule: the incumbent keeps exact ties, then the lowest index wins.
 // Returns the winner; Db and ub become its squared distance and distance
 // bound.
-__device__ inline int recheck64(const float* x, const double* C64, int d, int k, int inc, float& Db,
+__device__ __forceinline__ int recheck64(const float (&x)[kD], const double* C64, int k, int inc, float& Db,
                                  float& ub) {
-    int bb = -1;
-    double Dbb = INFINITY;
-    auto dist = [&](int j) {
+    auto dist = [&](int j) __attribute__((always_inline)) {
         double acc = 0.0;
-        for (int m = 0; m < d; ++m) {
-            const double t = (double)x[m] - C64[(int64_t)j * d + m];
+#pragma unroll
+        for (int m = 0; m < kD; ++m) {
+            const double t = (double)x[m] - C64[j * kD + m];
             acc = fma(t, t, acc);
         }
         return acc;
     };
+    int bb = -1;
+    double Dbb = INFINITY;
     if (inc >= 0) {
         Dbb = dist(inc);
         bb = inc;
@@ -89,213 +140,214 @@ __device__ inline int recheck64(const float* x, const double* C64, int d, int k,
     }
     Db = (float)Dbb;
     ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
-    return bb;
+    return bb < 0 ? 0 : bb;
+}
+
+// Exact fixed-point image of a row added to (or, neg, subtracted from) one
+// LDS sum row.
+__device__ __forceinline__ void add_row(uint64_t* dst, const float (&x)[kD], double qscale, bool neg) {
+#pragma unroll
+    for (int m = 0; m < kD; ++m) {
+        const uint64_t v = fixed_bits((double)x[m], qscale);
+        atomicAdd(reinterpret_cast<unsigned long long*>(dst + m), (unsigned long long)(neg ? 0 - v : v));
+    }
+}
+
+// Per-block tables and sums in LDS, shared by both kernels.
+struct Tables {
+    float* C;      // k rows of kCR floats: float32 centroids
+    float* h;      // k rows of kSmallMaxK: half centroid distances, rounded down
+    float* s;      // k: s(c) = min over other centroids of h, rounded down
+    float* ec;     // k: float32 rounding error of each centroid, rounded up
+    float* dup;    // k: cumulative drift, rounded up
+    float* ddn;    // k: cumulative drift, rounded down
+    uint64_t* acc; // kCopies copies (stride csu) of the k x 16 fixed-point sums
+    uint32_t* cnt; // kCopies copies of the k counts (stride kp)
+    int* qc;       // three queue counters
+    uint64_t* bst; // kNumStat block counters
+    int csu, kp;
+};
+
+__device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, const SmallLds& lay) {
+    Tables T;
+    T.C = reinterpret_cast<float*>(km_smem + lay.off_c);
+    T.h = reinterpret_cast<float*>(km_smem + lay.off_h);
+    T.s = reinterpret_cast<float*>(km_smem + lay.off_s);
+    T.ec = reinterpret_cast<float*>(km_smem + lay.off_ec);
+    T.dup = reinterpret_cast<float*>(km_smem + lay.off_du);
+    T.ddn = reinterpret_cast<float*>(km_smem + lay.off_dd);
+    T.acc = reinterpret_cast<uint64_t*>(km_smem + lay.off_acc);
+    T.cnt = reinterpret_cast<uint32_t*>(km_smem + lay.off_cnt);
+    T.qc = reinterpret_cast<int*>(km_smem + lay.off_misc);
+    T.bst = reinterpret_cast<uint64_t*>(km_smem + lay.off_misc + 16);
+    T.csu = lay.csu;
+    T.kp = lay.kp;
+    const int k = P.k, tid = threadIdx.x;
+    for (int i = tid; i < k * kD; i += kTp) T.C[(i / kD) * kCR + i % kD] = P.C32[i];
+    for (int i = tid; i < k * k; i += kTp) T.h[(i / k) * kSmallMaxK + i % k] = P.h[i];
+    for (int i = tid; i < k; i += kTp) {
+        T.s[i] = P.s[i];
+        T.ec[i] = P.ec[i];
+        T.dup[i] = F.dup[i];
+        T.ddn[i] = F.ddn[i];
+    }
+    for (int i = tid; i < kCopies * T.csu; i += kTp) T.acc[i] = 0;
+    for (int i = tid; i < kCopies * T.kp; i += kTp) T.cnt[i] = 0;
+    if (tid < kNumStat) T.bst[tid] = 0;
+    if (tid < 3) T.qc[tid] = 0;
+    return T;
+}
+
+struct Counters {
+    uint64_t changed = 0, comp = 0, c1 = 0, rc = 0, iq = 0;
+};
+
+struct StepFlags {
+    bool first, prune, want_inertia;
+    float gamma, ecmax;
+};
+
+// One survivor, row x in registers: the scan, the new state word and, after
+// the first step, the move of a changed point's row between the sums (cp
+// selects the copy of the LDS sums).  In the first step the new cluster is
+// stored to *first_b instead.  KC >= k: distance slots.
+//
+// The distances to all k centroids are formed first (independent chains),
+// then the MTI decisions are taken on them in scan order, so that the count
+// of computed distances is that of the scan:
+//   later steps: the incumbent first (the tightening of the bound), then c_j
+//     in index order, skipped when the tightened bound is at most half the
+//     distance from the incumbent to c_j (Clause 3);
+//   first step (no bound): Elkan's running best, c_j skipped when the best
+//     bound so far is at most half the distance from the best centroid to c_j.
+// A skipped c_j is not strictly closer than the best, and a tie goes to the
+// best (the incumbent, or a lower index), so the skips never change the
+// result.
+template <int KC>
+__device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, const Tables& T, const StepFlags& fl,
+                                       const float (&x)[kD], int64_t p, int inc, int cp, Counters& cn,
+                                       int* first_b) {
+    const int k = P.k;
+    float Dall[KC];
+#pragma unroll
+    for (int j = 0; j < KC; ++j) Dall[j] = j < k ? sqd_row(x, T.C + j * kCR) : INFINITY;
+    int b;
+    float Db, ub, D2 = INFINITY;
+    uint64_t nc = 1;
+    if (inc >= 0) {
+        float hrow[KC];
+#pragma unroll
+        for (int j = 0; j < KC; j += 4) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(T.h + inc * kSmallMaxK + j);
+            hrow[j] = v.x;
+            hrow[j + 1] = v.y;
+            hrow[j + 2] = v.z;
+            hrow[j + 3] = v.w;
+        }
+        Db = INFINITY;
+#pragma unroll
+        for (int j = 0; j < KC; ++j) Db = j == inc ? Dall[j] : Db;
+        const float u = upper_bound(Db, T.ec[inc], fl.gamma);
+        b = inc;
+#pragma unroll
+        for (int j = 0; j < KC; ++j) {
+            if (j >= k || j == inc || (fl.prune && u <= hrow[j])) continue;
+            nc += 1;
+            if (Dall[j] < Db) {
+                D2 = Db;
+                Db = Dall[j];
+                b = j;
+            } else {
+                D2 = fminf(D2, Dall[j]);
+            }
+        }
+        ub = b == inc ? u : upper_bound(Db, T.ec[b], fl.gamma);
+    } else {
+        b = 0;
+        Db = Dall[0];
+        ub = upper_bound(Db, T.ec[0], fl.gamma);
+#pragma unroll
+        for (int j = 1; j < KC; ++j) {
+            if (j >= k || (fl.prune && ub <= T.h[b * kSmallMaxK + j])) continue;
+            nc += 1;
+            if (Dall[j] < Db) {
+                D2 = Db;
+                Db = Dall[j];
+                b = j;
+                ub = upper_bound(Db, T.ec[j], fl.gamma);
+            } else {
+                D2 = fminf(D2, Dall[j]);
+            }
+        }
+    }
+    if (D2 != INFINITY) {
+        const float band = 2.f * fl.gamma * (Db + D2) + 4.f * (sqrtf(Db) + sqrtf(D2)) * fl.ecmax +
+                           8.f * fl.ecmax * fl.ecmax;
+        if (D2 - Db <= band) {   // near tie: float64 decision, the oracle's tie rule
+            b = recheck64(x, P.C64, k, inc, Db, ub);
+            cn.rc += 1;
+        }
+    }
+    cn.comp += nc;
+    if (fl.want_inertia) cn.iq += fixed_bits((double)Db, P.iscale) - kMagicBits;
+    F.w[p] = settle_state(ub, T.ddn[b], b);
+    if (b != inc) cn.changed += 1;
+    if (fl.first) {
+        *first_b = b;   // the caller adds the row to the sums of b
+    } else if (b != inc) {
+        add_row(T.acc + cp * T.csu + b * kD, x, P.qscale, false);
+        add_row(T.acc + cp * T.csu + inc * kD, x, P.qscale, true);
+        atomicAdd(&T.cnt[cp * T.kp + b], 1u);
+        atomicAdd(&T.cnt[cp * T.kp + inc], 0xFFFFFFFFu);
+    }
+}
+
+// Block counters, then the block's sums (copies added) into accumulation
+// row blockIdx % kSmallRows.  skip_zero: only nonzero words are added.
+__device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const Tables& T, Counters& cn,
+                                   bool skip_zero) {
+    const int k = P.k, tid = threadIdx.x, lane = tid & 63;
+    const uint64_t v0 = wave_sum_u64(cn.changed), v1 = wave_sum_u64(cn.comp), v2 = wave_sum_u64(cn.c1),
+                   v3 = wave_sum_u64(cn.rc), v4 = wave_sum_u64(cn.iq);
+    __syncthreads();   // every wave is done with the queue and the sums
+    if (lane == 0) {
+        unsigned long long* b = reinterpret_cast<unsigned long long*>(T.bst);
+        atomicAdd(b + kStChanged, (unsigned long long)v0);
+        atomicAdd(b + kStComputed, (unsigned long long)v1);
+        atomicAdd(b + kStClause1, (unsigned long long)v2);
+        atomicAdd(b + kStRecheck, (unsigned long long)v3);
+        atomicAdd(b + kStInertia, (unsigned long long)v4);
+    }
+    __syncthreads();
+    unsigned long long* row =
+        reinterpret_cast<unsigned long long*>(F.rows + (int64_t)(blockIdx.x % kSmallRows) * P.L);
+    for (int i = tid; i < k * kD; i += kTp) {
+        uint64_t v = 0;
+#pragma unroll
+        for (int c = 0; c < kCopies; ++c) v += T.acc[c * T.csu + i];
+        if (v || !skip_zero) atomicAdd(row + i, (unsigned long long)v);
+    }
+    for (int i = tid; i < k; i += kTp) {
+        uint32_t v = 0;
+#pragma unroll
+        for (int c = 0; c < kCopies; ++c) v += T.cnt[c * T.kp + i];
+        // A count change is a 32-bit two's-complement value (moves may be negative).
+        if (v || !skip_zero) atomicAdd(row + k * kD + i, (unsigned long long)(int64_t)(int32_t)v);
+    }
+    if (tid < kNumStat && (T.bst[tid] || !skip_zero))
+        atomicAdd(row + k * kD + k + tid, (unsigned long long)T.bst[tid]);
 }
 
 }  // namespace
 
-// All-reduce minimum within aligned groups of G lanes (G = 4, 8 or 16) on DPP
-// row operations.
-template <int G>
-__device__ inline uint32_t group_min_u32(uint32_t v) {
-    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0xB1, 0xF, 0xF, false));   // xor 1
-    v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x4E, 0xF, 0xF, false));   // xor 2
-    if constexpr (G >= 8)
-        v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x141, 0xF, 0xF, false));   // half mirror
-    if constexpr (G >= 16)
-        v = min(v, (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x140, 0xF, 0xF, false));   // mirror
-    return v;
-}
-
 // ---------------------------------------------------------------------------
-// Survivor processing shared by the streaming and the incremental kernel.
+// The streaming kernel.  Wave w of a tile owns points 64w .. 64w+63; lane j
+// holds the state of point 64w + j.  X is read per wave as 4 coalesced
+// 16-byte loads per lane: load i of lane l holds chunk q = l % 4 of the
+// wave's row rho = 16i + l / 4.
 
-struct SurvCtx {
-    const float* Cs;       // LDS centroid rows (stride D + 4)
-    const float* ecs;      // LDS rounding errors of the float32 centroids
-    const float* hs;       // LDS half-distance table
-    uint64_t* acc;         // LDS sums, kCopies copies of stride csu
-    uint32_t* cnt;         // LDS counts, kCopies copies of stride kp
-    int csu, kp;
-    const double* C64;     // float64 master centroids (near-tie decisions)
-    int32_t* a;            // point assignments
-    float* u;              // point bounds
-    int k;
-    bool prune, first, want_inertia;
-    float gamma, ecmax;
-    double qscale, iscale;
-};
-
-// One survivor: its LDS row, incumbent (-1 in the first step), drift-updated
-// bound, global index and tile row.
-struct Surv {
-    const float* xrow;
-    int inc;
-    float u;
-    int64_t p;
-    int r;
-};
-
-// Moves point row x from cluster inc to b in the LDS sums (coordinates
-// m0, m0 + step, ...; counts when count is set).
-template <int D>
-__device__ inline void move_sums(const SurvCtx& S, int cp, const float* x, int inc, int b, int m0, int step,
-                                 bool count) {
-    uint64_t* to = S.acc + cp * S.csu + b * D;
-    uint64_t* from = S.acc + cp * S.csu + inc * D;
-    for (int m = m0; m < D; m += step) {
-        const uint64_t v = fixed_bits((double)x[m], S.qscale);
-        atomicAdd(reinterpret_cast<unsigned long long*>(to + m), (unsigned long long)v);
-        atomicAdd(reinterpret_cast<unsigned long long*>(from + m), (unsigned long long)(0 - v));
-    }
-    if (count) {
-        atomicAdd(&S.cnt[cp * S.kp + b], 1u);
-        atomicAdd(&S.cnt[cp * S.kp + inc], 0xFFFFFFFFu);
-    }
-}
-
-// Survivors 0 .. nq-1 (nq <= kTp) of a block.  Many: one lane each, scanning
-// the centroids in index order and skipping one for the whole wave when
-// Clause 2 holds for every lane.  Few: G lanes each, lane j for centroid j.
-// Writes the bound, the assignment if it changed, sa[r] = b in the first
-// step, and moves the sums of a changed point (not in the first step).
-template <int D, int G, class Entry>
-__device__ inline void process_survivors(const SurvCtx& S, int nq, Entry entry, int* sa, uint64_t& changed,
-                                         uint64_t& comp, uint64_t& rechecks, uint64_t& iq) {
-    constexpr int CR = D + 4;
-    constexpr int PER = kTp / G;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int k = S.k;
-    if (nq > kLaneScanMin) {
-        if (tid >= nq) return;
-        const Surv v = entry(tid);
-        const int inc = v.inc;
-        float x[D];
-#pragma unroll
-        for (int m = 0; m < D; m += 4) {
-            const f32x4 q = *reinterpret_cast<const f32x4*>(v.xrow + m);
-            x[m] = q.x;
-            x[m + 1] = q.y;
-            x[m + 2] = q.z;
-            x[m + 3] = q.w;
-        }
-        // Best so far under the oracle's order: smaller distance, then the
-        // incumbent, then the lower index (key 0 = incumbent).
-        int b = -1;
-        uint32_t kb = 0xFFFFFFFFu;
-        float Db = INFINITY, D2 = INFINITY;
-        uint64_t nc = 0;
-        for (int jj = 0; jj < k; ++jj) {
-            // Clause 2: c_jj cannot be strictly closer than the incumbent.
-            const bool need = !(S.prune && inc >= 0 && jj != inc && v.u <= S.hs[max(inc, 0) * k + jj]);
-            if (!__any(need)) continue;   // the whole wave skips c_jj
-            const float Dj = sqd_row<D>(x, S.Cs + jj * CR);
-            if (need) {
-                nc += 1;
-                const uint32_t key = jj == inc ? 0u : (uint32_t)jj + 1u;
-                if (Dj < Db || (Dj == Db && key < kb)) {
-                    D2 = Db;
-                    Db = Dj;
-                    b = jj;
-                    kb = key;
-                } else {
-                    D2 = fminf(D2, Dj);
-                }
-            }
-        }
-        if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
-        float ub = upper_bound(Db, S.ecs[b], S.gamma);
-        if (D2 != INFINITY) {
-            const float band = 2.f * S.gamma * (Db + D2) + 4.f * (sqrtf(Db) + sqrtf(D2)) * S.ecmax +
-                               8.f * S.ecmax * S.ecmax;
-            if (D2 - Db <= band) {   // near tie: float64 decision, the oracle's tie rule
-                b = recheck64(v.xrow, S.C64, D, k, inc, Db, ub);
-                rechecks += 1;
-            }
-        }
-        S.u[v.p] = ub;
-        comp += nc;
-        if (S.want_inertia) iq += fixed_bits((double)Db, S.iscale) - kMagicBits;
-        if (b != inc) {
-            S.a[v.p] = b;
-            changed += 1;
-        }
-        if (S.first) sa[v.r] = b;
-        else if (b != inc) move_sums<D>(S, tid & (kCopies - 1), x, inc, b, 0, 1, true);
-        return;
-    }
-    const int g = tid / G, j = tid % G;
-    const uint64_t gmask = ((1ull << G) - 1ull) << (lane - j);
-    for (int p0 = 0; p0 < nq; p0 += PER) {
-        const int slot = p0 + g;
-        const bool act = slot < nq;
-        const Surv v = entry(act ? slot : p0);
-        const int inc = v.inc;
-        // Clause 2: c_j cannot be strictly closer than the incumbent.
-        const bool want = act && j < k && !(S.prune && inc >= 0 && j != inc && v.u <= S.hs[max(inc, 0) * k + j]);
-        float Dj = INFINITY;
-        if (want) {
-            float x[D];
-#pragma unroll
-            for (int m = 0; m < D; m += 4) {
-                const f32x4 q = *reinterpret_cast<const f32x4*>(v.xrow + m);
-                x[m] = q.x;
-                x[m + 1] = q.y;
-                x[m + 2] = q.z;
-                x[m + 3] = q.w;
-            }
-            Dj = sqd_row<D>(x, S.Cs + j * CR);
-        }
-        // D >= 0, so float order is the order of the bit patterns.
-        const uint32_t dbits = __float_as_uint(Dj);
-        const uint32_t m1 = group_min_u32<G>(dbits);
-        // Among the minimal lanes the incumbent wins, then the lowest index.
-        const uint32_t key = dbits == m1 && want ? (j == inc ? 0u : (uint32_t)j + 1u) : 0xFFFFFFFFu;
-        const uint32_t kmin = group_min_u32<G>(key);
-        int b = kmin == 0u ? inc : (int)kmin - 1;
-        const uint32_t m2 = group_min_u32<G>(want && j != b ? dbits : 0x7F800000u);
-        float Db = __uint_as_float(m1);
-        const float D2 = __uint_as_float(m2);
-        const uint64_t wm = __ballot(want);
-        if (b < 0) b = 0;   // only for non-finite rows (no comparison succeeded)
-        float ub = upper_bound(Db, S.ecs[b], S.gamma);
-        bool re = false;
-        if (D2 != INFINITY) {
-            const float band = 2.f * S.gamma * (Db + D2) + 4.f * (sqrtf(Db) + sqrtf(D2)) * S.ecmax +
-                               8.f * S.ecmax * S.ecmax;
-            re = act && D2 - Db <= band;
-        }
-        if (re) b = recheck64(v.xrow, S.C64, D, k, inc, Db, ub);   // every lane of the group alike
-        if (act && j == 0) {
-            S.u[v.p] = ub;
-            if (b != inc) {
-                S.a[v.p] = b;
-                changed += 1;
-            }
-            if (S.first) sa[v.r] = b;
-            comp += (uint64_t)__popcll(wm & gmask);
-            if (re) rechecks += 1;
-            if (S.want_inertia) iq += fixed_bits((double)Db, S.iscale) - kMagicBits;
-        }
-        if (act && !S.first && b != inc) move_sums<D>(S, g & (kCopies - 1), v.xrow, inc, b, j, G, j == 0);
-    }
-}
-
-// ---------------------------------------------------------------------------
-// The streaming kernel.  Block = kTp threads; wave w of a tile owns points
-// 64w .. 64w+63.  X is prefetched per wave as D/4 coalesced 16-byte loads per
-// lane: load i of lane l holds the 4-float chunk q = (64i + l) % (D/4) of the
-// wave's row rho = (64i + l) / (D/4).  G: lanes per survivor (k <= G).
-
-template <int D, int G>
-__global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k_small(Dev P, Fused F) {
-    static_assert(D == 16, "streaming kernel is specialised for d = 16");
-    static_assert(G == 4 || G == 8 || G == 16, "survivor groups are DPP rows or parts of one");
-    constexpr int QD = D / 4;      // 16-byte chunks per row
-    constexpr int CH = QD;         // chunks per lane per tile (64 rows * QD / 64 lanes)
-    constexpr int XS = D + 4;      // padded LDS row stride of the tile (floats)
-    constexpr int CR = D + 4;      // padded LDS centroid row stride (floats)
-
+template <int KC>
+__global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k_small(Dev P, Fused F) {
     IterState* st = P.st;
     if (st->done) {
         if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
@@ -303,236 +355,197 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 1;
 
-    const int k = P.k;
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-    const bool first = st->t == 0;
-    const bool prune = !(P.flags & KM_FLAG_NO_PRUNE);
-    const bool want_inertia = (P.flags & KM_FLAG_STATS) != 0;
-    const float ecmax = st->ec_max;
-    const float gamma = P.gamma;
+    const StepFlags fl{st->t == 0, !(P.flags & KM_FLAG_NO_PRUNE), (P.flags & KM_FLAG_STATS) != 0, P.gamma,
+                       st->ec_max};
+    const SmallLds lay = small_lds(P.k, true);
+    const Tables T = load_tables(P, F, lay);
+    float* qr = reinterpret_cast<float*>(km_smem + lay.off_qr);   // queued rows
+    int* qp = reinterpret_cast<int*>(km_smem + lay.off_qp);       // queued point index
+    int* qa = reinterpret_cast<int*>(km_smem + lay.off_qa);       // queued incumbent (-1: none)
+    __syncthreads();
 
-    const SmallLds lay = small_lds(k);
-    float* Cs = reinterpret_cast<float*>(km_smem + lay.off_c);
-    float* fs = reinterpret_cast<float*>(km_smem + lay.off_f);
-    float* ss = reinterpret_cast<float*>(km_smem + lay.off_s);
-    float* ecs = reinterpret_cast<float*>(km_smem + lay.off_ec);
-    float* hs = reinterpret_cast<float*>(km_smem + lay.off_h);
-    uint64_t* acc = reinterpret_cast<uint64_t*>(km_smem + lay.off_acc);
-    uint32_t* cnt = reinterpret_cast<uint32_t*>(km_smem + lay.off_cnt);
-    float* Xs = reinterpret_cast<float*>(km_smem + lay.off_x);
-    int* sq = reinterpret_cast<int*>(km_smem + lay.off_sq);
-    int* sa = reinterpret_cast<int*>(km_smem + lay.off_sa);
-    float* su = reinterpret_cast<float*>(km_smem + lay.off_su);
-    int* qlen = reinterpret_cast<int*>(km_smem + lay.off_misc);
-    uint64_t* bst = reinterpret_cast<uint64_t*>(km_smem + lay.off_misc + 16);
-    const int csu = lay.csu, kp = lay.kp;
-
-    for (int i = tid; i < k * D; i += kTp) Cs[(i / D) * CR + i % D] = P.C32[i];
-    for (int i = tid; i < k; i += kTp) {
-        fs[i] = P.f[i];
-        ss[i] = P.s[i];
-        ecs[i] = P.ec[i];
-    }
-    for (int i = tid; i < k * k; i += kTp) hs[i] = P.h[i];
-    for (int i = tid; i < kCopies * csu; i += kTp) acc[i] = 0;
-    for (int i = tid; i < kCopies * kp; i += kTp) cnt[i] = 0;
-    if (tid < kNumStat) bst[tid] = 0;
-    if (tid < 2) qlen[tid] = 0;
-
-    uint64_t my_changed = 0, my_comp = 0, my_c1 = 0, my_rc = 0, my_iq = 0;
+    Counters cn;
     const int64_t n = P.n;
     const int64_t ntiles = (n + kTp - 1) / kTp;
-    const int64_t nchunks = n * QD;
+    const int64_t nchunks = n * kQD;
+    const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
+    const int rho0 = lane >> 2, q = lane & 3;
+    const uint64_t lt = (1ull << lane) - 1ull;
 
-    f32x4 xbuf[CH];
-    int abuf = 0;
-    float ubuf = 0.f;
-    auto prefetch = [&](int64_t tl) {
-        const f32x4* s4 = reinterpret_cast<const f32x4*>(P.X);
-        const int64_t c0 = (tl * kTp + 64 * w) * QD + lane;
+    f32x4 xA[kQD], xB[kQD];
+    uint32_t wA = 0, wB = 0;
+    auto prefetch = [&](f32x4 (&xb)[kQD], uint32_t& wb, int64_t tl) __attribute__((always_inline)) {
+        if (tl >= ntiles) return;
+        const int64_t c0 = (tl * kTp + 64 * w) * kQD + lane;
 #pragma unroll
-        for (int i = 0; i < CH; ++i) xbuf[i] = __builtin_nontemporal_load(s4 + min(c0 + 64 * i, nchunks - 1));
-        const int64_t q = min(tl * kTp + tid, n - 1);
-        abuf = P.a[q];   // unset before the first step: read but not used then
-        ubuf = P.u[q];
+        for (int i = 0; i < kQD; ++i) xb[i] = __builtin_nontemporal_load(X4 + min(c0 + 64 * i, nchunks - 1));
+        wb = F.w[tl * kTp + tid];   // the state array is padded past n
     };
-    if ((int64_t)blockIdx.x < ntiles) prefetch(blockIdx.x);
-    int it = 0;
+    prefetch(xA, wA, blockIdx.x);
+    prefetch(xB, wB, (int64_t)blockIdx.x + gridDim.x);
 
-    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x, ++it) {
+    // Scans the queued survivors [e0, e0 + cnt), one per lane.
+    auto scan_batch = [&](int e0, int cnt) __attribute__((always_inline)) {
+        if (tid < cnt) {
+            const int e = e0 + tid;
+            float x[kD];
+#pragma unroll
+            for (int c = 0; c < kQD; ++c) {
+                const f32x4 v = *reinterpret_cast<const f32x4*>(qr + e * kCR + 4 * c);
+                x[4 * c] = v.x;
+                x[4 * c + 1] = v.y;
+                x[4 * c + 2] = v.z;
+                x[4 * c + 3] = v.w;
+            }
+            settle_survivor<KC>(P, F, T, fl, x, qp[e], qa[e], tid & (kCopies - 1), cn, qa + e);
+        }
+    };
+
+    // First step: the scanned entries [e0, e0 + cnt) (new cluster in qa) into
+    // the sums, four lanes per row as in the streaming sums.
+    auto first_sums = [&](int e0, int cnt) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < kQD; ++i) {
+            const int slot = 64 * w + 16 * i + rho0;
+            if (slot < cnt) {
+                const int e = e0 + slot;
+                const int b = qa[e];
+                const f32x4 v = *reinterpret_cast<const f32x4*>(qr + e * kCR + 4 * q);
+                const int cp = slot & (kCopies - 1);
+                uint64_t* dst = T.acc + cp * T.csu + b * kD + 4 * q;
+                atomicAdd(reinterpret_cast<unsigned long long*>(dst + 0),
+                          (unsigned long long)fixed_bits((double)v.x, P.qscale));
+                atomicAdd(reinterpret_cast<unsigned long long*>(dst + 1),
+                          (unsigned long long)fixed_bits((double)v.y, P.qscale));
+                atomicAdd(reinterpret_cast<unsigned long long*>(dst + 2),
+                          (unsigned long long)fixed_bits((double)v.z, P.qscale));
+                atomicAdd(reinterpret_cast<unsigned long long*>(dst + 3),
+                          (unsigned long long)fixed_bits((double)v.w, P.qscale));
+                if (q == 0) atomicAdd(&T.cnt[cp * T.kp + b], 1u);
+            }
+        }
+    };
+
+    int queued = 0;   // block-uniform
+    int it = 0;
+    auto tile_body = [&](f32x4 (&xb)[kQD], uint32_t& wb, int64_t tile) __attribute__((always_inline)) {
         const int64_t base = tile * kTp;
         const int rows = (int)min((int64_t)kTp, n - base);
-        __syncthreads();   // the previous tile's queue and rows are consumed
-        if (tid == 0) qlen[(it + 1) & 1] = 0;
-        int* qn = qlen + (it & 1);
-
-        // 1. Bound update and Clause 1 for this lane's point.
         const bool valid = tid < rows;
-        const int64_t p = base + tid;
+        int* qcount = T.qc + it % 3;
+        if (tid == 0) T.qc[(it + 1) % 3] = 0;   // last read two barriers ago
+
+        // 1. Clause 1 on the drift-updated bound.
+        const uint32_t ws = wb;
         int a_old = -1;
-        float u_cur = INFINITY;
-        bool surv = false;
-        if (valid) {
-            if (first) {
-                surv = true;
-            } else {
-                a_old = abuf;
-                u_cur = (ubuf + fs[a_old]) * kUp;
-                surv = !prune || u_cur > ss[a_old];
-            }
+        bool surv = valid;
+        if (valid && !fl.first) {
+            a_old = state_cluster(ws);
+            surv = !fl.prune || !(state_bound(ws, T.dup) <= T.s[a_old]);
+            if (!surv) cn.c1 += 1;
         }
 
-        // 2. Stage the rows (for the survivor groups and the sums), start the
-        //    next tile's loads, and add every row to the sums of its previous
-        //    cluster.  Each wave reads back only rows it staged itself.
+        // 2. Every row into the sums of its previous cluster; with inertia,
+        //    the distance of each Clause-1 row to its centroid, summed over
+        //    the row's four chunks in coordinate order.
+        if (!fl.first) {
 #pragma unroll
-        for (int i = 0; i < CH; ++i) {
-            const int c = 64 * i + lane;
-            const int rho = c / QD, q = c - rho * QD;
-            *reinterpret_cast<f32x4*>(Xs + (64 * w + rho) * XS + 4 * q) = xbuf[i];
-        }
-        if (tile + gridDim.x < ntiles) prefetch(tile + gridDim.x);
-        if (!first) {
-#pragma unroll
-            for (int i = 0; i < CH; ++i) {
-                const int c = 64 * i + lane;
-                const int rho = c / QD, q = c - rho * QD;
+            for (int i = 0; i < kQD; ++i) {
+                const int rho = 16 * i + rho0;
                 const int ar = __shfl(a_old, rho);
                 if (64 * w + rho < rows) {
-                    const f32x4 xv = *reinterpret_cast<const f32x4*>(Xs + (64 * w + rho) * XS + 4 * q);
                     const int cp = rho & (kCopies - 1);
-                    uint64_t* dst = acc + cp * csu + ar * D + 4 * q;
+                    uint64_t* dst = T.acc + cp * T.csu + ar * kD + 4 * q;
                     atomicAdd(reinterpret_cast<unsigned long long*>(dst + 0),
-                              (unsigned long long)fixed_bits((double)xv.x, P.qscale));
+                              (unsigned long long)fixed_bits((double)xb[i].x, P.qscale));
                     atomicAdd(reinterpret_cast<unsigned long long*>(dst + 1),
-                              (unsigned long long)fixed_bits((double)xv.y, P.qscale));
+                              (unsigned long long)fixed_bits((double)xb[i].y, P.qscale));
                     atomicAdd(reinterpret_cast<unsigned long long*>(dst + 2),
-                              (unsigned long long)fixed_bits((double)xv.z, P.qscale));
+                              (unsigned long long)fixed_bits((double)xb[i].z, P.qscale));
                     atomicAdd(reinterpret_cast<unsigned long long*>(dst + 3),
-                              (unsigned long long)fixed_bits((double)xv.w, P.qscale));
-                    if (q == 0) atomicAdd(&cnt[cp * kp + ar], 1u);
+                              (unsigned long long)fixed_bits((double)xb[i].w, P.qscale));
+                    if (q == 0) atomicAdd(&T.cnt[cp * T.kp + ar], 1u);
+                }
+            }
+            if (fl.want_inertia) {
+                const bool keep = valid && !surv;
+#pragma unroll
+                for (int i = 0; i < kQD; ++i) {
+                    const int rho = 16 * i + rho0;
+                    const int ar = max(__shfl(a_old, rho), 0);
+                    const int kept = __shfl(keep ? 1 : 0, rho);   // all lanes take part
+                    const float* cr = T.C + ar * kCR + 4 * q;
+                    float r = 0.f;
+#pragma unroll
+                    for (int qq = 0; qq < kQD; ++qq) {
+                        const float prev = __shfl(r, (lane + 63) & 63);   // the lane of chunk q - 1
+                        const float v = sqd_chunk(xb[i], cr, q == 0 ? 0.f : prev);
+                        if (q == qq) r = v;
+                    }
+                    if (q == kQD - 1 && kept)
+                        cn.iq += fixed_bits((double)r, P.iscale) - kMagicBits;
                 }
             }
         }
 
-        // Clause-1 points are done: only the bound moves.
-        if (valid && !surv) {
-            P.u[p] = u_cur;
-            my_c1 += 1;
+        // 3. Queue the survivors: index and incumbent by the owning lane,
+        //    the row's chunks by the lanes that loaded them.
+        const uint64_t bm = __ballot(surv);
+        int wbase = 0;
+        if (lane == 0 && bm) wbase = atomicAdd(qcount, __popcll(bm));
+        wbase = __shfl(wbase, 0);
+        const int pos = queued + wbase + __popcll(bm & lt);
+        if (surv) {
+            qp[pos] = (int)(base + tid);
+            qa[pos] = a_old;
         }
-        if (surv) su[tid] = u_cur;
-        {   // survivor queue: one LDS atomic per wave, ranks from the ballot
-            const uint64_t bm = __ballot(surv);
-            int wbase = 0;
-            if (lane == 0 && bm) wbase = atomicAdd(qn, __popcll(bm));
-            wbase = __shfl(wbase, 0);
-            if (surv) sq[wbase + __popcll(bm & ((1ull << lane) - 1ull))] = tid | ((a_old + 1) << 16);
+#pragma unroll
+        for (int i = 0; i < kQD; ++i) {
+            const int rho = 16 * i + rho0;
+            const int rpos = __shfl(pos, rho);
+            if ((bm >> rho) & 1ull) *reinterpret_cast<f32x4*>(qr + rpos * kCR + 4 * q) = xb[i];
         }
+        prefetch(xb, wb, tile + 2 * (int64_t)gridDim.x);
         __syncthreads();
-
-        if (want_inertia && valid && !surv) {   // inertia of an unmoved point
-            float x[D];
-#pragma unroll
-            for (int m = 0; m < D; m += 4) {
-                const f32x4 v = *reinterpret_cast<const f32x4*>(Xs + tid * XS + m);
-                x[m] = v.x;
-                x[m + 1] = v.y;
-                x[m + 2] = v.z;
-                x[m + 3] = v.w;
+        queued += *qcount;
+        if (queued >= kTp) {   // a full batch: the newest kTp entries
+            queued -= kTp;
+            scan_batch(queued, kTp);
+            __syncthreads();   // its rows are consumed before the next tile queues over them
+            if (fl.first) {
+                first_sums(queued, kTp);
+                __syncthreads();
             }
-            my_iq += fixed_bits((double)sqd_row<D>(x, Cs + a_old * CR), P.iscale) - kMagicBits;
         }
-
-        // 3. Survivors; 4. moves of the changed points' sums.
-        const int nq = *qn;
-        {
-            const SurvCtx S{Cs, ecs, hs, acc, cnt, csu, kp, P.C64, P.a, P.u, k, prune, first, want_inertia,
-                            gamma, ecmax, P.qscale, P.iscale};
-            process_survivors<D, G>(S, nq, [&](int i) {
-                const int e = sq[i];
-                const int r = e & 0xffff;
-                return Surv{Xs + r * XS, (e >> 16) - 1, su[r], base + r, r};
-            }, sa, my_changed, my_comp, my_rc, my_iq);
-        }
-        if (first) {   // first step: sums of the new assignment, from the staged rows
+        ++it;
+    };
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += 2 * (int64_t)gridDim.x) {
+        tile_body(xA, wA, tile);
+        if (tile + gridDim.x < ntiles) tile_body(xB, wB, tile + gridDim.x);
+    }
+    if (queued > 0) {
+        scan_batch(0, queued);
+        if (fl.first) {
             __syncthreads();
-#pragma unroll
-            for (int i = 0; i < CH; ++i) {
-                const int c = 64 * i + lane;
-                const int rho = c / QD, q = c - rho * QD;
-                const int r = 64 * w + rho;
-                if (r < rows) {
-                    const int ar = sa[r];
-                    const f32x4 v = *reinterpret_cast<const f32x4*>(Xs + r * XS + 4 * q);
-                    const int cp = rho & (kCopies - 1);
-                    uint64_t* dst = acc + cp * csu + ar * D + 4 * q;
-                    atomicAdd(reinterpret_cast<unsigned long long*>(dst + 0),
-                              (unsigned long long)fixed_bits((double)v.x, P.qscale));
-                    atomicAdd(reinterpret_cast<unsigned long long*>(dst + 1),
-                              (unsigned long long)fixed_bits((double)v.y, P.qscale));
-                    atomicAdd(reinterpret_cast<unsigned long long*>(dst + 2),
-                              (unsigned long long)fixed_bits((double)v.z, P.qscale));
-                    atomicAdd(reinterpret_cast<unsigned long long*>(dst + 3),
-                              (unsigned long long)fixed_bits((double)v.w, P.qscale));
-                    if (q == 0) atomicAdd(&cnt[cp * kp + ar], 1u);
-                }
-            }
+            first_sums(0, queued);
         }
     }
-    __syncthreads();
-
-    // Block counters, then the block's row (copies of the sums added) into
-    // accumulation row blockIdx % kSmallRows.
-    my_changed = wave_sum_u64(my_changed);
-    my_comp = wave_sum_u64(my_comp);
-    my_c1 = wave_sum_u64(my_c1);
-    my_rc = wave_sum_u64(my_rc);
-    my_iq = wave_sum_u64(my_iq);
-    if (lane == 0) {
-        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStChanged]), my_changed);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStComputed]), my_comp);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStClause1]), my_c1);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStRecheck]), my_rc);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStInertia]), my_iq);
-    }
-    __syncthreads();
-    unsigned long long* row =
-        reinterpret_cast<unsigned long long*>(F.rows + (int64_t)(blockIdx.x % kSmallRows) * P.L);
-    for (int i = tid; i < k * D; i += kTp) {
-        uint64_t v = 0;
-#pragma unroll
-        for (int c = 0; c < kCopies; ++c) v += acc[c * csu + i];
-        atomicAdd(row + i, (unsigned long long)v);
-    }
-    for (int i = tid; i < k; i += kTp) {
-        uint32_t v = 0;
-#pragma unroll
-        for (int c = 0; c < kCopies; ++c) v += cnt[c * kp + i];
-        atomicAdd(row + k * D + i, (unsigned long long)v);
-    }
-    if (tid < kNumStat) atomicAdd(row + k * D + k + tid, (unsigned long long)bst[tid]);
+    flush_block(P, F, T, cn, false);
 }
 
 // ---------------------------------------------------------------------------
-// The incremental kernel (the paper's skipping of the data of points that
-// Clause 1 keeps, section III-C; ||Lloyd's per-thread sums, section V).
-// Steps after the first only.  Block b owns a contiguous range of tiles of
-// kIncTile points (PT per thread).  Phase 1 streams their assignments and
-// bounds: a Clause-1 point moves only its bound and its X row is never read;
-// a survivor is appended to the block's list in global memory.  Phase 2
-// takes the list kTp survivors at a time: their rows and state are gathered
-// into LDS and they are scanned as in the streaming kernel.  The block's row
-// then holds the moves of the points that changed, which the finishing block
-// adds to the exact sums of the previous step.
+// The incremental kernel (steps after the first).  Block b owns the points
+// [b * span, min(n, (b + 1) * span)) in tiles of kIncTile; wave w takes points
+// 256w .. 256w+255 of each tile, four per lane, two tiles in flight.  The
+// waves of a block run independently (no block barrier before the end): each
+// queues its Clause-1 survivors in its own LDS queue and, whenever 64 are
+// queued, gathers their rows (16-byte loads, four lanes per row), stages them
+// in its own LDS rows and scans them one per lane.  Only the sums in LDS are
+// shared, through atomics.
 
-template <int D, int G>
+template <int KC>
 __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P, Fused F) {
-    static_assert(D == 16, "incremental kernel is specialised for d = 16");
-    constexpr int QD = D / 4;               // 16-byte chunks per row
-    constexpr int XS = D + 4;               // padded LDS row stride of the gathered rows
-    constexpr int CR = D + 4;               // padded LDS centroid row stride
-    constexpr int PT = kIncTile / kTp;      // points per thread per tile
-
     IterState* st = P.st;
     if (st->done || st->t == 0) {   // the first step always runs the streaming kernel
         if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
@@ -540,170 +553,119 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 1;
 
-    const int k = P.k;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const bool prune = !(P.flags & KM_FLAG_NO_PRUNE);
-    const float ecmax = st->ec_max;
-
-    const SmallLds lay = inc_lds(k);
-    float* Cs = reinterpret_cast<float*>(km_smem + lay.off_c);
-    float* fs = reinterpret_cast<float*>(km_smem + lay.off_f);
-    float* ss = reinterpret_cast<float*>(km_smem + lay.off_s);
-    float* ecs = reinterpret_cast<float*>(km_smem + lay.off_ec);
-    float* hs = reinterpret_cast<float*>(km_smem + lay.off_h);
-    uint64_t* acc = reinterpret_cast<uint64_t*>(km_smem + lay.off_acc);
-    uint32_t* cnt = reinterpret_cast<uint32_t*>(km_smem + lay.off_cnt);
-    float* Xs = reinterpret_cast<float*>(km_smem + lay.off_x);
-    int* cq = reinterpret_cast<int*>(km_smem + lay.off_sq);
-    int* ca = reinterpret_cast<int*>(km_smem + lay.off_sa);
-    float* cu = reinterpret_cast<float*>(km_smem + lay.off_su);
-    int* lenp = reinterpret_cast<int*>(km_smem + lay.off_misc);
-    uint64_t* bst = reinterpret_cast<uint64_t*>(km_smem + lay.off_misc + 16);
-    const int csu = lay.csu, kp = lay.kp;
-
-    for (int i = tid; i < k * D; i += kTp) Cs[(i / D) * CR + i % D] = P.C32[i];
-    for (int i = tid; i < k; i += kTp) {
-        fs[i] = P.f[i];
-        ss[i] = P.s[i];
-        ecs[i] = P.ec[i];
-    }
-    for (int i = tid; i < k * k; i += kTp) hs[i] = P.h[i];
-    for (int i = tid; i < kCopies * csu; i += kTp) acc[i] = 0;
-    for (int i = tid; i < kCopies * kp; i += kTp) cnt[i] = 0;
-    if (tid < kNumStat) bst[tid] = 0;
-    if (tid == 0) *lenp = 0;
+    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+    const StepFlags fl{false, !(P.flags & KM_FLAG_NO_PRUNE), false, P.gamma, st->ec_max};
+    const SmallLds lay = small_lds(P.k, false);
+    const Tables T = load_tables(P, F, lay);
+    int* wq_p = reinterpret_cast<int*>(km_smem + lay.off_qp) + w * kIncWaveQ;   // this wave's queue
+    int* wq_a = reinterpret_cast<int*>(km_smem + lay.off_qa) + w * kIncWaveQ;
+    float* wg = reinterpret_cast<float*>(km_smem + lay.off_qr) + 64 * w * kCR;  // its staged rows
     __syncthreads();
 
-    uint64_t my_changed = 0, my_comp = 0, my_c1 = 0, my_rc = 0, my_iq = 0;
+    Counters cn;
     const int64_t n = P.n;
-    const int64_t ntiles = (n + kIncTile - 1) / kIncTile;
-    const int64_t tpb = F.span / kIncTile;
-    const int64_t t_begin = (int64_t)blockIdx.x * tpb;
-    const int64_t t_end = min(ntiles, t_begin + tpb);
-    const int64_t lbase = (int64_t)blockIdx.x * F.span;   // this block's list
-
-    // Phase 1: stream the assignments and bounds, two tiles in flight.
-    int abA[PT], abB[PT];
-    float ubA[PT], ubB[PT];
-    auto prefetch = [&](int (&ab)[PT], float (&ub)[PT], int64_t tl) {
-        if (tl >= t_end) return;
-#pragma unroll
-        for (int i = 0; i < PT; ++i) {
-            const int64_t q = min(tl * kIncTile + tid + kTp * i, n - 1);
-            ab[i] = P.a[q];
-            ub[i] = P.u[q];
-        }
-    };
-    prefetch(abA, ubA, t_begin);
-    prefetch(abB, ubB, t_begin + 1);
-    auto tile_body = [&](int (&ab)[PT], float (&ub)[PT], int64_t tile) {
-        const int64_t base = tile * kIncTile;
-        const int rows = (int)min((int64_t)kIncTile, n - base);
-        int a_old[PT];
-        float u_cur[PT];
-        bool surv[PT];
-#pragma unroll
-        for (int i = 0; i < PT; ++i) {
-            const bool valid = tid + kTp * i < rows;
-            a_old[i] = valid ? ab[i] : 0;
-            u_cur[i] = (ub[i] + fs[a_old[i]]) * kUp;
-            surv[i] = valid && (!prune || u_cur[i] > ss[a_old[i]]);
-            if (valid && !surv[i]) {   // Clause 1: only the bound moves
-                P.u[base + tid + kTp * i] = u_cur[i];
-                my_c1 += 1;
-            }
-        }
-        prefetch(ab, ub, tile + 2);
-#pragma unroll
-        for (int i = 0; i < PT; ++i) {   // append to the list: one LDS atomic per wave and i
-            const uint64_t bm = __ballot(surv[i]);
-            int wbase = 0;
-            if (lane == 0 && bm) wbase = atomicAdd(lenp, __popcll(bm));
-            wbase = __shfl(wbase, 0);
-            if (surv[i]) {
-                const int64_t e = lbase + wbase + __popcll(bm & ((1ull << lane) - 1ull));
-                F.lq[e] = (int)(base + tid + kTp * i);
-                F.la[e] = a_old[i];
-                F.lu[e] = u_cur[i];
-            }
-        }
-    };
-    for (int64_t tile = t_begin; tile < t_end; tile += 2) {
-        tile_body(abA, ubA, tile);
-        if (tile + 1 < t_end) tile_body(abB, ubB, tile + 1);
-    }
-    __syncthreads();   // the list (global, this block's own writes) and its length are complete
-
-    // Phase 2: the survivors, kTp at a time.
-    const SurvCtx S{Cs, ecs, hs, acc, cnt, csu, kp, P.C64, P.a, P.u, k, prune, false, false,
-                    P.gamma, ecmax, P.qscale, P.iscale};
+    const int64_t lo = (int64_t)blockIdx.x * F.span;
+    const int64_t hi = min(n, lo + F.span);
+    const uint64_t lt = (1ull << lane) - 1ull;
+    const uint4* W4 = reinterpret_cast<const uint4*>(F.w);
     const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
-    const int len = *lenp;
-    for (int c0 = 0; c0 < len; c0 += kTp) {
-        const int nc = min(kTp, len - c0);
-        // Gather: the chunk's state, then its rows (QD 16-byte loads per thread).
-        int qi = 0;
-        if (tid < nc) {
-            qi = F.lq[lbase + c0 + tid];
-            cq[tid] = qi;
-            ca[tid] = F.la[lbase + c0 + tid];
-            cu[tid] = F.lu[lbase + c0 + tid];
-        }
-        __syncthreads();
-        f32x4 gbuf[QD];
-#pragma unroll
-        for (int i = 0; i < QD; ++i) {
-            const int idx = tid + kTp * i;
-            const int sl = idx < nc * QD ? idx / QD : 0;
-            gbuf[i] = __builtin_nontemporal_load(X4 + (int64_t)cq[sl] * QD + idx % QD);
-        }
-#pragma unroll
-        for (int i = 0; i < QD; ++i) {
-            const int idx = tid + kTp * i;
-            if (idx < nc * QD) *reinterpret_cast<f32x4*>(Xs + (idx / QD) * XS + 4 * (idx % QD)) = gbuf[i];
-        }
-        __syncthreads();
-        process_survivors<D, G>(S, nc, [&](int i) {
-            return Surv{Xs + i * XS, ca[i], cu[i], (int64_t)cq[i], 0};
-        }, nullptr, my_changed, my_comp, my_rc, my_iq);
-        __syncthreads();   // rows and chunk state consumed
-        (void)qi;
-    }
+    const int rho0 = lane >> 2, q = lane & 3;
 
-    // Block counters, then the block's moves into accumulation row
-    // blockIdx % kSmallRows.
-    my_changed = wave_sum_u64(my_changed);
-    my_comp = wave_sum_u64(my_comp);
-    my_c1 = wave_sum_u64(my_c1);
-    my_rc = wave_sum_u64(my_rc);
-    if (lane == 0) {
-        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStChanged]), my_changed);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStComputed]), my_comp);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStClause1]), my_c1);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&bst[kStRecheck]), my_rc);
-    }
-    __syncthreads();
-    unsigned long long* row =
-        reinterpret_cast<unsigned long long*>(F.rows + (int64_t)(blockIdx.x % kSmallRows) * P.L);
-    for (int i = tid; i < k * D; i += kTp) {
-        uint64_t v = 0;
+    uint4 sA = {0, 0, 0, 0}, sB = {0, 0, 0, 0};
+    auto prefetch = [&](uint4& s, int64_t base) __attribute__((always_inline)) {
+        if (base < hi) s = W4[(base + 256 * w) / 4 + lane];   // the state array is padded past n
+    };
+    prefetch(sA, lo);
+    prefetch(sB, lo + kIncTile);
+
+    // Batches of up to 64 of this wave's survivors, software-pipelined: a
+    // batch's rows are requested when it is taken from the queue (16-byte
+    // loads, load i of lane l = chunk l % 4 of batch entry 16i + l / 4) and
+    // staged and scanned, one survivor per lane, at the next batch point or
+    // at the end, so that the loads overlap the next tile's Clause-1 work.
+    f32x4 r[kQD];
+    int bp = 0, binc = 0, bcnt = 0;   // the batch in flight: its entry (one per lane), size
+    auto take_batch = [&](int e0, int cnt) __attribute__((always_inline)) {
 #pragma unroll
-        for (int c = 0; c < kCopies; ++c) v += acc[c * csu + i];
-        if (v) atomicAdd(row + i, (unsigned long long)v);
-    }
-    for (int i = tid; i < k; i += kTp) {
-        uint32_t v = 0;
+        for (int i = 0; i < kQD; ++i) {
+            const int slot = 16 * i + rho0;
+            const int64_t rp = slot < cnt ? (int64_t)wq_p[e0 + slot] : 0;
+            r[i] = __builtin_nontemporal_load(X4 + rp * kQD + q);
+        }
+        bp = lane < cnt ? wq_p[e0 + lane] : 0;
+        binc = lane < cnt ? wq_a[e0 + lane] : 0;
+        bcnt = cnt;
+    };
+    auto scan_batch = [&]() __attribute__((always_inline)) {
 #pragma unroll
-        for (int c = 0; c < kCopies; ++c) v += cnt[c * kp + i];
-        if (v) atomicAdd(row + k * D + i, (unsigned long long)(int64_t)(int32_t)v);
+        for (int i = 0; i < kQD; ++i) *reinterpret_cast<f32x4*>(wg + (16 * i + rho0) * kCR + 4 * q) = r[i];
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (lane < bcnt) {
+            float x[kD];
+#pragma unroll
+            for (int c = 0; c < kQD; ++c) {
+                const f32x4 v = *reinterpret_cast<const f32x4*>(wg + lane * kCR + 4 * c);
+                x[4 * c] = v.x;
+                x[4 * c + 1] = v.y;
+                x[4 * c + 2] = v.z;
+                x[4 * c + 3] = v.w;
+            }
+            settle_survivor<KC>(P, F, T, fl, x, bp, binc, lane & (kCopies - 1), cn, nullptr);
+        }
+        bcnt = 0;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();   // staged rows consumed before the next batch is staged
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+
+    int queued = 0;   // wave-uniform
+    auto tile_body = [&](uint4& s, int64_t base) __attribute__((always_inline)) {
+        const uint32_t ws[4] = {s.x, s.y, s.z, s.w};
+        prefetch(s, base + 2 * kIncTile);
+        const int64_t p0 = base + 256 * w + 4 * lane;
+        int pos = queued;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const bool valid = p0 + e < hi;
+            const int a = state_cluster(ws[e]);
+            const bool surv = valid && (!fl.prune || !(state_bound(ws[e], T.dup) <= T.s[a]));
+            if (valid && !surv) cn.c1 += 1;   // Clause 1: nothing to read or write
+            const uint64_t bm = __ballot(surv);
+            if (surv) {
+                const int e_pos = pos + __popcll(bm & lt);
+                wq_p[e_pos] = (int)(p0 + e);
+                wq_a[e_pos] = a;
+            }
+            pos += __popcll(bm);
+        }
+        queued = pos;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();   // queue entries visible to the whole wave
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        while (queued >= 64) {   // full batches: the newest 64 entries
+            if (bcnt > 0) scan_batch();
+            queued -= 64;
+            take_batch(queued, 64);
+        }
+    };
+    for (int64_t base = lo; base < hi; base += 2 * kIncTile) {
+        tile_body(sA, base);
+        if (base + kIncTile < hi) tile_body(sB, base + kIncTile);
     }
-    if (tid < kNumStat && bst[tid]) atomicAdd(row + k * D + k + tid, (unsigned long long)bst[tid]);
-    (void)my_iq;
+    if (bcnt > 0) scan_batch();
+    if (queued > 0) {
+        take_batch(0, queued);
+        scan_batch();
+    }
+    flush_block(P, F, T, cn, true);
 }
 
 // ---------------------------------------------------------------------------
 // End of a step (one block): totals of the accumulation rows (which it
-// clears), new centroids, drift, stop test, centroid table for the next step.
+// clears), new centroids, drift and cumulative drift, stop test, centroid
+// table for the next step.
 
 __global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F, int delta) {
     constexpr int nt = kFinishThreads;
@@ -774,7 +736,16 @@ __global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F,
             const double cv = (double)(float)cn[jc * d + m];
             c2 = fma(cv, cv, c2);
         }
-        P.f[jc] = f32_up(sqrt(a) * (1.0 + 0x1p-40));
+        // Drift f(c) and its cumulative sums, with margins far above the
+        // float64 rounding of the drift and of the running sums.
+        const double fd = sqrt(a);
+        P.f[jc] = f32_up(fd * (1.0 + 0x1p-40));
+        const double hi = (F.dhi[jc] + fd * (1.0 + 0x1p-40)) * (1.0 + 0x1p-50);
+        const double lo = (F.dlo[jc] + fd * (1.0 - 0x1p-40)) * (1.0 - 0x1p-50);
+        F.dhi[jc] = hi;
+        F.dlo[jc] = lo;
+        F.dup[jc] = f32_up(hi);
+        F.ddn[jc] = f32_down(lo);
         const float e = f32_up(sqrt(b) * (1.0 + 0x1p-40));
         P.ec[jc] = e;
         ecn[jc] = e;
@@ -834,57 +805,77 @@ __global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F,
     }
 }
 
+// Assignments from the point states.
+__global__ __launch_bounds__(256) void k_small_unpack(const uint32_t* __restrict__ w, int64_t n,
+                                                      int32_t* __restrict__ a) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        a[i] = (int32_t)(w[i] & 15u);
+}
+
 // ---------------------------------------------------------------------------
 // Host-side launchers and configuration.
 
 bool small_applies(int64_t n, int d, int k, bool aligned) {
-    return aligned && d == 16 && k <= kSmallMaxK && n <= INT_MAX;   // int32 point indices in the ring
+    return aligned && d == 16 && k <= kSmallMaxK && n <= INT_MAX;   // int32 point indices in the queues
 }
 
-int small_group(int k) { return k <= 4 ? 4 : (k <= 8 ? 8 : 16); }
+// Distance slots of the survivor scan for k centroids.
+int small_kc(int k) { return k <= 4 ? 4 : (k <= 8 ? 8 : (k <= 12 ? 12 : 16)); }
 
 const void* small_kernel_symbol(int k) {
-    switch (small_group(k)) {
-        case 4: return reinterpret_cast<const void*>(&k_small<16, 4>);
-        case 8: return reinterpret_cast<const void*>(&k_small<16, 8>);
-        default: return reinterpret_cast<const void*>(&k_small<16, 16>);
+    switch (small_kc(k)) {
+        case 4: return reinterpret_cast<const void*>(&k_small<4>);
+        case 8: return reinterpret_cast<const void*>(&k_small<8>);
+        case 12: return reinterpret_cast<const void*>(&k_small<12>);
+        default: return reinterpret_cast<const void*>(&k_small<16>);
     }
 }
 
 const void* inc_kernel_symbol(int k) {
-    switch (small_group(k)) {
-        case 4: return reinterpret_cast<const void*>(&k_inc<16, 4>);
-        case 8: return reinterpret_cast<const void*>(&k_inc<16, 8>);
-        default: return reinterpret_cast<const void*>(&k_inc<16, 16>);
+    switch (small_kc(k)) {
+        case 4: return reinterpret_cast<const void*>(&k_inc<4>);
+        case 8: return reinterpret_cast<const void*>(&k_inc<8>);
+        case 12: return reinterpret_cast<const void*>(&k_inc<12>);
+        default: return reinterpret_cast<const void*>(&k_inc<16>);
     }
 }
 
-int small_lds_bytes(int k) { return small_lds(k).bytes; }
+int small_lds_bytes(int k) { return small_lds(k, true).bytes; }
 
-int inc_lds_bytes(int k) { return inc_lds(k).bytes; }
+int inc_lds_bytes(int k) { return small_lds(k, false).bytes; }
 
 int small_finish_lds_bytes(int k) { return finish_lds(16, k); }
 
 hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, hipStream_t s) {
-    switch (small_group(dv.k)) {
-        case 4: hipLaunchKernelGGL((k_small<16, 4>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
-        case 8: hipLaunchKernelGGL((k_small<16, 8>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
-        default: hipLaunchKernelGGL((k_small<16, 16>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
+    switch (small_kc(dv.k)) {
+        case 4: hipLaunchKernelGGL((k_small<4>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
+        case 8: hipLaunchKernelGGL((k_small<8>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
+        case 12: hipLaunchKernelGGL((k_small<12>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
+        default: hipLaunchKernelGGL((k_small<16>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, hipStream_t s) {
-    switch (small_group(dv.k)) {
-        case 4: hipLaunchKernelGGL((k_inc<16, 4>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
-        case 8: hipLaunchKernelGGL((k_inc<16, 8>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
-        default: hipLaunchKernelGGL((k_inc<16, 16>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
+    switch (small_kc(dv.k)) {
+        case 4: hipLaunchKernelGGL((k_inc<4>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
+        case 8: hipLaunchKernelGGL((k_inc<8>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
+        case 12: hipLaunchKernelGGL((k_inc<12>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
+        default: hipLaunchKernelGGL((k_inc<16>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, hipStream_t s) {
     hipLaunchKernelGGL(k_small_finish, dim3(1), dim3(kFinishThreads), finish_lds(dv.d, dv.k), s, dv, F, delta);
+    return hipGetLastError();
+}
+
+hipError_t launch_small_unpack(const Fused& F, int64_t n, int32_t* assign_out, hipStream_t s) {
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(k_small_unpack, dim3((unsigned)blocks), dim3(256), 0, s, F.w, n, assign_out);
     return hipGetLastError();
 }
 
