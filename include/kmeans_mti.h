@@ -165,13 +165,14 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
 
 /*
  * Name of the kernel path the context uses, a static string: "stream-d16"
- * (d = 16, k <= 16: streaming kernel k_small in the first step, incremental
- * kernel k_inc after it, each followed by the one-block finish
- * k_small_finish), "stream-d16-full" (the same with KM_FLAG_FULL_SUMS or
- * KM_FLAG_STATS: k_small every step), "lds-vector" / "lds-mfma" (centroids and sums in LDS:
- * k_assign with vector or matrix-core survivors, then k_reduce, k_update,
- * k_centroid_table), "global-mfma" (centroids or sums too large for LDS:
- * dense MFMA survivors, sums by counting sort).  "" for a NULL context.
+ * (d = 16, k <= 16: the streaming kernel k_small in the first step and the
+ * incremental kernel k_inc after it, each followed by the one-block update
+ * k_small_finish), "stream-d16-full" (the same with
+ * KM_FLAG_FULL_SUMS or KM_FLAG_STATS: k_small every step), "lds-vector" /
+ * "lds-mfma" (centroids and sums in LDS: k_assign with vector or matrix-core
+ * survivors, then k_reduce, k_update, k_centroid_table), "global-mfma"
+ * (centroids or sums too large for LDS: dense MFMA survivors, sums by
+ * counting sort).  "" for a NULL context.
  */
 const char* kmeans_mti_path(const km_ctx* ctx);
 

@@ -242,11 +242,12 @@ int inc_lds_bytes(int k);
 int small_finish_lds_bytes(int k);
 hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, hipStream_t s);
 hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, hipStream_t s);
+// End of a step (one block).  delta: the rows hold the moves of one
+// incremental step (added to F.sum), else the full sums of a streaming step
+// (they replace F.sum).
+hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, hipStream_t s);
 // assign_out[i] = cluster of point i from the point states.
 hipError_t launch_small_unpack(const Fused& F, int64_t n, int32_t* assign_out, hipStream_t s);
-// delta: the rows hold the moves of one incremental step (added to F.sum),
-// else the full sums of a streaming step (replace F.sum).
-hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, hipStream_t s);
 
 // Global-memory path launchers (km_large.hip).  gb: blocks of the bound pass.
 hipError_t launch_large_assign(const Dev& dv, const Large& lg, int gb, hipStream_t s);

@@ -35,10 +35,10 @@
 //
 // The block's sums are integers, so their order does not matter; each block
 // adds its row into one of kSmallRows accumulation rows with device atomics.
-// k_small_finish (one block) adds those rows, forms the new centroids (member
-// means; an empty cluster keeps its centroid), the drift, the cumulative
-// drift, the stop test and the centroid table h, s(c) for the next step
-// (sections III-C and IV-A), and clears the rows.
+// k_small_finish (one block) then adds those rows, forms the new centroids
+// (member means; an empty cluster keeps its centroid), the drift, the
+// cumulative drift, the stop test and the centroid table h, s(c) for the next
+// step (sections III-C and IV-A), and clears the rows.
 #include <float.h>
 #include <limits.h>
 #include <math.h>
@@ -55,7 +55,6 @@ namespace {
 
 constexpr int kTp = kSmallTile;       // threads per block
 constexpr int kCopies = kSmallCopies;
-constexpr int kFinishThreads = 256;   // threads of the finishing block
 constexpr int kD = 16;                // dimension of this path
 constexpr int kQD = kD / 4;           // 16-byte chunks per row
 constexpr int kCR = kSmallRowStride;  // padded LDS row stride (floats)
@@ -235,7 +234,7 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
     float Db, ub, D2 = INFINITY;
     uint64_t nc = 1;
     if (inc >= 0) {
-        float hrow[KC];
+        float hrow[(KC + 3) / 4 * 4];
 #pragma unroll
         for (int j = 0; j < KC; j += 4) {
             const f32x4 v = *reinterpret_cast<const f32x4*>(T.h + inc * kSmallMaxK + j);
@@ -555,6 +554,17 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
 
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
     const StepFlags fl{false, !(P.flags & KM_FLAG_NO_PRUNE), false, P.gamma, st->ec_max};
+    const int64_t n = P.n;
+    const int64_t lo = (int64_t)blockIdx.x * F.span;
+    const int64_t hi = min(n, lo + F.span);
+    const uint4* W4 = reinterpret_cast<const uint4*>(F.w);
+    uint4 sA = {0, 0, 0, 0}, sB = {0, 0, 0, 0};
+    auto prefetch = [&](uint4& s, int64_t base) __attribute__((always_inline)) {
+        if (base < hi) s = W4[(base + 256 * w) / 4 + lane];   // the state array is padded past n
+    };
+    prefetch(sA, lo);   // the first states load while the tables are staged
+    prefetch(sB, lo + kIncTile);
+
     const SmallLds lay = small_lds(P.k, false);
     const Tables T = load_tables(P, F, lay);
     int* wq_p = reinterpret_cast<int*>(km_smem + lay.off_qp) + w * kIncWaveQ;   // this wave's queue
@@ -563,20 +573,9 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     __syncthreads();
 
     Counters cn;
-    const int64_t n = P.n;
-    const int64_t lo = (int64_t)blockIdx.x * F.span;
-    const int64_t hi = min(n, lo + F.span);
     const uint64_t lt = (1ull << lane) - 1ull;
-    const uint4* W4 = reinterpret_cast<const uint4*>(F.w);
     const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
     const int rho0 = lane >> 2, q = lane & 3;
-
-    uint4 sA = {0, 0, 0, 0}, sB = {0, 0, 0, 0};
-    auto prefetch = [&](uint4& s, int64_t base) __attribute__((always_inline)) {
-        if (base < hi) s = W4[(base + 256 * w) / 4 + lane];   // the state array is padded past n
-    };
-    prefetch(sA, lo);
-    prefetch(sB, lo + kIncTile);
 
     // Batches of up to 64 of this wave's survivors, software-pipelined: a
     // batch's rows are requested when it is taken from the queue (16-byte
@@ -663,13 +662,16 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
 }
 
 // ---------------------------------------------------------------------------
-// End of a step (one block): totals of the accumulation rows (which it
-// clears), new centroids, drift and cumulative drift, stop test, centroid
-// table for the next step.
+// End of a step (one block, launched after the step kernel): totals of the
+// accumulation rows (which it clears), new centroids, drift and cumulative
+// drift, stop test, centroid table for the next step.  delta: the rows hold
+// the moves of an incremental step (added to the previous sums), else the full
+// sums of a streaming step (they replace them).
 
-__global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F, int delta) {
-    constexpr int nt = kFinishThreads;
+__global__ __launch_bounds__(kTp) void k_small_finish(Dev P, Fused F, int delta) {
+    constexpr int nt = kTp;
     IterState* st = P.st;
+    if (!st->active) return;   // the step kernel found the run stopped
     const int tid = threadIdx.x;
     const int k = P.k, d = P.d, L = P.L;
     uint64_t* tot = reinterpret_cast<uint64_t*>(km_smem);
@@ -685,8 +687,6 @@ __global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F,
         const int e = tid + q * nt;
         cold[q] = e < k * d ? P.C64[e] : 0.0;
     }
-    // (Issued before the state flag is known: the loads are in bounds either way.)
-    const bool active = st->active != 0;
     for (int col = tid; col < L; col += nt) {
         uint64_t t[kSmallRows];
 #pragma unroll
@@ -694,17 +694,14 @@ __global__ __launch_bounds__(kFinishThreads) void k_small_finish(Dev P, Fused F,
         uint64_t v = 0;
 #pragma unroll
         for (int r = 0; r < kSmallRows; ++r) v += t[r];
-        if (col < k * d + k) {   // sums and counts: after the moves, or the full sums
+        if (col < k * d + k) {   // sums and counts: after the moves (delta), or the full sums
             if (delta) v += F.sum[col];
-            if (active) F.sum[col] = v;
+            F.sum[col] = v;
         }
         tot[col] = v;
-        if (active) {
 #pragma unroll
-            for (int r = 0; r < kSmallRows; ++r) F.rows[(int64_t)r * L + col] = 0;
-        }
+        for (int r = 0; r < kSmallRows; ++r) F.rows[(int64_t)r * L + col] = 0;
     }
-    if (!active) return;
     __syncthreads();
     // New centroids: member means of the exact sums; empty clusters keep theirs.
 #pragma unroll
@@ -820,24 +817,28 @@ bool small_applies(int64_t n, int d, int k, bool aligned) {
     return aligned && d == 16 && k <= kSmallMaxK && n <= INT_MAX;   // int32 point indices in the queues
 }
 
-// Distance slots of the survivor scan for k centroids.
-int small_kc(int k) { return k <= 4 ? 4 : (k <= 8 ? 8 : (k <= 12 ? 12 : 16)); }
+// Distance slots of the survivor scan for k centroids: k rounded up to even.
+#define KM_SMALL_KCS(X) X(2) X(4) X(6) X(8) X(10) X(12) X(14) X(16)
+
+static int small_kc(int k) { return (k + 1) / 2 * 2; }
 
 const void* small_kernel_symbol(int k) {
     switch (small_kc(k)) {
-        case 4: return reinterpret_cast<const void*>(&k_small<4>);
-        case 8: return reinterpret_cast<const void*>(&k_small<8>);
-        case 12: return reinterpret_cast<const void*>(&k_small<12>);
-        default: return reinterpret_cast<const void*>(&k_small<16>);
+#define KM_SYM(KC_) \
+    case KC_: return reinterpret_cast<const void*>(&k_small<KC_>);
+        KM_SMALL_KCS(KM_SYM)
+#undef KM_SYM
+        default: return nullptr;
     }
 }
 
 const void* inc_kernel_symbol(int k) {
     switch (small_kc(k)) {
-        case 4: return reinterpret_cast<const void*>(&k_inc<4>);
-        case 8: return reinterpret_cast<const void*>(&k_inc<8>);
-        case 12: return reinterpret_cast<const void*>(&k_inc<12>);
-        default: return reinterpret_cast<const void*>(&k_inc<16>);
+#define KM_SYM(KC_) \
+    case KC_: return reinterpret_cast<const void*>(&k_inc<KC_>);
+        KM_SMALL_KCS(KM_SYM)
+#undef KM_SYM
+        default: return nullptr;
     }
 }
 
@@ -849,26 +850,29 @@ int small_finish_lds_bytes(int k) { return finish_lds(16, k); }
 
 hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, hipStream_t s) {
     switch (small_kc(dv.k)) {
-        case 4: hipLaunchKernelGGL((k_small<4>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
-        case 8: hipLaunchKernelGGL((k_small<8>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
-        case 12: hipLaunchKernelGGL((k_small<12>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
-        default: hipLaunchKernelGGL((k_small<16>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
+#define KM_LAUNCH(KC_)                                                                       \
+    case KC_: hipLaunchKernelGGL((k_small<KC_>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
+        KM_SMALL_KCS(KM_LAUNCH)
+#undef KM_LAUNCH
+        default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, hipStream_t s) {
     switch (small_kc(dv.k)) {
-        case 4: hipLaunchKernelGGL((k_inc<4>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
-        case 8: hipLaunchKernelGGL((k_inc<8>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
-        case 12: hipLaunchKernelGGL((k_inc<12>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
-        default: hipLaunchKernelGGL((k_inc<16>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
+#define KM_LAUNCH(KC_)                                                                     \
+    case KC_: hipLaunchKernelGGL((k_inc<KC_>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
+        KM_SMALL_KCS(KM_LAUNCH)
+#undef KM_LAUNCH
+        default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
+
 hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, hipStream_t s) {
-    hipLaunchKernelGGL(k_small_finish, dim3(1), dim3(kFinishThreads), finish_lds(dv.d, dv.k), s, dv, F, delta);
+    hipLaunchKernelGGL(k_small_finish, dim3(1), dim3(kTp), finish_lds(dv.d, dv.k), s, dv, F, delta);
     return hipGetLastError();
 }
 
