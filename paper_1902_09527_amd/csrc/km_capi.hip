@@ -167,7 +167,8 @@ int enqueue_iteration(km_ctx* c) {
         if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "streaming step kernel"));
         if ((e = mark(1)) != hipSuccess || (e = mark(2)) != hipSuccess)
             return fail_ctx(c, hip_fail(e, "hipEventRecord"));
-        if ((e = km::launch_small_finish(c->dv, c->fz, delta ? 1 : 0, c->stream)) != hipSuccess)
+        if ((e = km::launch_small_finish(c->dv, c->fz, delta ? 1 : 0, delta ? c->gi : c->dv.G, c->stream)) !=
+            hipSuccess)
             return fail_ctx(c, hip_fail(e, "streaming step finish kernel"));
         ++c->enq;
         if ((e = mark(3)) != hipSuccess || (e = mark(4)) != hipSuccess)
@@ -249,13 +250,12 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             int per_cu_i = 0;
             KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_i, isym, c->tp, c->lds_inc));
             if (per_cu_i < 1) return KM_ERR_UNSUPPORTED;
-            // Contiguous ranges of tpb tiles per block, no block without a tile.
-            const int64_t nti = (n + km::kIncTile - 1) / km::kIncTile;
+            // Resident blocks (the same count on every CU), at least one wave
+            // tile per wave.
+            const int64_t nwt = (n + km::kIncWaveTile - 1) / km::kIncWaveTile;
             int64_t gi = (int64_t)per_cu_i * cus;
-            if (gi > nti) gi = nti;
-            const int64_t tpb = (nti + gi - 1) / gi;
-            c->gi = (int)((nti + tpb - 1) / tpb);
-            c->fz.span = tpb * km::kIncTile;
+            if (gi > nwt / 4) gi = nwt / 4 > 0 ? nwt / 4 : 1;
+            c->gi = (int)gi;
         }
     } else if (!(c->flags & KM_FLAG_LARGE_PATH)) {
         c->variant = km::assign_variant(d, k, aligned, (c->flags & KM_FLAG_VECTOR_ONLY) != 0);
@@ -331,7 +331,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         if ((rc = c->alloc(&c->fz.rows, (size_t)km::kSmallRows * v.L)) ||
             (rc = c->alloc(&c->fz.sum, (size_t)k * d + k)) || (rc = c->alloc(&c->fz.w, nw)) ||
             (rc = c->alloc(&c->fz.dhi, (size_t)k)) || (rc = c->alloc(&c->fz.dlo, (size_t)k)) ||
-            (rc = c->alloc(&c->fz.dup, (size_t)k)) || (rc = c->alloc(&c->fz.ddn, (size_t)k)))
+            (rc = c->alloc(&c->fz.dup, (size_t)k)) || (rc = c->alloc(&c->fz.ddn, (size_t)k)) ||
+            (rc = c->alloc(&c->fz.bcnt, (size_t)km::kNumStat * (v.G > c->gi ? v.G : c->gi))))
             return rc;
         KM_HIP(hipMemsetAsync(c->fz.rows, 0, sizeof(uint64_t) * (size_t)km::kSmallRows * v.L, c->stream));
         KM_HIP(hipMemsetAsync(c->fz.w, 0, sizeof(uint32_t) * nw, c->stream));

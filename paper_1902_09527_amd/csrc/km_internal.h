@@ -161,19 +161,21 @@ constexpr int kSmallRowStride = 20;   // padded LDS row stride (floats) of centr
 // them.
 constexpr int kSmallRows = 16;
 
-// Incremental kernel: each block owns a contiguous range of tiles of
-// kIncTile points; wave w of a block takes points 256w .. 256w+255 of each
-// tile (four per lane, one 16-byte state load).
-constexpr int kIncTile = 1024;
+// Incremental kernel: each block owns an equal share of the tiles of
+// kIncWaveTile points, which its waves take one at a time (16 points per lane,
+// four 16-byte state loads issued together), in four sub-tiles of 256.  The
+// state array is padded to whole kIncTile.
+constexpr int kIncWaveTile = 1024;
+constexpr int kIncTile = 4 * kIncWaveTile;
 
 // Survivor queues in LDS.  A batch of kSmallTile survivors is scanned as soon
 // as that many are queued, so a queue holds at most kSmallTile - 1 plus one
 // tile's points.
 constexpr int kSmallQ = 2 * kSmallTile;          // streaming kernel: rows staged with the entries
 // Incremental kernel: one queue per wave (point index and cluster); a wave
-// scans a batch of 64 as soon as that many are queued, and one wave tile
-// adds at most 256.
-constexpr int kIncWaveQ = 64 + kIncTile / 4;
+// takes a batch of 64 as soon as that many are queued, and one sub-tile adds
+// at most 256.
+constexpr int kIncWaveQ = 64 + 256;
 constexpr int kIncQ = 4 * kIncWaveQ;
 
 // Point state of the streaming path: one 32-bit word per point.  Bits 3..0
@@ -190,7 +192,7 @@ struct Fused {
     double* dlo;          // k: the same rounded down
     float* dup;           // k: dhi rounded up to float32
     float* ddn;           // k: dlo rounded down to float32
-    int64_t span;         // points per block of the incremental kernel (multiple of kIncTile)
+    uint64_t* bcnt;       // per-block counters of the step kernel: blocks x kNumStat
 };
 
 struct SmallLds {
@@ -244,8 +246,8 @@ hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, hipStream_
 hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, hipStream_t s);
 // End of a step (one block).  delta: the rows hold the moves of one
 // incremental step (added to F.sum), else the full sums of a streaming step
-// (they replace F.sum).
-hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, hipStream_t s);
+// (they replace F.sum).  nb: blocks of the step kernel (counter slots).
+hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, int nb, hipStream_t s);
 // assign_out[i] = cluster of point i from the point states.
 hipError_t launch_small_unpack(const Fused& F, int64_t n, int32_t* assign_out, hipStream_t s);
 

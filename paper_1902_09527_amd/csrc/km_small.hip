@@ -77,6 +77,17 @@ __device__ __forceinline__ uint32_t settle_state(float ub, float ddn_b, int b) {
     return pack_state(r + fabsf(r) * 0x1p-22f, b);
 }
 
+// Upper bound on sqrt(v): the hardware square root (within a few units in
+// the last place) scaled up by 2^-20.
+__device__ __forceinline__ float sqrt_up(float v) { return __builtin_amdgcn_sqrtf(v) * (1.0f + 0x1p-20f); }
+
+// Upper bound on the exact distance to the float64 centroid from a float32
+// squared distance D (relative error <= gamma) and the centroid's float32
+// rounding error ec.
+__device__ __forceinline__ float bound_of(float D, float ec, float gamma) {
+    return (sqrt_up(D) * (1.0f + gamma) + ec) * kUp;
+}
+
 // Drift-updated bound of a state word (cumulative drift rounded up).
 __device__ __forceinline__ float state_bound(uint32_t w, const float* dup) {
     return (state_value(w) + dup[state_cluster(w)]) * kUp;
@@ -246,7 +257,7 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
         Db = INFINITY;
 #pragma unroll
         for (int j = 0; j < KC; ++j) Db = j == inc ? Dall[j] : Db;
-        const float u = upper_bound(Db, T.ec[inc], fl.gamma);
+        const float u = bound_of(Db, T.ec[inc], fl.gamma);
         b = inc;
 #pragma unroll
         for (int j = 0; j < KC; ++j) {
@@ -257,14 +268,14 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
                 Db = Dall[j];
                 b = j;
             } else {
-                D2 = fminf(D2, Dall[j]);
+                D2 = Dall[j] < D2 ? Dall[j] : D2;
             }
         }
-        ub = b == inc ? u : upper_bound(Db, T.ec[b], fl.gamma);
+        ub = b == inc ? u : bound_of(Db, T.ec[b], fl.gamma);
     } else {
         b = 0;
         Db = Dall[0];
-        ub = upper_bound(Db, T.ec[0], fl.gamma);
+        ub = bound_of(Db, T.ec[0], fl.gamma);
 #pragma unroll
         for (int j = 1; j < KC; ++j) {
             if (j >= k || (fl.prune && ub <= T.h[b * kSmallMaxK + j])) continue;
@@ -273,14 +284,14 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
                 D2 = Db;
                 Db = Dall[j];
                 b = j;
-                ub = upper_bound(Db, T.ec[j], fl.gamma);
+                ub = bound_of(Db, T.ec[j], fl.gamma);
             } else {
-                D2 = fminf(D2, Dall[j]);
+                D2 = Dall[j] < D2 ? Dall[j] : D2;
             }
         }
     }
     if (D2 != INFINITY) {
-        const float band = 2.f * fl.gamma * (Db + D2) + 4.f * (sqrtf(Db) + sqrtf(D2)) * fl.ecmax +
+        const float band = 2.f * fl.gamma * (Db + D2) + 4.f * (sqrt_up(Db) + sqrt_up(D2)) * fl.ecmax +
                            8.f * fl.ecmax * fl.ecmax;
         if (D2 - Db <= band) {   // near tie: float64 decision, the oracle's tie rule
             b = recheck64(x, P.C64, k, inc, Db, ub);
@@ -301,8 +312,9 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
     }
 }
 
-// Block counters, then the block's sums (copies added) into accumulation
-// row blockIdx % kSmallRows.  skip_zero: only nonzero words are added.
+// Block counters into the block's counter slot, then the block's sums (copies
+// added) into accumulation row blockIdx % kSmallRows.  skip_zero: only nonzero
+// words are added.
 __device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const Tables& T, Counters& cn,
                                    bool skip_zero) {
     const int k = P.k, tid = threadIdx.x, lane = tid & 63;
@@ -333,8 +345,7 @@ __device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const 
         // A count change is a 32-bit two's-complement value (moves may be negative).
         if (v || !skip_zero) atomicAdd(row + k * kD + i, (unsigned long long)(int64_t)(int32_t)v);
     }
-    if (tid < kNumStat && (T.bst[tid] || !skip_zero))
-        atomicAdd(row + k * kD + k + tid, (unsigned long long)T.bst[tid]);
+    if (tid < kNumStat) F.bcnt[(int64_t)blockIdx.x * kNumStat + tid] = T.bst[tid];   // the block's own slot
 }
 
 }  // namespace
@@ -534,9 +545,11 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
 }
 
 // ---------------------------------------------------------------------------
-// The incremental kernel (steps after the first).  Block b owns the points
-// [b * span, min(n, (b + 1) * span)) in tiles of kIncTile; wave w takes points
-// 256w .. 256w+255 of each tile, four per lane, two tiles in flight.  The
+// The incremental kernel (steps after the first).  Block b owns an equal
+// share of the tiles of kIncWaveTile points; its waves take them one at a time
+// from an LDS counter until none is left (the GPU form of the paper's work
+// stealing against pruning skew), 16 points per lane loaded together, in four
+// sub-tiles of four per lane.  The
 // waves of a block run independently (no block barrier before the end): each
 // queues its Clause-1 survivors in its own LDS queue and, whenever 64 are
 // queued, gathers their rows (16-byte loads, four lanes per row), stages them
@@ -555,18 +568,31 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
     const StepFlags fl{false, !(P.flags & KM_FLAG_NO_PRUNE), false, P.gamma, st->ec_max};
     const int64_t n = P.n;
-    const int64_t lo = (int64_t)blockIdx.x * F.span;
-    const int64_t hi = min(n, lo + F.span);
+    const int nwt = (int)((n + kIncWaveTile - 1) / kIncWaveTile);   // wave tiles
+    // Block b owns wave tiles [b * nwt / G, (b + 1) * nwt / G); its waves take
+    // them one at a time from an LDS counter (work stealing within the block).
+    const int wt_lo = (int)((int64_t)blockIdx.x * nwt / gridDim.x);
+    const int wt_hi = (int)((int64_t)(blockIdx.x + 1) * nwt / gridDim.x);
     const uint4* W4 = reinterpret_cast<const uint4*>(F.w);
-    uint4 sA = {0, 0, 0, 0}, sB = {0, 0, 0, 0};
-    auto prefetch = [&](uint4& s, int64_t base) __attribute__((always_inline)) {
-        if (base < hi) s = W4[(base + 256 * w) / 4 + lane];   // the state array is padded past n
+    // The states of a wave tile: sub-tile c of lane l holds points
+    // base + 256c + 4l .. +3.
+    uint4 sn[4];
+    auto load_states = [&](int wt) __attribute__((always_inline)) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) sn[c] = W4[((int64_t)wt * kIncWaveTile + 256 * c) / 4 + lane];   // padded past n
     };
-    prefetch(sA, lo);   // the first states load while the tables are staged
-    prefetch(sB, lo + kIncTile);
+    int wt = wt_lo + w;   // each wave's first tile
+    if (wt < wt_hi) load_states(wt);   // the first states load while the tables are staged
 
     const SmallLds lay = small_lds(P.k, false);
     const Tables T = load_tables(P, F, lay);
+    // Further tiles: lane 0 takes one from the block's counter (in the queue
+    // counters, which this kernel does not otherwise use).
+    auto grab = [&]() __attribute__((always_inline)) {
+        int t = 0;
+        if (lane == 0) t = wt_lo + 4 + atomicAdd(T.qc, 1);
+        return __shfl(t, 0);
+    };
     int* wq_p = reinterpret_cast<int*>(km_smem + lay.off_qp) + w * kIncWaveQ;   // this wave's queue
     int* wq_a = reinterpret_cast<int*>(km_smem + lay.off_qa) + w * kIncWaveQ;
     float* wg = reinterpret_cast<float*>(km_smem + lay.off_qr) + 64 * w * kCR;  // its staged rows
@@ -620,14 +646,13 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     };
 
     int queued = 0;   // wave-uniform
-    auto tile_body = [&](uint4& s, int64_t base) __attribute__((always_inline)) {
-        const uint32_t ws[4] = {s.x, s.y, s.z, s.w};
-        prefetch(s, base + 2 * kIncTile);
-        const int64_t p0 = base + 256 * w + 4 * lane;
+    auto tile_body = [&](int64_t base, const uint4 s4) __attribute__((always_inline)) {
+        const uint32_t ws[4] = {s4.x, s4.y, s4.z, s4.w};
+        const int64_t p0 = base + 4 * lane;
         int pos = queued;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const bool valid = p0 + e < hi;
+            const bool valid = p0 + e < n;
             const int a = state_cluster(ws[e]);
             const bool surv = valid && (!fl.prune || !(state_bound(ws[e], T.dup) <= T.s[a]));
             if (valid && !surv) cn.c1 += 1;   // Clause 1: nothing to read or write
@@ -643,20 +668,39 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();   // queue entries visible to the whole wave
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        while (queued >= 64) {   // full batches: the newest 64 entries
-            if (bcnt > 0) scan_batch();
-            queued -= 64;
-            take_batch(queued, 64);
-        }
     };
-    for (int64_t base = lo; base < hi; base += 2 * kIncTile) {
-        tile_body(sA, base);
-        if (base + kIncTile < hi) tile_body(sB, base + kIncTile);
-    }
-    if (bcnt > 0) scan_batch();
-    if (queued > 0) {
-        take_batch(0, queued);
-        scan_batch();
+    // Sub-tiles, each followed by the batch point: while a full batch is
+    // queued (at the end: any entry), scan the batch in flight and take the
+    // newest entries as the next one; at the end the last batch is scanned
+    // too.  One call site each keeps the scan code in one copy.  The next
+    // wave tile is taken at the first sub-tile and its states requested at
+    // the last.
+    int sub = 0, wt_next = 0;
+    for (;;) {
+        const bool more = wt < wt_hi;
+        if (more) {
+            const uint4 s4 = sn[0];
+            sn[0] = sn[1];   // the next sub-tile's states move to the front
+            sn[1] = sn[2];
+            sn[2] = sn[3];
+            const int64_t base = (int64_t)wt * kIncWaveTile + 256 * sub;
+            if (sub == 0) wt_next = grab();
+            if (sub == 3) {
+                wt = wt_next;
+                if (wt < wt_hi) load_states(wt);
+            }
+            sub = (sub + 1) & 3;
+            tile_body(base, s4);
+        }
+        for (;;) {
+            const bool take = more ? queued >= 64 : queued > 0;
+            if (bcnt > 0 && (take || !more)) scan_batch();
+            if (!take) break;
+            const int c = queued < 64 ? queued : 64;
+            queued -= c;
+            take_batch(queued, c);
+        }
+        if (!more) break;
     }
     flush_block(P, F, T, cn, true);
 }
@@ -668,7 +712,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
 // the moves of an incremental step (added to the previous sums), else the full
 // sums of a streaming step (they replace them).
 
-__global__ __launch_bounds__(kTp) void k_small_finish(Dev P, Fused F, int delta) {
+__global__ __launch_bounds__(kTp) void k_small_finish(Dev P, Fused F, int delta, int nb) {
     constexpr int nt = kTp;
     IterState* st = P.st;
     if (!st->active) return;   // the step kernel found the run stopped
@@ -701,6 +745,25 @@ __global__ __launch_bounds__(kTp) void k_small_finish(Dev P, Fused F, int delta)
         tot[col] = v;
 #pragma unroll
         for (int r = 0; r < kSmallRows; ++r) F.rows[(int64_t)r * L + col] = 0;
+    }
+    {   // counters: the blocks' slots, summed per wave, then over the waves
+        uint64_t c[kNumStat] = {0, 0, 0, 0, 0};
+        for (int b = tid; b < nb; b += nt)
+#pragma unroll
+            for (int q = 0; q < kNumStat; ++q) c[q] += F.bcnt[(int64_t)b * kNumStat + q];
+        __syncthreads();   // tot is complete; its counter words are rebuilt below
+        uint64_t* red = tot + L;   // scratch before the centroid arrays are written
+#pragma unroll
+        for (int q = 0; q < kNumStat; ++q) {
+            const uint64_t v = wave_sum_u64(c[q]);
+            if ((tid & 63) == 0) red[(tid >> 6) * kNumStat + q] = v;
+        }
+        __syncthreads();
+        if (tid < kNumStat) {
+            uint64_t v = 0;
+            for (int wv = 0; wv < nt / 64; ++wv) v += red[wv * kNumStat + tid];
+            tot[k * d + k + tid] = v;
+        }
     }
     __syncthreads();
     // New centroids: member means of the exact sums; empty clusters keep theirs.
@@ -871,8 +934,8 @@ hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, hi
 }
 
 
-hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, hipStream_t s) {
-    hipLaunchKernelGGL(k_small_finish, dim3(1), dim3(kTp), finish_lds(dv.d, dv.k), s, dv, F, delta);
+hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, int nb, hipStream_t s) {
+    hipLaunchKernelGGL(k_small_finish, dim3(1), dim3(kTp), finish_lds(dv.d, dv.k), s, dv, F, delta, nb);
     return hipGetLastError();
 }
 
