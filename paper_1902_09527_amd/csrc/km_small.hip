@@ -13,7 +13,8 @@
 // k_small streams every row of X (persistent blocks, 256-point tiles, two
 // tiles in flight per block).  Per tile it
 //   1. applies Clause 1 to each point's drift-updated bound: u <= s(c_a) with
-//      s(c) half the distance to the nearest other centroid (Elkan's lemma);
+//      s(c) half the distance to the nearest other centroid (Elkan's lemma),
+//      tested as v <= s(c_a) - D_a with the right side computed per cluster;
 //   2. adds every row, from registers, to the fixed-point sums of its
 //      PREVIOUS cluster (all points contribute, the sums are Lloyd's);
 //   3. queues the Clause-1 survivors, rows included, in LDS.
@@ -88,10 +89,6 @@ __device__ __forceinline__ float bound_of(float D, float ec, float gamma) {
     return (sqrt_up(D) * (1.0f + gamma) + ec) * kUp;
 }
 
-// Drift-updated bound of a state word (cumulative drift rounded up).
-__device__ __forceinline__ float state_bound(uint32_t w, const float* dup) {
-    return (state_value(w) + dup[state_cluster(w)]) * kUp;
-}
 
 // Squared float32 distance, coordinates in order (the same rounding as the
 // other kernels of the library).
@@ -167,9 +164,8 @@ __device__ __forceinline__ void add_row(uint64_t* dst, const float (&x)[kD], dou
 struct Tables {
     float* C;      // k rows of kCR floats: float32 centroids
     float* h;      // k rows of kSmallMaxK: half centroid distances, rounded down
-    float* s;      // k: s(c) = min over other centroids of h, rounded down
+    float* thr;    // k: Clause-1 threshold on a state value (below)
     float* ec;     // k: float32 rounding error of each centroid, rounded up
-    float* dup;    // k: cumulative drift, rounded up
     float* ddn;    // k: cumulative drift, rounded down
     uint64_t* acc; // kCopies copies (stride csu) of the k x 16 fixed-point sums
     uint32_t* cnt; // kCopies copies of the k counts (stride kp)
@@ -182,9 +178,8 @@ __device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, cons
     Tables T;
     T.C = reinterpret_cast<float*>(km_smem + lay.off_c);
     T.h = reinterpret_cast<float*>(km_smem + lay.off_h);
-    T.s = reinterpret_cast<float*>(km_smem + lay.off_s);
+    T.thr = reinterpret_cast<float*>(km_smem + lay.off_s);
     T.ec = reinterpret_cast<float*>(km_smem + lay.off_ec);
-    T.dup = reinterpret_cast<float*>(km_smem + lay.off_du);
     T.ddn = reinterpret_cast<float*>(km_smem + lay.off_dd);
     T.acc = reinterpret_cast<uint64_t*>(km_smem + lay.off_acc);
     T.cnt = reinterpret_cast<uint32_t*>(km_smem + lay.off_cnt);
@@ -196,9 +191,12 @@ __device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, cons
     for (int i = tid; i < k * kD; i += kTp) T.C[(i / kD) * kCR + i % kD] = P.C32[i];
     for (int i = tid; i < k * k; i += kTp) T.h[(i / k) * kSmallMaxK + i % k] = P.h[i];
     for (int i = tid; i < k; i += kTp) {
-        T.s[i] = P.s[i];
+        // Clause 1 holds when v + D_a <= s(a) (D_a the cumulative drift
+        // rounded up, s(a) rounded down): thr is the largest float with
+        // thr + D_a <= s(a), so that the test is v <= thr.
+        const double x = (double)P.s[i] - F.dhi[i];   // +inf when k = 1
+        T.thr[i] = isinf(x) ? (float)x : f32_down(x - fabs(x) * 0x1p-50);
         T.ec[i] = P.ec[i];
-        T.dup[i] = F.dup[i];
         T.ddn[i] = F.ddn[i];
     }
     for (int i = tid; i < kCopies * T.csu; i += kTp) T.acc[i] = 0;
@@ -452,7 +450,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
         bool surv = valid;
         if (valid && !fl.first) {
             a_old = state_cluster(ws);
-            surv = !fl.prune || !(state_bound(ws, T.dup) <= T.s[a_old]);
+            surv = !fl.prune || !(state_value(ws) <= T.thr[a_old]);
             if (!surv) cn.c1 += 1;
         }
 
@@ -646,24 +644,26 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     };
 
     int queued = 0;   // wave-uniform
-    auto tile_body = [&](int64_t base, const uint4 s4) __attribute__((always_inline)) {
+    auto tile_body = [&](int base, const uint4 s4) __attribute__((always_inline)) {
         const uint32_t ws[4] = {s4.x, s4.y, s4.z, s4.w};
-        const int64_t p0 = base + 4 * lane;
-        int pos = queued;
+        const int p0 = base + 4 * lane;
+        const bool full = (int64_t)base + 256 <= n;   // no point past n in this sub-tile
+        int pos = queued, c1 = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const bool valid = p0 + e < n;
+            const bool valid = full || (int64_t)(p0 + e) < n;
             const int a = state_cluster(ws[e]);
-            const bool surv = valid && (!fl.prune || !(state_bound(ws[e], T.dup) <= T.s[a]));
-            if (valid && !surv) cn.c1 += 1;   // Clause 1: nothing to read or write
+            const bool surv = valid && (!fl.prune || !(state_value(ws[e]) <= T.thr[a]));
+            c1 += valid && !surv ? 1 : 0;   // Clause 1: nothing to read or write
             const uint64_t bm = __ballot(surv);
             if (surv) {
                 const int e_pos = pos + __popcll(bm & lt);
-                wq_p[e_pos] = (int)(p0 + e);
+                wq_p[e_pos] = p0 + e;
                 wq_a[e_pos] = a;
             }
             pos += __popcll(bm);
         }
+        cn.c1 += (uint64_t)c1;
         queued = pos;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();   // queue entries visible to the whole wave
@@ -683,7 +683,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
             sn[0] = sn[1];   // the next sub-tile's states move to the front
             sn[1] = sn[2];
             sn[2] = sn[3];
-            const int64_t base = (int64_t)wt * kIncWaveTile + 256 * sub;
+            const int base = wt * kIncWaveTile + 256 * sub;
             if (sub == 0) wt_next = grab();
             if (sub == 3) {
                 wt = wt_next;
@@ -877,7 +877,8 @@ __global__ __launch_bounds__(256) void k_small_unpack(const uint32_t* __restrict
 // Host-side launchers and configuration.
 
 bool small_applies(int64_t n, int d, int k, bool aligned) {
-    return aligned && d == 16 && k <= kSmallMaxK && n <= INT_MAX;   // int32 point indices in the queues
+    // int32 point indices, also over the state array's padding
+    return aligned && d == 16 && k <= kSmallMaxK && n <= (int64_t)INT_MAX - kIncTile;
 }
 
 // Distance slots of the survivor scan for k centroids: k rounded up to even.
