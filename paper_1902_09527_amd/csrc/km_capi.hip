@@ -283,8 +283,7 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     } else {
         c->large = true;
         km::Large& L = c->lg;
-        L.dp = (d + 31) / 32 * 32;
-        const int mlds = km::large_mfma_lds(L.dp);
+        const int mlds = km::large_mfma_lds();
         if (d > km::kLgMaxD || mlds > max_lds || 4 * k > max_lds || km::large_table_lds(d) > max_lds) {
             snprintf(g_last_hip, sizeof g_last_hip,
                      "k = %d, d = %d: no kernel path (d <= %d and k <= %d needed)", k, d, km::kLgMaxD,
@@ -292,7 +291,7 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             return KM_ERR_UNSUPPORTED;
         }
         const void* sym = km::large_mfma_symbol();
-        KM_HIP(km::large_set_attributes(k, d, L.dp));
+        KM_HIP(km::large_set_attributes(k, d));
         int per_cu = 0;
         KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, 256, mlds));
         if (per_cu < 1) return KM_ERR_UNSUPPORTED;

@@ -74,10 +74,13 @@ inline int row_len(int d, int k) { return k * d + k + kNumStat; }
 // Global-memory path (centroids or per-cluster sums too large for LDS): dense
 // matrix-core distances for the Clause-1 survivors, then per-cluster sums
 // through a counting sort of the points by cluster.
-constexpr int kLgSurvTile = 64;    // survivors per workgroup tile
-constexpr int kLgCentTile = 128;   // centroids per workgroup tile (32 per wave)
-constexpr int kLgChunkRows = 256;  // rows per segment-sum chunk
-constexpr int kLgMaxD = 320;       // largest d of the global-memory path (LDS-resident survivor tile)
+constexpr int kLgM = 128;            // survivors per block tile (matrix-core columns)
+constexpr int kLgN = 128;            // centroids per block tile (matrix-core rows)
+constexpr int kLgK = 16;             // dimensions per streamed chunk
+constexpr int kLgAS = kLgN + 32;     // LDS stride (floats) of one dimension of a centroid chunk
+constexpr int kLgBS = kLgM + 32;     // LDS stride (floats) of one dimension of a survivor chunk
+constexpr int kLgChunkRows = 256;    // rows per segment-sum chunk
+constexpr int kLgMaxD = 4096;        // largest d of the global-memory path
 
 struct Large {
     int32_t* surv;        // n: survivor point indices of the current step
@@ -93,15 +96,15 @@ struct Large {
     int32_t NCmax;        // n / kLgChunkRows + k
     int64_t span;         // points per histogram / scatter block (contiguous)
     int32_t Gm;           // resident blocks of the matrix-core kernel
-    int32_t dp;           // d rounded up to 32
 };
 
-// LDS bytes of the global-memory matrix-core kernel.
-__host__ __device__ inline int large_mfma_lds(int dp) {
-    return 4 * dp * (kLgSurvTile + 1)              // survivor tile, dimension-major
-           + 2 * 4 * 32 * (kLgCentTile + 1)        // centroid chunk, double buffered
-           + 8 * kLgSurvTile * 4 * 2 * 4           // candidate lists for the merge
-           + 4 * kLgSurvTile + 64;
+// LDS bytes of the global-memory matrix-core kernel: the double-buffered
+// chunks (reused for the candidate lists after the last chunk), the
+// survivors' squared norms and a few reduction words.
+__host__ __device__ inline int large_mfma_lds() {
+    const int bufs = 2 * kLgK * (kLgAS + kLgBS) * 4;
+    const int cand = kLgM * 16 * 8;
+    return (bufs > cand ? bufs : cand) + 4 * kLgM + 64;
 }
 
 // Padded LDS row stride of the X tile: 16-byte aligned rows, offset by 4
@@ -258,7 +261,7 @@ hipError_t launch_large_table(const Dev& dv, int force, hipStream_t s);
 int large_table_lds(int d);
 const void* large_mfma_symbol();
 // Raises the dynamic-LDS limits of the global-memory path's kernels.
-hipError_t large_set_attributes(int k, int d, int dp);
+hipError_t large_set_attributes(int k, int d);
 
 // Kernel launchers (km_kernels.hip).  Each returns the launch status.
 hipError_t launch_absmax(const float* X, int64_t count, uint32_t* absmax_bits, int32_t* nonfinite,

@@ -5,10 +5,11 @@
 //   k_bound_large       drift-updated bound and Clause 1 (section III-C) for
 //                       every point; survivors compacted into a global list;
 //   k_mfma_large        float32 MFMA distances of the survivors to all
-//                       centroids (dense 64-survivor x 128-centroid tiles,
-//                       expanded form), a top-4 candidate list per survivor,
-//                       direct-form refinement of the candidates within the
-//                       expanded form's error bound, float64 near-tie rule;
+//                       centroids (128-centroid x 128-survivor tiles over
+//                       double-buffered 16-dimension chunks, expanded form), a
+//                       top-4 candidate list per survivor, direct-form
+//                       refinement of the candidates within the expanded
+//                       form's error bound, float64 near-tie rule;
 //   k_hist_large        per-block cluster counts of the new assignment;
 //   k_scan_large_cols,
 //   k_scan_large_clusters  cluster starts and per-block write offsets;
@@ -51,16 +52,6 @@ __device__ inline void top4_insert(float (&L)[4], int (&J)[4], float v, int j) {
     }
 }
 
-__device__ inline float quad_sum(float v) {
-    v += __shfl_xor(v, 1);
-    v += __shfl_xor(v, 2);
-    return v;
-}
-__device__ inline double quad_sum(double v) {
-    v += __shfl_xor(v, 1);
-    v += __shfl_xor(v, 2);
-    return v;
-}
 
 }  // namespace
 
@@ -111,28 +102,36 @@ __global__ __launch_bounds__(256) void k_bound_large(Dev P, Large Lg) {
 }
 
 // ---------------------------------------------------------------------------
-// Dense survivor distances on the matrix cores.  Workgroup tile: 64
-// survivors (two 32-column MFMA blocks) x 128 centroids (32 per wave); the
-// survivor tile stays in LDS dimension-major for all centroid tiles, the
-// centroid tile streams through LDS in 32-dimension chunks (double
-// buffered).  MFMA k-step s pairs chunk dimensions s and 16 + s.
+// Dense survivor distances on the matrix cores, as a tiled product of the
+// centroids (rows) and the survivors (columns) over the dimensions.  Block
+// tile: kLgN = 128 centroids x kLgM = 128 survivors; wave (wr, wc) owns
+// centroid rows 64 wr .. 64 wr + 63 and survivor columns 64 wc .. 64 wc + 63,
+// four 32x32 float32 accumulators.  The dimensions stream in chunks
+// of kLgK through double-buffered LDS (dimension-major); the next chunk's
+// global loads are issued before the current chunk's products.  Each lane
+// keeps, for its two survivor columns, the four smallest expanded-form
+// distances |x|^2 + |c|^2 - 2 x.c with their centroids; the 4 lists of a
+// survivor (2 waves x 2 half-waves) are merged in LDS, and the candidates
+// within the expanded form's error bound of the smallest are re-evaluated in
+// the direct form, followed by the float64 near-tie rule.
 
-__global__ __launch_bounds__(256) void k_mfma_large(Dev P, Large Lg) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_mfma_large(Dev P, Large Lg) {
     IterState* st = P.st;
     if (!st->active) return;
-    const int k = P.k, d = P.d, dp = Lg.dp;
+    const int k = P.k, d = P.d;
     const bool first = st->t == 0;
     const uint32_t ns = *Lg.nsurv;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 31, half = lane >> 5;
-    constexpr int XW = kLgSurvTile + 1;   // padded survivor-tile row (per dimension)
-    constexpr int CW = kLgCentTile + 1;   // padded centroid-chunk row (per dimension)
+    const int wr = wave >> 1, wc = wave & 1;   // the wave's 64-centroid row block and 64-survivor column block
     extern __shared__ __align__(16) unsigned char smem[];
-    float* XT = reinterpret_cast<float*>(smem);             // [dp][XW]
-    float* CT = XT + dp * XW;                                // [2][32][CW]
-    float* candD = CT + 2 * 32 * CW;                         // [64][32]
-    int* candJ = reinterpret_cast<int*>(candD + kLgSurvTile * 32);
-    float* x2s = reinterpret_cast<float*>(candJ + kLgSurvTile * 32);   // [64]
-    float* red = x2s + kLgSurvTile;                          // [16]
+    constexpr int kBufBytes = 2 * kLgK * (kLgAS + kLgBS) * 4;
+    constexpr int kCandBytes = kLgM * 16 * 8;
+    float* Ab = reinterpret_cast<float*>(smem);                    // [2][kLgK][kLgAS]
+    float* Bb = Ab + 2 * kLgK * kLgAS;                             // [2][kLgK][kLgBS]
+    float* candD = reinterpret_cast<float*>(smem);                 // [kLgM][16], after the products
+    int* candJ = reinterpret_cast<int*>(candD + kLgM * 16);
+    float* x2s = reinterpret_cast<float*>(smem + (kBufBytes > kCandBytes ? kBufBytes : kCandBytes));   // [kLgM]
+    float* red = x2s + kLgM;                                       // [4]
 
     const float ecm = st->ec_max;
     const float gamma = P.gamma;
@@ -147,81 +146,162 @@ __global__ __launch_bounds__(256) void k_mfma_large(Dev P, Large Lg) {
     const float cnmax = sqrtf(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))) * kUp;
 
     uint64_t my_changed = 0, my_comp = 0, my_rc = 0;
-    const int ntiles = (int)((ns + kLgSurvTile - 1) / kLgSurvTile);
-    const int nct = (k + kLgCentTile - 1) / kLgCentTile;
-    const int nch = dp / 32;
+    const int ntiles = (int)((ns + kLgM - 1) / kLgM);
+    const int nct = (k + kLgN - 1) / kLgN;
+    const int nch = (d + kLgK - 1) / kLgK;
+    const bool vec = (d & 3) == 0;   // 16-byte row chunks (every chunk start is then aligned)
+    const f32x4* C4 = reinterpret_cast<const f32x4*>(P.C32);
+    const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
+
+    // Chunk loads, two 4-float pieces per thread for each operand: centroid
+    // row n0 + 64i + tid / 4 and survivor 64i + tid / 4, dimensions
+    // 4 (tid % 4) .. +3 of the chunk; zero outside k, the survivors and d.
+    f32x4 ra[2], rb[2];
+    float x2p[2] = {0.f, 0.f};   // partial squared norms of this thread's two survivors (first centroid tile)
+    int srow[2];                 // this thread's two survivors' point indices (-1: none)
+    const int q4 = tid & 3, r4 = tid >> 2;
+    auto load_chunk = [&](int n0, int c) __attribute__((always_inline)) {
+        const int m0 = c * kLgK + 4 * q4;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int j = n0 + 64 * i + r4;
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if (j < k) {
+                if (vec) {
+                    if (m0 < d) v = C4[((int64_t)j * d + m0) >> 2];
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (m0 + e < d) v[e] = P.C32[(int64_t)j * d + m0 + e];
+                }
+            }
+            ra[i] = v;
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            f32x4 v = {0.f, 0.f, 0.f, 0.f};
+            if (srow[i] >= 0) {
+                if (vec) {
+                    if (m0 < d) v = __builtin_nontemporal_load(X4 + (((int64_t)srow[i] * d + m0) >> 2));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (m0 + e < d) v[e] = P.X[(int64_t)srow[i] * d + m0 + e];
+                }
+            }
+            rb[i] = v;
+        }
+    };
+    auto store_chunk = [&](int buf) __attribute__((always_inline)) {
+        float* A = Ab + buf * kLgK * kLgAS;
+        float* B = Bb + buf * kLgK * kLgBS;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) A[(4 * q4 + e) * kLgAS + 64 * i + r4] = ra[i][e];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) B[(4 * q4 + e) * kLgBS + 64 * i + r4] = rb[i][e];
+    };
 
     for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-        const int s0 = tile * kLgSurvTile;
-        const int rows = min(kLgSurvTile, (int)ns - s0);
-        __syncthreads();   // the previous tile's LDS data is consumed
-        // Survivor tile, dimension-major, zero padded.
-        for (int e = tid; e < kLgSurvTile * dp; e += blockDim.x) {
-            const int c = e / dp, m = e - c * dp;
-            float v = 0.f;
-            if (c < rows && m < d) v = P.X[(int64_t)Lg.surv[s0 + c] * d + m];
-            XT[m * XW + c] = v;
-        }
-        __syncthreads();
-        if (tid < kLgSurvTile) {
-            float acc = 0.f;
-            for (int m = 0; m < d; ++m) acc = fmaf(XT[m * XW + tid], XT[m * XW + tid], acc);
-            x2s[tid] = acc;
-        }
-        float L0[4], L1[4];
-        int J0[4], J1[4];
+        const int s0 = tile * kLgM;
+        const int rows = min(kLgM, (int)ns - s0);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            L0[q] = L1[q] = INFINITY;
-            J0[q] = J1[q] = INT_MAX;
+        for (int i = 0; i < 2; ++i) {
+            const int sl = 64 * i + r4;
+            srow[i] = sl < rows ? Lg.surv[s0 + sl] : -1;
+            x2p[i] = 0.f;
         }
-        int g = 0;   // running chunk count: buffer parity alternates across centroid tiles too
+        float L[2][4];
+        int J[2][4];
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                L[cb][q] = INFINITY;
+                J[cb][q] = INT_MAX;
+            }
         for (int ct = 0; ct < nct; ++ct) {
-            f32x16 acc0, acc1;
+            const int n0 = ct * kLgN;
+            f32x16 acc[2][2];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) acc0[e] = acc1[e] = 0.f;
-            for (int c = 0; c < nch; ++c, ++g) {
-                float* cb = CT + (g & 1) * 32 * CW;
-                for (int e = tid; e < kLgCentTile * 32; e += blockDim.x) {
-                    const int cj = e >> 5, m = e & 31;
-                    const int j = ct * kLgCentTile + cj, dim = c * 32 + m;
-                    cb[m * CW + cj] = (j < k && dim < d) ? P.C32[(int64_t)j * d + dim] : 0.f;
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+                for (int b = 0; b < 2; ++b)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
+            __syncthreads();   // the previous tile's buffers and lists are consumed
+            load_chunk(n0, 0);
+            store_chunk(0);
+            if (ct == 0)
+#pragma unroll
+                for (int i = 0; i < 2; ++i) x2p[i] += rb[i].x * rb[i].x + rb[i].y * rb[i].y + rb[i].z * rb[i].z + rb[i].w * rb[i].w;
+            __syncthreads();
+            for (int c = 0; c < nch; ++c) {
+                const bool more = c + 1 < nch;
+                if (more) load_chunk(n0, c + 1);
+                const float* A = Ab + (c & 1) * kLgK * kLgAS + 64 * wr + col;
+                const float* B = Bb + (c & 1) * kLgK * kLgBS + 64 * wc + col;
+#pragma unroll
+                for (int s = 0; s < kLgK / 2; ++s) {
+                    const int dm = 2 * s + half;
+                    const float a0 = A[dm * kLgAS], a1 = A[dm * kLgAS + 32];
+                    const float b0 = B[dm * kLgBS], b1 = B[dm * kLgBS + 32];
+                    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+                    acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+                    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+                    acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+                }
+                if (more) {
+                    store_chunk((c + 1) & 1);
+                    if (ct == 0)
+#pragma unroll
+                        for (int i = 0; i < 2; ++i)
+                            x2p[i] += rb[i].x * rb[i].x + rb[i].y * rb[i].y + rb[i].z * rb[i].z + rb[i].w * rb[i].w;
                 }
                 __syncthreads();
-                const float* xb = XT + (c * 32) * XW;
+            }
+            if (ct == 0) {   // squared norms of the survivors: the 4 lanes of each row
 #pragma unroll
-                for (int s = 0; s < 16; ++s) {
-                    const int dm = s + 16 * half;
-                    const float a = cb[dm * CW + wave * 32 + col];
-                    const float b0 = xb[dm * XW + col];
-                    const float b1 = xb[dm * XW + 32 + col];
-                    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b0, acc0, 0, 0, 0);
-                    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b1, acc1, 0, 0, 0);
+                for (int i = 0; i < 2; ++i) {
+                    float v = x2p[i];
+                    v += __shfl_xor(v, 1);
+                    v += __shfl_xor(v, 2);
+                    if (q4 == 0) x2s[64 * i + r4] = v;
                 }
+                __syncthreads();
             }
-            // Register e holds centroid ct*128 + wave*32 + 8*(e/4) + 4*half + e%4.
-            const float xa = x2s[col], xb2 = x2s[32 + col];
+            // Register e of accumulator [a][cb]: centroid n0 + 64 wr + 32 a + 8 (e / 4) + 4 half + e % 4,
+            // survivor column 64 wc + 32 cb + col.
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int j = ct * kLgCentTile + wave * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
-                const float cn = j < k ? P.cn2[j] : INFINITY;
-                top4_insert(L0, J0, xa + cn - 2.f * acc0[e], j);
-                top4_insert(L1, J1, xb2 + cn - 2.f * acc1[e], j);
+            for (int cb = 0; cb < 2; ++cb) {
+                const float xa = x2s[64 * wc + 32 * cb + col];
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        const int j = n0 + 64 * wr + 32 * a + 8 * (e >> 2) + 4 * half + (e & 3);
+                        const float cn = j < k ? P.cn2[j] : INFINITY;
+                        top4_insert(L[cb], J[cb], xa + cn - 2.f * acc[a][cb][e], j);
+                    }
             }
         }
-        // Merge the 8 partial lists of each survivor (4 waves x 2 halves).
+        // Merge the 4 lists of each survivor (2 waves x 2 half-waves).
+        __syncthreads();   // the chunk buffers are no longer read
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int slot = (wave * 2 + half) * 4 + q;
-            candD[col * 32 + slot] = L0[q];
-            candJ[col * 32 + slot] = J0[q];
-            candD[(32 + col) * 32 + slot] = L1[q];
-            candJ[(32 + col) * 32 + slot] = J1[q];
-        }
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int slot = (wr * 2 + half) * 4 + q;
+                candD[(64 * wc + 32 * cb + col) * 16 + slot] = L[cb][q];
+                candJ[(64 * wc + 32 * cb + col) * 16 + slot] = J[cb][q];
+            }
         __syncthreads();
 
-        // Refinement: 4 threads per survivor, each a quarter of the dimensions.
-        const int c = tid >> 2, part = tid & 3;
+        // Refinement: 2 threads per survivor, each half of the dimensions.
+        const int c = tid >> 1, part = tid & 1;
         if (c < rows) {
             float T[4];
             int TJ[4];
@@ -230,28 +310,65 @@ __global__ __launch_bounds__(256) void k_mfma_large(Dev P, Large Lg) {
                 T[q] = INFINITY;
                 TJ[q] = INT_MAX;
             }
-            for (int q = 0; q < 32; ++q) top4_insert(T, TJ, candD[c * 32 + q], candJ[c * 32 + q]);
+            for (int q = 0; q < 16; ++q) top4_insert(T, TJ, candD[c * 16 + q], candJ[c * 16 + q]);
             const int64_t i = Lg.surv[s0 + c];
+            const float* xr = P.X + i * d;
             const int inc = first ? -1 : P.a[i];
-            const int qd = (d + 3) / 4, m0 = part * qd, m1 = min(d, m0 + qd);
+            const int hd = (d + 1) / 2, m0 = part * hd, m1 = min(d, m0 + hd);
             const float R = sqrtf(fmaxf(x2s[c], 0.f)) * kUp + cnmax;
             const float thr = T[0] + 2.f * (gexp * R * R + 4.f * R * ecm + 2.f * ecm * ecm);
-            // A fourth candidate inside the bound means more may lie outside
-            // the list: decide in float64 then.
-            bool re = T[3] <= thr;
+            // Only centroids whose expanded distance lies within thr of the
+            // smallest can be the nearest: any other one is certified
+            // farther than the smallest's centroid.  A fourth candidate
+            // inside the bound means more may lie outside the list: all
+            // centroids are decided in float64 then.
+            const bool full = T[3] <= thr;
+            int nq = 0;
+            while (nq < 3 && T[nq] <= thr && TJ[nq] < k) ++nq;   // uniform in the pair
+            // Direct-form distance of x to centroid j over this thread's half
+            // of the dimensions, both halves added (equal in the pair).
+            auto dist32 = [&](int j) {
+                const float* cr = P.C32 + (int64_t)j * d;
+                float accd = 0.f;
+                if (vec && (m0 & 3) == 0) {
+                    int m = m0;
+                    for (; m + 4 <= m1; m += 4) {
+                        const f32x4 xv = *reinterpret_cast<const f32x4*>(xr + m);
+                        const f32x4 cv = *reinterpret_cast<const f32x4*>(cr + m);
+                        const float t0 = xv.x - cv.x, t1 = xv.y - cv.y, t2 = xv.z - cv.z, t3 = xv.w - cv.w;
+                        accd = fmaf(t0, t0, accd);
+                        accd = fmaf(t1, t1, accd);
+                        accd = fmaf(t2, t2, accd);
+                        accd = fmaf(t3, t3, accd);
+                    }
+                    for (; m < m1; ++m) {
+                        const float t = xr[m] - cr[m];
+                        accd = fmaf(t, t, accd);
+                    }
+                } else {
+                    for (int m = m0; m < m1; ++m) {
+                        const float t = xr[m] - cr[m];
+                        accd = fmaf(t, t, accd);
+                    }
+                }
+                return accd + __shfl_xor(accd, 1);
+            };
+            auto dist64 = [&](int j) {
+                const double* cr = P.C64 + (int64_t)j * d;
+                double accd = 0.0;
+                for (int m = m0; m < m1; ++m) {
+                    const double t = (double)xr[m] - cr[m];
+                    accd = fma(t, t, accd);
+                }
+                return accd + __shfl_xor(accd, 1);
+            };
+            bool re = full;
             float d1 = INFINITY, d2 = INFINITY;
             int rk1 = INT_MAX, j1 = 0;
-            if (!re) {
-                for (int q = 0; q < 3; ++q) {
-                    if (!(T[q] <= thr) || TJ[q] >= k) continue;   // uniform in the quad
+            if (!full) {
+                for (int q = 0; q < nq; ++q) {
                     const int j = TJ[q];
-                    const float* cr = P.C32 + (int64_t)j * d;
-                    float acc = 0.f;
-                    for (int m = m0; m < m1; ++m) {
-                        const float t = XT[m * XW + c] - cr[m];
-                        acc = fmaf(t, t, acc);
-                    }
-                    const float Dd = quad_sum(acc);
+                    const float Dd = dist32(j);
                     const int rk = j == inc ? -1 : j;
                     if (Dd < d1 || (Dd == d1 && rk < rk1)) {
                         d2 = d1;
@@ -271,29 +388,25 @@ __global__ __launch_bounds__(256) void k_mfma_large(Dev P, Large Lg) {
             int b = j1;
             float ub = upper_bound(d1, P.ec[j1], gamma);
             if (re) {
-                // float64 decision against the master centroids, oracle's tie rule.
+                // float64 decision against the master centroids with the
+                // oracle's rule (smaller distance, then the incumbent, then
+                // the lower index): among the candidates inside the bound, or
+                // among all centroids when the list may be incomplete.
                 double Dbb = INFINITY;
-                int bb = -1;
-                auto d64 = [&](int j) {
-                    const double* cr = P.C64 + (int64_t)j * d;
-                    double acc = 0.0;
-                    for (int m = m0; m < m1; ++m) {
-                        const double t = (double)XT[m * XW + c] - cr[m];
-                        acc = fma(t, t, acc);
-                    }
-                    return quad_sum(acc);
-                };
-                if (inc >= 0) {
-                    Dbb = d64(inc);
-                    bb = inc;
-                }
-                for (int j = 0; j < k; ++j) {
-                    if (j == inc) continue;
-                    const double Dj = d64(j);
-                    if (Dj < Dbb) {
+                int bb = -1, kb = INT_MAX;
+                auto consider = [&](int j) {
+                    const double Dj = dist64(j);
+                    const int rk = j == inc ? -1 : j;
+                    if (Dj < Dbb || (Dj == Dbb && rk < kb)) {
                         Dbb = Dj;
                         bb = j;
+                        kb = rk;
                     }
+                };
+                if (full) {
+                    for (int j = 0; j < k; ++j) consider(j);
+                } else {
+                    for (int q = 0; q < nq; ++q) consider(TJ[q]);
                 }
                 b = bb < 0 ? 0 : bb;
                 ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
@@ -549,7 +662,7 @@ const void* large_mfma_symbol() { return reinterpret_cast<const void*>(&k_mfma_l
 
 hipError_t launch_large_assign(const Dev& dv, const Large& lg, int gb, hipStream_t s) {
     hipLaunchKernelGGL(k_bound_large, dim3(gb), dim3(256), 0, s, dv, lg);
-    hipLaunchKernelGGL(k_mfma_large, dim3(lg.Gm), dim3(256), large_mfma_lds(lg.dp), s, dv, lg);
+    hipLaunchKernelGGL(k_mfma_large, dim3(lg.Gm), dim3(256), large_mfma_lds(), s, dv, lg);
     return hipGetLastError();
 }
 
@@ -567,11 +680,11 @@ hipError_t launch_large_reduce(const Dev& dv, const Large& lg, hipStream_t s) {
 
 int large_table_lds(int d) { return 8 * kTiTile * d + 4 * kTiTile * 256; }
 
-hipError_t large_set_attributes(int k, int d, int dp) {
+hipError_t large_set_attributes(int k, int d) {
     hipError_t e;
     const auto attr = hipFuncAttributeMaxDynamicSharedMemorySize;
-    if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_mfma_large), attr,
-                                 large_mfma_lds(dp))) != hipSuccess)
+    if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_mfma_large), attr, large_mfma_lds())) !=
+        hipSuccess)
         return e;
     if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_hist_large), attr, 4 * k)) != hipSuccess)
         return e;
