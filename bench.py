@@ -24,6 +24,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_F32_PEAK_TFS = 157.3   # MI355X dense float32 matrix peak
 DEFAULT_WORKLOAD = "aniso-8M-d16-k10"
 METRIC = "k-means iters/sec + effective dist evals/sec; % HBM peak (low d) / % MFMA (big k·d)"
 
@@ -85,6 +86,18 @@ def roofline_entry(kernel: str, workload: str, bytes_per_launch: float, launch_m
     return {"kernel": kernel, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "traffic_source": source,
             "bytes_per_launch": bytes_per_launch, "bytes_def": what, "kernel_us": launch_ms * 1e3}
+
+
+def mfma_roofline_entry(kernel: str, workload: str, flops_per_launch: float, launch_ms: float,
+                        what: str) -> dict:
+    """Matrix-core roofline of one kernel: algorithmic float32 flops per launch
+    over its mean launch time (HIP events), against the dense float32 peak."""
+    achieved = flops_per_launch / (launch_ms / 1e3) / 1e12
+    traffic, source = measured_traffic(kernel, workload)
+    return {"kernel": kernel, "bound": "mfma", "achieved": achieved, "peak": MFMA_F32_PEAK_TFS,
+            "unit": "TFLOP/s", "frac": achieved / MFMA_F32_PEAK_TFS, "traffic": traffic,
+            "traffic_source": source, "flops_per_launch": flops_per_launch, "flops_def": what,
+            "kernel_us": launch_ms * 1e3}
 
 
 def cpu_baseline(X, C0, w, budget_s: float = 15.0) -> dict:
@@ -213,8 +226,19 @@ def main() -> int:
         else:
             bytes_per_launch = n * (4 * d + 12) + 4 * ch / (K - 1)
             what = "steps 2..K: n*(4d+12) + changed*4"
-        rooflines.append(roofline_entry(kernel, w.name, bytes_per_launch, later_t["assign_ms"] / (K - 1),
-                                        what))
+        launch_ms = later_t["assign_ms"] / (K - 1)
+        flops = 2.0 * d * k * surv / (K - 1)
+        if path == "global-mfma":
+            # The matrix-core distance product of the survivors dominates (the
+            # bound pass before it streams 8 bytes per point).
+            rooflines.append(mfma_roofline_entry(kernel, w.name, flops, launch_ms,
+                                                 "steps 2..K: 2*d*k per Clause-1 survivor (bound pass included in the time)"))
+            rooflines.append(roofline_entry(kernel, w.name, bytes_per_launch, launch_ms, what))
+        else:
+            rooflines.append(roofline_entry(kernel, w.name, bytes_per_launch, launch_ms, what))
+            if path == "lds-mfma":
+                rooflines.append(mfma_roofline_entry(kernel, w.name, flops, launch_ms,
+                                                     "steps 2..K: 2*d*k per Clause-1 survivor"))
         if path == "stream-d16":   # the full-read streaming kernel on the same steps
             _, later_f, h_f = kernel_pass(full_sums=True)
             surv_f = n * (K - 1) - int(h_f["clause1"][1:].sum())

@@ -435,7 +435,7 @@ __device__ inline void klane_survivors(const ScanCtx& W, const float* hl, int ns
 // path's.
 
 template <int D, int KB>
-__global__ __launch_bounds__(256) void k_assign(Dev P) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1 : 2))) void k_assign(Dev P) {
     IterState* st = P.st;
     if (st->done) {
         if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
@@ -666,6 +666,7 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
                     for (int e = 0; e < 16; ++e)
                         if (x2 + cn2s[cent(cb, e)] - 2.f * dot[cb][e] <= thr) cmask |= 1ull << (16 * cb + e);
                 const int inc = live ? sa[r] : -1;
+                const uint64_t cmask0 = cmask;
                 float d1 = INFINITY, d2 = INFINITY;
                 int rk1 = INT_MAX, j1 = 0, ncand = 0;
                 while (cmask) {
@@ -694,33 +695,50 @@ __global__ __launch_bounds__(256) void k_assign(Dev P) {
                 } else {
                     d2 = fminf(d2, fminf(od1, od2));
                 }
+                // Near tie: float64 decision among the candidates (the only
+                // centroids that can be nearest), each half-wave over its own,
+                // then the smaller (distance, incumbent first, lower index).
+                bool re = false;
+                if (d2 != INFINITY) {
+                    const float band = 2.f * gamma * (d1 + d2) +
+                                       4.f * (sqrtf(d1) + sqrtf(d2)) * ecmax + 8.f * ecmax * ecmax;
+                    re = live && d2 - d1 <= band;
+                }
+                double Dbb = INFINITY;
+                int kb = INT_MAX, bb = -1;
+                if (re) {
+                    uint64_t cm = cmask0;
+                    while (cm) {
+                        const int bit = __builtin_ctzll(cm);
+                        cm &= cm - 1;
+                        const int j = cent(bit >> 4, bit & 15);
+                        const double Dj = sqd64(xr, P.C64 + (int64_t)j * d, d);
+                        const int rk = j == inc ? -1 : j;
+                        if (Dj < Dbb || (Dj == Dbb && rk < kb)) {
+                            Dbb = Dj;
+                            kb = rk;
+                            bb = j;
+                        }
+                    }
+                }
+                {
+                    const double oD = __shfl_xor(Dbb, 32);
+                    const int okb = __shfl_xor(kb, 32), obb = __shfl_xor(bb, 32);
+                    if (oD < Dbb || (oD == Dbb && okb < kb)) {
+                        Dbb = oD;
+                        kb = okb;
+                        bb = obb;
+                    }
+                }
                 if (live && half == 0) {
                     int b = j1;
                     float Db = d1;
                     float ub = upper_bound(Db, ecs[b], gamma);
-                    if (d2 != INFINITY) {
-                        const float band = 2.f * gamma * (d1 + d2) +
-                                           4.f * (sqrtf(d1) + sqrtf(d2)) * ecmax + 8.f * ecmax * ecmax;
-                        if (d2 - d1 <= band) {
-                            int bb = -1;
-                            double Dbb = INFINITY;
-                            if (inc >= 0) {
-                                Dbb = sqd64(xr, P.C64 + (int64_t)inc * d, d);
-                                bb = inc;
-                            }
-                            for (int j = 0; j < k; ++j) {
-                                if (j == inc) continue;
-                                const double Dj = sqd64(xr, P.C64 + (int64_t)j * d, d);
-                                if (Dj < Dbb) {
-                                    Dbb = Dj;
-                                    bb = j;
-                                }
-                            }
-                            b = bb < 0 ? 0 : bb;
-                            Db = (float)Dbb;
-                            ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
-                            my_rc += 1;
-                        }
+                    if (re) {
+                        b = bb < 0 ? 0 : bb;
+                        Db = (float)Dbb;
+                        ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
+                        my_rc += 1;
                     }
                     sa[r] = b;
                     su[r] = ub;
