@@ -667,6 +667,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
                         if (x2 + cn2s[cent(cb, e)] - 2.f * dot[cb][e] <= thr) cmask |= 1ull << (16 * cb + e);
                 const int inc = live ? sa[r] : -1;
                 const uint64_t cmask0 = cmask;
+                // A single candidate over both half-waves is the nearest
+                // centroid: its bound comes from its expanded value and the
+                // error bound, without the direct form (kept with inertia).
+                const int own = __popcll(cmask0);
+                const bool single = !want_inertia && own + __shfl_xor(own, 32) == 1;
+                const int jown = own ? cent(__builtin_ctzll(cmask0) >> 4, __builtin_ctzll(cmask0) & 15) : -1;
+                const int jsingle = max(jown, __shfl_xor(jown, 32));
+                if (single) cmask = 0;
                 float d1 = INFINITY, d2 = INFINITY;
                 int rk1 = INT_MAX, j1 = 0, ncand = 0;
                 while (cmask) {
@@ -734,6 +742,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
                     int b = j1;
                     float Db = d1;
                     float ub = upper_bound(Db, ecs[b], gamma);
+                    if (single) {
+                        const float e1b = gexp * R * R + 4.f * R * ecmax + 2.f * ecmax * ecmax;
+                        b = jsingle;
+                        Db = e1;
+                        ub = __builtin_amdgcn_sqrtf(fmaxf(e1 + e1b, 0.f)) * (1.0f + 0x1p-20f) * kUp;
+                    }
                     if (re) {
                         b = bb < 0 ? 0 : bb;
                         Db = (float)Dbb;
