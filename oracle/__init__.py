@@ -6,8 +6,9 @@ in the product path imports it.
 
 ``lloyd`` / ``assign`` / ``update`` wrap plain float64 Lloyd's k-means (no
 pruning) from ``lloyd.c``; ``mti`` wraps the separately written float64 MTI
-reference from ``mti_ref.c``.  Both are compiled with gcc into
-``liboracle.so`` next to this file by :func:`build`.
+reference from ``mti_ref.c``; ``spherical`` wraps float64 spherical k-means
+(cosine proximity on the unit sphere) from ``spherical.c``.  All are compiled
+with gcc into ``liboracle.so`` next to this file by :func:`build`.
 """
 from __future__ import annotations
 
@@ -20,7 +21,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liboracle.so")
-SOURCES = [os.path.join(_HERE, "lloyd.c"), os.path.join(_HERE, "mti_ref.c")]
+SOURCES = [os.path.join(_HERE, "lloyd.c"), os.path.join(_HERE, "mti_ref.c"), os.path.join(_HERE, "spherical.c")]
 
 _lib = None
 
@@ -60,6 +61,8 @@ def _load():
     lib.oracle_lloyd.restype = i32
     lib.mti_lloyd.argtypes = [P, i64, i32, i32, P, i32, f64, i32, P, P, P, P, P, P, P, P]
     lib.mti_lloyd.restype = i32
+    lib.oracle_spherical.argtypes = [P, i64, i32, i32, P, i32, f64, P, P, P, P, P, P, P]
+    lib.oracle_spherical.restype = i32
     _lib = lib
     return lib
 
@@ -186,3 +189,31 @@ def mti(X: np.ndarray, C0: np.ndarray, max_iters: int, tol: float = 0.0, halve: 
     if check_bounds:
         res["bound_violations"] = int(bv.value)
     return res
+
+
+def spherical(X: np.ndarray, C0: np.ndarray, max_iters: int, tol: float = 0.0) -> Dict[str, np.ndarray]:
+    """float64 spherical k-means from C0 (rows of C0 nonzero).
+
+    Returns ``assign``, ``C`` (unit centroids after the last update),
+    ``iters``, ``objective`` (sum of squared chord distances 2 - 2 cos per
+    step), ``changed``, and ``best`` / ``second`` (last step's smallest and
+    second-smallest squared chord distances).
+    """
+    X = _x(X)
+    n, d = X.shape
+    k = np.asarray(C0).shape[0]
+    C0 = _c(C0, k, d)
+    T = int(max_iters)
+    a = np.empty(n, np.int32)
+    Cout = np.empty((k, d), np.float64)
+    it = C.c_int32(0)
+    J = np.zeros(T, np.float64)
+    ch = np.zeros(T, np.int64)
+    b = np.empty(n, np.float64)
+    s = np.empty(n, np.float64)
+    rc = _load().oracle_spherical(_ptr(X), n, d, k, _ptr(C0), T, float(tol), _ptr(a), _ptr(Cout),
+                                  C.byref(it), _ptr(J), _ptr(ch), _ptr(b), _ptr(s))
+    if rc != 0:
+        raise ValueError("oracle_spherical rejected its arguments")
+    t = it.value
+    return dict(assign=a, C=Cout, iters=t, objective=J[:t], changed=ch[:t], best=b, second=s)
