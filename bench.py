@@ -10,7 +10,7 @@ bracketed by device synchronisation; the reported value is iterations per
 second.  Per-kernel device times come from HIP events recorded by the
 library on its stream around every launch.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--spherical] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -100,19 +100,22 @@ def mfma_roofline_entry(kernel: str, workload: str, flops_per_launch: float, lau
             "kernel_us": launch_ms * 1e3}
 
 
-def cpu_baseline(X, C0, w, budget_s: float = 15.0) -> dict:
-    """Time the CPU oracle (plain float64 Lloyd's, as it stands) on this host."""
+def cpu_baseline(X, C0, w, budget_s: float = 15.0, spherical: bool = False) -> dict:
+    """Time the CPU oracle (plain float64 Lloyd's or spherical k-means, as it
+    stands) on this host."""
     import oracle
+    fn = oracle.spherical if spherical else oracle.lloyd
     t0 = time.perf_counter()
-    oracle.lloyd(X, C0, 1, 0.0)
+    fn(X, C0, 1, 0.0)
     t1 = time.perf_counter() - t0
     iters = int(max(1, min(w.max_iters, budget_s // max(t1, 1e-3))))
     t0 = time.perf_counter()
-    r = oracle.lloyd(X, C0, iters, 0.0)
+    r = fn(X, C0, iters, 0.0)
     el = time.perf_counter() - t0
     ips = r["iters"] / el
     return {
-        "value": ips, "unit": "iters/s", "cores": oracle.get_threads(), "kind": "oracle",
+        # the spherical oracle is a single-threaded loop
+        "value": ips, "unit": "iters/s", "cores": 1 if spherical else oracle.get_threads(), "kind": "oracle",
         "sample": "all %d rows of %s, first %d iterations from the seeded centroids (tol ignored); "
                   "%.3g effective dist evals/s" % (w.n, w.name, r["iters"], ips * w.n * w.k),
     }
@@ -129,6 +132,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--full-sums", action="store_true",
                     help="recompute the sums from every point each step (KM_FLAG_FULL_SUMS)")
+    ap.add_argument("--spherical", action="store_true",
+                    help="spherical k-means on the same workload (KM_FLAG_SPHERICAL: rows and "
+                         "centroids on the unit sphere, cosine assignment)")
     ap.add_argument("--profile", action="store_true",
                     help="run only the warmup and the timed region (no event pass, no job run, no "
                          "CPU leg), so a profiler sees warmup + K launches of each kernel")
@@ -171,6 +177,10 @@ def main() -> int:
     if args.profile:
         args.no_cpu_baseline = True
     base_flags = {"full_sums": True} if args.full_sums else {}
+    if args.spherical:
+        base_flags["spherical"] = True
+    # profiles/<kernel>_<tag>.txt holds the counters of this workload and method
+    tag = w.name + ("-spherical" if args.spherical else "")
     if args.warmup > 0:
         with km.KMeansMTI(Xg, Cg, **base_flags) as ctx:
             for _ in range(args.warmup):
@@ -231,18 +241,18 @@ def main() -> int:
         if path == "global-mfma":
             # The matrix-core distance product of the survivors dominates (the
             # bound pass before it streams 8 bytes per point).
-            rooflines.append(mfma_roofline_entry(kernel, w.name, flops, launch_ms,
+            rooflines.append(mfma_roofline_entry(kernel, tag, flops, launch_ms,
                                                  "steps 2..K: 2*d*k per Clause-1 survivor (bound pass included in the time)"))
-            rooflines.append(roofline_entry(kernel, w.name, bytes_per_launch, launch_ms, what))
+            rooflines.append(roofline_entry(kernel, tag, bytes_per_launch, launch_ms, what))
         else:
-            rooflines.append(roofline_entry(kernel, w.name, bytes_per_launch, launch_ms, what))
+            rooflines.append(roofline_entry(kernel, tag, bytes_per_launch, launch_ms, what))
             if path == "lds-mfma":
-                rooflines.append(mfma_roofline_entry(kernel, w.name, flops, launch_ms,
+                rooflines.append(mfma_roofline_entry(kernel, tag, flops, launch_ms,
                                                      "steps 2..K: 2*d*k per Clause-1 survivor"))
         if path == "stream-d16":   # the full-read streaming kernel on the same steps
-            _, later_f, h_f = kernel_pass(full_sums=True)
+            _, later_f, h_f = kernel_pass(**dict(base_flags, full_sums=True))
             surv_f = n * (K - 1) - int(h_f["clause1"][1:].sum())
-            rooflines.append(roofline_entry("k_small", w.name, (n * (4 * d + 4) * (K - 1) + 4 * surv_f) / (K - 1),
+            rooflines.append(roofline_entry("k_small", tag, (n * (4 * d + 4) * (K - 1) + 4 * surv_f) / (K - 1),
                                             later_f["assign_ms"] / (K - 1),
                                             "steps 2..K with KM_FLAG_FULL_SUMS: n*(4d+4) + survivors*4"))
 
@@ -271,7 +281,8 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "n": n, "d": d, "k": k, "max_iters": w.max_iters, "tol": w.tol,
+        "config": {"workload": w.name, "method": "spherical" if args.spherical else "kmeans",
+                   "n": n, "d": d, "k": k, "max_iters": w.max_iters, "tol": w.tol,
                    "timed": "first %d iterations from the seeded centroids" % K, "path": path},
         "eff_dist_evals_per_s": lloyd / elapsed,
         "computed_dist_evals_per_s": computed / elapsed,
@@ -289,7 +300,7 @@ def main() -> int:
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
-        result["cpu_baseline"] = cpu_baseline(X, C0, w)
+        result["cpu_baseline"] = cpu_baseline(X, C0, w, spherical=args.spherical)
     print(json.dumps(result), flush=True)
     return 0
 

@@ -77,11 +77,20 @@ enum {
     KM_FLAG_GENERIC = 64u,     /* use the general assignment kernel and separate reduction,
                                   update and table launches even where the streaming step
                                   (d = 16, k <= 16) applies; same results */
-    KM_FLAG_FULL_SUMS = 128u   /* streaming step: recompute the per-cluster sums from every
+    KM_FLAG_FULL_SUMS = 128u,  /* streaming step: recompute the per-cluster sums from every
                                   point (one full read of X) in every step instead of moving
                                   the sums of the points whose assignment changed (after the
                                   first step only the Clause-1 survivors' rows are read);
                                   same results.  Implied by KM_FLAG_STATS. */
+    KM_FLAG_SPHERICAL = 256u   /* spherical k-means (the paper's sk-means application): the
+                                  rows of X are projected to the unit sphere (into a copy the
+                                  context owns; a zero row stays zero) and C0 likewise, the
+                                  assignment maximises the cosine (the nearest unit centroid),
+                                  and each update projects the members' mean to the sphere (a
+                                  cluster with no member or a zero mean keeps its centroid).
+                                  C0 rows must be nonzero (else KM_ERR_INVALID_ARG).  Centroid
+                                  outputs are unit vectors; the inertia is the sum of squared
+                                  chord distances 2 - 2 cos. */
 };
 
 /* Totals over the iterations run so far (kmeans_mti_get_stats, kmeans_mti_run). */

@@ -26,6 +26,7 @@ KM_FLAG_VECTOR_ONLY = 16
 KM_FLAG_LARGE_PATH = 32
 KM_FLAG_GENERIC = 64
 KM_FLAG_FULL_SUMS = 128
+KM_FLAG_SPHERICAL = 256
 
 #: Every symbol include/kmeans_mti.h declares.
 EXPORTS = (

@@ -209,6 +209,16 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     if ((rc0 = check_device_range(C0, (size_t)k * (size_t)d * sizeof(float), c->device, "C0")) != KM_OK)
         return rc0;
 
+    // Spherical k-means: the context works on its own copy of X projected to
+    // the unit sphere (X itself is only read here).
+    if (c->flags & KM_FLAG_SPHERICAL) {
+        float* Xn = nullptr;
+        int rcn;
+        if ((rcn = c->alloc(&Xn, (size_t)n * (size_t)d))) return rcn;
+        KM_HIP(km::launch_normalize_rows(X, n, d, Xn, c->stream));
+        X = Xn;
+    }
+
     int cus = 0, max_lds = 0;
     KM_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, c->device));
     KM_HIP(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, c->device));
@@ -341,17 +351,30 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         KM_HIP(hipMemsetAsync(c->fz.ddn, 0, sizeof(float) * (size_t)k, c->stream));
     }
     uint32_t* scratch = nullptr;
-    if ((rc = c->alloc(&scratch, 4))) return rc;
+    if ((rc = c->alloc(&scratch, 5))) return rc;
 
-    // Largest magnitude of X and C0 (and non-finite detection) -> fixed-point scales.
-    KM_HIP(hipMemsetAsync(scratch, 0, 4 * sizeof(uint32_t), c->stream));
+    // Largest magnitude of X and C0 (and non-finite detection) -> fixed-point
+    // scales; with spherical k-means also the unit centroids and whether C0
+    // has a zero row.
+    KM_HIP(hipMemsetAsync(scratch, 0, 5 * sizeof(uint32_t), c->stream));
     KM_HIP(km::launch_absmax(X, n * d, scratch, reinterpret_cast<int32_t*>(scratch + 1), c->stream));
     KM_HIP(km::launch_absmax(C0, (int64_t)k * d, scratch + 2, reinterpret_cast<int32_t*>(scratch + 3),
                              c->stream));
-    uint32_t host[4];
+    if (c->flags & KM_FLAG_SPHERICAL)
+        KM_HIP(km::launch_set_centroids_unit(C0, v.C64, v.C32, v.ec, k, d, reinterpret_cast<int32_t*>(scratch + 4),
+                                             c->stream));
+    uint32_t host[5];
     KM_HIP(hipMemcpyAsync(host, scratch, sizeof host, hipMemcpyDeviceToHost, c->stream));
     KM_HIP(hipStreamSynchronize(c->stream));
     if ((c->flags & KM_FLAG_VALIDATE) && (host[1] || host[3])) return KM_ERR_NONFINITE;
+    if (host[4]) {
+        snprintf(g_last_hip, sizeof g_last_hip, "spherical k-means: C0 has a zero row");
+        return KM_ERR_INVALID_ARG;
+    }
+    if (c->flags & KM_FLAG_SPHERICAL) {   // the centroids and the data are unit vectors
+        const float one = 1.0f;
+        memcpy(&host[2], &one, 4);
+    }
     float xmax, cmax;
     memcpy(&xmax, &host[0], 4);
     memcpy(&cmax, &host[2], 4);
@@ -386,7 +409,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     KM_HIP(hipMemcpyAsync(v.st, &st0, sizeof st0, hipMemcpyHostToDevice, c->stream));
     KM_HIP(hipMemsetAsync(v.total, 0, sizeof(uint64_t) * (size_t)v.L, c->stream));
     KM_HIP(hipMemsetAsync(v.rec, 0, sizeof(km::IterRec) * km::kHistCap, c->stream));
-    KM_HIP(km::launch_set_centroids(C0, v.C64, v.C32, v.ec, (int64_t)k * d, k, c->stream));
+    if (!(c->flags & KM_FLAG_SPHERICAL))
+        KM_HIP(km::launch_set_centroids(C0, v.C64, v.C32, v.ec, (int64_t)k * d, k, c->stream));
     if (c->large) {
         KM_HIP(km::launch_large_table(v, 1, c->stream));
     } else {
@@ -415,7 +439,7 @@ int kmeans_mti_init(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t 
     if (rc != KM_OK) return rc;
     if (flags & ~(uint32_t)(KM_FLAG_NO_PRUNE | KM_FLAG_STATS | KM_FLAG_VALIDATE | KM_FLAG_TIMING |
                             KM_FLAG_VECTOR_ONLY | KM_FLAG_LARGE_PATH | KM_FLAG_GENERIC |
-                            KM_FLAG_FULL_SUMS))
+                            KM_FLAG_FULL_SUMS | KM_FLAG_SPHERICAL))
         return KM_ERR_INVALID_ARG;
     km_ctx* c = new (std::nothrow) km_ctx;
     if (!c) return KM_ERR_OOM;

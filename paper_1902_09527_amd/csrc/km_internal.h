@@ -268,6 +268,11 @@ hipError_t launch_absmax(const float* X, int64_t count, uint32_t* absmax_bits, i
                          hipStream_t s);
 hipError_t launch_set_centroids(const float* C0, double* C64, float* C32, float* ec, int64_t kd,
                                 int32_t k, hipStream_t s);
+// Spherical k-means: rows of X projected to the unit sphere into Xn; unit
+// centroids from C0 (*zero set for a zero row).
+hipError_t launch_normalize_rows(const float* X, int64_t n, int32_t d, float* Xn, hipStream_t s);
+hipError_t launch_set_centroids_unit(const float* C0, double* C64, float* C32, float* ec, int32_t k, int32_t d,
+                                     int32_t* zero, hipStream_t s);
 hipError_t launch_assign(const Dev& dv, int variant, int tp, int lds_bytes, hipStream_t s);
 hipError_t launch_reduce(const Dev& dv, hipStream_t s);
 hipError_t launch_update(const Dev& dv, hipStream_t s);

@@ -8,7 +8,8 @@
 //                     fixed-point partial sums/counts of ALL points
 //                     (section III-C; section V "per-thread local centroids");
 //   k_reduce          sums the per-block partial rows (integer, exact);
-//   k_update          new centroids (member means, empty clusters kept),
+//   k_update          new centroids (member means, empty clusters kept; for
+//                     spherical k-means projected to the unit sphere),
 //                     drift f(c) (Table I), loop counters and the stop test;
 //   k_centroid_table  half centroid-to-centroid distances h and
 //                     s(c) = min_{c' != c} h(c, c') for the next step.
@@ -126,6 +127,46 @@ __global__ void k_set_centroids(const float* __restrict__ C0, double* C64, float
         C32[i] = v;
     }
     if (i < k) ec[i] = 0.f;
+}
+
+// Spherical k-means (the paper's sk-means application): row i of X projected
+// to the unit sphere, x / |x| with the norm and the quotient in float64
+// (a zero row stays zero).
+__global__ void k_normalize_rows(const float* __restrict__ X, int64_t n, int32_t d, float* __restrict__ Xn) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const float* x = X + i * d;
+        double s = 0.0;
+        for (int m = 0; m < d; ++m) s = fma((double)x[m], (double)x[m], s);
+        const double r = sqrt(s);
+        float* o = Xn + i * d;
+        for (int m = 0; m < d; ++m) o[m] = r > 0.0 ? (float)((double)x[m] / r) : 0.f;
+    }
+}
+
+// Unit centroids from C0 (one thread per row): float64 master, its float32
+// copy and that copy's rounding error; *zero is set for a zero row.
+__global__ void k_set_centroids_unit(const float* __restrict__ C0, double* C64, float* C32, float* ec, int32_t k,
+                                     int32_t d, int32_t* zero) {
+    const int j = blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= k) return;
+    const float* c = C0 + (int64_t)j * d;
+    double s = 0.0;
+    for (int m = 0; m < d; ++m) s = fma((double)c[m], (double)c[m], s);
+    if (!(s > 0.0)) {
+        atomicOr(zero, 1);
+        s = 1.0;
+    }
+    const double r = sqrt(s);
+    double e2 = 0.0;
+    for (int m = 0; m < d; ++m) {
+        const double v = (double)c[m] / r;
+        const float v32 = (float)v;
+        C64[(int64_t)j * d + m] = v;
+        C32[(int64_t)j * d + m] = v32;
+        e2 = fma((double)v32 - v, (double)v32 - v, e2);
+    }
+    ec[j] = f32_up(sqrt(e2) * (1.0 + 0x1p-40));
 }
 
 // ---------------------------------------------------------------------------
@@ -964,17 +1005,31 @@ __global__ __launch_bounds__(64) void k_update(Dev P) {
     if (!st->active) return;
     const int j = blockIdx.x, d = P.d, k = P.k;
     const uint64_t count = P.total[(int64_t)k * d + j];
+    auto mean = [&](int64_t o) {
+        const int64_t q = (int64_t)(P.total[o] - count * kMagicBits);
+        return ((double)q * P.qinv) / (double)count;
+    };
+    // Spherical k-means: the mean is projected to the unit sphere (a zero
+    // mean keeps the centroid).
+    double scale = 1.0;
+    bool keep = count == 0;
+    if ((P.flags & KM_FLAG_SPHERICAL) && count > 0) {
+        double s = 0.0;
+        for (int m = threadIdx.x; m < d; m += 64) {
+            const double v = mean((int64_t)j * d + m);
+            s = fma(v, v, s);
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+        if (s > 0.0) scale = sqrt(s);
+        else keep = true;
+    }
     double dr = 0.0, de = 0.0;
     for (int m = threadIdx.x; m < d; m += 64) {
         const int64_t o = (int64_t)j * d + m;
-        const uint64_t raw = P.total[o];
-        P.total[o] = 0;
         const double cold = P.C64[o];
-        double cnew = cold;
-        if (count > 0) {
-            const int64_t q = (int64_t)(raw - count * kMagicBits);
-            cnew = ((double)q * P.qinv) / (double)count;
-        }
+        const double cnew = keep ? cold : mean(o) / scale;
+        P.total[o] = 0;
         const double df = cnew - cold;
         dr = fma(df, df, dr);
         const float c32 = (float)cnew;
@@ -1052,6 +1107,20 @@ hipError_t launch_absmax(const float* X, int64_t count, uint32_t* absmax_bits, i
     if (blocks < 1) blocks = 1;
     hipLaunchKernelGGL(k_absmax, dim3((unsigned)blocks), dim3(256), 0, s, X, count, absmax_bits,
                        nonfinite);
+    return hipGetLastError();
+}
+
+hipError_t launch_normalize_rows(const float* X, int64_t n, int32_t d, float* Xn, hipStream_t s) {
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 16384) blocks = 16384;
+    hipLaunchKernelGGL(k_normalize_rows, dim3((unsigned)blocks), dim3(256), 0, s, X, n, d, Xn);
+    return hipGetLastError();
+}
+
+hipError_t launch_set_centroids_unit(const float* C0, double* C64, float* C32, float* ec, int32_t k, int32_t d,
+                                     int32_t* zero, hipStream_t s) {
+    hipLaunchKernelGGL(k_set_centroids_unit, dim3((unsigned)((k + 255) / 256)), dim3(256), 0, s, C0, C64, C32, ec,
+                       k, d, zero);
     return hipGetLastError();
 }
 

@@ -778,12 +778,33 @@ __global__ __launch_bounds__(kTp) void k_small_finish(Dev P, Fused F, int delta,
             const int64_t qs = (int64_t)(tot[e] - count * kMagicBits);
             cnew = ((double)qs * P.qinv) / (double)count;
         }
+        cn[e] = cnew;
+    }
+    if (P.flags & KM_FLAG_SPHERICAL) {   // spherical k-means: means projected to the unit sphere
+        __syncthreads();
+        for (int jc = tid; jc < k; jc += nt) {
+            if (tot[k * d + jc] == 0) continue;   // empty: the old (unit) centroid is kept
+            double ss = 0.0;
+            for (int m = 0; m < d; ++m) ss = fma(cn[jc * d + m], cn[jc * d + m], ss);
+            if (ss > 0.0) {
+                const double r = sqrt(ss);
+                for (int m = 0; m < d; ++m) cn[jc * d + m] /= r;
+            } else {
+                for (int m = 0; m < d; ++m) cn[jc * d + m] = P.C64[jc * d + m];   // zero mean: kept
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int q = 0; q * nt < kSmallMaxK * 16; ++q) {
+        const int e = tid + q * nt;
+        if (e >= k * d) break;
+        const double cnew = cn[e];
         const double df = cnew - cold[q];
         const float c32 = (float)cnew;
         const double rr = (double)c32 - cnew;
         dr[e] = df * df;
         de[e] = rr * rr;
-        cn[e] = cnew;
         P.C64[e] = cnew;
         P.C32[e] = c32;
     }
