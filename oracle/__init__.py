@@ -7,7 +7,8 @@ in the product path imports it.
 ``lloyd`` / ``assign`` / ``update`` wrap plain float64 Lloyd's k-means (no
 pruning) from ``lloyd.c``; ``mti`` wraps the separately written float64 MTI
 reference from ``mti_ref.c``; ``spherical`` wraps float64 spherical k-means
-(cosine proximity on the unit sphere) from ``spherical.c``.  All are compiled
+(cosine proximity on the unit sphere) from ``spherical.c``; ``kmeanspp`` wraps
+k-means++ seeding with caller-drawn uniforms from ``kmeanspp.c``.  All are compiled
 with gcc into ``liboracle.so`` next to this file by :func:`build`.
 """
 from __future__ import annotations
@@ -21,7 +22,8 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liboracle.so")
-SOURCES = [os.path.join(_HERE, "lloyd.c"), os.path.join(_HERE, "mti_ref.c"), os.path.join(_HERE, "spherical.c")]
+SOURCES = [os.path.join(_HERE, "lloyd.c"), os.path.join(_HERE, "mti_ref.c"), os.path.join(_HERE, "spherical.c"),
+           os.path.join(_HERE, "kmeanspp.c")]
 
 _lib = None
 
@@ -63,6 +65,8 @@ def _load():
     lib.mti_lloyd.restype = i32
     lib.oracle_spherical.argtypes = [P, i64, i32, i32, P, i32, f64, P, P, P, P, P, P, P]
     lib.oracle_spherical.restype = i32
+    lib.oracle_kmeanspp.argtypes = [P, i64, i32, i32, P, P, P]
+    lib.oracle_kmeanspp.restype = i32
     _lib = lib
     return lib
 
@@ -217,3 +221,22 @@ def spherical(X: np.ndarray, C0: np.ndarray, max_iters: int, tol: float = 0.0) -
         raise ValueError("oracle_spherical rejected its arguments")
     t = it.value
     return dict(assign=a, C=Cout, iters=t, objective=J[:t], changed=ch[:t], best=b, second=s)
+
+
+def kmeanspp(X: np.ndarray, k: int, u: np.ndarray) -> Dict[str, np.ndarray]:
+    """k-means++ seeding of k rows of X with the uniforms u[0..k-1] in [0, 1).
+
+    Returns ``idx`` (int64[k], seed row indices in draw order), ``C`` (the
+    seed rows, float32[k, d]) and ``D2`` (float64[n], squared distance of each
+    row to its nearest seed).
+    """
+    X = _x(X)
+    n, d = X.shape
+    u = np.ascontiguousarray(u, dtype=np.float64)
+    if u.shape != (int(k),):
+        raise ValueError("u must hold k uniforms")
+    idx = np.empty(int(k), np.int64)
+    D2 = np.empty(n, np.float64)
+    if _load().oracle_kmeanspp(_ptr(X), n, d, int(k), _ptr(u), _ptr(idx), _ptr(D2)) != 0:
+        raise ValueError("oracle_kmeanspp rejected its arguments")
+    return dict(idx=idx, C=X[idx].copy(), D2=D2)
