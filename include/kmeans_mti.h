@@ -47,6 +47,7 @@
 #ifndef KMEANS_MTI_H
 #define KMEANS_MTI_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -184,6 +185,46 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
  * counting sort).  "" for a NULL context.
  */
 const char* kmeans_mti_path(const km_ctx* ctx);
+
+/*
+ * k-means++ seeding (section IV-C, the equation of the D^2 weighting): seed 0
+ * is row min(floor(u[0] * n), n - 1); seed t+1 is row i drawn with probability
+ * D2_i / sum D2, D2_i the squared distance from row i to its nearest seed so
+ * far.  The caller draws the uniforms, so the result is a deterministic
+ * function of (X, k, u):
+ *   - D2 is float64 with the coordinate differences summed in index order by
+ *     fused multiply-add;
+ *   - the draw of seed t+1 uses integer weights w_i = floor(D2_i * 2^S),
+ *     S = 62 - e - ceil(log2 n) with M < 2^e for M = max D2 after the pass
+ *     with seed max(t - 1, 0); W = sum w_i, T = min(floor(u[t+1] * W), W - 1)
+ *     (float64 product), and the seed is the smallest i whose inclusive
+ *     prefix sum of w exceeds T; W = 0 (every row lies on a seed) draws
+ *     min(floor(u[t+1] * n), n - 1).
+ * A pass skips row i when its nearest seed a satisfies
+ * ||c_a - c_new||^2 >= 4 D2_i (with rounding margins): exact, since such a
+ * seed cannot be nearer (KM_PP_NO_PRUNE computes every distance; same
+ * results).
+ *
+ * X: device, n x d float32 rows (finite; non-finite rows give unspecified
+ * seeds).  u: HOST, k doubles in [0, 1), read before the call returns.
+ * C_out: device, k x d float32, receives the seed rows in draw order.
+ * idx_out: device int64[k] (nullable), the seed row indices.  d2_out: device
+ * float64[n] (nullable), each row's squared distance to its nearest seed.
+ * workspace: device, at least kmeans_pp_workspace_bytes(n, d, k) bytes,
+ * 256-byte aligned, owned by the caller; its contents on entry do not matter
+ * and it must not be used by another call until this one's work completes.
+ * Requires 1 <= k <= n, d >= 1.  Work is ordered on hip_stream (NULL = null
+ * stream) with 2k + 1 kernel launches and no allocation; asynchronous unless
+ * computed_out (HOST, nullable) is given, in which case it synchronizes and
+ * stores the number of point-seed distances computed.  Errors:
+ * KM_ERR_INVALID_ARG for bad sizes or pointers, a u outside [0, 1), unknown
+ * flags or a short or misaligned workspace; KM_ERR_HIP on a launch failure.
+ */
+enum { KM_PP_NO_PRUNE = 1u };
+size_t kmeans_pp_workspace_bytes(int64_t n, int32_t d, int32_t k);   /* 0 for bad sizes */
+int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double* u, float* C_out,
+                   int64_t* idx_out, double* d2_out, void* workspace, size_t workspace_bytes,
+                   uint32_t flags, void* hip_stream, int64_t* computed_out);
 
 /* Release a context and its device scratch.  NULL-safe.  Synchronizes. */
 void kmeans_mti_destroy(km_ctx* ctx);

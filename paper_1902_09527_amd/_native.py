@@ -28,12 +28,15 @@ KM_FLAG_GENERIC = 64
 KM_FLAG_FULL_SUMS = 128
 KM_FLAG_SPHERICAL = 256
 
+KM_PP_NO_PRUNE = 1
+
 #: Every symbol include/kmeans_mti.h declares.
 EXPORTS = (
     "kmeans_mti_init", "kmeans_mti_iterate", "kmeans_mti_get", "kmeans_mti_get_centroids64",
     "kmeans_mti_get_stats", "kmeans_mti_get_history", "kmeans_mti_get_timing", "kmeans_mti_run",
     "kmeans_mti_path", "kmeans_mti_destroy",
     "kmeans_mti_strerror", "kmeans_mti_last_hip_error",
+    "kmeans_pp_workspace_bytes", "kmeans_pp_seed",
 )
 
 
@@ -98,6 +101,10 @@ def load() -> C.CDLL:
     lib.kmeans_mti_destroy.restype = None
     lib.kmeans_mti_strerror.argtypes = [C.c_int]
     lib.kmeans_mti_strerror.restype = C.c_char_p
+    lib.kmeans_pp_workspace_bytes.argtypes = [i64, i32, i32]
+    lib.kmeans_pp_workspace_bytes.restype = C.c_size_t
+    lib.kmeans_pp_seed.argtypes = [P, i64, i32, i32, P, P, P, P, P, C.c_size_t, u32, P, C.POINTER(i64)]
+    lib.kmeans_pp_seed.restype = C.c_int
     lib.kmeans_mti_last_hip_error.argtypes = []
     lib.kmeans_mti_last_hip_error.restype = C.c_char_p
     _lib = lib

@@ -18,7 +18,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libkmeans_mti.so")
 SOURCES = [os.path.join(CSRC, "km_kernels.hip"), os.path.join(CSRC, "km_large.hip"),
-           os.path.join(CSRC, "km_small.hip"), os.path.join(CSRC, "km_capi.hip")]
+           os.path.join(CSRC, "km_small.hip"), os.path.join(CSRC, "km_pp.hip"),
+           os.path.join(CSRC, "km_capi.hip")]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

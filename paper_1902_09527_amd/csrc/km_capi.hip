@@ -427,6 +427,28 @@ int check_shape(const float* X, int64_t n, int32_t d, int32_t k, const float* C0
     return KM_OK;
 }
 
+// Workspace of kmeans_pp_seed: 256-byte aligned segments.
+struct PPLayout {
+    size_t d2, a, bs, mb, dcc, cnt, u, idx, total;
+};
+
+PPLayout pp_layout(int64_t n, int32_t k) {
+    auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
+    const size_t G = (size_t)((n + km::kPPChunk - 1) / km::kPPChunk);
+    PPLayout L{};
+    size_t o = 0;
+    L.d2 = o;  o += up((size_t)n * 8);
+    L.a = o;   o += up((size_t)n * 4);
+    L.bs = o;  o += up(G * 8);
+    L.mb = o;  o += up((size_t)k * 8);
+    L.dcc = o; o += up((size_t)k * 8);
+    L.cnt = o; o += up((size_t)k * 8);
+    L.u = o;   o += up((size_t)k * 8);
+    L.idx = o; o += up((size_t)k * 8);
+    L.total = o;
+    return L;
+}
+
 }  // namespace
 
 extern "C" {
@@ -656,6 +678,80 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
     cleanup();
     return KM_OK;
 #undef RUN_HIP
+}
+
+size_t kmeans_pp_workspace_bytes(int64_t n, int32_t d, int32_t k) {
+    if (n < 1 || d < 1 || k < 1 || k > n || n > INT64_MAX / 16 / d) return 0;
+    return pp_layout(n, k).total;
+}
+
+int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double* u, float* C_out,
+                   int64_t* idx_out, double* d2_out, void* workspace, size_t workspace_bytes, uint32_t flags,
+                   void* hip_stream, int64_t* computed_out) {
+    if (!X || !u || !C_out || !workspace || n < 1 || d < 1 || k < 1 || k > n || n > INT64_MAX / 16 / d)
+        return KM_ERR_INVALID_ARG;
+    if (flags & ~(uint32_t)KM_PP_NO_PRUNE) return KM_ERR_INVALID_ARG;
+    if ((n + km::kPPChunk - 1) / km::kPPChunk > INT_MAX) return KM_ERR_INVALID_ARG;
+    for (int32_t t = 0; t < k; ++t)
+        if (!(u[t] >= 0.0 && u[t] < 1.0)) {
+            snprintf(g_last_hip, sizeof g_last_hip, "u[%d] is not in [0, 1)", (int)t);
+            return KM_ERR_INVALID_ARG;
+        }
+    const PPLayout L = pp_layout(n, k);
+    if (workspace_bytes < L.total || ((uintptr_t)workspace & 255)) {
+        snprintf(g_last_hip, sizeof g_last_hip, "workspace: %zu bytes, 256-byte aligned, needed", L.total);
+        return KM_ERR_INVALID_ARG;
+    }
+    int dev = 0, rc;
+    KM_HIP(hipGetDevice(&dev));
+    if ((rc = check_device_range(X, (size_t)n * d * 4, dev, "X")) != KM_OK) return rc;
+    if ((rc = check_device_range(C_out, (size_t)k * d * 4, dev, "C_out")) != KM_OK) return rc;
+    if ((rc = check_device_range(workspace, L.total, dev, "workspace")) != KM_OK) return rc;
+    if (idx_out && (rc = check_device_range(idx_out, (size_t)k * 8, dev, "idx_out")) != KM_OK) return rc;
+    if (d2_out && (rc = check_device_range(d2_out, (size_t)n * 8, dev, "d2_out")) != KM_OK) return rc;
+    hipStream_t st = static_cast<hipStream_t>(hip_stream);
+    char* ws = static_cast<char*>(workspace);
+
+    km::PPArgs P{};
+    P.X = X;
+    P.n = n;
+    P.d = d;
+    P.k = k;
+    P.C = C_out;
+    P.idx = reinterpret_cast<int64_t*>(ws + L.idx);
+    P.u = reinterpret_cast<const double*>(ws + L.u);
+    P.D2 = reinterpret_cast<double*>(ws + L.d2);
+    P.A = reinterpret_cast<int32_t*>(ws + L.a);
+    P.bs = reinterpret_cast<uint64_t*>(ws + L.bs);
+    P.Mb = reinterpret_cast<uint64_t*>(ws + L.mb);
+    P.dcc = reinterpret_cast<double*>(ws + L.dcc);
+    P.cnt = computed_out ? reinterpret_cast<uint64_t*>(ws + L.cnt) : nullptr;
+    P.G = (int32_t)((n + km::kPPChunk - 1) / km::kPPChunk);
+    P.L = ceil_log2_u64((uint64_t)n);
+    P.prune = (flags & KM_PP_NO_PRUNE) ? 0 : 1;
+    const bool vec4 = d % 4 == 0 && ((uintptr_t)X & 15) == 0 && ((uintptr_t)C_out & 15) == 0;
+
+    int64_t i0 = (int64_t)(u[0] * (double)n);   // first seed: uniform
+    if (i0 > n - 1) i0 = n - 1;
+    KM_HIP(hipMemcpyAsync(ws + L.u, u, (size_t)k * 8, hipMemcpyHostToDevice, st));
+    KM_HIP(km::launch_pp_seed(P, i0, vec4, st));
+    if (idx_out) KM_HIP(hipMemcpyAsync(idx_out, P.idx, (size_t)k * 8, hipMemcpyDeviceToDevice, st));
+    if (d2_out) KM_HIP(hipMemcpyAsync(d2_out, P.D2, (size_t)n * 8, hipMemcpyDeviceToDevice, st));
+    if (computed_out) {
+        uint64_t* h = new (std::nothrow) uint64_t[k];
+        if (!h) return KM_ERR_OOM;
+        hipError_t e = hipMemcpyAsync(h, P.cnt, (size_t)k * 8, hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess) {
+            delete[] h;
+            return hip_fail(e, "kmeans_pp_seed counters");
+        }
+        int64_t tot = 0;
+        for (int32_t t = 0; t < k; ++t) tot += (int64_t)h[t];
+        delete[] h;
+        *computed_out = tot;
+    }
+    return KM_OK;
 }
 
 const char* kmeans_mti_path(const km_ctx* ctx) {

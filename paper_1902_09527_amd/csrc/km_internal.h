@@ -287,4 +287,30 @@ int assign_variant(int d, int k, bool aligned, bool vector_only);
 // Kernel symbol of an assignment-kernel variant (for occupancy queries).
 const void* assign_kernel_symbol(int variant);
 
+
+// k-means++ seeding (km_pp.hip).  Points are processed in chunks of
+// kPPChunk rows, one workgroup per chunk; the block weight sums are per chunk.
+constexpr int kPPChunk = 2048;
+
+struct PPArgs {
+    const float* X;       // n x d rows
+    int64_t n;
+    int32_t d, k;
+    float* C;             // k x d seed rows (output)
+    int64_t* idx;         // k seed indices
+    const double* u;      // k uniforms in [0, 1)
+    double* D2;           // n: squared distance to the nearest seed so far
+    int32_t* A;           // n: index of that seed (pruning only)
+    uint64_t* bs;         // G: block weight sums of the next draw
+    uint64_t* Mb;         // k: bits of max D2 after the pass with seed t
+    double* dcc;          // k: lower bounds of ||c_a - c_new||^2 (pruning only)
+    uint64_t* cnt;        // k: distances computed per pass, or null
+    int32_t G;            // chunks = ceil(n / kPPChunk)
+    int32_t L;            // smallest L with n <= 2^L
+    int32_t prune;        // 1: triangle-inequality skip test
+};
+
+// Enqueues the whole seeding (2k + 1 launches).  i0 = first seed index.
+hipError_t launch_pp_seed(const PPArgs& P, int64_t i0, bool vec4, hipStream_t s);
+
 }  // namespace km

@@ -198,3 +198,81 @@ def run(X: torch.Tensor, C0: torch.Tensor, max_iters: int, tol: float = 0.0, pru
                                 C.byref(s))
     N.check(st, "kmeans_mti_run")
     return a, c, s.as_dict()
+
+
+def kmeanspp(X: torch.Tensor, k: int, u, prune: bool = True, count: bool = False,
+             workspace: Optional[torch.Tensor] = None, stream: Optional[torch.cuda.Stream] = None
+             ) -> Dict[str, object]:
+    """k-means++ seeding (kmeans_pp_seed) of k rows of X with the uniforms u.
+
+    u: k floats in [0, 1) (host).  Returns ``C`` (float32 [k, d], the seed
+    rows in draw order), ``idx`` (int64 [k]) and ``D2`` (float64 [n], squared
+    distance of each row to its nearest seed), all on X's device, and with
+    ``count`` also ``computed`` (point-seed distances evaluated; synchronizes).
+    ``workspace``: optional uint8 device tensor of at least
+    :func:`kmeanspp_workspace_bytes` bytes, reused across calls.
+    """
+    _check_matrix(X, "X")
+    lib = N.load()
+    n, d = X.shape
+    k = int(k)
+    uu = np.ascontiguousarray(np.asarray(u, dtype=np.float64).reshape(-1))
+    if uu.shape != (k,):
+        raise ValueError("u must hold k = %d uniforms" % k)
+    need = int(lib.kmeans_pp_workspace_bytes(n, d, k))
+    if need == 0:
+        raise N.KMError(N.KM_ERR_INVALID_ARG, "kmeans_pp_workspace_bytes")
+    if workspace is None:
+        workspace = torch.empty(need + 256, dtype=torch.uint8, device=X.device)
+    if workspace.device != X.device or workspace.dtype != torch.uint8 or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 tensor on X's device")
+    off = (-workspace.data_ptr()) % 256
+    if workspace.numel() - off < need:
+        raise ValueError("workspace needs %d bytes (256-byte aligned)" % need)
+    c = torch.empty(k, d, dtype=torch.float32, device=X.device)
+    idx = torch.empty(k, dtype=torch.int64, device=X.device)
+    d2 = torch.empty(n, dtype=torch.float64, device=X.device)
+    comp = C.c_int64(0)
+    with torch.cuda.device(X.device):
+        st = lib.kmeans_pp_seed(C.c_void_p(X.data_ptr()), n, d, k, uu.ctypes.data_as(C.c_void_p),
+                                C.c_void_p(c.data_ptr()), C.c_void_p(idx.data_ptr()),
+                                C.c_void_p(d2.data_ptr()), C.c_void_p(workspace.data_ptr() + off),
+                                workspace.numel() - off, 0 if prune else N.KM_PP_NO_PRUNE,
+                                _stream_ptr(X.device, stream), C.byref(comp) if count else None)
+    N.check(st, "kmeans_pp_seed")
+    out = {"C": c, "idx": idx, "D2": d2}
+    if count:
+        out["computed"] = int(comp.value)
+    return out
+
+
+def kmeanspp_workspace_bytes(n: int, d: int, k: int) -> int:
+    """Bytes of workspace kmeans_pp_seed needs (plus up to 255 for alignment)."""
+    return int(N.load().kmeans_pp_workspace_bytes(int(n), int(d), int(k)))
+
+
+def run_pp_best(X: torch.Tensor, k: int, U, max_iters: int, tol: float = 0.0, prune: bool = True,
+                stream: Optional[torch.cuda.Stream] = None) -> Dict[str, object]:
+    """The paper's k-means++ with r restarts: for each row of U (r x k
+    uniforms) seed with k-means++, run k-means from the seeds, and keep the
+    run with the least final inertia (ties: the earlier run).
+
+    Returns ``best`` (the run index), ``assign``, ``C``, ``stats`` of that run
+    and ``inertia`` (every run's final inertia).
+    """
+    U = np.asarray(U, dtype=np.float64)
+    if U.ndim != 2 or U.shape[1] != int(k):
+        raise ValueError("U must be r x k")
+    best = None
+    inertia = []
+    ws = None
+    for r in range(U.shape[0]):
+        if ws is None:
+            ws = torch.empty(kmeanspp_workspace_bytes(X.shape[0], X.shape[1], k) + 256, dtype=torch.uint8,
+                             device=X.device)
+        seeds = kmeanspp(X, k, U[r], prune=prune, workspace=ws, stream=stream)
+        a, c, st = run(X, seeds["C"], max_iters, tol, prune=prune, stats=True, stream=stream)
+        inertia.append(st["inertia_last"])
+        if best is None or st["inertia_last"] < best[3]["inertia_last"]:
+            best = (r, a, c, st)
+    return {"best": best[0], "assign": best[1], "C": best[2], "stats": best[3], "inertia": inertia}

@@ -17,7 +17,7 @@ HEADER = os.path.join(ROOT, "include", "kmeans_mti.h")
 def _declared():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(kmeans_mti_\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(kmeans_(?:mti|pp)_\w+)\s*\(", text)))
 
 
 def test_header_declares_the_binding_exports():
@@ -89,6 +89,33 @@ def test_run_rejects_bad_arguments_without_a_device():
     assert call(c=None) == N.KM_ERR_INVALID_ARG
     assert call(k=11) == N.KM_ERR_INVALID_ARG
     assert call(X=None) == N.KM_ERR_INVALID_ARG
+
+
+def test_pp_seed_rejects_bad_arguments_without_a_device():
+    lib = N.load()
+    fake = C.c_void_p(0x1000)
+    need = lib.kmeans_pp_workspace_bytes(10, 2, 3)
+    assert need > 10 * 12
+    assert lib.kmeans_pp_workspace_bytes(10, 2, 11) == 0
+    assert lib.kmeans_pp_workspace_bytes(0, 2, 1) == 0
+    good = dict(X=fake, n=10, d=2, k=3, u=[0.1, 0.5, 0.9], C=fake, ws=fake, wsb=need, flags=0)
+
+    def call(**kw):
+        a = dict(good, **kw)
+        u = (C.c_double * len(a["u"]))(*a["u"])
+        return lib.kmeans_pp_seed(a["X"], a["n"], a["d"], a["k"], u, a["C"], None, None, a["ws"], a["wsb"],
+                                  a["flags"], None, None)
+
+    assert call(k=11, u=[0.5] * 11) == N.KM_ERR_INVALID_ARG
+    assert call(k=0, u=[0.5]) == N.KM_ERR_INVALID_ARG
+    assert call(X=None) == N.KM_ERR_INVALID_ARG
+    assert call(C=None) == N.KM_ERR_INVALID_ARG
+    assert call(u=[0.1, 1.0, 0.2]) == N.KM_ERR_INVALID_ARG
+    assert call(u=[0.1, -0.5, 0.2]) == N.KM_ERR_INVALID_ARG
+    assert call(u=[0.1, math.nan, 0.2]) == N.KM_ERR_INVALID_ARG
+    assert call(flags=2) == N.KM_ERR_INVALID_ARG
+    assert call(wsb=need - 1) == N.KM_ERR_INVALID_ARG
+    assert call(ws=C.c_void_p(0x1008)) == N.KM_ERR_INVALID_ARG
 
 
 def test_null_context_calls():
