@@ -11,6 +11,7 @@ second.  Per-kernel device times come from HIP events recorded by the
 library on its stream around every launch.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--spherical] [--no-cpu-baseline]
+    python bench.py --kmeanspp [--workload NAME]      (k-means++ seeding)
 """
 from __future__ import annotations
 
@@ -44,6 +45,7 @@ KERNEL_SOURCES = {
     "k_inc": ["km_small.hip", "km_device.h", "km_internal.h"],
     "k_assign": ["km_kernels.hip", "km_device.h", "km_internal.h"],
     "k_mfma_large": ["km_large.hip", "km_device.h", "km_internal.h"],
+    "k_pp_step": ["km_pp.hip", "km_device.h", "km_internal.h"],
 }
 
 
@@ -121,6 +123,79 @@ def cpu_baseline(X, C0, w, budget_s: float = 15.0, spherical: bool = False) -> d
     }
 
 
+def bench_kmeanspp(args, w, X) -> dict:
+    """k-means++ seeding of the workload's k seeds: a step is one whole
+    seeding (k passes over the points and k - 1 draws)."""
+    import numpy as np
+    import torch
+
+    import paper_1902_09527_amd as km
+
+    n, d, k = w.n, w.d, w.k
+    K = args.steps or 5
+    Xg = torch.from_numpy(X).to("cuda:0")
+    ws = torch.empty(km.kmeanspp_workspace_bytes(n, d, k) + 256, dtype=torch.uint8, device="cuda:0")
+    U = np.random.default_rng(20190225).random((args.warmup + K + 1, k))
+    for r in range(args.warmup):
+        km.kmeanspp(Xg, k, U[r], workspace=ws)
+    torch.cuda.synchronize()
+    log("warmup done (%d seedings)" % args.warmup)
+    t0 = time.perf_counter()
+    for r in range(K):
+        km.kmeanspp(Xg, k, U[args.warmup + r], workspace=ws)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    log("timed %d seedings in %.3f ms" % (K, elapsed * 1e3))
+    tm = km.kmeanspp(Xg, k, U[-1], workspace=ws, timing=True)["stats"]
+    G = (n + 2047) // 2048
+    roof = {"kernel": "k_pp_step", "bound": "hbm", "achieved": None, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": None, "traffic": None}
+    if k > 1 and tm["later_pass_ms"] > 0:
+        # Passes 2..k: D2 and the nearest-seed index of every row read (12 B),
+        # the block weight sum written (8 B per 2048 rows), a surviving row
+        # read (4d B) and an improved row's D2 and index written (12 B).
+        bytes_later = (k - 1) * (12.0 * n + 8.0 * G) + 4.0 * d * (tm["computed"] - n) + 12.0 * tm["improved"]
+        roof = roofline_entry("k_pp_step", w.name + "-kmeanspp", bytes_later / (k - 1),
+                              tm["later_pass_ms"] / (k - 1),
+                              "passes 2..k: 12n (D2, nearest seed) + 8 per block sum + 4d per survivor row "
+                              "+ 12 per improved row")
+    result = {
+        "metric": "k-means++ seedings/s (k seeds each)",
+        "value": K / elapsed,
+        "unit": "seedings/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": w.name, "method": "kmeans++ seeding", "n": n, "d": d, "k": k,
+                   "timed": "%d seedings with seeded uniforms" % K},
+        "seeds_per_s": k * K / elapsed,
+        "dist_computed_frac": tm["computed"] / float(n * k),
+        "kernel_ms_per_step": {"passes": tm["pass_ms"], "draws": tm["draw_ms"]},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        log("cpu baseline (oracle) ...")
+        t0 = time.perf_counter()
+        oracle.kmeanspp(X, 1, U[-1][:1])
+        t1 = time.perf_counter() - t0
+        kk = int(max(1, min(k, 15.0 // max(t1, 1e-3))))
+        t0 = time.perf_counter()
+        oracle.kmeanspp(X, kk, U[-1][:kk])
+        el = time.perf_counter() - t0
+        result["cpu_baseline"] = {
+            "value": kk / (el * k), "unit": "seedings/s", "cores": oracle.get_threads(), "kind": "oracle",
+            "sample": "all %d rows of %s, the first %d of the %d draws (one pass each), scaled to k" % (
+                n, w.name, kk, k)}
+    return result
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -135,6 +210,8 @@ def main() -> int:
     ap.add_argument("--spherical", action="store_true",
                     help="spherical k-means on the same workload (KM_FLAG_SPHERICAL: rows and "
                          "centroids on the unit sphere, cosine assignment)")
+    ap.add_argument("--kmeanspp", action="store_true",
+                    help="time k-means++ seeding of the workload's k seeds instead of the k-means steps")
     ap.add_argument("--profile", action="store_true",
                     help="run only the warmup and the timed region (no event pass, no job run, no "
                          "CPU leg), so a profiler sees warmup + K launches of each kernel")
@@ -168,6 +245,9 @@ def main() -> int:
     K = args.steps or w.max_iters
     log("workload %s: n=%d d=%d k=%d; generating" % (w.name, w.n, w.d, w.k))
     X, C0, _ = synth.make(w.name)
+    if args.kmeanspp:
+        print(json.dumps(bench_kmeanspp(args, w, X)), flush=True)
+        return 0
     dev = torch.device("cuda:0")
     Xg = torch.from_numpy(X).to(dev)
     Cg = torch.from_numpy(C0).to(dev)

@@ -214,17 +214,31 @@ const char* kmeans_mti_path(const km_ctx* ctx);
  * 256-byte aligned, owned by the caller; its contents on entry do not matter
  * and it must not be used by another call until this one's work completes.
  * Requires 1 <= k <= n, d >= 1.  Work is ordered on hip_stream (NULL = null
- * stream) with 2k + 1 kernel launches and no allocation; asynchronous unless
- * computed_out (HOST, nullable) is given, in which case it synchronizes and
- * stores the number of point-seed distances computed.  Errors:
- * KM_ERR_INVALID_ARG for bad sizes or pointers, a u outside [0, 1), unknown
- * flags or a short or misaligned workspace; KM_ERR_HIP on a launch failure.
+ * stream) with at most 3k kernel launches and no allocation; asynchronous unless
+ * stats (HOST, nullable) is given, in which case it synchronizes and fills
+ * it.  Errors: KM_ERR_INVALID_ARG for bad sizes or pointers, a u outside
+ * [0, 1), unknown flags or a short or misaligned workspace; KM_ERR_HIP on a
+ * launch failure.
  */
-enum { KM_PP_NO_PRUNE = 1u };
+enum {
+    KM_PP_NO_PRUNE = 1u,   /* compute every point-seed distance (same results) */
+    KM_PP_TIMING = 2u      /* with stats: HIP events around every launch */
+};
+
+typedef struct {
+    int64_t computed;      /* point-seed distances evaluated over all passes */
+    int64_t improved;      /* rows whose D2 decreased, summed over the passes after the first */
+    int32_t passes;        /* passes over the points (k) */
+    int32_t pad_;
+    double pass_ms;        /* KM_PP_TIMING: device time of the k passes (k_pp_step), else 0 */
+    double later_pass_ms;  /* KM_PP_TIMING: of passes 2..k only */
+    double draw_ms;        /* KM_PP_TIMING: set-up, first weights, the k - 1 draws and seed tables */
+} km_pp_stats;
+
 size_t kmeans_pp_workspace_bytes(int64_t n, int32_t d, int32_t k);   /* 0 for bad sizes */
 int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double* u, float* C_out,
                    int64_t* idx_out, double* d2_out, void* workspace, size_t workspace_bytes,
-                   uint32_t flags, void* hip_stream, int64_t* computed_out);
+                   uint32_t flags, void* hip_stream, km_pp_stats* stats);
 
 /* Release a context and its device scratch.  NULL-safe.  Synchronizes. */
 void kmeans_mti_destroy(km_ctx* ctx);

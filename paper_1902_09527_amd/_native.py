@@ -29,6 +29,7 @@ KM_FLAG_FULL_SUMS = 128
 KM_FLAG_SPHERICAL = 256
 
 KM_PP_NO_PRUNE = 1
+KM_PP_TIMING = 2
 
 #: Every symbol include/kmeans_mti.h declares.
 EXPORTS = (
@@ -55,6 +56,21 @@ class KmStats(C.Structure):
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class KmPPStats(C.Structure):
+    _fields_ = [
+        ("computed", C.c_int64),
+        ("improved", C.c_int64),
+        ("passes", C.c_int32),
+        ("pad_", C.c_int32),
+        ("pass_ms", C.c_double),
+        ("later_pass_ms", C.c_double),
+        ("draw_ms", C.c_double),
+    ]
+
+    def as_dict(self) -> dict:
+        return {name: getattr(self, name) for name, _ in self._fields_ if name != "pad_"}
 
 
 class KMError(RuntimeError):
@@ -103,7 +119,7 @@ def load() -> C.CDLL:
     lib.kmeans_mti_strerror.restype = C.c_char_p
     lib.kmeans_pp_workspace_bytes.argtypes = [i64, i32, i32]
     lib.kmeans_pp_workspace_bytes.restype = C.c_size_t
-    lib.kmeans_pp_seed.argtypes = [P, i64, i32, i32, P, P, P, P, P, C.c_size_t, u32, P, C.POINTER(i64)]
+    lib.kmeans_pp_seed.argtypes = [P, i64, i32, i32, P, P, P, P, P, C.c_size_t, u32, P, C.POINTER(KmPPStats)]
     lib.kmeans_pp_seed.restype = C.c_int
     lib.kmeans_mti_last_hip_error.argtypes = []
     lib.kmeans_mti_last_hip_error.restype = C.c_char_p

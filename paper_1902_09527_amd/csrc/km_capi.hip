@@ -442,7 +442,7 @@ PPLayout pp_layout(int64_t n, int32_t k) {
     L.bs = o;  o += up(G * 8);
     L.mb = o;  o += up((size_t)k * 8);
     L.dcc = o; o += up((size_t)k * 8);
-    L.cnt = o; o += up((size_t)k * 8);
+    L.cnt = o; o += up((size_t)k * 16);
     L.u = o;   o += up((size_t)k * 8);
     L.idx = o; o += up((size_t)k * 8);
     L.total = o;
@@ -687,10 +687,10 @@ size_t kmeans_pp_workspace_bytes(int64_t n, int32_t d, int32_t k) {
 
 int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double* u, float* C_out,
                    int64_t* idx_out, double* d2_out, void* workspace, size_t workspace_bytes, uint32_t flags,
-                   void* hip_stream, int64_t* computed_out) {
+                   void* hip_stream, km_pp_stats* stats) {
     if (!X || !u || !C_out || !workspace || n < 1 || d < 1 || k < 1 || k > n || n > INT64_MAX / 16 / d)
         return KM_ERR_INVALID_ARG;
-    if (flags & ~(uint32_t)KM_PP_NO_PRUNE) return KM_ERR_INVALID_ARG;
+    if (flags & ~(uint32_t)(KM_PP_NO_PRUNE | KM_PP_TIMING)) return KM_ERR_INVALID_ARG;
     if ((n + km::kPPChunk - 1) / km::kPPChunk > INT_MAX) return KM_ERR_INVALID_ARG;
     for (int32_t t = 0; t < k; ++t)
         if (!(u[t] >= 0.0 && u[t] < 1.0)) {
@@ -725,32 +725,62 @@ int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double
     P.bs = reinterpret_cast<uint64_t*>(ws + L.bs);
     P.Mb = reinterpret_cast<uint64_t*>(ws + L.mb);
     P.dcc = reinterpret_cast<double*>(ws + L.dcc);
-    P.cnt = computed_out ? reinterpret_cast<uint64_t*>(ws + L.cnt) : nullptr;
+    P.cnt = stats ? reinterpret_cast<uint64_t*>(ws + L.cnt) : nullptr;
     P.G = (int32_t)((n + km::kPPChunk - 1) / km::kPPChunk);
     P.L = ceil_log2_u64((uint64_t)n);
     P.prune = (flags & KM_PP_NO_PRUNE) ? 0 : 1;
     const bool vec4 = d % 4 == 0 && ((uintptr_t)X & 15) == 0 && ((uintptr_t)C_out & 15) == 0;
+    const int vw = vec4 ? (d % 32 == 0 && d >= 64 ? 2 : 1) : 0;
 
     int64_t i0 = (int64_t)(u[0] * (double)n);   // first seed: uniform
     if (i0 > n - 1) i0 = n - 1;
     KM_HIP(hipMemcpyAsync(ws + L.u, u, (size_t)k * 8, hipMemcpyHostToDevice, st));
-    KM_HIP(km::launch_pp_seed(P, i0, vec4, st));
-    if (idx_out) KM_HIP(hipMemcpyAsync(idx_out, P.idx, (size_t)k * 8, hipMemcpyDeviceToDevice, st));
-    if (d2_out) KM_HIP(hipMemcpyAsync(d2_out, P.D2, (size_t)n * 8, hipMemcpyDeviceToDevice, st));
-    if (computed_out) {
-        uint64_t* h = new (std::nothrow) uint64_t[k];
-        if (!h) return KM_ERR_OOM;
-        hipError_t e = hipMemcpyAsync(h, P.cnt, (size_t)k * 8, hipMemcpyDeviceToHost, st);
-        if (e == hipSuccess) e = hipStreamSynchronize(st);
-        if (e != hipSuccess) {
-            delete[] h;
-            return hip_fail(e, "kmeans_pp_seed counters");
-        }
-        int64_t tot = 0;
-        for (int32_t t = 0; t < k; ++t) tot += (int64_t)h[t];
-        delete[] h;
-        *computed_out = tot;
+    if (!stats) {
+        KM_HIP(km::launch_pp_seed(P, i0, vw, nullptr, nullptr, st));
+        if (idx_out) KM_HIP(hipMemcpyAsync(idx_out, P.idx, (size_t)k * 8, hipMemcpyDeviceToDevice, st));
+        if (d2_out) KM_HIP(hipMemcpyAsync(d2_out, P.D2, (size_t)n * 8, hipMemcpyDeviceToDevice, st));
+        return KM_OK;
     }
+    // With stats: counters (and with KM_PP_TIMING events around every
+    // launch), then one synchronisation.  Host memory released on every path.
+    const int nev = (flags & KM_PP_TIMING) ? km::pp_launches(k, d, P.prune != 0) + 1 : 0;
+    hipEvent_t* ev = nev ? new (std::nothrow) hipEvent_t[nev]() : nullptr;
+    int8_t* kind = nev ? new (std::nothrow) int8_t[nev]() : nullptr;
+    uint64_t* h = new (std::nothrow) uint64_t[2 * (size_t)k];
+    auto release = [&]() {
+        for (int j = 0; ev && j < nev; ++j)
+            if (ev[j]) (void)hipEventDestroy(ev[j]);
+        delete[] ev;
+        delete[] kind;
+        delete[] h;
+    };
+    if (!h || (nev && (!ev || !kind))) {
+        release();
+        return KM_ERR_OOM;
+    }
+    hipError_t e = hipSuccess;
+    for (int j = 0; j < nev && e == hipSuccess; ++j) e = hipEventCreate(&ev[j]);
+    if (e == hipSuccess) e = km::launch_pp_seed(P, i0, vw, ev, kind, st);
+    if (e == hipSuccess && idx_out) e = hipMemcpyAsync(idx_out, P.idx, (size_t)k * 8, hipMemcpyDeviceToDevice, st);
+    if (e == hipSuccess && d2_out) e = hipMemcpyAsync(d2_out, P.D2, (size_t)n * 8, hipMemcpyDeviceToDevice, st);
+    if (e == hipSuccess) e = hipMemcpyAsync(h, P.cnt, (size_t)k * 16, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    km_pp_stats out{};
+    out.passes = k;
+    for (int32_t t = 0; t < k && e == hipSuccess; ++t) {
+        out.computed += (int64_t)h[2 * t];
+        if (t > 0) out.improved += (int64_t)h[2 * t + 1];
+    }
+    for (int j = 0; j + 1 < nev && e == hipSuccess; ++j) {
+        float ms = 0.f;
+        e = hipEventElapsedTime(&ms, ev[j], ev[j + 1]);
+        if (kind[j] != 2) out.pass_ms += ms;
+        if (kind[j] == 1) out.later_pass_ms += ms;
+        if (kind[j] == 2) out.draw_ms += ms;
+    }
+    release();
+    if (e != hipSuccess) return hip_fail(e, "kmeans_pp_seed");
+    *stats = out;
     return KM_OK;
 }
 

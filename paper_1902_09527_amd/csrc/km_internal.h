@@ -304,13 +304,20 @@ struct PPArgs {
     uint64_t* bs;         // G: block weight sums of the next draw
     uint64_t* Mb;         // k: bits of max D2 after the pass with seed t
     double* dcc;          // k: lower bounds of ||c_a - c_new||^2 (pruning only)
-    uint64_t* cnt;        // k: distances computed per pass, or null
+    uint64_t* cnt;        // 2k: distances computed and rows improved per pass, or null
     int32_t G;            // chunks = ceil(n / kPPChunk)
     int32_t L;            // smallest L with n <= 2^L
     int32_t prune;        // 1: triangle-inequality skip test
 };
 
-// Enqueues the whole seeding (2k + 1 launches).  i0 = first seed index.
-hipError_t launch_pp_seed(const PPArgs& P, int64_t i0, bool vec4, hipStream_t s);
+// Kernel launches of one seeding.
+int pp_launches(int k, int d, bool prune);
+// Enqueues the whole seeding.  i0 = first seed index.  ev (nullable):
+// pp_launches + 1 events, recorded before the first launch and after every
+// launch; kind[j] (with ev) = 0 for the first pass, 1 for a later pass and 2
+// for the other kernels, per launch j.
+// vw: row loads, 0 scalar, 1 16-byte (d % 4 == 0, 16-byte aligned rows), 2 the
+// same with whole 128-byte lines per step (d % 32 == 0).
+hipError_t launch_pp_seed(const PPArgs& P, int64_t i0, int vw, hipEvent_t* ev, int8_t* kind, hipStream_t s);
 
 }  // namespace km

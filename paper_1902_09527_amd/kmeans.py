@@ -200,7 +200,7 @@ def run(X: torch.Tensor, C0: torch.Tensor, max_iters: int, tol: float = 0.0, pru
     return a, c, s.as_dict()
 
 
-def kmeanspp(X: torch.Tensor, k: int, u, prune: bool = True, count: bool = False,
+def kmeanspp(X: torch.Tensor, k: int, u, prune: bool = True, count: bool = False, timing: bool = False,
              workspace: Optional[torch.Tensor] = None, stream: Optional[torch.cuda.Stream] = None
              ) -> Dict[str, object]:
     """k-means++ seeding (kmeans_pp_seed) of k rows of X with the uniforms u.
@@ -208,7 +208,9 @@ def kmeanspp(X: torch.Tensor, k: int, u, prune: bool = True, count: bool = False
     u: k floats in [0, 1) (host).  Returns ``C`` (float32 [k, d], the seed
     rows in draw order), ``idx`` (int64 [k]) and ``D2`` (float64 [n], squared
     distance of each row to its nearest seed), all on X's device, and with
-    ``count`` also ``computed`` (point-seed distances evaluated; synchronizes).
+    ``count`` or ``timing`` also ``stats`` (km_pp_stats as a dict: distances
+    computed, rows improved, and with ``timing`` the device milliseconds of
+    the passes and the draws; synchronizes).
     ``workspace``: optional uint8 device tensor of at least
     :func:`kmeanspp_workspace_bytes` bytes, reused across calls.
     """
@@ -232,17 +234,18 @@ def kmeanspp(X: torch.Tensor, k: int, u, prune: bool = True, count: bool = False
     c = torch.empty(k, d, dtype=torch.float32, device=X.device)
     idx = torch.empty(k, dtype=torch.int64, device=X.device)
     d2 = torch.empty(n, dtype=torch.float64, device=X.device)
-    comp = C.c_int64(0)
+    ps = N.KmPPStats()
+    flags = (0 if prune else N.KM_PP_NO_PRUNE) | (N.KM_PP_TIMING if timing else 0)
     with torch.cuda.device(X.device):
         st = lib.kmeans_pp_seed(C.c_void_p(X.data_ptr()), n, d, k, uu.ctypes.data_as(C.c_void_p),
                                 C.c_void_p(c.data_ptr()), C.c_void_p(idx.data_ptr()),
                                 C.c_void_p(d2.data_ptr()), C.c_void_p(workspace.data_ptr() + off),
-                                workspace.numel() - off, 0 if prune else N.KM_PP_NO_PRUNE,
-                                _stream_ptr(X.device, stream), C.byref(comp) if count else None)
+                                workspace.numel() - off, flags, _stream_ptr(X.device, stream),
+                                C.byref(ps) if (count or timing) else None)
     N.check(st, "kmeans_pp_seed")
     out = {"C": c, "idx": idx, "D2": d2}
-    if count:
-        out["computed"] = int(comp.value)
+    if count or timing:
+        out["stats"] = ps.as_dict()
     return out
 
 

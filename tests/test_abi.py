@@ -45,6 +45,10 @@ def test_path_of_null_context_is_empty():
     assert N.load().kmeans_mti_path(None) == b""
 
 
+def test_pp_stats_layout():
+    assert C.sizeof(N.KmPPStats) == 48
+
+
 def test_struct_layout_matches_header():
     # int32 x2, int64 x5, double x2 with natural alignment
     assert C.sizeof(N.KmStats) == 4 * 2 + 8 * 5 + 8 * 2
@@ -113,7 +117,7 @@ def test_pp_seed_rejects_bad_arguments_without_a_device():
     assert call(u=[0.1, 1.0, 0.2]) == N.KM_ERR_INVALID_ARG
     assert call(u=[0.1, -0.5, 0.2]) == N.KM_ERR_INVALID_ARG
     assert call(u=[0.1, math.nan, 0.2]) == N.KM_ERR_INVALID_ARG
-    assert call(flags=2) == N.KM_ERR_INVALID_ARG
+    assert call(flags=4) == N.KM_ERR_INVALID_ARG
     assert call(wsb=need - 1) == N.KM_ERR_INVALID_ARG
     assert call(ws=C.c_void_p(0x1008)) == N.KM_ERR_INVALID_ARG
 

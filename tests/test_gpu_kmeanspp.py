@@ -55,18 +55,22 @@ def test_seeding_is_bit_exact(case, prune):
     ref = oracle.kmeanspp(X, k, u)
     got = km.kmeanspp(_gpu(X), k, u, prune=prune, count=True)
     _check(got, ref, X)
-    assert 0 < got["computed"] <= n * k
+    st = got["stats"]
+    assert 0 < st["computed"] <= n * k and st["passes"] == k
+    assert 0 <= st["improved"] <= st["computed"] - n
     if not prune:
-        assert got["computed"] == n * k
+        assert st["computed"] == n * k
 
 
 def test_pruning_skips_distances_on_clustered_data():
     X, _ = synth.blobs(100000 + 7, 16, 50, seed=308, spread=20.0, sigma=1.0)
     u = np.random.default_rng(308).random(50)
     ref = oracle.kmeanspp(X, 50, u)
-    got = km.kmeanspp(_gpu(X), 50, u, count=True)
+    got = km.kmeanspp(_gpu(X), 50, u, timing=True)
     _check(got, ref, X)
-    assert got["computed"] < 0.7 * X.shape[0] * 50, got["computed"]
+    st = got["stats"]
+    assert st["computed"] < 0.7 * X.shape[0] * 50, st
+    assert st["pass_ms"] > st["later_pass_ms"] > 0 and st["draw_ms"] > 0
 
 
 def test_degenerate_cases():
@@ -135,4 +139,4 @@ def test_large_k_workload_prefix_and_sampled_rows():
     bf = ((xs * xs).sum(1)[:, None] - 2.0 * xs @ S.T + (S * S).sum(1)[None, :]).min(axis=1)
     D2 = got["D2"].cpu().numpy()[rows]
     np.testing.assert_allclose(D2, np.maximum(bf, 0.0), rtol=1e-9, atol=1e-9 * float(bf.max()))
-    assert got["computed"] < X.shape[0] * w.k
+    assert got["stats"]["computed"] < X.shape[0] * w.k
