@@ -36,7 +36,7 @@ def log(msg: str) -> None:
 
 # Dominant (assignment-step) kernel of each library path.
 DOMINANT_KERNEL = {"stream-d16": "k_inc", "stream-d16-full": "k_small", "lds-vector": "k_assign",
-                   "lds-mfma": "k_assign",
+                   "lds-mfma": "k_assign", "lds-elkan": "k_assign",
                    "global-mfma": "k_mfma_large"}
 # Sources of each dominant kernel: the hardware byte counts of a committed
 # profile summary are used only while these files are unchanged.
@@ -210,6 +210,8 @@ def main() -> int:
     ap.add_argument("--spherical", action="store_true",
                     help="spherical k-means on the same workload (KM_FLAG_SPHERICAL: rows and "
                          "centroids on the unit sphere, cosine assignment)")
+    ap.add_argument("--elkan", action="store_true",
+                    help="Elkan's triangle-inequality comparator (KM_FLAG_ELKAN) instead of MTI")
     ap.add_argument("--kmeanspp", action="store_true",
                     help="time k-means++ seeding of the workload's k seeds instead of the k-means steps")
     ap.add_argument("--profile", action="store_true",
@@ -259,8 +261,10 @@ def main() -> int:
     base_flags = {"full_sums": True} if args.full_sums else {}
     if args.spherical:
         base_flags["spherical"] = True
+    if args.elkan:
+        base_flags["elkan"] = True
     # profiles/<kernel>_<tag>.txt holds the counters of this workload and method
-    tag = w.name + ("-spherical" if args.spherical else "")
+    tag = w.name + ("-spherical" if args.spherical else "") + ("-elkan" if args.elkan else "")
     if args.warmup > 0:
         with km.KMeansMTI(Xg, Cg, **base_flags) as ctx:
             for _ in range(args.warmup):
@@ -313,6 +317,11 @@ def main() -> int:
         elif path == "stream-d16-full":
             bytes_per_launch = (n * (4 * d + 4) * (K - 1) + 4 * surv) / (K - 1)
             what = "steps 2..K: n*(4d+4) (rows, states) + survivors*4 (new states)"
+        elif path == "lds-elkan":
+            comp = int(h_ev["computed"][1:].sum())
+            bytes_per_launch = n * (4 * d + 12) + (4.0 * k * surv + 4.0 * comp + 4 * ch) / (K - 1)
+            what = ("steps 2..K: n*(4d+12) + 4k per Clause-1 survivor (lower bounds read) "
+                    "+ 4 per computed distance (lower bound written) + changed*4")
         else:
             bytes_per_launch = n * (4 * d + 12) + 4 * ch / (K - 1)
             what = "steps 2..K: n*(4d+12) + changed*4"
@@ -361,7 +370,8 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "method": "spherical" if args.spherical else "kmeans",
+        "config": {"workload": w.name, "method": ("spherical" if args.spherical else "kmeans") +
+                   ("+elkan-ti" if args.elkan else ""),
                    "n": n, "d": d, "k": k, "max_iters": w.max_iters, "tol": w.tol,
                    "timed": "first %d iterations from the seeded centroids" % K, "path": path},
         "eff_dist_evals_per_s": lloyd / elapsed,

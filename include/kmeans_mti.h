@@ -83,7 +83,7 @@ enum {
                                   the sums of the points whose assignment changed (after the
                                   first step only the Clause-1 survivors' rows are read);
                                   same results.  Implied by KM_FLAG_STATS. */
-    KM_FLAG_SPHERICAL = 256u   /* spherical k-means (the paper's sk-means application): the
+    KM_FLAG_SPHERICAL = 256u,  /* spherical k-means (the paper's sk-means application): the
                                   rows of X are projected to the unit sphere (into a copy the
                                   context owns; a zero row stays zero) and C0 likewise, the
                                   assignment maximises the cosine (the nearest unit centroid),
@@ -92,6 +92,15 @@ enum {
                                   C0 rows must be nonzero (else KM_ERR_INVALID_ARG).  Centroid
                                   outputs are unit vectors; the inertia is the sum of squared
                                   chord distances 2 - 2 cos. */
+    KM_FLAG_ELKAN = 512u       /* comparator: Elkan's triangle-inequality pruning (the TI that
+                                  MTI relaxes, section III-C) instead of MTI: one lower bound per
+                                  point and centroid (4 n k bytes of device memory), a centroid
+                                  is skipped when the point's bound is within its lower bound or
+                                  within half the centroid distance, and the incumbent's
+                                  distance is computed only when some centroid passes both
+                                  tests.  Centroids and sums must fit in LDS (else
+                                  KM_ERR_UNSUPPORTED); not with KM_FLAG_LARGE_PATH.  Same
+                                  results as MTI; path "lds-elkan". */
 };
 
 /* Totals over the iterations run so far (kmeans_mti_get_stats, kmeans_mti_run). */
@@ -180,7 +189,8 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
  * k_small_finish), "stream-d16-full" (the same with
  * KM_FLAG_FULL_SUMS or KM_FLAG_STATS: k_small every step), "lds-vector" /
  * "lds-mfma" (centroids and sums in LDS: k_assign with vector or matrix-core
- * survivors, then k_reduce, k_update, k_centroid_table), "global-mfma"
+ * survivors, then k_reduce, k_update, k_centroid_table), "lds-elkan" (the
+ * same with KM_FLAG_ELKAN's lower-bound scan), "global-mfma"
  * (centroids or sums too large for LDS: dense MFMA survivors, sums by
  * counting sort).  "" for a NULL context.
  */

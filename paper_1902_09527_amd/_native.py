@@ -27,6 +27,7 @@ KM_FLAG_LARGE_PATH = 32
 KM_FLAG_GENERIC = 64
 KM_FLAG_FULL_SUMS = 128
 KM_FLAG_SPHERICAL = 256
+KM_FLAG_ELKAN = 512
 
 KM_PP_NO_PRUNE = 1
 KM_PP_TIMING = 2

@@ -237,7 +237,9 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     // (centroids, fixed-point sums, X tile) fits; else the global-memory path.
     c->tp = 0;
     const bool aligned = reinterpret_cast<uintptr_t>(X) % 16 == 0;
-    if (!(c->flags & (KM_FLAG_LARGE_PATH | KM_FLAG_GENERIC)) && km::small_applies(n, d, k, aligned)) {
+    const bool elkan = (c->flags & KM_FLAG_ELKAN) != 0;
+    if (elkan && (c->flags & KM_FLAG_LARGE_PATH)) return KM_ERR_INVALID_ARG;
+    if (!elkan && !(c->flags & (KM_FLAG_LARGE_PATH | KM_FLAG_GENERIC)) && km::small_applies(n, d, k, aligned)) {
         c->small = true;
         c->tp = km::kSmallTile;
         c->lds = km::small_lds_bytes(k);
@@ -268,8 +270,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             c->gi = (int)gi;
         }
     } else if (!(c->flags & KM_FLAG_LARGE_PATH)) {
-        c->variant = km::assign_variant(d, k, aligned, (c->flags & KM_FLAG_VECTOR_ONLY) != 0);
-        const bool h_lds = c->variant % 16 == 0 && k <= km::kHLdsMaxK;
+        c->variant = km::assign_variant(d, k, aligned, (c->flags & KM_FLAG_VECTOR_ONLY) != 0, elkan);
+        const bool h_lds = km::assign_h_lds(c->variant % 16, k);
         for (int tp = 256; c->tp == 0 && tp >= 64; tp /= 2) {
             int bytes = km::assign_lds(d, k, tp, h_lds).bytes;
             if (bytes <= max_lds) {
@@ -290,6 +292,9 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         int64_t G = (int64_t)per_cu * cus;
         if (G > ntiles) G = ntiles;
         v.G = (int32_t)G;
+    } else if (elkan) {
+        snprintf(g_last_hip, sizeof g_last_hip, "Elkan's lower bounds need the centroids and sums in LDS");
+        return KM_ERR_UNSUPPORTED;
     } else {
         c->large = true;
         km::Large& L = c->lg;
@@ -327,6 +332,16 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     int rc;
     if (!c->small && ((rc = c->alloc(&v.a, (size_t)n)) || (rc = c->alloc(&v.u, (size_t)n))))
         return rc;
+    if (elkan) {   // O(nk) lower bounds (zero: valid before any distance is known)
+        if ((uint64_t)n > (uint64_t)INT64_MAX / 4 / (uint64_t)k) return KM_ERR_INVALID_ARG;
+        if ((rc = c->alloc(&v.lb, (size_t)n * (size_t)k)) || (rc = c->alloc(&v.dhi, (size_t)k)) ||
+            (rc = c->alloc(&v.dlo, (size_t)k)) || (rc = c->alloc(&v.dupf, (size_t)k)))
+            return rc;
+        KM_HIP(hipMemsetAsync(v.dupf, 0, sizeof(float) * (size_t)k, c->stream));
+        KM_HIP(hipMemsetAsync(v.lb, 0, sizeof(float) * (size_t)n * (size_t)k, c->stream));
+        KM_HIP(hipMemsetAsync(v.dhi, 0, sizeof(double) * (size_t)k, c->stream));
+        KM_HIP(hipMemsetAsync(v.dlo, 0, sizeof(double) * (size_t)k, c->stream));
+    }
     if ((rc = c->alloc(&v.C64, (size_t)k * d)) || (rc = c->alloc(&v.C32, (size_t)k * d)) ||
         (rc = c->alloc(&v.ec, (size_t)k)) || (rc = c->alloc(&v.h, (size_t)k * k)) ||
         (rc = c->alloc(&v.s, (size_t)k)) || (rc = c->alloc(&v.f, (size_t)k)) ||
@@ -461,7 +476,7 @@ int kmeans_mti_init(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t 
     if (rc != KM_OK) return rc;
     if (flags & ~(uint32_t)(KM_FLAG_NO_PRUNE | KM_FLAG_STATS | KM_FLAG_VALIDATE | KM_FLAG_TIMING |
                             KM_FLAG_VECTOR_ONLY | KM_FLAG_LARGE_PATH | KM_FLAG_GENERIC |
-                            KM_FLAG_FULL_SUMS | KM_FLAG_SPHERICAL))
+                            KM_FLAG_FULL_SUMS | KM_FLAG_SPHERICAL | KM_FLAG_ELKAN))
         return KM_ERR_INVALID_ARG;
     km_ctx* c = new (std::nothrow) km_ctx;
     if (!c) return KM_ERR_OOM;
@@ -788,6 +803,7 @@ const char* kmeans_mti_path(const km_ctx* ctx) {
     if (!ctx) return "";
     if (ctx->small) return ctx->inc ? "stream-d16" : "stream-d16-full";
     if (ctx->large) return "global-mfma";
+    if (ctx->variant % 16 == 8) return "lds-elkan";
     return ctx->variant % 16 ? "lds-mfma" : "lds-vector";
 }
 

@@ -57,6 +57,10 @@ struct Dev {
     float* s;             // k: min_{j != i} h[i][j] rounded down (+inf if k == 1)
     float* f;             // k: drift ||c_j^t - c_j^{t-1}|| rounded up
     float* cn2;           // k: ||c32_j||^2 (matrix-core path)
+    float* lb;            // Elkan only: k x n lower bounds (centroid-major), offset by the cumulative drift
+    double* dhi;          // Elkan only: k cumulative drifts, rounded up (else null)
+    double* dlo;          // Elkan only: k cumulative drifts, rounded down
+    float* dupf;          // Elkan only: k cumulative drifts, rounded up to float32
     uint64_t* part;       // G x L per-block partial rows
     uint64_t* total;      // L reduced row (zero between iterations)
     IterState* st;
@@ -117,8 +121,11 @@ struct AssignLds {
         off_sq, off_misc, bytes;
 };
 
-// The vector survivor scan keeps the half-distance table in LDS up to this k.
+// The vector survivor scans keep the half-distance table in LDS up to this k.
 constexpr int kHLdsMaxK = 64;
+// Whether the assignment kernel with KB (the variant's low 4 bits) keeps the
+// half-distance table in LDS; the host sizes the LDS image with the same rule.
+__host__ __device__ inline bool assign_h_lds(int kb, int k) { return (kb == 0 || kb == 8) && k <= kHLdsMaxK; }
 
 // Centroid count rounded up to the 32-row blocks of the matrix-core path.
 __host__ __device__ inline int k_pad32(int k) { return (k + 31) / 32 * 32; }
@@ -280,10 +287,11 @@ hipError_t launch_centroid_table(const Dev& dv, int force, hipStream_t s);
 
 // Assignment-kernel variant for (d, k): 16 * D + KB, where D is the
 // compile-time dimension (16, 32; 0 = generic, any d) and KB the number of
-// 32-centroid blocks of the matrix-core survivor path (0 = vector path).
+// 32-centroid blocks of the matrix-core survivor path (0 = vector path,
+// 8 = Elkan's lower-bound scan on the vector units).
 // The specialised dimensions read X with 16-byte loads and need a 16-byte
 // aligned X; vector_only selects KB = 0.
-int assign_variant(int d, int k, bool aligned, bool vector_only);
+int assign_variant(int d, int k, bool aligned, bool vector_only, bool elkan);
 // Kernel symbol of an assignment-kernel variant (for occupancy queries).
 const void* assign_kernel_symbol(int variant);
 

@@ -468,7 +468,9 @@ __device__ inline void klane_survivors(const ScanCtx& W, const float* hl, int ns
 // Assignment + partial sums.  Block = tp threads = one tile of tp points;
 // blocks stride over tiles.  D > 0: the row lives in registers (D % 4 == 0);
 // D == 0: any d, rows read from LDS.  KB == 0: the survivors run the
-// per-point MTI scan on the vector units.  KB > 0 (D = 16 or 32, k <= 32*KB):
+// per-point MTI scan on the vector units.  KB == 8: Elkan's triangle
+// inequality scan (one lane per survivor) with a lower bound per point and
+// centroid in addition to MTI's tests.  KB = 1, 2, 4 (D = 16 or 32, k <= 32*KB):
 // the survivors' distances to all centroids come from float32 MFMA tiles
 // (X . C^T in the expanded form |x|^2 + |c|^2 - 2 x.c), and every centroid
 // within the expanded form's error bound of the best is re-evaluated in the
@@ -477,6 +479,8 @@ __device__ inline void klane_survivors(const ScanCtx& W, const float* hl, int ns
 
 template <int D, int KB>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1 : 2))) void k_assign(Dev P) {
+    constexpr bool ELK = KB == 8;          // Elkan's lower bounds, vector scan
+    constexpr int MB = ELK ? 0 : KB;       // 32-centroid blocks of the matrix-core path
     IterState* st = P.st;
     if (st->done) {
         if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
@@ -495,7 +499,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
     const float gamma = P.gamma;
     const int xs = xs_stride(d);
 
-    const bool h_lds = KB == 0 && k <= kHLdsMaxK;
+    const bool h_lds = assign_h_lds(KB, k);
     const AssignLds lay = assign_lds(d, k, tp, h_lds);
     unsigned char* smem = km_smem;
     uint64_t* acc = reinterpret_cast<uint64_t*>(smem + lay.off_acc);
@@ -526,27 +530,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
         fs[i] = P.f[i];
         ss[i] = P.s[i];
         ecs[i] = P.ec[i];
+        if constexpr (ELK) cn2s[i] = P.dupf[i];   // the matrix-core norms' slot holds the drifts
     }
     if (tid < kNumStat) bst[tid] = 0;
 
     // Matrix-core path: this lane's A operands (centroid rows) for the whole
     // kernel.  Lane l feeds row (32*cb + l%32) and dimension half l/32; the
     // MFMA k-step s pairs dimension s with dimension D/2 + s.
-    constexpr int kCb = KB > 0 ? KB : 1;
+    constexpr int kCb = MB > 0 ? MB : 1;
     constexpr int kHalf = D > 0 ? D / 2 : 1;
     float creg[kCb][kHalf];
     float cnmax = 0.f;
-    if constexpr (KB > 0) {
+    if constexpr (MB > 0) {
         static_assert(D == 16 || D == 32, "matrix-core path needs d = 16 or 32");
         const int lane = tid & 63, half = lane >> 5;
 #pragma unroll
-        for (int cb = 0; cb < KB; ++cb) {
+        for (int cb = 0; cb < MB; ++cb) {
             const int j = cb * 32 + (lane & 31);
 #pragma unroll
             for (int q = 0; q < kHalf; ++q)
                 creg[cb][q] = j < k ? P.C32[(int64_t)j * D + half * kHalf + q] : 0.f;
         }
-        for (int i = tid; i < KB * 32; i += tp) cn2s[i] = i < k ? P.cn2[i] : INFINITY;
+        for (int i = tid; i < MB * 32; i += tp) cn2s[i] = i < k ? P.cn2[i] : INFINITY;
         __syncthreads();
         float m2 = 0.f;
         for (int i = lane; i < k; i += 64) m2 = fmaxf(m2, cn2s[i]);
@@ -650,7 +655,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
 
         // Survivors, compacted into sq[0, nq).
         const int nq = *qn;
-        if constexpr (KB > 0) {
+        if constexpr (MB > 0) {
             // Matrix cores: one wave per block of 32 survivors.  Lanes l and
             // l + 32 serve survivor l % 32 and hold 16 of its centroid
             // distances per 32-centroid block.
@@ -676,19 +681,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
                 x2 += __shfl_xor(x2, 32);
                 f32x16 dot[kCb];
 #pragma unroll
-                for (int cb = 0; cb < KB; ++cb)
+                for (int cb = 0; cb < MB; ++cb)
 #pragma unroll
                     for (int e = 0; e < 16; ++e) dot[cb][e] = 0.f;
 #pragma unroll
                 for (int q = 0; q < kHalf; ++q)
 #pragma unroll
-                    for (int cb = 0; cb < KB; ++cb)
+                    for (int cb = 0; cb < MB; ++cb)
                         dot[cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(creg[cb][q], xh[q], dot[cb], 0, 0, 0);
                 // Register e of block cb holds centroid 32*cb + 8*(e/4) + 4*half + e%4.
                 auto cent = [&](int cb, int e) { return cb * 32 + 8 * (e >> 2) + 4 * half + (e & 3); };
                 float e1 = INFINITY;
 #pragma unroll
-                for (int cb = 0; cb < KB; ++cb)
+                for (int cb = 0; cb < MB; ++cb)
 #pragma unroll
                     for (int e = 0; e < 16; ++e)
                         e1 = fminf(e1, x2 + cn2s[cent(cb, e)] - 2.f * dot[cb][e]);
@@ -702,7 +707,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
                 // of the candidates from the LDS rows.
                 uint64_t cmask = 0;
 #pragma unroll
-                for (int cb = 0; cb < KB; ++cb)
+                for (int cb = 0; cb < MB; ++cb)
 #pragma unroll
                     for (int e = 0; e < 16; ++e)
                         if (x2 + cn2s[cent(cb, e)] - 2.f * dot[cb][e] <= thr) cmask |= 1ull << (16 * cb + e);
@@ -801,7 +806,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
                     my_comp += (uint64_t)k;   // the dense pairs; refinements re-evaluate some
                 }
             }
-        } else if constexpr (D > 0) {
+        } else if constexpr (D > 0 && !ELK) {
             ScanCtx W{Cs, lay.off_h, P.h, ss, ecs, P.C64, Xs, sa, su, sD, sq, k, prune, gamma, ecmax};
             const float* hl = reinterpret_cast<const float*>(km_smem + lay.off_h);
             if (k <= 4) {
@@ -838,6 +843,90 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
                 int b = -1;
                 float Db = INFINITY, D2 = INFINITY, ub = 0.f;
                 uint64_t nc = 0;
+                if constexpr (ELK) {
+                    // Elkan: skip c_j when the bound is within h(b, j) or
+                    // within the lower bound l(x, c_j); the incumbent's
+                    // distance is computed only when a centroid passes both
+                    // tests with the loose bound.  Lower bounds are stored
+                    // offset by the cumulative drift D_j of their centroid
+                    // (l' = l + D_j then; l = l' - D_j now, rounded down).
+                    float* lbp = P.lb + (base + r);
+                    auto hv_of = [&](int bb, int j) -> float {
+                        return h_lds ? reinterpret_cast<const float*>(smem + lay.off_h)[bb * k + j]
+                                     : P.h[(int64_t)bb * k + j];
+                    };
+                    auto store_lb = [&](int j, float Dq) {
+                        const double lo = ((double)sqrtf(Dq) * (1.0 - (double)gamma) - (double)ecs[j]) *
+                                          (1.0 - 0x1p-20);
+                        const double v = ((lo > 0.0 ? lo : 0.0) + P.dlo[j]) * (1.0 - 0x1p-50);
+                        lbp[(int64_t)j * P.n] = f32_down(v);
+                    };
+                    bool tight = inc < 0;
+                    if (inc >= 0) {
+                        b = inc;
+                        ub = su[r];
+                    }
+                    // ub <= l(x, c_j) = l' - D_j, tested as ub + D_j <= l' with
+                    // the sum rounded up (D_j rounded up in dups).
+                    const float* dups = cn2s;
+                    auto below_lb = [&](float lp, int j) -> bool {
+                        return !first && (ub + dups[j]) * (1.0f + 0x1p-22f) <= lp;
+                    };
+                    // Chunks of centroids: their lower bounds are loaded at
+                    // once and tested against the bound at the chunk's start
+                    // (tests only get stronger as the best improves); the
+                    // candidates are then visited in ascending order and
+                    // tested again with the current best and bound.
+                    constexpr int kCh = D >= 32 ? 16 : 32;
+                    for (int j0 = 0; j0 < k; j0 += kCh) {
+                        float lv[kCh];
+#pragma unroll
+                        for (int q = 0; q < kCh; ++q)
+                            lv[q] = (!first && j0 + q < k) ? lbp[(int64_t)(j0 + q) * P.n] : 0.f;
+                        uint32_t m = 0;
+#pragma unroll
+                        for (int q = 0; q < kCh; ++q) {
+                            const int j = j0 + q;
+                            if (j < k && j != inc) {
+                                const bool cut = prune && b >= 0 && (ub <= hv_of(b, j) || below_lb(lv[q], j));
+                                m |= (cut ? 0u : 1u) << q;
+                            }
+                        }
+                        while (m) {
+                            const int q = __builtin_ctz(m);
+                            m &= m - 1u;
+                            const int j = j0 + q;
+                            float lp = 0.f;
+                            if (prune && b >= 0) {
+                                if (ub <= hv_of(b, j)) continue;
+                                if (!first) {
+                                    lp = lbp[(int64_t)j * P.n];
+                                    if (below_lb(lp, j)) continue;
+                                }
+                            }
+                            if (!tight) {   // tighten: exact distance to the incumbent (U(u))
+                                Db = dist(inc);
+                                nc += 1;
+                                tight = true;
+                                ub = upper_bound(Db, ecs[inc], gamma);
+                                store_lb(inc, Db);
+                                if (prune && (ub <= hv_of(b, j) || below_lb(lp, j))) continue;
+                            }
+                            const float Dj = dist(j);
+                            nc += 1;
+                            store_lb(j, Dj);
+                            if (Dj < Db) {
+                                D2 = Db;
+                                Db = Dj;
+                                b = j;
+                                ub = upper_bound(Db, ecs[j], gamma);
+                            } else if (Dj < D2) {
+                                D2 = Dj;
+                            }
+                        }
+                    }
+                    if (!tight) Db = -1.f;   // incumbent kept on the loose bound; distance not formed
+                } else {
                 if (inc >= 0) {   // tighten: exact distance to the incumbent (U(u))
                     Db = dist(inc);
                     b = inc;
@@ -863,6 +952,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
                             D2 = Dj;
                         }
                     }
+                }
                 }
                 // Near tie within the float32 error bound: decide in float64
                 // against the master centroids with the oracle's tie rule.
@@ -909,7 +999,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
             P.u[p] = su[tid];
             if (want_inertia) {
                 float Dv;
-                if (surv) {
+                if (surv && sD[tid] >= 0.f) {
                     Dv = sD[tid];
                 } else if constexpr (D > 0) {
                     Row<D> x;
@@ -1047,6 +1137,13 @@ __global__ __launch_bounds__(64) void k_update(Dev P) {
         P.f[j] = f32_up(sqrt(dr) * (1.0 + 0x1p-40));
         P.ec[j] = f32_up(sqrt(de) * (1.0 + 0x1p-40));
         P.total[(int64_t)k * d + j] = 0;
+        if (P.dhi) {   // cumulative drift, bracketed, for the Elkan lower bounds
+            const double fd = sqrt(dr);
+            const double hi = (P.dhi[j] + fd * (1.0 + 0x1p-40)) * (1.0 + 0x1p-50);
+            P.dhi[j] = hi;
+            P.dlo[j] = (P.dlo[j] + fd * (1.0 - 0x1p-40)) * (1.0 - 0x1p-50);
+            P.dupf[j] = f32_up(hi);
+        }
     }
     if (j == 0 && threadIdx.x == 0) {
         uint64_t* sc = P.total + (int64_t)k * d + k;
@@ -1081,14 +1178,16 @@ __global__ __launch_bounds__(64) void k_update(Dev P) {
 // ---------------------------------------------------------------------------
 // Launchers
 
-int assign_variant(int d, int k, bool aligned, bool vector_only) {
+int assign_variant(int d, int k, bool aligned, bool vector_only, bool elkan) {
     const int D = aligned && (d == 16 || d == 32) ? d : 0;
+    if (elkan) return 16 * D + 8;
     int KB = 0;
     if (D > 0 && !vector_only && k > 16 && k <= 128) KB = k <= 32 ? 1 : (k <= 64 ? 2 : 4);
     return 16 * D + KB;
 }
 
-#define KM_ASSIGN_VARIANTS(X) X(0, 0) X(16, 0) X(32, 0) X(16, 1) X(16, 2) X(16, 4) X(32, 1) X(32, 2) X(32, 4)
+#define KM_ASSIGN_VARIANTS(X) \
+    X(0, 0) X(16, 0) X(32, 0) X(16, 1) X(16, 2) X(16, 4) X(32, 1) X(32, 2) X(32, 4) X(0, 8) X(16, 8) X(32, 8)
 
 const void* assign_kernel_symbol(int variant) {
     switch (variant) {

@@ -33,8 +33,10 @@ def _check_matrix(t: torch.Tensor, name: str, cols: Optional[int] = None) -> Non
 
 def _flags(prune: bool, stats: bool, validate: bool, timing: bool = False,
            vector_only: bool = False, large_path: bool = False, generic: bool = False,
-           full_sums: bool = False, spherical: bool = False) -> int:
+           full_sums: bool = False, spherical: bool = False, elkan: bool = False) -> int:
     f = N.KM_FLAG_TIMING if timing else 0
+    if elkan:
+        f |= N.KM_FLAG_ELKAN
     if spherical:
         f |= N.KM_FLAG_SPHERICAL
     if full_sums:
@@ -69,7 +71,7 @@ class KMeansMTI:
     def __init__(self, X: torch.Tensor, C0: torch.Tensor, prune: bool = True, stats: bool = False,
                  validate: bool = False, timing: bool = False, vector_only: bool = False,
                  large_path: bool = False, generic: bool = False, full_sums: bool = False,
-                 spherical: bool = False, stream: Optional[torch.cuda.Stream] = None):
+                 spherical: bool = False, elkan: bool = False, stream: Optional[torch.cuda.Stream] = None):
         _check_matrix(X, "X")
         _check_matrix(C0, "C0", X.shape[1])
         if C0.device != X.device:
@@ -86,7 +88,7 @@ class KMeansMTI:
                                            self.d, self.k, C.c_void_p(C0.data_ptr()),
                                            _stream_ptr(self.device, stream),
                                            _flags(prune, stats, validate, timing, vector_only,
-                                                  large_path, generic, full_sums, spherical))
+                                                  large_path, generic, full_sums, spherical, elkan))
         N.check(st, "kmeans_mti_init")
 
     def _live(self) -> C.c_void_p:
@@ -176,7 +178,7 @@ class KMeansMTI:
 def run(X: torch.Tensor, C0: torch.Tensor, max_iters: int, tol: float = 0.0, prune: bool = True,
         stats: bool = False, validate: bool = False, vector_only: bool = False,
         large_path: bool = False, generic: bool = False, full_sums: bool = False,
-        spherical: bool = False, stream: Optional[torch.cuda.Stream] = None
+        spherical: bool = False, elkan: bool = False, stream: Optional[torch.cuda.Stream] = None
         ) -> Tuple[torch.Tensor, torch.Tensor, Dict[str, float]]:
     """Whole k-means run (kmeans_mti_run): (assign int32 [n], C float32 [k, d], stats)."""
     _check_matrix(X, "X")
@@ -194,7 +196,7 @@ def run(X: torch.Tensor, C0: torch.Tensor, max_iters: int, tol: float = 0.0, pru
                                 int(max_iters), float(tol), C.c_void_p(a.data_ptr()),
                                 C.c_void_p(c.data_ptr()), _stream_ptr(X.device, stream),
                                 _flags(prune, stats, validate, False, vector_only, large_path,
-                                       generic, full_sums, spherical),
+                                       generic, full_sums, spherical, elkan),
                                 C.byref(s))
     N.check(st, "kmeans_mti_run")
     return a, c, s.as_dict()
