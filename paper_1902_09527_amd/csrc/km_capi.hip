@@ -92,6 +92,7 @@ struct km_ctx {
     int nbufs = 0;
     bool broken = false;
     bool stepped = false;
+    bool pending = false;   // streaming path: the end of the last incremental step has not run
 
     // KM_FLAG_TIMING: events around the four launches of each iteration,
     // harvested into per-kernel totals when the pool fills or on request.
@@ -160,16 +161,22 @@ int enqueue_iteration(km_ctx* c) {
     }
     auto mark = [&](int i) -> hipError_t { return ev ? hipEventRecord(ev[i], c->stream) : hipSuccess; };
     if ((e = mark(0)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
-    if (c->small) {   // two launches: streaming or incremental step, then the finishing block
-        const bool delta = c->inc && c->enq > 0;
-        e = delta ? km::launch_inc(c->dv, c->fz, c->gi, c->lds_inc, c->stream)
-                  : km::launch_small(c->dv, c->fz, c->lds, c->stream);
+    if (c->small) {
+        // Streaming step t then its end in one block; or an incremental step
+        // that first ends step t - 1 itself when that has not run yet (one
+        // launch per step while incremental steps follow each other).
+        const int t = (int)c->enq;
+        km::Dev dv = c->dv;
+        dv.C64 = c->fz.c64 + (size_t)km::slot2(t) * c->k * c->d;   // C^t
+        const bool inc = c->inc && t > 0;
+        e = inc ? km::launch_inc(dv, c->fz, c->gi, c->lds_inc, t, c->pending ? 1 : 0, c->stream)
+                : km::launch_small(dv, c->fz, c->lds, t, c->stream);
         if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "streaming step kernel"));
         if ((e = mark(1)) != hipSuccess || (e = mark(2)) != hipSuccess)
             return fail_ctx(c, hip_fail(e, "hipEventRecord"));
-        if ((e = km::launch_small_finish(c->dv, c->fz, delta ? 1 : 0, delta ? c->gi : c->dv.G, c->stream)) !=
-            hipSuccess)
+        if (!inc && (e = km::launch_small_finish(dv, c->fz, t, 0, c->stream)) != hipSuccess)
             return fail_ctx(c, hip_fail(e, "streaming step finish kernel"));
+        c->pending = inc;
         ++c->enq;
         if ((e = mark(3)) != hipSuccess || (e = mark(4)) != hipSuccess)
             return fail_ctx(c, hip_fail(e, "hipEventRecord"));
@@ -193,7 +200,22 @@ int enqueue_iteration(km_ctx* c) {
     return KM_OK;
 }
 
+// Streaming path: enqueue the end of the last step if it has not run (its
+// results are about to be read).
+int flush_pending(km_ctx* c) {
+    if (!c->pending) return KM_OK;
+    const int t = (int)c->enq - 1;
+    km::Dev dv = c->dv;
+    dv.C64 = c->fz.c64 + (size_t)km::slot2(t) * c->k * c->d;
+    hipError_t e = km::launch_small_finish(dv, c->fz, t, 1, c->stream);
+    if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "streaming step finish kernel"));
+    c->pending = false;
+    return KM_OK;
+}
+
 int read_state(km_ctx* c, km::IterState* out) {
+    int rc = flush_pending(c);
+    if (rc != KM_OK) return rc;
     hipError_t e = hipStreamSynchronize(c->stream);
     if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "hipStreamSynchronize"));
     e = hipMemcpy(out, c->dv.st, sizeof(km::IterState), hipMemcpyDeviceToHost);
@@ -342,7 +364,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         KM_HIP(hipMemsetAsync(v.dhi, 0, sizeof(double) * (size_t)k, c->stream));
         KM_HIP(hipMemsetAsync(v.dlo, 0, sizeof(double) * (size_t)k, c->stream));
     }
-    if ((rc = c->alloc(&v.C64, (size_t)k * d)) || (rc = c->alloc(&v.C32, (size_t)k * d)) ||
+    // The streaming path keeps C^t in two slots (t % 2); slot 0 holds C0.
+    if ((rc = c->alloc(&v.C64, (size_t)k * d * (c->small ? 2 : 1))) || (rc = c->alloc(&v.C32, (size_t)k * d)) ||
         (rc = c->alloc(&v.ec, (size_t)k)) || (rc = c->alloc(&v.h, (size_t)k * k)) ||
         (rc = c->alloc(&v.s, (size_t)k)) || (rc = c->alloc(&v.f, (size_t)k)) ||
         (rc = c->alloc(&v.cn2, (size_t)k)) ||
@@ -352,16 +375,19 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     if (c->small) {
         // Point states padded to whole incremental tiles (the padding stays zero).
         const size_t nw = (size_t)((n + km::kIncTile - 1) / km::kIncTile) * km::kIncTile;
-        if ((rc = c->alloc(&c->fz.rows, (size_t)km::kSmallRows * v.L)) ||
-            (rc = c->alloc(&c->fz.sum, (size_t)k * d + k)) || (rc = c->alloc(&c->fz.w, nw)) ||
-            (rc = c->alloc(&c->fz.dhi, (size_t)k)) || (rc = c->alloc(&c->fz.dlo, (size_t)k)) ||
-            (rc = c->alloc(&c->fz.dup, (size_t)k)) || (rc = c->alloc(&c->fz.ddn, (size_t)k)) ||
-            (rc = c->alloc(&c->fz.bcnt, (size_t)km::kNumStat * (v.G > c->gi ? v.G : c->gi))))
+        c->fz.c64 = v.C64;
+        const size_t nrows = (size_t)3 * km::kSmallRows * v.L;
+        if ((rc = c->alloc(&c->fz.rows, nrows)) || (rc = c->alloc(&c->fz.stat, 3 * km::kNumStat)) ||
+            (rc = c->alloc(&c->fz.sum, (size_t)2 * (k * d + k))) || (rc = c->alloc(&c->fz.w, nw)) ||
+            (rc = c->alloc(&c->fz.dhi, (size_t)2 * k)) || (rc = c->alloc(&c->fz.dlo, (size_t)2 * k)) ||
+            (rc = c->alloc(&c->fz.dup, (size_t)k)) || (rc = c->alloc(&c->fz.ddn, (size_t)k)))
             return rc;
-        KM_HIP(hipMemsetAsync(c->fz.rows, 0, sizeof(uint64_t) * (size_t)km::kSmallRows * v.L, c->stream));
+        KM_HIP(hipMemsetAsync(c->fz.rows, 0, sizeof(uint64_t) * nrows, c->stream));
+        KM_HIP(hipMemsetAsync(c->fz.stat, 0, sizeof(uint64_t) * 3 * km::kNumStat, c->stream));
+        KM_HIP(hipMemsetAsync(c->fz.sum, 0, sizeof(uint64_t) * 2 * (size_t)(k * d + k), c->stream));
         KM_HIP(hipMemsetAsync(c->fz.w, 0, sizeof(uint32_t) * nw, c->stream));
-        KM_HIP(hipMemsetAsync(c->fz.dhi, 0, sizeof(double) * (size_t)k, c->stream));
-        KM_HIP(hipMemsetAsync(c->fz.dlo, 0, sizeof(double) * (size_t)k, c->stream));
+        KM_HIP(hipMemsetAsync(c->fz.dhi, 0, sizeof(double) * 2 * (size_t)k, c->stream));
+        KM_HIP(hipMemsetAsync(c->fz.dlo, 0, sizeof(double) * 2 * (size_t)k, c->stream));
         KM_HIP(hipMemsetAsync(c->fz.dup, 0, sizeof(float) * (size_t)k, c->stream));
         KM_HIP(hipMemsetAsync(c->fz.ddn, 0, sizeof(float) * (size_t)k, c->stream));
     }
@@ -518,6 +544,7 @@ int kmeans_mti_get(km_ctx* ctx, int32_t* assign_out, float* C_out) {
     if (C_out && (rc = check_device_range(C_out, (size_t)ctx->k * ctx->d * 4, ctx->device, "C_out")) !=
                      KM_OK)
         return rc;
+    if ((rc = flush_pending(ctx)) != KM_OK) return rc;
     hipError_t e;
     if (assign_out && ctx->small &&
         (e = km::launch_small_unpack(ctx->fz, ctx->n, assign_out, ctx->stream)) != hipSuccess)
@@ -536,9 +563,11 @@ int kmeans_mti_get(km_ctx* ctx, int32_t* assign_out, float* C_out) {
 int kmeans_mti_get_centroids64(km_ctx* ctx, double* C_out) {
     if (!ctx || !C_out) return KM_ERR_INVALID_ARG;
     if (ctx->broken) return KM_ERR_STATE;
-    hipError_t e = hipStreamSynchronize(ctx->stream);
-    if (e != hipSuccess) return fail_ctx(ctx, hip_fail(e, "hipStreamSynchronize"));
-    e = hipMemcpy(C_out, ctx->dv.C64, (size_t)ctx->k * ctx->d * sizeof(double), hipMemcpyDeviceToHost);
+    km::IterState st;
+    int rc = read_state(ctx, &st);   // ends the last step, synchronizes
+    if (rc != KM_OK) return rc;
+    const double* src = ctx->small ? ctx->fz.c64 + (size_t)km::slot2(st.t) * ctx->k * ctx->d : ctx->dv.C64;
+    hipError_t e = hipMemcpy(C_out, src, (size_t)ctx->k * ctx->d * sizeof(double), hipMemcpyDeviceToHost);
     if (e != hipSuccess) return fail_ctx(ctx, hip_fail(e, "hipMemcpy centroids"));
     return KM_OK;
 }

@@ -195,18 +195,26 @@ constexpr int kIncQ = 4 * kIncWaveQ;
 // is then added by the reader, so a point whose bound needs no tightening is
 // never written.
 struct Fused {
-    uint64_t* rows;       // kSmallRows x L, zero between steps
-    uint64_t* sum;        // k*d + k: exact sums and counts after the last update
+    // Buffers that one launch both reads and writes are kept in slots by step
+    // index t (steps counted from 0): an incremental step finishes the step
+    // before it in the same launch, so the step's inputs and outputs differ.
+    uint64_t* rows;       // 3 slots x kSmallRows x L: slot t % 3 receives step t's sums (zero before)
+    uint64_t* stat;       // 3 slots x kNumStat: step t's counters (device atomics of every block)
+    uint64_t* sum;        // 2 slots x (k*d + k): exact sums and counts after step t, slot t % 2
+    double* c64;          // 2 slots x k*d: float64 centroids used by step t (C^t), slot t % 2
     uint32_t* w;          // point states, n rounded up to kIncTile (padding zero)
-    double* dhi;          // k: cumulative drift sum_t f_j^t, rounded up (float64)
-    double* dlo;          // k: the same rounded down
-    float* dup;           // k: dhi rounded up to float32
-    float* ddn;           // k: dlo rounded down to float32
-    uint64_t* bcnt;       // per-block counters of the step kernel: blocks x kNumStat
+    double* dhi;          // 2 slots x k: cumulative drift after t updates (D^t), rounded up, slot t % 2
+    double* dlo;          // 2 slots x k: the same rounded down
+    float* dup;           // k: the latest D rounded up to float32
+    float* ddn;           // k: the latest D rounded down to float32
 };
 
+__host__ __device__ inline int slot3(int t) { return ((t % 3) + 3) % 3; }
+__host__ __device__ inline int slot2(int t) { return t & 1; }
+
 struct SmallLds {
-    int off_c, off_h, off_s, off_ec, off_du, off_dd, off_acc, off_cnt, off_qr, off_qp, off_qa, off_misc, bytes;
+    int off_c, off_h, off_s, off_ec, off_du, off_dd, off_acc, off_cnt, off_qr, off_qp, off_qa, off_misc, off_c64,
+        bytes;
     int csu, kp;          // stride (uint64) of one copy of the sums; of one copy of the counts
 };
 
@@ -237,14 +245,16 @@ __host__ __device__ inline SmallLds small_lds(int k, bool staged) {
     L.off_qp = take(4 * q, 16);
     L.off_qa = take(4 * q, 16);
     L.off_misc = take(64, 16);   // three queue counters (int) at 0, kNumStat uint64 counters at 16
+    // Incremental kernel: float64 centroids for near-tie decisions when the
+    // step finishes the previous one itself (then they are not in memory yet).
+    L.off_c64 = take(staged ? 0 : 8 * k * 16, 16);
     L.bytes = (o + 15) / 16 * 16;
     return L;
 }
 
-// LDS bytes of the finishing block (totals, centroids, drift terms, table).
-__host__ __device__ inline int finish_lds(int d, int k) {
-    return 8 * row_len(d, k) + 3 * 8 * k * d + 4 * k * k + 4 * k;
-}
+// LDS bytes of the end-of-step computation (new centroids in float64, the
+// rounding errors of their float32 copies).
+__host__ __device__ inline int finish_lds(int d, int k) { return 8 * k * d + 4 * k; }
 
 bool small_applies(int64_t n, int d, int k, bool aligned);
 const void* small_kernel_symbol(int k);
@@ -252,12 +262,16 @@ const void* inc_kernel_symbol(int k);
 int small_lds_bytes(int k);
 int inc_lds_bytes(int k);
 int small_finish_lds_bytes(int k);
-hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, hipStream_t s);
-hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, hipStream_t s);
-// End of a step (one block).  delta: the rows hold the moves of one
-// incremental step (added to F.sum), else the full sums of a streaming step
-// (they replace F.sum).  nb: blocks of the step kernel (counter slots).
-hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, int nb, hipStream_t s);
+// Step t of the streaming kernel (dv.C64 = the slot of C^t).
+hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, int t, hipStream_t s);
+// Step t of the incremental kernel.  fused: the end of step t - 1 (an
+// incremental step of the same grid) has not run; every block computes it
+// first and block 0 stores it.  Else dv.C64 = the slot of C^t.
+hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, int fused, hipStream_t s);
+// End of step t (one block).  delta: the rows hold the moves of an
+// incremental step (added to the sums of step t - 1), else the full sums of
+// a streaming step (they replace them).
+hipError_t launch_small_finish(const Dev& dv, const Fused& F, int t, int delta, hipStream_t s);
 // assign_out[i] = cluster of point i from the point states.
 hipError_t launch_small_unpack(const Fused& F, int64_t n, int32_t* assign_out, hipStream_t s);
 

@@ -174,7 +174,8 @@ struct Tables {
     int csu, kp;
 };
 
-__device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, const SmallLds& lay) {
+// Table pointers into LDS, and the block's sums and counters cleared.
+__device__ __forceinline__ Tables table_ptrs(const Dev& P, const SmallLds& lay) {
     Tables T;
     T.C = reinterpret_cast<float*>(km_smem + lay.off_c);
     T.h = reinterpret_cast<float*>(km_smem + lay.off_h);
@@ -187,23 +188,44 @@ __device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, cons
     T.bst = reinterpret_cast<uint64_t*>(km_smem + lay.off_misc + 16);
     T.csu = lay.csu;
     T.kp = lay.kp;
-    const int k = P.k, tid = threadIdx.x;
-    for (int i = tid; i < k * kD; i += kTp) T.C[(i / kD) * kCR + i % kD] = P.C32[i];
-    for (int i = tid; i < k * k; i += kTp) T.h[(i / k) * kSmallMaxK + i % k] = P.h[i];
-    for (int i = tid; i < k; i += kTp) {
-        // Clause 1 holds when v + D_a <= s(a) (D_a the cumulative drift
-        // rounded up, s(a) rounded down): thr is the largest float with
-        // thr + D_a <= s(a), so that the test is v <= thr.
-        const double x = (double)P.s[i] - F.dhi[i];   // +inf when k = 1
-        T.thr[i] = isinf(x) ? (float)x : f32_down(x - fabs(x) * 0x1p-50);
-        T.ec[i] = P.ec[i];
-        T.ddn[i] = F.ddn[i];
-    }
+    const int tid = threadIdx.x;
     for (int i = tid; i < kCopies * T.csu; i += kTp) T.acc[i] = 0;
     for (int i = tid; i < kCopies * T.kp; i += kTp) T.cnt[i] = 0;
     if (tid < kNumStat) T.bst[tid] = 0;
     if (tid < 3) T.qc[tid] = 0;
     return T;
+}
+
+// Clause-1 threshold of a cluster: Clause 1 holds when v + D_a <= s(a) (D_a
+// the cumulative drift rounded up, s(a) rounded down); thr is the largest
+// float with thr + D_a <= s(a), so that the test is v <= thr (+inf when k = 1).
+__device__ __forceinline__ float clause1_thr(float s, double dhi) {
+    const double x = (double)s - dhi;
+    return isinf(x) ? (float)x : f32_down(x - fabs(x) * 0x1p-50);
+}
+
+// The tables of step t from memory (the end of step t - 1 has run).
+__device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, const SmallLds& lay, int t) {
+    Tables T = table_ptrs(P, lay);
+    const int k = P.k, tid = threadIdx.x;
+    const double* dhi = F.dhi + (int64_t)slot2(t) * k;
+    for (int i = tid; i < k * kD; i += kTp) T.C[(i / kD) * kCR + i % kD] = P.C32[i];
+    for (int i = tid; i < k * k; i += kTp) T.h[(i / k) * kSmallMaxK + i % k] = P.h[i];
+    for (int i = tid; i < k; i += kTp) {
+        T.thr[i] = clause1_thr(P.s[i], dhi[i]);
+        T.ec[i] = P.ec[i];
+        T.ddn[i] = F.ddn[i];
+    }
+    return T;
+}
+
+// Block 0 of a step kernel clears the slots that step t + 1 accumulates into
+// (last read by the end of step t - 2, which has run).
+__device__ __forceinline__ void clear_next_slots(const Dev& P, const Fused& F, int t) {
+    if (blockIdx.x != 0) return;
+    uint64_t* r = F.rows + (int64_t)slot3(t + 1) * kSmallRows * P.L;
+    for (int i = threadIdx.x; i < kSmallRows * P.L; i += kTp) r[i] = 0;
+    if (threadIdx.x < kNumStat) F.stat[slot3(t + 1) * kNumStat + threadIdx.x] = 0;
 }
 
 struct Counters {
@@ -233,8 +255,8 @@ struct StepFlags {
 // result.
 template <int KC>
 __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, const Tables& T, const StepFlags& fl,
-                                       const float (&x)[kD], int64_t p, int inc, int cp, Counters& cn,
-                                       int* first_b) {
+                                       const double* C64, const float (&x)[kD], int64_t p, int inc, int cp,
+                                       Counters& cn, int* first_b) {
     const int k = P.k;
     float Dall[KC];
 #pragma unroll
@@ -292,7 +314,7 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
         const float band = 2.f * fl.gamma * (Db + D2) + 4.f * (sqrt_up(Db) + sqrt_up(D2)) * fl.ecmax +
                            8.f * fl.ecmax * fl.ecmax;
         if (D2 - Db <= band) {   // near tie: float64 decision, the oracle's tie rule
-            b = recheck64(x, P.C64, k, inc, Db, ub);
+            b = recheck64(x, C64, k, inc, Db, ub);
             cn.rc += 1;
         }
     }
@@ -314,7 +336,7 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
 // added) into accumulation row blockIdx % kSmallRows.  skip_zero: only nonzero
 // words are added.
 __device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const Tables& T, Counters& cn,
-                                   bool skip_zero) {
+                                   bool skip_zero, int t) {
     const int k = P.k, tid = threadIdx.x, lane = tid & 63;
     const uint64_t v0 = wave_sum_u64(cn.changed), v1 = wave_sum_u64(cn.comp), v2 = wave_sum_u64(cn.c1),
                    v3 = wave_sum_u64(cn.rc), v4 = wave_sum_u64(cn.iq);
@@ -328,8 +350,8 @@ __device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const 
         atomicAdd(b + kStInertia, (unsigned long long)v4);
     }
     __syncthreads();
-    unsigned long long* row =
-        reinterpret_cast<unsigned long long*>(F.rows + (int64_t)(blockIdx.x % kSmallRows) * P.L);
+    unsigned long long* row = reinterpret_cast<unsigned long long*>(
+        F.rows + ((int64_t)slot3(t) * kSmallRows + blockIdx.x % kSmallRows) * P.L);
     for (int i = tid; i < k * kD; i += kTp) {
         uint64_t v = 0;
 #pragma unroll
@@ -343,10 +365,170 @@ __device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const 
         // A count change is a 32-bit two's-complement value (moves may be negative).
         if (v || !skip_zero) atomicAdd(row + k * kD + i, (unsigned long long)(int64_t)(int32_t)v);
     }
-    if (tid < kNumStat) F.bcnt[(int64_t)blockIdx.x * kNumStat + tid] = T.bst[tid];   // the block's own slot
+    // The block's counters into the step's totals (the next step's stop test
+    // and bookkeeping read them).
+    if (tid < kNumStat)
+        atomicAdd(reinterpret_cast<unsigned long long*>(F.stat + slot3(t) * kNumStat + tid),
+                  (unsigned long long)T.bst[tid]);
 }
 
 }  // namespace
+
+// ---------------------------------------------------------------------------
+// End of step t: exact sums, new centroids C^{t+1} (member means; an empty
+// cluster keeps its centroid; spherical k-means projects them to the unit
+// sphere), drift and cumulative drift, centroid table h and s for step t + 1
+// (sections III-C and IV-A).  Run by one block of kTp threads: thread 16j + m
+// owns coordinate m of centroid j (k <= 16, d = 16), so that the per-centroid
+// terms are reductions over 16 lanes and one barrier separates the centroids
+// from the table.  LDS scratch: finish_lds(16, k) bytes.  delta: the rows of
+// step t hold the moves of an incremental step, added to the sums of step
+// t - 1; else they hold the full sums.  writer: this block stores the
+// results (sums of step t, C^{t+1}, D^{t+1}, the float32 tables).  T
+// (nullable): the LDS tables of step t + 1 are filled too (Clause-1
+// thresholds, float32 rows, h rows, ec, ddn) and c64n receives C^{t+1} in
+// float64.  Returns the largest centroid rounding error ec.
+
+__device__ __forceinline__ double sum16(double v) {
+#pragma unroll
+    for (int o = 8; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+__device__ float end_of_step(const Dev& P, const Fused& F, int t, bool delta, bool writer, unsigned char* scratch,
+                             Tables* T, double* c64n) {
+    const int tid = threadIdx.x, j = tid >> 4, m = tid & 15;
+    const int k = P.k, L = P.L, kd = k * kD;
+    const bool live = j < k;
+    double* cn = reinterpret_cast<double*>(scratch);    // k x 16 new centroids
+    float* ecn = reinterpret_cast<float*>(cn + kd);     // k rounding errors
+    const uint64_t* rows = F.rows + (int64_t)slot3(t) * kSmallRows * L;
+    const uint64_t* sprev = F.sum + (int64_t)slot2(t - 1) * (kd + k);
+    uint64_t* snow = F.sum + (int64_t)slot2(t) * (kd + k);
+    const double* cold_p = F.c64 + (int64_t)slot2(t) * kd;
+    double* cnew_p = F.c64 + (int64_t)slot2(t + 1) * kd;
+
+    // One round of loads: the old coordinate, its column of every
+    // accumulation row and the centroid's count column.
+    const int e = live ? j * kD + m : 0;
+    const int ce = live ? kd + j : 0;
+    const double cold = cold_p[e];
+    uint64_t tv[kSmallRows], tc[kSmallRows];
+#pragma unroll
+    for (int r = 0; r < kSmallRows; ++r) {
+        tv[r] = rows[(int64_t)r * L + e];
+        tc[r] = rows[(int64_t)r * L + ce];
+    }
+    uint64_t v = delta ? sprev[e] : 0, cnt = delta ? sprev[ce] : 0;   // the moves add to the sums of step t - 1
+#pragma unroll
+    for (int r = 0; r < kSmallRows; ++r) {
+        v += tv[r];
+        cnt += tc[r];
+    }
+    if (writer && live) {
+        snow[e] = v;
+        if (m == 0) snow[ce] = cnt;
+    }
+    // Member mean of the exact sums; an empty cluster keeps its centroid.
+    double cnew = cold;
+    if (cnt > 0) cnew = ((double)(int64_t)(v - cnt * kMagicBits) * P.qinv) / (double)cnt;
+    if (P.flags & KM_FLAG_SPHERICAL) {   // spherical k-means: the mean projected to the unit sphere
+        const double ss = sum16(cnew * cnew);
+        if (cnt > 0) cnew = ss > 0.0 ? cnew / sqrt(ss) : cold;   // a zero mean keeps the centroid
+    }
+    const float c32 = (float)cnew;
+    const double df = cnew - cold, rr = (double)c32 - cnew;
+    const double a = sum16(df * df), b = sum16(rr * rr), c2 = sum16((double)c32 * (double)c32);
+    // Drift f(c) and its cumulative sums, with margins far above the float64
+    // rounding of the drift and of the running sums.
+    const double fd = sqrt(a);
+    const double hi = (F.dhi[(int64_t)slot2(t) * k + (live ? j : 0)] + fd * (1.0 + 0x1p-40)) * (1.0 + 0x1p-50);
+    const double lo = (F.dlo[(int64_t)slot2(t) * k + (live ? j : 0)] + fd * (1.0 - 0x1p-40)) * (1.0 - 0x1p-50);
+    const float ec = f32_up(sqrt(b) * (1.0 + 0x1p-40));
+    if (live) {
+        cn[e] = cnew;
+        if (m == 0) ecn[j] = ec;
+        if (writer) {
+            cnew_p[e] = cnew;
+            P.C32[e] = c32;
+            if (m == 0) {
+                P.f[j] = f32_up(fd * (1.0 + 0x1p-40));
+                F.dhi[(int64_t)slot2(t + 1) * k + j] = hi;
+                F.dlo[(int64_t)slot2(t + 1) * k + j] = lo;
+                F.dup[j] = f32_up(hi);
+                F.ddn[j] = f32_down(lo);
+                P.ec[j] = ec;
+                P.cn2[j] = (float)c2;
+            }
+        }
+        if (T) {
+            T->C[j * kCR + m] = c32;
+            c64n[e] = cnew;
+            if (m == 0) {
+                T->ec[j] = ec;
+                T->ddn[j] = f32_down(lo);
+            }
+        }
+    }
+    __syncthreads();
+    // Half distance from centroid j to centroid m, rounded down; s(j) is
+    // the smallest over m != j.
+    float hv = 0.f;
+    if (live && m < k && m != j) {
+        double acc = 0.0;
+#pragma unroll
+        for (int q = 0; q < kD; ++q) {
+            const double tq = cn[j * kD + q] - cn[m * kD + q];
+            acc = fma(tq, tq, acc);
+        }
+        hv = f32_down(0.5 * sqrt(acc) * (1.0 - 0x1p-40));
+    }
+    float sv = (live && m < k && m != j) ? hv : INFINITY;
+#pragma unroll
+    for (int o = 8; o > 0; o >>= 1) sv = fminf(sv, __shfl_xor(sv, o));
+    if (live) {
+        if (m < k && writer) P.h[j * k + m] = hv;
+        if (T) T->h[j * kSmallMaxK + m] = hv;
+        if (m == 0) {
+            if (writer) P.s[j] = sv;
+            if (T) T->thr[j] = clause1_thr(sv, hi);
+        }
+    }
+    float em = 0.f;
+    for (int jc = 0; jc < k; ++jc) em = fmaxf(em, ecn[jc]);
+    return em;
+}
+
+// Bookkeeping of step t by one thread: the step's counters, the history
+// record and totals, the iteration count and the stop test.
+__device__ void step_books(const Dev& P, const Fused& F, int t, float ecmax) {
+    const uint64_t* sc = F.stat + slot3(t) * kNumStat;
+    IterState* st = P.st;
+    st->ec_max = ecmax;
+    const int64_t changed = (int64_t)sc[kStChanged];
+    const int64_t computed = (int64_t)sc[kStComputed];
+    const int64_t c1 = (int64_t)sc[kStClause1];
+    const int64_t rc = (int64_t)sc[kStRecheck];
+    const int64_t iq = (int64_t)sc[kStInertia];
+    const double inertia = (P.flags & KM_FLAG_STATS) ? (double)iq * P.iinv : NAN;
+    IterRec& r = P.rec[t % kHistCap];
+    r.changed = changed;
+    r.computed = computed;
+    r.clause1 = c1;
+    r.rechecks = rc;
+    r.inertia = inertia;
+    st->changed_last = changed;
+    st->tot_computed += computed;
+    st->tot_clause1 += c1;
+    st->tot_rechecks += rc;
+    st->inertia_last = inertia;
+    st->t = t + 1;
+    const bool tol_hit = (double)changed < st->tol_n;
+    if (tol_hit || t + 1 >= st->max_iters) {
+        st->done = 1;
+        st->converged = tol_hit ? 1 : 0;
+    }
+}
 
 // ---------------------------------------------------------------------------
 // The streaming kernel.  Wave w of a tile owns points 64w .. 64w+63; lane j
@@ -355,7 +537,7 @@ __device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const 
 // wave's row rho = 16i + l / 4.
 
 template <int KC>
-__global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k_small(Dev P, Fused F) {
+__global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k_small(Dev P, Fused F, int t) {
     IterState* st = P.st;
     if (st->done) {
         if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
@@ -364,10 +546,11 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
     if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 1;
 
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-    const StepFlags fl{st->t == 0, !(P.flags & KM_FLAG_NO_PRUNE), (P.flags & KM_FLAG_STATS) != 0, P.gamma,
+    const StepFlags fl{t == 0, !(P.flags & KM_FLAG_NO_PRUNE), (P.flags & KM_FLAG_STATS) != 0, P.gamma,
                        st->ec_max};
     const SmallLds lay = small_lds(P.k, true);
-    const Tables T = load_tables(P, F, lay);
+    const Tables T = load_tables(P, F, lay, t);
+    clear_next_slots(P, F, t);
     float* qr = reinterpret_cast<float*>(km_smem + lay.off_qr);   // queued rows
     int* qp = reinterpret_cast<int*>(km_smem + lay.off_qp);       // queued point index
     int* qa = reinterpret_cast<int*>(km_smem + lay.off_qa);       // queued incumbent (-1: none)
@@ -406,7 +589,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
                 x[4 * c + 2] = v.z;
                 x[4 * c + 3] = v.w;
             }
-            settle_survivor<KC>(P, F, T, fl, x, qp[e], qa[e], tid & (kCopies - 1), cn, qa + e);
+            settle_survivor<KC>(P, F, T, fl, P.C64, x, qp[e], qa[e], tid & (kCopies - 1), cn, qa + e);
         }
     };
 
@@ -539,7 +722,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
             first_sums(0, queued);
         }
     }
-    flush_block(P, F, T, cn, false);
+    flush_block(P, F, T, cn, false, t);
 }
 
 // ---------------------------------------------------------------------------
@@ -555,16 +738,16 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
 // shared, through atomics.
 
 template <int KC>
-__global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P, Fused F) {
+__global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P, Fused F, int t,
+                                                                                      int fused) {
     IterState* st = P.st;
-    if (st->done || st->t == 0) {   // the first step always runs the streaming kernel
+    if (st->done) {   // an earlier end of step stopped the run
         if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
         return;
     }
-    if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 1;
-
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-    const StepFlags fl{false, !(P.flags & KM_FLAG_NO_PRUNE), false, P.gamma, st->ec_max};
+    // The changed count of step t - 1, for the stop test of a fused start.
+    const uint64_t chg_prev = fused ? F.stat[slot3(t - 1) * kNumStat + kStChanged] : 0;
     const int64_t n = P.n;
     const int nwt = (int)((n + kIncWaveTile - 1) / kIncWaveTile);   // wave tiles
     // Block b owns wave tiles [b * nwt / G, (b + 1) * nwt / G); its waves take
@@ -583,7 +766,30 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     if (wt < wt_hi) load_states(wt);   // the first states load while the tables are staged
 
     const SmallLds lay = small_lds(P.k, false);
-    const Tables T = load_tables(P, F, lay);
+    // Fused start: every block forms the end of step t - 1 itself (the same
+    // integer totals and float64 operations, so the same tables) in the LDS of
+    // the gathered rows, and block 0 stores it (and the bookkeeping).  The
+    // float64 centroids of near-tie decisions are then the LDS copy.
+    double* c64n = reinterpret_cast<double*>(km_smem + lay.off_c64);
+    Tables T;
+    float ecmax;
+    if (fused) {
+        T = table_ptrs(P, lay);
+        unsigned char* scr = km_smem + lay.off_qr;
+        ecmax = end_of_step(P, F, t - 1, true, blockIdx.x == 0, scr, &T, c64n);
+        if (blockIdx.x == 0 && tid == 0) step_books(P, F, t - 1, ecmax);
+        if ((double)chg_prev < st->tol_n || t >= st->max_iters) {   // the run stops after step t - 1
+            if (blockIdx.x == 0 && tid == 0) st->active = 0;
+            return;
+        }
+    } else {
+        T = load_tables(P, F, lay, t);
+        ecmax = st->ec_max;
+    }
+    if (blockIdx.x == 0 && tid == 0) st->active = 1;
+    clear_next_slots(P, F, t);
+    const StepFlags fl{false, !(P.flags & KM_FLAG_NO_PRUNE), false, P.gamma, ecmax};
+    const double* C64 = fused ? c64n : P.C64;
     // Further tiles: lane 0 takes one from the block's counter (in the queue
     // counters, which this kernel does not otherwise use).
     auto grab = [&]() __attribute__((always_inline)) {
@@ -635,7 +841,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
                 x[4 * c + 2] = v.z;
                 x[4 * c + 3] = v.w;
             }
-            settle_survivor<KC>(P, F, T, fl, x, bp, binc, lane & (kCopies - 1), cn, nullptr);
+            settle_survivor<KC>(P, F, T, fl, C64, x, bp, binc, lane & (kCopies - 1), cn, nullptr);
         }
         bcnt = 0;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -702,188 +908,16 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
         }
         if (!more) break;
     }
-    flush_block(P, F, T, cn, true);
+    flush_block(P, F, T, cn, true, t);
 }
 
-// ---------------------------------------------------------------------------
-// End of a step (one block, launched after the step kernel): totals of the
-// accumulation rows (which it clears), new centroids, drift and cumulative
-// drift, stop test, centroid table for the next step.  delta: the rows hold
-// the moves of an incremental step (added to the previous sums), else the full
-// sums of a streaming step (they replace them).
-
-__global__ __launch_bounds__(kTp) void k_small_finish(Dev P, Fused F, int delta, int nb) {
-    constexpr int nt = kTp;
-    IterState* st = P.st;
-    if (!st->active) return;   // the step kernel found the run stopped
-    const int tid = threadIdx.x;
-    const int k = P.k, d = P.d, L = P.L;
-    uint64_t* tot = reinterpret_cast<uint64_t*>(km_smem);
-    double* cn = reinterpret_cast<double*>(tot + L);
-    double* dr = cn + k * d;
-    double* de = dr + k * d;
-    float* hl = reinterpret_cast<float*>(de + k * d);
-    float* ecn = hl + k * k;
-    // One round of loads: the old centroids and every accumulation row.
-    double cold[kSmallMaxK * 16 / 256 + 1];
-#pragma unroll
-    for (int q = 0; q * nt < kSmallMaxK * 16; ++q) {
-        const int e = tid + q * nt;
-        cold[q] = e < k * d ? P.C64[e] : 0.0;
-    }
-    for (int col = tid; col < L; col += nt) {
-        uint64_t t[kSmallRows];
-#pragma unroll
-        for (int r = 0; r < kSmallRows; ++r) t[r] = F.rows[(int64_t)r * L + col];
-        uint64_t v = 0;
-#pragma unroll
-        for (int r = 0; r < kSmallRows; ++r) v += t[r];
-        if (col < k * d + k) {   // sums and counts: after the moves (delta), or the full sums
-            if (delta) v += F.sum[col];
-            F.sum[col] = v;
-        }
-        tot[col] = v;
-#pragma unroll
-        for (int r = 0; r < kSmallRows; ++r) F.rows[(int64_t)r * L + col] = 0;
-    }
-    {   // counters: the blocks' slots, summed per wave, then over the waves
-        uint64_t c[kNumStat] = {0, 0, 0, 0, 0};
-        for (int b = tid; b < nb; b += nt)
-#pragma unroll
-            for (int q = 0; q < kNumStat; ++q) c[q] += F.bcnt[(int64_t)b * kNumStat + q];
-        __syncthreads();   // tot is complete; its counter words are rebuilt below
-        uint64_t* red = tot + L;   // scratch before the centroid arrays are written
-#pragma unroll
-        for (int q = 0; q < kNumStat; ++q) {
-            const uint64_t v = wave_sum_u64(c[q]);
-            if ((tid & 63) == 0) red[(tid >> 6) * kNumStat + q] = v;
-        }
-        __syncthreads();
-        if (tid < kNumStat) {
-            uint64_t v = 0;
-            for (int wv = 0; wv < nt / 64; ++wv) v += red[wv * kNumStat + tid];
-            tot[k * d + k + tid] = v;
-        }
-    }
-    __syncthreads();
-    // New centroids: member means of the exact sums; empty clusters keep theirs.
-#pragma unroll
-    for (int q = 0; q * nt < kSmallMaxK * 16; ++q) {
-        const int e = tid + q * nt;
-        if (e >= k * d) break;
-        const int jc = e / d;
-        const uint64_t count = tot[k * d + jc];
-        double cnew = cold[q];
-        if (count > 0) {
-            const int64_t qs = (int64_t)(tot[e] - count * kMagicBits);
-            cnew = ((double)qs * P.qinv) / (double)count;
-        }
-        cn[e] = cnew;
-    }
-    if (P.flags & KM_FLAG_SPHERICAL) {   // spherical k-means: means projected to the unit sphere
-        __syncthreads();
-        for (int jc = tid; jc < k; jc += nt) {
-            if (tot[k * d + jc] == 0) continue;   // empty: the old (unit) centroid is kept
-            double ss = 0.0;
-            for (int m = 0; m < d; ++m) ss = fma(cn[jc * d + m], cn[jc * d + m], ss);
-            if (ss > 0.0) {
-                const double r = sqrt(ss);
-                for (int m = 0; m < d; ++m) cn[jc * d + m] /= r;
-            } else {
-                for (int m = 0; m < d; ++m) cn[jc * d + m] = P.C64[jc * d + m];   // zero mean: kept
-            }
-        }
-        __syncthreads();
-    }
-#pragma unroll
-    for (int q = 0; q * nt < kSmallMaxK * 16; ++q) {
-        const int e = tid + q * nt;
-        if (e >= k * d) break;
-        const double cnew = cn[e];
-        const double df = cnew - cold[q];
-        const float c32 = (float)cnew;
-        const double rr = (double)c32 - cnew;
-        dr[e] = df * df;
-        de[e] = rr * rr;
-        P.C64[e] = cnew;
-        P.C32[e] = c32;
-    }
-    __syncthreads();
-    for (int jc = tid; jc < k; jc += nt) {
-        double a = 0.0, b = 0.0, c2 = 0.0;
-        for (int m = 0; m < d; ++m) {
-            a += dr[jc * d + m];
-            b += de[jc * d + m];
-            const double cv = (double)(float)cn[jc * d + m];
-            c2 = fma(cv, cv, c2);
-        }
-        // Drift f(c) and its cumulative sums, with margins far above the
-        // float64 rounding of the drift and of the running sums.
-        const double fd = sqrt(a);
-        P.f[jc] = f32_up(fd * (1.0 + 0x1p-40));
-        const double hi = (F.dhi[jc] + fd * (1.0 + 0x1p-40)) * (1.0 + 0x1p-50);
-        const double lo = (F.dlo[jc] + fd * (1.0 - 0x1p-40)) * (1.0 - 0x1p-50);
-        F.dhi[jc] = hi;
-        F.dlo[jc] = lo;
-        F.dup[jc] = f32_up(hi);
-        F.ddn[jc] = f32_down(lo);
-        const float e = f32_up(sqrt(b) * (1.0 + 0x1p-40));
-        P.ec[jc] = e;
-        ecn[jc] = e;
-        P.cn2[jc] = (float)c2;
-    }
-    // Half centroid distances of the new centroids, rounded down.
-    for (int pr = tid; pr < k * k; pr += nt) {
-        const int i = pr / k, jc = pr - i * k;
-        float hv = 0.f;
-        if (i != jc) {
-            double acc = 0.0;
-            for (int m = 0; m < d; ++m) {
-                const double t = cn[i * d + m] - cn[jc * d + m];
-                acc = fma(t, t, acc);
-            }
-            hv = f32_down(0.5 * sqrt(acc) * (1.0 - 0x1p-40));
-        }
-        hl[pr] = hv;
-        P.h[pr] = hv;
-    }
-    __syncthreads();
-    for (int i = tid; i < k; i += nt) {
-        float mn = INFINITY;
-        for (int jc = 0; jc < k; ++jc)
-            if (jc != i) mn = fminf(mn, hl[i * k + jc]);
-        P.s[i] = mn;
-    }
-    if (tid == 0) {
-        float em = 0.f;
-        for (int jc = 0; jc < k; ++jc) em = fmaxf(em, ecn[jc]);
-        st->ec_max = em;
-        const uint64_t* sc = tot + k * d + k;
-        const int64_t changed = (int64_t)sc[kStChanged];
-        const int64_t computed = (int64_t)sc[kStComputed];
-        const int64_t c1 = (int64_t)sc[kStClause1];
-        const int64_t rc = (int64_t)sc[kStRecheck];
-        const int64_t iq = (int64_t)sc[kStInertia];
-        const double inertia = (P.flags & KM_FLAG_STATS) ? (double)iq * P.iinv : NAN;
-        const int t = st->t;
-        IterRec& r = P.rec[t % kHistCap];
-        r.changed = changed;
-        r.computed = computed;
-        r.clause1 = c1;
-        r.rechecks = rc;
-        r.inertia = inertia;
-        st->changed_last = changed;
-        st->tot_computed += computed;
-        st->tot_clause1 += c1;
-        st->tot_rechecks += rc;
-        st->inertia_last = inertia;
-        st->t = t + 1;
-        const bool tol_hit = (double)changed < st->tol_n;
-        if (tol_hit || t + 1 >= st->max_iters) {
-            st->done = 1;
-            st->converged = tol_hit ? 1 : 0;
-        }
-    }
+// End of step t as its own launch (one block): after a streaming step, and
+// after an incremental step whose results are needed before the next step
+// (then the next step starts unfused).
+__global__ __launch_bounds__(kTp) void k_small_finish(Dev P, Fused F, int t, int delta) {
+    if (!P.st->active) return;   // step t did not run (the run had stopped)
+    const float em = end_of_step(P, F, t, delta != 0, true, km_smem, nullptr, nullptr);
+    if (threadIdx.x == 0) step_books(P, F, t, em);
 }
 
 // Assignments from the point states.
@@ -933,10 +967,10 @@ int inc_lds_bytes(int k) { return small_lds(k, false).bytes; }
 
 int small_finish_lds_bytes(int k) { return finish_lds(16, k); }
 
-hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, hipStream_t s) {
+hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, int t, hipStream_t s) {
     switch (small_kc(dv.k)) {
-#define KM_LAUNCH(KC_)                                                                       \
-    case KC_: hipLaunchKernelGGL((k_small<KC_>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F); break;
+#define KM_LAUNCH(KC_)                                                                          \
+    case KC_: hipLaunchKernelGGL((k_small<KC_>), dim3(dv.G), dim3(kTp), lds_bytes, s, dv, F, t); break;
         KM_SMALL_KCS(KM_LAUNCH)
 #undef KM_LAUNCH
         default: return hipErrorInvalidValue;
@@ -944,10 +978,10 @@ hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, hipStream_
     return hipGetLastError();
 }
 
-hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, hipStream_t s) {
+hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, int fused, hipStream_t s) {
     switch (small_kc(dv.k)) {
-#define KM_LAUNCH(KC_)                                                                     \
-    case KC_: hipLaunchKernelGGL((k_inc<KC_>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F); break;
+#define KM_LAUNCH(KC_)                                                                                \
+    case KC_: hipLaunchKernelGGL((k_inc<KC_>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F, t, fused); break;
         KM_SMALL_KCS(KM_LAUNCH)
 #undef KM_LAUNCH
         default: return hipErrorInvalidValue;
@@ -956,8 +990,8 @@ hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, hi
 }
 
 
-hipError_t launch_small_finish(const Dev& dv, const Fused& F, int delta, int nb, hipStream_t s) {
-    hipLaunchKernelGGL(k_small_finish, dim3(1), dim3(kTp), finish_lds(dv.d, dv.k), s, dv, F, delta, nb);
+hipError_t launch_small_finish(const Dev& dv, const Fused& F, int t, int delta, hipStream_t s) {
+    hipLaunchKernelGGL(k_small_finish, dim3(1), dim3(kTp), finish_lds(dv.d, dv.k), s, dv, F, t, delta);
     return hipGetLastError();
 }
 
