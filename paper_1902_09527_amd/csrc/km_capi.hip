@@ -285,10 +285,14 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_i, isym, c->tp, c->lds_inc));
             if (per_cu_i < 1) return KM_ERR_UNSUPPORTED;
             // Resident blocks (the same count on every CU), at least one wave
-            // tile per wave.
+            // tile per wave; small inputs still spread over up to one block
+            // per CU (one tile per block), which shortens each block's chain
+            // of dependent tiles.
             const int64_t nwt = (n + km::kIncWaveTile - 1) / km::kIncWaveTile;
             int64_t gi = (int64_t)per_cu_i * cus;
-            if (gi > nwt / 4) gi = nwt / 4 > 0 ? nwt / 4 : 1;
+            const int64_t spread = nwt < cus ? nwt : cus;
+            const int64_t want = nwt / 4 > spread ? nwt / 4 : spread;
+            if (gi > want) gi = want > 0 ? want : 1;
             c->gi = (int)gi;
         }
     } else if (!(c->flags & KM_FLAG_LARGE_PATH)) {
