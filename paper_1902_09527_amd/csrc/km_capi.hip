@@ -298,8 +298,9 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     } else if (!(c->flags & KM_FLAG_LARGE_PATH)) {
         c->variant = km::assign_variant(d, k, aligned, (c->flags & KM_FLAG_VECTOR_ONLY) != 0, elkan);
         const bool h_lds = km::assign_h_lds(c->variant % 16, k);
-        for (int tp = 256; c->tp == 0 && tp >= 64; tp /= 2) {
-            int bytes = km::assign_lds(d, k, tp, h_lds).bytes;
+        const bool wide = km::assign_wide(c->variant);   // blocks of 512 threads only
+        for (int tp = wide ? 512 : 256; c->tp == 0 && tp >= (wide ? 512 : 64); tp /= 2) {
+            int bytes = km::assign_lds(d, k, tp, h_lds, wide).bytes;
             if (bytes <= max_lds) {
                 c->tp = tp;
                 c->lds = bytes;

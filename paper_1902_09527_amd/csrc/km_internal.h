@@ -118,8 +118,15 @@ __host__ __device__ inline int xs_stride(int d) { return ((d + 3) / 4) * 4 + 4; 
 // Dynamic LDS layout of the assignment kernel for tile size tp.
 struct AssignLds {
     int off_acc, off_cnt, off_c, off_f, off_s, off_ec, off_cn, off_h, off_x, off_sa, off_su, off_sd,
-        off_sq, off_misc, bytes;
+        off_sq, off_misc, off_ca, bytes;
 };
+
+// The matrix-core variants with four 32-centroid blocks run blocks of 512
+// threads (two waves per SIMD) and read their centroid operands from LDS
+// instead of registers.
+__host__ __device__ inline bool assign_wide(int variant) { return variant % 16 == 4; }
+// LDS bytes of those operands: 4 blocks x d/2 k-steps x 64 lanes.
+__host__ __device__ inline int wide_ca_bytes(int d) { return 4 * (d / 2) * 64 * 4; }
 
 // The vector survivor scans keep the half-distance table in LDS up to this k.
 constexpr int kHLdsMaxK = 64;
@@ -130,7 +137,7 @@ __host__ __device__ inline bool assign_h_lds(int kb, int k) { return (kb == 0 ||
 // Centroid count rounded up to the 32-row blocks of the matrix-core path.
 __host__ __device__ inline int k_pad32(int k) { return (k + 31) / 32 * 32; }
 
-__host__ __device__ inline AssignLds assign_lds(int d, int k, int tp, bool h_lds) {
+__host__ __device__ inline AssignLds assign_lds(int d, int k, int tp, bool h_lds, bool wide = false) {
     AssignLds L;
     int o = 0;
     auto take = [&](int bytes, int align) {
@@ -153,6 +160,7 @@ __host__ __device__ inline AssignLds assign_lds(int d, int k, int tp, bool h_lds
     L.off_sd = take(4 * tp, 16);
     L.off_sq = take(4 * tp, 16);
     L.off_misc = take(64, 16);   // two survivor counters (int) at 0, kNumStat uint64 counters at 16
+    L.off_ca = take(wide ? wide_ca_bytes(d) : 0, 16);
     L.bytes = (o + 15) / 16 * 16;
     return L;
 }

@@ -478,9 +478,10 @@ __device__ inline void klane_survivors(const ScanCtx& W, const float* hl, int ns
 // path's.
 
 template <int D, int KB>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1 : 2))) void k_assign(Dev P) {
+__global__ __launch_bounds__(KB == 4 ? 512 : 256) __attribute__((amdgpu_waves_per_eu(2))) void k_assign(Dev P) {
     constexpr bool ELK = KB == 8;          // Elkan's lower bounds, vector scan
     constexpr int MB = ELK ? 0 : KB;       // 32-centroid blocks of the matrix-core path
+    constexpr bool WIDE = KB == 4;         // 512 threads, centroid operands in LDS
     IterState* st = P.st;
     if (st->done) {
         if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
@@ -500,7 +501,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
     const int xs = xs_stride(d);
 
     const bool h_lds = assign_h_lds(KB, k);
-    const AssignLds lay = assign_lds(d, k, tp, h_lds);
+    const AssignLds lay = assign_lds(d, k, tp, h_lds, WIDE);
     unsigned char* smem = km_smem;
     uint64_t* acc = reinterpret_cast<uint64_t*>(smem + lay.off_acc);
     uint32_t* cnt = reinterpret_cast<uint32_t*>(smem + lay.off_cnt);
@@ -539,17 +540,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
     // MFMA k-step s pairs dimension s with dimension D/2 + s.
     constexpr int kCb = MB > 0 ? MB : 1;
     constexpr int kHalf = D > 0 ? D / 2 : 1;
-    float creg[kCb][kHalf];
+    float creg[WIDE ? 1 : kCb][WIDE ? 1 : kHalf];
+    float* ca = reinterpret_cast<float*>(smem + lay.off_ca);   // WIDE: operand (cb, q) of lane l at (cb*kHalf + q)*64 + l
     float cnmax = 0.f;
     if constexpr (MB > 0) {
         static_assert(D == 16 || D == 32, "matrix-core path needs d = 16 or 32");
         const int lane = tid & 63, half = lane >> 5;
+        if constexpr (WIDE) {
+            for (int i = tid; i < MB * kHalf * 64; i += tp) {
+                const int l = i & 63, q = (i >> 6) % kHalf, cb = i / (64 * kHalf);
+                const int j = cb * 32 + (l & 31);
+                ca[i] = j < k ? P.C32[(int64_t)j * D + (l >> 5) * kHalf + q] : 0.f;
+            }
+        } else {
 #pragma unroll
-        for (int cb = 0; cb < MB; ++cb) {
-            const int j = cb * 32 + (lane & 31);
+            for (int cb = 0; cb < MB; ++cb) {
+                const int j = cb * 32 + (lane & 31);
 #pragma unroll
-            for (int q = 0; q < kHalf; ++q)
-                creg[cb][q] = j < k ? P.C32[(int64_t)j * D + half * kHalf + q] : 0.f;
+                for (int q = 0; q < kHalf; ++q)
+                    creg[cb][q] = j < k ? P.C32[(int64_t)j * D + half * kHalf + q] : 0.f;
+            }
         }
         for (int i = tid; i < MB * 32; i += tp) cn2s[i] = i < k ? P.cn2[i] : INFINITY;
         __syncthreads();
@@ -688,7 +698,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(KB == 4 ? 1
                 for (int q = 0; q < kHalf; ++q)
 #pragma unroll
                     for (int cb = 0; cb < MB; ++cb)
-                        dot[cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(creg[cb][q], xh[q], dot[cb], 0, 0, 0);
+                        dot[cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                            WIDE ? ca[(cb * kHalf + q) * 64 + lane] : creg[WIDE ? 0 : cb][WIDE ? 0 : q], xh[q],
+                            dot[cb], 0, 0, 0);
                 // Register e of block cb holds centroid 32*cb + 8*(e/4) + 4*half + e%4.
                 auto cent = [&](int cb, int e) { return cb * 32 + 8 * (e >> 2) + 4 * half + (e & 3); };
                 float e1 = INFINITY;
