@@ -375,6 +375,10 @@ def main() -> int:
                    "n": n, "d": d, "k": k, "max_iters": w.max_iters, "tol": w.tol,
                    "timed": "first %d iterations from the seeded centroids" % K, "path": path},
         "eff_dist_evals_per_s": lloyd / elapsed,
+        # The bytes a full-read Lloyd step moves (every row and its point
+        # state) over the measured step time, against the HBM peak: above 1
+        # when pruning skips rows.
+        "full_read_equiv_hbm_frac": n * (4 * d + 4) / (elapsed / K) / (HBM_PEAK_GBS * 1e9),
         "computed_dist_evals_per_s": computed / elapsed,
         "pruned_frac": 1.0 - computed / lloyd,
         "clause1_frac": float(hist["clause1"].sum()) / (n * K),

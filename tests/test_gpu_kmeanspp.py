@@ -14,6 +14,7 @@ import torch
 
 import oracle
 import synth
+from parity import check_assign, check_centroids
 
 import paper_1902_09527_amd as km
 from paper_1902_09527_amd import _native as N
@@ -140,3 +141,25 @@ def test_large_k_workload_prefix_and_sampled_rows():
     D2 = got["D2"].cpu().numpy()[rows]
     np.testing.assert_allclose(D2, np.maximum(bf, 0.0), rtol=1e-9, atol=1e-9 * float(bf.max()))
     assert got["stats"]["computed"] < X.shape[0] * w.k
+
+
+def test_best_of_restarts_matches_the_oracle():
+    # The paper's k-means++ with r restarts: seed, run, keep the least final
+    # inertia.  Each run against the oracle's seeding and Lloyd's run.
+    X, _ = synth.blobs(20000 + 13, 16, 12, seed=314, spread=3.0, sigma=1.5)
+    k, r, iters = 12, 4, 15
+    U = np.random.default_rng(314).random((r, k))
+    got = km.run_pp_best(_gpu(X), k, U, iters)
+    inert = []
+    for i in range(r):
+        seeds = oracle.kmeanspp(X, k, U[i])
+        ref = oracle.lloyd(X, seeds["C"], iters)
+        inert.append(ref["inertia"][-1])
+        assert got["inertia"][i] == pytest.approx(inert[-1], rel=1e-5)
+    want = int(np.argmin(inert))
+    srt = np.sort(inert)
+    if srt[1] - srt[0] > 1e-4 * srt[0]:   # a clear winner
+        assert got["best"] == want
+    ref = oracle.lloyd(X, oracle.kmeanspp(X, k, U[got["best"]])["C"], iters)
+    check_assign(got["assign"].cpu().numpy(), ref["assign"], ref["best"], ref["second"], "best run")
+    check_centroids(got["C"].cpu().numpy(), ref["C"], X, "best run")
