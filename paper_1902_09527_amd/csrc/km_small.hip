@@ -378,7 +378,8 @@ __device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const 
 // End of step t: exact sums, new centroids C^{t+1} (member means; an empty
 // cluster keeps its centroid; spherical k-means projects them to the unit
 // sphere), drift and cumulative drift, centroid table h and s for step t + 1
-// (sections III-C and IV-A).  Run by one block of kTp threads: thread 16j + m
+// (sections III-C and IV-A), as eos_load then eos_finish.  Run by one
+// block of kTp threads: thread 16j + m
 // owns coordinate m of centroid j (k <= 16, d = 16), so that the per-centroid
 // terms are reductions over 16 lanes and one barrier separates the centroids
 // from the table.  LDS scratch: finish_lds(16, k) bytes.  delta: the rows of
@@ -395,35 +396,54 @@ __device__ __forceinline__ double sum16(double v) {
     return v;
 }
 
-__device__ float end_of_step(const Dev& P, const Fused& F, int t, bool delta, bool writer, unsigned char* scratch,
-                             Tables* T, double* c64n) {
+// The loads of the end of step t (issued together; summed by eos_finish):
+// the thread's old coordinate, its column of every accumulation row, the
+// centroid's count column, the sums of step t - 1 (delta) and the
+// cumulative drifts.
+struct EosIn {
+    double cold, dhi, dlo;
+    uint64_t tv[kSmallRows], tc[kSmallRows], sv, sc;
+};
+
+__device__ __forceinline__ EosIn eos_load(const Dev& P, const Fused& F, int t, bool delta) {
     const int tid = threadIdx.x, j = tid >> 4, m = tid & 15;
     const int k = P.k, L = P.L, kd = k * kD;
     const bool live = j < k;
-    double* cn = reinterpret_cast<double*>(scratch);    // k x 16 new centroids
-    float* ecn = reinterpret_cast<float*>(cn + kd);     // k rounding errors
     const uint64_t* rows = F.rows + (int64_t)slot3(t) * kSmallRows * L;
     const uint64_t* sprev = F.sum + (int64_t)slot2(t - 1) * (kd + k);
-    uint64_t* snow = F.sum + (int64_t)slot2(t) * (kd + k);
-    const double* cold_p = F.c64 + (int64_t)slot2(t) * kd;
-    double* cnew_p = F.c64 + (int64_t)slot2(t + 1) * kd;
-
-    // One round of loads: the old coordinate, its column of every
-    // accumulation row and the centroid's count column.
     const int e = live ? j * kD + m : 0;
     const int ce = live ? kd + j : 0;
-    const double cold = cold_p[e];
-    uint64_t tv[kSmallRows], tc[kSmallRows];
+    EosIn in;
+    in.cold = F.c64[(int64_t)slot2(t) * kd + e];
 #pragma unroll
     for (int r = 0; r < kSmallRows; ++r) {
-        tv[r] = rows[(int64_t)r * L + e];
-        tc[r] = rows[(int64_t)r * L + ce];
+        in.tv[r] = rows[(int64_t)r * L + e];
+        in.tc[r] = rows[(int64_t)r * L + ce];
     }
-    uint64_t v = delta ? sprev[e] : 0, cnt = delta ? sprev[ce] : 0;   // the moves add to the sums of step t - 1
+    in.sv = delta ? sprev[e] : 0;   // the moves add to the sums of step t - 1
+    in.sc = delta ? sprev[ce] : 0;
+    in.dhi = F.dhi[(int64_t)slot2(t) * k + (live ? j : 0)];
+    in.dlo = F.dlo[(int64_t)slot2(t) * k + (live ? j : 0)];
+    return in;
+}
+
+__device__ float eos_finish(const Dev& P, const Fused& F, int t, const EosIn& in, bool writer, unsigned char* scratch,
+                            Tables* T, double* c64n) {
+    const int tid = threadIdx.x, j = tid >> 4, m = tid & 15;
+    const int k = P.k, kd = k * kD;
+    const bool live = j < k;
+    double* cn = reinterpret_cast<double*>(scratch);    // k x 16 new centroids
+    float* ecn = reinterpret_cast<float*>(cn + kd);     // k rounding errors
+    uint64_t* snow = F.sum + (int64_t)slot2(t) * (kd + k);
+    double* cnew_p = F.c64 + (int64_t)slot2(t + 1) * kd;
+    const int e = live ? j * kD + m : 0;
+    const int ce = live ? kd + j : 0;
+    const double cold = in.cold;
+    uint64_t v = in.sv, cnt = in.sc;
 #pragma unroll
     for (int r = 0; r < kSmallRows; ++r) {
-        v += tv[r];
-        cnt += tc[r];
+        v += in.tv[r];
+        cnt += in.tc[r];
     }
     if (writer && live) {
         snow[e] = v;
@@ -442,8 +462,8 @@ __device__ float end_of_step(const Dev& P, const Fused& F, int t, bool delta, bo
     // Drift f(c) and its cumulative sums, with margins far above the float64
     // rounding of the drift and of the running sums.
     const double fd = sqrt(a);
-    const double hi = (F.dhi[(int64_t)slot2(t) * k + (live ? j : 0)] + fd * (1.0 + 0x1p-40)) * (1.0 + 0x1p-50);
-    const double lo = (F.dlo[(int64_t)slot2(t) * k + (live ? j : 0)] + fd * (1.0 - 0x1p-40)) * (1.0 - 0x1p-50);
+    const double hi = (in.dhi + fd * (1.0 + 0x1p-40)) * (1.0 + 0x1p-50);
+    const double lo = (in.dlo + fd * (1.0 - 0x1p-40)) * (1.0 - 0x1p-50);
     const float ec = f32_up(sqrt(b) * (1.0 + 0x1p-40));
     if (live) {
         cn[e] = cnew;
@@ -741,13 +761,15 @@ template <int KC>
 __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P, Fused F, int t,
                                                                                       int fused) {
     IterState* st = P.st;
-    if (st->done) {   // an earlier end of step stopped the run
-        if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
-        return;
-    }
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-    // The changed count of step t - 1, for the stop test of a fused start.
+    // Every load that does not depend on the stop flag is issued before the
+    // flag is tested: the end of step t - 1 (fused start), the changed count
+    // of step t - 1 and the stop settings, and (below) the first states.
+    EosIn ein;
+    if (fused) ein = eos_load(P, F, t - 1, true);
     const uint64_t chg_prev = fused ? F.stat[slot3(t - 1) * kNumStat + kStChanged] : 0;
+    const double tol_n = st->tol_n;
+    const int max_iters = st->max_iters;
     const int64_t n = P.n;
     const int nwt = (int)((n + kIncWaveTile - 1) / kIncWaveTile);   // wave tiles
     // Block b owns wave tiles [b * nwt / G, (b + 1) * nwt / G); its waves take
@@ -764,6 +786,10 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     };
     int wt = wt_lo + w;   // each wave's first tile
     if (wt < wt_hi) load_states(wt);   // the first states load while the tables are staged
+    if (st->done) {   // an earlier end of step stopped the run
+        if (blockIdx.x == 0 && tid == 0) st->active = 0;
+        return;
+    }
 
     const SmallLds lay = small_lds(P.k, false);
     // Fused start: every block forms the end of step t - 1 itself (the same
@@ -776,9 +802,9 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     if (fused) {
         T = table_ptrs(P, lay);
         unsigned char* scr = km_smem + lay.off_qr;
-        ecmax = end_of_step(P, F, t - 1, true, blockIdx.x == 0, scr, &T, c64n);
+        ecmax = eos_finish(P, F, t - 1, ein, blockIdx.x == 0, scr, &T, c64n);
         if (blockIdx.x == 0 && tid == 0) step_books(P, F, t - 1, ecmax);
-        if ((double)chg_prev < st->tol_n || t >= st->max_iters) {   // the run stops after step t - 1
+        if ((double)chg_prev < tol_n || t >= max_iters) {   // the run stops after step t - 1
             if (blockIdx.x == 0 && tid == 0) st->active = 0;
             return;
         }
@@ -916,7 +942,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
 // (then the next step starts unfused).
 __global__ __launch_bounds__(kTp) void k_small_finish(Dev P, Fused F, int t, int delta) {
     if (!P.st->active) return;   // step t did not run (the run had stopped)
-    const float em = end_of_step(P, F, t, delta != 0, true, km_smem, nullptr, nullptr);
+    const float em = eos_finish(P, F, t, eos_load(P, F, t, delta != 0), true, km_smem, nullptr, nullptr);
     if (threadIdx.x == 0) step_books(P, F, t, em);
 }
 
