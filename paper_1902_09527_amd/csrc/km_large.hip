@@ -182,7 +182,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
             f32x4 v = {0.f, 0.f, 0.f, 0.f};
             if (srow[i] >= 0) {
                 if (vec) {
-                    if (m0 < d) v = __builtin_nontemporal_load(X4 + (((int64_t)srow[i] * d + m0) >> 2));
+                    if (m0 < d) v = X4[((int64_t)srow[i] * d + m0) >> 2];   // cached: re-read per centroid tile
                 } else {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
