@@ -167,16 +167,16 @@ __host__ __device__ inline AssignLds assign_lds(int d, int k, int tp, bool h_lds
 
 // Streaming path for small k and d = 16 (km_small.hip): the streaming kernel
 // (every row of X read) or the incremental kernel (only the Clause-1
-// survivors' rows read), then one block that reduces, updates and rebuilds
-// the centroid table.
+// survivors' rows read); the end of each step (sums, update, centroid table)
+// runs in the next incremental kernel or in one block of its own.
 constexpr int kSmallTile = 256;   // threads per block; points per tile of the streaming kernel
 constexpr int kSmallMaxK = 16;    // the cluster index fits in the 4 low bits of the point state
 constexpr int kSmallCopies = 4;   // copies of the LDS sums (spread rows over banks and addresses)
 constexpr int kSmallRowStride = 20;   // padded LDS row stride (floats) of centroid and queued rows
 
-// Accumulation rows of the streaming step: block b adds its partial row into
-// row b % kSmallRows with device atomics; the finishing block sums and clears
-// them.
+// Accumulation rows of a streaming step: block b adds its partial row into
+// row b % kSmallRows of the step's slot with device atomics; the end of the
+// step sums them, and a later step's block 0 clears the slot for reuse.
 constexpr int kSmallRows = 16;
 
 // Incremental kernel: each block owns an equal share of the tiles of

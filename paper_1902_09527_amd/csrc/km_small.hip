@@ -1,5 +1,5 @@
-// Streaming MTI iteration for small k (k <= 16) and d = 16: two launches per
-// merged ||Lloyd's step (paper section III-B).
+// Streaming MTI iteration for small k (k <= 16) and d = 16 (paper section
+// III-B's merged ||Lloyd's step).
 //
 // Point state.  Every point keeps one 32-bit word: its cluster in the low 4
 // bits and, in the rest, a float32 value v such that v plus the cumulative
@@ -31,15 +31,18 @@
 // Clause 1 keeps, section III-C) reads only the point states, one 16-byte
 // load of four states per thread; the survivors are queued by index and
 // their rows gathered from X when a batch is scanned.  Its sums hold only the
-// moves, which the finishing block adds to the exact sums of the previous
+// moves, which the end of the step adds to the exact sums of the previous
 // step.
 //
 // The block's sums are integers, so their order does not matter; each block
-// adds its row into one of kSmallRows accumulation rows with device atomics.
-// k_small_finish (one block) then adds those rows, forms the new centroids
-// (member means; an empty cluster keeps its centroid), the drift, the
-// cumulative drift, the stop test and the centroid table h, s(c) for the next
-// step (sections III-C and IV-A), and clears the rows.
+// adds its row into one of kSmallRows accumulation rows of the step's slot
+// with device atomics, and its counters into the step's counter slot.  The
+// end of step t (eos_load + eos_finish) then adds those rows, forms the new
+// centroids (member means; an empty cluster keeps its centroid), the drift,
+// the cumulative drift and the centroid table h, s(c) for the next step
+// (sections III-C and IV-A), and step_books the history and the stop test.
+// It runs inside the next k_inc (every block, block 0 storing) when
+// incremental steps follow each other, else as the one-block k_small_finish.
 #include <float.h>
 #include <limits.h>
 #include <math.h>
