@@ -231,8 +231,11 @@ __device__ __forceinline__ void clear_next_slots(const Dev& P, const Fused& F, i
     if (threadIdx.x < kNumStat) F.stat[slot3(t + 1) * kNumStat + threadIdx.x] = 0;
 }
 
+// Per-lane step counters (32 bits: a lane counts far fewer than 2^32
+// events; fewer live registers keep the incremental kernel free of spills).
 struct Counters {
-    uint64_t changed = 0, comp = 0, c1 = 0, rc = 0, iq = 0;
+    uint32_t changed = 0, comp = 0, c1 = 0, rc = 0;
+    uint64_t iq = 0;
 };
 
 struct StepFlags {
@@ -898,7 +901,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
             }
             pos += __popcll(bm);
         }
-        cn.c1 += (uint64_t)c1;
+        cn.c1 += (uint32_t)c1;
         queued = pos;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();   // queue entries visible to the whole wave
