@@ -103,17 +103,43 @@ struct km_ctx {
     double t_ms[4] = {0, 0, 0, 0};
     int64_t t_iters = 0;
 
+    // Small buffers (the per-step sums, counters, tables and state) are
+    // carved from shared chunks, so that the few pages every block touches at
+    // the start of a step stay few: fewer address-translation misses when all
+    // blocks start at once.
+    static constexpr size_t kSmallBuf = 256 << 10, kChunk = 2 << 20, kAlign = 256;
+    unsigned char* chunk = nullptr;
+    size_t chunk_used = 0;
+
     template <class T>
     int alloc(T** p, size_t count) {
-        if (nbufs >= kMaxBufs) {
-            snprintf(g_last_hip, sizeof g_last_hip, "internal: more than %d scratch buffers", kMaxBufs);
-            return KM_ERR_STATE;
+        const size_t bytes = count * sizeof(T) > 0 ? count * sizeof(T) : 16;
+        if (bytes <= kSmallBuf) {
+            const size_t at = (chunk_used + kAlign - 1) / kAlign * kAlign;
+            if (!chunk || at + bytes > kChunk) {
+                void* q = nullptr;
+                if (int rc = raw_alloc(&q, kChunk)) return rc;
+                chunk = static_cast<unsigned char*>(q);
+                chunk_used = 0;
+                return alloc(p, count);
+            }
+            chunk_used = at + bytes;
+            *p = reinterpret_cast<T*>(chunk + at);
+            return KM_OK;
         }
         void* q = nullptr;
-        hipError_t e = hipMalloc(&q, count * sizeof(T) > 0 ? count * sizeof(T) : 16);
-        if (e != hipSuccess) return hip_fail(e, "hipMalloc");
-        bufs[nbufs++] = q;
+        if (int rc = raw_alloc(&q, bytes)) return rc;
         *p = static_cast<T*>(q);
+        return KM_OK;
+    }
+    int raw_alloc(void** q, size_t bytes) {
+        if (nbufs >= kMaxBufs) {
+            snprintf(g_last_hip, sizeof g_last_hip, "internal: more than %d device buffers", kMaxBufs);
+            return KM_ERR_STATE;
+        }
+        hipError_t e = hipMalloc(q, bytes);
+        if (e != hipSuccess) return hip_fail(e, "hipMalloc");
+        bufs[nbufs++] = *q;
         return KM_OK;
     }
     ~km_ctx() {
@@ -282,7 +308,7 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             const void* isym = km::inc_kernel_symbol(k);
             KM_HIP(hipFuncSetAttribute(isym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds_inc));
             int per_cu_i = 0;
-            KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_i, isym, c->tp, c->lds_inc));
+            KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_i, isym, km::kIncThreads, c->lds_inc));
             if (per_cu_i < 1) return KM_ERR_UNSUPPORTED;
             // Resident blocks (the same count on every CU), at least one wave
             // tile per wave; small inputs still spread over up to one block
@@ -291,7 +317,7 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             const int64_t nwt = (n + km::kIncWaveTile - 1) / km::kIncWaveTile;
             int64_t gi = (int64_t)per_cu_i * cus;
             const int64_t spread = nwt < cus ? nwt : cus;
-            const int64_t want = nwt / 4 > spread ? nwt / 4 : spread;
+            const int64_t want = nwt / km::kIncWaves > spread ? nwt / km::kIncWaves : spread;
             if (gi > want) gi = want > 0 ? want : 1;
             c->gi = (int)gi;
         }

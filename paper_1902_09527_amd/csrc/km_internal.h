@@ -179,10 +179,17 @@ constexpr int kSmallRowStride = 20;   // padded LDS row stride (floats) of centr
 // step sums them, and a later step's block 0 clears the slot for reuse.
 constexpr int kSmallRows = 16;
 
-// Incremental kernel: each block owns an equal share of the tiles of
+// Incremental kernel: each block (kIncWaves waves: two blocks per CU at four
+// waves per SIMD, so that the end of the previous step, which every block
+// forms itself, is formed only twice per CU) owns an equal share of the tiles of
 // kIncWaveTile points, which its waves take one at a time (16 points per lane,
 // four 16-byte state loads issued together), in four sub-tiles of 256.  The
 // state array is padded to whole kIncTile.
+#ifndef KM_INC_WAVES
+#define KM_INC_WAVES 8
+#endif
+constexpr int kIncWaves = KM_INC_WAVES;
+constexpr int kIncThreads = 64 * kIncWaves;
 constexpr int kIncWaveTile = 1024;
 constexpr int kIncTile = 4 * kIncWaveTile;
 
@@ -194,7 +201,7 @@ constexpr int kSmallQ = 2 * kSmallTile;          // streaming kernel: rows stage
 // takes a batch of 64 as soon as that many are queued, and one sub-tile adds
 // at most 256.
 constexpr int kIncWaveQ = 64 + 256;
-constexpr int kIncQ = 4 * kIncWaveQ;
+constexpr int kIncQ = kIncWaves * kIncWaveQ;
 
 // Point state of the streaming path: one 32-bit word per point.  Bits 3..0
 // hold the assigned cluster; the word with those bits cleared is a float32
@@ -249,7 +256,7 @@ __host__ __device__ inline SmallLds small_lds(int k, bool staged) {
     L.off_acc = take(8 * kSmallCopies * L.csu, 16);
     L.off_cnt = take(4 * kSmallCopies * L.kp, 16);
     // Queued rows (streaming kernel) or one gathered batch (incremental kernel).
-    L.off_qr = take(4 * (staged ? kSmallQ : kSmallTile) * kSmallRowStride, 16);
+    L.off_qr = take(4 * (staged ? kSmallQ : 64 * kIncWaves) * kSmallRowStride, 16);
     L.off_qp = take(4 * q, 16);
     L.off_qa = take(4 * q, 16);
     L.off_misc = take(64, 16);   // three queue counters (int) at 0, kNumStat uint64 counters at 16

@@ -192,8 +192,9 @@ __device__ __forceinline__ Tables table_ptrs(const Dev& P, const SmallLds& lay) 
     T.csu = lay.csu;
     T.kp = lay.kp;
     const int tid = threadIdx.x;
-    for (int i = tid; i < kCopies * T.csu; i += kTp) T.acc[i] = 0;
-    for (int i = tid; i < kCopies * T.kp; i += kTp) T.cnt[i] = 0;
+    const int nt = (int)blockDim.x;
+    for (int i = tid; i < kCopies * T.csu; i += nt) T.acc[i] = 0;
+    for (int i = tid; i < kCopies * T.kp; i += nt) T.cnt[i] = 0;
     if (tid < kNumStat) T.bst[tid] = 0;
     if (tid < 3) T.qc[tid] = 0;
     return T;
@@ -212,9 +213,10 @@ __device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, cons
     Tables T = table_ptrs(P, lay);
     const int k = P.k, tid = threadIdx.x;
     const double* dhi = F.dhi + (int64_t)slot2(t) * k;
-    for (int i = tid; i < k * kD; i += kTp) T.C[(i / kD) * kCR + i % kD] = P.C32[i];
-    for (int i = tid; i < k * k; i += kTp) T.h[(i / k) * kSmallMaxK + i % k] = P.h[i];
-    for (int i = tid; i < k; i += kTp) {
+    const int nt = (int)blockDim.x;
+    for (int i = tid; i < k * kD; i += nt) T.C[(i / kD) * kCR + i % kD] = P.C32[i];
+    for (int i = tid; i < k * k; i += nt) T.h[(i / k) * kSmallMaxK + i % k] = P.h[i];
+    for (int i = tid; i < k; i += nt) {
         T.thr[i] = clause1_thr(P.s[i], dhi[i]);
         T.ec[i] = P.ec[i];
         T.ddn[i] = F.ddn[i];
@@ -227,7 +229,7 @@ __device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, cons
 __device__ __forceinline__ void clear_next_slots(const Dev& P, const Fused& F, int t) {
     if (blockIdx.x != 0) return;
     uint64_t* r = F.rows + (int64_t)slot3(t + 1) * kSmallRows * P.L;
-    for (int i = threadIdx.x; i < kSmallRows * P.L; i += kTp) r[i] = 0;
+    for (int i = threadIdx.x; i < kSmallRows * P.L; i += (int)blockDim.x) r[i] = 0;
     if (threadIdx.x < kNumStat) F.stat[slot3(t + 1) * kNumStat + threadIdx.x] = 0;
 }
 
@@ -358,13 +360,14 @@ __device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const 
     __syncthreads();
     unsigned long long* row = reinterpret_cast<unsigned long long*>(
         F.rows + ((int64_t)slot3(t) * kSmallRows + blockIdx.x % kSmallRows) * P.L);
-    for (int i = tid; i < k * kD; i += kTp) {
+    const int nt = (int)blockDim.x;
+    for (int i = tid; i < k * kD; i += nt) {
         uint64_t v = 0;
 #pragma unroll
         for (int c = 0; c < kCopies; ++c) v += T.acc[c * T.csu + i];
         if (v || !skip_zero) atomicAdd(row + i, (unsigned long long)v);
     }
-    for (int i = tid; i < k; i += kTp) {
+    for (int i = tid; i < k; i += nt) {
         uint32_t v = 0;
 #pragma unroll
         for (int c = 0; c < kCopies; ++c) v += T.cnt[c * T.kp + i];
@@ -385,7 +388,7 @@ __device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const 
 // cluster keeps its centroid; spherical k-means projects them to the unit
 // sphere), drift and cumulative drift, centroid table h and s for step t + 1
 // (sections III-C and IV-A), as eos_load then eos_finish.  Run by one
-// block of kTp threads: thread 16j + m
+// block of at least 256 threads: thread 16j + m
 // owns coordinate m of centroid j (k <= 16, d = 16), so that the per-centroid
 // terms are reductions over 16 lanes and one barrier separates the centroids
 // from the table.  LDS scratch: finish_lds(16, k) bytes.  delta: the rows of
@@ -417,9 +420,10 @@ __device__ __forceinline__ EosIn eos_load(const Dev& P, const Fused& F, int t, b
     const bool live = j < k;
     const uint64_t* rows = F.rows + (int64_t)slot3(t) * kSmallRows * L;
     const uint64_t* sprev = F.sum + (int64_t)slot2(t - 1) * (kd + k);
-    const int e = live ? j * kD + m : 0;
-    const int ce = live ? kd + j : 0;
-    EosIn in;
+    const int e = j * kD + m;
+    const int ce = kd + j;
+    EosIn in{};
+    if (!live) return in;   // threads past the k centroids load nothing (whole waves skip)
     in.cold = F.c64[(int64_t)slot2(t) * kd + e];
 #pragma unroll
     for (int r = 0; r < kSmallRows; ++r) {
@@ -428,8 +432,8 @@ __device__ __forceinline__ EosIn eos_load(const Dev& P, const Fused& F, int t, b
     }
     in.sv = delta ? sprev[e] : 0;   // the moves add to the sums of step t - 1
     in.sc = delta ? sprev[ce] : 0;
-    in.dhi = F.dhi[(int64_t)slot2(t) * k + (live ? j : 0)];
-    in.dlo = F.dlo[(int64_t)slot2(t) * k + (live ? j : 0)];
+    in.dhi = F.dhi[(int64_t)slot2(t) * k + j];
+    in.dlo = F.dlo[(int64_t)slot2(t) * k + j];
     return in;
 }
 
@@ -442,36 +446,39 @@ __device__ float eos_finish(const Dev& P, const Fused& F, int t, const EosIn& in
     float* ecn = reinterpret_cast<float*>(cn + kd);     // k rounding errors
     uint64_t* snow = F.sum + (int64_t)slot2(t) * (kd + k);
     double* cnew_p = F.c64 + (int64_t)slot2(t + 1) * kd;
-    const int e = live ? j * kD + m : 0;
-    const int ce = live ? kd + j : 0;
-    const double cold = in.cold;
-    uint64_t v = in.sv, cnt = in.sc;
-#pragma unroll
-    for (int r = 0; r < kSmallRows; ++r) {
-        v += in.tv[r];
-        cnt += in.tc[r];
-    }
-    if (writer && live) {
-        snow[e] = v;
-        if (m == 0) snow[ce] = cnt;
-    }
-    // Member mean of the exact sums; an empty cluster keeps its centroid.
-    double cnew = cold;
-    if (cnt > 0) cnew = ((double)(int64_t)(v - cnt * kMagicBits) * P.qinv) / (double)cnt;
-    if (P.flags & KM_FLAG_SPHERICAL) {   // spherical k-means: the mean projected to the unit sphere
-        const double ss = sum16(cnew * cnew);
-        if (cnt > 0) cnew = ss > 0.0 ? cnew / sqrt(ss) : cold;   // a zero mean keeps the centroid
-    }
-    const float c32 = (float)cnew;
-    const double df = cnew - cold, rr = (double)c32 - cnew;
-    const double a = sum16(df * df), b = sum16(rr * rr), c2 = sum16((double)c32 * (double)c32);
-    // Drift f(c) and its cumulative sums, with margins far above the float64
-    // rounding of the drift and of the running sums.
-    const double fd = sqrt(a);
-    const double hi = (in.dhi + fd * (1.0 + 0x1p-40)) * (1.0 + 0x1p-50);
-    const double lo = (in.dlo + fd * (1.0 - 0x1p-40)) * (1.0 - 0x1p-50);
-    const float ec = f32_up(sqrt(b) * (1.0 + 0x1p-40));
+    // Threads past the k centroids (whole 16-lane groups, so the group
+    // reductions stay within live lanes; whole waves for the larger blocks)
+    // skip the arithmetic and only meet the barrier.
+    double hi = 0.0;
     if (live) {
+        const int e = j * kD + m, ce = kd + j;
+        const double cold = in.cold;
+        uint64_t v = in.sv, cnt = in.sc;
+#pragma unroll
+        for (int r = 0; r < kSmallRows; ++r) {
+            v += in.tv[r];
+            cnt += in.tc[r];
+        }
+        if (writer) {
+            snow[e] = v;
+            if (m == 0) snow[ce] = cnt;
+        }
+        // Member mean of the exact sums; an empty cluster keeps its centroid.
+        double cnew = cold;
+        if (cnt > 0) cnew = ((double)(int64_t)(v - cnt * kMagicBits) * P.qinv) / (double)cnt;
+        if (P.flags & KM_FLAG_SPHERICAL) {   // spherical k-means: the mean projected to the unit sphere
+            const double ss = sum16(cnew * cnew);
+            if (cnt > 0) cnew = ss > 0.0 ? cnew / sqrt(ss) : cold;   // a zero mean keeps the centroid
+        }
+        const float c32 = (float)cnew;
+        const double df = cnew - cold, rr = (double)c32 - cnew;
+        const double a = sum16(df * df), b = sum16(rr * rr), c2 = sum16((double)c32 * (double)c32);
+        // Drift f(c) and its cumulative sums, with margins far above the
+        // float64 rounding of the drift and of the running sums.
+        const double fd = sqrt(a);
+        hi = (in.dhi + fd * (1.0 + 0x1p-40)) * (1.0 + 0x1p-50);
+        const double lo = (in.dlo + fd * (1.0 - 0x1p-40)) * (1.0 - 0x1p-50);
+        const float ec = f32_up(sqrt(b) * (1.0 + 0x1p-40));
         cn[e] = cnew;
         if (m == 0) ecn[j] = ec;
         if (writer) {
@@ -497,22 +504,22 @@ __device__ float eos_finish(const Dev& P, const Fused& F, int t, const EosIn& in
         }
     }
     __syncthreads();
-    // Half distance from centroid j to centroid m, rounded down; s(j) is
-    // the smallest over m != j.
-    float hv = 0.f;
-    if (live && m < k && m != j) {
-        double acc = 0.0;
-#pragma unroll
-        for (int q = 0; q < kD; ++q) {
-            const double tq = cn[j * kD + q] - cn[m * kD + q];
-            acc = fma(tq, tq, acc);
-        }
-        hv = f32_down(0.5 * sqrt(acc) * (1.0 - 0x1p-40));
-    }
-    float sv = (live && m < k && m != j) ? hv : INFINITY;
-#pragma unroll
-    for (int o = 8; o > 0; o >>= 1) sv = fminf(sv, __shfl_xor(sv, o));
     if (live) {
+        // Half distance from centroid j to centroid m, rounded down; s(j) is
+        // the smallest over m != j.
+        float hv = 0.f;
+        if (m < k && m != j) {
+            double acc = 0.0;
+#pragma unroll
+            for (int q = 0; q < kD; ++q) {
+                const double tq = cn[j * kD + q] - cn[m * kD + q];
+                acc = fma(tq, tq, acc);
+            }
+            hv = f32_down(0.5 * sqrt(acc) * (1.0 - 0x1p-40));
+        }
+        float sv = (m < k && m != j) ? hv : INFINITY;
+#pragma unroll
+        for (int o = 8; o > 0; o >>= 1) sv = fminf(sv, __shfl_xor(sv, o));
         if (m < k && writer) P.h[j * k + m] = hv;
         if (T) T->h[j * kSmallMaxK + m] = hv;
         if (m == 0) {
@@ -764,7 +771,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
 // shared, through atomics.
 
 template <int KC>
-__global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P, Fused F, int t,
+__global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P, Fused F, int t,
                                                                                       int fused) {
     IterState* st = P.st;
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
@@ -826,7 +833,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
     // counters, which this kernel does not otherwise use).
     auto grab = [&]() __attribute__((always_inline)) {
         int t = 0;
-        if (lane == 0) t = wt_lo + 4 + atomicAdd(T.qc, 1);
+        if (lane == 0) t = wt_lo + kIncWaves + atomicAdd(T.qc, 1);
         return __shfl(t, 0);
     };
     int* wq_p = reinterpret_cast<int*>(km_smem + lay.off_qp) + w * kIncWaveQ;   // this wave's queue
@@ -1013,7 +1020,7 @@ hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, int t, hip
 hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, int fused, hipStream_t s) {
     switch (small_kc(dv.k)) {
 #define KM_LAUNCH(KC_)                                                                                \
-    case KC_: hipLaunchKernelGGL((k_inc<KC_>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F, t, fused); break;
+    case KC_: hipLaunchKernelGGL((k_inc<KC_>), dim3(grid), dim3(kIncThreads), lds_bytes, s, dv, F, t, fused); break;
         KM_SMALL_KCS(KM_LAUNCH)
 #undef KM_LAUNCH
         default: return hipErrorInvalidValue;
