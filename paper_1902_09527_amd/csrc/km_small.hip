@@ -74,6 +74,11 @@ __device__ __forceinline__ uint32_t pack_state(float v, int a) {
 __device__ __forceinline__ int state_cluster(uint32_t w) { return (int)(w & 15u); }
 __device__ __forceinline__ float state_value(uint32_t w) { return __uint_as_float(w & ~15u); }
 
+// Set bits of a wave mask below the calling lane.
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
 // State of a point now assigned to b with distance bound ub: v = ub - D_b,
 // with D_b rounded down and the subtraction rounded up.
 __device__ __forceinline__ uint32_t settle_state(float ub, float ddn_b, int b) {
@@ -595,7 +600,6 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
     const int64_t nchunks = n * kQD;
     const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
     const int rho0 = lane >> 2, q = lane & 3;
-    const uint64_t lt = (1ull << lane) - 1ull;
 
     f32x4 xA[kQD], xB[kQD];
     uint32_t wA = 0, wB = 0;
@@ -719,7 +723,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
         int wbase = 0;
         if (lane == 0 && bm) wbase = atomicAdd(qcount, __popcll(bm));
         wbase = __shfl(wbase, 0);
-        const int pos = queued + wbase + __popcll(bm & lt);
+        const int pos = queued + wbase + lanes_below(bm);
         if (surv) {
             qp[pos] = (int)(base + tid);
             qa[pos] = a_old;
@@ -774,7 +778,9 @@ template <int KC>
 __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P, Fused F, int t,
                                                                                       int fused) {
     IterState* st = P.st;
-    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+    // The wave index is uniform across the wave: held in a scalar register, so
+    // that the tile loop below branches on scalars instead of lane masks.
+    const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     // Every load that does not depend on the stop flag is issued before the
     // flag is tested: the end of step t - 1 (fused start), the changed count
     // of step t - 1 and the stop settings, and (below) the first states.
@@ -798,7 +804,6 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
         for (int c = 0; c < 4; ++c) sn[c] = W4[((int64_t)wt * kIncWaveTile + 256 * c) / 4 + lane];   // padded past n
     };
     int wt = wt_lo + w;   // each wave's first tile
-    if (wt < wt_hi) load_states(wt);   // the first states load while the tables are staged
     if (st->done) {   // an earlier end of step stopped the run
         if (blockIdx.x == 0 && tid == 0) st->active = 0;
         return;
@@ -825,6 +830,9 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
         T = load_tables(P, F, lay, t);
         ecmax = st->ec_max;
     }
+    // The first states are requested once the tables are formed (the end of
+    // step holds many registers; the loads arrive during the table staging).
+    if (wt < wt_hi) load_states(wt);
     if (blockIdx.x == 0 && tid == 0) st->active = 1;
     clear_next_slots(P, F, t);
     const StepFlags fl{false, !(P.flags & KM_FLAG_NO_PRUNE), false, P.gamma, ecmax};
@@ -834,7 +842,7 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
     auto grab = [&]() __attribute__((always_inline)) {
         int t = 0;
         if (lane == 0) t = wt_lo + kIncWaves + atomicAdd(T.qc, 1);
-        return __shfl(t, 0);
+        return __builtin_amdgcn_readfirstlane(t);
     };
     int* wq_p = reinterpret_cast<int*>(km_smem + lay.off_qp) + w * kIncWaveQ;   // this wave's queue
     int* wq_a = reinterpret_cast<int*>(km_smem + lay.off_qa) + w * kIncWaveQ;
@@ -842,7 +850,6 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
     __syncthreads();
 
     Counters cn;
-    const uint64_t lt = (1ull << lane) - 1ull;
     const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
     const int rho0 = lane >> 2, q = lane & 3;
 
@@ -892,17 +899,20 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
     auto tile_body = [&](int base, const uint4 s4) __attribute__((always_inline)) {
         const uint32_t ws[4] = {s4.x, s4.y, s4.z, s4.w};
         const int p0 = base + 4 * lane;
-        const bool full = (int64_t)base + 256 <= n;   // no point past n in this sub-tile
+        const int lim = (int)min((int64_t)256, n - base);   // points of the sub-tile before n
+        float thr[4];   // the four thresholds requested together (padding states read cluster 0)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) thr[e] = T.thr[state_cluster(ws[e])];
         int pos = queued, c1 = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const bool valid = full || (int64_t)(p0 + e) < n;
+            const bool valid = 4 * lane + e < lim;
             const int a = state_cluster(ws[e]);
-            const bool surv = valid && (!fl.prune || !(state_value(ws[e]) <= T.thr[a]));
+            const bool surv = valid && !(fl.prune && state_value(ws[e]) <= thr[e]);
             c1 += valid && !surv ? 1 : 0;   // Clause 1: nothing to read or write
             const uint64_t bm = __ballot(surv);
             if (surv) {
-                const int e_pos = pos + __popcll(bm & lt);
+                const int e_pos = pos + lanes_below(bm);
                 wq_p[e_pos] = p0 + e;
                 wq_a[e_pos] = a;
             }
