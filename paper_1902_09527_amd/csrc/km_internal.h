@@ -260,8 +260,7 @@ __host__ __device__ inline SmallLds small_lds(int k, bool staged) {
     L.off_qp = take(4 * q, 16);
     L.off_qa = take(4 * q, 16);
     L.off_misc = take(64, 16);   // three queue counters (int) at 0, kNumStat uint64 counters at 16
-    // Incremental kernel: float64 centroids for near-tie decisions when the
-    // step finishes the previous one itself (then they are not in memory yet).
+    // Incremental kernel: the float64 centroids of near-tie decisions.
     L.off_c64 = take(staged ? 0 : 8 * k * 16, 16);
     L.bytes = (o + 15) / 16 * 16;
     return L;

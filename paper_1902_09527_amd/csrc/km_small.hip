@@ -799,9 +799,15 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
     // The states of a wave tile: sub-tile c of lane l holds points
     // base + 256c + 4l .. +3.
     uint4 sn[4];
+    // Addressed as a scalar tile base plus the lane's 32-bit offset (kept
+    // opaque so that it is not folded into a 64-bit per-lane address, which
+    // would hold two more registers through the loop).
     auto load_states = [&](int wt) __attribute__((always_inline)) {
+        const char* tw = reinterpret_cast<const char*>(W4) + (int64_t)wt * (4 * kIncWaveTile);   // padded past n
+        uint32_t off = 16u * (uint32_t)lane;
+        asm volatile("" : "+v"(off));
 #pragma unroll
-        for (int c = 0; c < 4; ++c) sn[c] = W4[((int64_t)wt * kIncWaveTile + 256 * c) / 4 + lane];   // padded past n
+        for (int c = 0; c < 4; ++c) sn[c] = *reinterpret_cast<const uint4*>(tw + off + 1024 * c);
     };
     int wt = wt_lo + w;   // each wave's first tile
     if (st->done) {   // an earlier end of step stopped the run
@@ -809,7 +815,9 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
         return;
     }
 
-    const SmallLds lay = small_lds(P.k, false);
+    // The layout for the largest k: every LDS offset is a constant of the
+    // code (immediate offsets, no registers held for them).
+    const SmallLds lay = small_lds(kSmallMaxK, false);
     // Fused start: every block forms the end of step t - 1 itself (the same
     // integer totals and float64 operations, so the same tables) in the LDS of
     // the gathered rows, and block 0 stores it (and the bookkeeping).  The
@@ -829,6 +837,7 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
     } else {
         T = load_tables(P, F, lay, t);
         ecmax = st->ec_max;
+        for (int i = tid; i < P.k * kD; i += kIncThreads) c64n[i] = P.C64[i];
     }
     // The first states are requested once the tables are formed (the end of
     // step holds many registers; the loads arrive during the table staging).
@@ -836,7 +845,9 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
     if (blockIdx.x == 0 && tid == 0) st->active = 1;
     clear_next_slots(P, F, t);
     const StepFlags fl{false, !(P.flags & KM_FLAG_NO_PRUNE), false, P.gamma, ecmax};
-    const double* C64 = fused ? c64n : P.C64;
+    // Near-tie decisions read the float64 centroids from LDS (one address
+    // space: plain LDS loads, whose waits the compiler counts exactly).
+    const double* C64 = c64n;
     // Further tiles: lane 0 takes one from the block's counter (in the queue
     // counters, which this kernel does not otherwise use).
     auto grab = [&]() __attribute__((always_inline)) {
@@ -859,7 +870,9 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
     // staged and scanned, one survivor per lane, at the next batch point or
     // at the end, so that the loads overlap the next tile's Clause-1 work.
     f32x4 r[kQD];
-    int bp = 0, binc = 0, bcnt = 0;   // the batch in flight: its entry (one per lane), size
+    // The batch in flight: its size, and each lane's entry (point, cluster)
+    // parked in the spare words of the lane's staged row.
+    int bcnt = 0;
     auto take_batch = [&](int e0, int cnt) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < kQD; ++i) {
@@ -867,8 +880,9 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
             const int64_t rp = slot < cnt ? (int64_t)wq_p[e0 + slot] : 0;
             r[i] = __builtin_nontemporal_load(X4 + rp * kQD + q);
         }
-        bp = lane < cnt ? wq_p[e0 + lane] : 0;
-        binc = lane < cnt ? wq_a[e0 + lane] : 0;
+        int* park = reinterpret_cast<int*>(wg + lane * kCR + kD);
+        park[0] = lane < cnt ? wq_p[e0 + lane] : 0;
+        park[1] = lane < cnt ? wq_a[e0 + lane] : 0;
         bcnt = cnt;
     };
     auto scan_batch = [&]() __attribute__((always_inline)) {
@@ -887,7 +901,8 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
                 x[4 * c + 2] = v.z;
                 x[4 * c + 3] = v.w;
             }
-            settle_survivor<KC>(P, F, T, fl, C64, x, bp, binc, lane & (kCopies - 1), cn, nullptr);
+            const int* park = reinterpret_cast<const int*>(wg + lane * kCR + kD);
+            settle_survivor<KC>(P, F, T, fl, C64, x, park[0], park[1], lane & (kCopies - 1), cn, nullptr);
         }
         bcnt = 0;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -895,7 +910,8 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
 
-    int queued = 0;   // wave-uniform
+    int queued = 0;      // wave-uniform
+    uint32_t c1w = 0;    // wave-uniform: points Clause 1 kept
     auto tile_body = [&](int base, const uint4 s4) __attribute__((always_inline)) {
         const uint32_t ws[4] = {s4.x, s4.y, s4.z, s4.w};
         const int p0 = base + 4 * lane;
@@ -903,13 +919,12 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
         float thr[4];   // the four thresholds requested together (padding states read cluster 0)
 #pragma unroll
         for (int e = 0; e < 4; ++e) thr[e] = T.thr[state_cluster(ws[e])];
-        int pos = queued, c1 = 0;
+        int pos = queued;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const bool valid = 4 * lane + e < lim;
             const int a = state_cluster(ws[e]);
             const bool surv = valid && !(fl.prune && state_value(ws[e]) <= thr[e]);
-            c1 += valid && !surv ? 1 : 0;   // Clause 1: nothing to read or write
             const uint64_t bm = __ballot(surv);
             if (surv) {
                 const int e_pos = pos + lanes_below(bm);
@@ -918,7 +933,8 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
             }
             pos += __popcll(bm);
         }
-        cn.c1 += (uint32_t)c1;
+        // Clause 1 kept every valid point that was not queued (a wave count).
+        c1w += (uint32_t)(min(max(lim, 0), 256) - (pos - queued));
         queued = pos;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();   // queue entries visible to the whole wave
@@ -957,6 +973,7 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
         }
         if (!more) break;
     }
+    cn.c1 = lane == 0 ? c1w : 0u;
     flush_block(P, F, T, cn, true, t);
 }
 
@@ -1012,7 +1029,7 @@ const void* inc_kernel_symbol(int k) {
 
 int small_lds_bytes(int k) { return small_lds(k, true).bytes; }
 
-int inc_lds_bytes(int k) { return small_lds(k, false).bytes; }
+int inc_lds_bytes(int) { return small_lds(kSmallMaxK, false).bytes; }
 
 int small_finish_lds_bytes(int k) { return finish_lds(16, k); }
 
