@@ -266,7 +266,7 @@ struct StepFlags {
 // A skipped c_j is not strictly closer than the best, and a tie goes to the
 // best (the incumbent, or a lower index), so the skips never change the
 // result.
-template <int KC>
+template <int KC, bool INC_ONLY = false>
 __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, const Tables& T, const StepFlags& fl,
                                        const double* C64, const float (&x)[kD], int64_t p, int inc, int cp,
                                        Counters& cn, int* first_b) {
@@ -277,7 +277,7 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
     int b;
     float Db, ub, D2 = INFINITY;
     uint64_t nc = 1;
-    if (inc >= 0) {
+    if (INC_ONLY || inc >= 0) {   // the incremental kernel's survivors always have an incumbent
         float hrow[(KC + 3) / 4 * 4];
 #pragma unroll
         for (int j = 0; j < KC; j += 4) {
@@ -292,17 +292,19 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
         for (int j = 0; j < KC; ++j) Db = j == inc ? Dall[j] : Db;
         const float u = bound_of(Db, T.ec[inc], fl.gamma);
         b = inc;
+        // Branch-free (selects, no lane-mask branches): c_j is taken unless
+        // Clause 3 skips it.
 #pragma unroll
         for (int j = 0; j < KC; ++j) {
-            if (j >= k || j == inc || (fl.prune && u <= hrow[j])) continue;
-            nc += 1;
-            if (Dall[j] < Db) {
-                D2 = Db;
-                Db = Dall[j];
-                b = j;
-            } else {
-                D2 = Dall[j] < D2 ? Dall[j] : D2;
-            }
+            if (j >= k) continue;   // uniform
+            const bool c = j != inc && !(fl.prune && u <= hrow[j]);
+            const float dj = Dall[j];
+            const bool lt = c && dj < Db;
+            const bool le2 = c && !lt && dj < D2;
+            nc += c ? 1 : 0;
+            D2 = lt ? Db : (le2 ? dj : D2);
+            Db = lt ? dj : Db;
+            b = lt ? j : b;
         }
         ub = b == inc ? u : bound_of(Db, T.ec[b], fl.gamma);
     } else {
@@ -311,16 +313,16 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
         ub = bound_of(Db, T.ec[0], fl.gamma);
 #pragma unroll
         for (int j = 1; j < KC; ++j) {
-            if (j >= k || (fl.prune && ub <= T.h[b * kSmallMaxK + j])) continue;
-            nc += 1;
-            if (Dall[j] < Db) {
-                D2 = Db;
-                Db = Dall[j];
-                b = j;
-                ub = bound_of(Db, T.ec[j], fl.gamma);
-            } else {
-                D2 = Dall[j] < D2 ? Dall[j] : D2;
-            }
+            if (j >= k) continue;   // uniform
+            const bool c = !(fl.prune && ub <= T.h[b * kSmallMaxK + j]);
+            const float dj = Dall[j];
+            const bool lt = c && dj < Db;
+            const bool le2 = c && !lt && dj < D2;
+            nc += c ? 1 : 0;
+            D2 = lt ? Db : (le2 ? dj : D2);
+            Db = lt ? dj : Db;
+            ub = lt ? bound_of(dj, T.ec[j], fl.gamma) : ub;
+            b = lt ? j : b;
         }
     }
     if (D2 != INFINITY) {
@@ -902,7 +904,7 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
                 x[4 * c + 3] = v.w;
             }
             const int* park = reinterpret_cast<const int*>(wg + lane * kCR + kD);
-            settle_survivor<KC>(P, F, T, fl, C64, x, park[0], park[1], lane & (kCopies - 1), cn, nullptr);
+            settle_survivor<KC, true>(P, F, T, fl, C64, x, park[0], park[1], lane & (kCopies - 1), cn, nullptr);
         }
         bcnt = 0;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
