@@ -358,7 +358,7 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
                      max_lds / 4);
             return KM_ERR_UNSUPPORTED;
         }
-        const void* sym = km::large_mfma_symbol();
+        const void* sym = km::large_mfma_symbol(d);
         KM_HIP(km::large_set_attributes(k, d));
         int per_cu = 0;
         KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, 256, mlds));

@@ -81,8 +81,7 @@ inline int row_len(int d, int k) { return k * d + k + kNumStat; }
 constexpr int kLgM = 128;            // survivors per block tile (matrix-core columns)
 constexpr int kLgN = 128;            // centroids per block tile (matrix-core rows)
 constexpr int kLgK = 16;             // dimensions per streamed chunk
-constexpr int kLgAS = kLgN + 32;     // LDS stride (floats) of one dimension of a centroid chunk
-constexpr int kLgBS = kLgM + 32;     // LDS stride (floats) of one dimension of a survivor chunk
+constexpr int kLgRS = kLgK + 4;      // LDS row stride (floats) of a chunk: 16-byte rows, spread over banks
 constexpr int kLgChunkRows = 256;    // rows per segment-sum chunk
 constexpr int kLgMaxD = 4096;        // largest d of the global-memory path
 
@@ -104,11 +103,12 @@ struct Large {
 
 // LDS bytes of the global-memory matrix-core kernel: the double-buffered
 // chunks (reused for the candidate lists after the last chunk), the
-// survivors' squared norms and a few reduction words.
+// survivors' squared norms, a few reduction words and the centroid tile's
+// squared norms.
 __host__ __device__ inline int large_mfma_lds() {
-    const int bufs = 2 * kLgK * (kLgAS + kLgBS) * 4;
+    const int bufs = 2 * (kLgN + kLgM) * kLgRS * 4;
     const int cand = kLgM * 16 * 8;
-    return (bufs > cand ? bufs : cand) + 4 * kLgM + 64;
+    return (bufs > cand ? bufs : cand) + 4 * kLgM + 16 + 4 * kLgN;
 }
 
 // Padded LDS row stride of the X tile: 16-byte aligned rows, offset by 4
@@ -294,7 +294,7 @@ hipError_t launch_large_assign(const Dev& dv, const Large& lg, int gb, hipStream
 hipError_t launch_large_reduce(const Dev& dv, const Large& lg, hipStream_t s);
 hipError_t launch_large_table(const Dev& dv, int force, hipStream_t s);
 int large_table_lds(int d);
-const void* large_mfma_symbol();
+const void* large_mfma_symbol(int d);   // the matrix-core kernel for row length d
 // Raises the dynamic-LDS limits of the global-memory path's kernels.
 hipError_t large_set_attributes(int k, int d);
 

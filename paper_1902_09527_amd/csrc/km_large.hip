@@ -52,6 +52,25 @@ __device__ inline void top4_insert(float (&L)[4], int (&J)[4], float v, int j) {
     }
 }
 
+// The same insertion when j is larger than every index in the list (the
+// centroids arrive in increasing index order): a tie keeps the earlier,
+// lower index, so only strict comparisons are needed.
+__device__ __forceinline__ void top4_insert_next(float (&L)[4], int (&J)[4], float v, int j) {
+    if (!(v < L[3])) return;
+    L[3] = v;
+    J[3] = j;
+#pragma unroll
+    for (int q = 3; q > 0; --q) {
+        if (L[q] < L[q - 1]) {
+            const float tv = L[q];
+            L[q] = L[q - 1];
+            L[q - 1] = tv;
+            const int tj = J[q];
+            J[q] = J[q - 1];
+            J[q - 1] = tj;
+        }
+    }
+}
 
 }  // namespace
 
@@ -107,14 +126,19 @@ __global__ __launch_bounds__(256) void k_bound_large(Dev P, Large Lg) {
 // tile: kLgN = 128 centroids x kLgM = 128 survivors; wave (wr, wc) owns
 // centroid rows 64 wr .. 64 wr + 63 and survivor columns 64 wc .. 64 wc + 63,
 // four 32x32 float32 accumulators.  The dimensions stream in chunks
-// of kLgK through double-buffered LDS (dimension-major); the next chunk's
-// global loads are issued before the current chunk's products.  Each lane
+// of kLgK through double-buffered LDS (row-major, 16-byte rows: one 16-byte
+// store per thread and row piece, two 16-byte reads per lane and operand);
+// the next chunk's global loads are issued before the current chunk's
+// products.  Within a chunk, product step s sums dimensions s (lanes 0-31)
+// and 8 + s (lanes 32-63), so each lane's operands for the whole chunk are 8
+// consecutive floats of one row.  Each lane
 // keeps, for its two survivor columns, the four smallest expanded-form
 // distances |x|^2 + |c|^2 - 2 x.c with their centroids; the 4 lists of a
 // survivor (2 waves x 2 half-waves) are merged in LDS, and the candidates
 // within the expanded form's error bound of the smallest are re-evaluated in
 // the direct form, followed by the float64 near-tie rule.
 
+template <bool VEC>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_mfma_large(Dev P, Large Lg) {
     IterState* st = P.st;
     if (!st->active) return;
@@ -124,14 +148,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 31, half = lane >> 5;
     const int wr = wave >> 1, wc = wave & 1;   // the wave's 64-centroid row block and 64-survivor column block
     extern __shared__ __align__(16) unsigned char smem[];
-    constexpr int kBufBytes = 2 * kLgK * (kLgAS + kLgBS) * 4;
+    constexpr int kBufBytes = 2 * (kLgN + kLgM) * kLgRS * 4;
     constexpr int kCandBytes = kLgM * 16 * 8;
-    float* Ab = reinterpret_cast<float*>(smem);                    // [2][kLgK][kLgAS]
-    float* Bb = Ab + 2 * kLgK * kLgAS;                             // [2][kLgK][kLgBS]
+    float* Ab = reinterpret_cast<float*>(smem);                    // [2][kLgN][kLgRS]
+    float* Bb = Ab + 2 * kLgN * kLgRS;                             // [2][kLgM][kLgRS]
     float* candD = reinterpret_cast<float*>(smem);                 // [kLgM][16], after the products
     int* candJ = reinterpret_cast<int*>(candD + kLgM * 16);
     float* x2s = reinterpret_cast<float*>(smem + (kBufBytes > kCandBytes ? kBufBytes : kCandBytes));   // [kLgM]
     float* red = x2s + kLgM;                                       // [4]
+    float* cnt = red + 4;                                          // [kLgN]: the centroid tile's |c|^2
 
     const float ecm = st->ec_max;
     const float gamma = P.gamma;
@@ -149,7 +174,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     const int ntiles = (int)((ns + kLgM - 1) / kLgM);
     const int nct = (k + kLgN - 1) / kLgN;
     const int nch = (d + kLgK - 1) / kLgK;
-    const bool vec = (d & 3) == 0;   // 16-byte row chunks (every chunk start is then aligned)
+    constexpr bool vec = VEC;   // d % 4 == 0: 16-byte row chunks (every chunk start is then aligned)
     const f32x4* C4 = reinterpret_cast<const f32x4*>(P.C32);
     const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
 
@@ -193,16 +218,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         }
     };
     auto store_chunk = [&](int buf) __attribute__((always_inline)) {
-        float* A = Ab + buf * kLgK * kLgAS;
-        float* B = Bb + buf * kLgK * kLgBS;
+        float* A = Ab + buf * kLgN * kLgRS;
+        float* B = Bb + buf * kLgM * kLgRS;
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 2; ++i) *reinterpret_cast<f32x4*>(A + (64 * i + r4) * kLgRS + 4 * q4) = ra[i];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) A[(4 * q4 + e) * kLgAS + 64 * i + r4] = ra[i][e];
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) B[(4 * q4 + e) * kLgBS + 64 * i + r4] = rb[i][e];
+        for (int i = 0; i < 2; ++i) *reinterpret_cast<f32x4*>(B + (64 * i + r4) * kLgRS + 4 * q4) = rb[i];
     };
 
     for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
@@ -234,6 +255,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
                     for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
             __syncthreads();   // the previous tile's buffers and lists are consumed
             load_chunk(n0, 0);
+            if (tid < kLgN) cnt[tid] = n0 + tid < k ? P.cn2[n0 + tid] : INFINITY;
             store_chunk(0);
             if (ct == 0)
 #pragma unroll
@@ -242,17 +264,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
             for (int c = 0; c < nch; ++c) {
                 const bool more = c + 1 < nch;
                 if (more) load_chunk(n0, c + 1);
-                const float* A = Ab + (c & 1) * kLgK * kLgAS + 64 * wr + col;
-                const float* B = Bb + (c & 1) * kLgK * kLgBS + 64 * wc + col;
+                // Lane (col, half): rows 64 wr + col (+ 32) of the centroid
+                // chunk and 64 wc + col (+ 32) of the survivor chunk,
+                // dimensions 8 half .. 8 half + 7.
+                const float* A = Ab + (c & 1) * kLgN * kLgRS + (64 * wr + col) * kLgRS + 8 * half;
+                const float* B = Bb + (c & 1) * kLgM * kLgRS + (64 * wc + col) * kLgRS + 8 * half;
+                float a0[8], a1[8], b0[8], b1[8];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const f32x4 va0 = *reinterpret_cast<const f32x4*>(A + 4 * h);
+                    const f32x4 va1 = *reinterpret_cast<const f32x4*>(A + 32 * kLgRS + 4 * h);
+                    const f32x4 vb0 = *reinterpret_cast<const f32x4*>(B + 4 * h);
+                    const f32x4 vb1 = *reinterpret_cast<const f32x4*>(B + 32 * kLgRS + 4 * h);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        a0[4 * h + e] = va0[e];
+                        a1[4 * h + e] = va1[e];
+                        b0[4 * h + e] = vb0[e];
+                        b1[4 * h + e] = vb1[e];
+                    }
+                }
 #pragma unroll
                 for (int s = 0; s < kLgK / 2; ++s) {
-                    const int dm = 2 * s + half;
-                    const float a0 = A[dm * kLgAS], a1 = A[dm * kLgAS + 32];
-                    const float b0 = B[dm * kLgBS], b1 = B[dm * kLgBS + 32];
-                    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
-                    acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
-                    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
-                    acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+                    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[s], b0[s], acc[0][0], 0, 0, 0);
+                    acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[s], b1[s], acc[0][1], 0, 0, 0);
+                    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[s], b0[s], acc[1][0], 0, 0, 0);
+                    acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[s], b1[s], acc[1][1], 0, 0, 0);
                 }
                 if (more) {
                     store_chunk((c + 1) & 1);
@@ -281,10 +318,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 #pragma unroll
                 for (int a = 0; a < 2; ++a)
 #pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        const int j = n0 + 64 * wr + 32 * a + 8 * (e >> 2) + 4 * half + (e & 3);
-                        const float cn = j < k ? P.cn2[j] : INFINITY;
-                        top4_insert(L[cb], J[cb], xa + cn - 2.f * acc[a][cb][e], j);
+                    for (int g = 0; g < 4; ++g) {
+                        const int jl = 64 * wr + 32 * a + 8 * g + 4 * half;   // 4 consecutive centroids
+                        const f32x4 cn = *reinterpret_cast<const f32x4*>(cnt + jl);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            top4_insert_next(L[cb], J[cb], xa + cn[e] - 2.f * acc[a][cb][4 * g + e], n0 + jl + e);
                     }
             }
         }
@@ -658,11 +697,17 @@ __global__ __launch_bounds__(256) void k_centroid_table_tiled(Dev P, int force) 
 // ---------------------------------------------------------------------------
 // Launchers
 
-const void* large_mfma_symbol() { return reinterpret_cast<const void*>(&k_mfma_large); }
+const void* large_mfma_symbol(int d) {
+    return (d & 3) == 0 ? reinterpret_cast<const void*>(&k_mfma_large<true>)
+                        : reinterpret_cast<const void*>(&k_mfma_large<false>);
+}
 
 hipError_t launch_large_assign(const Dev& dv, const Large& lg, int gb, hipStream_t s) {
     hipLaunchKernelGGL(k_bound_large, dim3(gb), dim3(256), 0, s, dv, lg);
-    hipLaunchKernelGGL(k_mfma_large, dim3(lg.Gm), dim3(256), large_mfma_lds(), s, dv, lg);
+    if ((dv.d & 3) == 0)
+        hipLaunchKernelGGL(k_mfma_large<true>, dim3(lg.Gm), dim3(256), large_mfma_lds(), s, dv, lg);
+    else
+        hipLaunchKernelGGL(k_mfma_large<false>, dim3(lg.Gm), dim3(256), large_mfma_lds(), s, dv, lg);
     return hipGetLastError();
 }
 
@@ -683,9 +728,7 @@ int large_table_lds(int d) { return 8 * kTiTile * d + 4 * kTiTile * 256; }
 hipError_t large_set_attributes(int k, int d) {
     hipError_t e;
     const auto attr = hipFuncAttributeMaxDynamicSharedMemorySize;
-    if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_mfma_large), attr, large_mfma_lds())) !=
-        hipSuccess)
-        return e;
+    if ((e = hipFuncSetAttribute(large_mfma_symbol(d), attr, large_mfma_lds())) != hipSuccess) return e;
     if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_hist_large), attr, 4 * k)) != hipSuccess)
         return e;
     if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_scatter_large), attr, 4 * k)) != hipSuccess)
