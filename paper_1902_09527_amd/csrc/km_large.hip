@@ -404,7 +404,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
             bool re = full;
             float d1 = INFINITY, d2 = INFINITY;
             int rk1 = INT_MAX, j1 = 0;
-            if (!full) {
+            // One candidate is the nearest centroid (every other one is
+            // certified farther): as on the LDS paths, its bound then comes
+            // from its expanded value and the error bound, without the
+            // direct form (kept when statistics are gathered).
+            const bool single = !full && nq == 1 && !(P.flags & KM_FLAG_STATS);
+            if (!full && !single) {
                 for (int q = 0; q < nq; ++q) {
                     const int j = TJ[q];
                     const float Dd = dist32(j);
@@ -425,7 +430,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
                 }
             }
             int b = j1;
-            float ub = upper_bound(d1, P.ec[j1], gamma);
+            float ub;
+            if (single) {
+                const float e1b = gexp * R * R + 4.f * R * ecm + 2.f * ecm * ecm;
+                b = TJ[0];
+                ub = __builtin_amdgcn_sqrtf(fmaxf(T[0] + e1b, 0.f)) * (1.0f + 0x1p-20f) * kUp;
+            } else {
+                ub = upper_bound(d1, P.ec[j1], gamma);
+            }
             if (re) {
                 // float64 decision against the master centroids with the
                 // oracle's rule (smaller distance, then the incumbent, then
