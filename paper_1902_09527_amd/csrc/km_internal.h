@@ -179,16 +179,13 @@ constexpr int kSmallRowStride = 20;   // padded LDS row stride (floats) of centr
 // step sums them, and a later step's block 0 clears the slot for reuse.
 constexpr int kSmallRows = 16;
 
-// Incremental kernel: each block (kIncWaves waves: two blocks per CU at four
-// waves per SIMD, so that the end of the previous step, which every block
-// forms itself, is formed only twice per CU) owns an equal share of the tiles of
-// kIncWaveTile points, which its waves take one at a time (16 points per lane,
-// four 16-byte state loads issued together), in four sub-tiles of 256.  The
-// state array is padded to whole kIncTile.
-#ifndef KM_INC_WAVES
-#define KM_INC_WAVES 8
-#endif
-constexpr int kIncWaves = KM_INC_WAVES;
+// Incremental kernel: each block of kIncWaves waves (two blocks per CU at
+// four waves per SIMD, so that the end of the previous step, which every
+// block forms itself, is formed only twice per CU) owns an equal share of
+// the tiles of kIncWaveTile points, which its waves take one at a time (16
+// points per lane, four 16-byte state loads issued together), in four
+// sub-tiles of 256.  The state array is padded to whole kIncTile.
+constexpr int kIncWaves = 8;
 constexpr int kIncThreads = 64 * kIncWaves;
 constexpr int kIncWaveTile = 1024;
 constexpr int kIncTile = 4 * kIncWaveTile;
