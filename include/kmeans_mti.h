@@ -184,10 +184,12 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
 
 /*
  * Name of the kernel path the context uses, a static string: "stream-d16"
- * (d = 16, k <= 16: the streaming kernel k_small in the first step and the
- * incremental kernel k_inc after it, each followed by the one-block update
- * k_small_finish), "stream-d16-full" (the same with
- * KM_FLAG_FULL_SUMS or KM_FLAG_STATS: k_small every step), "lds-vector" /
+ * (d = 16, k <= 16: the streaming kernel k_small in the first step, then
+ * the incremental kernel k_inc, each launch of which also ends the step
+ * before it; the one-block update k_small_finish runs after k_small and
+ * before results are read), "stream-d16-full" (k_small every step, each
+ * followed by k_small_finish, with KM_FLAG_FULL_SUMS or KM_FLAG_STATS),
+ * "lds-vector" /
  * "lds-mfma" (centroids and sums in LDS: k_assign with vector or matrix-core
  * survivors, then k_reduce, k_update, k_centroid_table), "lds-elkan" (the
  * same with KM_FLAG_ELKAN's lower-bound scan), "global-mfma"
