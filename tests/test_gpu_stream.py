@@ -148,3 +148,28 @@ def test_path_selection(d, k, flags, path):
     X, C0 = synth.blobs(1000, d, k, seed=131)
     with km.KMeansMTI(_gpu(X), _gpu(C0), **flags) as ctx:
         assert ctx.path() == path
+
+
+# Sizes at the incremental kernel's tiling edges: 1024-point wave tiles, eight
+# waves per block, blocks owning fewer tiles than waves, one tile short of or
+# past a whole number of blocks' tiles, and a ragged last sub-tile.
+EDGE_N = [1023, 1024, 1025, 8 * 1024 - 1, 8 * 1024, 8 * 1024 + 1, 16 * 1024 + 3, 300 * 1024 + 257]
+
+
+@pytest.mark.parametrize("n", EDGE_N)
+def test_incremental_tiling_edges_match_oracle_and_generic_path(n):
+    rng = np.random.default_rng(9000 + n)
+    k = int(rng.integers(1, 17))
+    print("n", n, "k", k, flush=True)
+    X, C0 = synth.blobs(n, 16, k, seed=9000 + n, spread=3.0, sigma=1.5)
+    iters = 12
+    ref = oracle.lloyd(X, C0, iters, 0.0)
+    Xg, Cg = _gpu(X), _gpu(C0)
+    with km.KMeansMTI(Xg, Cg) as ctx:
+        assert ctx.path() == "stream-d16"
+    a, c, st = km.run(Xg, Cg, iters, 0.0, stats=False)
+    assert st["iterations"] == ref["iters"]
+    check_assign(a.cpu().numpy(), ref["assign"], ref["best"], ref["second"], "final assignment")
+    check_centroids(c.cpu().numpy(), ref["C"], X, "final centroids")
+    a2, c2, _ = km.run(Xg, Cg, iters, 0.0, generic=True)
+    assert torch.equal(a, a2) and torch.equal(c, c2)
