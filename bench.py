@@ -243,7 +243,7 @@ def main() -> int:
         return 0
     if args.gpus != 1:
         print("bench.py measures the one-GPU hot path only; --gpus %d is not supported "
-              "(this build runs on a single GPU)" % args.gpus, file=sys.stderr)
+              "(the path runs on one GPU; the multi-GPU design is not built)" % args.gpus, file=sys.stderr)
         return 2
 
     import numpy as np
