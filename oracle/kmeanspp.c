@@ -20,13 +20,14 @@
  *   first    : i_0 = min(floor(u_0 * n), n - 1).
  *   weights  : the draw of seed t+1 (after D2 holds the distances to seeds
  *              0..t) uses integer weights w_i = floor(D2[i] * 2^S_t) whose sum
- *              is exact in any order.  S_t = 62 - e - L, where L is the
+ *              is exact in any order, so the draw is D2 / sum D2 up to the
+ *              rounding of each weight.  S_t = 62 - e - L, where L is the
  *              smallest integer with n <= 2^L and e the smallest integer with
- *              M < 2^e for the bound M = max_i D2[i] after the update with
- *              seed max(t - 1, 0) (D2 only decreases, so M bounds the current
- *              values and every w_i < 2^(62 - L), sum <= 2^62).  M = 0 gives
- *              all-zero weights.  The largest current weight keeps at least
- *              61 - L - log2(M / max_i D2[i]) significant bits.
+ *              M < 2^e for M = max_i D2[i], the current maximum; then every
+ *              w_i < 2^(62 - L) and the sum is <= 2^62.  M = 0 gives all-zero
+ *              weights.  The largest weight keeps at least 61 - L
+ *              significant bits, and each weight is D2[i] * 2^S_t less a
+ *              fraction below one unit.
  *   draw     : W = sum_i w_i, T = min(floor(u_{t+1} * W), W - 1) (the
  *              product in float64), and seed t+1 is the smallest i whose
  *              inclusive prefix sum of w exceeds T.  If W = 0 (every point
@@ -95,12 +96,10 @@ int32_t oracle_kmeanspp(const float* X, int64_t n, int32_t d, int32_t k, const d
     if (!D2) return -1;
 
     idx_out[0] = uniform_index(u[0], n);
-    double M_prev = 0.0;
     for (int32_t t = 0; t < k; ++t) {
         const double M = update_d2(X, n, d, X + idx_out[t] * (int64_t)d, t == 0, D2);
         if (t == k - 1) break;   /* the last update only completes D2_out */
-        const int32_t S = weight_scale(t == 0 ? M : M_prev, n);
-        M_prev = M;
+        const int32_t S = weight_scale(M, n);
         uint64_t W = 0;
         for (int64_t i = 0; i < n; ++i) W += weight_of(D2[i], S);
         int64_t pick;

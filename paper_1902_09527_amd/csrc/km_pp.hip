@@ -7,20 +7,19 @@
 //     index order by fused multiply-add; one lane owns a row, so the order
 //     is the sequential one;
 //   - the draw uses integer weights w_i = floor(D2_i * 2^S) (exact sums in any
-//     order; S from a bound of max D2 known before the pass, so the weights
-//     are formed in the same pass that updates D2), T = floor(u * W) and the
+//     order; S from the maximum of the current D2), T = floor(u * W) and the
 //     smallest i whose inclusive prefix exceeds T.
 //
 // Kernels, per seed t (t = 0 first):
 //   k_pp_step    one pass over the points: D2 = min(D2, ||x - c_t||^2) (all
-//                points for t = 0), the block's weight sum for the next draw
-//                and the block's max of D2 (atomic max into a per-step slot);
+//                points for t = 0) and the block's max of D2 (atomic max into
+//                the slot of seed t);
 //                with pruning a point is skipped when its nearest seed a is
 //                at least twice as far from c_t as the point (triangle
 //                inequality, Elkan's lemma; margins cover the float64
 //                rounding, so D2 is unchanged by construction);
-//   k_pp_weights the weight sums of the first draw (its scale needs the max
-//                of the first pass);
+//   k_pp_weights the block sums of the next draw's weights, with the scale of
+//                the maximum the pass before it left in its slot;
 //   k_pp_select  one workgroup: scans the block sums, finds the block and
 //                then the point of the draw, writes the seed index and row;
 //   k_pp_dcc     the distances from the new seed to the earlier seeds (the
@@ -137,18 +136,17 @@ __device__ __forceinline__ void dist2_pair(const float* __restrict__ x0, const f
 }
 
 // One pass with seed t over a chunk of kPPChunk rows.  FIRST: D2 starts as
-// the distance to seed 0.  WEIGHTS: block sum of the next draw's weights,
-// scale from Mb[s_slot].  PRUNE: skip test against the seed-to-seed table.
+// the distance to seed 0.  PRUNE: skip test against the seed-to-seed table.
 //   1. every row's D2 (and nearest seed) read with coalesced loads, the skip
 //      test, and the rows that must be computed appended to an LDS list;
 //   2. the listed rows spread over all lanes, two per lane at a time;
-//   3. weights and max from the chunk's D2 values kept in LDS.
-template <bool FIRST, bool WEIGHTS, bool PRUNE, int VW>
-__global__ __launch_bounds__(kPPThreads) void k_pp_step(PPArgs P, int t, int s_slot) {
+//   3. the max of the chunk's D2 values kept in LDS.
+template <bool FIRST, bool PRUNE, int VW>
+__global__ __launch_bounds__(kPPThreads) void k_pp_step(PPArgs P, int t) {
     __shared__ double sD[kPPChunk];
     __shared__ uint16_t sL[kPPChunk];
     __shared__ int sN;
-    __shared__ uint64_t red[4][kPPThreads / 64];
+    __shared__ uint64_t red[3][kPPThreads / 64];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t base = (int64_t)blockIdx.x * kPPChunk;
     const int nloc = P.n - base < kPPChunk ? (int)(P.n - base) : kPPChunk;
@@ -214,41 +212,34 @@ __global__ __launch_bounds__(kPPThreads) void k_pp_step(PPArgs P, int t, int s_s
         if (s1 < ns) settle(j1, v1);
     }
     __syncthreads();
-    const int S = WEIGHTS ? weight_scale(__longlong_as_double((long long)P.Mb[s_slot]), P.L) : 0;
-    uint64_t wsum = 0, dmax = 0;
+    uint64_t dmax = 0;
 #pragma unroll
     for (int q = 0; q < kPPPer; ++q) {
         const int j = q * kPPThreads + tid;
         if (j < nloc) {
-            const double D = sD[j];
-            const uint64_t db = (uint64_t)__double_as_longlong(D);   // D >= 0: bits order as values
+            const uint64_t db = (uint64_t)__double_as_longlong(sD[j]);   // D >= 0: bits order as values
             dmax = db > dmax ? db : dmax;
-            if (WEIGHTS) wsum += weight_of(D, S);
         }
     }
-    wsum = wave_sum_u64(wsum);
     dmax = wave_max_u64(dmax);
     if (P.cnt) {
         ncomp = wave_sum_u64(ncomp);
         nimp = wave_sum_u64(nimp);
     }
     if (lane == 0) {
-        red[0][w] = wsum;
-        red[1][w] = dmax;
-        red[2][w] = ncomp;
-        red[3][w] = nimp;
+        red[0][w] = dmax;
+        red[1][w] = ncomp;
+        red[2][w] = nimp;
     }
     __syncthreads();
     if (tid == 0) {
-        uint64_t a = 0, b = 0, cc = 0, ci = 0;
+        uint64_t b = 0, cc = 0, ci = 0;
 #pragma unroll
         for (int j = 0; j < kPPThreads / 64; ++j) {
-            a += red[0][j];
-            b = red[1][j] > b ? red[1][j] : b;
-            cc += red[2][j];
-            ci += red[3][j];
+            b = red[0][j] > b ? red[0][j] : b;
+            cc += red[1][j];
+            ci += red[2][j];
         }
-        if (WEIGHTS) P.bs[blockIdx.x] = a;
         atomicMax(reinterpret_cast<unsigned long long*>(P.Mb + t), (unsigned long long)b);
         if (P.cnt) {   // counters of the pass: distances computed, rows improved
             atomicAdd(reinterpret_cast<unsigned long long*>(P.cnt + 2 * t), (unsigned long long)cc);
@@ -257,12 +248,13 @@ __global__ __launch_bounds__(kPPThreads) void k_pp_step(PPArgs P, int t, int s_s
     }
 }
 
-// Weight sums of the first draw (scale from the max of the first pass).
-__global__ __launch_bounds__(kPPThreads) void k_pp_weights(PPArgs P) {
+// Block sums of the weights of the draw after the pass with seed t (scale
+// from that pass's maximum of D2).
+__global__ __launch_bounds__(kPPThreads) void k_pp_weights(PPArgs P, int t) {
     __shared__ uint64_t red[kPPThreads / 64];
     const int tid = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * kPPChunk;
-    const int S = weight_scale(__longlong_as_double((long long)P.Mb[0]), P.L);
+    const int S = weight_scale(__longlong_as_double((long long)P.Mb[t]), P.L);
     uint64_t wsum = 0;
 #pragma unroll
     for (int q = 0; q < kPPPer; ++q) {
@@ -292,7 +284,7 @@ __global__ __launch_bounds__(256) void k_pp_init(PPArgs P, int64_t i0) {
 }
 
 // Draw of seed t + 1 from the weights after the pass with seed t.
-__global__ __launch_bounds__(kPPSelThreads) void k_pp_select(PPArgs P, int t, int s_slot, int table) {
+__global__ __launch_bounds__(kPPSelThreads) void k_pp_select(PPArgs P, int t, int table) {
     __shared__ uint64_t scan_lds[16];
     __shared__ int64_t s_pick;
     __shared__ int64_t s_blk;
@@ -331,7 +323,7 @@ __global__ __launch_bounds__(kPPSelThreads) void k_pp_select(PPArgs P, int t, in
         __syncthreads();
         const int64_t blk = s_blk;
         if (blk >= 0) {   // always, as the block sums add up to W
-            const int S = weight_scale(__longlong_as_double((long long)P.Mb[s_slot]), P.L);
+            const int S = weight_scale(__longlong_as_double((long long)P.Mb[t]), P.L);
             const int64_t i0 = blk * kPPChunk + 2 * tid;
             const uint64_t w0 = i0 < P.n ? weight_of(P.D2[i0], S) : 0;
             const uint64_t w1 = i0 + 1 < P.n ? weight_of(P.D2[i0 + 1], S) : 0;
@@ -400,15 +392,15 @@ __global__ __launch_bounds__(256) void k_pp_dcc(PPArgs P, int t, int G, int vec4
     if (a <= t && r == 0) P.dcc[a] = acc * (1.0 - 0x1p-28);
 }
 
-template <bool FIRST, bool WEIGHTS, bool PRUNE>
-hipError_t step_vec(const PPArgs& P, int t, int s_slot, int vw, hipStream_t s) {
+template <bool FIRST, bool PRUNE>
+hipError_t step_vec(const PPArgs& P, int t, int vw, hipStream_t s) {
     const dim3 grid((unsigned)P.G), block(kPPThreads);
     if (vw == 2)
-        hipLaunchKernelGGL((k_pp_step<FIRST, WEIGHTS, PRUNE, 2>), grid, block, 0, s, P, t, s_slot);
+        hipLaunchKernelGGL((k_pp_step<FIRST, PRUNE, 2>), grid, block, 0, s, P, t);
     else if (vw == 1)
-        hipLaunchKernelGGL((k_pp_step<FIRST, WEIGHTS, PRUNE, 1>), grid, block, 0, s, P, t, s_slot);
+        hipLaunchKernelGGL((k_pp_step<FIRST, PRUNE, 1>), grid, block, 0, s, P, t);
     else
-        hipLaunchKernelGGL((k_pp_step<FIRST, WEIGHTS, PRUNE, 0>), grid, block, 0, s, P, t, s_slot);
+        hipLaunchKernelGGL((k_pp_step<FIRST, PRUNE, 0>), grid, block, 0, s, P, t);
     return hipGetLastError();
 }
 
@@ -421,7 +413,7 @@ constexpr int64_t kPPTableInline = 4096;
 
 int pp_launches(int k, int d, bool prune) {
     if (k == 1) return 2;
-    int n = 3 + 2 * (k - 1);
+    int n = 3 + 3 * (k - 1) - 1;   // set-up, first pass, weights; per draw: select, pass, weights (not after the last)
     if (prune)
         for (int t = 0; t + 1 < k; ++t) n += (int64_t)(t + 1) * d > kPPTableInline;
     return n;
@@ -439,17 +431,16 @@ hipError_t launch_pp_seed(const PPArgs& P, int64_t i0, int vw, hipEvent_t* ev, i
     if ((e = mark(2)) != hipSuccess) return e;
     hipLaunchKernelGGL(k_pp_init, dim3(1), dim3(256), 0, s, P, i0);
     if ((e = hipGetLastError()) != hipSuccess || (e = mark(2)) != hipSuccess) return e;
-    e = P.prune ? step_vec<true, false, true>(P, 0, 0, vw, s) : step_vec<true, false, false>(P, 0, 0, vw, s);
+    e = P.prune ? step_vec<true, true>(P, 0, vw, s) : step_vec<true, false>(P, 0, vw, s);
     if (e != hipSuccess || (e = mark(0)) != hipSuccess) return e;
     if (P.k == 1) return hipSuccess;
-    hipLaunchKernelGGL(k_pp_weights, dim3((unsigned)P.G), dim3(kPPThreads), 0, s, P);
+    hipLaunchKernelGGL(k_pp_weights, dim3((unsigned)P.G), dim3(kPPThreads), 0, s, P, 0);
     if ((e = hipGetLastError()) != hipSuccess || (e = mark(2)) != hipSuccess) return e;
     int G = 1;   // lanes per earlier seed in k_pp_dcc
     while (G < 64 && 16 * G < P.d) G *= 2;
     for (int t = 0; t + 1 < P.k; ++t) {
         const bool own = P.prune && (int64_t)(t + 1) * P.d > kPPTableInline;
-        hipLaunchKernelGGL(k_pp_select, dim3(1), dim3(kPPSelThreads), 0, s, P, t, t == 0 ? 0 : t - 1,
-                           (P.prune && !own) ? 1 : 0);
+        hipLaunchKernelGGL(k_pp_select, dim3(1), dim3(kPPSelThreads), 0, s, P, t, (P.prune && !own) ? 1 : 0);
         if ((e = hipGetLastError()) != hipSuccess || (e = mark(2)) != hipSuccess) return e;
         if (own) {
             const int64_t thr = (int64_t)(t + 1) * G;
@@ -457,15 +448,13 @@ hipError_t launch_pp_seed(const PPArgs& P, int64_t i0, int vw, hipEvent_t* ev, i
                                vw > 0 ? 1 : 0);
             if ((e = hipGetLastError()) != hipSuccess || (e = mark(2)) != hipSuccess) return e;
         }
-        const int tn = t + 1;   // pass with the new seed; its weights serve the next draw
-        const bool weights = tn + 1 < P.k;
-        if (P.prune)
-            e = weights ? step_vec<false, true, true>(P, tn, tn - 1, vw, s)
-                        : step_vec<false, false, true>(P, tn, 0, vw, s);
-        else
-            e = weights ? step_vec<false, true, false>(P, tn, tn - 1, vw, s)
-                        : step_vec<false, false, false>(P, tn, 0, vw, s);
+        const int tn = t + 1;   // pass with the new seed, then the weights of the next draw
+        e = P.prune ? step_vec<false, true>(P, tn, vw, s) : step_vec<false, false>(P, tn, vw, s);
         if (e != hipSuccess || (e = mark(1)) != hipSuccess) return e;
+        if (tn + 1 < P.k) {
+            hipLaunchKernelGGL(k_pp_weights, dim3((unsigned)P.G), dim3(kPPThreads), 0, s, P, tn);
+            if ((e = hipGetLastError()) != hipSuccess || (e = mark(2)) != hipSuccess) return e;
+        }
     }
     return hipSuccess;
 }

@@ -63,6 +63,26 @@ def test_every_draw_lands_in_its_d2_interval(seed, n, d, k):
             assert got[t] == i, (t, i, got[t])
 
 
+def test_draw_follows_d2_after_the_maximum_collapses():
+    # Ten points on a line with spacing 1e-5 and one point at 1e6.  Seed 0 is
+    # the first point; seed 1 is the far point (its D^2 ~ 1e12 dominates).
+    # After that the maximum of D^2 falls by about 2^60, to 8.1e-9.  The draw
+    # of seed 2 must still follow D^2 / sum D^2 among the near points: a
+    # weight scale taken from an earlier, larger maximum would round every
+    # weight to zero here.
+    X = np.zeros((11, 1), np.float32)
+    X[:10, 0] = (np.arange(10) * 1e-5).astype(np.float32)
+    X[10, 0] = 1e6
+    assert oracle.kmeanspp(X, 2, np.array([0.0, 0.5]))["idx"].tolist() == [0, 10]
+    D2 = _d2_numpy(X, [0, 10])
+    p = D2 / D2.sum()
+    hi = np.cumsum(p)
+    lo = hi - p
+    for i in range(1, 10):
+        u = np.array([0.0, 0.5, 0.5 * (lo[i] + hi[i])])
+        assert oracle.kmeanspp(X, 3, u)["idx"].tolist() == [0, 10, i], i
+
+
 def test_draw_frequencies_follow_d2():
     # many seeded draws of the second seed: chi-square against D^2 / sum D^2
     rng = np.random.default_rng(4)
