@@ -208,7 +208,8 @@ const char* kmeans_mti_path(const km_ctx* ctx);
  *     fused multiply-add;
  *   - the draw of seed t+1 uses integer weights w_i = floor(D2_i * 2^S),
  *     S = 62 - e - ceil(log2 n) with M < 2^e for M = max D2 after the pass
- *     with seed max(t - 1, 0); W = sum w_i, T = min(floor(u[t+1] * W), W - 1)
+ *     with seed t (the current maximum); W = sum w_i,
+ *     T = min(floor(u[t+1] * W), W - 1)
  *     (float64 product), and the seed is the smallest i whose inclusive
  *     prefix sum of w exceeds T; W = 0 (every row lies on a seed) draws
  *     min(floor(u[t+1] * n), n - 1).
@@ -226,7 +227,7 @@ const char* kmeans_mti_path(const km_ctx* ctx);
  * 256-byte aligned, owned by the caller; its contents on entry do not matter
  * and it must not be used by another call until this one's work completes.
  * Requires 1 <= k <= n, d >= 1.  Work is ordered on hip_stream (NULL = null
- * stream) with at most 3k kernel launches and no allocation; asynchronous unless
+ * stream) with at most 4k kernel launches and no allocation; asynchronous unless
  * stats (HOST, nullable) is given, in which case it synchronizes and fills
  * it.  Errors: KM_ERR_INVALID_ARG for bad sizes or pointers, a u outside
  * [0, 1), unknown flags or a short or misaligned workspace; KM_ERR_HIP on a
@@ -251,6 +252,30 @@ size_t kmeans_pp_workspace_bytes(int64_t n, int32_t d, int32_t k);   /* 0 for ba
 int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double* u, float* C_out,
                    int64_t* idx_out, double* d2_out, void* workspace, size_t workspace_bytes,
                    uint32_t flags, void* hip_stream, km_pp_stats* stats);
+
+/*
+ * k-means++ with restarts (section IV-C: the best of several seeded runs).
+ * For each run q = 0..r-1: seed k rows with kmeans_pp_seed from the uniforms
+ * U[q*k .. q*k + k - 1], run k-means from those seeds as kmeans_mti_run does
+ * (max_iters, tol, flags with KM_FLAG_STATS added), and keep the run with the
+ * least final inertia (float32 distances summed exactly); an exact tie keeps
+ * the earlier run.
+ *
+ * X: device, n x d float32.  U: HOST, r * k doubles in [0, 1).  assign_out
+ * (n int32) and C_out (k x d float32): device, receive the kept run's
+ * assignment and centroids.  best_out (HOST, nullable): the kept run's index.
+ * inertia_out (HOST, nullable, r doubles): every run's final inertia.  stats
+ * (HOST, nullable): the kept run's totals.  Requires r >= 1 and the sizes of
+ * kmeans_mti_run; flags as for kmeans_mti_run (KM_FLAG_NO_PRUNE also
+ * computes every seeding distance).  Allocates its device workspace (the
+ * seeding workspace, the seeds and one spare run's outputs) and frees it
+ * before returning.  Synchronizes.  Errors as kmeans_mti_run and
+ * kmeans_pp_seed.
+ */
+int kmeans_pp_run_best(const float* X, int64_t n, int32_t d, int32_t k, const double* U, int32_t r,
+                       int32_t max_iters, double tol, int32_t* assign_out, float* C_out,
+                       void* hip_stream, uint32_t flags, int32_t* best_out, double* inertia_out,
+                       km_stats* stats);
 
 /* Release a context and its device scratch.  NULL-safe.  Synchronizes. */
 void kmeans_mti_destroy(km_ctx* ctx);

@@ -859,6 +859,70 @@ int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double
     return KM_OK;
 }
 
+int kmeans_pp_run_best(const float* X, int64_t n, int32_t d, int32_t k, const double* U, int32_t r,
+                       int32_t max_iters, double tol, int32_t* assign_out, float* C_out, void* hip_stream,
+                       uint32_t flags, int32_t* best_out, double* inertia_out, km_stats* stats) {
+    if (!U || r < 1 || max_iters < 1 || !(tol >= 0.0) || !assign_out || !C_out) return KM_ERR_INVALID_ARG;
+    int rc = check_shape(X, n, d, k, X);
+    if (rc != KM_OK) return rc;
+    if ((int64_t)r > INT64_MAX / k) return KM_ERR_INVALID_ARG;
+    for (int64_t j = 0; j < (int64_t)r * k; ++j)
+        if (!(U[j] >= 0.0 && U[j] < 1.0)) {
+            snprintf(g_last_hip, sizeof g_last_hip, "U[%lld] is not in [0, 1)", (long long)j);
+            return KM_ERR_INVALID_ARG;
+        }
+    const size_t wsb = kmeans_pp_workspace_bytes(n, d, k);
+    if (wsb == 0) return KM_ERR_INVALID_ARG;
+    int dev = 0;
+    KM_HIP(hipGetDevice(&dev));
+    if ((rc = check_device_range(assign_out, (size_t)n * 4, dev, "assign_out")) != KM_OK) return rc;
+    if ((rc = check_device_range(C_out, (size_t)k * d * 4, dev, "C_out")) != KM_OK) return rc;
+    hipStream_t st = static_cast<hipStream_t>(hip_stream);
+    // One allocation: seeding workspace | seeds | spare assignment | spare centroids.
+    auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
+    const size_t o_seed = up(wsb), o_a = o_seed + up((size_t)k * d * 4), o_c = o_a + up((size_t)n * 4);
+    const size_t total = o_c + up((size_t)k * d * 4);
+    char* buf = nullptr;
+    KM_HIP(hipMalloc(reinterpret_cast<void**>(&buf), total));
+    float* seeds = reinterpret_cast<float*>(buf + o_seed);
+    int32_t* spare_a = reinterpret_cast<int32_t*>(buf + o_a);
+    float* spare_c = reinterpret_cast<float*>(buf + o_c);
+    const uint32_t ppf = (flags & KM_FLAG_NO_PRUNE) ? KM_PP_NO_PRUNE : 0u;
+    int32_t best = -1;
+    km_stats best_st{};
+    for (int32_t q = 0; q < r && rc == KM_OK; ++q) {
+        rc = kmeans_pp_seed(X, n, d, k, U + (int64_t)q * k, seeds, nullptr, nullptr, buf, wsb, ppf, hip_stream,
+                            nullptr);
+        if (rc != KM_OK) break;
+        // The first run writes the outputs directly; later runs write the
+        // spare buffers, copied over the outputs when they are better.
+        int32_t* a_dst = q == 0 ? assign_out : spare_a;
+        float* c_dst = q == 0 ? C_out : spare_c;
+        km_stats s{};
+        rc = kmeans_mti_run(X, n, d, k, seeds, max_iters, tol, a_dst, c_dst, hip_stream, flags | KM_FLAG_STATS, &s);
+        if (rc != KM_OK) break;
+        if (inertia_out) inertia_out[q] = s.inertia_last;
+        if (best < 0 || s.inertia_last < best_st.inertia_last) {
+            best = q;
+            best_st = s;
+            if (q > 0) {
+                hipError_t e = hipMemcpyAsync(assign_out, spare_a, (size_t)n * 4, hipMemcpyDeviceToDevice, st);
+                if (e == hipSuccess)
+                    e = hipMemcpyAsync(C_out, spare_c, (size_t)k * d * 4, hipMemcpyDeviceToDevice, st);
+                if (e == hipSuccess) e = hipStreamSynchronize(st);
+                if (e != hipSuccess) rc = hip_fail(e, "kmeans_pp_run_best copy");
+            }
+        }
+    }
+    (void)hipStreamSynchronize(st);
+    hipError_t ef = hipFree(buf);
+    if (rc != KM_OK) return rc;
+    if (ef != hipSuccess) return hip_fail(ef, "hipFree");
+    if (best_out) *best_out = best;
+    if (stats) *stats = best_st;
+    return KM_OK;
+}
+
 const char* kmeans_mti_path(const km_ctx* ctx) {
     if (!ctx) return "";
     if (ctx->small) return ctx->inc ? "stream-d16" : "stream-d16-full";

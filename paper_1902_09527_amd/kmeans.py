@@ -258,26 +258,32 @@ def kmeanspp_workspace_bytes(n: int, d: int, k: int) -> int:
 
 def run_pp_best(X: torch.Tensor, k: int, U, max_iters: int, tol: float = 0.0, prune: bool = True,
                 stream: Optional[torch.cuda.Stream] = None) -> Dict[str, object]:
-    """The paper's k-means++ with r restarts: for each row of U (r x k
-    uniforms) seed with k-means++, run k-means from the seeds, and keep the
-    run with the least final inertia (ties: the earlier run).
+    """The paper's k-means++ with r restarts (kmeans_pp_run_best): for each
+    row of U (r x k uniforms) seed with k-means++ and run k-means from the
+    seeds; the library keeps the run with the least final inertia (ties: the
+    earlier run).
 
-    Returns ``best`` (the run index), ``assign``, ``C``, ``stats`` of that run
-    and ``inertia`` (every run's final inertia).
+    Returns ``best`` (the kept run's index), ``assign``, ``C``, ``stats`` of
+    that run and ``inertia`` (every run's final inertia).
     """
-    U = np.asarray(U, dtype=np.float64)
+    _check_matrix(X, "X")
+    U = np.ascontiguousarray(np.asarray(U, dtype=np.float64))
     if U.ndim != 2 or U.shape[1] != int(k):
         raise ValueError("U must be r x k")
-    best = None
-    inertia = []
-    ws = None
-    for r in range(U.shape[0]):
-        if ws is None:
-            ws = torch.empty(kmeanspp_workspace_bytes(X.shape[0], X.shape[1], k) + 256, dtype=torch.uint8,
-                             device=X.device)
-        seeds = kmeanspp(X, k, U[r], prune=prune, workspace=ws, stream=stream)
-        a, c, st = run(X, seeds["C"], max_iters, tol, prune=prune, stats=True, stream=stream)
-        inertia.append(st["inertia_last"])
-        if best is None or st["inertia_last"] < best[3]["inertia_last"]:
-            best = (r, a, c, st)
-    return {"best": best[0], "assign": best[1], "C": best[2], "stats": best[3], "inertia": inertia}
+    lib = N.load()
+    n, d = X.shape
+    k = int(k)
+    r = U.shape[0]
+    a = torch.empty(n, dtype=torch.int32, device=X.device)
+    c = torch.empty(k, d, dtype=torch.float32, device=X.device)
+    best = C.c_int32(-1)
+    inertia = np.zeros(r, np.float64)
+    s = N.KmStats()
+    with torch.cuda.device(X.device):
+        st = lib.kmeans_pp_run_best(C.c_void_p(X.data_ptr()), n, d, k, U.ctypes.data_as(C.c_void_p), r,
+                                    int(max_iters), float(tol), C.c_void_p(a.data_ptr()),
+                                    C.c_void_p(c.data_ptr()), _stream_ptr(X.device, stream),
+                                    _flags(prune, False, False), C.byref(best),
+                                    inertia.ctypes.data_as(C.c_void_p), C.byref(s))
+    N.check(st, "kmeans_pp_run_best")
+    return {"best": int(best.value), "assign": a, "C": c, "stats": s.as_dict(), "inertia": inertia.tolist()}
