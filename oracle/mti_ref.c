@@ -98,6 +98,10 @@ int32_t mti_lloyd(const float* X, int64_t n, int32_t d, int32_t k, const double*
     for (; t < max_iters; ++t) {
         mti_centroid_table(C, k, d, scale, h, s);
         int64_t n_changed = 0, n_computed = 0, n_clause1 = 0;
+        /* Points are independent within a step (each reads the shared tables
+           and writes only its own a[i], u[i]), so they run in parallel; the
+           counts are integer sums, the same for any thread count. */
+#pragma omp parallel for schedule(static) reduction(+ : n_changed, n_computed, n_clause1)
         for (int64_t i = 0; i < n; ++i) {
             const float* x = X + i * (int64_t)d;
             if (t == 0) {
