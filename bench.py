@@ -1,14 +1,17 @@
 #!/usr/bin/env python3
 """Benchmark of the MTI k-means hot path on one MI355X.
 
-A step is one Lloyd iteration with MTI pruning: centroid table and drift,
+An iteration is one Lloyd step with MTI pruning: centroid table and drift,
 bound update and Clause-1 test, fused distance + argmin of the survivors,
-per-cluster reduction into new centroids and the convergence counters.  The
-timed region enqueues K consecutive iterations of a run started from the
-workload's seeded initial centroids (inputs already resident in HBM) and is
-bracketed by device synchronisation; the reported value is iterations per
-second.  Per-kernel device times come from HIP events recorded by the
-library on its stream around every launch.
+per-cluster reduction into new centroids and the convergence counters.  A
+timed step is one whole run of the workload as it is defined: a
+kmeans_mti_run call from the seeded initial centroids until fewer than
+tol * n points change assignment (or max_iters), context set-up and release
+included, with the inputs already resident in HBM.  K runs are timed between
+device synchronisations; the reported value is iterations per second over
+them.  The steady state (steps after the first) and the first step are
+reported beside it from HIP events the library records on its stream around
+every launch.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--spherical] [--no-cpu-baseline]
     python bench.py --kmeanspp [--workload NAME]      (k-means++ seeding)
@@ -111,25 +114,75 @@ def mfma_roofline_entry(kernel: str, workload: str, flops_per_launch: float, lau
             "kernel_us": launch_ms * 1e3}
 
 
-def cpu_baseline(X, C0, w, budget_s: float = 15.0, spherical: bool = False) -> dict:
-    """Time the CPU oracle (plain float64 Lloyd's or spherical k-means, as it
-    stands) on this host."""
+def host_cpu() -> dict:
+    """CPU model and the cores this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count() or 1
+    return {"cpu_model": model, "nproc": nproc}
+
+
+def cpu_baseline(X, C0, w, spherical: bool = False) -> dict:
+    """Time the CPU oracle as it stands on this host: plain float64 Lloyd's
+    on every thread OpenMP gives it (value), on one thread, and the float64
+    MTI reference on every thread (the paper's method on the host).  Each leg
+    is bounded to about 10 s of CPU work and scaled to iterations/s."""
     import oracle
-    fn = oracle.spherical if spherical else oracle.lloyd
+    if spherical:   # the spherical oracle is a single-threaded loop
+        t0 = time.perf_counter()
+        r = oracle.spherical(X, C0, 1, 0.0)
+        t1 = time.perf_counter() - t0
+        iters = int(max(1, min(w.max_iters, 10.0 // max(t1, 1e-3))))
+        t0 = time.perf_counter()
+        r = oracle.spherical(X, C0, iters, w.tol)
+        el = time.perf_counter() - t0
+        return dict(host_cpu(), value=r["iters"] / el, unit="iters/s", cores=1, kind="oracle",
+                    sample="all %d rows of %s, spherical k-means run from the seeded centroids "
+                           "(tol %g), first %d iterations" % (w.n, w.name, w.tol, r["iters"]))
+    P = oracle.get_threads()
     t0 = time.perf_counter()
-    fn(X, C0, 1, 0.0)
+    oracle.lloyd(X, C0, 1, 0.0)
     t1 = time.perf_counter() - t0
-    iters = int(max(1, min(w.max_iters, budget_s // max(t1, 1e-3))))
+    # P threads: the workload's own run (tol stop), at most ~10 s of iterations
+    cap = int(max(1, min(w.max_iters, 10.0 // max(t1, 1e-3))))
     t0 = time.perf_counter()
-    r = fn(X, C0, iters, 0.0)
+    r = oracle.lloyd(X, C0, cap, w.tol)
     el = time.perf_counter() - t0
-    ips = r["iters"] / el
-    return {
-        # the spherical oracle is a single-threaded loop
-        "value": ips, "unit": "iters/s", "cores": 1 if spherical else oracle.get_threads(), "kind": "oracle",
-        "sample": "all %d rows of %s, first %d iterations from the seeded centroids (tol ignored); "
-                  "%.3g effective dist evals/s" % (w.n, w.name, r["iters"], ips * w.n * w.k),
-    }
+    out = dict(host_cpu(), value=r["iters"] / el, unit="iters/s", cores=P, kind="oracle",
+               sample="all %d rows of %s, the run from the seeded centroids with tol %g: %d iterations%s "
+                      "(%.3g effective dist evals/s)" % (
+                          w.n, w.name, w.tol, r["iters"],
+                          " (capped)" if r["iters"] == cap and cap < w.max_iters else "",
+                          r["iters"] * w.n * w.k / el))
+    # one thread: one iteration on a row prefix sized to ~10 s, scaled to all rows
+    rows = int(min(w.n, max(w.k, w.n * 10.0 / max(t1 * P, 1e-3))))
+    oracle.set_threads(1)
+    try:
+        t0 = time.perf_counter()
+        oracle.lloyd(X[:rows], C0, 1, 0.0)
+        el1 = time.perf_counter() - t0
+    finally:
+        oracle.set_threads(P)
+    out["one_thread"] = {"value": rows / (el1 * w.n), "unit": "iters/s", "cores": 1,
+                         "sample": "first iteration on the first %d rows, scaled to %d rows" % (rows, w.n)}
+    # the float64 MTI reference (pruned Lloyd's on the host) on P threads
+    t0 = time.perf_counter()
+    rm = oracle.mti(X, C0, cap, w.tol)
+    elm = time.perf_counter() - t0
+    out["mti_ref"] = {"value": rm["iters"] / elm, "unit": "iters/s", "cores": P,
+                      "pruned_frac": 1.0 - float(rm["computed"].sum()) / (w.n * w.k * rm["iters"]),
+                      "sample": "the same run with the float64 MTI reference (%d iterations)" % rm["iters"]}
+    return out
 
 
 def bench_kmeanspp(args, w, X) -> dict:
@@ -208,7 +261,8 @@ def bench_kmeanspp(args, w, X) -> dict:
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=None, help="timed iterations (default: workload max_iters)")
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed whole runs of the workload (default 20; k-means++: seedings, default 5)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(
         ["blobs-10k-d16-k8", "blobs-1M-d32-k100", "aniso-8M-d16-k10", "blobs-2M-d256-k1000",
@@ -253,7 +307,7 @@ def main() -> int:
     import paper_1902_09527_amd as km
 
     w = synth.WORKLOADS[args.workload]
-    K = args.steps or w.max_iters
+    K = args.steps or 20
     log("workload %s: n=%d d=%d k=%d; generating" % (w.name, w.n, w.d, w.k))
     X, C0, _ = synth.make(w.name)
     if args.kmeanspp:
@@ -264,7 +318,6 @@ def main() -> int:
     Cg = torch.from_numpy(C0).to(dev)
     torch.cuda.synchronize()
 
-    # Warmup: W iterations on a throwaway context (kernel load, caches, clocks).
     if args.profile:
         args.no_cpu_baseline = True
     base_flags = {"full_sums": True} if args.full_sums else {}
@@ -274,101 +327,113 @@ def main() -> int:
         base_flags["elkan"] = True
     # profiles/<kernel>_<tag>.txt holds the counters of this workload and method
     tag = w.name + ("-spherical" if args.spherical else "") + ("-elkan" if args.elkan else "")
-    if args.warmup > 0:
-        with km.KMeansMTI(Xg, Cg, **base_flags) as ctx:
-            for _ in range(args.warmup):
-                ctx.iterate()
-            torch.cuda.synchronize()
-    log("warmup done (%d iterations)" % args.warmup)
 
-    # Timed region: K iterations from C0, nothing else on the stream.
-    ctx = km.KMeansMTI(Xg, Cg, **base_flags)
-    path = ctx.path()
+    def job():
+        return km.run(Xg, Cg, w.max_iters, w.tol, **base_flags)
+
+    # Warmup: W whole runs (kernel load, caches, clocks).
+    for _ in range(args.warmup):
+        job()
+    torch.cuda.synchronize()
+    log("warmup done (%d runs)" % args.warmup)
+
+    # Timed region: K whole runs of the workload as it is defined (from the
+    # seeded centroids until fewer than tol * n points change, or max_iters),
+    # each a kmeans_mti_run call: context set-up, iterations, results, release.
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(K):
-        ctx.iterate()
+    runs = [job()[2] for _ in range(K)]
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    hist = ctx.history()
-    ctx.close()
-    log("timed %d iterations in %.3f ms (path %s)" % (K, elapsed * 1e3, path))
+    iters = runs[0]["iterations"]
+    assert all(r["iterations"] == iters for r in runs), "runs differ in their iteration count"
+    loop_ms = sum(r["device_ms"] for r in runs) / K
+    n, d, k = w.n, w.d, w.k
+    with km.KMeansMTI(Xg, Cg, **base_flags) as pctx:
+        path = pctx.path()
+    log("timed %d runs of %d iterations in %.3f ms (path %s)" % (K, iters, elapsed * 1e3, path))
 
-    # The same K iterations again with HIP events around every launch (on the
-    # library's stream) for the per-kernel device times; the first step is
-    # timed on its own, since it runs the full streaming kernel on every path.
-    def kernel_pass(**flags):
+    # The same run's iterations again with HIP events around every launch (on
+    # the library's stream): the first step on its own, then steps 1..T-1 as
+    # the steady state.
+    def kernel_pass(T, **flags):
         with km.KMeansMTI(Xg, Cg, timing=True, **flags) as tctx:
             tctx.iterate()
             t_first = tctx.timing()
-            for _ in range(K - 1):
+            for _ in range(T - 1):
                 tctx.iterate()
             t_all = tctx.timing()
             h = tctx.history()
         later = {key: t_all[key] - t_first[key] for key in t_all if key.endswith("_ms")}
         return t_first, later, h
 
-    n, d, k = w.n, w.d, w.k
-    tm = first_t = later_t = None
+    KS = max(iters, 2)   # steps of the steady-state pass (a one-step run adds one step)
+    first_t = later_t = None
     rooflines = []
-    if not args.profile and K > 1:
-        first_t, later_t, h_ev = kernel_pass(**base_flags)
-        tm = {key: first_t[key] + later_t[key] for key in later_t}
-        tm["iters"] = K
+    steady = None
+    hist = None
+    if not args.profile:
+        first_t, later_t, hist = kernel_pass(KS, **base_flags)
+        m = KS - 1
+        steady_ms = sum(later_t[key] for key in ("assign_ms", "reduce_ms", "update_ms", "table_ms")) / m
+        steady = {"steps": "1..%d" % (KS - 1), "ms_per_iter": steady_ms, "iters_per_s": 1e3 / steady_ms,
+                  "kernel_ms_per_iter": {key[:-3]: later_t[key] / m for key in
+                                         ("assign_ms", "reduce_ms", "update_ms", "table_ms")}}
         kernel = DOMINANT_KERNEL.get(path, path)
-        surv = n * (K - 1) - int(h_ev["clause1"][1:].sum())
-        ch = int(h_ev["changed"][1:].sum())
+        surv = n * m - int(hist["clause1"][1:KS].sum())
+        ch = int(hist["changed"][1:KS].sum())
+        comp = int(hist["computed"][1:KS].sum())
+        launch_ms = later_t["assign_ms"] / m
+        # Algorithmic bytes per step: every point's assignment read and bound
+        # read and written (12 B) plus, with incremental sums, the rows of the
+        # Clause-1 survivors and of the changed points (4d B each), or with
+        # full sums every row (4d B) and the changed assignments (4 B).
         if path == "stream-d16":
-            # Incremental steps: every point's 4-byte state read; a survivor's
-            # row read and its state rewritten (Clause-1 points are not written).
-            bytes_per_launch = (4 * n * (K - 1) + (4 * d + 4) * surv) / (K - 1)
-            what = "steps 2..K: 4n (states) + survivors*(4d+4) (rows, new states)"
-        elif path == "stream-d16-full":
-            bytes_per_launch = (n * (4 * d + 4) * (K - 1) + 4 * surv) / (K - 1)
-            what = "steps 2..K: n*(4d+4) (rows, states) + survivors*4 (new states)"
+            bytes_per_launch = 12.0 * n + 4.0 * d * (surv + ch) / m
+            what = "steps 1..T-1: 12n (assignment, bound) + 4d per Clause-1 survivor and per changed point"
         elif path == "lds-elkan":
-            comp = int(h_ev["computed"][1:].sum())
-            bytes_per_launch = n * (4 * d + 12) + (4.0 * k * surv + 4.0 * comp + 4 * ch) / (K - 1)
-            what = ("steps 2..K: n*(4d+12) + 4k per Clause-1 survivor (lower bounds read) "
+            bytes_per_launch = n * (4 * d + 12) + (4.0 * k * surv + 4.0 * comp + 4 * ch) / m
+            what = ("steps 1..T-1: n*(4d+12) + 4k per Clause-1 survivor (lower bounds read) "
                     "+ 4 per computed distance (lower bound written) + changed*4")
         else:
-            bytes_per_launch = n * (4 * d + 12) + 4 * ch / (K - 1)
-            what = "steps 2..K: n*(4d+12) + changed*4"
-        launch_ms = later_t["assign_ms"] / (K - 1)
-        flops = 2.0 * d * k * surv / (K - 1)
+            bytes_per_launch = n * (4 * d + 12) + 4.0 * ch / m
+            what = "steps 1..T-1: n*(4d+12) (rows, assignment, bound) + changed*4"
+        flops = 2.0 * d * k * surv / m
         if path == "global-mfma":
-            # The matrix-core distance product of the survivors dominates (the
-            # bound pass before it streams 8 bytes per point).
             rooflines.append(mfma_roofline_entry(kernel, tag, flops, launch_ms,
-                                                 "steps 2..K: 2*d*k per Clause-1 survivor (bound pass included in the time)"))
+                                                 "steps 1..T-1: 2*d*k per Clause-1 survivor (bound pass included in the time)"))
             rooflines.append(roofline_entry(kernel, tag, bytes_per_launch, launch_ms, what))
         else:
             rooflines.append(roofline_entry(kernel, tag, bytes_per_launch, launch_ms, what))
             if path == "lds-mfma":
                 rooflines.append(mfma_roofline_entry(kernel, tag, flops, launch_ms,
-                                                     "steps 2..K: 2*d*k per Clause-1 survivor"))
+                                                     "steps 1..T-1: 2*d*k per Clause-1 survivor"))
         if path == "stream-d16":   # the full-read streaming kernel on the same steps
-            _, later_f, h_f = kernel_pass(**dict(base_flags, full_sums=True))
-            surv_f = n * (K - 1) - int(h_f["clause1"][1:].sum())
-            rooflines.append(roofline_entry("k_small", tag, (n * (4 * d + 4) * (K - 1) + 4 * surv_f) / (K - 1),
-                                            later_f["assign_ms"] / (K - 1),
-                                            "steps 2..K with KM_FLAG_FULL_SUMS: n*(4d+4) + survivors*4"))
+            _, later_f, h_f = kernel_pass(KS, **dict(base_flags, full_sums=True))
+            ch_f = int(h_f["changed"][1:KS].sum())
+            rooflines.append(roofline_entry("k_small", tag, n * (4 * d + 12) + 4.0 * ch_f / m,
+                                            later_f["assign_ms"] / m,
+                                            "steps 1..T-1 with KM_FLAG_FULL_SUMS: n*(4d+12) + changed*4"))
+        # The first step (no bounds yet): every row read and every point's
+        # assignment and bound written; on the global path every point's k
+        # distances go through the matrix cores.
+        first_kernel = "k_small" if path.startswith("stream") else kernel
+        if path == "global-mfma":
+            rooflines.append(mfma_roofline_entry(first_kernel, tag + "-first-step", 2.0 * d * k * n,
+                                                 first_t["assign_ms"], "first step: 2*d*k per point"))
+        else:
+            rooflines.append(roofline_entry(first_kernel, tag + "-first-step", n * (4.0 * d + 8),
+                                            first_t["assign_ms"],
+                                            "first step: n*(4d+8) (rows read, assignment and bound written)"))
 
-    # The job as the workload defines it (tol stop), for the iteration count.
-    job = {"iterations": 0, "converged": 0, "device_ms": 0.0}
-    if not args.profile:
-        _, _, job = km.run(Xg, Cg, w.max_iters, w.tol, **base_flags)
-        torch.cuda.synchronize()
-
-    ips = K / elapsed
-    computed = int(hist["computed"].sum())
-    lloyd = n * k * K
+    value = K * iters / elapsed
+    lloyd = n * k * KS
     roof = rooflines[0] if rooflines else {"kernel": DOMINANT_KERNEL.get(path, path), "bound": "hbm",
                                           "achieved": None, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                           "frac": None, "traffic": None}
     result = {
         "metric": METRIC,
-        "value": ips,
+        "value": value,
         "unit": "iters/s",
         "n_gpus": 1,
         "steps": K,
@@ -382,25 +447,27 @@ def main() -> int:
         "config": {"workload": w.name, "method": ("spherical" if args.spherical else "kmeans") +
                    ("+elkan-ti" if args.elkan else ""),
                    "n": n, "d": d, "k": k, "max_iters": w.max_iters, "tol": w.tol,
-                   "timed": "first %d iterations from the seeded centroids" % K, "path": path},
-        "eff_dist_evals_per_s": lloyd / elapsed,
-        # The bytes a full-read Lloyd step moves (every row and its point
-        # state) over the measured step time, against the HBM peak: above 1
-        # when pruning skips rows.
-        "full_read_equiv_hbm_frac": n * (4 * d + 4) / (elapsed / K) / (HBM_PEAK_GBS * 1e9),
-        "computed_dist_evals_per_s": computed / elapsed,
-        "pruned_frac": 1.0 - computed / lloyd,
-        "clause1_frac": float(hist["clause1"].sum()) / (n * K),
-        "kernel_ms_per_iter": None if tm is None else
-            {key[:-3]: tm[key] / max(1, tm["iters"]) for key in ("assign_ms", "reduce_ms", "update_ms", "table_ms")},
+                   "step": "one whole run (kmeans_mti_run from the seeded centroids to the tol stop, "
+                           "set-up and release included)",
+                   "iters_per_step": iters, "converged": bool(runs[0]["converged"]), "path": path},
+        "ms_per_iter": elapsed * 1e3 / (K * iters),
+        "eff_dist_evals_per_s": value * n * k,
+        "run_loop_device_ms": loop_ms,
+        "run_setup_ms": elapsed * 1e3 / K - loop_ms,
+        "steady_state": steady,
         "first_step_ms": None if first_t is None else
             {key[:-3]: first_t[key] for key in ("assign_ms", "reduce_ms", "update_ms", "table_ms")},
-        "job": {"iterations": job["iterations"], "converged": bool(job["converged"]),
-                "device_ms": job["device_ms"],
-                "iters_per_s": job["iterations"] / (job["device_ms"] / 1e3) if job["device_ms"] else None},
         "roofline": roof,
         "rooflines_all": rooflines[1:],
     }
+    if hist is not None:
+        computed = int(hist["computed"][:KS].sum())
+        result.update({
+            "computed_dist_evals_per_s": value * computed / KS,
+            "pruned_frac": 1.0 - computed / lloyd,
+            "pruned_frac_steady": 1.0 - int(hist["computed"][1:KS].sum()) / (n * k * (KS - 1)),
+            "clause1_frac_steady": float(hist["clause1"][1:KS].sum()) / (n * (KS - 1)),
+        })
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         result["cpu_baseline"] = cpu_baseline(X, C0, w, spherical=args.spherical)
