@@ -101,6 +101,41 @@ def test_global_memory_path_is_bitwise_identical_to_lds_path(case):
     assert s2["inertia_last"] == pytest.approx(s1["inertia_last"], rel=1e-5)
 
 
+# The global path (and the LDS matrix-core path) take a lone certified
+# candidate's bound from its expanded value plus the error bound only when
+# statistics are off; with statistics on, the candidate's direct-form distance
+# is computed.  These runs check the stats-off results against the oracle and
+# against the stats-on run, bit for bit.
+STATS_OFF = CASES[14:17] + [c for c in LARGE_FORCED]
+
+
+@pytest.mark.parametrize("case", STATS_OFF, ids=lambda c: "s%d-n%d-d%d-k%d" % c[:4])
+def test_global_path_without_stats_matches_oracle(case):
+    seed, n, d, k, spread, sigma, iters, tol = case
+    print("case", case, flush=True)
+    X, C0 = synth.blobs(n, d, k, seed=seed, spread=spread, sigma=sigma)
+    ref = oracle.lloyd(X, C0, iters, tol)
+    Xg, Cg = _gpu(X), _gpu(C0)
+    a1, c1, s1 = km.run(Xg, Cg, iters, tol, large_path=True)
+    a2, c2, s2 = km.run(Xg, Cg, iters, tol, large_path=True, stats=True)
+    assert s1["iterations"] == ref["iters"] == s2["iterations"]
+    check_assign(a1.cpu().numpy(), ref["assign"], ref["best"], ref["second"], "stats off")
+    check_centroids(c1.cpu().numpy(), ref["C"], X, "stats off")
+    assert torch.equal(a1, a2) and torch.equal(c1, c2)
+    assert s1["clause1_skips"] == s2["clause1_skips"]
+
+
+@pytest.mark.parametrize("case", CASES[9:14], ids=lambda c: "s%d-n%d-d%d-k%d" % c[:4])
+def test_lds_matrix_core_path_stats_on_and_off_are_bitwise_identical(case):
+    seed, n, d, k, spread, sigma, iters, tol = case
+    X, C0 = synth.blobs(n, d, k, seed=seed, spread=spread, sigma=sigma)
+    Xg, Cg = _gpu(X), _gpu(C0)
+    a1, c1, s1 = km.run(Xg, Cg, iters, tol)
+    a2, c2, s2 = km.run(Xg, Cg, iters, tol, stats=True)
+    assert torch.equal(a1, a2) and torch.equal(c1, c2)
+    assert s1["iterations"] == s2["iterations"]
+
+
 @pytest.mark.parametrize("case", CASES[9:14], ids=lambda c: "s%d-n%d-d%d-k%d" % c[:4])
 def test_matrix_core_and_vector_paths_are_bitwise_identical(case):
     seed, n, d, k, spread, sigma, iters, tol = case
@@ -147,6 +182,40 @@ def test_determinism_bitwise():
     np.testing.assert_array_equal(outs[0][0], outs[1][0])
     np.testing.assert_array_equal(outs[0][1], outs[1][1])
     np.testing.assert_array_equal(outs[0][2], outs[1][2])
+
+
+# Prune counters against the float64 MTI reference (oracle.mti), which keeps
+# the same per-point bound and scans centroids in the same running-best order
+# as the LDS vector scan.  The assignments are identical; the counts differ
+# only where a Clause-1 or Clauses-2/3 test lies within the float32 margins
+# the GPU adds to stay exact (bounds rounded up, centroid half-distances
+# rounded down), and through the bounds those points then carry.  Slack per
+# step: 0.2 % of n points for Clause 1, 0.2 % of n * k for computed distances.
+COUNTER_CASES = [
+    # seed, n, d, k, spread, sigma, iters, flags
+    (91, 200000, 32, 100, 20.0, 1.5, 12, {"vector_only": True}),
+    (92, 150000, 16, 10, 6.0, 1.5, 12, {"generic": True}),
+    (93, 120000, 5, 30, 5.0, 1.0, 12, {}),
+]
+
+
+@pytest.mark.parametrize("case", COUNTER_CASES, ids=lambda c: "s%d-n%d-d%d-k%d" % c[:4])
+def test_prune_counters_match_the_mti_reference(case):
+    seed, n, d, k, spread, sigma, iters, flags = case
+    X, C0 = synth.blobs(n, d, k, seed=seed, spread=spread, sigma=sigma)
+    ref = oracle.mti(X, C0, iters)
+    with km.KMeansMTI(_gpu(X), _gpu(C0), **flags) as ctx:
+        assert ctx.path() == "lds-vector"
+        for _ in range(iters):
+            ctx.iterate()
+        h = ctx.history()
+    np.testing.assert_array_equal(h["changed"], ref["changed"])
+    d1 = np.abs(h["clause1"] - ref["clause1"])
+    dc = np.abs(h["computed"] - ref["computed"])
+    print("clause1 gpu", h["clause1"].tolist(), "ref", ref["clause1"].tolist(), flush=True)
+    print("computed gpu", h["computed"].tolist(), "ref", ref["computed"].tolist(), flush=True)
+    assert (d1 <= 2e-3 * n).all(), d1
+    assert (dc <= 2e-3 * n * k).all(), dc
 
 
 def test_k1_every_point_clause1_after_first_step():
