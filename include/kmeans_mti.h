@@ -254,6 +254,30 @@ int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double
                    uint32_t flags, void* hip_stream, km_pp_stats* stats);
 
 /*
+ * kmeans_pp_seed for callers that cannot allocate (code under HIP stream
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * workspace is a fixed device array of KMEANS_PP_STATIC_WORKSPACE_BYTES
+ * (64 MiB) that the library holds on every device it runs on until the
+ * process ends, instead of a caller's buffer.  The call makes no hipMalloc,
+ * hipFree, event or host allocation.
+ *
+ * Arguments, results and errors as kmeans_pp_seed (without workspace and
+ * stats), except: KM_ERR_INVALID_ARG when kmeans_pp_workspace_bytes(n, d, k)
+ * exceeds KMEANS_PP_STATIC_WORKSPACE_BYTES (about 12 bytes per row: n up to
+ * about 5.5 million for small k), and when flags hold anything but
+ * KM_PP_NO_PRUNE.  The first call on a device looks up the array's device
+ * address there (hipGetSymbolAddress, with that device current).
+ *
+ * All calls on one device share its array and leave their contents in it
+ * (each call overwrites what it reads).  Calls that overlap on one device --
+ * on different streams, or from host threads without ordering between them --
+ * race and give unspecified seeds; calls ordered on one stream are safe.
+ */
+#define KMEANS_PP_STATIC_WORKSPACE_BYTES ((size_t)64 << 20)
+int kmeans_pp_seed_noalloc(const float* X, int64_t n, int32_t d, int32_t k, const double* u, float* C_out,
+                           int64_t* idx_out, double* d2_out, uint32_t flags, void* hip_stream);
+
+/*
  * k-means++ with restarts (section IV-C: the best of several seeded runs).
  * For each run q = 0..r-1: seed k rows with kmeans_pp_seed from the uniforms
  * U[q*k .. q*k + k - 1], run k-means from those seeds as kmeans_mti_run does

@@ -38,8 +38,11 @@ EXPORTS = (
     "kmeans_mti_get_stats", "kmeans_mti_get_history", "kmeans_mti_get_timing", "kmeans_mti_run",
     "kmeans_mti_path", "kmeans_mti_destroy",
     "kmeans_mti_strerror", "kmeans_mti_last_hip_error",
-    "kmeans_pp_workspace_bytes", "kmeans_pp_seed", "kmeans_pp_run_best",
+    "kmeans_pp_workspace_bytes", "kmeans_pp_seed", "kmeans_pp_seed_noalloc", "kmeans_pp_run_best",
 )
+
+#: Size of the static workspace of kmeans_pp_seed_noalloc (KMEANS_PP_STATIC_WORKSPACE_BYTES).
+KMEANS_PP_STATIC_WORKSPACE_BYTES = 64 << 20
 
 
 class KmStats(C.Structure):
@@ -122,6 +125,8 @@ def load() -> C.CDLL:
     lib.kmeans_pp_workspace_bytes.restype = C.c_size_t
     lib.kmeans_pp_seed.argtypes = [P, i64, i32, i32, P, P, P, P, P, C.c_size_t, u32, P, C.POINTER(KmPPStats)]
     lib.kmeans_pp_seed.restype = C.c_int
+    lib.kmeans_pp_seed_noalloc.argtypes = [P, i64, i32, i32, P, P, P, P, u32, P]
+    lib.kmeans_pp_seed_noalloc.restype = C.c_int
     lib.kmeans_pp_run_best.argtypes = [P, i64, i32, i32, P, i32, i32, f64, P, P, P, u32, P, P,
                                        C.POINTER(KmStats)]
     lib.kmeans_pp_run_best.restype = C.c_int

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <climits>
+#include <mutex>
 #include <new>
 
 #include "kmeans_mti.h"
@@ -521,6 +522,35 @@ PPLayout pp_layout(int64_t n, int32_t k) {
     return L;
 }
 
+// Static workspace of kmeans_pp_seed_noalloc: one array per device, allocated
+// with the code object when the library loads on that device and held until
+// the process ends.  Host code never passes the array's name to a kernel or
+// a copy (on the host it is a stand-in, not a device address): the device
+// address is looked up once per device with hipGetSymbolAddress and kept.
+__device__ __align__(256) unsigned char pp_scratch[KMEANS_PP_STATIC_WORKSPACE_BYTES];
+
+constexpr int kMaxDevices = 256;
+void* g_pp_scratch_addr[kMaxDevices] = {};
+std::mutex g_pp_scratch_mu;
+
+int pp_static_workspace(void** out) {
+    int dev = 0;
+    KM_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return KM_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_pp_scratch_mu);
+    if (!g_pp_scratch_addr[dev]) {
+        void* p = nullptr;
+        KM_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(pp_scratch)));
+        if (!p || (reinterpret_cast<uintptr_t>(p) & 255)) {
+            snprintf(g_last_hip, sizeof g_last_hip, "static workspace: unexpected device address");
+            return KM_ERR_HIP;
+        }
+        g_pp_scratch_addr[dev] = p;
+    }
+    *out = g_pp_scratch_addr[dev];
+    return KM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -760,9 +790,11 @@ size_t kmeans_pp_workspace_bytes(int64_t n, int32_t d, int32_t k) {
     return pp_layout(n, k).total;
 }
 
-int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double* u, float* C_out,
-                   int64_t* idx_out, double* d2_out, void* workspace, size_t workspace_bytes, uint32_t flags,
-                   void* hip_stream, km_pp_stats* stats) {
+// kmeans_pp_seed on a given workspace; own_ws: the workspace is the
+// library's static array (its range is known, not looked up).
+static int pp_seed_impl(const float* X, int64_t n, int32_t d, int32_t k, const double* u, float* C_out,
+                        int64_t* idx_out, double* d2_out, void* workspace, size_t workspace_bytes, uint32_t flags,
+                        void* hip_stream, km_pp_stats* stats, bool own_ws) {
     if (!X || !u || !C_out || !workspace || n < 1 || d < 1 || k < 1 || k > n || n > INT64_MAX / 16 / d)
         return KM_ERR_INVALID_ARG;
     if (flags & ~(uint32_t)(KM_PP_NO_PRUNE | KM_PP_TIMING)) return KM_ERR_INVALID_ARG;
@@ -781,7 +813,7 @@ int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double
     KM_HIP(hipGetDevice(&dev));
     if ((rc = check_device_range(X, (size_t)n * d * 4, dev, "X")) != KM_OK) return rc;
     if ((rc = check_device_range(C_out, (size_t)k * d * 4, dev, "C_out")) != KM_OK) return rc;
-    if ((rc = check_device_range(workspace, L.total, dev, "workspace")) != KM_OK) return rc;
+    if (!own_ws && (rc = check_device_range(workspace, L.total, dev, "workspace")) != KM_OK) return rc;
     if (idx_out && (rc = check_device_range(idx_out, (size_t)k * 8, dev, "idx_out")) != KM_OK) return rc;
     if (d2_out && (rc = check_device_range(d2_out, (size_t)n * 8, dev, "d2_out")) != KM_OK) return rc;
     hipStream_t st = static_cast<hipStream_t>(hip_stream);
@@ -857,6 +889,35 @@ int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double
     if (e != hipSuccess) return hip_fail(e, "kmeans_pp_seed");
     *stats = out;
     return KM_OK;
+}
+
+int kmeans_pp_seed(const float* X, int64_t n, int32_t d, int32_t k, const double* u, float* C_out,
+                   int64_t* idx_out, double* d2_out, void* workspace, size_t workspace_bytes, uint32_t flags,
+                   void* hip_stream, km_pp_stats* stats) {
+    return pp_seed_impl(X, n, d, k, u, C_out, idx_out, d2_out, workspace, workspace_bytes, flags, hip_stream,
+                        stats, false);
+}
+
+int kmeans_pp_seed_noalloc(const float* X, int64_t n, int32_t d, int32_t k, const double* u, float* C_out,
+                           int64_t* idx_out, double* d2_out, uint32_t flags, void* hip_stream) {
+    if (!X || !u || !C_out || n < 1 || d < 1 || k < 1 || k > n) return KM_ERR_INVALID_ARG;
+    if (flags & ~(uint32_t)KM_PP_NO_PRUNE) {   // KM_PP_TIMING would create events
+        snprintf(g_last_hip, sizeof g_last_hip, "kmeans_pp_seed_noalloc: only KM_PP_NO_PRUNE is accepted");
+        return KM_ERR_INVALID_ARG;
+    }
+    const size_t need = kmeans_pp_workspace_bytes(n, d, k);
+    if (need == 0) return KM_ERR_INVALID_ARG;
+    if (need > KMEANS_PP_STATIC_WORKSPACE_BYTES) {
+        snprintf(g_last_hip, sizeof g_last_hip,
+                 "kmeans_pp_seed_noalloc: n = %lld, k = %d need %zu workspace bytes, more than the %zu of the "
+                 "static workspace", (long long)n, (int)k, need, (size_t)KMEANS_PP_STATIC_WORKSPACE_BYTES);
+        return KM_ERR_INVALID_ARG;
+    }
+    void* ws = nullptr;
+    const int rc = pp_static_workspace(&ws);
+    if (rc != KM_OK) return rc;
+    return pp_seed_impl(X, n, d, k, u, C_out, idx_out, d2_out, ws, KMEANS_PP_STATIC_WORKSPACE_BYTES, flags,
+                        hip_stream, nullptr, true);
 }
 
 int kmeans_pp_run_best(const float* X, int64_t n, int32_t d, int32_t k, const double* U, int32_t r,

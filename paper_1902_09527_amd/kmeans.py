@@ -251,6 +251,31 @@ def kmeanspp(X: torch.Tensor, k: int, u, prune: bool = True, count: bool = False
     return out
 
 
+def kmeanspp_noalloc(X: torch.Tensor, k: int, u, prune: bool = True,
+                     stream: Optional[torch.cuda.Stream] = None) -> Dict[str, object]:
+    """k-means++ seeding with the library's static device workspace
+    (kmeans_pp_seed_noalloc): the library allocates nothing.  Returns ``C``,
+    ``idx`` and ``D2`` as :func:`kmeanspp` (those outputs are allocated here,
+    by the caller's side)."""
+    _check_matrix(X, "X")
+    lib = N.load()
+    n, d = X.shape
+    k = int(k)
+    uu = np.ascontiguousarray(np.asarray(u, dtype=np.float64).reshape(-1))
+    if uu.shape != (k,):
+        raise ValueError("u must hold k = %d uniforms" % k)
+    c = torch.empty(k, d, dtype=torch.float32, device=X.device)
+    idx = torch.empty(k, dtype=torch.int64, device=X.device)
+    d2 = torch.empty(n, dtype=torch.float64, device=X.device)
+    with torch.cuda.device(X.device):
+        st = lib.kmeans_pp_seed_noalloc(C.c_void_p(X.data_ptr()), n, d, k, uu.ctypes.data_as(C.c_void_p),
+                                        C.c_void_p(c.data_ptr()), C.c_void_p(idx.data_ptr()),
+                                        C.c_void_p(d2.data_ptr()), 0 if prune else N.KM_PP_NO_PRUNE,
+                                        _stream_ptr(X.device, stream))
+    N.check(st, "kmeans_pp_seed_noalloc")
+    return {"C": c, "idx": idx, "D2": d2}
+
+
 def kmeanspp_workspace_bytes(n: int, d: int, k: int) -> int:
     """Bytes of workspace kmeans_pp_seed needs (plus up to 255 for alignment)."""
     return int(N.load().kmeans_pp_workspace_bytes(int(n), int(d), int(k)))
