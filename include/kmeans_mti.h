@@ -301,8 +301,17 @@ int kmeans_pp_run_best(const float* X, int64_t n, int32_t d, int32_t k, const do
                        void* hip_stream, uint32_t flags, int32_t* best_out, double* inertia_out,
                        km_stats* stats);
 
-/* Release a context and its device scratch.  NULL-safe.  Synchronizes. */
+/*
+ * Release a context.  NULL-safe.  Synchronizes.  Its device buffers are kept
+ * by the library (per device and size, at most 8 GiB in all) for the next
+ * context that needs the same sizes, so that repeated runs of a problem make
+ * no hipMalloc / hipFree calls; kmeans_mti_release_cache frees them.
+ */
 void kmeans_mti_destroy(km_ctx* ctx);
+
+/* Free the device buffers kept from released contexts (all devices).  Call
+ * it with no context in use on another host thread. */
+void kmeans_mti_release_cache(void);
 
 /* Static text for a KM_* status code. */
 const char* kmeans_mti_strerror(int status);

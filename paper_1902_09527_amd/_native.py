@@ -36,7 +36,7 @@ KM_PP_TIMING = 2
 EXPORTS = (
     "kmeans_mti_init", "kmeans_mti_iterate", "kmeans_mti_get", "kmeans_mti_get_centroids64",
     "kmeans_mti_get_stats", "kmeans_mti_get_history", "kmeans_mti_get_timing", "kmeans_mti_run",
-    "kmeans_mti_path", "kmeans_mti_destroy",
+    "kmeans_mti_path", "kmeans_mti_destroy", "kmeans_mti_release_cache",
     "kmeans_mti_strerror", "kmeans_mti_last_hip_error",
     "kmeans_pp_workspace_bytes", "kmeans_pp_seed", "kmeans_pp_seed_noalloc", "kmeans_pp_run_best",
 )
@@ -119,6 +119,8 @@ def load() -> C.CDLL:
     lib.kmeans_mti_path.restype = C.c_char_p
     lib.kmeans_mti_destroy.argtypes = [P]
     lib.kmeans_mti_destroy.restype = None
+    lib.kmeans_mti_release_cache.argtypes = []
+    lib.kmeans_mti_release_cache.restype = None
     lib.kmeans_mti_strerror.argtypes = [C.c_int]
     lib.kmeans_mti_strerror.restype = C.c_char_p
     lib.kmeans_pp_workspace_bytes.argtypes = [i64, i32, i32]

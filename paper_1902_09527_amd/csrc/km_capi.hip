@@ -69,6 +69,77 @@ int check_device_range(const void* p, size_t bytes, int device, const char* what
     return KM_OK;
 }
 
+// Device buffers of released contexts, kept per device and size for the
+// next context that needs the same size: repeated runs of a problem then
+// make no hipMalloc / hipFree calls (hipFree also waits for the device).
+// A context returns its buffers only after its stream has drained, so a
+// buffer handed out again has no work pending.  At most kCacheMax bytes are
+// kept; kmeans_mti_release_cache frees them.
+struct CachedBuf {
+    int dev;
+    size_t bytes;
+    void* p;
+};
+constexpr size_t kCacheMax = (size_t)8 << 30;
+constexpr int kCacheSlots = 256;
+std::mutex g_cache_mu;
+CachedBuf g_cache[kCacheSlots];
+int g_cache_n = 0;
+size_t g_cache_bytes = 0;
+
+void* cache_take(int dev, size_t bytes) {
+    std::lock_guard<std::mutex> lock(g_cache_mu);
+    for (int i = g_cache_n - 1; i >= 0; --i)
+        if (g_cache[i].dev == dev && g_cache[i].bytes == bytes) {
+            void* p = g_cache[i].p;
+            g_cache[i] = g_cache[--g_cache_n];
+            g_cache_bytes -= bytes;
+            return p;
+        }
+    return nullptr;
+}
+
+// Keeps p for reuse, or frees it when the cache is full.
+void cache_give(int dev, size_t bytes, void* p) {
+    {
+        std::lock_guard<std::mutex> lock(g_cache_mu);
+        if (g_cache_n < kCacheSlots && g_cache_bytes + bytes <= kCacheMax) {
+            g_cache[g_cache_n++] = CachedBuf{dev, bytes, p};
+            g_cache_bytes += bytes;
+            return;
+        }
+    }
+    (void)hipFree(p);
+}
+
+// Pinned host words for polling a run's stop flag, reused across runs
+// (hipHostMalloc and hipHostFree cost tens of microseconds each).
+std::mutex g_pin_mu;
+int32_t* g_pin_free[64];
+int g_pin_n = 0;
+
+int32_t* pinned_take() {
+    {
+        std::lock_guard<std::mutex> lock(g_pin_mu);
+        if (g_pin_n > 0) return g_pin_free[--g_pin_n];
+    }
+    void* p = nullptr;
+    if (hipHostMalloc(&p, 64, hipHostMallocDefault) != hipSuccess) return nullptr;
+    return static_cast<int32_t*>(p);
+}
+
+void pinned_give(int32_t* p) {
+    if (!p) return;
+    {
+        std::lock_guard<std::mutex> lock(g_pin_mu);
+        if (g_pin_n < 64) {
+            g_pin_free[g_pin_n++] = p;
+            return;
+        }
+    }
+    (void)hipHostFree(p);
+}
+
 }  // namespace
 
 struct km_ctx {
@@ -90,6 +161,7 @@ struct km_ctx {
     km::Dev dv{};
     static constexpr int kMaxBufs = 32;
     void* bufs[kMaxBufs] = {};
+    size_t buf_bytes[kMaxBufs] = {};
     int nbufs = 0;
     bool broken = false;
     bool stepped = false;
@@ -138,14 +210,24 @@ struct km_ctx {
             snprintf(g_last_hip, sizeof g_last_hip, "internal: more than %d device buffers", kMaxBufs);
             return KM_ERR_STATE;
         }
-        hipError_t e = hipMalloc(q, bytes);
-        if (e != hipSuccess) return hip_fail(e, "hipMalloc");
+        *q = cache_take(device, bytes);
+        if (!*q) {
+            hipError_t e = hipMalloc(q, bytes);
+            if (e != hipSuccess) return hip_fail(e, "hipMalloc");
+        }
+        buf_bytes[nbufs] = bytes;
         bufs[nbufs++] = *q;
         return KM_OK;
     }
     ~km_ctx() {
-        (void)hipStreamSynchronize(stream);
-        for (int i = 0; i < nbufs; ++i) (void)hipFree(bufs[i]);
+        // Buffers go back to the cache only once no work on them is pending.
+        if (hipStreamSynchronize(stream) == hipSuccess && !broken) {
+            for (int i = 0; i < nbufs; ++i) cache_give(device, buf_bytes[i], bufs[i]);
+        } else {
+            (void)hipGetLastError();
+            (void)hipDeviceSynchronize();
+            for (int i = 0; i < nbufs; ++i) (void)hipFree(bufs[i]);
+        }
         for (auto& row : ev)
             for (auto& e : row)
                 if (e) (void)hipEventDestroy(e);
@@ -250,8 +332,12 @@ int read_state(km_ctx* c, km::IterState* out) {
     return KM_OK;
 }
 
-int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const float* C0) {
+// Set-up of a context.  max_iters / tol_n: the stop rule written into the
+// loop state; sync: wait for the set-up work before returning.
+int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const float* C0, int32_t max_iters,
+              double tol_n, bool sync) {
     KM_HIP(hipGetDevice(&c->device));
+    km::ZeroRanges zr{};   // buffers cleared by the set-up launch
     int rc0;
     if ((rc0 = check_device_range(X, (size_t)n * (size_t)d * sizeof(float), c->device, "X")) != KM_OK)
         return rc0;
@@ -380,7 +466,7 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             (rc2 = c->alloc(&L.perm, (size_t)n)) || (rc2 = c->alloc(&L.cpart, (size_t)L.NCmax * d)) ||
             (rc2 = c->alloc(&L.ciq, (size_t)L.NCmax)))
             return rc2;
-        KM_HIP(hipMemsetAsync(L.nsurv, 0, 4 * sizeof(uint32_t), c->stream));
+        zr.add(L.nsurv, 4 * sizeof(uint32_t));
     }
 
     int rc;
@@ -391,10 +477,10 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         if ((rc = c->alloc(&v.lb, (size_t)n * (size_t)k)) || (rc = c->alloc(&v.dhi, (size_t)k)) ||
             (rc = c->alloc(&v.dlo, (size_t)k)) || (rc = c->alloc(&v.dupf, (size_t)k)))
             return rc;
-        KM_HIP(hipMemsetAsync(v.dupf, 0, sizeof(float) * (size_t)k, c->stream));
-        KM_HIP(hipMemsetAsync(v.lb, 0, sizeof(float) * (size_t)n * (size_t)k, c->stream));
-        KM_HIP(hipMemsetAsync(v.dhi, 0, sizeof(double) * (size_t)k, c->stream));
-        KM_HIP(hipMemsetAsync(v.dlo, 0, sizeof(double) * (size_t)k, c->stream));
+        zr.add(v.dupf, sizeof(float) * (size_t)k);
+        zr.add(v.lb, sizeof(float) * (size_t)n * (size_t)k);
+        zr.add(v.dhi, sizeof(double) * (size_t)k);
+        zr.add(v.dlo, sizeof(double) * (size_t)k);
     }
     // The streaming path keeps C^t in two slots (t % 2); slot 0 holds C0.
     if ((rc = c->alloc(&v.C64, (size_t)k * d * (c->small ? 2 : 1))) || (rc = c->alloc(&v.C32, (size_t)k * d)) ||
@@ -414,31 +500,40 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             (rc = c->alloc(&c->fz.dhi, (size_t)2 * k)) || (rc = c->alloc(&c->fz.dlo, (size_t)2 * k)) ||
             (rc = c->alloc(&c->fz.dup, (size_t)k)) || (rc = c->alloc(&c->fz.ddn, (size_t)k)))
             return rc;
-        KM_HIP(hipMemsetAsync(c->fz.rows, 0, sizeof(uint64_t) * nrows, c->stream));
-        KM_HIP(hipMemsetAsync(c->fz.stat, 0, sizeof(uint64_t) * 3 * km::kNumStat, c->stream));
-        KM_HIP(hipMemsetAsync(c->fz.sum, 0, sizeof(uint64_t) * 2 * (size_t)(k * d + k), c->stream));
-        KM_HIP(hipMemsetAsync(c->fz.w, 0, sizeof(uint32_t) * nw, c->stream));
-        KM_HIP(hipMemsetAsync(c->fz.dhi, 0, sizeof(double) * 2 * (size_t)k, c->stream));
-        KM_HIP(hipMemsetAsync(c->fz.dlo, 0, sizeof(double) * 2 * (size_t)k, c->stream));
-        KM_HIP(hipMemsetAsync(c->fz.dup, 0, sizeof(float) * (size_t)k, c->stream));
-        KM_HIP(hipMemsetAsync(c->fz.ddn, 0, sizeof(float) * (size_t)k, c->stream));
+        zr.add(c->fz.rows, sizeof(uint64_t) * nrows);
+        zr.add(c->fz.stat, sizeof(uint64_t) * 3 * km::kNumStat);
+        zr.add(c->fz.sum, sizeof(uint64_t) * 2 * (size_t)(k * d + k));
+        zr.add(c->fz.w, sizeof(uint32_t) * nw);
+        zr.add(c->fz.dhi, sizeof(double) * 2 * (size_t)k);
+        zr.add(c->fz.dlo, sizeof(double) * 2 * (size_t)k);
+        zr.add(c->fz.dup, sizeof(float) * (size_t)k);
+        zr.add(c->fz.ddn, sizeof(float) * (size_t)k);
     }
     uint32_t* scratch = nullptr;
-    if ((rc = c->alloc(&scratch, 5))) return rc;
+    if ((rc = c->alloc(&scratch, 8))) return rc;
+    zr.add(scratch, 8 * sizeof(uint32_t));
+    zr.add(v.total, sizeof(uint64_t) * (size_t)v.L);
+    zr.add(v.rec, sizeof(km::IterRec) * km::kHistCap);
+    zr.st = v.st;
+    zr.max_iters = max_iters;
+    zr.tol_n = tol_n;
+    KM_HIP(km::launch_init_buffers(zr, cus, c->stream));
 
     // Largest magnitude of X and C0 (and non-finite detection) -> fixed-point
     // scales; with spherical k-means also the unit centroids and whether C0
     // has a zero row.
-    KM_HIP(hipMemsetAsync(scratch, 0, 5 * sizeof(uint32_t), c->stream));
-    KM_HIP(km::launch_absmax(X, n * d, scratch, reinterpret_cast<int32_t*>(scratch + 1), c->stream));
-    KM_HIP(km::launch_absmax(C0, (int64_t)k * d, scratch + 2, reinterpret_cast<int32_t*>(scratch + 3),
-                             c->stream));
+    KM_HIP(km::launch_absmax(X, n * d, C0, (int64_t)k * d, cus, scratch, c->stream));
     if (c->flags & KM_FLAG_SPHERICAL)
         KM_HIP(km::launch_set_centroids_unit(C0, v.C64, v.C32, v.ec, k, d, reinterpret_cast<int32_t*>(scratch + 4),
                                              c->stream));
     uint32_t host[5];
-    KM_HIP(hipMemcpyAsync(host, scratch, sizeof host, hipMemcpyDeviceToHost, c->stream));
-    KM_HIP(hipStreamSynchronize(c->stream));
+    int32_t* pin = pinned_take();
+    if (!pin) return KM_ERR_OOM;
+    hipError_t ec5 = hipMemcpyAsync(pin, scratch, sizeof host, hipMemcpyDeviceToHost, c->stream);
+    if (ec5 == hipSuccess) ec5 = hipStreamSynchronize(c->stream);
+    if (ec5 == hipSuccess) memcpy(host, pin, sizeof host);
+    pinned_give(pin);
+    if (ec5 != hipSuccess) return hip_fail(ec5, "set-up read-back");
     if ((c->flags & KM_FLAG_VALIDATE) && (host[1] || host[3])) return KM_ERR_NONFINITE;
     if (host[4]) {
         snprintf(g_last_hip, sizeof g_last_hip, "spherical k-means: C0 has a zero row");
@@ -476,12 +571,6 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             for (auto& e : row) KM_HIP(hipEventCreate(&e));
     }
 
-    km::IterState st0{};
-    st0.max_iters = INT_MAX;
-    st0.tol_n = -1.0;
-    KM_HIP(hipMemcpyAsync(v.st, &st0, sizeof st0, hipMemcpyHostToDevice, c->stream));
-    KM_HIP(hipMemsetAsync(v.total, 0, sizeof(uint64_t) * (size_t)v.L, c->stream));
-    KM_HIP(hipMemsetAsync(v.rec, 0, sizeof(km::IterRec) * km::kHistCap, c->stream));
     if (!(c->flags & KM_FLAG_SPHERICAL))
         KM_HIP(km::launch_set_centroids(C0, v.C64, v.C32, v.ec, (int64_t)k * d, k, c->stream));
     if (c->large) {
@@ -489,7 +578,7 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     } else {
         KM_HIP(km::launch_centroid_table(v, 1, c->stream));
     }
-    KM_HIP(hipStreamSynchronize(c->stream));
+    if (sync) KM_HIP(hipStreamSynchronize(c->stream));
     return KM_OK;
 }
 
@@ -555,8 +644,9 @@ int pp_static_workspace(void** out) {
 
 extern "C" {
 
-int kmeans_mti_init(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t k, const float* C0,
-                    void* hip_stream, uint32_t flags) {
+// A new context; max_iters / tol_n: its stop rule; sync: wait for the set-up.
+static int create_ctx(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t k, const float* C0,
+                      void* hip_stream, uint32_t flags, int32_t max_iters, double tol_n, bool sync) {
     if (!out) return KM_ERR_INVALID_ARG;
     *out = nullptr;
     int rc = check_shape(X, n, d, k, C0);
@@ -572,13 +662,18 @@ int kmeans_mti_init(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t 
     c->k = k;
     c->flags = flags;
     c->stream = static_cast<hipStream_t>(hip_stream);
-    rc = init_impl(c, X, n, d, k, C0);
+    rc = init_impl(c, X, n, d, k, C0, max_iters, tol_n, sync);
     if (rc != KM_OK) {
         delete c;
         return rc;
     }
     *out = c;
     return KM_OK;
+}
+
+int kmeans_mti_init(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t k, const float* C0,
+                    void* hip_stream, uint32_t flags) {
+    return create_ctx(out, X, n, d, k, C0, hip_stream, flags, INT_MAX, -1.0, true);
 }
 
 int kmeans_mti_iterate(km_ctx* ctx, int64_t* changed_out) {
@@ -707,7 +802,8 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
     if ((rc = check_device_range(assign_out, (size_t)n * 4, dev, "assign_out")) != KM_OK) return rc;
     if ((rc = check_device_range(C_out, (size_t)k * d * 4, dev, "C_out")) != KM_OK) return rc;
     km_ctx* c = nullptr;
-    if ((rc = kmeans_mti_init(&c, X, n, d, k, C0, hip_stream, flags)) != KM_OK) return rc;
+    if ((rc = create_ctx(&c, X, n, d, k, C0, hip_stream, flags, max_iters, tol * (double)n, false)) != KM_OK)
+        return rc;
 
     hipEvent_t ev0 = nullptr, ev1 = nullptr, evc[2] = {nullptr, nullptr};
     int32_t* pinned = nullptr;
@@ -717,7 +813,7 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
         if (ev1) (void)hipEventDestroy(ev1);
         for (auto& e : evc)
             if (e) (void)hipEventDestroy(e);
-        if (pinned) (void)hipHostFree(pinned);
+        pinned_give(pinned);
         kmeans_mti_destroy(c);
     };
 #define RUN_HIP(call)                                   \
@@ -730,15 +826,15 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
         }                                               \
     } while (0)
 
-    km::IterState st0{};
-    st0.max_iters = max_iters;
-    st0.tol_n = tol * (double)n;
-    RUN_HIP(hipMemcpyAsync(c->dv.st, &st0, sizeof st0, hipMemcpyHostToDevice, c->stream));
     RUN_HIP(hipEventCreate(&ev0));
     RUN_HIP(hipEventCreate(&ev1));
     RUN_HIP(hipEventCreateWithFlags(&evc[0], hipEventDisableTiming));
     RUN_HIP(hipEventCreateWithFlags(&evc[1], hipEventDisableTiming));
-    RUN_HIP(hipHostMalloc(reinterpret_cast<void**>(&pinned), 2 * sizeof(int32_t), hipHostMallocDefault));
+    pinned = pinned_take();
+    if (!pinned) {
+        cleanup();
+        return KM_ERR_OOM;
+    }
     pinned[0] = pinned[1] = 0;
 
     // Enqueue chunks of iterations; the device stop flag makes surplus
@@ -993,6 +1089,18 @@ const char* kmeans_mti_path(const km_ctx* ctx) {
 }
 
 void kmeans_mti_destroy(km_ctx* ctx) { delete ctx; }
+
+void kmeans_mti_release_cache(void) {
+    CachedBuf held[kCacheSlots];
+    int m = 0;
+    {
+        std::lock_guard<std::mutex> lock(g_cache_mu);
+        for (int i = 0; i < g_cache_n; ++i) held[m++] = g_cache[i];
+        g_cache_n = 0;
+        g_cache_bytes = 0;
+    }
+    for (int i = 0; i < m; ++i) (void)hipFree(held[i].p);
+}
 
 const char* kmeans_mti_strerror(int status) {
     switch (status) {

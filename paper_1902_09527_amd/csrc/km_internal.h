@@ -296,8 +296,33 @@ const void* large_mfma_symbol(int d);   // the matrix-core kernel for row length
 hipError_t large_set_attributes(int k, int d);
 
 // Kernel launchers (km_kernels.hip).  Each returns the launch status.
-hipError_t launch_absmax(const float* X, int64_t count, uint32_t* absmax_bits, int32_t* nonfinite,
+// Largest |value| of a (na floats) and of b (nb floats) in one launch:
+// out[0], out[2] receive their float bits (atomic max) and out[1], out[3]
+// become nonzero for a non-finite value; out[0..3] must be zero before.
+hipError_t launch_absmax(const float* a, int64_t na, const float* b, int64_t nb, int cus, uint32_t* out,
                          hipStream_t s);
+
+// Buffers cleared and the loop state written by one set-up launch.
+struct ZeroRanges {
+    static constexpr int kMax = 16;
+    void* p[kMax];        // 16-byte aligned
+    uint64_t bytes[kMax]; // multiples of 4
+    int32_t n;
+    int32_t max_iters;    // loop state written to *st (when st is not null)
+    double tol_n;
+    IterState* st;
+    bool overflow;        // more than kMax ranges were added (the launch refuses)
+    void add(void* q, uint64_t b) {
+        if (n >= kMax) {
+            overflow = true;
+            return;
+        }
+        p[n] = q;
+        bytes[n] = b;
+        ++n;
+    }
+};
+hipError_t launch_init_buffers(const ZeroRanges& z, int cus, hipStream_t s);
 hipError_t launch_set_centroids(const float* C0, double* C64, float* C32, float* ec, int64_t kd,
                                 int32_t k, hipStream_t s);
 // Spherical k-means: rows of X projected to the unit sphere into Xn; unit

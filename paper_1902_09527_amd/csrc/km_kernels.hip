@@ -96,16 +96,52 @@ __device__ inline double sqd64(const float* x, const double* c, int d) {
 // ---------------------------------------------------------------------------
 // Init helpers
 
-__global__ void k_absmax(const float* __restrict__ X, int64_t count, uint32_t* absmax_bits,
-                         int32_t* nonfinite) {
-    uint32_t m = 0;
-    int bad = 0;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) {
-        const uint32_t b = __float_as_uint(X[i]) & 0x7fffffffu;
-        if (b >= 0x7f800000u) bad = 1;
-        else m = b > m ? b : m;
+// Largest |value| (as float bits: non-negative floats order as their bits)
+// and whether any value is not finite, over one array: 16-byte loads when it
+// is 16-byte aligned, four in flight per lane, then the scalar tail.
+__device__ __forceinline__ void absmax_range(const float* __restrict__ p, int64_t count, int64_t t0,
+                                             int64_t stride, uint32_t& m, uint32_t& bad) {
+    auto take = [&](float v) __attribute__((always_inline)) {
+        const uint32_t u = __float_as_uint(v) & 0x7fffffffu;
+        bad |= u >= 0x7f800000u ? 1u : 0u;
+        m = (u < 0x7f800000u && u > m) ? u : m;
+    };
+    const int64_t nq = (reinterpret_cast<uintptr_t>(p) & 15) == 0 ? count / 4 : 0;
+    const f32x4* __restrict__ q = reinterpret_cast<const f32x4*>(p);
+    int64_t i = t0;
+    for (; i + 3 * stride < nq; i += 4 * stride) {
+        f32x4 v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = __builtin_nontemporal_load(q + i + r * stride);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            take(v[r].x);
+            take(v[r].y);
+            take(v[r].z);
+            take(v[r].w);
+        }
     }
+    for (; i < nq; i += stride) {
+        const f32x4 v = __builtin_nontemporal_load(q + i);
+        take(v.x);
+        take(v.y);
+        take(v.z);
+        take(v.w);
+    }
+    for (int64_t j = 4 * nq + t0; j < count; j += stride) take(p[j]);
+}
+
+// Two arrays in one launch: blocks [0, blocks_a) scan a, the others b.
+// out[0] / out[2]: max bits of a / b; out[1] / out[3]: nonzero if a / b
+// holds a non-finite value (all zero before the launch).
+__global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ a, int64_t na, const float* __restrict__ b,
+                                               int64_t nb, int blocks_a, uint32_t* out) {
+    const bool first = (int)blockIdx.x < blocks_a;
+    const int blk = first ? (int)blockIdx.x : (int)blockIdx.x - blocks_a;
+    const int nblk = first ? blocks_a : (int)gridDim.x - blocks_a;
+    uint32_t m = 0, bad = 0;
+    absmax_range(first ? a : b, first ? na : nb, (int64_t)blk * blockDim.x + threadIdx.x,
+                 (int64_t)nblk * blockDim.x, m, bad);
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
         const uint32_t o = __shfl_xor(m, off);
@@ -113,8 +149,31 @@ __global__ void k_absmax(const float* __restrict__ X, int64_t count, uint32_t* a
     }
     const bool any_bad = __any(bad);
     if ((threadIdx.x & 63) == 0) {
-        atomicMax(absmax_bits, m);
-        if (any_bad) atomicOr(nonfinite, 1);
+        atomicMax(out + (first ? 0 : 2), m);
+        if (any_bad) atomicOr(out + (first ? 1 : 3), 1u);
+    }
+}
+
+// Set-up of a context's device state in one launch: the listed ranges are
+// cleared (16-byte stores, then the 4-byte tail; every range starts 16-byte
+// aligned and is a whole number of 4-byte words) and the loop state is
+// written.
+__global__ __launch_bounds__(256) void k_init_buffers(ZeroRanges z) {
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int r = 0; r < z.n; ++r) {
+        uint4* q = reinterpret_cast<uint4*>(z.p[r]);
+        const int64_t n16 = (int64_t)(z.bytes[r] / 16);
+        for (int64_t i = t0; i < n16; i += stride) q[i] = make_uint4(0u, 0u, 0u, 0u);
+        uint32_t* w = reinterpret_cast<uint32_t*>(z.p[r]);
+        const int64_t nw = (int64_t)(z.bytes[r] / 4);
+        for (int64_t i = 4 * n16 + t0; i < nw; i += stride) w[i] = 0u;
+    }
+    if (t0 == 0 && z.st) {
+        IterState st{};
+        st.max_iters = z.max_iters;
+        st.tol_n = z.tol_n;
+        *z.st = st;
     }
 }
 
@@ -1211,13 +1270,29 @@ const void* assign_kernel_symbol(int variant) {
     }
 }
 
-hipError_t launch_absmax(const float* X, int64_t count, uint32_t* absmax_bits, int32_t* nonfinite,
+hipError_t launch_absmax(const float* a, int64_t na, const float* b, int64_t nb, int cus, uint32_t* out,
                          hipStream_t s) {
-    int64_t blocks = (count + 255) / 256;
-    if (blocks > 4096) blocks = 4096;
-    if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL(k_absmax, dim3((unsigned)blocks), dim3(256), 0, s, X, count, absmax_bits,
-                       nonfinite);
+    // a (X): up to 8 blocks per CU, each lane with 16 values per round; b (C0): a few blocks.
+    int64_t ba = (na + 4 * 4 * 256 - 1) / (4 * 4 * 256);
+    if (ba > 8 * (int64_t)cus) ba = 8 * (int64_t)cus;
+    if (ba < 1) ba = 1;
+    int64_t bb = (nb + 4 * 4 * 256 - 1) / (4 * 4 * 256);
+    if (bb > 64) bb = 64;
+    if (bb < 1) bb = 1;
+    hipLaunchKernelGGL(k_absmax, dim3((unsigned)(ba + bb)), dim3(256), 0, s, a, na, b, nb, (int)ba, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_init_buffers(const ZeroRanges& z, int cus, hipStream_t s) {
+    if (z.overflow || z.n < 0 || z.n > ZeroRanges::kMax) return hipErrorInvalidValue;
+    uint64_t total = 0;
+    for (int r = 0; r < z.n; ++r) {
+        if ((reinterpret_cast<uintptr_t>(z.p[r]) & 15) || (z.bytes[r] & 3)) return hipErrorInvalidValue;
+        total += z.bytes[r];
+    }
+    int64_t blocks = (int64_t)(total / (16 * 256 * 4)) + 1;
+    if (blocks > 8 * (int64_t)cus) blocks = 8 * (int64_t)cus;
+    hipLaunchKernelGGL(k_init_buffers, dim3((unsigned)blocks), dim3(256), 0, s, z);
     return hipGetLastError();
 }
 

@@ -276,6 +276,12 @@ def kmeanspp_noalloc(X: torch.Tensor, k: int, u, prune: bool = True,
     return {"C": c, "idx": idx, "D2": d2}
 
 
+def release_cache() -> None:
+    """Free the device buffers the library keeps from released contexts
+    (kmeans_mti_release_cache)."""
+    N.load().kmeans_mti_release_cache()
+
+
 def kmeanspp_workspace_bytes(n: int, d: int, k: int) -> int:
     """Bytes of workspace kmeans_pp_seed needs (plus up to 255 for alignment)."""
     return int(N.load().kmeans_pp_workspace_bytes(int(n), int(d), int(k)))
