@@ -225,8 +225,8 @@ __host__ __device__ inline int slot3(int t) { return ((t % 3) + 3) % 3; }
 __host__ __device__ inline int slot2(int t) { return t & 1; }
 
 struct SmallLds {
-    int off_c, off_h, off_s, off_ec, off_du, off_dd, off_acc, off_cnt, off_qr, off_qp, off_qa, off_misc, off_c64,
-        bytes;
+    int off_c, off_h, off_s, off_ec, off_du, off_dd, off_cn, off_acc, off_cnt, off_qr, off_qp, off_qa, off_misc,
+        off_c64, bytes;
     int csu, kp;          // stride (uint64) of one copy of the sums; of one copy of the counts
 };
 
@@ -250,6 +250,7 @@ __host__ __device__ inline SmallLds small_lds(int k, bool staged) {
     L.off_ec = take(4 * k, 16);
     L.off_du = take(4 * k, 16);
     L.off_dd = take(4 * k, 16);
+    L.off_cn = take(4 * k, 16);
     L.off_acc = take(8 * kSmallCopies * L.csu, 16);
     L.off_cnt = take(4 * kSmallCopies * L.kp, 16);
     // Queued rows (streaming kernel) or one gathered batch (incremental kernel).

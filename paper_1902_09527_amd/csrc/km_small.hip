@@ -62,6 +62,9 @@ constexpr int kCopies = kSmallCopies;
 constexpr int kD = 16;                // dimension of this path
 constexpr int kQD = kD / 4;           // 16-byte chunks per row
 constexpr int kCR = kSmallRowStride;  // padded LDS row stride (floats)
+// Error factor of a float32 squared distance in the expanded form, relative
+// to (|x| + |c|)^2.
+constexpr float kExpGamma = (float)(kD + 8) * 0x1p-24f;
 
 // Point state word: v rounded up to a multiple of 16 units in the last place
 // (for v >= 0 the bit pattern grows, for v < 0 the magnitude shrinks), with
@@ -175,6 +178,7 @@ struct Tables {
     float* thr;    // k: Clause-1 threshold on a state value (below)
     float* ec;     // k: float32 rounding error of each centroid, rounded up
     float* ddn;    // k: cumulative drift, rounded down
+    float* cn;     // k: squared norms of the float32 centroids (float32 of the float64 sum)
     uint64_t* acc; // kCopies copies (stride csu) of the k x 16 fixed-point sums
     uint32_t* cnt; // kCopies copies of the k counts (stride kp)
     int* qc;       // three queue counters
@@ -190,6 +194,7 @@ __device__ __forceinline__ Tables table_ptrs(const Dev& P, const SmallLds& lay) 
     T.thr = reinterpret_cast<float*>(km_smem + lay.off_s);
     T.ec = reinterpret_cast<float*>(km_smem + lay.off_ec);
     T.ddn = reinterpret_cast<float*>(km_smem + lay.off_dd);
+    T.cn = reinterpret_cast<float*>(km_smem + lay.off_cn);
     T.acc = reinterpret_cast<uint64_t*>(km_smem + lay.off_acc);
     T.cnt = reinterpret_cast<uint32_t*>(km_smem + lay.off_cnt);
     T.qc = reinterpret_cast<int*>(km_smem + lay.off_misc);
@@ -225,6 +230,7 @@ __device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, cons
         T.thr[i] = clause1_thr(P.s[i], dhi[i]);
         T.ec[i] = P.ec[i];
         T.ddn[i] = F.ddn[i];
+        T.cn[i] = P.cn2[i];
     }
     return T;
 }
@@ -248,89 +254,128 @@ struct Counters {
 struct StepFlags {
     bool first, prune, want_inertia;
     float gamma, ecmax;
+    float cnmax;   // largest centroid norm, rounded up (bound of the expanded form)
 };
 
-// One survivor, row x in registers: the scan, the new state word and, after
-// the first step, the move of a changed point's row between the sums (cp
-// selects the copy of the LDS sums).  In the first step the new cluster is
-// stored to *first_b instead.  KC >= k: distance slots.
+// Largest norm of the step's float32 centroids, rounded up (from the squared
+// norms in LDS).
+__device__ __forceinline__ float centroid_norm_max(const Tables& T, int k) {
+    float m2 = 0.f;
+    for (int j = 0; j < k; ++j) m2 = fmaxf(m2, T.cn[j]);
+    return sqrtf(m2) * kUp * kUp;
+}
+
+// One survivor, row x in registers: its assignment, the new state word and,
+// after the first step, the move of a changed point's row between the sums
+// (cp selects the copy of the LDS sums).  In the first step the new cluster
+// is stored to *first_b instead.  KC >= k: distance slots.
 //
-// The distances to all k centroids are formed first (independent chains),
-// then the MTI decisions are taken on them in scan order, so that the count
-// of computed distances is that of the scan:
-//   later steps: the incumbent first (the tightening of the bound), then c_j
-//     in index order, skipped when the tightened bound is at most half the
-//     distance from the incumbent to c_j (Clause 3);
-//   first step (no bound): Elkan's running best, c_j skipped when the best
-//     bound so far is at most half the distance from the best centroid to c_j.
-// A skipped c_j is not strictly closer than the best, and a tie goes to the
-// best (the incumbent, or a lower index), so the skips never change the
-// result.
+// The k squared distances are first formed in the expanded form
+// |x|^2 + |c|^2 - 2 x.c (one fused multiply-add per coordinate and centroid,
+// half the work of the direct form).  Its float32 error is at most
+// E = (d + 8) 2^-24 (|x| + |c|)^2 + 4 (|x| + |c|) ec + 2 ec^2, with ec the
+// centroids' float32 rounding errors, so every centroid whose expanded value
+// exceeds the smallest by more than 2E is strictly farther than the nearest
+// and only the others are candidates:
+//   - a single candidate is the nearest centroid; its bound is the square
+//     root of its expanded value plus E (with inertia, its direct-form
+//     distance is formed for the sum);
+//   - several candidates are decided on their direct-form distances with the
+//     oracle's tie rule, and a near tie again in float64 against the master
+//     centroids.
+// The decision is therefore the same as a scan of all direct-form distances.
+// The count of distances is that of the MTI scan: in later steps the
+// incumbent (the tightening of the bound) and every c_j that Clause 3 does
+// not skip (the tightened bound at most half the distance from the incumbent
+// to c_j); in the first step, which has no bound, all k.
 template <int KC, bool INC_ONLY = false>
 __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, const Tables& T, const StepFlags& fl,
                                        const double* C64, const float (&x)[kD], int64_t p, int inc, int cp,
                                        Counters& cn, int* first_b) {
     const int k = P.k;
-    float Dall[KC];
+    float x2 = 0.f;
 #pragma unroll
-    for (int j = 0; j < KC; ++j) Dall[j] = j < k ? sqd_row(x, T.C + j * kCR) : INFINITY;
+    for (int m = 0; m < kD; ++m) x2 = fmaf(x[m], x[m], x2);
+    float V[KC];
+    float vmin = INFINITY;
+#pragma unroll
+    for (int j = 0; j < KC; ++j) {
+        if (j < k) {   // uniform
+            const float* c = T.C + j * kCR;
+            float dt = 0.f;
+#pragma unroll
+            for (int m = 0; m < kD; m += 4) {
+                const f32x4 cv = *reinterpret_cast<const f32x4*>(c + m);
+                dt = fmaf(x[m], cv.x, dt);
+                dt = fmaf(x[m + 1], cv.y, dt);
+                dt = fmaf(x[m + 2], cv.z, dt);
+                dt = fmaf(x[m + 3], cv.w, dt);
+            }
+            V[j] = fmaf(-2.f, dt, x2 + T.cn[j]);
+        } else {
+            V[j] = INFINITY;
+        }
+        vmin = fminf(vmin, V[j]);
+    }
+    const float R = sqrtf(x2) * (1.0f + 0x1p-20f) + fl.cnmax;
+    const float E = (kExpGamma * R * R + 4.f * R * fl.ecmax + 2.f * fl.ecmax * fl.ecmax) * kUp;
+    const float lim = vmin + 2.f * E;
+    uint32_t cmask = 0;
+#pragma unroll
+    for (int j = 0; j < KC; ++j) cmask |= (V[j] <= lim ? 1u : 0u) << j;
     int b;
-    float Db, ub, D2 = INFINITY;
-    uint64_t nc = 1;
-    if (INC_ONLY || inc >= 0) {   // the incremental kernel's survivors always have an incumbent
-        float hrow[(KC + 3) / 4 * 4];
-#pragma unroll
-        for (int j = 0; j < KC; j += 4) {
-            const f32x4 v = *reinterpret_cast<const f32x4*>(T.h + inc * kSmallMaxK + j);
-            hrow[j] = v.x;
-            hrow[j + 1] = v.y;
-            hrow[j + 2] = v.z;
-            hrow[j + 3] = v.w;
-        }
-        Db = INFINITY;
-#pragma unroll
-        for (int j = 0; j < KC; ++j) Db = j == inc ? Dall[j] : Db;
-        const float u = bound_of(Db, T.ec[inc], fl.gamma);
-        b = inc;
-        // Branch-free (selects, no lane-mask branches): c_j is taken unless
-        // Clause 3 skips it.
-#pragma unroll
-        for (int j = 0; j < KC; ++j) {
-            if (j >= k) continue;   // uniform
-            const bool c = j != inc && !(fl.prune && u <= hrow[j]);
-            const float dj = Dall[j];
-            const bool lt = c && dj < Db;
-            const bool le2 = c && !lt && dj < D2;
-            nc += c ? 1 : 0;
-            D2 = lt ? Db : (le2 ? dj : D2);
-            Db = lt ? dj : Db;
-            b = lt ? j : b;
-        }
-        ub = b == inc ? u : bound_of(Db, T.ec[b], fl.gamma);
+    float Db, ub;
+    if (__popc(cmask) == 1 && !fl.want_inertia) {
+        b = __builtin_ctz(cmask);
+        Db = vmin;
+        ub = sqrt_up(fmaxf(vmin + E, 0.f)) * kUp;
     } else {
+        // Direct-form distances of the candidates, in ascending index; the
+        // incumbent wins an exact tie, then the lower index.
+        float d2 = INFINITY;
+        int rk1 = INT_MAX;
         b = 0;
-        Db = Dall[0];
-        ub = bound_of(Db, T.ec[0], fl.gamma);
-#pragma unroll
-        for (int j = 1; j < KC; ++j) {
-            if (j >= k) continue;   // uniform
-            const bool c = !(fl.prune && ub <= T.h[b * kSmallMaxK + j]);
-            const float dj = Dall[j];
-            const bool lt = c && dj < Db;
-            const bool le2 = c && !lt && dj < D2;
-            nc += c ? 1 : 0;
-            D2 = lt ? Db : (le2 ? dj : D2);
-            Db = lt ? dj : Db;
-            ub = lt ? bound_of(dj, T.ec[j], fl.gamma) : ub;
-            b = lt ? j : b;
+        Db = INFINITY;
+        uint32_t cm = cmask;
+        while (cm) {
+            const int j = __builtin_ctz(cm);
+            cm &= cm - 1;
+            const float dj = sqd_row(x, T.C + j * kCR);
+            const int rk = j == inc ? -1 : j;
+            if (dj < Db || (dj == Db && rk < rk1)) {
+                d2 = Db;
+                Db = dj;
+                rk1 = rk;
+                b = j;
+            } else if (dj < d2) {
+                d2 = dj;
+            }
+        }
+        ub = bound_of(Db, T.ec[b], fl.gamma);
+        if (d2 != INFINITY) {
+            const float band = 2.f * fl.gamma * (Db + d2) + 4.f * (sqrt_up(Db) + sqrt_up(d2)) * fl.ecmax +
+                               8.f * fl.ecmax * fl.ecmax;
+            if (d2 - Db <= band) {   // near tie: float64 decision, the oracle's tie rule
+                b = recheck64(x, C64, k, inc, Db, ub);
+                cn.rc += 1;
+            }
         }
     }
-    if (D2 != INFINITY) {
-        const float band = 2.f * fl.gamma * (Db + D2) + 4.f * (sqrt_up(Db) + sqrt_up(D2)) * fl.ecmax +
-                           8.f * fl.ecmax * fl.ecmax;
-        if (D2 - Db <= band) {   // near tie: float64 decision, the oracle's tie rule
-            b = recheck64(x, C64, k, inc, Db, ub);
-            cn.rc += 1;
+    // The MTI scan's count of distances.
+    uint32_t nc = (uint32_t)k;
+    if ((INC_ONLY || inc >= 0) && fl.prune) {
+        float vi = INFINITY;
+#pragma unroll
+        for (int j = 0; j < KC; ++j) vi = j == inc ? V[j] : vi;
+        const float u = b == inc ? ub : sqrt_up(fmaxf(vi + E, 0.f)) * kUp;   // the incumbent's tightened bound
+        nc = 1;
+#pragma unroll
+        for (int j = 0; j < KC; j += 4) {
+            const f32x4 hv = *reinterpret_cast<const f32x4*>(T.h + inc * kSmallMaxK + j);
+            nc += (j < k && j != inc && !(u <= hv.x)) ? 1u : 0u;
+            nc += (j + 1 < k && j + 1 != inc && !(u <= hv.y)) ? 1u : 0u;
+            nc += (j + 2 < k && j + 2 != inc && !(u <= hv.z)) ? 1u : 0u;
+            nc += (j + 3 < k && j + 3 != inc && !(u <= hv.w)) ? 1u : 0u;
         }
     }
     cn.comp += nc;
@@ -507,6 +552,7 @@ __device__ float eos_finish(const Dev& P, const Fused& F, int t, const EosIn& in
             if (m == 0) {
                 T->ec[j] = ec;
                 T->ddn[j] = f32_down(lo);
+                T->cn[j] = (float)c2;
             }
         }
     }
@@ -586,8 +632,8 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
     if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 1;
 
     const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-    const StepFlags fl{t == 0, !(P.flags & KM_FLAG_NO_PRUNE), (P.flags & KM_FLAG_STATS) != 0, P.gamma,
-                       st->ec_max};
+    StepFlags fl{t == 0, !(P.flags & KM_FLAG_NO_PRUNE), (P.flags & KM_FLAG_STATS) != 0, P.gamma,
+                 st->ec_max, 0.f};
     const SmallLds lay = small_lds(P.k, true);
     const Tables T = load_tables(P, F, lay, t);
     clear_next_slots(P, F, t);
@@ -595,6 +641,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
     int* qp = reinterpret_cast<int*>(km_smem + lay.off_qp);       // queued point index
     int* qa = reinterpret_cast<int*>(km_smem + lay.off_qa);       // queued incumbent (-1: none)
     __syncthreads();
+    fl.cnmax = centroid_norm_max(T, P.k);
 
     Counters cn;
     const int64_t n = P.n;
@@ -846,7 +893,7 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
     if (wt < wt_hi) load_states(wt);
     if (blockIdx.x == 0 && tid == 0) st->active = 1;
     clear_next_slots(P, F, t);
-    const StepFlags fl{false, !(P.flags & KM_FLAG_NO_PRUNE), false, P.gamma, ecmax};
+    StepFlags fl{false, !(P.flags & KM_FLAG_NO_PRUNE), false, P.gamma, ecmax, 0.f};
     // Near-tie decisions read the float64 centroids from LDS (one address
     // space: plain LDS loads, whose waits the compiler counts exactly).
     const double* C64 = c64n;
@@ -861,6 +908,7 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
     int* wq_a = reinterpret_cast<int*>(km_smem + lay.off_qa) + w * kIncWaveQ;
     float* wg = reinterpret_cast<float*>(km_smem + lay.off_qr) + 64 * w * kCR;  // its staged rows
     __syncthreads();
+    fl.cnmax = centroid_norm_max(T, P.k);
 
     Counters cn;
     const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);

@@ -75,7 +75,13 @@ def test_stream_paths_are_bitwise_identical_to_generic_path(case, prune):
         np.testing.assert_array_equal(outs[0][1], o[1])
         np.testing.assert_array_equal(outs[0][2], o[2])
         np.testing.assert_array_equal(hists[0]["changed"], h["changed"])
-    np.testing.assert_allclose(hists[2]["inertia"], hists[3]["inertia"], rtol=1e-12)
+    # The inertia sums each point's float32 distance; a near tie decided again
+    # in float64 contributes that distance rounded to float32.  The paths
+    # form their candidate sets differently (certified expanded-form
+    # candidates on the streaming path), so a few near-tie points can take the
+    # float64 decision on one path only: a difference of a few float32 units
+    # of one term.
+    np.testing.assert_allclose(hists[2]["inertia"], hists[3]["inertia"], rtol=1e-9)
     if not prune:
         assert (hists[0]["computed"] == n * k).all()
 
