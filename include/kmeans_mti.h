@@ -78,11 +78,13 @@ enum {
     KM_FLAG_GENERIC = 64u,     /* use the general assignment kernel and separate reduction,
                                   update and table launches even where the streaming step
                                   (d = 16, k <= 16) applies; same results */
-    KM_FLAG_FULL_SUMS = 128u,  /* streaming step: recompute the per-cluster sums from every
-                                  point (one full read of X) in every step instead of moving
-                                  the sums of the points whose assignment changed (after the
-                                  first step only the Clause-1 survivors' rows are read);
-                                  same results.  Implied by KM_FLAG_STATS. */
+    KM_FLAG_FULL_SUMS = 128u,  /* recompute the per-cluster sums from every point (one full
+                                  read of X) in every step instead of moving the sums of the
+                                  points whose assignment changed, where only the Clause-1
+                                  survivors' rows are read after the first step (the
+                                  streaming path, d = 16 and k <= 16, and the incremental
+                                  matrix-core path, d = 16 or 32 and k <= 128); same results.
+                                  Implied by KM_FLAG_STATS. */
     KM_FLAG_SPHERICAL = 256u,  /* spherical k-means (the paper's sk-means application): the
                                   rows of X are projected to the unit sphere (into a copy the
                                   context owns; a zero row stays zero) and C0 likewise, the
@@ -191,7 +193,11 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
  * followed by k_small_finish, with KM_FLAG_FULL_SUMS or KM_FLAG_STATS),
  * "lds-vector" /
  * "lds-mfma" (centroids and sums in LDS: k_assign with vector or matrix-core
- * survivors, then k_reduce, k_update, k_centroid_table), "lds-elkan" (the
+ * survivors, then k_reduce, k_update, k_centroid_table), "lds-inc" (d = 16
+ * or 32, k <= 128, where the streaming path does not apply: k_inc_mm reads
+ * the point states and only the Clause-1 survivors' rows, settles the
+ * survivors on the matrix cores and sums the moves of the points whose
+ * cluster changed; then k_reduce, k_update, k_centroid_table), "lds-elkan" (the
  * same with KM_FLAG_ELKAN's lower-bound scan), "global-mfma"
  * (centroids or sums too large for LDS: dense MFMA survivors, sums by
  * counting sort).  "" for a NULL context.

@@ -19,6 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libkmeans_mti.so")
 SOURCES = [os.path.join(CSRC, "km_kernels.hip"), os.path.join(CSRC, "km_large.hip"),
            os.path.join(CSRC, "km_small.hip"), os.path.join(CSRC, "km_pp.hip"),
+           os.path.join(CSRC, "km_incmm.hip"),
            os.path.join(CSRC, "km_capi.hip")]
 ARCH = "gfx950"
 

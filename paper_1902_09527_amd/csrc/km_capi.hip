@@ -153,6 +153,8 @@ struct km_ctx {
     bool large = false;   // global-memory path (centroids / sums too large for LDS)
     bool small = false;   // streaming step (d = 16, k <= 16)
     bool inc = false;     // ... with incremental steps after the first
+    bool incmm = false;   // incremental matrix-core step (d = 16 or 32, k <= 128)
+    int gim = 0, lds_im = 0;   // its grid and LDS
     int gi = 0, lds_inc = 0;   // grid and LDS of the incremental kernel
     int64_t enq = 0;      // steps enqueued so far
     km::Fused fz{};
@@ -292,8 +294,9 @@ int enqueue_iteration(km_ctx* c) {
         c->stepped = true;
         return KM_OK;
     }
-    e = c->large ? km::launch_large_assign(c->dv, c->lg, c->gb, c->stream)
-                 : km::launch_assign(c->dv, c->variant, c->tp, c->lds, c->stream);
+    e = c->incmm   ? km::launch_inc_mm(c->dv, c->gim, c->lds_im, c->enq == 0 ? 1 : 0, c->stream)
+        : c->large ? km::launch_large_assign(c->dv, c->lg, c->gb, c->stream)
+                   : km::launch_assign(c->dv, c->variant, c->tp, c->lds, c->stream);
     if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "assign kernel"));
     if ((e = mark(1)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
     e = c->large ? km::launch_large_reduce(c->dv, c->lg, c->stream) : km::launch_reduce(c->dv, c->stream);
@@ -305,6 +308,7 @@ int enqueue_iteration(km_ctx* c) {
     e = c->large ? km::launch_large_table(c->dv, 0, c->stream) : km::launch_centroid_table(c->dv, 0, c->stream);
     if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "centroid table kernel"));
     if ((e = mark(4)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
+    ++c->enq;
     c->stepped = true;
     return KM_OK;
 }
@@ -408,6 +412,24 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             if (gi > want) gi = want > 0 ? want : 1;
             c->gi = (int)gi;
         }
+    } else if (!elkan && !(c->flags & (KM_FLAG_LARGE_PATH | KM_FLAG_GENERIC | KM_FLAG_VECTOR_ONLY | KM_FLAG_STATS |
+                                         KM_FLAG_FULL_SUMS | KM_FLAG_NO_PRUNE)) &&
+               km::inc_mm_applies(n, d, k, aligned) && km::inc_mm_lds(d, km::inc_mm_kb(k)).bytes <= max_lds) {
+        // Incremental matrix-core step: only the Clause-1 survivors' rows are read.
+        c->incmm = true;
+        c->lds_im = km::inc_mm_lds(d, km::inc_mm_kb(k)).bytes;
+        const void* sym = km::inc_mm_symbol(d, k);
+        KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds_im));
+        int per_cu = 0;
+        KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, km::kIMWaves * 64, c->lds_im));
+        if (per_cu < 1) return KM_ERR_UNSUPPORTED;
+        // Resident blocks, at most one wave tile per wave.
+        const int64_t nwt = (n + km::kIMTile - 1) / km::kIMTile;
+        int64_t G = (int64_t)per_cu * cus;
+        const int64_t want = (nwt + km::kIMWaves - 1) / km::kIMWaves;
+        if (G > want) G = want > 0 ? want : 1;
+        c->gim = (int)G;
+        v.G = (int32_t)G;
     } else if (!(c->flags & KM_FLAG_LARGE_PATH)) {
         c->variant = km::assign_variant(d, k, aligned, (c->flags & KM_FLAG_VECTOR_ONLY) != 0, elkan);
         const bool h_lds = km::assign_h_lds(c->variant % 16, k);
@@ -420,7 +442,7 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             }
         }
     }
-    if (c->small) {
+    if (c->small || c->incmm) {
         // configured above
     } else if (c->tp > 0) {
         const void* sym = km::assign_kernel_symbol(c->variant);
@@ -470,8 +492,21 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     }
 
     int rc;
-    if (!c->small && ((rc = c->alloc(&v.a, (size_t)n)) || (rc = c->alloc(&v.u, (size_t)n))))
+    if (!c->small && !c->incmm && ((rc = c->alloc(&v.a, (size_t)n)) || (rc = c->alloc(&v.u, (size_t)n))))
         return rc;
+    if (c->incmm) {   // point states padded to whole wave tiles, running sums, cumulative drifts
+        const size_t nw = (size_t)((n + km::kIMTile - 1) / km::kIMTile) * km::kIMTile;
+        if ((rc = c->alloc(&v.w, nw)) || (rc = c->alloc(&v.sums, (size_t)k * d + k)) ||
+            (rc = c->alloc(&v.dhi, (size_t)k)) || (rc = c->alloc(&v.dlo, (size_t)k)) ||
+            (rc = c->alloc(&v.dupf, (size_t)k)) || (rc = c->alloc(&v.ddnf, (size_t)k)))
+            return rc;
+        zr.add(v.w, sizeof(uint32_t) * nw);
+        zr.add(v.sums, sizeof(uint64_t) * ((size_t)k * d + k));
+        zr.add(v.dhi, sizeof(double) * (size_t)k);
+        zr.add(v.dlo, sizeof(double) * (size_t)k);
+        zr.add(v.dupf, sizeof(float) * (size_t)k);
+        zr.add(v.ddnf, sizeof(float) * (size_t)k);
+    }
     if (elkan) {   // O(nk) lower bounds (zero: valid before any distance is known)
         if ((uint64_t)n > (uint64_t)INT64_MAX / 4 / (uint64_t)k) return KM_ERR_INVALID_ARG;
         if ((rc = c->alloc(&v.lb, (size_t)n * (size_t)k)) || (rc = c->alloc(&v.dhi, (size_t)k)) ||
@@ -705,7 +740,9 @@ int kmeans_mti_get(km_ctx* ctx, int32_t* assign_out, float* C_out) {
     if (assign_out && ctx->small &&
         (e = km::launch_small_unpack(ctx->fz, ctx->n, assign_out, ctx->stream)) != hipSuccess)
         return fail_ctx(ctx, hip_fail(e, "assignment unpack kernel"));
-    if (assign_out && !ctx->small &&
+    if (assign_out && ctx->incmm && (e = km::launch_inc_mm_unpack(ctx->dv, assign_out, ctx->stream)) != hipSuccess)
+        return fail_ctx(ctx, hip_fail(e, "assignment unpack kernel"));
+    if (assign_out && !ctx->small && !ctx->incmm &&
         (e = hipMemcpyAsync(assign_out, ctx->dv.a, (size_t)ctx->n * sizeof(int32_t),
                             hipMemcpyDeviceToDevice, ctx->stream)) != hipSuccess)
         return fail_ctx(ctx, hip_fail(e, "hipMemcpyAsync assign"));
@@ -1084,6 +1121,7 @@ const char* kmeans_mti_path(const km_ctx* ctx) {
     if (!ctx) return "";
     if (ctx->small) return ctx->inc ? "stream-d16" : "stream-d16-full";
     if (ctx->large) return "global-mfma";
+    if (ctx->incmm) return "lds-inc";
     if (ctx->variant % 16 == 8) return "lds-elkan";
     return ctx->variant % 16 ? "lds-mfma" : "lds-vector";
 }

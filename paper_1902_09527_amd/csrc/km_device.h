@@ -41,6 +41,49 @@ __device__ inline uint64_t fixed_bits(double v, double scale) {
     return (uint64_t)__double_as_longlong(fma(v, scale, kMagic));
 }
 
+// Squared float32 distance (direct-difference form, coordinates in order) of
+// two rows, compile-time D (16-byte aligned rows).
+template <int D>
+__device__ inline float sqd_lds_fixed(const float* x, const float* c) {
+    float acc = 0.f;
+#pragma unroll
+    for (int m = 0; m < D; m += 4) {
+        const float4 xv = *reinterpret_cast<const float4*>(x + m);
+        const float4 cv = *reinterpret_cast<const float4*>(c + m);
+        float t0 = xv.x - cv.x, t1 = xv.y - cv.y, t2 = xv.z - cv.z, t3 = xv.w - cv.w;
+        acc = fmaf(t0, t0, acc);
+        acc = fmaf(t1, t1, acc);
+        acc = fmaf(t2, t2, acc);
+        acc = fmaf(t3, t3, acc);
+    }
+    return acc;
+}
+
+// Squared float64 distance (direct-difference form) of a float row to a
+// float64 centroid row.
+__device__ inline double sqd64(const float* x, const double* c, int d) {
+    double acc = 0.0;
+    for (int m = 0; m < d; ++m) {
+        double t = (double)x[m] - c[m];
+        acc = fma(t, t, acc);
+    }
+    return acc;
+}
+
+// Clause-1 threshold on a bound kept relative to the cumulative drift: when
+// Clause 1 holds for v + D_a <= s(a) (D_a rounded up, s(a) rounded down), thr
+// is the largest float with thr + D_a <= s(a), so that the test is v <= thr
+// (+inf when k = 1).
+__device__ inline float clause1_thr(float s, double dhi) {
+    const double x = (double)s - dhi;
+    return isinf(x) ? (float)x : f32_down(x - fabs(x) * 0x1p-50);
+}
+
+// Set bits of a wave mask below the calling lane.
+__device__ inline int lanes_below(uint64_t m) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
 __device__ inline uint64_t wave_sum_u64(uint64_t v) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);

@@ -58,9 +58,12 @@ struct Dev {
     float* f;             // k: drift ||c_j^t - c_j^{t-1}|| rounded up
     float* cn2;           // k: ||c32_j||^2 (matrix-core path)
     float* lb;            // Elkan only: k x n lower bounds (centroid-major), offset by the cumulative drift
-    double* dhi;          // Elkan only: k cumulative drifts, rounded up (else null)
-    double* dlo;          // Elkan only: k cumulative drifts, rounded down
-    float* dupf;          // Elkan only: k cumulative drifts, rounded up to float32
+    double* dhi;          // Elkan and incremental path: k cumulative drifts, rounded up (else null)
+    double* dlo;          // Elkan and incremental path: k cumulative drifts, rounded down
+    float* dupf;          // Elkan and incremental path: k cumulative drifts, rounded up to float32
+    float* ddnf;          // incremental path: k cumulative drifts, rounded down to float32 (else null)
+    uint32_t* w;          // incremental path: point states (cluster and bound, below), padded
+    uint64_t* sums;       // incremental path: k*d + k exact sums and counts, carried across steps (else null)
     uint64_t* part;       // G x L per-block partial rows
     uint64_t* total;      // L reduced row (zero between iterations)
     IterState* st;
@@ -134,8 +137,12 @@ constexpr int kHLdsMaxK = 64;
 // half-distance table in LDS; the host sizes the LDS image with the same rule.
 __host__ __device__ inline bool assign_h_lds(int kb, int k) { return (kb == 0 || kb == 8) && k <= kHLdsMaxK; }
 
-// Centroid count rounded up to the 32-row blocks of the matrix-core path.
-__host__ __device__ inline int k_pad32(int k) { return (k + 31) / 32 * 32; }
+// Centroid count rounded up to the 32-row blocks of the matrix-core path,
+// whose variants use 1, 2 or 4 blocks (k <= 32, <= 64, <= 128).
+__host__ __device__ inline int k_pad32(int k) {
+    const int p = (k + 31) / 32 * 32;
+    return p > 64 && p < 128 ? 128 : p;
+}
 
 __host__ __device__ inline AssignLds assign_lds(int d, int k, int tp, bool h_lds, bool wide = false) {
     AssignLds L;
@@ -346,6 +353,61 @@ int assign_variant(int d, int k, bool aligned, bool vector_only, bool elkan);
 // Kernel symbol of an assignment-kernel variant (for occupancy queries).
 const void* assign_kernel_symbol(int variant);
 
+
+// Incremental matrix-core step (km_incmm.hip), d = 16 or 32, k <= 128: the
+// point states are streamed (4 bytes per point), only the Clause-1
+// survivors' rows are gathered, and the sums move the rows of the points
+// whose cluster changed (the running sums are carried in Dev::sums).
+// Point state: bits 6..0 the cluster, the word with those bits cleared a
+// float32 value v (rounded up) with v + D_a an upper bound on the point's
+// distance to its centroid, D_a the cumulative drift of its cluster.
+constexpr int kIMWaves = 8;          // waves per block
+constexpr int kIMBatch = 32;         // survivors per matrix-core batch
+constexpr int kIMSub = 64;           // points per Clause-1 sub-step of a wave (one per lane)
+constexpr int kIMTile = 4 * kIMSub;  // points a wave takes at once; the state array is padded to it
+constexpr int kIMQcap = kIMBatch + kIMSub;   // entries of one survivor queue
+constexpr int kIMMaxK = 128;
+
+struct IncMMLds {
+    int off_c, off_ca, off_cn, off_thr, off_ec, off_ddn, off_dup, off_hm, off_acc, off_cnt, off_misc, off_q, off_x,
+        bytes;
+};
+
+// Every offset depends on D and KB only (constants of each kernel variant).
+__host__ __device__ inline IncMMLds inc_mm_lds(int D, int KB) {
+    IncMMLds L;
+    int o = 0;
+    auto take = [&](int bytes) {
+        o = (o + 15) / 16 * 16;
+        int r = o;
+        o += bytes;
+        return r;
+    };
+    const int kp = 32 * KB;
+    L.off_c = take(4 * kp * D);                          // float32 centroid rows
+    L.off_ca = take(KB == 4 ? 4 * KB * (D / 2) * 64 : 0); // matrix-core operands (KB = 4)
+    L.off_cn = take(4 * kp);                             // squared centroid norms
+    L.off_thr = take(4 * kIMMaxK);                       // Clause-1 thresholds
+    L.off_ec = take(4 * kIMMaxK);
+    L.off_ddn = take(4 * kIMMaxK);
+    L.off_dup = take(4 * kIMMaxK);
+    L.off_hm = take(4 * kIMMaxK * 4);                    // min half-distance from a cluster to each block
+    L.off_acc = take(8 * kp * D);                        // fixed-point sums of the moves
+    L.off_cnt = take(4 * kp);
+    L.off_misc = take(64);                               // tile counter at 0, kNumStat uint64 counters at 16
+    L.off_q = take(kIMWaves * 2 * KB * kIMQcap * 4);     // per wave: KB queues of (point, state)
+    L.off_x = take(kIMWaves * kIMBatch * (D + 4) * 4);   // per wave: the batch's rows (+ 4 spare words)
+    L.bytes = (o + 15) / 16 * 16;
+    return L;
+}
+
+bool inc_mm_applies(int64_t n, int d, int k, bool aligned);
+int inc_mm_kb(int k);
+const void* inc_mm_symbol(int d, int k);
+// One step (first: no bounds yet, every point is scanned).
+hipError_t launch_inc_mm(const Dev& dv, int grid, int lds_bytes, int first, hipStream_t s);
+// assign_out[i] = cluster of point i from the point states.
+hipError_t launch_inc_mm_unpack(const Dev& dv, int32_t* assign_out, hipStream_t s);
 
 // k-means++ seeding (km_pp.hip).  Points are processed in chunks of
 // kPPChunk rows, one workgroup per chunk; the block weight sums are per chunk.

@@ -53,40 +53,12 @@ __device__ inline float sqd_reg(const Row<D>& x, const float* c) {
     return acc;
 }
 
-// Both rows in LDS, compile-time D (16-byte aligned rows).
-template <int D>
-__device__ inline float sqd_lds_fixed(const float* x, const float* c) {
-    float acc = 0.f;
-#pragma unroll
-    for (int m = 0; m < D; m += 4) {
-        const float4 xv = *reinterpret_cast<const float4*>(x + m);
-        const float4 cv = *reinterpret_cast<const float4*>(c + m);
-        float t0 = xv.x - cv.x, t1 = xv.y - cv.y, t2 = xv.z - cv.z, t3 = xv.w - cv.w;
-        acc = fmaf(t0, t0, acc);
-        acc = fmaf(t1, t1, acc);
-        acc = fmaf(t2, t2, acc);
-        acc = fmaf(t3, t3, acc);
-    }
-    return acc;
-}
-
 // Generic-d form: both rows in LDS.
 __device__ inline float sqd_lds(const float* x, const float* c, int d) {
     float acc = 0.f;
     for (int m = 0; m < d; ++m) {
         float t = x[m] - c[m];
         acc = fmaf(t, t, acc);
-    }
-    return acc;
-}
-
-// Squared float64 distance (direct-difference form) of an LDS float row to a
-// float64 centroid row in global memory.
-__device__ inline double sqd64(const float* x, const double* c, int d) {
-    double acc = 0.0;
-    for (int m = 0; m < d; ++m) {
-        double t = (double)x[m] - c[m];
-        acc = fma(t, t, acc);
     }
     return acc;
 }
@@ -1165,9 +1137,12 @@ __global__ __launch_bounds__(64) void k_update(Dev P) {
     IterState* st = P.st;
     if (!st->active) return;
     const int j = blockIdx.x, d = P.d, k = P.k;
-    const uint64_t count = P.total[(int64_t)k * d + j];
-    auto mean = [&](int64_t o) {
-        const int64_t q = (int64_t)(P.total[o] - count * kMagicBits);
+    // The exact sums of the step: the reduced row, or on the incremental
+    // path the running sums plus the reduced moves (wrap-around integers).
+    auto total = [&](int64_t o) { return P.sums ? P.sums[o] + P.total[o] : P.total[o]; };
+    const uint64_t count = total((int64_t)k * d + j);
+    auto mean = [&](uint64_t v) {
+        const int64_t q = (int64_t)(v - count * kMagicBits);
         return ((double)q * P.qinv) / (double)count;
     };
     // Spherical k-means: the mean is projected to the unit sphere (a zero
@@ -1177,7 +1152,7 @@ __global__ __launch_bounds__(64) void k_update(Dev P) {
     if ((P.flags & KM_FLAG_SPHERICAL) && count > 0) {
         double s = 0.0;
         for (int m = threadIdx.x; m < d; m += 64) {
-            const double v = mean((int64_t)j * d + m);
+            const double v = mean(total((int64_t)j * d + m));
             s = fma(v, v, s);
         }
 #pragma unroll
@@ -1189,7 +1164,9 @@ __global__ __launch_bounds__(64) void k_update(Dev P) {
     for (int m = threadIdx.x; m < d; m += 64) {
         const int64_t o = (int64_t)j * d + m;
         const double cold = P.C64[o];
-        const double cnew = keep ? cold : mean(o) / scale;
+        const uint64_t tv = total(o);
+        const double cnew = keep ? cold : mean(tv) / scale;
+        if (P.sums) P.sums[o] = tv;
         P.total[o] = 0;
         const double df = cnew - cold;
         dr = fma(df, df, dr);
@@ -1207,13 +1184,16 @@ __global__ __launch_bounds__(64) void k_update(Dev P) {
     if (threadIdx.x == 0) {
         P.f[j] = f32_up(sqrt(dr) * (1.0 + 0x1p-40));
         P.ec[j] = f32_up(sqrt(de) * (1.0 + 0x1p-40));
+        if (P.sums) P.sums[(int64_t)k * d + j] = count;
         P.total[(int64_t)k * d + j] = 0;
-        if (P.dhi) {   // cumulative drift, bracketed, for the Elkan lower bounds
+        if (P.dhi) {   // cumulative drift, bracketed (Elkan lower bounds, incremental bounds)
             const double fd = sqrt(dr);
             const double hi = (P.dhi[j] + fd * (1.0 + 0x1p-40)) * (1.0 + 0x1p-50);
+            const double lo = (P.dlo[j] + fd * (1.0 - 0x1p-40)) * (1.0 - 0x1p-50);
             P.dhi[j] = hi;
-            P.dlo[j] = (P.dlo[j] + fd * (1.0 - 0x1p-40)) * (1.0 - 0x1p-50);
+            P.dlo[j] = lo;
             P.dupf[j] = f32_up(hi);
+            if (P.ddnf) P.ddnf[j] = f32_down(lo);
         }
     }
     if (j == 0 && threadIdx.x == 0) {

@@ -77,11 +77,6 @@ __device__ __forceinline__ uint32_t pack_state(float v, int a) {
 __device__ __forceinline__ int state_cluster(uint32_t w) { return (int)(w & 15u); }
 __device__ __forceinline__ float state_value(uint32_t w) { return __uint_as_float(w & ~15u); }
 
-// Set bits of a wave mask below the calling lane.
-__device__ __forceinline__ int lanes_below(uint64_t m) {
-    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-}
-
 // State of a point now assigned to b with distance bound ub: v = ub - D_b,
 // with D_b rounded down and the subtraction rounded up.
 __device__ __forceinline__ uint32_t settle_state(float ub, float ddn_b, int b) {
@@ -208,14 +203,6 @@ __device__ __forceinline__ Tables table_ptrs(const Dev& P, const SmallLds& lay) 
     if (tid < kNumStat) T.bst[tid] = 0;
     if (tid < 3) T.qc[tid] = 0;
     return T;
-}
-
-// Clause-1 threshold of a cluster: Clause 1 holds when v + D_a <= s(a) (D_a
-// the cumulative drift rounded up, s(a) rounded down); thr is the largest
-// float with thr + D_a <= s(a), so that the test is v <= thr (+inf when k = 1).
-__device__ __forceinline__ float clause1_thr(float s, double dhi) {
-    const double x = (double)s - dhi;
-    return isinf(x) ? (float)x : f32_down(x - fabs(x) * 0x1p-50);
 }
 
 // The tables of step t from memory (the end of step t - 1 has run).

@@ -42,6 +42,7 @@ CASES = [
     (206, 5000, 64, 200, 6.0, 2.0, 12, 0.0, {"stats": True}, "global-mfma"),
     (207, 4000 + 3, 64, 50, 3.0, 1.0, 10, 0.0, {"large_path": True, "stats": True}, "global-mfma"),
     (208, 3000, 16, 12, 3.0, 1.0, 15, 0.0, {"generic": True, "stats": True}, "lds-vector"),
+    (209, 6000 + 5, 32, 40, 4.0, 2.0, 20, 0.0, {}, "lds-inc"),
 ]
 
 

@@ -148,7 +148,9 @@ def test_stream_repeated_runs_reuse_accumulation_rows():
 @pytest.mark.parametrize("d,k,flags,path", [
     (16, 10, {}, "stream-d16"), (16, 16, {}, "stream-d16"), (16, 10, {"full_sums": True}, "stream-d16-full"),
     (16, 10, {"stats": True}, "stream-d16-full"), (16, 10, {"generic": True}, "lds-vector"),
-    (16, 17, {}, "lds-mfma"), (32, 10, {}, "lds-vector"), (16, 10, {"large_path": True}, "global-mfma"),
+    (16, 17, {}, "lds-inc"), (32, 10, {}, "lds-inc"), (32, 100, {}, "lds-inc"),
+    (16, 17, {"full_sums": True}, "lds-mfma"), (32, 10, {"full_sums": True}, "lds-vector"),
+    (32, 100, {"vector_only": True}, "lds-vector"), (16, 10, {"large_path": True}, "global-mfma"),
 ])
 def test_path_selection(d, k, flags, path):
     X, C0 = synth.blobs(1000, d, k, seed=131)
