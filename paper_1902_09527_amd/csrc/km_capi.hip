@@ -498,7 +498,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         const size_t nw = (size_t)((n + km::kIMTile - 1) / km::kIMTile) * km::kIMTile;
         if ((rc = c->alloc(&v.w, nw)) || (rc = c->alloc(&v.sums, (size_t)k * d + k)) ||
             (rc = c->alloc(&v.dhi, (size_t)k)) || (rc = c->alloc(&v.dlo, (size_t)k)) ||
-            (rc = c->alloc(&v.dupf, (size_t)k)) || (rc = c->alloc(&v.ddnf, (size_t)k)))
+            (rc = c->alloc(&v.dupf, (size_t)k)) || (rc = c->alloc(&v.ddnf, (size_t)k)) ||
+            (rc = c->alloc(&v.hm, (size_t)4 * k)))
             return rc;
         zr.add(v.w, sizeof(uint32_t) * nw);
         zr.add(v.sums, sizeof(uint64_t) * ((size_t)k * d + k));

@@ -14,8 +14,9 @@
 // (work stealing within the block) and for each point
 //   1. applies Clause 1 to its state (v <= thr(a), thr(a) the largest float
 //      with thr + D_a <= s(a));
-//   2. queues a survivor by the 32-centroid block of its cluster (one queue
-//      per block), so that a batch shares its incumbents' block;
+//   2. queues a survivor by the 32-centroid blocks it needs (k <= 64: its
+//      own block and every block Clause 2 does not skip for it, one queue
+//      per set) or by the block of its cluster (k > 64);
 // and whenever a queue holds kIMBatch survivors, gathers their rows
 // (16-byte loads, requested one batch ahead of their use), stages them in its
 // own LDS rows and settles them:
@@ -24,8 +25,10 @@
 //     incumbent to each centroid of the block (the incumbent's own block is
 //     never skipped, its half-distance to itself being zero);
 //   - the other blocks' distances come from float32 MFMA tiles in the
-//     expanded form |x|^2 + |c|^2 - 2 x.c; every centroid within twice the
-//     expanded form's error bound of the smallest is a candidate, a single
+//     expanded form |x|^2 - 2 (x.c - |c|^2 / 2), the bracket formed by the
+//     matrix cores with -|c|^2 / 2 as one more dimension; every centroid
+//     within twice the expanded form's error bound of the smallest is a
+//     candidate, a single
 //     candidate is the nearest centroid (its bound from the expanded value
 //     plus the error bound), several are decided in the direct form and a
 //     near tie again in float64 against the master centroids;
@@ -102,8 +105,10 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     int* cnt = reinterpret_cast<int*>(km_smem + lay.off_cnt);
     int* tcount = reinterpret_cast<int*>(km_smem + lay.off_misc);
     uint64_t* bst = reinterpret_cast<uint64_t*>(km_smem + lay.off_misc + 16);
-    int* qp = reinterpret_cast<int*>(km_smem + lay.off_q) + w * (2 * KB * kQ);   // this wave's queues: points
-    uint32_t* qw = reinterpret_cast<uint32_t*>(qp + KB * kQ);                      // and their states
+    constexpr int NQ = inc_mm_queues(KB);
+    int* qp = reinterpret_cast<int*>(km_smem + lay.off_q) + w * (2 * NQ * kQ);   // this wave's queues: points
+    uint32_t* qw = reinterpret_cast<uint32_t*>(qp + NQ * kQ);                      // and their states
+    float* nb = reinterpret_cast<float*>(km_smem + lay.off_nb);
     float* wg = reinterpret_cast<float*>(km_smem + lay.off_x) + w * kB * XS;       // its staged rows
 
     // Tables of the step.
@@ -113,6 +118,9 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     }
     for (int i = tid; i < KP; i += kW * 64) {
         cn2s[i] = i < k ? P.cn2[i] : INFINITY;
+        // -|c|^2 / 2 (exact halving) enters the matrix-core product as one
+        // more dimension; padding centroids get a value no point reaches.
+        nb[i] = i < k ? -0.5f * P.cn2[i] : -0x1p100f;
         cnt[i] = 0;
     }
     for (int i = tid; i < k; i += kW * 64) {
@@ -122,14 +130,8 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         dup[i] = P.dupf[i];
     }
     // hm[4a + cb]: the smallest half-distance from centroid a to a centroid
-    // of block cb (zero for a's own block).
-    for (int i = tid; i < k * KB; i += kW * 64) {
-        const int a = i / KB, cb = i - a * KB;
-        const int j1 = min(32 * cb + 32, k);
-        float m = INFINITY;
-        for (int j = 32 * cb; j < j1; ++j) m = fminf(m, j == a ? 0.f : P.h[(int64_t)a * k + j]);
-        hm[4 * a + cb] = m;
-    }
+    // of block cb (zero for a's own block), from the centroid table.
+    for (int i = tid; i < 4 * k; i += kW * 64) hm[i] = P.hm[i];
     if (tid < kNumStat) bst[tid] = 0;
     if (tid == 0) *tcount = 0;
     // Matrix-core A operands: lane l feeds centroid row 32*cb + l%32 and
@@ -223,45 +225,64 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
                 if (eval[cb]) nreal += min(32, max(k - 32 * cb, 0));
             }
         }
+        // dot'_j = x.c_j - |c_j|^2 / 2 from the matrix cores: the k-steps of
+        // the dimension pairs, then one step with the extra dimension (1 on
+        // half 0, 0 on half 1).  The squared distance is |x|^2 - 2 dot'_j, so
+        // the nearest centroid has the largest dot'.
         f32x16 dot[KB];
+        const float ext = half == 0 ? 1.f : 0.f;
 #pragma unroll
         for (int cb = 0; cb < KB; ++cb) {
-#pragma unroll
-            for (int e = 0; e < 16; ++e) dot[cb][e] = 0.f;
             if (eval[cb]) {   // uniform
+                const float aext = half == 0 ? nb[cb * 32 + col] : 0.f;
+                dot[cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(aext, ext, f32x16{}, 0, 0, 0);
 #pragma unroll
                 for (int q = 0; q < kHalf; ++q)
                     dot[cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(
                         WIDE ? ca[(cb * kHalf + q) * 64 + lane] : creg[WIDE ? 0 : cb][WIDE ? 0 : q], xh[q], dot[cb],
                         0, 0, 0);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) dot[cb][e] = -INFINITY;
             }
         }
         // Register e of block cb holds centroid 32*cb + 8*(e/4) + 4*half + e%4.
         auto cent = [&](int cb, int e) { return cb * 32 + 8 * (e >> 2) + 4 * half + (e & 3); };
-        auto val = [&](int cb, int e) { return eval[cb] ? x2 + cn2s[cent(cb, e)] - 2.f * dot[cb][e] : INFINITY; };
-        float e1 = INFINITY;
+        float dmax = -INFINITY;
 #pragma unroll
         for (int cb = 0; cb < KB; ++cb)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) e1 = fminf(e1, val(cb, e));
-        e1 = fminf(e1, __shfl_xor(e1, 32));
-        // Candidates: within twice the error bound of the smallest; every
-        // other evaluated centroid is certified farther than the nearest.
+            for (int e = 0; e < 16; ++e) dmax = fmaxf(dmax, dot[cb][e]);
+        dmax = fmaxf(dmax, __shfl_xor(dmax, 32));
+        const float e1 = fmaf(-2.f, dmax, x2);   // the smallest squared distance, expanded form
+        // Candidates: dot' within E of the largest (squared distances within
+        // 2E of the smallest); every other evaluated centroid is certified
+        // farther than the nearest.  A single candidate is counted and found
+        // in the same pass.
         const float R = sqrtf(fmaxf(x2, 0.f)) * (1.0f + 0x1p-20f) + cnmax;
         const float E = (gexp * R * R + 4.f * R * ecmax + 2.f * ecmax * ecmax) * kUp;
-        const float lim = e1 + 2.f * E;
-        uint64_t cmask = 0;
+        const float lim = dmax - E;
+        int own = 0, jown = -1;
 #pragma unroll
         for (int cb = 0; cb < KB; ++cb)
 #pragma unroll
-            for (int e = 0; e < 16; ++e)
-                if (val(cb, e) <= lim) cmask |= 1ull << (16 * cb + e);
-        const uint64_t cmask0 = cmask;
-        const int own = __popcll(cmask0);
+            for (int e = 0; e < 16; ++e) {
+                const bool c = dot[cb][e] >= lim;
+                own += c ? 1 : 0;
+                jown = c ? cb * 32 + 8 * (e >> 2) + (e & 3) : jown;
+            }
+        jown = jown >= 0 ? jown + 4 * half : -1;
         const bool single = own + __shfl_xor(own, 32) == 1;
-        const int jown = own ? cent(__builtin_ctzll(cmask0) >> 4, __builtin_ctzll(cmask0) & 15) : -1;
         const int jsingle = max(jown, __shfl_xor(jown, 32));
-        if (single) cmask = 0;
+        uint64_t cmask = 0;
+        if (!single) {   // the candidate mask (rarely needed)
+#pragma unroll
+            for (int cb = 0; cb < KB; ++cb)
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    if (dot[cb][e] >= lim) cmask |= 1ull << (16 * cb + e);
+        }
+        const uint64_t cmask0 = cmask;
         // Several candidates: direct-form distances, each half over its own,
         // then the smaller (distance, incumbent first, lower index).
         float d1 = INFINITY, d2 = INFINITY;
@@ -366,16 +387,16 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     };
 
     // Queue lengths (wave-uniform).
-    int qn[KB];
+    int qn[NQ];
 #pragma unroll
-    for (int qi = 0; qi < KB; ++qi) qn[qi] = 0;
+    for (int qi = 0; qi < NQ; ++qi) qn[qi] = 0;
     // Settles the batch in flight and takes the next from the fullest queue
     // while one holds a whole batch (at the end: while any holds entries).
     auto batch_point = [&](bool drain) __attribute__((always_inline)) {
         for (;;) {
             int qsel = -1, best = drain ? 0 : kB - 1;
 #pragma unroll
-            for (int qi = 0; qi < KB; ++qi)
+            for (int qi = 0; qi < NQ; ++qi)
                 if (qn[qi] > best) {
                     best = qn[qi];
                     qsel = qi;
@@ -387,7 +408,7 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
             if (bcnt > 0) scan_batch();
             const int c = min(best, kB);
 #pragma unroll
-            for (int qi = 0; qi < KB; ++qi)
+            for (int qi = 0; qi < NQ; ++qi)
                 if (qi == qsel) qn[qi] -= c;
             take_batch(qsel, best - c, c);   // the newest c entries
         }
@@ -415,10 +436,27 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
             const bool surv = valid && (first || !prune || !(st_value(ws) <= thr[a]));
             const uint64_t kept = __ballot(valid && !surv);
             c1w += (uint32_t)__popcll(kept);
-            const int home = first ? 0 : a >> 5;
+            // Queue: for KB <= 2 the set of blocks the survivor needs (its
+            // own block and every block Clause 2 does not skip for it), so
+            // that a batch skips the blocks none of its survivors needs; for
+            // KB = 4 the block of its cluster.
+            int key;
+            if constexpr (KB == 4) {
+                key = a >> 5;
+            } else {
+                int mask = (1 << KB) - 1;
+                if (!first && prune) {
+                    const float u = (st_value(ws) + dup[a]) * kUp;
+                    mask = 0;
 #pragma unroll
-            for (int qi = 0; qi < KB; ++qi) {
-                const bool mine = surv && home == qi;
+                    for (int cb = 0; cb < KB; ++cb)
+                        mask |= (cb == (a >> 5) || !(u <= hm[4 * a + cb])) ? 1 << cb : 0;
+                }
+                key = mask - 1;
+            }
+#pragma unroll
+            for (int qi = 0; qi < NQ; ++qi) {
+                const bool mine = surv && key == qi;
                 const uint64_t bm = __ballot(mine);
                 if (mine) {
                     const int e = qn[qi] + lanes_below(bm);

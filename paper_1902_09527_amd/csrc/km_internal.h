@@ -64,6 +64,7 @@ struct Dev {
     float* ddnf;          // incremental path: k cumulative drifts, rounded down to float32 (else null)
     uint32_t* w;          // incremental path: point states (cluster and bound, below), padded
     uint64_t* sums;       // incremental path: k*d + k exact sums and counts, carried across steps (else null)
+    float* hm;            // incremental path: k x 4, min over centroid block cb of h[a][j] (h[a][a] = 0), else null
     uint64_t* part;       // G x L per-block partial rows
     uint64_t* total;      // L reduced row (zero between iterations)
     IterState* st;
@@ -368,9 +369,13 @@ constexpr int kIMTile = 4 * kIMSub;  // points a wave takes at once; the state a
 constexpr int kIMQcap = kIMBatch + kIMSub;   // entries of one survivor queue
 constexpr int kIMMaxK = 128;
 
+// Survivor queues of a wave: one per set of 32-centroid blocks a survivor
+// needs (KB <= 2: 1 or 3 sets), or one per block of its cluster (KB = 4).
+__host__ __device__ constexpr int inc_mm_queues(int KB) { return KB == 4 ? 4 : (1 << KB) - 1; }
+
 struct IncMMLds {
-    int off_c, off_ca, off_cn, off_thr, off_ec, off_ddn, off_dup, off_hm, off_acc, off_cnt, off_misc, off_q, off_x,
-        bytes;
+    int off_c, off_ca, off_cn, off_thr, off_ec, off_ddn, off_dup, off_hm, off_nb, off_acc, off_cnt, off_misc, off_q,
+        off_x, bytes;
 };
 
 // Every offset depends on D and KB only (constants of each kernel variant).
@@ -392,10 +397,11 @@ __host__ __device__ inline IncMMLds inc_mm_lds(int D, int KB) {
     L.off_ddn = take(4 * kIMMaxK);
     L.off_dup = take(4 * kIMMaxK);
     L.off_hm = take(4 * kIMMaxK * 4);                    // min half-distance from a cluster to each block
+    L.off_nb = take(4 * kp);                             // -|c|^2 / 2 of each centroid (-huge for padding)
     L.off_acc = take(8 * kp * D);                        // fixed-point sums of the moves
     L.off_cnt = take(4 * kp);
     L.off_misc = take(64);                               // tile counter at 0, kNumStat uint64 counters at 16
-    L.off_q = take(kIMWaves * 2 * KB * kIMQcap * 4);     // per wave: KB queues of (point, state)
+    L.off_q = take(kIMWaves * 2 * inc_mm_queues(KB) * kIMQcap * 4);   // per wave: queues of (point, state)
     L.off_x = take(kIMWaves * kIMBatch * (D + 4) * 4);   // per wave: the batch's rows (+ 4 spare words)
     L.bytes = (o + 15) / 16 * 16;
     return L;

@@ -225,6 +225,17 @@ __global__ __launch_bounds__(256) void k_centroid_table(Dev P, int force) {
         }
         P.h[(int64_t)i * k + j] = hv;
     }
+    if (P.hm) {   // incremental path (k <= 128): min of row i over each 32-centroid block
+        __shared__ float hrow[kIMMaxK];
+        for (int j = threadIdx.x; j < k; j += blockDim.x) hrow[j] = P.h[(int64_t)i * k + j];
+        __syncthreads();
+        if ((int)threadIdx.x < 4) {
+            const int cb = threadIdx.x, j1 = min(32 * cb + 32, k);
+            float m = INFINITY;
+            for (int j = 32 * cb; j < j1; ++j) m = fminf(m, hrow[j]);   // h[i][i] = 0
+            P.hm[4 * i + cb] = m;
+        }
+    }
     if (threadIdx.x == 0) {   // ||c32_i||^2 for the expansion form of the matrix-core path
         const float* c = P.C32 + (int64_t)i * d;
         double n2 = 0.0;
