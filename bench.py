@@ -39,16 +39,18 @@ def log(msg: str) -> None:
 
 # Dominant (assignment-step) kernel of each library path.
 DOMINANT_KERNEL = {"stream-d16": "k_inc", "stream-d16-full": "k_small", "lds-vector": "k_assign",
-                   "lds-mfma": "k_assign", "lds-elkan": "k_assign",
+                   "lds-mfma": "k_assign", "lds-elkan": "k_assign", "lds-inc": "k_inc_mm",
                    "global-mfma": "k_mfma_large"}
 # Sources of each dominant kernel: the hardware byte counts of a committed
 # profile summary are used only while these files are unchanged.
+# km_capi.hip sets each kernel's grid and LDS, so it is part of every hash.
 KERNEL_SOURCES = {
-    "k_small": ["km_small.hip", "km_device.h", "km_internal.h"],
-    "k_inc": ["km_small.hip", "km_device.h", "km_internal.h"],
-    "k_assign": ["km_kernels.hip", "km_device.h", "km_internal.h"],
-    "k_mfma_large": ["km_large.hip", "km_device.h", "km_internal.h"],
-    "k_pp_step": ["km_pp.hip", "km_device.h", "km_internal.h"],
+    "k_small": ["km_small.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
+    "k_inc": ["km_small.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
+    "k_assign": ["km_kernels.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
+    "k_inc_mm": ["km_incmm.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
+    "k_mfma_large": ["km_large.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
+    "k_pp_step": ["km_pp.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
 }
 
 
@@ -388,7 +390,7 @@ def main() -> int:
         # read and written (12 B) plus, with incremental sums, the rows of the
         # Clause-1 survivors and of the changed points (4d B each), or with
         # full sums every row (4d B) and the changed assignments (4 B).
-        if path == "stream-d16":
+        if path in ("stream-d16", "lds-inc"):
             bytes_per_launch = 12.0 * n + 4.0 * d * (surv + ch) / m
             what = "steps 1..T-1: 12n (assignment, bound) + 4d per Clause-1 survivor and per changed point"
         elif path == "lds-elkan":
@@ -399,6 +401,8 @@ def main() -> int:
             bytes_per_launch = n * (4 * d + 12) + 4.0 * ch / m
             what = "steps 1..T-1: n*(4d+12) (rows, assignment, bound) + changed*4"
         flops = 2.0 * d * k * surv / m
+        if path == "lds-inc":   # the dense products of the centroid blocks evaluated
+            flops = 2.0 * d * comp / m
         if path == "global-mfma":
             rooflines.append(mfma_roofline_entry(kernel, tag, flops, launch_ms,
                                                  "steps 1..T-1: 2*d*k per Clause-1 survivor (bound pass included in the time)"))
@@ -408,6 +412,10 @@ def main() -> int:
             if path == "lds-mfma":
                 rooflines.append(mfma_roofline_entry(kernel, tag, flops, launch_ms,
                                                      "steps 1..T-1: 2*d*k per Clause-1 survivor"))
+            if path == "lds-inc":
+                rooflines.append(mfma_roofline_entry(kernel, tag, flops, launch_ms,
+                                                     "steps 1..T-1: 2*d per distance of the evaluated "
+                                                     "32-centroid blocks"))
         if path == "stream-d16":   # the full-read streaming kernel on the same steps
             _, later_f, h_f = kernel_pass(KS, **dict(base_flags, full_sums=True))
             ch_f = int(h_f["changed"][1:KS].sum())
