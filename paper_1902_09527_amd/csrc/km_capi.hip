@@ -140,6 +140,37 @@ void pinned_give(int32_t* p) {
     (void)hipHostFree(p);
 }
 
+// Launch configuration of a kernel: its dynamic-LDS limit raised to lds
+// bytes and the resident blocks per CU for (block, lds), both remembered per
+// device (hipFuncSetAttribute costs tens of microseconds a call).
+struct KernelCfg {
+    int dev;
+    const void* sym;
+    int block, lds, per_cu;
+};
+constexpr int kCfgSlots = 256;
+std::mutex g_cfg_mu;
+KernelCfg g_cfg[kCfgSlots];
+int g_cfg_n = 0;
+
+int kernel_config(int dev, const void* sym, int block, int lds, int* per_cu) {
+    {
+        std::lock_guard<std::mutex> lock(g_cfg_mu);
+        for (int i = 0; i < g_cfg_n; ++i)
+            if (g_cfg[i].dev == dev && g_cfg[i].sym == sym && g_cfg[i].block == block && g_cfg[i].lds == lds) {
+                *per_cu = g_cfg[i].per_cu;
+                return KM_OK;
+            }
+    }
+    KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, lds));
+    int pc = 0;
+    KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&pc, sym, block, lds));
+    std::lock_guard<std::mutex> lock(g_cfg_mu);
+    if (g_cfg_n < kCfgSlots) g_cfg[g_cfg_n++] = KernelCfg{dev, sym, block, lds, pc};
+    *per_cu = pc;
+    return KM_OK;
+}
+
 }  // namespace
 
 struct km_ctx {
@@ -384,9 +415,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         c->lds = km::small_lds_bytes(k);
         if (c->lds > max_lds || km::small_finish_lds_bytes(k) > max_lds) return KM_ERR_UNSUPPORTED;
         const void* sym = km::small_kernel_symbol(k);
-        KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds));
-        int per_cu = 0;
-        KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, c->tp, c->lds));
+        int per_cu = 0, rcc;
+        if ((rcc = kernel_config(c->device, sym, c->tp, c->lds, &per_cu)) != KM_OK) return rcc;
         if (per_cu < 1) return KM_ERR_UNSUPPORTED;
         const int64_t ntiles = (n + c->tp - 1) / c->tp;
         int64_t G = (int64_t)per_cu * cus;
@@ -397,9 +427,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             c->lds_inc = km::inc_lds_bytes(k);
             if (c->lds_inc > max_lds) return KM_ERR_UNSUPPORTED;
             const void* isym = km::inc_kernel_symbol(k);
-            KM_HIP(hipFuncSetAttribute(isym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds_inc));
             int per_cu_i = 0;
-            KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_i, isym, km::kIncThreads, c->lds_inc));
+            if ((rcc = kernel_config(c->device, isym, km::kIncThreads, c->lds_inc, &per_cu_i)) != KM_OK) return rcc;
             if (per_cu_i < 1) return KM_ERR_UNSUPPORTED;
             // Resident blocks (the same count on every CU), at least one wave
             // tile per wave; small inputs still spread over up to one block
@@ -419,9 +448,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         c->incmm = true;
         c->lds_im = km::inc_mm_lds(d, km::inc_mm_kb(k)).bytes;
         const void* sym = km::inc_mm_symbol(d, k);
-        KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds_im));
-        int per_cu = 0;
-        KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, km::kIMWaves * 64, c->lds_im));
+        int per_cu = 0, rcc;
+        if ((rcc = kernel_config(c->device, sym, km::kIMWaves * 64, c->lds_im, &per_cu)) != KM_OK) return rcc;
         if (per_cu < 1) return KM_ERR_UNSUPPORTED;
         // Resident blocks, at most one wave tile per wave.
         const int64_t nwt = (n + km::kIMTile - 1) / km::kIMTile;
@@ -446,9 +474,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         // configured above
     } else if (c->tp > 0) {
         const void* sym = km::assign_kernel_symbol(c->variant);
-        KM_HIP(hipFuncSetAttribute(sym, hipFuncAttributeMaxDynamicSharedMemorySize, c->lds));
-        int per_cu = 0;
-        KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, c->tp, c->lds));
+        int per_cu = 0, rcc;
+        if ((rcc = kernel_config(c->device, sym, c->tp, c->lds, &per_cu)) != KM_OK) return rcc;
         if (per_cu < 1) return KM_ERR_UNSUPPORTED;
         const int64_t ntiles = (n + c->tp - 1) / c->tp;
         int64_t G = (int64_t)per_cu * cus;
@@ -501,7 +528,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             (rc = c->alloc(&v.dupf, (size_t)k)) || (rc = c->alloc(&v.ddnf, (size_t)k)) ||
             (rc = c->alloc(&v.hm, (size_t)4 * k)))
             return rc;
-        zr.add(v.w, sizeof(uint32_t) * nw);
+        const size_t n4 = (size_t)n & ~(size_t)3;   // states are written by the first step; padding cleared
+        zr.add(v.w + n4, sizeof(uint32_t) * (nw - n4));
         zr.add(v.sums, sizeof(uint64_t) * ((size_t)k * d + k));
         zr.add(v.dhi, sizeof(double) * (size_t)k);
         zr.add(v.dlo, sizeof(double) * (size_t)k);
@@ -539,7 +567,10 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         zr.add(c->fz.rows, sizeof(uint64_t) * nrows);
         zr.add(c->fz.stat, sizeof(uint64_t) * 3 * km::kNumStat);
         zr.add(c->fz.sum, sizeof(uint64_t) * 2 * (size_t)(k * d + k));
-        zr.add(c->fz.w, sizeof(uint32_t) * nw);
+        // The first step writes every point's state; only the padding (read,
+        // never used) is cleared.
+        const size_t n4 = (size_t)n & ~(size_t)3;
+        zr.add(c->fz.w + n4, sizeof(uint32_t) * (nw - n4));
         zr.add(c->fz.dhi, sizeof(double) * 2 * (size_t)k);
         zr.add(c->fz.dlo, sizeof(double) * 2 * (size_t)k);
         zr.add(c->fz.dup, sizeof(float) * (size_t)k);
@@ -562,44 +593,26 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     if (c->flags & KM_FLAG_SPHERICAL)
         KM_HIP(km::launch_set_centroids_unit(C0, v.C64, v.C32, v.ec, k, d, reinterpret_cast<int32_t*>(scratch + 4),
                                              c->stream));
-    uint32_t host[5];
-    int32_t* pin = pinned_take();
-    if (!pin) return KM_ERR_OOM;
-    hipError_t ec5 = hipMemcpyAsync(pin, scratch, sizeof host, hipMemcpyDeviceToHost, c->stream);
-    if (ec5 == hipSuccess) ec5 = hipStreamSynchronize(c->stream);
-    if (ec5 == hipSuccess) memcpy(host, pin, sizeof host);
-    pinned_give(pin);
-    if (ec5 != hipSuccess) return hip_fail(ec5, "set-up read-back");
-    if ((c->flags & KM_FLAG_VALIDATE) && (host[1] || host[3])) return KM_ERR_NONFINITE;
-    if (host[4]) {
-        snprintf(g_last_hip, sizeof g_last_hip, "spherical k-means: C0 has a zero row");
-        return KM_ERR_INVALID_ARG;
+    // Fixed-point scales: computed on the device from the largest |x| (the
+    // host does not wait for them).  Only the checks that decide the call's
+    // status read the set-up back: non-finite input (KM_FLAG_VALIDATE) and a
+    // zero C0 row (spherical k-means).
+    KM_HIP(km::launch_set_scales(v.st, scratch, n, d, (c->flags & KM_FLAG_SPHERICAL) ? 1 : 0, c->stream));
+    if (c->flags & (KM_FLAG_VALIDATE | KM_FLAG_SPHERICAL)) {
+        uint32_t host[5];
+        int32_t* pin = pinned_take();
+        if (!pin) return KM_ERR_OOM;
+        hipError_t ec5 = hipMemcpyAsync(pin, scratch, sizeof host, hipMemcpyDeviceToHost, c->stream);
+        if (ec5 == hipSuccess) ec5 = hipStreamSynchronize(c->stream);
+        if (ec5 == hipSuccess) memcpy(host, pin, sizeof host);
+        pinned_give(pin);
+        if (ec5 != hipSuccess) return hip_fail(ec5, "set-up read-back");
+        if ((c->flags & KM_FLAG_VALIDATE) && (host[1] || host[3])) return KM_ERR_NONFINITE;
+        if (host[4]) {
+            snprintf(g_last_hip, sizeof g_last_hip, "spherical k-means: C0 has a zero row");
+            return KM_ERR_INVALID_ARG;
+        }
     }
-    if (c->flags & KM_FLAG_SPHERICAL) {   // the centroids and the data are unit vectors
-        const float one = 1.0f;
-        memcpy(&host[2], &one, 4);
-    }
-    float xmax, cmax;
-    memcpy(&xmax, &host[0], 4);
-    memcpy(&cmax, &host[2], 4);
-    int ex = 0, ec0 = 0;
-    if (xmax > 0) frexp((double)xmax, &ex);   // xmax <= 2^ex
-    // Coordinate sums: |x * 2^S| <= 2^50 per point and n * 2^(ex+S) <= 2^61 overall.
-    const int lgn = ceil_log2_u64((uint64_t)n);
-    int S = 61 - lgn - ex;
-    if (S > 50 - ex) S = 50 - ex;
-    v.qscale = ldexp(1.0, S);
-    v.qinv = ldexp(1.0, -S);
-    // Inertia: every squared distance is <= d * (2 * max|coordinate|)^2.
-    const double amax = xmax > cmax ? (double)xmax : (double)cmax;
-    const double dmax = (double)d * 4.0 * amax * amax;
-    int eD = 0;
-    if (dmax > 0) frexp(dmax, &eD);
-    (void)ec0;
-    int SI = 61 - lgn - eD;
-    if (SI > 50 - eD) SI = 50 - eD;
-    v.iscale = ldexp(1.0, SI);
-    v.iinv = ldexp(1.0, -SI);
 
     if (c->flags & KM_FLAG_TIMING) {
         c->timing = true;

@@ -41,6 +41,17 @@ __device__ inline uint64_t fixed_bits(double v, double scale) {
     return (uint64_t)__double_as_longlong(fma(v, scale, kMagic));
 }
 
+// The kernel's Dev with the fixed-point scales the set-up kernel left in the
+// loop state (the host does not wait for them).
+__device__ inline Dev with_scales(Dev P) {
+    const IterState* st = P.st;
+    P.qscale = st->qscale;
+    P.qinv = st->qinv;
+    P.iscale = st->iscale;
+    P.iinv = st->iinv;
+    return P;
+}
+
 // Squared float32 distance (direct-difference form, coordinates in order) of
 // two rows, compile-time D (16-byte aligned rows).
 template <int D>

@@ -72,7 +72,8 @@ __device__ __forceinline__ float st_value(uint32_t w) { return __uint_as_float(w
 __device__ __forceinline__ float sqrt_up(float v) { return __builtin_amdgcn_sqrtf(v) * (1.0f + 0x1p-20f); }
 
 template <int D, int KB>
-__global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) void k_inc_mm(Dev P, int first) {
+__global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) void k_inc_mm(Dev P_, int first) {
+    const Dev P = with_scales(P_);
     IterState* st = P.st;
     if (st->done) {
         if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;

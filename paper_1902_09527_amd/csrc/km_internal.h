@@ -41,6 +41,9 @@ struct IterState {
     double inertia_last;  // update kernel
     float ec_max;         // max_j ||c32_j - c64_j|| (centroid-table kernel)
     float pad2_;
+    // Fixed-point scales (set-up kernel k_set_scales, from the largest |x|):
+    // 2^S, 2^-S of the coordinate sums and the same for the inertia sum.
+    double qscale, qinv, iscale, iinv;
 };
 
 // Everything the kernels need, passed by value.
@@ -71,8 +74,8 @@ struct Dev {
     IterRec* rec;
     int32_t G;            // assignment blocks = partial rows
     int32_t L;            // partial row length
-    double qscale, qinv;  // 2^S, 2^-S: fixed-point scale of coordinate sums
-    double iscale, iinv;  // fixed-point scale of the inertia sum
+    double qscale, qinv;  // 2^S, 2^-S: fixed-point scale of coordinate sums (copied from st by each kernel)
+    double iscale, iinv;  // fixed-point scale of the inertia sum (likewise)
     float gamma;          // relative error bound of a float32 squared distance, d-dependent
     uint32_t flags;
 };
@@ -332,6 +335,9 @@ struct ZeroRanges {
     }
 };
 hipError_t launch_init_buffers(const ZeroRanges& z, int cus, hipStream_t s);
+// Fixed-point scales into st from the largest |x| and |c0| (float bits in
+// absmax[0] and absmax[2]; unit = 1: spherical k-means, centroids of norm 1).
+hipError_t launch_set_scales(IterState* st, const uint32_t* absmax, int64_t n, int32_t d, int unit, hipStream_t s);
 hipError_t launch_set_centroids(const float* C0, double* C64, float* C32, float* ec, int64_t kd,
                                 int32_t k, hipStream_t s);
 // Spherical k-means: rows of X projected to the unit sphere into Xn; unit

@@ -70,7 +70,9 @@ __device__ inline float sqd_lds(const float* x, const float* c, int d) {
 
 // Largest |value| (as float bits: non-negative floats order as their bits)
 // and whether any value is not finite, over one array: 16-byte loads when it
-// is 16-byte aligned, four in flight per lane, then the scalar tail.
+// is 16-byte aligned, kAbsLoads in flight per lane, then the scalar tail.
+constexpr int kAbsLoads = 8;
+constexpr int kAbsBlocksPerCU = 1;
 __device__ __forceinline__ void absmax_range(const float* __restrict__ p, int64_t count, int64_t t0,
                                              int64_t stride, uint32_t& m, uint32_t& bad) {
     auto take = [&](float v) __attribute__((always_inline)) {
@@ -81,12 +83,12 @@ __device__ __forceinline__ void absmax_range(const float* __restrict__ p, int64_
     const int64_t nq = (reinterpret_cast<uintptr_t>(p) & 15) == 0 ? count / 4 : 0;
     const f32x4* __restrict__ q = reinterpret_cast<const f32x4*>(p);
     int64_t i = t0;
-    for (; i + 3 * stride < nq; i += 4 * stride) {
-        f32x4 v[4];
+    for (; i + (kAbsLoads - 1) * stride < nq; i += kAbsLoads * stride) {
+        f32x4 v[kAbsLoads];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = __builtin_nontemporal_load(q + i + r * stride);
+        for (int r = 0; r < kAbsLoads; ++r) v[r] = __builtin_nontemporal_load(q + i + r * stride);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
+        for (int r = 0; r < kAbsLoads; ++r) {
             take(v[r].x);
             take(v[r].y);
             take(v[r].z);
@@ -147,6 +149,32 @@ __global__ __launch_bounds__(256) void k_init_buffers(ZeroRanges z) {
         st.tol_n = z.tol_n;
         *z.st = st;
     }
+}
+
+// Fixed-point scales from the largest |x| and |c0|.  Coordinate sums:
+// |x * 2^S| <= 2^50 per value and n * max|x| * 2^S <= 2^61 overall, so every
+// image is exact and no sum can overflow.  Inertia: every squared distance
+// is at most d * (2 max(|x|, |c|))^2, with the same two limits.
+__global__ void k_set_scales(IterState* st, const uint32_t* absmax, int64_t n, int32_t d, int unit) {
+    if (threadIdx.x != 0) return;
+    const float xmax = __uint_as_float(absmax[0]);
+    const float cmax = unit ? 1.0f : __uint_as_float(absmax[2]);
+    int lgn = 0;
+    while (lgn < 64 && (1ull << lgn) < (uint64_t)n) ++lgn;
+    int ex = 0;
+    if (xmax > 0.f) (void)frexp((double)xmax, &ex);   // xmax <= 2^ex
+    int S = 61 - lgn - ex;
+    if (S > 50 - ex) S = 50 - ex;
+    const double amax = xmax > cmax ? (double)xmax : (double)cmax;
+    const double dmax = (double)d * 4.0 * amax * amax;
+    int eD = 0;
+    if (dmax > 0.0) (void)frexp(dmax, &eD);
+    int SI = 61 - lgn - eD;
+    if (SI > 50 - eD) SI = 50 - eD;
+    st->qscale = ldexp(1.0, S);
+    st->qinv = ldexp(1.0, -S);
+    st->iscale = ldexp(1.0, SI);
+    st->iinv = ldexp(1.0, -SI);
 }
 
 __global__ void k_set_centroids(const float* __restrict__ C0, double* C64, float* C32, float* ec,
@@ -520,7 +548,8 @@ __device__ inline void klane_survivors(const ScanCtx& W, const float* hl, int ns
 // path's.
 
 template <int D, int KB>
-__global__ __launch_bounds__(KB == 4 ? 512 : 256) __attribute__((amdgpu_waves_per_eu(2))) void k_assign(Dev P) {
+__global__ __launch_bounds__(KB == 4 ? 512 : 256) __attribute__((amdgpu_waves_per_eu(2))) void k_assign(Dev P_) {
+    const Dev P = with_scales(P_);
     constexpr bool ELK = KB == 8;          // Elkan's lower bounds, vector scan
     constexpr int MB = ELK ? 0 : KB;       // 32-centroid blocks of the matrix-core path
     constexpr bool WIDE = KB == 4;         // 512 threads, centroid operands in LDS
@@ -1144,7 +1173,8 @@ __global__ __launch_bounds__(256) void k_reduce(Dev P) {
 // rounding error.  Block 0 also closes the iteration: counters, history
 // record, step count and the stop test.  Leaves total[] zero.
 
-__global__ __launch_bounds__(64) void k_update(Dev P) {
+__global__ __launch_bounds__(64) void k_update(Dev P_) {
+    const Dev P = with_scales(P_);
     IterState* st = P.st;
     if (!st->active) return;
     const int j = blockIdx.x, d = P.d, k = P.k;
@@ -1263,14 +1293,19 @@ const void* assign_kernel_symbol(int variant) {
 
 hipError_t launch_absmax(const float* a, int64_t na, const float* b, int64_t nb, int cus, uint32_t* out,
                          hipStream_t s) {
-    // a (X): up to 8 blocks per CU, each lane with 16 values per round; b (C0): a few blocks.
+    // a (X): up to kAbsBlocksPerCU blocks per CU; b (C0): a few blocks.
     int64_t ba = (na + 4 * 4 * 256 - 1) / (4 * 4 * 256);
-    if (ba > 8 * (int64_t)cus) ba = 8 * (int64_t)cus;
+    if (ba > kAbsBlocksPerCU * (int64_t)cus) ba = kAbsBlocksPerCU * (int64_t)cus;
     if (ba < 1) ba = 1;
     int64_t bb = (nb + 4 * 4 * 256 - 1) / (4 * 4 * 256);
     if (bb > 64) bb = 64;
     if (bb < 1) bb = 1;
     hipLaunchKernelGGL(k_absmax, dim3((unsigned)(ba + bb)), dim3(256), 0, s, a, na, b, nb, (int)ba, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_set_scales(IterState* st, const uint32_t* absmax, int64_t n, int32_t d, int unit, hipStream_t s) {
+    hipLaunchKernelGGL(k_set_scales, dim3(1), dim3(64), 0, s, st, absmax, n, d, unit);
     return hipGetLastError();
 }
 

@@ -573,7 +573,8 @@ __global__ __launch_bounds__(256) void k_scatter_large(Dev P, Large Lg) {
 // One block per chunk of <= kLgChunkRows points of one cluster: exact
 // fixed-point coordinate sums (and, with KM_FLAG_STATS, the squared
 // distances to the cluster's current centroid, element by element).
-__global__ __launch_bounds__(256) void k_segsum_large(Dev P, Large Lg) {
+__global__ __launch_bounds__(256) void k_segsum_large(Dev P_, Large Lg) {
+    const Dev P = with_scales(P_);
     if (!P.st->active) return;
     const int c = blockIdx.x;
     const int k = P.k, d = P.d;

@@ -610,7 +610,8 @@ __device__ void step_books(const Dev& P, const Fused& F, int t, float ecmax) {
 // wave's row rho = 16i + l / 4.
 
 template <int KC>
-__global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k_small(Dev P, Fused F, int t) {
+__global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k_small(Dev P_, Fused F, int t) {
+    const Dev P = with_scales(P_);
     IterState* st = P.st;
     if (st->done) {
         if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
@@ -811,8 +812,9 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
 // shared, through atomics.
 
 template <int KC>
-__global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P, Fused F, int t,
+__global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P_, Fused F, int t,
                                                                                       int fused) {
+    const Dev P = with_scales(P_);
     IterState* st = P.st;
     // The wave index is uniform across the wave: held in a scalar register, so
     // that the tile loop below branches on scalars instead of lane masks.
@@ -1017,7 +1019,8 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
 // End of step t as its own launch (one block): after a streaming step, and
 // after an incremental step whose results are needed before the next step
 // (then the next step starts unfused).
-__global__ __launch_bounds__(kTp) void k_small_finish(Dev P, Fused F, int t, int delta) {
+__global__ __launch_bounds__(kTp) void k_small_finish(Dev P_, Fused F, int t, int delta) {
+    const Dev P = with_scales(P_);
     if (!P.st->active) return;   // step t did not run (the run had stopped)
     const float em = eos_finish(P, F, t, eos_load(P, F, t, delta != 0), true, km_smem, nullptr, nullptr);
     if (threadIdx.x == 0) step_books(P, F, t, em);
