@@ -113,10 +113,9 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     float* wg = reinterpret_cast<float*>(km_smem + lay.off_x) + w * kB * XS;       // its staged rows
 
     // Tables of the step.
-    for (int i = tid; i < KP * D; i += kW * 64) {
-        Cs[i] = i < k * D ? P.C32[i] : 0.f;
-        acc[i] = 0;
-    }
+    constexpr int AR = D + 1;   // LDS stride (uint64) of a cluster's sums: one pad word spreads clusters over banks
+    for (int i = tid; i < KP * D; i += kW * 64) Cs[i] = i < k * D ? P.C32[i] : 0.f;
+    for (int i = tid; i < KP * AR; i += kW * 64) acc[i] = 0;
     for (int i = tid; i < KP; i += kW * 64) {
         cn2s[i] = i < k ? P.cn2[i] : INFINITY;
         // -|c|^2 / 2 (exact halving) enters the matrix-core product as one
@@ -373,10 +372,10 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
                 for (int q = 0; q < kHalf; ++q) {
                     const uint64_t v = fixed_bits((double)xh[q], P.qscale);
-                    atomicAdd(reinterpret_cast<unsigned long long*>(acc + b * D + half * kHalf + q),
+                    atomicAdd(reinterpret_cast<unsigned long long*>(acc + b * AR + half * kHalf + q),
                               (unsigned long long)v);
                     if (inc >= 0)
-                        atomicAdd(reinterpret_cast<unsigned long long*>(acc + inc * D + half * kHalf + q),
+                        atomicAdd(reinterpret_cast<unsigned long long*>(acc + inc * AR + half * kHalf + q),
                                   (unsigned long long)(0 - v));
                 }
             }
@@ -487,7 +486,7 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     }
     __syncthreads();
     uint64_t* row = P.part + (int64_t)blockIdx.x * P.L;
-    for (int i = tid; i < k * D; i += kW * 64) row[i] = acc[i];
+    for (int i = tid; i < k * D; i += kW * 64) row[i] = acc[(i / D) * AR + i % D];
     for (int i = tid; i < k; i += kW * 64) row[k * D + i] = (uint64_t)(int64_t)cnt[i];
     if (tid < kNumStat) row[k * D + k + tid] = bst[tid];
 }

@@ -184,6 +184,7 @@ constexpr int kSmallTile = 256;   // threads per block; points per tile of the s
 constexpr int kSmallMaxK = 16;    // the cluster index fits in the 4 low bits of the point state
 constexpr int kSmallCopies = 4;   // copies of the LDS sums (spread rows over banks and addresses)
 constexpr int kSmallRowStride = 20;   // padded LDS row stride (floats) of centroid and queued rows
+constexpr int kSmallAccRow = 17;      // LDS stride (uint64) of one cluster's 16 fixed-point sums
 
 // Accumulation rows of a streaming step: block b adds its partial row into
 // row b % kSmallRows of the step's slot with device atomics; the end of the
@@ -253,7 +254,10 @@ __host__ __device__ inline SmallLds small_lds(int k, bool staged) {
         return r;
     };
     const int q = staged ? kSmallQ : kIncQ;
-    L.csu = 16 * k + 1;   // odd: the copies start on different banks
+    // Cluster rows of kSmallAccRow uint64 (16 sums and one pad word), so that
+    // the same coordinate of different clusters falls on different banks;
+    // odd: the copies start on different banks.
+    L.csu = kSmallAccRow * k + 1;
     L.kp = k + 1;
     L.off_c = take(4 * k * kSmallRowStride, 16);
     L.off_h = take(4 * k * kSmallMaxK, 16);   // rows padded to kSmallMaxK (16-byte row loads)
@@ -404,7 +408,7 @@ __host__ __device__ inline IncMMLds inc_mm_lds(int D, int KB) {
     L.off_dup = take(4 * kIMMaxK);
     L.off_hm = take(4 * kIMMaxK * 4);                    // min half-distance from a cluster to each block
     L.off_nb = take(4 * kp);                             // -|c|^2 / 2 of each centroid (-huge for padding)
-    L.off_acc = take(8 * kp * D);                        // fixed-point sums of the moves
+    L.off_acc = take(8 * kp * (D + 1));                  // fixed-point sums of the moves (rows of D + 1)
     L.off_cnt = take(4 * kp);
     L.off_misc = take(64);                               // tile counter at 0, kNumStat uint64 counters at 16
     L.off_q = take(kIMWaves * 2 * inc_mm_queues(KB) * kIMQcap * 4);   // per wave: queues of (point, state)

@@ -174,7 +174,7 @@ struct Tables {
     float* ec;     // k: float32 rounding error of each centroid, rounded up
     float* ddn;    // k: cumulative drift, rounded down
     float* cn;     // k: squared norms of the float32 centroids (float32 of the float64 sum)
-    uint64_t* acc; // kCopies copies (stride csu) of the k x 16 fixed-point sums
+    uint64_t* acc; // kCopies copies (stride csu) of the k rows (stride kSmallAccRow) of 16 fixed-point sums
     uint32_t* cnt; // kCopies copies of the k counts (stride kp)
     int* qc;       // three queue counters
     uint64_t* bst; // kNumStat block counters
@@ -372,8 +372,8 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
     if (fl.first) {
         *first_b = b;   // the caller adds the row to the sums of b
     } else if (b != inc) {
-        add_row(T.acc + cp * T.csu + b * kD, x, P.qscale, false);
-        add_row(T.acc + cp * T.csu + inc * kD, x, P.qscale, true);
+        add_row(T.acc + cp * T.csu + b * kSmallAccRow, x, P.qscale, false);
+        add_row(T.acc + cp * T.csu + inc * kSmallAccRow, x, P.qscale, true);
         atomicAdd(&T.cnt[cp * T.kp + b], 1u);
         atomicAdd(&T.cnt[cp * T.kp + inc], 0xFFFFFFFFu);
     }
@@ -403,7 +403,7 @@ __device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const 
     for (int i = tid; i < k * kD; i += nt) {
         uint64_t v = 0;
 #pragma unroll
-        for (int c = 0; c < kCopies; ++c) v += T.acc[c * T.csu + i];
+        for (int c = 0; c < kCopies; ++c) v += T.acc[c * T.csu + (i / kD) * kSmallAccRow + i % kD];
         if (v || !skip_zero) atomicAdd(row + i, (unsigned long long)v);
     }
     for (int i = tid; i < k; i += nt) {
@@ -678,7 +678,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
                 const int b = qa[e];
                 const f32x4 v = *reinterpret_cast<const f32x4*>(qr + e * kCR + 4 * q);
                 const int cp = slot & (kCopies - 1);
-                uint64_t* dst = T.acc + cp * T.csu + b * kD + 4 * q;
+                uint64_t* dst = T.acc + cp * T.csu + b * kSmallAccRow + 4 * q;
                 atomicAdd(reinterpret_cast<unsigned long long*>(dst + 0),
                           (unsigned long long)fixed_bits((double)v.x, P.qscale));
                 atomicAdd(reinterpret_cast<unsigned long long*>(dst + 1),
@@ -721,7 +721,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
                 const int ar = __shfl(a_old, rho);
                 if (64 * w + rho < rows) {
                     const int cp = rho & (kCopies - 1);
-                    uint64_t* dst = T.acc + cp * T.csu + ar * kD + 4 * q;
+                    uint64_t* dst = T.acc + cp * T.csu + ar * kSmallAccRow + 4 * q;
                     atomicAdd(reinterpret_cast<unsigned long long*>(dst + 0),
                               (unsigned long long)fixed_bits((double)xb[i].x, P.qscale));
                     atomicAdd(reinterpret_cast<unsigned long long*>(dst + 1),
