@@ -280,8 +280,9 @@ def main() -> int:
     ap.add_argument("--kmeanspp", action="store_true",
                     help="time k-means++ seeding of the workload's k seeds instead of the k-means steps")
     ap.add_argument("--profile", action="store_true",
-                    help="run only the warmup and the timed region (no event pass, no job run, no "
-                         "CPU leg), so a profiler sees warmup + K launches of each kernel")
+                    help="for a profiler: the warmup runs, then K contexts that each run exactly the "
+                         "workload's T iterations (no launches past the stop, no event pass, no CPU "
+                         "leg); prints T and the path")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run 5 plain device-to-device copies of 512 MiB (reference kernel "
                          "for scaling hardware byte counters)")
@@ -310,6 +311,8 @@ def main() -> int:
 
     w = synth.WORKLOADS[args.workload]
     K = args.steps or 20
+    if args.profile:
+        args.no_cpu_baseline = True
     log("workload %s: n=%d d=%d k=%d; generating" % (w.name, w.n, w.d, w.k))
     X, C0, _ = synth.make(w.name)
     if args.kmeanspp:
@@ -320,8 +323,6 @@ def main() -> int:
     Cg = torch.from_numpy(C0).to(dev)
     torch.cuda.synchronize()
 
-    if args.profile:
-        args.no_cpu_baseline = True
     base_flags = {"full_sums": True} if args.full_sums else {}
     if args.spherical:
         base_flags["spherical"] = True
@@ -338,6 +339,22 @@ def main() -> int:
         job()
     torch.cuda.synchronize()
     log("warmup done (%d runs)" % args.warmup)
+
+    if args.profile:
+        # K contexts of exactly the run's T steps: each kernel's dispatches
+        # are then T per context (the first step first), in order.
+        T = job()[2]["iterations"]
+        torch.cuda.synchronize()
+        for _ in range(K):
+            with km.KMeansMTI(Xg, Cg, **base_flags) as pctx:
+                path = pctx.path()
+                for _ in range(T):
+                    pctx.iterate()
+                pctx.get()
+        torch.cuda.synchronize()
+        print(json.dumps({"profile": True, "workload": w.name, "contexts": K, "iterations": T, "path": path}),
+              flush=True)
+        return 0
 
     # Timed region: K whole runs of the workload as it is defined (from the
     # seeded centroids until fewer than tol * n points change, or max_iters),
