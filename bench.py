@@ -47,6 +47,7 @@ DOMINANT_KERNEL = {"stream-d16": "k_inc", "stream-d16-full": "k_small", "lds-vec
 KERNEL_SOURCES = {
     "k_small": ["km_small.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
     "k_inc": ["km_small.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
+    "k_first": ["km_small.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
     "k_assign": ["km_kernels.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
     "k_inc_mm": ["km_incmm.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
     "k_mfma_large": ["km_large.hip", "km_device.h", "km_internal.h", "km_capi.hip"],
@@ -442,7 +443,8 @@ def main() -> int:
         # The first step (no bounds yet): every row read and every point's
         # assignment and bound written; on the global path every point's k
         # distances go through the matrix cores.
-        first_kernel = "k_small" if path.startswith("stream") else kernel
+        # (the stream path's first step runs in k_first unless statistics are gathered)
+        first_kernel = "k_first" if path.startswith("stream") else kernel
         if path == "global-mfma":
             rooflines.append(mfma_roofline_entry(first_kernel, tag + "-first-step", 2.0 * d * k * n,
                                                  first_t["assign_ms"], "first step: 2*d*k per point"))

@@ -187,6 +187,7 @@ struct km_ctx {
     bool incmm = false;   // incremental matrix-core step (d = 16 or 32, k <= 128)
     int gim = 0, lds_im = 0;   // its grid and LDS
     int gi = 0, lds_inc = 0;   // grid and LDS of the incremental kernel
+    int gf = 0, lds_first = 0;  // grid and LDS of the matrix-core first step (0: k_small runs it)
     int64_t enq = 0;      // steps enqueued so far
     km::Fused fz{};
     km::Large lg{};
@@ -311,8 +312,9 @@ int enqueue_iteration(km_ctx* c) {
         km::Dev dv = c->dv;
         dv.C64 = c->fz.c64 + (size_t)km::slot2(t) * c->k * c->d;   // C^t
         const bool inc = c->inc && t > 0;
-        e = inc ? km::launch_inc(dv, c->fz, c->gi, c->lds_inc, t, c->pending ? 1 : 0, c->stream)
-                : km::launch_small(dv, c->fz, c->lds, t, c->stream);
+        e = inc                 ? km::launch_inc(dv, c->fz, c->gi, c->lds_inc, t, c->pending ? 1 : 0, c->stream)
+            : t == 0 && c->gf ? km::launch_first(dv, c->fz, c->gf, c->lds_first, t, c->stream)
+                              : km::launch_small(dv, c->fz, c->lds, t, c->stream);
         if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "streaming step kernel"));
         if ((e = mark(1)) != hipSuccess || (e = mark(2)) != hipSuccess)
             return fail_ctx(c, hip_fail(e, "hipEventRecord"));
@@ -423,6 +425,20 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         if (G > ntiles) G = ntiles;
         v.G = (int32_t)G;
         c->inc = !(c->flags & (KM_FLAG_FULL_SUMS | KM_FLAG_STATS));
+        if (!(c->flags & KM_FLAG_STATS)) {
+            // The first step on the matrix cores (no inertia to sum): resident
+            // blocks, at most one 64-point tile per wave.
+            c->lds_first = km::first_lds_bytes(k);
+            int per_cu_f = 0;
+            if (c->lds_first > max_lds) return KM_ERR_UNSUPPORTED;
+            if ((rcc = kernel_config(c->device, km::first_kernel_symbol(k), c->tp, c->lds_first, &per_cu_f)) != KM_OK)
+                return rcc;
+            if (per_cu_f < 1) return KM_ERR_UNSUPPORTED;
+            const int64_t want = ((n + 63) / 64 + 3) / 4;
+            int64_t gf = (int64_t)per_cu_f * cus;
+            if (gf > want) gf = want > 0 ? want : 1;
+            c->gf = (int)gf;
+        }
         if (c->inc) {
             c->lds_inc = km::inc_lds_bytes(k);
             if (c->lds_inc > max_lds) return KM_ERR_UNSUPPORTED;

@@ -240,11 +240,12 @@ struct SmallLds {
     int off_c, off_h, off_s, off_ec, off_du, off_dd, off_cn, off_acc, off_cnt, off_qr, off_qp, off_qa, off_misc,
         off_c64, bytes;
     int csu, kp;          // stride (uint64) of one copy of the sums; of one copy of the counts
+    int copies;           // copies of the sums and counts
 };
 
 // Dynamic LDS layout of the streaming (staged = true: queued rows kept in
 // LDS) and incremental (staged = false: one batch of gathered rows) kernels.
-__host__ __device__ inline SmallLds small_lds(int k, bool staged) {
+__host__ __device__ inline SmallLds small_lds(int k, bool staged, bool queue = true) {
     SmallLds L;
     int o = 0;
     auto take = [&](int bytes, int align) {
@@ -266,15 +267,22 @@ __host__ __device__ inline SmallLds small_lds(int k, bool staged) {
     L.off_du = take(4 * k, 16);
     L.off_dd = take(4 * k, 16);
     L.off_cn = take(4 * k, 16);
-    L.off_acc = take(8 * kSmallCopies * L.csu, 16);
-    L.off_cnt = take(4 * kSmallCopies * L.kp, 16);
+    // (the first step, whose rows all go to the sums, spreads them over twice
+    // as many copies)
+    L.copies = queue ? kSmallCopies : 2 * kSmallCopies;
+    L.off_acc = take(8 * L.copies * L.csu, 16);
+    L.off_cnt = take(4 * L.copies * L.kp, 16);
     // Queued rows (streaming kernel) or one gathered batch (incremental kernel).
-    L.off_qr = take(4 * (staged ? kSmallQ : 64 * kIncWaves) * kSmallRowStride, 16);
-    L.off_qp = take(4 * q, 16);
-    L.off_qa = take(4 * q, 16);
+    // Without a queue (the matrix-core first step): per wave of the block, 64
+    // rows of products and partial norms and 64 cluster words.
+    L.off_qr = take(queue ? 4 * (staged ? kSmallQ : 64 * kIncWaves) * kSmallRowStride
+                          : 4 * (kSmallTile / 64) * (64 * kSmallRowStride + 64),
+                    16);
+    L.off_qp = take(queue ? 4 * q : 0, 16);
+    L.off_qa = take(queue ? 4 * q : 0, 16);
     L.off_misc = take(64, 16);   // three queue counters (int) at 0, kNumStat uint64 counters at 16
     // Incremental kernel: the float64 centroids of near-tie decisions.
-    L.off_c64 = take(staged ? 0 : 8 * k * 16, 16);
+    L.off_c64 = take(staged || !queue ? 0 : 8 * k * 16, 16);
     L.bytes = (o + 15) / 16 * 16;
     return L;
 }
@@ -291,6 +299,11 @@ int inc_lds_bytes(int k);
 int small_finish_lds_bytes(int k);
 // Step t of the streaming kernel (dv.C64 = the slot of C^t).
 hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, int t, hipStream_t s);
+// The first step without statistics on the matrix cores (k_first): LDS bytes,
+// kernel symbol (occupancy query) and launch on `grid` blocks of kSmallTile.
+int first_lds_bytes(int k);
+const void* first_kernel_symbol(int k);
+hipError_t launch_first(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, hipStream_t s);
 // Step t of the incremental kernel.  fused: the end of step t - 1 (an
 // incremental step of the same grid) has not run; every block computes it
 // first and block 0 stores it.  Else dv.C64 = the slot of C^t.

@@ -174,11 +174,11 @@ struct Tables {
     float* ec;     // k: float32 rounding error of each centroid, rounded up
     float* ddn;    // k: cumulative drift, rounded down
     float* cn;     // k: squared norms of the float32 centroids (float32 of the float64 sum)
-    uint64_t* acc; // kCopies copies (stride csu) of the k rows (stride kSmallAccRow) of 16 fixed-point sums
-    uint32_t* cnt; // kCopies copies of the k counts (stride kp)
+    uint64_t* acc; // copies (stride csu) of the k rows (stride kSmallAccRow) of 16 fixed-point sums
+    uint32_t* cnt; // copies of the k counts (stride kp)
     int* qc;       // three queue counters
     uint64_t* bst; // kNumStat block counters
-    int csu, kp;
+    int csu, kp, copies;
 };
 
 // Table pointers into LDS, and the block's sums and counters cleared.
@@ -195,11 +195,12 @@ __device__ __forceinline__ Tables table_ptrs(const Dev& P, const SmallLds& lay) 
     T.qc = reinterpret_cast<int*>(km_smem + lay.off_misc);
     T.bst = reinterpret_cast<uint64_t*>(km_smem + lay.off_misc + 16);
     T.csu = lay.csu;
+    T.copies = lay.copies;
     T.kp = lay.kp;
     const int tid = threadIdx.x;
     const int nt = (int)blockDim.x;
-    for (int i = tid; i < kCopies * T.csu; i += nt) T.acc[i] = 0;
-    for (int i = tid; i < kCopies * T.kp; i += nt) T.cnt[i] = 0;
+    for (int i = tid; i < T.copies * T.csu; i += nt) T.acc[i] = 0;
+    for (int i = tid; i < T.copies * T.kp; i += nt) T.cnt[i] = 0;
     if (tid < kNumStat) T.bst[tid] = 0;
     if (tid < 3) T.qc[tid] = 0;
     return T;
@@ -250,6 +251,44 @@ __device__ __forceinline__ float centroid_norm_max(const Tables& T, int k) {
     float m2 = 0.f;
     for (int j = 0; j < k; ++j) m2 = fmaxf(m2, T.cn[j]);
     return sqrtf(m2) * kUp * kUp;
+}
+
+// The nearest of the candidate centroids (bits of cmask) on their
+// direct-form distances, in ascending index: the incumbent wins an exact tie,
+// then the lower index; a near tie is decided again in float64 against the
+// master centroids.  Db and ub become the winner's squared distance and
+// distance bound.
+__device__ __forceinline__ int decide_direct(const Tables& T, const StepFlags& fl, const double* C64,
+                                             const float (&x)[kD], int k, int inc, uint32_t cmask, float& Db,
+                                             float& ub, Counters& cn) {
+    float d2 = INFINITY;
+    int rk1 = INT_MAX;
+    int b = 0;
+    Db = INFINITY;
+    while (cmask) {
+        const int j = __builtin_ctz(cmask);
+        cmask &= cmask - 1;
+        const float dj = sqd_row(x, T.C + j * kCR);
+        const int rk = j == inc ? -1 : j;
+        if (dj < Db || (dj == Db && rk < rk1)) {
+            d2 = Db;
+            Db = dj;
+            rk1 = rk;
+            b = j;
+        } else if (dj < d2) {
+            d2 = dj;
+        }
+    }
+    ub = bound_of(Db, T.ec[b], fl.gamma);
+    if (d2 != INFINITY) {
+        const float band = 2.f * fl.gamma * (Db + d2) + 4.f * (sqrt_up(Db) + sqrt_up(d2)) * fl.ecmax +
+                           8.f * fl.ecmax * fl.ecmax;
+        if (d2 - Db <= band) {   // near tie: float64 decision, the oracle's tie rule
+            b = recheck64(x, C64, k, inc, Db, ub);
+            cn.rc += 1;
+        }
+    }
+    return b;
 }
 
 // One survivor, row x in registers: its assignment, the new state word and,
@@ -310,6 +349,7 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
     uint32_t cmask = 0;
 #pragma unroll
     for (int j = 0; j < KC; ++j) cmask |= (V[j] <= lim ? 1u : 0u) << j;
+    cmask &= (1u << k) - 1u;   // (an infinite minimum would admit the slots past k)
     int b;
     float Db, ub;
     if (__popc(cmask) == 1 && !fl.want_inertia) {
@@ -317,36 +357,7 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
         Db = vmin;
         ub = sqrt_up(fmaxf(vmin + E, 0.f)) * kUp;
     } else {
-        // Direct-form distances of the candidates, in ascending index; the
-        // incumbent wins an exact tie, then the lower index.
-        float d2 = INFINITY;
-        int rk1 = INT_MAX;
-        b = 0;
-        Db = INFINITY;
-        uint32_t cm = cmask;
-        while (cm) {
-            const int j = __builtin_ctz(cm);
-            cm &= cm - 1;
-            const float dj = sqd_row(x, T.C + j * kCR);
-            const int rk = j == inc ? -1 : j;
-            if (dj < Db || (dj == Db && rk < rk1)) {
-                d2 = Db;
-                Db = dj;
-                rk1 = rk;
-                b = j;
-            } else if (dj < d2) {
-                d2 = dj;
-            }
-        }
-        ub = bound_of(Db, T.ec[b], fl.gamma);
-        if (d2 != INFINITY) {
-            const float band = 2.f * fl.gamma * (Db + d2) + 4.f * (sqrt_up(Db) + sqrt_up(d2)) * fl.ecmax +
-                               8.f * fl.ecmax * fl.ecmax;
-            if (d2 - Db <= band) {   // near tie: float64 decision, the oracle's tie rule
-                b = recheck64(x, C64, k, inc, Db, ub);
-                cn.rc += 1;
-            }
-        }
+        b = decide_direct(T, fl, C64, x, k, inc, cmask, Db, ub, cn);
     }
     // The MTI scan's count of distances.
     uint32_t nc = (uint32_t)k;
@@ -403,13 +414,13 @@ __device__ __forceinline__ void flush_block(const Dev& P, const Fused& F, const 
     for (int i = tid; i < k * kD; i += nt) {
         uint64_t v = 0;
 #pragma unroll
-        for (int c = 0; c < kCopies; ++c) v += T.acc[c * T.csu + (i / kD) * kSmallAccRow + i % kD];
+        for (int c = 0; c < T.copies; ++c) v += T.acc[c * T.csu + (i / kD) * kSmallAccRow + i % kD];
         if (v || !skip_zero) atomicAdd(row + i, (unsigned long long)v);
     }
     for (int i = tid; i < k; i += nt) {
         uint32_t v = 0;
 #pragma unroll
-        for (int c = 0; c < kCopies; ++c) v += T.cnt[c * T.kp + i];
+        for (int c = 0; c < T.copies; ++c) v += T.cnt[c * T.kp + i];
         // A count change is a 32-bit two's-complement value (moves may be negative).
         if (v || !skip_zero) atomicAdd(row + k * kD + i, (unsigned long long)(int64_t)(int32_t)v);
     }
@@ -800,6 +811,174 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(3))) void k
 }
 
 // ---------------------------------------------------------------------------
+// The first step without statistics (no bounds yet: every point is scanned
+// over all k centroids and adds its row to its new cluster's sums).  A wave
+// takes 64-point tiles, four groups of 16 points.  The dot products of a
+// group are a dense 16 x 16 x 16 product on the matrix cores
+// (v_mfma_f32_16x16x4f32, four steps of four coordinates): lane
+// l = 16 qd + pl loads chunk qd (coordinates 4qd .. 4qd+3) of point pl of the
+// group, a coalesced kilobyte per group, and supplies coordinate 4qd + s at
+// step s as the B operand; the A operand is coordinate 4qd + s of centroid pl
+// (zero rows past k).  The lane then holds the dot products of point pl with
+// centroids 4qd .. 4qd+3 and the partial squared norm of its chunk; through
+// a wave-private LDS tile (one 16-byte store per group, four 16-byte loads),
+// lane l gathers the k dot products and four partial norms of point l of
+// the tile, and decides it alone: the expanded-form values, their minimum,
+// and the candidates within twice the error bound E of the minimum (as in
+// settle_survivor).  A single candidate is the nearest centroid; a point of
+// several candidates reads its row and is decided on the direct-form
+// distances (float64 for a near tie).  The clusters go back through LDS to
+// the lanes that hold the rows, which add their chunks to the sums of the
+// points' clusters.  Two tiles of loads are in flight per wave.
+template <int KC>
+__global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k_first(Dev P_, Fused F, int t) {
+    const Dev P = with_scales(P_);
+    IterState* st = P.st;
+    if (st->done) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
+        return;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 1;
+
+    const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+    const int pl = lane & 15, qd = lane >> 4;
+    StepFlags fl{true, true, false, P.gamma, st->ec_max, 0.f};
+    const SmallLds lay = small_lds(P.k, false, false);
+    const Tables T = load_tables(P, F, lay, t);
+    clear_next_slots(P, F, t);
+    // Wave-private tile: 64 rows of kCR floats (16 dot products, 4 partial
+    // norms), then 64 cluster words ordered [pl][group].
+    float* dt = reinterpret_cast<float*>(km_smem + lay.off_qr) + w * (64 * kCR + 64);
+    int* bt = reinterpret_cast<int*>(dt + 64 * kCR);
+    __syncthreads();
+    fl.cnmax = centroid_norm_max(T, P.k);
+    const int k = P.k;
+
+    float a[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) a[s] = pl < k ? T.C[pl * kCR + 4 * qd + s] : 0.f;
+
+    Counters cn;
+    const int64_t n = P.n;
+    const int64_t ntiles = (n + 63) / 64;
+    const int64_t nw = 4 * (int64_t)gridDim.x;
+    const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
+
+    f32x4 xA[4], xB[4];   // [g]: chunk qd of point 16g + pl of the tile
+    auto prefetch = [&](f32x4 (&xb)[4], int64_t tl) __attribute__((always_inline)) {
+        if (tl >= ntiles) return;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int64_t row = min(tl * 64 + 16 * g + pl, n - 1);
+            xb[g] = __builtin_nontemporal_load(X4 + row * kQD + qd);
+        }
+    };
+    auto wave_sync = []() __attribute__((always_inline)) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+
+    auto tile_body = [&](f32x4 (&xb)[4], int64_t tl) __attribute__((always_inline)) {
+        const int64_t base = tl * 64;
+        // 1. Products and partial norms of the four groups into the tile.
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const f32x4 xv = xb[g];
+            f32x4 dot = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], xv.x, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            dot = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], xv.y, dot, 0, 0, 0);
+            dot = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], xv.z, dot, 0, 0, 0);
+            dot = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], xv.w, dot, 0, 0, 0);
+            float* row = dt + (16 * g + pl) * kCR;
+            *reinterpret_cast<f32x4*>(row + 4 * qd) = dot;
+            row[16 + qd] = fmaf(xv.x, xv.x, fmaf(xv.y, xv.y, fmaf(xv.z, xv.z, xv.w * xv.w)));
+        }
+        wave_sync();
+        // 2. Point `lane` of the tile, decided by its own lane.
+        const float* row = dt + lane * kCR;
+        const f32x4 pn = *reinterpret_cast<const f32x4*>(row + 16);
+        const float x2 = ((pn.x + pn.y) + pn.z) + pn.w;
+        float V[KC];
+        float vmin = INFINITY;
+#pragma unroll
+        for (int j = 0; j < KC; j += 4) {
+            const f32x4 dv = *reinterpret_cast<const f32x4*>(row + j);
+            const f32x4 cv = *reinterpret_cast<const f32x4*>(T.cn + j);
+            const float dd[4] = {dv.x, dv.y, dv.z, dv.w};
+            const float cc[4] = {cv.x, cv.y, cv.z, cv.w};
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                if (j + r < KC) {
+                    V[j + r] = j + r < k ? fmaf(-2.f, dd[r], x2 + cc[r]) : INFINITY;
+                    vmin = fminf(vmin, V[j + r]);
+                }
+            }
+        }
+        const float R = sqrtf(x2) * (1.0f + 0x1p-20f) + fl.cnmax;
+        const float E = (kExpGamma * R * R + 4.f * R * fl.ecmax + 2.f * fl.ecmax * fl.ecmax) * kUp;
+        const float lim = vmin + 2.f * E;
+        uint32_t cm = 0;
+#pragma unroll
+        for (int j = 0; j < KC; ++j) cm |= (V[j] <= lim ? 1u : 0u) << j;
+        cm &= (1u << k) - 1u;   // (an infinite minimum would admit the slots past k)
+        int b = cm ? __builtin_ctz(cm) : 0;
+        float ub = sqrt_up(fmaxf(vmin + E, 0.f)) * kUp;
+        const bool valid = base + lane < n;
+        if (__popc(cm) != 1 && valid) {   // rare: several candidates (none: a row that is not finite)
+            float x[kD];
+#pragma unroll
+            for (int m = 0; m < kQD; ++m) {
+                const f32x4 v = X4[(base + lane) * kQD + m];
+                x[4 * m] = v.x;
+                x[4 * m + 1] = v.y;
+                x[4 * m + 2] = v.z;
+                x[4 * m + 3] = v.w;
+            }
+            float Db;
+            b = decide_direct(T, fl, P.C64, x, k, -1, cm, Db, ub, cn);
+        }
+        if (valid) {
+            F.w[base + lane] = settle_state(ub, T.ddn[b], b);
+            atomicAdd(&T.cnt[(lane & (2 * kCopies - 1)) * T.kp + b], 1u);
+            cn.changed += 1;
+            cn.comp += (uint32_t)k;
+        }
+        bt[(lane & 15) * 4 + (lane >> 4)] = b;
+        wave_sync();
+        // 3. The rows into the sums of their clusters, by the lanes that hold them.
+        const int4 bs = *reinterpret_cast<const int4*>(bt + pl * 4);
+        const int bb[4] = {bs.x, bs.y, bs.z, bs.w};
+        const int cp = pl & (2 * kCopies - 1);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            if (base + 16 * g + pl < n) {
+                const f32x4 xv = xb[g];
+                unsigned long long* dst =
+                    reinterpret_cast<unsigned long long*>(T.acc + cp * T.csu + bb[g] * kSmallAccRow + 4 * qd);
+                atomicAdd(dst + 0, (unsigned long long)fixed_bits((double)xv.x, P.qscale));
+                atomicAdd(dst + 1, (unsigned long long)fixed_bits((double)xv.y, P.qscale));
+                atomicAdd(dst + 2, (unsigned long long)fixed_bits((double)xv.z, P.qscale));
+                atomicAdd(dst + 3, (unsigned long long)fixed_bits((double)xv.w, P.qscale));
+            }
+        }
+        wave_sync();   // the tile is read before the next one is written
+    };
+
+    const int64_t w0 = 4 * (int64_t)blockIdx.x + w;
+    prefetch(xA, w0);
+    prefetch(xB, w0 + nw);
+    for (int64_t tl = w0; tl < ntiles; tl += 2 * nw) {
+        tile_body(xA, tl);
+        prefetch(xA, tl + 2 * nw);
+        if (tl + nw < ntiles) {
+            tile_body(xB, tl + nw);
+            prefetch(xB, tl + 3 * nw);
+        }
+    }
+    flush_block(P, F, T, cn, false, t);
+}
+
+// ---------------------------------------------------------------------------
 // The incremental kernel (steps after the first).  Block b owns an equal
 // share of the tiles of kIncWaveTile points; its waves take them one at a time
 // from an LDS counter until none is left (the GPU form of the paper's work
@@ -1068,6 +1247,29 @@ const void* inc_kernel_symbol(int k) {
 }
 
 int small_lds_bytes(int k) { return small_lds(k, true).bytes; }
+
+int first_lds_bytes(int k) { return small_lds(k, false, false).bytes; }
+
+const void* first_kernel_symbol(int k) {
+    switch (small_kc(k)) {
+#define KM_SYM(KC_) \
+    case KC_: return reinterpret_cast<const void*>(&k_first<KC_>);
+        KM_SMALL_KCS(KM_SYM)
+#undef KM_SYM
+        default: return nullptr;
+    }
+}
+
+hipError_t launch_first(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, hipStream_t s) {
+    switch (small_kc(dv.k)) {
+#define KM_LAUNCH(KC_) \
+    case KC_: hipLaunchKernelGGL((k_first<KC_>), dim3(grid), dim3(kTp), lds_bytes, s, dv, F, t); break;
+        KM_SMALL_KCS(KM_LAUNCH)
+#undef KM_LAUNCH
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
 
 int inc_lds_bytes(int) { return small_lds(kSmallMaxK, false).bytes; }
 

@@ -86,6 +86,33 @@ def test_stream_paths_are_bitwise_identical_to_generic_path(case, prune):
         assert (hists[0]["computed"] == n * k).all()
 
 
+def test_first_step_exact_ties_take_the_lowest_index():
+    # Every other row lies on the bisector of c0 and c1 (their only difference
+    # is the sign of coordinate 0, which is 0 in those rows): exact ties in
+    # float32 and float64.  The matrix-core first step finds both centroids
+    # inside its candidate band, decides those rows on their direct-form
+    # distances and in float64, and must give the oracle's lowest index; the
+    # rows are spread over many 64-point tiles with a ragged end.
+    rng = np.random.default_rng(120)
+    n, k = 9000 + 21, 7
+    C0 = rng.uniform(-30.0, 30.0, size=(k, 16)).astype(np.float32)
+    C0[1] = C0[0]
+    C0[0, 0], C0[1, 0] = 2.0, -2.0
+    X = (C0[rng.integers(0, k, n)] + rng.integers(-3, 4, size=(n, 16))).astype(np.float32)
+    X[::2] = C0[0] + rng.integers(-3, 4, size=(len(X[::2]), 16)).astype(np.float32)
+    X[::2, 0] = 0.0
+    ref = oracle.lloyd(X, C0, 1, 0.0)
+    tied = (X[:, 0] == 0.0) & (ref["assign"] == 0)
+    assert tied.sum() > n // 4
+    with km.KMeansMTI(_gpu(X), _gpu(C0)) as ctx:
+        assert ctx.path() == "stream-d16"
+        ctx.iterate()
+        a, _ = ctx.get(centroids=False)
+        np.testing.assert_array_equal(a.cpu().numpy(), ref["assign"])
+        np.testing.assert_allclose(ctx.centroids64(), ref["C"], rtol=1e-12, atol=1e-12)
+        assert ctx.history()["rechecks"][0] >= tied.sum()
+
+
 def test_incremental_trajectory_every_step_matches_oracle():
     X, C0 = synth.blobs(70000 + 9, 16, 12, seed=112, spread=3.0, sigma=1.5)
     T = 15
