@@ -120,6 +120,150 @@ __global__ __launch_bounds__(256) void k_bound_large(Dev P, Large Lg) {
                   (unsigned long long)c1);
 }
 
+// Refinement of survivor c of a tile (entry s0 + c of the survivor list) by
+// a thread pair (part 0 and 1, each over half of the dimensions) from the
+// survivor's 16 candidate slots (candD, candJ: 4 lists of 4) and its squared
+// norm x2: the candidates within twice the expanded form's error bound of the
+// smallest are re-evaluated in the direct form, followed by the float64
+// near-tie rule; the point's assignment and bound are written.
+template <bool VEC>
+__device__ __forceinline__ void refine_survivor(const Dev& P, const Large& Lg, const float* candD, const int* candJ,
+                                                int s0, int c, int part, bool first, float x2, float cnmax,
+                                                float gexp, float ecm, float gamma, uint64_t& my_changed,
+                                                uint64_t& my_comp, uint64_t& my_rc) {
+    const int k = P.k, d = P.d;
+    constexpr bool vec = VEC;
+    float T[4];
+    int TJ[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        T[q] = INFINITY;
+        TJ[q] = INT_MAX;
+    }
+    for (int q = 0; q < 16; ++q) top4_insert(T, TJ, candD[c * 16 + q], candJ[c * 16 + q]);
+    const int64_t i = Lg.surv[s0 + c];
+    const float* xr = P.X + i * d;
+    const int inc = first ? -1 : P.a[i];
+    const int hd = (d + 1) / 2, m0 = part * hd, m1 = min(d, m0 + hd);
+    const float R = sqrtf(fmaxf(x2, 0.f)) * kUp + cnmax;
+    const float thr = T[0] + 2.f * (gexp * R * R + 4.f * R * ecm + 2.f * ecm * ecm);
+    // Only centroids whose expanded distance lies within thr of the
+    // smallest can be the nearest: any other one is certified
+    // farther than the smallest's centroid.  A fourth candidate
+    // inside the bound means more may lie outside the list: all
+    // centroids are decided in float64 then.
+    const bool full = T[3] <= thr;
+    int nq = 0;
+    while (nq < 3 && T[nq] <= thr && TJ[nq] < k) ++nq;   // uniform in the pair
+    // Direct-form distance of x to centroid j over this thread's half
+    // of the dimensions, both halves added (equal in the pair).
+    auto dist32 = [&](int j) {
+        const float* cr = P.C32 + (int64_t)j * d;
+        float accd = 0.f;
+        if (vec && (m0 & 3) == 0) {
+            int m = m0;
+            for (; m + 4 <= m1; m += 4) {
+                const f32x4 xv = *reinterpret_cast<const f32x4*>(xr + m);
+                const f32x4 cv = *reinterpret_cast<const f32x4*>(cr + m);
+                const float t0 = xv.x - cv.x, t1 = xv.y - cv.y, t2 = xv.z - cv.z, t3 = xv.w - cv.w;
+                accd = fmaf(t0, t0, accd);
+                accd = fmaf(t1, t1, accd);
+                accd = fmaf(t2, t2, accd);
+                accd = fmaf(t3, t3, accd);
+            }
+            for (; m < m1; ++m) {
+                const float t = xr[m] - cr[m];
+                accd = fmaf(t, t, accd);
+            }
+        } else {
+            for (int m = m0; m < m1; ++m) {
+                const float t = xr[m] - cr[m];
+                accd = fmaf(t, t, accd);
+            }
+        }
+        return accd + __shfl_xor(accd, 1);
+    };
+    auto dist64 = [&](int j) {
+        const double* cr = P.C64 + (int64_t)j * d;
+        double accd = 0.0;
+        for (int m = m0; m < m1; ++m) {
+            const double t = (double)xr[m] - cr[m];
+            accd = fma(t, t, accd);
+        }
+        return accd + __shfl_xor(accd, 1);
+    };
+    bool re = full;
+    float d1 = INFINITY, d2 = INFINITY;
+    int rk1 = INT_MAX, j1 = 0;
+    // One candidate is the nearest centroid (every other one is
+    // certified farther): as on the LDS paths, its bound then comes
+    // from its expanded value and the error bound, without the
+    // direct form (kept when statistics are gathered).
+    const bool single = !full && nq == 1 && !(P.flags & KM_FLAG_STATS);
+    if (!full && !single) {
+        for (int q = 0; q < nq; ++q) {
+            const int j = TJ[q];
+            const float Dd = dist32(j);
+            const int rk = j == inc ? -1 : j;
+            if (Dd < d1 || (Dd == d1 && rk < rk1)) {
+                d2 = d1;
+                d1 = Dd;
+                rk1 = rk;
+                j1 = j;
+            } else if (Dd < d2) {
+                d2 = Dd;
+            }
+        }
+        if (d2 != INFINITY) {
+            const float band =
+                2.f * gamma * (d1 + d2) + 4.f * (sqrtf(d1) + sqrtf(d2)) * ecm + 8.f * ecm * ecm;
+            if (d2 - d1 <= band) re = true;
+        }
+    }
+    int b = j1;
+    float ub;
+    if (single) {
+        const float e1b = gexp * R * R + 4.f * R * ecm + 2.f * ecm * ecm;
+        b = TJ[0];
+        ub = __builtin_amdgcn_sqrtf(fmaxf(T[0] + e1b, 0.f)) * (1.0f + 0x1p-20f) * kUp;
+    } else {
+        ub = upper_bound(d1, P.ec[j1], gamma);
+    }
+    if (re) {
+        // float64 decision against the master centroids with the
+        // oracle's rule (smaller distance, then the incumbent, then
+        // the lower index): among the candidates inside the bound, or
+        // among all centroids when the list may be incomplete.
+        double Dbb = INFINITY;
+        int bb = -1, kb = INT_MAX;
+        auto consider = [&](int j) {
+            const double Dj = dist64(j);
+            const int rk = j == inc ? -1 : j;
+            if (Dj < Dbb || (Dj == Dbb && rk < kb)) {
+                Dbb = Dj;
+                bb = j;
+                kb = rk;
+            }
+        };
+        if (full) {
+            for (int j = 0; j < k; ++j) consider(j);
+        } else {
+            for (int q = 0; q < nq; ++q) consider(TJ[q]);
+        }
+        b = bb < 0 ? 0 : bb;
+        ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
+    }
+    if (part == 0) {
+        if (b != inc) {
+            P.a[i] = b;
+            my_changed += 1;
+        }
+        P.u[i] = ub;
+        my_comp += (uint64_t)k;
+        my_rc += re ? 1 : 0;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Dense survivor distances on the matrix cores, as a tiled product of the
 // centroids (rows) and the survivors (columns) over the dimensions.  Block
@@ -341,137 +485,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 
         // Refinement: 2 threads per survivor, each half of the dimensions.
         const int c = tid >> 1, part = tid & 1;
-        if (c < rows) {
-            float T[4];
-            int TJ[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                T[q] = INFINITY;
-                TJ[q] = INT_MAX;
-            }
-            for (int q = 0; q < 16; ++q) top4_insert(T, TJ, candD[c * 16 + q], candJ[c * 16 + q]);
-            const int64_t i = Lg.surv[s0 + c];
-            const float* xr = P.X + i * d;
-            const int inc = first ? -1 : P.a[i];
-            const int hd = (d + 1) / 2, m0 = part * hd, m1 = min(d, m0 + hd);
-            const float R = sqrtf(fmaxf(x2s[c], 0.f)) * kUp + cnmax;
-            const float thr = T[0] + 2.f * (gexp * R * R + 4.f * R * ecm + 2.f * ecm * ecm);
-            // Only centroids whose expanded distance lies within thr of the
-            // smallest can be the nearest: any other one is certified
-            // farther than the smallest's centroid.  A fourth candidate
-            // inside the bound means more may lie outside the list: all
-            // centroids are decided in float64 then.
-            const bool full = T[3] <= thr;
-            int nq = 0;
-            while (nq < 3 && T[nq] <= thr && TJ[nq] < k) ++nq;   // uniform in the pair
-            // Direct-form distance of x to centroid j over this thread's half
-            // of the dimensions, both halves added (equal in the pair).
-            auto dist32 = [&](int j) {
-                const float* cr = P.C32 + (int64_t)j * d;
-                float accd = 0.f;
-                if (vec && (m0 & 3) == 0) {
-                    int m = m0;
-                    for (; m + 4 <= m1; m += 4) {
-                        const f32x4 xv = *reinterpret_cast<const f32x4*>(xr + m);
-                        const f32x4 cv = *reinterpret_cast<const f32x4*>(cr + m);
-                        const float t0 = xv.x - cv.x, t1 = xv.y - cv.y, t2 = xv.z - cv.z, t3 = xv.w - cv.w;
-                        accd = fmaf(t0, t0, accd);
-                        accd = fmaf(t1, t1, accd);
-                        accd = fmaf(t2, t2, accd);
-                        accd = fmaf(t3, t3, accd);
-                    }
-                    for (; m < m1; ++m) {
-                        const float t = xr[m] - cr[m];
-                        accd = fmaf(t, t, accd);
-                    }
-                } else {
-                    for (int m = m0; m < m1; ++m) {
-                        const float t = xr[m] - cr[m];
-                        accd = fmaf(t, t, accd);
-                    }
-                }
-                return accd + __shfl_xor(accd, 1);
-            };
-            auto dist64 = [&](int j) {
-                const double* cr = P.C64 + (int64_t)j * d;
-                double accd = 0.0;
-                for (int m = m0; m < m1; ++m) {
-                    const double t = (double)xr[m] - cr[m];
-                    accd = fma(t, t, accd);
-                }
-                return accd + __shfl_xor(accd, 1);
-            };
-            bool re = full;
-            float d1 = INFINITY, d2 = INFINITY;
-            int rk1 = INT_MAX, j1 = 0;
-            // One candidate is the nearest centroid (every other one is
-            // certified farther): as on the LDS paths, its bound then comes
-            // from its expanded value and the error bound, without the
-            // direct form (kept when statistics are gathered).
-            const bool single = !full && nq == 1 && !(P.flags & KM_FLAG_STATS);
-            if (!full && !single) {
-                for (int q = 0; q < nq; ++q) {
-                    const int j = TJ[q];
-                    const float Dd = dist32(j);
-                    const int rk = j == inc ? -1 : j;
-                    if (Dd < d1 || (Dd == d1 && rk < rk1)) {
-                        d2 = d1;
-                        d1 = Dd;
-                        rk1 = rk;
-                        j1 = j;
-                    } else if (Dd < d2) {
-                        d2 = Dd;
-                    }
-                }
-                if (d2 != INFINITY) {
-                    const float band =
-                        2.f * gamma * (d1 + d2) + 4.f * (sqrtf(d1) + sqrtf(d2)) * ecm + 8.f * ecm * ecm;
-                    if (d2 - d1 <= band) re = true;
-                }
-            }
-            int b = j1;
-            float ub;
-            if (single) {
-                const float e1b = gexp * R * R + 4.f * R * ecm + 2.f * ecm * ecm;
-                b = TJ[0];
-                ub = __builtin_amdgcn_sqrtf(fmaxf(T[0] + e1b, 0.f)) * (1.0f + 0x1p-20f) * kUp;
-            } else {
-                ub = upper_bound(d1, P.ec[j1], gamma);
-            }
-            if (re) {
-                // float64 decision against the master centroids with the
-                // oracle's rule (smaller distance, then the incumbent, then
-                // the lower index): among the candidates inside the bound, or
-                // among all centroids when the list may be incomplete.
-                double Dbb = INFINITY;
-                int bb = -1, kb = INT_MAX;
-                auto consider = [&](int j) {
-                    const double Dj = dist64(j);
-                    const int rk = j == inc ? -1 : j;
-                    if (Dj < Dbb || (Dj == Dbb && rk < kb)) {
-                        Dbb = Dj;
-                        bb = j;
-                        kb = rk;
-                    }
-                };
-                if (full) {
-                    for (int j = 0; j < k; ++j) consider(j);
-                } else {
-                    for (int q = 0; q < nq; ++q) consider(TJ[q]);
-                }
-                b = bb < 0 ? 0 : bb;
-                ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
-            }
-            if (part == 0) {
-                if (b != inc) {
-                    P.a[i] = b;
-                    my_changed += 1;
-                }
-                P.u[i] = ub;
-                my_comp += (uint64_t)k;
-                my_rc += re ? 1 : 0;
-            }
-        }
+        if (c < rows)
+            refine_survivor<VEC>(P, Lg, candD, candJ, s0, c, part, first, x2s[c], cnmax, gexp, ecm, gamma,
+                                 my_changed, my_comp, my_rc);
     }
     my_changed = wave_sum_u64(my_changed);
     my_comp = wave_sum_u64(my_comp);
