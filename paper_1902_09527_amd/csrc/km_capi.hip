@@ -112,8 +112,9 @@ void cache_give(int dev, size_t bytes, void* p) {
     (void)hipFree(p);
 }
 
-// Pinned host words for polling a run's stop flag, reused across runs
-// (hipHostMalloc and hipHostFree cost tens of microseconds each).
+// Pinned host blocks (256 bytes, coherent: kernels may store to them while
+// the host polls) for a run's progress word and read-backs, reused across
+// runs (hipHostMalloc and hipHostFree cost tens of microseconds each).
 std::mutex g_pin_mu;
 int32_t* g_pin_free[64];
 int g_pin_n = 0;
@@ -124,7 +125,7 @@ int32_t* pinned_take() {
         if (g_pin_n > 0) return g_pin_free[--g_pin_n];
     }
     void* p = nullptr;
-    if (hipHostMalloc(&p, 64, hipHostMallocDefault) != hipSuccess) return nullptr;
+    if (hipHostMalloc(&p, 256, hipHostMallocCoherent) != hipSuccess) return nullptr;
     return static_cast<int32_t*>(p);
 }
 
@@ -372,7 +373,7 @@ int read_state(km_ctx* c, km::IterState* out) {
 // Set-up of a context.  max_iters / tol_n: the stop rule written into the
 // loop state; sync: wait for the set-up work before returning.
 int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const float* C0, int32_t max_iters,
-              double tol_n, bool sync) {
+              double tol_n, bool sync, int32_t* host_word) {
     KM_HIP(hipGetDevice(&c->device));
     km::ZeroRanges zr{};   // buffers cleared by the set-up launch
     int rc0;
@@ -600,6 +601,7 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     zr.st = v.st;
     zr.max_iters = max_iters;
     zr.tol_n = tol_n;
+    zr.host = host_word;
     KM_HIP(km::launch_init_buffers(zr, cus, c->stream));
 
     // Largest magnitude of X and C0 (and non-finite detection) -> fixed-point
@@ -709,9 +711,12 @@ int pp_static_workspace(void** out) {
 
 extern "C" {
 
-// A new context; max_iters / tol_n: its stop rule; sync: wait for the set-up.
+// A new context; max_iters / tol_n: its stop rule; sync: wait for the set-up;
+// host_word (nullable, device address of pinned host memory): the progress
+// word the ends of steps write.
 static int create_ctx(km_ctx** out, const float* X, int64_t n, int32_t d, int32_t k, const float* C0,
-                      void* hip_stream, uint32_t flags, int32_t max_iters, double tol_n, bool sync) {
+                      void* hip_stream, uint32_t flags, int32_t max_iters, double tol_n, bool sync,
+                      int32_t* host_word = nullptr) {
     if (!out) return KM_ERR_INVALID_ARG;
     *out = nullptr;
     int rc = check_shape(X, n, d, k, C0);
@@ -727,7 +732,7 @@ static int create_ctx(km_ctx** out, const float* X, int64_t n, int32_t d, int32_
     c->k = k;
     c->flags = flags;
     c->stream = static_cast<hipStream_t>(hip_stream);
-    rc = init_impl(c, X, n, d, k, C0, max_iters, tol_n, sync);
+    rc = init_impl(c, X, n, d, k, C0, max_iters, tol_n, sync, host_word);
     if (rc != KM_OK) {
         delete c;
         return rc;
@@ -754,17 +759,9 @@ int kmeans_mti_iterate(km_ctx* ctx, int64_t* changed_out) {
     return KM_OK;
 }
 
-int kmeans_mti_get(km_ctx* ctx, int32_t* assign_out, float* C_out) {
-    if (!ctx) return KM_ERR_INVALID_ARG;
-    if (ctx->broken) return KM_ERR_STATE;
-    if (assign_out && !ctx->stepped) return KM_ERR_STATE;
+// kmeans_mti_get once the output ranges are checked.
+static int get_outputs(km_ctx* ctx, int32_t* assign_out, float* C_out) {
     int rc;
-    if (assign_out &&
-        (rc = check_device_range(assign_out, (size_t)ctx->n * 4, ctx->device, "assign_out")) != KM_OK)
-        return rc;
-    if (C_out && (rc = check_device_range(C_out, (size_t)ctx->k * ctx->d * 4, ctx->device, "C_out")) !=
-                     KM_OK)
-        return rc;
     if ((rc = flush_pending(ctx)) != KM_OK) return rc;
     hipError_t e;
     if (assign_out && ctx->small &&
@@ -781,6 +778,20 @@ int kmeans_mti_get(km_ctx* ctx, int32_t* assign_out, float* C_out) {
                             hipMemcpyDeviceToDevice, ctx->stream)) != hipSuccess)
         return fail_ctx(ctx, hip_fail(e, "hipMemcpyAsync centroids"));
     return KM_OK;
+}
+
+int kmeans_mti_get(km_ctx* ctx, int32_t* assign_out, float* C_out) {
+    if (!ctx) return KM_ERR_INVALID_ARG;
+    if (ctx->broken) return KM_ERR_STATE;
+    if (assign_out && !ctx->stepped) return KM_ERR_STATE;
+    int rc;
+    if (assign_out &&
+        (rc = check_device_range(assign_out, (size_t)ctx->n * 4, ctx->device, "assign_out")) != KM_OK)
+        return rc;
+    if (C_out && (rc = check_device_range(C_out, (size_t)ctx->k * ctx->d * 4, ctx->device, "C_out")) !=
+                     KM_OK)
+        return rc;
+    return get_outputs(ctx, assign_out, C_out);
 }
 
 int kmeans_mti_get_centroids64(km_ctx* ctx, double* C_out) {
@@ -868,20 +879,32 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
     if (e0 != hipSuccess) return hip_fail(e0, "hipGetDevice");
     if ((rc = check_device_range(assign_out, (size_t)n * 4, dev, "assign_out")) != KM_OK) return rc;
     if ((rc = check_device_range(C_out, (size_t)k * d * 4, dev, "C_out")) != KM_OK) return rc;
+    // The progress word: pinned host memory that the end of every step sets
+    // (steps ended, negated at the stop), polled below.
+    int32_t* pinned = pinned_take();
+    if (!pinned) return KM_ERR_OOM;
+    volatile int32_t* word = pinned;
+    word[0] = 0;
+    int32_t* word_dev = nullptr;
+    hipError_t eh = hipHostGetDevicePointer(reinterpret_cast<void**>(&word_dev), pinned, 0);
+    if (eh != hipSuccess) {
+        pinned_give(pinned);
+        return hip_fail(eh, "hipHostGetDevicePointer");
+    }
     km_ctx* c = nullptr;
-    if ((rc = create_ctx(&c, X, n, d, k, C0, hip_stream, flags, max_iters, tol * (double)n, false)) != KM_OK)
+    if ((rc = create_ctx(&c, X, n, d, k, C0, hip_stream, flags, max_iters, tol * (double)n, false, word_dev)) !=
+        KM_OK) {
+        pinned_give(pinned);
         return rc;
+    }
 
-    hipEvent_t ev0 = nullptr, ev1 = nullptr, evc[2] = {nullptr, nullptr};
-    int32_t* pinned = nullptr;
+    hipEvent_t ev0 = nullptr, ev1 = nullptr;
     float ms = 0.f;
     auto cleanup = [&]() {
         if (ev0) (void)hipEventDestroy(ev0);
         if (ev1) (void)hipEventDestroy(ev1);
-        for (auto& e : evc)
-            if (e) (void)hipEventDestroy(e);
+        kmeans_mti_destroy(c);   // waits for the stream: no kernel writes the word afterwards
         pinned_give(pinned);
-        kmeans_mti_destroy(c);
     };
 #define RUN_HIP(call)                                   \
     do {                                                \
@@ -895,49 +918,57 @@ int kmeans_mti_run(const float* X, int64_t n, int32_t d, int32_t k, const float*
 
     RUN_HIP(hipEventCreate(&ev0));
     RUN_HIP(hipEventCreate(&ev1));
-    RUN_HIP(hipEventCreateWithFlags(&evc[0], hipEventDisableTiming));
-    RUN_HIP(hipEventCreateWithFlags(&evc[1], hipEventDisableTiming));
-    pinned = pinned_take();
-    if (!pinned) {
-        cleanup();
-        return KM_ERR_OOM;
-    }
-    pinned[0] = pinned[1] = 0;
 
-    // Enqueue chunks of iterations; the device stop flag makes surplus
-    // launches return at once.  The host polls the flag one chunk behind,
-    // so at most two chunks are enqueued past convergence.
-    const int chunk = 4;
+    // Keep kAhead steps enqueued past the last one whose end the device has
+    // reported (on the streaming path a step's end runs at the start of the
+    // next launch); the device stop flag makes launches past the stop return
+    // at once, so at most kAhead - 1 are enqueued past convergence.  While
+    // waiting, the stream is queried now and then, so that an error ends the
+    // wait; an idle stream whose steps reported nothing new is an error too.
+    constexpr int kAhead = 2;   // measured best: fewer launches past the stop outweigh the bubbles
     RUN_HIP(hipEventRecord(ev0, c->stream));
-    int enq = 0, ci = 0;
+    int enq = 0;
     while (enq < max_iters) {
-        const int m = max_iters - enq < chunk ? max_iters - enq : chunk;
-        for (int i = 0; i < m; ++i) {
+        const int32_t v = word[0];
+        if (v < 0) break;
+        if (enq < v + kAhead) {
             if ((rc = enqueue_iteration(c)) != KM_OK) {
                 cleanup();
                 return rc;
             }
+            ++enq;
+            continue;
         }
-        enq += m;
-        RUN_HIP(hipMemcpyAsync(&pinned[ci & 1], &c->dv.st->done, sizeof(int32_t), hipMemcpyDeviceToHost,
-                               c->stream));
-        RUN_HIP(hipEventRecord(evc[ci & 1], c->stream));
-        if (ci >= 1) {
-            RUN_HIP(hipEventSynchronize(evc[(ci - 1) & 1]));
-            if (pinned[(ci - 1) & 1]) break;
+        bool stalled = false;
+        for (int spin = 1; word[0] == v; ++spin) {
+            if ((spin & 1023) == 0) {
+                const hipError_t q = hipStreamQuery(c->stream);
+                if (q == hipSuccess) {
+                    stalled = word[0] == v;
+                    break;
+                }
+                if (q != hipErrorNotReady) RUN_HIP(q);
+            }
         }
-        ++ci;
+        if (stalled) {
+            snprintf(g_last_hip, sizeof g_last_hip, "run loop: the steps ended without reporting progress");
+            cleanup();
+            return KM_ERR_STATE;
+        }
     }
     RUN_HIP(hipEventRecord(ev1, c->stream));
-    if ((rc = kmeans_mti_get(c, assign_out, C_out)) != KM_OK) {
+    if ((rc = get_outputs(c, assign_out, C_out)) != KM_OK) {   // ranges checked on entry
         cleanup();
         return rc;
     }
+    // The loop state after the last step, read back with the outputs' stream
+    // work (one wait for both).
     km::IterState st;
-    if ((rc = read_state(c, &st)) != KM_OK) {
-        cleanup();
-        return rc;
-    }
+    static_assert(sizeof(km::IterState) <= 256 - 64, "loop state fits the pinned block");
+    km::IterState* pst = reinterpret_cast<km::IterState*>(reinterpret_cast<char*>(pinned) + 64);
+    RUN_HIP(hipMemcpyAsync(pst, c->dv.st, sizeof(km::IterState), hipMemcpyDeviceToHost, c->stream));
+    RUN_HIP(hipStreamSynchronize(c->stream));
+    memcpy(&st, pst, sizeof st);
     RUN_HIP(hipEventElapsedTime(&ms, ev0, ev1));
     if (stats) {
         fill_stats(c, st, stats);

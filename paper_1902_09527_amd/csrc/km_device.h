@@ -41,6 +41,13 @@ __device__ inline uint64_t fixed_bits(double v, double scale) {
     return (uint64_t)__double_as_longlong(fma(v, scale, kMagic));
 }
 
+// The end of step t (one thread): the progress word of a run's host loop, if
+// any, becomes t + 1, negated when the run stops (a system-scope store to
+// pinned host memory).
+__device__ inline void report_step(const IterState* st, int t, bool done) {
+    if (st->host) __hip_atomic_store(st->host, done ? -(t + 1) : t + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 // The kernel's Dev with the fixed-point scales the set-up kernel left in the
 // loop state (the host does not wait for them).
 __device__ inline Dev with_scales(Dev P) {

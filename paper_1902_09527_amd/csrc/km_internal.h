@@ -44,6 +44,10 @@ struct IterState {
     // Fixed-point scales (set-up kernel k_set_scales, from the largest |x|):
     // 2^S, 2^-S of the coordinate sums and the same for the inertia sum.
     double qscale, qinv, iscale, iinv;
+    // Nullable: a pinned, coherent host word that the end of every step sets
+    // to the steps ended, negated once the stop test is met (a run's host
+    // loop polls it instead of copying the flag).
+    int32_t* host;
 };
 
 // Everything the kernels need, passed by value.
@@ -340,6 +344,7 @@ struct ZeroRanges {
     int32_t max_iters;    // loop state written to *st (when st is not null)
     double tol_n;
     IterState* st;
+    int32_t* host;        // its progress word (nullable)
     bool overflow;        // more than kMax ranges were added (the launch refuses)
     void add(void* q, uint64_t b) {
         if (n >= kMax) {

@@ -147,6 +147,7 @@ __global__ __launch_bounds__(256) void k_init_buffers(ZeroRanges z) {
         IterState st{};
         st.max_iters = z.max_iters;
         st.tol_n = z.tol_n;
+        st.host = z.host;
         *z.st = st;
     }
 }
@@ -1264,6 +1265,7 @@ __global__ __launch_bounds__(64) void k_update(Dev P_) {
             st->done = 1;
             st->converged = tol_hit ? 1 : 0;
         }
+        report_step(st, t, tol_hit || t + 1 >= st->max_iters);
     }
 }
 

@@ -612,6 +612,7 @@ __device__ void step_books(const Dev& P, const Fused& F, int t, float ecmax) {
         st->done = 1;
         st->converged = tol_hit ? 1 : 0;
     }
+    report_step(st, t, tol_hit || t + 1 >= st->max_iters);
 }
 
 // ---------------------------------------------------------------------------
