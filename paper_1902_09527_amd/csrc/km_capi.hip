@@ -339,7 +339,8 @@ int enqueue_iteration(km_ctx* c) {
     if ((e = km::launch_update(c->dv, c->stream)) != hipSuccess)
         return fail_ctx(c, hip_fail(e, "update kernel"));
     if ((e = mark(3)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
-    e = c->large ? km::launch_large_table(c->dv, 0, c->stream) : km::launch_centroid_table(c->dv, 0, c->stream);
+    e = c->large ? km::launch_large_table(c->dv, c->lg, 0, c->stream)
+                 : km::launch_centroid_table(c->dv, 0, c->stream);
     if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "centroid table kernel"));
     if ((e = mark(4)) != hipSuccess) return fail_ctx(c, hip_fail(e, "hipEventRecord"));
     ++c->enq;
@@ -511,12 +512,15 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
                      max_lds / 4);
             return KM_ERR_UNSUPPORTED;
         }
-        const void* sym = km::large_mfma_symbol(d);
+        const void* sym = km::large_mfma_symbol();
         KM_HIP(km::large_set_attributes(k, d));
         int per_cu = 0;
         KM_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sym, 256, mlds));
         if (per_cu < 1) return KM_ERR_UNSUPPORTED;
         L.Gm = per_cu * cus;
+        L.Gr = 4 * cus;
+        L.nch = km::split_chunks(d);
+        L.nct = (k + km::kLgN - 1) / km::kLgN;
         int64_t gs = (n + 4095) / 4096;
         if (gs > 2048) gs = 2048;
         L.Gs = (int32_t)gs;
@@ -530,9 +534,16 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             (rc2 = c->alloc(&L.cnt, (size_t)L.Gs * k)) || (rc2 = c->alloc(&L.off, (size_t)L.Gs * k)) ||
             (rc2 = c->alloc(&L.base, (size_t)k + 1)) || (rc2 = c->alloc(&L.cbase, (size_t)k + 1)) ||
             (rc2 = c->alloc(&L.perm, (size_t)n)) || (rc2 = c->alloc(&L.cpart, (size_t)L.NCmax * d)) ||
-            (rc2 = c->alloc(&L.ciq, (size_t)L.NCmax)))
+            (rc2 = c->alloc(&L.ciq, (size_t)L.NCmax)) ||
+            (rc2 = c->alloc(&L.xs, (size_t)n * L.nch * 16)) || (rc2 = c->alloc(&L.x2, (size_t)n)) ||
+            (rc2 = c->alloc(&L.sx2, (size_t)n)) || (rc2 = c->alloc(&L.fq, (size_t)n)) ||
+            (rc2 = c->alloc(&L.nfull, 4)) ||
+            (rc2 = c->alloc(&L.cs, (size_t)L.nct * km::kLgN * L.nch * 16)) ||
+            (rc2 = c->alloc(&L.cn2p, (size_t)L.nct * km::kLgN)) ||
+            (rc2 = c->alloc(&L.cand, (size_t)n * L.nct * 8)))
             return rc2;
         zr.add(L.nsurv, 4 * sizeof(uint32_t));
+        zr.add(L.nfull, 4 * sizeof(uint32_t));
     }
 
     int rc;
@@ -641,7 +652,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     if (!(c->flags & KM_FLAG_SPHERICAL))
         KM_HIP(km::launch_set_centroids(C0, v.C64, v.C32, v.ec, (int64_t)k * d, k, c->stream));
     if (c->large) {
-        KM_HIP(km::launch_large_table(v, 1, c->stream));
+        KM_HIP(km::launch_large_table(v, c->lg, 1, c->stream));
+        KM_HIP(km::launch_large_split_x(v, c->lg, cus, c->stream));
     } else {
         KM_HIP(km::launch_centroid_table(v, 1, c->stream));
     }

@@ -92,9 +92,17 @@ inline int row_len(int d, int k) { return k * d + k + kNumStat; }
 constexpr int kLgM = 128;            // survivors per block tile (matrix-core columns)
 constexpr int kLgN = 128;            // centroids per block tile (matrix-core rows)
 constexpr int kLgK = 16;             // dimensions per streamed chunk
-constexpr int kLgRS = kLgK + 4;      // LDS row stride (floats) of a chunk: 16-byte rows, spread over banks
+constexpr int kLgStages = 4;         // chunks in flight per block (LDS ring)
+constexpr int kLgStageBytes = 2 * kLgN * 4 * kLgK;   // one chunk of the centroid and survivor tiles
 constexpr int kLgChunkRows = 256;    // rows per segment-sum chunk
 constexpr int kLgMaxD = 4096;        // largest d of the global-memory path
+
+// Split rows (the matrix-core operands of the global path): every float32
+// value x is held as hi = bf16(x) and lo = bf16(x - hi), both rounded to
+// nearest.  Row r, chunk c (dimensions 16c .. 16c + 15, zero past d) takes 16
+// words: hi of dimensions 16c .. +7, hi of 16c + 8 .. +15, lo of 16c .. +7, lo
+// of 16c + 8 .. +15 (two bf16 per word, the lower dimension in the low half).
+inline int split_chunks(int d) { return (d + kLgK - 1) / kLgK; }
 
 struct Large {
     int32_t* surv;        // n: survivor point indices of the current step
@@ -106,20 +114,29 @@ struct Large {
     int32_t* perm;        // n point indices grouped by cluster
     uint64_t* cpart;      // NCmax x d chunk partial sums (fixed point)
     uint64_t* ciq;        // NCmax chunk inertia partials (fixed point)
+    uint32_t* xs;         // n split rows of X (set-up)
+    float* x2;            // n: float32 squared norms of the rows of X (set-up)
+    float* sx2;           // n: x2 of the survivors, in list order
+    int32_t* fq;          // n: survivors (list entries) decided over all centroids
+    uint32_t* nfull;      // their count (zeroed by the histogram pass for the next step)
+    uint32_t* cs;         // nct * kLgN split rows of the float32 centroids (rows >= k zero)
+    float* cn2p;          // nct * kLgN: their float32 squared norms (rows >= k: +inf)
+    uint2* cand;          // n x nct x 2 x 4: per survivor, centroid tile and half of it, the four
+                          // smallest expanded distances (float bits) with their centroids
+    int32_t nch;          // chunks per split row
+    int32_t nct;          // centroid tiles
     int32_t Gs;           // blocks of the histogram / scatter passes
     int32_t NCmax;        // n / kLgChunkRows + k
     int64_t span;         // points per histogram / scatter block (contiguous)
     int32_t Gm;           // resident blocks of the matrix-core kernel
+    int32_t Gr;           // blocks of the refinement pass
 };
 
-// LDS bytes of the global-memory matrix-core kernel: the double-buffered
-// chunks (reused for the candidate lists after the last chunk), the
-// survivors' squared norms, a few reduction words and the centroid tile's
-// squared norms.
+// LDS bytes of the global-memory matrix-core kernel: the ring of streamed
+// chunks and, by item parity, the centroid tile's and the survivors' squared
+// norms and every wave's survivor rows.
 __host__ __device__ inline int large_mfma_lds() {
-    const int bufs = 2 * (kLgN + kLgM) * kLgRS * 4;
-    const int cand = kLgM * 16 * 8;
-    return (bufs > cand ? bufs : cand) + 4 * kLgM + 16 + 4 * kLgN;
+    return kLgStages * kLgStageBytes + 2 * 4 * (kLgN + kLgM) + 2 * 4 * 256;
 }
 
 // Padded LDS row stride of the X tile: 16-byte aligned rows, offset by 4
@@ -322,9 +339,11 @@ hipError_t launch_small_unpack(const Fused& F, int64_t n, int32_t* assign_out, h
 // Global-memory path launchers (km_large.hip).  gb: blocks of the bound pass.
 hipError_t launch_large_assign(const Dev& dv, const Large& lg, int gb, hipStream_t s);
 hipError_t launch_large_reduce(const Dev& dv, const Large& lg, hipStream_t s);
-hipError_t launch_large_table(const Dev& dv, int force, hipStream_t s);
+hipError_t launch_large_table(const Dev& dv, const Large& lg, int force, hipStream_t s);
+// Split rows (and, with norms, float32 squared norms) of X, once at set-up.
+hipError_t launch_large_split_x(const Dev& dv, const Large& lg, int cus, hipStream_t s);
 int large_table_lds(int d);
-const void* large_mfma_symbol(int d);   // the matrix-core kernel for row length d
+const void* large_mfma_symbol();   // the matrix-core kernel
 // Raises the dynamic-LDS limits of the global-memory path's kernels.
 hipError_t large_set_attributes(int k, int d);
 

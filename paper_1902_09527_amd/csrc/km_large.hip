@@ -4,12 +4,14 @@
 // section III-B) is:
 //   k_bound_large       drift-updated bound and Clause 1 (section III-C) for
 //                       every point; survivors compacted into a global list;
-//   k_mfma_large        float32 MFMA distances of the survivors to all
-//                       centroids (128-centroid x 128-survivor tiles over
-//                       double-buffered 16-dimension chunks, expanded form), a
-//                       top-4 candidate list per survivor, direct-form
-//                       refinement of the candidates within the expanded
-//                       form's error bound, float64 near-tie rule;
+//   k_mfma_large        distances of the survivors to all centroids on the
+//                       matrix cores (128-survivor x 128-centroid work items,
+//                       split-bf16 products over 16-dimension chunks streamed
+//                       into LDS by direct loads, expanded form): the four
+//                       smallest per survivor and centroid tile;
+//   k_refine_large      per survivor, the candidates within the expanded
+//                       form's error bound refined in the direct form,
+//                       float64 near-tie rule;
 //   k_hist_large        per-block cluster counts of the new assignment;
 //   k_scan_large_cols,
 //   k_scan_large_clusters  cluster starts and per-block write offsets;
@@ -17,9 +19,12 @@
 //   k_segsum_large      exact fixed-point sums over chunks of each cluster;
 //   k_chunk_reduce_large  per-cluster sums, counts and the inertia into the
 //                       reduced row read by k_update;
-//   k_centroid_table_tiled  half centroid distances for the next step.
+//   k_centroid_table_tiled  half centroid distances for the next step;
+//   k_split_rows        split operand rows of the new centroids (and, once at
+//                       set-up, of X with its squared norms).
 // The order of points inside a cluster segment is not fixed, but every sum
 // is an exact integer sum, so results are bitwise reproducible.
+#include <float.h>
 #include <limits.h>
 #include <math.h>
 
@@ -111,7 +116,11 @@ __global__ __launch_bounds__(256) void k_bound_large(Dev P, Large Lg) {
             uint32_t b = 0;
             if (lane == 0) b = atomicAdd(Lg.nsurv, (uint32_t)__popcll(m));
             b = __shfl(b, 0);
-            if (surv) Lg.surv[b + __popcll(m & ((1ull << lane) - 1ull))] = (int32_t)i;
+            if (surv) {
+                const uint32_t pos = b + __popcll(m & ((1ull << lane) - 1ull));
+                Lg.surv[pos] = (int32_t)i;
+                Lg.sx2[pos] = Lg.x2[i];
+            }
         }
     }
     c1 = wave_sum_u64(c1);
@@ -120,384 +129,662 @@ __global__ __launch_bounds__(256) void k_bound_large(Dev P, Large Lg) {
                   (unsigned long long)c1);
 }
 
-// Refinement of survivor c of a tile (entry s0 + c of the survivor list) by
-// a thread pair (part 0 and 1, each over half of the dimensions) from the
-// survivor's 16 candidate slots (candD, candJ: 4 lists of 4) and its squared
-// norm x2: the candidates within twice the expanded form's error bound of the
-// smallest are re-evaluated in the direct form, followed by the float64
-// near-tie rule; the point's assignment and bound are written.
-template <bool VEC>
-__device__ __forceinline__ void refine_survivor(const Dev& P, const Large& Lg, const float* candD, const int* candJ,
-                                                int s0, int c, int part, bool first, float x2, float cnmax,
-                                                float gexp, float ecm, float gamma, uint64_t& my_changed,
-                                                uint64_t& my_comp, uint64_t& my_rc) {
-    const int k = P.k, d = P.d;
-    constexpr bool vec = VEC;
-    float T[4];
-    int TJ[4];
+// ---------------------------------------------------------------------------
+// Split rows: hi = bf16(x), lo = bf16(x - hi) (both rounded to nearest; x - hi
+// is exact in float32), in the chunk layout of the matrix-core operands, and
+// the float32 squared norm of every row (each lane sums its dimensions in
+// order, then a fixed butterfly over the wave: deterministic).  Rows from
+// valid to rows are padding: zero operands, norm +inf.  One wave per row.
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ uint32_t split_hi(float a, float b, float& ra, float& rb) {
+    const f32x2 v = {a, b};
+    const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+    ra = a - __uint_as_float(h << 16);
+    rb = b - __uint_as_float(h & 0xffff0000u);
+    return h;
+}
+
+__device__ __forceinline__ uint32_t split_lo(float a, float b) {
+    const f32x2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+__global__ __launch_bounds__(256) void k_split_rows(const float* __restrict__ src, int64_t rows, int64_t valid, int d,
+                                                    int nch, uint32_t* __restrict__ dst, float* __restrict__ norms,
+                                                    const IterState* st, int force) {
+    if (st && !force && !st->active) return;
+    const int lane = threadIdx.x & 63;
+    const int64_t wstride = (int64_t)gridDim.x * (blockDim.x >> 6);
+    for (int64_t r = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); r < rows; r += wstride) {
+        const bool pad = r >= valid;
+        const float* x = src + (pad ? 0 : r) * d;
+        uint32_t* o = dst + r * nch * 16;
+        float sq = 0.f;
+        for (int g = lane; g < 2 * nch; g += 64) {   // 8-dimension group g: chunk g / 2, half g % 2
+            const int m0 = 8 * g;
+            float v[8];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        T[q] = INFINITY;
-        TJ[q] = INT_MAX;
-    }
-    for (int q = 0; q < 16; ++q) top4_insert(T, TJ, candD[c * 16 + q], candJ[c * 16 + q]);
-    const int64_t i = Lg.surv[s0 + c];
-    const float* xr = P.X + i * d;
-    const int inc = first ? -1 : P.a[i];
-    const int hd = (d + 1) / 2, m0 = part * hd, m1 = min(d, m0 + hd);
-    const float R = sqrtf(fmaxf(x2, 0.f)) * kUp + cnmax;
-    const float thr = T[0] + 2.f * (gexp * R * R + 4.f * R * ecm + 2.f * ecm * ecm);
-    // Only centroids whose expanded distance lies within thr of the
-    // smallest can be the nearest: any other one is certified
-    // farther than the smallest's centroid.  A fourth candidate
-    // inside the bound means more may lie outside the list: all
-    // centroids are decided in float64 then.
-    const bool full = T[3] <= thr;
-    int nq = 0;
-    while (nq < 3 && T[nq] <= thr && TJ[nq] < k) ++nq;   // uniform in the pair
-    // Direct-form distance of x to centroid j over this thread's half
-    // of the dimensions, both halves added (equal in the pair).
-    auto dist32 = [&](int j) {
-        const float* cr = P.C32 + (int64_t)j * d;
-        float accd = 0.f;
-        if (vec && (m0 & 3) == 0) {
-            int m = m0;
-            for (; m + 4 <= m1; m += 4) {
-                const f32x4 xv = *reinterpret_cast<const f32x4*>(xr + m);
-                const f32x4 cv = *reinterpret_cast<const f32x4*>(cr + m);
-                const float t0 = xv.x - cv.x, t1 = xv.y - cv.y, t2 = xv.z - cv.z, t3 = xv.w - cv.w;
-                accd = fmaf(t0, t0, accd);
-                accd = fmaf(t1, t1, accd);
-                accd = fmaf(t2, t2, accd);
-                accd = fmaf(t3, t3, accd);
+            for (int e = 0; e < 8; ++e) v[e] = !pad && m0 + e < d ? x[m0 + e] : 0.f;
+            uint32_t hw[4], lw[4];
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                float ra, rb;
+                hw[p] = split_hi(v[2 * p], v[2 * p + 1], ra, rb);
+                lw[p] = split_lo(ra, rb);
+                sq = fmaf(v[2 * p], v[2 * p], sq);
+                sq = fmaf(v[2 * p + 1], v[2 * p + 1], sq);
             }
-            for (; m < m1; ++m) {
-                const float t = xr[m] - cr[m];
-                accd = fmaf(t, t, accd);
-            }
-        } else {
-            for (int m = m0; m < m1; ++m) {
-                const float t = xr[m] - cr[m];
-                accd = fmaf(t, t, accd);
-            }
+            uint32_t* oc = o + (g >> 1) * 16 + 4 * (g & 1);
+            *reinterpret_cast<uint4*>(oc) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+            *reinterpret_cast<uint4*>(oc + 8) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
         }
-        return accd + __shfl_xor(accd, 1);
-    };
-    auto dist64 = [&](int j) {
-        const double* cr = P.C64 + (int64_t)j * d;
-        double accd = 0.0;
-        for (int m = m0; m < m1; ++m) {
-            const double t = (double)xr[m] - cr[m];
-            accd = fma(t, t, accd);
-        }
-        return accd + __shfl_xor(accd, 1);
-    };
-    bool re = full;
-    float d1 = INFINITY, d2 = INFINITY;
-    int rk1 = INT_MAX, j1 = 0;
-    // One candidate is the nearest centroid (every other one is
-    // certified farther): as on the LDS paths, its bound then comes
-    // from its expanded value and the error bound, without the
-    // direct form (kept when statistics are gathered).
-    const bool single = !full && nq == 1 && !(P.flags & KM_FLAG_STATS);
-    if (!full && !single) {
-        for (int q = 0; q < nq; ++q) {
-            const int j = TJ[q];
-            const float Dd = dist32(j);
-            const int rk = j == inc ? -1 : j;
-            if (Dd < d1 || (Dd == d1 && rk < rk1)) {
-                d2 = d1;
-                d1 = Dd;
-                rk1 = rk;
-                j1 = j;
-            } else if (Dd < d2) {
-                d2 = Dd;
-            }
-        }
-        if (d2 != INFINITY) {
-            const float band =
-                2.f * gamma * (d1 + d2) + 4.f * (sqrtf(d1) + sqrtf(d2)) * ecm + 8.f * ecm * ecm;
-            if (d2 - d1 <= band) re = true;
-        }
-    }
-    int b = j1;
-    float ub;
-    if (single) {
-        const float e1b = gexp * R * R + 4.f * R * ecm + 2.f * ecm * ecm;
-        b = TJ[0];
-        ub = __builtin_amdgcn_sqrtf(fmaxf(T[0] + e1b, 0.f)) * (1.0f + 0x1p-20f) * kUp;
-    } else {
-        ub = upper_bound(d1, P.ec[j1], gamma);
-    }
-    if (re) {
-        // float64 decision against the master centroids with the
-        // oracle's rule (smaller distance, then the incumbent, then
-        // the lower index): among the candidates inside the bound, or
-        // among all centroids when the list may be incomplete.
-        double Dbb = INFINITY;
-        int bb = -1, kb = INT_MAX;
-        auto consider = [&](int j) {
-            const double Dj = dist64(j);
-            const int rk = j == inc ? -1 : j;
-            if (Dj < Dbb || (Dj == Dbb && rk < kb)) {
-                Dbb = Dj;
-                bb = j;
-                kb = rk;
-            }
-        };
-        if (full) {
-            for (int j = 0; j < k; ++j) consider(j);
-        } else {
-            for (int q = 0; q < nq; ++q) consider(TJ[q]);
-        }
-        b = bb < 0 ? 0 : bb;
-        ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
-    }
-    if (part == 0) {
-        if (b != inc) {
-            P.a[i] = b;
-            my_changed += 1;
-        }
-        P.u[i] = ub;
-        my_comp += (uint64_t)k;
-        my_rc += re ? 1 : 0;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
+        if (lane == 0) norms[r] = pad ? INFINITY : sq;
     }
 }
 
 // ---------------------------------------------------------------------------
-// Dense survivor distances on the matrix cores, as a tiled product of the
-// centroids (rows) and the survivors (columns) over the dimensions.  Block
-// tile: kLgN = 128 centroids x kLgM = 128 survivors; wave (wr, wc) owns
-// centroid rows 64 wr .. 64 wr + 63 and survivor columns 64 wc .. 64 wc + 63,
-// four 32x32 float32 accumulators.  The dimensions stream in chunks
-// of kLgK through double-buffered LDS (row-major, 16-byte rows: one 16-byte
-// store per thread and row piece, two 16-byte reads per lane and operand);
-// the next chunk's global loads are issued before the current chunk's
-// products.  Within a chunk, product step s sums dimensions s (lanes 0-31)
-// and 8 + s (lanes 32-63), so each lane's operands for the whole chunk are 8
-// consecutive floats of one row.  Each lane
-// keeps, for its two survivor columns, the four smallest expanded-form
-// distances |x|^2 + |c|^2 - 2 x.c with their centroids; the 4 lists of a
-// survivor (2 waves x 2 half-waves) are merged in LDS, and the candidates
-// within the expanded form's error bound of the smallest are re-evaluated in
-// the direct form, followed by the float64 near-tie rule.
+// Dense survivor distances on the matrix cores.  A work item is one tile of
+// kLgM = 128 survivors against one tile of kLgN = 128 centroids; wave
+// (wr, wc) of the block owns centroid rows 64 wr .. +63 and survivor columns
+// 64 wc .. +63, four 32x32 float32 accumulators.  Each product x.c is formed
+// from the split operands as hi.hi + hi.lo + lo.hi: three bf16 products on
+// v_mfma_f32_32x32x16_bf16 (16 dimensions each) in place of eight float32
+// ones, with the dropped lo.lo term and the accumulation inside the error
+// bound used by the refinement pass.
+//
+// The 16-dimension chunks of a block's items form one stream that runs
+// kLgStages - 1 chunks ahead of the products, across item boundaries (the
+// next item's first chunks load during the current item's selection).  They
+// go from the split rows straight into a ring of kLgStages LDS stages by
+// global_load_lds_dwordx4 (no registers held); a stage is two tiles of 128
+// rows x 64 bytes in 1 KB groups of 16 rows, the four 16-byte pieces of each
+// row permuted by lg_swz so that the operand reads of eight (and of sixteen)
+// consecutive lanes fall on distinct banks.  Loads return in order, so chunk
+// g has landed once at most the loads issued after it are outstanding.
+//
+// Work items are ordered so that the nct items of a survivor tile carry
+// indices congruent modulo 8: with a resident grid whose size is a multiple
+// of 8, they run at the same time on one XCD and its L2 serves the survivor
+// rows to all of them (each row leaves HBM about once per step).
+//
+// Selection: each expanded distance |x|^2 + |c|^2 - 2 x.c is clamped at 0
+// (the true distance is >= 0, so the error bound still holds) and packed
+// with its centroid into one ordered 32-bit key: the float's bits with the
+// low 7 bits (5 within a lane's list) replaced by the centroid's place in
+// the item, which lowers the value by less than 2^-16 of itself.  A lane
+// keeps, per survivor column, the four smallest keys by min and med3
+// (branch-free); the two half-waves' lists of a column are merged by a lane
+// swap, and each wave writes the four smallest (value, centroid) pairs of
+// its 64 centroids to the candidate buffer.
 
-template <bool VEC>
+__device__ __forceinline__ int lg_swz(int rho) { return ((rho >> 2) & 3) ^ (((rho >> 1) & 1) << 1); }
+
+__device__ __forceinline__ uint32_t med3u(uint32_t a, uint32_t b, uint32_t c) {
+    uint32_t r;
+    asm("v_med3_u32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+
+// Insert key v into the ascending 4-list L.
+__device__ __forceinline__ void key4_insert(uint32_t (&L)[4], uint32_t v) {
+    const uint32_t l0 = min(L[0], v), l1 = med3u(L[0], L[1], v), l2 = med3u(L[1], L[2], v),
+                   l3 = med3u(L[2], L[3], v);
+    L[0] = l0;
+    L[1] = l1;
+    L[2] = l2;
+    L[3] = l3;
+}
+
+// Sort 4 keys ascending (five compare-exchanges).
+__device__ __forceinline__ void sort4(uint32_t (&L)[4]) {
+    auto cx = [&](int i, int j) __attribute__((always_inline)) {
+        const uint32_t a = L[i], b = L[j];
+        L[i] = min(a, b);
+        L[j] = max(a, b);
+    };
+    cx(0, 1);
+    cx(2, 3);
+    cx(0, 2);
+    cx(1, 3);
+    cx(1, 2);
+}
+
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_mfma_large(Dev P, Large Lg) {
     IterState* st = P.st;
     if (!st->active) return;
-    const int k = P.k, d = P.d;
-    const bool first = st->t == 0;
-    const uint32_t ns = *Lg.nsurv;
+    const int k = P.k;
+    const int ns = (int)*Lg.nsurv;
+    const int nch = Lg.nch, nct = Lg.nct;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 31, half = lane >> 5;
-    const int wr = wave >> 1, wc = wave & 1;   // the wave's 64-centroid row block and 64-survivor column block
+    const int wr = wave >> 1, wc = wave & 1;
     extern __shared__ __align__(16) unsigned char smem[];
-    constexpr int kBufBytes = 2 * (kLgN + kLgM) * kLgRS * 4;
-    constexpr int kCandBytes = kLgM * 16 * 8;
-    float* Ab = reinterpret_cast<float*>(smem);                    // [2][kLgN][kLgRS]
-    float* Bb = Ab + 2 * kLgN * kLgRS;                             // [2][kLgM][kLgRS]
-    float* candD = reinterpret_cast<float*>(smem);                 // [kLgM][16], after the products
-    int* candJ = reinterpret_cast<int*>(candD + kLgM * 16);
-    float* x2s = reinterpret_cast<float*>(smem + (kBufBytes > kCandBytes ? kBufBytes : kCandBytes));   // [kLgM]
-    float* red = x2s + kLgM;                                       // [4]
-    float* cnt = red + 4;                                          // [kLgN]: the centroid tile's |c|^2
+    float* nrm = reinterpret_cast<float*>(smem + kLgStages * kLgStageBytes);   // [2][kLgN + kLgM]: |c|^2 of the centroid tile,
+                                                             // then |x|^2 of the survivors (by item parity)
+    int32_t* meta = reinterpret_cast<int32_t*>(nrm + 2 * (kLgN + kLgM));   // [2][4 waves][64]: survivor rows
 
-    const float ecm = st->ec_max;
-    const float gamma = P.gamma;
-    const float gexp = (float)(d + 8) * 0x1p-24f;
-    // Largest centroid norm (for the expanded-form error bound).
-    float m2 = 0.f;
-    for (int j = tid; j < k; j += blockDim.x) m2 = fmaxf(m2, P.cn2[j]);
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) m2 = fmaxf(m2, __shfl_xor(m2, off));
-    if (lane == 0) red[wave] = m2;
-    __syncthreads();
-    const float cnmax = sqrtf(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))) * kUp;
-
-    uint64_t my_changed = 0, my_comp = 0, my_rc = 0;
-    const int ntiles = (int)((ns + kLgM - 1) / kLgM);
-    const int nct = (k + kLgN - 1) / kLgN;
-    const int nch = (d + kLgK - 1) / kLgK;
-    constexpr bool vec = VEC;   // d % 4 == 0: 16-byte row chunks (every chunk start is then aligned)
-    const f32x4* C4 = reinterpret_cast<const f32x4*>(P.C32);
-    const f32x4* X4 = reinterpret_cast<const f32x4*>(P.X);
-
-    // Chunk loads, two 4-float pieces per thread for each operand: centroid
-    // row n0 + 64i + tid / 4 and survivor 64i + tid / 4, dimensions
-    // 4 (tid % 4) .. +3 of the chunk; zero outside k, the survivors and d.
-    f32x4 ra[2], rb[2];
-    float x2p[2] = {0.f, 0.f};   // partial squared norms of this thread's two survivors (first centroid tile)
-    int srow[2];                 // this thread's two survivors' point indices (-1: none)
-    const int q4 = tid & 3, r4 = tid >> 2;
-    auto load_chunk = [&](int n0, int c) __attribute__((always_inline)) {
-        const int m0 = c * kLgK + 4 * q4;
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int j = n0 + 64 * i + r4;
-            f32x4 v = {0.f, 0.f, 0.f, 0.f};
-            if (j < k) {
-                if (vec) {
-                    if (m0 < d) v = C4[((int64_t)j * d + m0) >> 2];
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (m0 + e < d) v[e] = P.C32[(int64_t)j * d + m0 + e];
-                }
-            }
-            ra[i] = v;
-        }
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            f32x4 v = {0.f, 0.f, 0.f, 0.f};
-            if (srow[i] >= 0) {
-                if (vec) {
-                    if (m0 < d) v = X4[((int64_t)srow[i] * d + m0) >> 2];   // cached: re-read per centroid tile
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (m0 + e < d) v[e] = P.X[(int64_t)srow[i] * d + m0 + e];
-                }
-            }
-            rb[i] = v;
-        }
+    const int nst = (ns + kLgM - 1) / kLgM;
+    const int per_round = 8 * nct;
+    const int64_t nitems = (int64_t)((nst + 7) / 8) * per_round;
+    const int G = gridDim.x;
+    auto tile_of = [&](int64_t w, int& s0, int& n0) __attribute__((always_inline)) {
+        const int64_t r = w / per_round;
+        const int rem = (int)(w - r * per_round);
+        s0 = (int)(r * 8 + (rem & 7)) * kLgM;
+        n0 = (rem >> 3) * kLgN;
     };
-    auto store_chunk = [&](int buf) __attribute__((always_inline)) {
-        float* A = Ab + buf * kLgN * kLgRS;
-        float* B = Bb + buf * kLgM * kLgRS;
-#pragma unroll
-        for (int i = 0; i < 2; ++i) *reinterpret_cast<f32x4*>(A + (64 * i + r4) * kLgRS + 4 * q4) = ra[i];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) *reinterpret_cast<f32x4*>(B + (64 * i + r4) * kLgRS + 4 * q4) = rb[i];
+    auto next_valid = [&](int64_t w) __attribute__((always_inline)) {
+        for (; w < nitems; w += G) {
+            int s0, n0;
+            tile_of(w, s0, n0);
+            if (s0 < ns) break;
+        }
+        return w;
     };
 
-    for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-        const int s0 = tile * kLgM;
-        const int rows = min(kLgM, (int)ns - s0);
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int sl = 64 * i + r4;
-            srow[i] = sl < rows ? Lg.surv[s0 + sl] : -1;
-            x2p[i] = 0.f;
+    // DMA role of this lane in a 16-row group: row rho, LDS slot lane, piece
+    // (lane % 4) ^ lg_swz(rho) of the row's chunk; this wave streams row
+    // groups 2 wave and 2 wave + 1 of both tiles.
+    const int rho = lane >> 2, piece = (lane & 3) ^ lg_swz(rho);
+    const int sr0 = 32 * wave + rho;
+    // Operand reads of lane (col, half): row col of a 32-row block, pieces
+    // half (hi) and 2 + half (lo), at these offsets in its 1 KB group.
+    const int rr = col & 15;
+    const int offh = 16 * (4 * rr + (half ^ lg_swz(rr))), offl = 16 * (4 * rr + ((2 + half) ^ lg_swz(rr)));
+    const int ga = (4 * wr + (col >> 4)) * 1024, gb = kLgN * 64 + (4 * wc + (col >> 4)) * 1024;
+    const int64_t rowb = (int64_t)nch * 64;   // bytes per split row
+    const unsigned char* csb = reinterpret_cast<const unsigned char*>(Lg.cs) + 16 * piece;
+    const unsigned char* xsb = reinterpret_cast<const unsigned char*>(Lg.xs) + 16 * piece;
+    const float* __restrict__ cn2p = Lg.cn2p;
+    const float* __restrict__ sx2 = Lg.sx2;
+    const int32_t* __restrict__ surv = Lg.surv;
+    // Item metadata goes to LDS by direct loads too (nothing loaded is held
+    // in registers across the loop): the survivor rows of this wave's two
+    // row groups (lane l: row 32 wave + l % 32; rows past the list repeat
+    // the first), and the 128 centroid and 128 survivor squared norms
+    // (waves 0-1 and 2-3, one per lane; survivors past the list read the
+    // first).
+    auto load_meta = [&](int s0, int par) __attribute__((always_inline)) {
+        const int r = 32 * wave + (lane & 31);
+        __builtin_amdgcn_global_load_lds(surv + s0 + (s0 + r < ns ? r : 0), (lds_ptr)(meta + par * 256 + wave * 64),
+                                         4, 0, 0);
+    };
+    auto load_norms = [&](int s0, int n0, int par) __attribute__((always_inline)) {
+        const float* src;
+        if (wave < 2) {
+            src = cn2p + n0 + tid;
+        } else {
+            const int sl = tid - kLgN;
+            src = sx2 + s0 + (s0 + sl < ns ? sl : 0);
         }
-        float L[2][4];
-        int J[2][4];
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                L[cb][q] = INFINITY;
-                J[cb][q] = INT_MAX;
+        __builtin_amdgcn_global_load_lds(src, (lds_ptr)(nrm + par * (kLgN + kLgM) + wave * 64), 4, 0, 0);
+    };
+
+    // Issue cursor: item wi, its next chunk ci, its parity ipar; wn the item
+    // after it.
+    int64_t wi = next_valid(blockIdx.x);
+    if (wi >= nitems) return;
+    int is0, in0;
+    tile_of(wi, is0, in0);
+    int64_t wn = next_valid(wi + G);
+    const unsigned char *pa, *pb0, *pb1;
+    {
+        const int rows = min(kLgM, ns - is0);
+        const int q0 = surv[is0 + (sr0 < rows ? sr0 : 0)], q1 = surv[is0 + (sr0 + 16 < rows ? sr0 + 16 : 0)];
+        pa = csb + (int64_t)(in0 + sr0) * rowb;
+        pb0 = xsb + (int64_t)q0 * rowb;
+        pb1 = xsb + (int64_t)q1 * rowb;
+    }
+    int ipar = 0;
+    load_norms(is0, in0, 0);
+    if (wn < nitems) {
+        int s1, n1;
+        tile_of(wn, s1, n1);
+        load_meta(s1, 1);
+    }
+    int ci = 0;
+    bool more = true;
+    int64_t issued = 0;
+    auto issue_one = [&]() __attribute__((always_inline)) {
+        if (ci == nch) {   // the issue cursor enters the next item (its survivor rows landed long ago)
+            ci = 0;
+            wi = wn;
+            ipar ^= 1;
+            tile_of(wi, is0, in0);
+            const int* mrow = meta + ipar * 256 + wave * 64;
+            const int q0 = mrow[rho], q1 = mrow[16 + rho];
+            pa = csb + (int64_t)(in0 + sr0) * rowb;
+            pb0 = xsb + (int64_t)q0 * rowb;
+            pb1 = xsb + (int64_t)q1 * rowb;
+            load_norms(is0, in0, ipar);
+            wn = next_valid(wn + G);
+            if (wn < nitems) {
+                int s1, n1;
+                tile_of(wn, s1, n1);
+                load_meta(s1, ipar ^ 1);
             }
-        for (int ct = 0; ct < nct; ++ct) {
-            const int n0 = ct * kLgN;
-            f32x16 acc[2][2];
+        }
+        unsigned char* base = smem + (int)(issued % kLgStages) * kLgStageBytes + 2 * wave * 1024;
+        const int64_t o = (int64_t)ci * 64;
+        __builtin_amdgcn_global_load_lds(pa + o, (lds_ptr)(base), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(pa + 16 * rowb + o, (lds_ptr)(base + 1024), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(pb0 + o, (lds_ptr)(base + kLgN * 64), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(pb1 + o, (lds_ptr)(base + kLgN * 64 + 1024), 16, 0, 0);
+        ++issued;
+        if (++ci == nch && wn >= nitems) more = false;
+    };
+    // Compute cursor: item wcur (tile cs0, cn0), chunk cc, parity par.
+    int64_t wcur = wi;
+    int cs0 = is0, cn0 = in0, cc = 0, par = 0;
+    const int ahead = min(kLgStages - 1, nch);
+    for (int e = 0; e < ahead && more; ++e) issue_one();
+
+    f32x16 acc[2][2];
+    for (int64_t g = 0; g < issued; ++g) {
+        if (cc == 0) {
 #pragma unroll
             for (int a = 0; a < 2; ++a)
 #pragma unroll
                 for (int b = 0; b < 2; ++b)
 #pragma unroll
                     for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
-            __syncthreads();   // the previous tile's buffers and lists are consumed
-            load_chunk(n0, 0);
-            if (tid < kLgN) cnt[tid] = n0 + tid < k ? P.cn2[n0 + tid] : INFINITY;
-            store_chunk(0);
-            if (ct == 0)
+        }
+        // Chunk g has landed once at most the chunks issued after it (four
+        // loads each per wave) are outstanding (with it every older load:
+        // the item's norms and the next item's survivor rows); the barrier
+        // then makes every wave's part visible and frees the stage of chunk
+        // g - 1.
+        const int later = (int)(issued - 1 - g);
+        if (later >= 2)
+            asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        else if (later == 1)
+            asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        else
+            asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (more) issue_one();
+        const unsigned char* S = smem + (int)(g % kLgStages) * kLgStageBytes;
+        bf16x8 ah[2], al[2], bh[2], bl[2];
 #pragma unroll
-                for (int i = 0; i < 2; ++i) x2p[i] += rb[i].x * rb[i].x + rb[i].y * rb[i].y + rb[i].z * rb[i].z + rb[i].w * rb[i].w;
-            __syncthreads();
-            for (int c = 0; c < nch; ++c) {
-                const bool more = c + 1 < nch;
-                if (more) load_chunk(n0, c + 1);
-                // Lane (col, half): rows 64 wr + col (+ 32) of the centroid
-                // chunk and 64 wc + col (+ 32) of the survivor chunk,
-                // dimensions 8 half .. 8 half + 7.
-                const float* A = Ab + (c & 1) * kLgN * kLgRS + (64 * wr + col) * kLgRS + 8 * half;
-                const float* B = Bb + (c & 1) * kLgM * kLgRS + (64 * wc + col) * kLgRS + 8 * half;
-                float a0[8], a1[8], b0[8], b1[8];
+        for (int a = 0; a < 2; ++a) {
+            ah[a] = *reinterpret_cast<const bf16x8*>(S + ga + 2048 * a + offh);
+            al[a] = *reinterpret_cast<const bf16x8*>(S + ga + 2048 * a + offl);
+            bh[a] = *reinterpret_cast<const bf16x8*>(S + gb + 2048 * a + offh);
+            bl[a] = *reinterpret_cast<const bf16x8*>(S + gb + 2048 * a + offl);
+        }
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const f32x4 va0 = *reinterpret_cast<const f32x4*>(A + 4 * h);
-                    const f32x4 va1 = *reinterpret_cast<const f32x4*>(A + 32 * kLgRS + 4 * h);
-                    const f32x4 vb0 = *reinterpret_cast<const f32x4*>(B + 4 * h);
-                    const f32x4 vb1 = *reinterpret_cast<const f32x4*>(B + 32 * kLgRS + 4 * h);
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[a], bh[b], acc[a][b], 0, 0, 0);
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[a], bl[b], acc[a][b], 0, 0, 0);
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[a], bh[b], acc[a][b], 0, 0, 0);
+        if (++cc < nch) continue;
+
+        // Item done.  Register e of accumulator [a][cb]: centroid cn0 + 64 wr
+        // + 32 a + 8 (e / 4) + 4 half + e % 4, survivor column 64 wc + 32 cb +
+        // col; its place in the lane's list: 16 a + 4 (e / 4) + e % 4.
+        const float* nr = nrm + par * (kLgN + kLgM);
+        uint32_t KP[2][4];
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) {
+            uint32_t K[4] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
+            const float xa = nr[kLgN + 64 * wc + 32 * cb + col];
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const f32x4 cn = *reinterpret_cast<const f32x4*>(nr + 64 * wr + 32 * a + 8 * q + 4 * half);
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        a0[4 * h + e] = va0[e];
-                        a1[4 * h + e] = va1[e];
-                        b0[4 * h + e] = vb0[e];
-                        b1[4 * h + e] = vb1[e];
+                        const float v = fmaxf(fmaf(-2.f, acc[a][cb][4 * q + e], xa + cn[e]), 0.f);
+                        key4_insert(K, (__float_as_uint(v) & ~31u) | (uint32_t)(16 * a + 4 * q + e));
                     }
                 }
-#pragma unroll
-                for (int s = 0; s < kLgK / 2; ++s) {
-                    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[s], b0[s], acc[0][0], 0, 0, 0);
-                    acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[s], b1[s], acc[0][1], 0, 0, 0);
-                    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[s], b0[s], acc[1][0], 0, 0, 0);
-                    acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[s], b1[s], acc[1][1], 0, 0, 0);
-                }
-                if (more) {
-                    store_chunk((c + 1) & 1);
-                    if (ct == 0)
-#pragma unroll
-                        for (int i = 0; i < 2; ++i)
-                            x2p[i] += rb[i].x * rb[i].x + rb[i].y * rb[i].y + rb[i].z * rb[i].z + rb[i].w * rb[i].w;
-                }
-                __syncthreads();
-            }
-            if (ct == 0) {   // squared norms of the survivors: the 4 lanes of each row
-#pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    float v = x2p[i];
-                    v += __shfl_xor(v, 1);
-                    v += __shfl_xor(v, 2);
-                    if (q4 == 0) x2s[64 * i + r4] = v;
-                }
-                __syncthreads();
-            }
-            // Register e of accumulator [a][cb]: centroid n0 + 64 wr + 32 a + 8 (e / 4) + 4 half + e % 4,
-            // survivor column 64 wc + 32 cb + col.
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb) {
-                const float xa = x2s[64 * wc + 32 * cb + col];
-#pragma unroll
-                for (int a = 0; a < 2; ++a)
-#pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        const int jl = 64 * wr + 32 * a + 8 * g + 4 * half;   // 4 consecutive centroids
-                        const f32x4 cn = *reinterpret_cast<const f32x4*>(cnt + jl);
-#pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            top4_insert_next(L[cb], J[cb], xa + cn[e] - 2.f * acc[a][cb][4 * g + e], n0 + jl + e);
-                    }
-            }
-        }
-        // Merge the 4 lists of each survivor (2 waves x 2 half-waves).
-        __syncthreads();   // the chunk buffers are no longer read
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
+            // Place in the item: 64 wr + 32 a + 8 q + 4 half + e.  Clearing
+            // two more value bits can reorder the list: sort it again.
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const int slot = (wr * 2 + half) * 4 + q;
-                candD[(64 * wc + 32 * cb + col) * 16 + slot] = L[cb][q];
-                candJ[(64 * wc + 32 * cb + col) * 16 + slot] = J[cb][q];
+                const uint32_t lo = K[q] & 31u;
+                const uint32_t place = 64 * wr + 4 * half + (lo & 3u) + 8 * ((lo >> 2) & 3u) + 32 * (lo >> 4);
+                KP[cb][q] = (K[q] & ~127u) | place;
             }
-        __syncthreads();
+            sort4(KP[cb]);
+        }
+        // Half-wave h keeps column 32 h + col and merges in the other half's
+        // list of it (a lane swap; no LDS store may follow the ring's
+        // loads without waiting for them).
+        uint32_t mine[4], other[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            mine[q] = half ? KP[1][q] : KP[0][q];
+            other[q] = __shfl_xor(half ? KP[0][q] : KP[1][q], 32);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) key4_insert(mine, other[q]);
+        const int rows = min(kLgM, ns - cs0);
+        const int sc = 64 * wc + 32 * half + col;
+        if (sc < rows) {
+            uint32_t o[8];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                o[2 * q] = mine[q] & ~127u;
+                o[2 * q + 1] = (uint32_t)cn0 + (mine[q] & 127u);
+            }
+            uint4* dst = reinterpret_cast<uint4*>(Lg.cand + (((int64_t)(cs0 + sc) * nct + cn0 / kLgN) * 2 + wr) * 4);
+            dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+            dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
+        }
+        // Next item of the compute cursor.
+        cc = 0;
+        par ^= 1;
+        wcur = next_valid(wcur + G);
+        if (wcur < nitems) tile_of(wcur, cs0, cn0);
+    }
+}
 
-        // Refinement: 2 threads per survivor, each half of the dimensions.
-        const int c = tid >> 1, part = tid & 1;
-        if (c < rows)
-            refine_survivor<VEC>(P, Lg, candD, candJ, s0, c, part, first, x2s[c], cnmax, gexp, ecm, gamma,
-                                 my_changed, my_comp, my_rc);
+// ---------------------------------------------------------------------------
+// Refinement of every survivor by a thread pair (part 0 and 1, each over half
+// of the dimensions) from its candidate lists (four per centroid tile and
+// half of it): the
+// candidates within twice the expanded form's error bound of the smallest are
+// re-evaluated in the direct form, followed by the float64 near-tie rule; the
+// point's assignment and bound are written.  A survivor whose four smallest
+// all lie inside the bound (more may lie outside the lists) is queued for
+// k_full_large, which decides it in float64 over all centroids.
+//
+// Error bound of an expanded value (x and c the float32 row and centroid):
+//   - |x|^2, |c|^2, the float32 roundings: (d + 8) 2^-24 R^2 with
+//     R = |x| + max |c| (the float32 model of the other paths);
+//   - the split product: dropping lo.lo and the residuals of the two
+//     roundings costs at most 3.04 2^-16 |x_m| |c_m| per dimension;
+//   - the bf16 products are exact in float32 and each instruction adds 16
+//     of them to its accumulator; assuming an error of at most 18 units of
+//     2^-23 relative to |C| + sum |p| per instruction (true of sequential
+//     float32 additions, rounded or truncated, and of one alignment of all
+//     17 addends to the largest), the 3 ceil(d/16) instructions of a
+//     product contribute at most 6.9 d' 2^-24 sum_m |x_m| |c_m|, d' = 16
+//     ceil(d / 16);
+//   - the packed key lowers a value by less than 2^-16 of itself (<= R^2);
+//   so a value is within gexp R^2 + 2 (778 + 6.9 d') 2^-24 |x| max |c| +
+//   2^-16 R^2 of the distance, plus an absolute 2^-100 (1 + R) for bf16
+//   values below the normal range.  Rows with |x|^2 or R out of range
+//   (non-finite data) are decided in float64 over all centroids.
+
+__global__ __launch_bounds__(256) void k_refine_large(Dev P, Large Lg) {
+    IterState* st = P.st;
+    if (!st->active) return;
+    const int k = P.k, d = P.d, nct = Lg.nct;
+    const bool first = st->t == 0;
+    const uint32_t ns = *Lg.nsurv;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __shared__ float red[4];
+    float m2 = 0.f;
+    for (int j = tid; j < k; j += blockDim.x) {
+        const float v = P.cn2[j];
+        m2 = fmaxf(m2, v <= FLT_MAX ? v : INFINITY);   // a non-finite centroid: every row in float64
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) m2 = fmaxf(m2, __shfl_xor(m2, off));
+    if (lane == 0) red[wave] = m2;
+    __syncthreads();
+    const float cnmax = sqrtf(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))) * kUp;
+    const float ecm = st->ec_max;
+    const float gamma = P.gamma;
+    const float gexp = (float)(d + 8) * 0x1p-24f + 0x1p-16f;
+    const float gsp2 = 2.f * (778.f + 6.9f * (float)(16 * Lg.nch)) * 0x1p-24f * (1.f + 0x1p-10f);
+    const bool vec = (d & 3) == 0;
+    uint64_t my_changed = 0, my_comp = 0, my_rc = 0;
+    const int part = tid & 1;
+    const int hd = (d + 1) / 2, m0 = part * hd, m1 = min(d, m0 + hd);
+
+    for (int64_t c0 = (int64_t)blockIdx.x * 128; c0 < (int64_t)ns; c0 += (int64_t)gridDim.x * 128) {
+        const int64_t c = c0 + (tid >> 1);
+        if (c >= (int64_t)ns) continue;   // both threads of a pair
+        float T[4];
+        int TJ[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            T[q] = INFINITY;
+            TJ[q] = INT_MAX;
+        }
+        // The pair reads half of the 8 nct candidates each, then each merges
+        // in the other's four: the same list in both (a total order).
+        const uint4* cl = reinterpret_cast<const uint4*>(Lg.cand + c * nct * 8) + part * 2 * nct;
+        for (int q = 0; q < 2 * nct; ++q) {
+            const uint4 v = cl[q];
+            top4_insert(T, TJ, __uint_as_float(v.x), (int)v.y);
+            top4_insert(T, TJ, __uint_as_float(v.z), (int)v.w);
+        }
+        {
+            float OT[4];
+            int OJ[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                OT[q] = __shfl_xor(T[q], 1);
+                OJ[q] = __shfl_xor(TJ[q], 1);
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) top4_insert(T, TJ, OT[q], OJ[q]);
+        }
+        const int64_t i = Lg.surv[c];
+        const float* xr = P.X + i * d;
+        const int inc = first ? -1 : P.a[i];
+        const float x2 = Lg.sx2[c];
+        const float xn = sqrtf(fmaxf(x2, 0.f)) * kUp;
+        const float R = xn + cnmax;
+        const float e1 = gexp * R * R + gsp2 * xn * cnmax + 4.f * R * ecm + 2.f * ecm * ecm + 0x1p-100f * (1.f + R);
+        const float thr = T[0] + 2.f * e1;
+        // Only centroids whose expanded distance lies within thr of the
+        // smallest can be the nearest: any other one is certified farther
+        // than the smallest's centroid.
+        const bool full = T[3] <= thr || !(x2 <= 0x1p120f) || !(R <= 0x1p60f);
+        if (full) {
+            if (part == 0) {
+                Lg.fq[atomicAdd(Lg.nfull, 1u)] = (int32_t)c;
+                my_comp += (uint64_t)k;
+                my_rc += 1;
+            }
+            continue;
+        }
+        int nq = 0;
+        while (nq < 3 && T[nq] <= thr && TJ[nq] < k) ++nq;   // uniform in the pair
+        // Direct-form distance of x to centroid j over this thread's half of
+        // the dimensions, both halves added (equal in the pair).
+        auto dist32 = [&](int j) {
+            const float* cr = P.C32 + (int64_t)j * d;
+            float accd = 0.f;
+            if (vec && (m0 & 3) == 0) {
+                int m = m0;
+                for (; m + 4 <= m1; m += 4) {
+                    const f32x4 xv = *reinterpret_cast<const f32x4*>(xr + m);
+                    const f32x4 cv = *reinterpret_cast<const f32x4*>(cr + m);
+                    const float t0 = xv.x - cv.x, t1 = xv.y - cv.y, t2 = xv.z - cv.z, t3 = xv.w - cv.w;
+                    accd = fmaf(t0, t0, accd);
+                    accd = fmaf(t1, t1, accd);
+                    accd = fmaf(t2, t2, accd);
+                    accd = fmaf(t3, t3, accd);
+                }
+                for (; m < m1; ++m) {
+                    const float t = xr[m] - cr[m];
+                    accd = fmaf(t, t, accd);
+                }
+            } else {
+                for (int m = m0; m < m1; ++m) {
+                    const float t = xr[m] - cr[m];
+                    accd = fmaf(t, t, accd);
+                }
+            }
+            return accd + __shfl_xor(accd, 1);
+        };
+        auto dist64 = [&](int j) {
+            const double* cr = P.C64 + (int64_t)j * d;
+            double accd = 0.0;
+            for (int m = m0; m < m1; ++m) {
+                const double t = (double)xr[m] - cr[m];
+                accd = fma(t, t, accd);
+            }
+            return accd + __shfl_xor(accd, 1);
+        };
+        bool re = false;
+        float d1 = INFINITY, d2 = INFINITY;
+        int rk1 = INT_MAX, j1 = 0;
+        // One candidate is the nearest centroid (every other one is certified
+        // farther): as on the LDS paths, its bound then comes from its
+        // expanded value and the error bound, without the direct form (kept
+        // when statistics are gathered).
+        const bool single = nq == 1 && !(P.flags & KM_FLAG_STATS);
+        if (!single) {
+            for (int q = 0; q < nq; ++q) {
+                const int j = TJ[q];
+                const float Dd = dist32(j);
+                const int rk = j == inc ? -1 : j;
+                if (Dd < d1 || (Dd == d1 && rk < rk1)) {
+                    d2 = d1;
+                    d1 = Dd;
+                    rk1 = rk;
+                    j1 = j;
+                } else if (Dd < d2) {
+                    d2 = Dd;
+                }
+            }
+            if (d2 != INFINITY) {
+                const float band =
+                    2.f * gamma * (d1 + d2) + 4.f * (sqrtf(d1) + sqrtf(d2)) * ecm + 8.f * ecm * ecm;
+                if (d2 - d1 <= band) re = true;
+            }
+        }
+        int b = j1;
+        float ub;
+        if (single) {
+            b = TJ[0];
+            ub = __builtin_amdgcn_sqrtf(fmaxf(T[0] + e1, 0.f)) * (1.0f + 0x1p-20f) * kUp;
+        } else {
+            ub = upper_bound(d1, P.ec[j1], gamma);
+        }
+        if (re) {
+            // float64 decision against the master centroids with the oracle's
+            // rule (smaller distance, then the incumbent, then the lower
+            // index) among the candidates inside the bound.
+            double Dbb = INFINITY;
+            int bb = -1, kb = INT_MAX;
+            for (int q = 0; q < nq; ++q) {
+                const int j = TJ[q];
+                const double Dj = dist64(j);
+                const int rk = j == inc ? -1 : j;
+                if (Dj < Dbb || (Dj == Dbb && rk < kb)) {
+                    Dbb = Dj;
+                    bb = j;
+                    kb = rk;
+                }
+            }
+            b = bb < 0 ? 0 : bb;
+            ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
+        }
+        if (part == 0) {
+            if (b != inc) {
+                P.a[i] = b;
+                my_changed += 1;
+            }
+            P.u[i] = ub;
+            my_comp += (uint64_t)k;
+            my_rc += re ? 1 : 0;
+        }
     }
     my_changed = wave_sum_u64(my_changed);
     my_comp = wave_sum_u64(my_comp);
     my_rc = wave_sum_u64(my_rc);
     if (lane == 0) {
-        unsigned long long* sc =
-            reinterpret_cast<unsigned long long*>(P.total + (int64_t)k * d + k);
+        unsigned long long* sc = reinterpret_cast<unsigned long long*>(P.total + (int64_t)k * d + k);
         if (my_changed) atomicAdd(&sc[kStChanged], (unsigned long long)my_changed);
         if (my_comp) atomicAdd(&sc[kStComputed], (unsigned long long)my_comp);
         if (my_rc) atomicAdd(&sc[kStRecheck], (unsigned long long)my_rc);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Float64 decision over all centroids for the queued survivors, one block
+// each: the row in LDS as float64, every thread a strided set of centroids
+// (each distance summed over the dimensions in order), then the oracle's
+// rule (smaller distance, then the incumbent, then the lower index) across
+// the block.
+
+__global__ __launch_bounds__(256) void k_full_large(Dev P, Large Lg) {
+    IterState* st = P.st;
+    if (!st->active) return;
+    const int k = P.k, d = P.d;
+    const bool first = st->t == 0;
+    const uint32_t nf = *Lg.nfull;
+    extern __shared__ __align__(16) unsigned char smem[];
+    double* xd = reinterpret_cast<double*>(smem);   // [d]
+    __shared__ double rD[256];
+    __shared__ int rJ[256], rK[256];
+    const int tid = threadIdx.x;
+    uint64_t my_changed = 0;
+    for (uint32_t q = blockIdx.x; q < nf; q += gridDim.x) {
+        const int64_t i = Lg.surv[Lg.fq[q]];
+        __syncthreads();   // the previous survivor's row and reduction are consumed
+        for (int m = tid; m < d; m += blockDim.x) xd[m] = (double)P.X[i * d + m];
+        __syncthreads();
+        const int inc = first ? -1 : P.a[i];
+        double Db = INFINITY;
+        int bb = -1, kb = INT_MAX;
+        for (int j = tid; j < k; j += blockDim.x) {
+            const double* cr = P.C64 + (int64_t)j * d;
+            double acc = 0.0;
+            for (int m = 0; m < d; ++m) {
+                const double t = xd[m] - cr[m];
+                acc = fma(t, t, acc);
+            }
+            const int rk = j == inc ? -1 : j;
+            if (acc < Db || (acc == Db && rk < kb)) {
+                Db = acc;
+                bb = j;
+                kb = rk;
+            }
+        }
+        rD[tid] = Db;
+        rJ[tid] = bb;
+        rK[tid] = kb;
+        __syncthreads();
+        for (int w = 128; w > 0; w >>= 1) {
+            if (tid < w) {
+                const double D2 = rD[tid + w];
+                const int k2 = rK[tid + w];
+                if (D2 < rD[tid] || (D2 == rD[tid] && k2 < rK[tid])) {
+                    rD[tid] = D2;
+                    rJ[tid] = rJ[tid + w];
+                    rK[tid] = k2;
+                }
+            }
+            __syncthreads();
+        }
+        if (tid == 0) {
+            const int b = rJ[0] < 0 ? 0 : rJ[0];
+            if (b != inc) {
+                P.a[i] = b;
+                my_changed += 1;
+            }
+            P.u[i] = f32_up(sqrt(rD[0]) * (1.0 + 0x1p-40));
+        }
+    }
+    if (tid == 0 && my_changed) {
+        unsigned long long* sc = reinterpret_cast<unsigned long long*>(P.total + (int64_t)k * d + k);
+        atomicAdd(&sc[kStChanged], (unsigned long long)my_changed);
     }
 }
 
@@ -509,7 +796,10 @@ __global__ __launch_bounds__(256) void k_hist_large(Dev P, Large Lg) {
     extern __shared__ __align__(16) unsigned char smem[];
     uint32_t* h = reinterpret_cast<uint32_t*>(smem);
     const int k = P.k;
-    if (blockIdx.x == 0 && threadIdx.x == 0) *Lg.nsurv = 0;   // for the next step
+    if (blockIdx.x == 0 && threadIdx.x == 0) {   // for the next step
+        *Lg.nsurv = 0;
+        *Lg.nfull = 0;
+    }
     for (int j = threadIdx.x; j < k; j += blockDim.x) h[j] = 0;
     __syncthreads();
     const int64_t lo = (int64_t)blockIdx.x * Lg.span;
@@ -726,17 +1016,21 @@ __global__ __launch_bounds__(256) void k_centroid_table_tiled(Dev P, int force) 
 // ---------------------------------------------------------------------------
 // Launchers
 
-const void* large_mfma_symbol(int d) {
-    return (d & 3) == 0 ? reinterpret_cast<const void*>(&k_mfma_large<true>)
-                        : reinterpret_cast<const void*>(&k_mfma_large<false>);
-}
+const void* large_mfma_symbol() { return reinterpret_cast<const void*>(&k_mfma_large); }
 
 hipError_t launch_large_assign(const Dev& dv, const Large& lg, int gb, hipStream_t s) {
     hipLaunchKernelGGL(k_bound_large, dim3(gb), dim3(256), 0, s, dv, lg);
-    if ((dv.d & 3) == 0)
-        hipLaunchKernelGGL(k_mfma_large<true>, dim3(lg.Gm), dim3(256), large_mfma_lds(), s, dv, lg);
-    else
-        hipLaunchKernelGGL(k_mfma_large<false>, dim3(lg.Gm), dim3(256), large_mfma_lds(), s, dv, lg);
+    hipLaunchKernelGGL(k_mfma_large, dim3(lg.Gm), dim3(256), large_mfma_lds(), s, dv, lg);
+    hipLaunchKernelGGL(k_refine_large, dim3(lg.Gr), dim3(256), 0, s, dv, lg);
+    hipLaunchKernelGGL(k_full_large, dim3(lg.Gr), dim3(256), 8 * dv.d, s, dv, lg);
+    return hipGetLastError();
+}
+
+hipError_t launch_large_split_x(const Dev& dv, const Large& lg, int cus, hipStream_t s) {
+    int64_t g = (dv.n + 3) / 4;
+    if (g > (int64_t)cus * 16) g = (int64_t)cus * 16;
+    hipLaunchKernelGGL(k_split_rows, dim3((unsigned)g), dim3(256), 0, s, dv.X, dv.n, dv.n, dv.d, lg.nch, lg.xs,
+                       lg.x2, static_cast<const IterState*>(nullptr), 1);
     return hipGetLastError();
 }
 
@@ -757,7 +1051,9 @@ int large_table_lds(int d) { return 8 * kTiTile * d + 4 * kTiTile * 256; }
 hipError_t large_set_attributes(int k, int d) {
     hipError_t e;
     const auto attr = hipFuncAttributeMaxDynamicSharedMemorySize;
-    if ((e = hipFuncSetAttribute(large_mfma_symbol(d), attr, large_mfma_lds())) != hipSuccess) return e;
+    if ((e = hipFuncSetAttribute(large_mfma_symbol(), attr, large_mfma_lds())) != hipSuccess) return e;
+    if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_full_large), attr, 8 * d)) != hipSuccess)
+        return e;
     if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_hist_large), attr, 4 * k)) != hipSuccess)
         return e;
     if ((e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_scatter_large), attr, 4 * k)) != hipSuccess)
@@ -766,9 +1062,12 @@ hipError_t large_set_attributes(int k, int d) {
                                large_table_lds(d));
 }
 
-hipError_t launch_large_table(const Dev& dv, int force, hipStream_t s) {
+hipError_t launch_large_table(const Dev& dv, const Large& lg, int force, hipStream_t s) {
     hipLaunchKernelGGL(k_centroid_table_tiled, dim3((dv.k + kTiTile - 1) / kTiTile), dim3(256),
                        large_table_lds(dv.d), s, dv, force);
+    const int64_t kp = (int64_t)lg.nct * kLgN;   // padded to whole centroid tiles
+    hipLaunchKernelGGL(k_split_rows, dim3((unsigned)((kp + 3) / 4)), dim3(256), 0, s, static_cast<const float*>(dv.C32),
+                       kp, (int64_t)dv.k, dv.d, lg.nch, lg.cs, lg.cn2p, static_cast<const IterState*>(dv.st), force);
     return hipGetLastError();
 }
 
