@@ -90,10 +90,10 @@ inline int row_len(int d, int k) { return k * d + k + kNumStat; }
 // matrix-core distances for the Clause-1 survivors, then per-cluster sums
 // through a counting sort of the points by cluster.
 constexpr int kLgM = 128;            // survivors per block tile (matrix-core columns)
-constexpr int kLgN = 128;            // centroids per block tile (matrix-core rows)
+constexpr int kLgN = 256;            // centroids per block tile (matrix-core rows)
 constexpr int kLgK = 16;             // dimensions per streamed chunk
-constexpr int kLgStages = 4;         // chunks in flight per block (LDS ring)
-constexpr int kLgStageBytes = 2 * kLgN * 4 * kLgK;   // one chunk of the centroid and survivor tiles
+constexpr int kLgStages = 3;         // LDS ring stages (chunks loaded ahead: kLgStages - 1)
+constexpr int kLgStageBytes = (kLgN + kLgM) * 4 * kLgK;   // one chunk of the centroid and survivor tiles
 constexpr int kLgChunkRows = 256;    // rows per segment-sum chunk
 constexpr int kLgMaxD = 4096;        // largest d of the global-memory path
 

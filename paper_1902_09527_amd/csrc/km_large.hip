@@ -190,23 +190,25 @@ __global__ __launch_bounds__(256) void k_split_rows(const float* __restrict__ sr
 
 // ---------------------------------------------------------------------------
 // Dense survivor distances on the matrix cores.  A work item is one tile of
-// kLgM = 128 survivors against one tile of kLgN = 128 centroids; wave
-// (wr, wc) of the block owns centroid rows 64 wr .. +63 and survivor columns
-// 64 wc .. +63, four 32x32 float32 accumulators.  Each product x.c is formed
-// from the split operands as hi.hi + hi.lo + lo.hi: three bf16 products on
-// v_mfma_f32_32x32x16_bf16 (16 dimensions each) in place of eight float32
-// ones, with the dropped lo.lo term and the accumulation inside the error
-// bound used by the refinement pass.
+// kLgM = 128 survivors against one tile of kLgN = 256 centroids; wave
+// (wr, wc) of the block owns centroid rows 128 wr .. +127 and survivor
+// columns 64 wc .. +63, eight 32x32 float32 accumulators.  Each product x.c
+// is formed from the split operands as hi.hi + hi.lo + lo.hi: three bf16
+// products on v_mfma_f32_32x32x16_bf16 (16 dimensions each) in place of
+// eight float32 ones, with the dropped lo.lo term and the accumulation
+// inside the error bound used by the refinement pass.
 //
 // The 16-dimension chunks of a block's items form one stream that runs
 // kLgStages - 1 chunks ahead of the products, across item boundaries (the
 // next item's first chunks load during the current item's selection).  They
 // go from the split rows straight into a ring of kLgStages LDS stages by
-// global_load_lds_dwordx4 (no registers held); a stage is two tiles of 128
-// rows x 64 bytes in 1 KB groups of 16 rows, the four 16-byte pieces of each
-// row permuted by lg_swz so that the operand reads of eight (and of sixteen)
-// consecutive lanes fall on distinct banks.  Loads return in order, so chunk
-// g has landed once at most the loads issued after it are outstanding.
+// global_load_lds_dwordx4 (no registers held); a stage is two tiles (256
+// and 128 rows x 64 bytes) in 1 KB groups of 16 rows, the four 16-byte
+// pieces of each row permuted by lg_swz so that the operand reads of eight
+// (and of sixteen) consecutive lanes fall on distinct banks.  Loads return
+// in order, so chunk g has landed once at most the loads issued after it
+// are outstanding.  Loads in flight per CU are bounded by LDS, so the tile
+// is wide: 24 products per wave and chunk for 24 KB.
 //
 // Work items are ordered so that the nct items of a survivor tile carry
 // indices congruent modulo 8: with a resident grid whose size is a multiple
@@ -216,12 +218,12 @@ __global__ __launch_bounds__(256) void k_split_rows(const float* __restrict__ sr
 // Selection: each expanded distance |x|^2 + |c|^2 - 2 x.c is clamped at 0
 // (the true distance is >= 0, so the error bound still holds) and packed
 // with its centroid into one ordered 32-bit key: the float's bits with the
-// low 7 bits (5 within a lane's list) replaced by the centroid's place in
-// the item, which lowers the value by less than 2^-16 of itself.  A lane
+// low 8 bits (6 within a lane's list) replaced by the centroid's place in
+// the item, which lowers the value by less than 2^-15 of itself.  A lane
 // keeps, per survivor column, the four smallest keys by min and med3
 // (branch-free); the two half-waves' lists of a column are merged by a lane
 // swap, and each wave writes the four smallest (value, centroid) pairs of
-// its 64 centroids to the candidate buffer.
+// its 128 centroids to the candidate buffer.
 
 __device__ __forceinline__ int lg_swz(int rho) { return ((rho >> 2) & 3) ^ (((rho >> 1) & 1) << 1); }
 
@@ -266,8 +268,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 31, half = lane >> 5;
     const int wr = wave >> 1, wc = wave & 1;
     extern __shared__ __align__(16) unsigned char smem[];
-    float* nrm = reinterpret_cast<float*>(smem + kLgStages * kLgStageBytes);   // [2][kLgN + kLgM]: |c|^2 of the centroid tile,
-                                                             // then |x|^2 of the survivors (by item parity)
+    // [2][kLgN + kLgM] by item parity: |c|^2 of the centroid tile, then |x|^2 of the survivors.
+    float* nrm = reinterpret_cast<float*>(smem + kLgStages * kLgStageBytes);
     int32_t* meta = reinterpret_cast<int32_t*>(nrm + 2 * (kLgN + kLgM));   // [2][4 waves][64]: survivor rows
 
     const int nst = (ns + kLgM - 1) / kLgM;
@@ -290,15 +292,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     };
 
     // DMA role of this lane in a 16-row group: row rho, LDS slot lane, piece
-    // (lane % 4) ^ lg_swz(rho) of the row's chunk; this wave streams row
-    // groups 2 wave and 2 wave + 1 of both tiles.
+    // (lane % 4) ^ lg_swz(rho) of the row's chunk.  This wave streams
+    // centroid rows 64 wave .. +63 (groups 4 wave .. 4 wave + 3) and
+    // survivor rows 32 wave .. +31 (groups 2 wave, 2 wave + 1).
     const int rho = lane >> 2, piece = (lane & 3) ^ lg_swz(rho);
     const int sr0 = 32 * wave + rho;
     // Operand reads of lane (col, half): row col of a 32-row block, pieces
     // half (hi) and 2 + half (lo), at these offsets in its 1 KB group.
     const int rr = col & 15;
     const int offh = 16 * (4 * rr + (half ^ lg_swz(rr))), offl = 16 * (4 * rr + ((2 + half) ^ lg_swz(rr)));
-    const int ga = (4 * wr + (col >> 4)) * 1024, gb = kLgN * 64 + (4 * wc + (col >> 4)) * 1024;
+    const int ga = (8 * wr + (col >> 4)) * 1024, gb = kLgN * 64 + (4 * wc + (col >> 4)) * 1024;
     const int64_t rowb = (int64_t)nch * 64;   // bytes per split row
     const unsigned char* csb = reinterpret_cast<const unsigned char*>(Lg.cs) + 16 * piece;
     const unsigned char* xsb = reinterpret_cast<const unsigned char*>(Lg.xs) + 16 * piece;
@@ -308,8 +311,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     // Item metadata goes to LDS by direct loads too (nothing loaded is held
     // in registers across the loop): the survivor rows of this wave's two
     // row groups (lane l: row 32 wave + l % 32; rows past the list repeat
-    // the first), and the 128 centroid and 128 survivor squared norms
-    // (waves 0-1 and 2-3, one per lane; survivors past the list read the
+    // the first), the 256 centroid squared norms (64 per wave) and the 128
+    // survivor squared norms (waves 0-1; survivors past the list read the
     // first).
     auto load_meta = [&](int s0, int par) __attribute__((always_inline)) {
         const int r = 32 * wave + (lane & 31);
@@ -317,14 +320,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
                                          4, 0, 0);
     };
     auto load_norms = [&](int s0, int n0, int par) __attribute__((always_inline)) {
-        const float* src;
+        float* dst = nrm + par * (kLgN + kLgM) + 64 * wave;
+        __builtin_amdgcn_global_load_lds(cn2p + n0 + tid, (lds_ptr)(dst), 4, 0, 0);
         if (wave < 2) {
-            src = cn2p + n0 + tid;
-        } else {
-            const int sl = tid - kLgN;
-            src = sx2 + s0 + (s0 + sl < ns ? sl : 0);
+            const int sl = tid;
+            __builtin_amdgcn_global_load_lds(sx2 + s0 + (s0 + sl < ns ? sl : 0), (lds_ptr)(dst + kLgN), 4, 0, 0);
         }
-        __builtin_amdgcn_global_load_lds(src, (lds_ptr)(nrm + par * (kLgN + kLgM) + wave * 64), 4, 0, 0);
     };
 
     // Issue cursor: item wi, its next chunk ci, its parity ipar; wn the item
@@ -338,7 +339,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     {
         const int rows = min(kLgM, ns - is0);
         const int q0 = surv[is0 + (sr0 < rows ? sr0 : 0)], q1 = surv[is0 + (sr0 + 16 < rows ? sr0 + 16 : 0)];
-        pa = csb + (int64_t)(in0 + sr0) * rowb;
+        pa = csb + (int64_t)(in0 + 64 * wave + rho) * rowb;
         pb0 = xsb + (int64_t)q0 * rowb;
         pb1 = xsb + (int64_t)q1 * rowb;
     }
@@ -360,7 +361,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
             tile_of(wi, is0, in0);
             const int* mrow = meta + ipar * 256 + wave * 64;
             const int q0 = mrow[rho], q1 = mrow[16 + rho];
-            pa = csb + (int64_t)(in0 + sr0) * rowb;
+            pa = csb + (int64_t)(in0 + 64 * wave + rho) * rowb;
             pb0 = xsb + (int64_t)q0 * rowb;
             pb1 = xsb + (int64_t)q1 * rowb;
             load_norms(is0, in0, ipar);
@@ -371,12 +372,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
                 load_meta(s1, ipar ^ 1);
             }
         }
-        unsigned char* base = smem + (int)(issued % kLgStages) * kLgStageBytes + 2 * wave * 1024;
+        unsigned char* base = smem + (int)(issued % kLgStages) * kLgStageBytes;
         const int64_t o = (int64_t)ci * 64;
-        __builtin_amdgcn_global_load_lds(pa + o, (lds_ptr)(base), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(pa + 16 * rowb + o, (lds_ptr)(base + 1024), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(pb0 + o, (lds_ptr)(base + kLgN * 64), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(pb1 + o, (lds_ptr)(base + kLgN * 64 + 1024), 16, 0, 0);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            __builtin_amdgcn_global_load_lds(pa + 16 * t * rowb + o, (lds_ptr)(base + (4 * wave + t) * 1024), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(pb0 + o, (lds_ptr)(base + kLgN * 64 + 2 * wave * 1024), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(pb1 + o, (lds_ptr)(base + kLgN * 64 + (2 * wave + 1) * 1024), 16, 0, 0);
         ++issued;
         if (++ci == nch && wn >= nitems) more = false;
     };
@@ -386,56 +388,54 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     const int ahead = min(kLgStages - 1, nch);
     for (int e = 0; e < ahead && more; ++e) issue_one();
 
-    f32x16 acc[2][2];
+    f32x16 acc[4][2];
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
     for (int64_t g = 0; g < issued; ++g) {
-        if (cc == 0) {
-#pragma unroll
-            for (int a = 0; a < 2; ++a)
-#pragma unroll
-                for (int b = 0; b < 2; ++b)
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
-        }
-        // Chunk g has landed once at most the chunks issued after it (four
+        // Chunk g has landed once at most the chunks issued after it (six
         // loads each per wave) are outstanding (with it every older load:
         // the item's norms and the next item's survivor rows); the barrier
         // then makes every wave's part visible and frees the stage of chunk
-        // g - 1.
-        const int later = (int)(issued - 1 - g);
-        if (later >= 2)
-            asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-        else if (later == 1)
-            asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        // g - 1 for the load issued next.
+        if (issued - 1 - g >= 1)
+            asm volatile("s_waitcnt vmcnt(6) lgkmcnt(0)\n\ts_barrier" ::: "memory");
         else
             asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
         if (more) issue_one();
         const unsigned char* S = smem + (int)(g % kLgStages) * kLgStageBytes;
-        bf16x8 ah[2], al[2], bh[2], bl[2];
+        bf16x8 ah[4], al[4], bh[2], bl[2];
 #pragma unroll
-        for (int a = 0; a < 2; ++a) {
+        for (int a = 0; a < 4; ++a) {
             ah[a] = *reinterpret_cast<const bf16x8*>(S + ga + 2048 * a + offh);
             al[a] = *reinterpret_cast<const bf16x8*>(S + ga + 2048 * a + offl);
-            bh[a] = *reinterpret_cast<const bf16x8*>(S + gb + 2048 * a + offh);
-            bl[a] = *reinterpret_cast<const bf16x8*>(S + gb + 2048 * a + offl);
         }
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int b = 0; b < 2; ++b) {
+            bh[b] = *reinterpret_cast<const bf16x8*>(S + gb + 2048 * b + offh);
+            bl[b] = *reinterpret_cast<const bf16x8*>(S + gb + 2048 * b + offl);
+        }
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
 #pragma unroll
             for (int b = 0; b < 2; ++b)
                 acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[a], bh[b], acc[a][b], 0, 0, 0);
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int a = 0; a < 4; ++a)
 #pragma unroll
             for (int b = 0; b < 2; ++b)
                 acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[a], bl[b], acc[a][b], 0, 0, 0);
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int a = 0; a < 4; ++a)
 #pragma unroll
             for (int b = 0; b < 2; ++b)
                 acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[a], bh[b], acc[a][b], 0, 0, 0);
         if (++cc < nch) continue;
 
-        // Item done.  Register e of accumulator [a][cb]: centroid cn0 + 64 wr
+        // Item done.  Register e of accumulator [a][cb]: centroid cn0 + 128 wr
         // + 32 a + 8 (e / 4) + 4 half + e % 4, survivor column 64 wc + 32 cb +
         // col; its place in the lane's list: 16 a + 4 (e / 4) + e % 4.
         const float* nr = nrm + par * (kLgN + kLgM);
@@ -445,29 +445,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
             uint32_t K[4] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
             const float xa = nr[kLgN + 64 * wc + 32 * cb + col];
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
+            for (int a = 0; a < 4; ++a)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const f32x4 cn = *reinterpret_cast<const f32x4*>(nr + 64 * wr + 32 * a + 8 * q + 4 * half);
+                    const f32x4 cn = *reinterpret_cast<const f32x4*>(nr + 128 * wr + 32 * a + 8 * q + 4 * half);
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const float v = fmaxf(fmaf(-2.f, acc[a][cb][4 * q + e], xa + cn[e]), 0.f);
-                        key4_insert(K, (__float_as_uint(v) & ~31u) | (uint32_t)(16 * a + 4 * q + e));
+                        key4_insert(K, (__float_as_uint(v) & ~63u) | (uint32_t)(16 * a + 4 * q + e));
                     }
                 }
-            // Place in the item: 64 wr + 32 a + 8 q + 4 half + e.  Clearing
+            // Place in the item: 128 wr + 32 a + 8 q + 4 half + e.  Clearing
             // two more value bits can reorder the list: sort it again.
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const uint32_t lo = K[q] & 31u;
-                const uint32_t place = 64 * wr + 4 * half + (lo & 3u) + 8 * ((lo >> 2) & 3u) + 32 * (lo >> 4);
-                KP[cb][q] = (K[q] & ~127u) | place;
+                const uint32_t lo = K[q] & 63u;
+                const uint32_t place = 128 * wr + 4 * half + (lo & 3u) + 8 * ((lo >> 2) & 3u) + 32 * (lo >> 4);
+                KP[cb][q] = (K[q] & ~255u) | place;
             }
             sort4(KP[cb]);
         }
         // Half-wave h keeps column 32 h + col and merges in the other half's
-        // list of it (a lane swap; no LDS store may follow the ring's
-        // loads without waiting for them).
+        // list of it (a lane swap; no LDS store may follow the ring's loads
+        // without waiting for them).
         uint32_t mine[4], other[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -482,8 +482,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
             uint32_t o[8];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                o[2 * q] = mine[q] & ~127u;
-                o[2 * q + 1] = (uint32_t)cn0 + (mine[q] & 127u);
+                o[2 * q] = mine[q] & ~255u;
+                o[2 * q + 1] = (uint32_t)cn0 + (mine[q] & 255u);
             }
             uint4* dst = reinterpret_cast<uint4*>(Lg.cand + (((int64_t)(cs0 + sc) * nct + cn0 / kLgN) * 2 + wr) * 4);
             dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
@@ -494,6 +494,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         par ^= 1;
         wcur = next_valid(wcur + G);
         if (wcur < nitems) tile_of(wcur, cs0, cn0);
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
     }
 }
 
@@ -519,9 +525,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 //     17 addends to the largest), the 3 ceil(d/16) instructions of a
 //     product contribute at most 6.9 d' 2^-24 sum_m |x_m| |c_m|, d' = 16
 //     ceil(d / 16);
-//   - the packed key lowers a value by less than 2^-16 of itself (<= R^2);
+//   - the packed key lowers a value by less than 2^-15 of itself (<= R^2);
 //   so a value is within gexp R^2 + 2 (778 + 6.9 d') 2^-24 |x| max |c| +
-//   2^-16 R^2 of the distance, plus an absolute 2^-100 (1 + R) for bf16
+//   2^-15 R^2 of the distance, plus an absolute 2^-100 (1 + R) for bf16
 //   values below the normal range.  Rows with |x|^2 or R out of range
 //   (non-finite data) are decided in float64 over all centroids.
 
@@ -545,7 +551,7 @@ __global__ __launch_bounds__(256) void k_refine_large(Dev P, Large Lg) {
     const float cnmax = sqrtf(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))) * kUp;
     const float ecm = st->ec_max;
     const float gamma = P.gamma;
-    const float gexp = (float)(d + 8) * 0x1p-24f + 0x1p-16f;
+    const float gexp = (float)(d + 8) * 0x1p-24f + 0x1p-15f;
     const float gsp2 = 2.f * (778.f + 6.9f * (float)(16 * Lg.nch)) * 0x1p-24f * (1.f + 0x1p-10f);
     const bool vec = (d & 3) == 0;
     uint64_t my_changed = 0, my_comp = 0, my_rc = 0;
