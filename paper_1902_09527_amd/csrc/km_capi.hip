@@ -521,13 +521,14 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         L.Gr = 4 * cus;
         L.nch = km::split_chunks(d);
         L.nct = (k + km::kLgN - 1) / km::kLgN;
+        L.mvcap = (int32_t)(n / 16 > 1024 ? n / 16 : (n < 1024 ? n : 1024));
         int64_t gs = (n + 4095) / 4096;
         if (gs > 2048) gs = 2048;
         L.Gs = (int32_t)gs;
         L.span = (n + gs - 1) / gs;
         L.NCmax = (int32_t)(n / km::kLgChunkRows + k + 1);
-        int64_t gb = (n + 255) / 256;
-        if (gb > (int64_t)cus * 8) gb = (int64_t)cus * 8;
+        const int64_t gb = (n + km::kLgBoundSpan - 1) / km::kLgBoundSpan;   // one block per span of points
+        if (gb > INT_MAX) return KM_ERR_INVALID_ARG;
         c->gb = (int)gb;
         v.G = 1;
         if ((rc2 = c->alloc(&L.surv, (size_t)n)) || (rc2 = c->alloc(&L.nsurv, 4)) ||
@@ -537,13 +538,16 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             (rc2 = c->alloc(&L.ciq, (size_t)L.NCmax)) ||
             (rc2 = c->alloc(&L.xs, (size_t)n * L.nch * 16)) || (rc2 = c->alloc(&L.x2, (size_t)n)) ||
             (rc2 = c->alloc(&L.sx2, (size_t)n)) || (rc2 = c->alloc(&L.fq, (size_t)n)) ||
-            (rc2 = c->alloc(&L.nfull, 4)) ||
+            (rc2 = c->alloc(&L.nfull, 4)) || (rc2 = c->alloc(&L.nmv, 4)) ||
+            (rc2 = c->alloc(&L.mv, (size_t)L.mvcap)) || (rc2 = c->alloc(&v.sums, (size_t)k * d + k)) ||
             (rc2 = c->alloc(&L.cs, (size_t)L.nct * km::kLgN * L.nch * 16)) ||
-            (rc2 = c->alloc(&L.cn2p, (size_t)L.nct * km::kLgN)) ||
+            (rc2 = c->alloc(&L.cn2p, (size_t)L.nct * km::kLgN)) || (rc2 = c->alloc(&L.smin, (size_t)km::kLgTableSplit * k)) ||
             (rc2 = c->alloc(&L.cand, (size_t)n * L.nct * 8)))
             return rc2;
         zr.add(L.nsurv, 4 * sizeof(uint32_t));
         zr.add(L.nfull, 4 * sizeof(uint32_t));
+        zr.add(L.nmv, 4 * sizeof(uint32_t));
+        zr.add(v.sums, sizeof(uint64_t) * ((size_t)k * d + k));
     }
 
     int rc;

@@ -95,6 +95,9 @@ constexpr int kLgK = 16;             // dimensions per streamed chunk
 constexpr int kLgStages = 3;         // LDS ring stages (chunks loaded ahead: kLgStages - 1)
 constexpr int kLgStageBytes = (kLgN + kLgM) * 4 * kLgK;   // one chunk of the centroid and survivor tiles
 constexpr int kLgChunkRows = 256;    // rows per segment-sum chunk
+constexpr int kLgBoundRounds = 4;    // rounds of 256 points per block of the bound pass
+constexpr int kLgBoundSpan = 256 * kLgBoundRounds;
+constexpr int kLgTableSplit = 4;     // block columns (centroid ranges) of the tiled centroid table
 constexpr int kLgMaxD = 4096;        // largest d of the global-memory path
 
 // Split rows (the matrix-core operands of the global path): every float32
@@ -106,7 +109,7 @@ inline int split_chunks(int d) { return (d + kLgK - 1) / kLgK; }
 
 struct Large {
     int32_t* surv;        // n: survivor point indices of the current step
-    uint32_t* nsurv;      // survivor count (zeroed by the histogram pass for the next step)
+    uint32_t* nsurv;      // survivor count
     uint32_t* cnt;        // Gs x k per-block cluster counts
     uint32_t* off;        // Gs x k per-block write offsets
     uint32_t* base;       // k + 1 cluster starts in perm
@@ -118,9 +121,13 @@ struct Large {
     float* x2;            // n: float32 squared norms of the rows of X (set-up)
     float* sx2;           // n: x2 of the survivors, in list order
     int32_t* fq;          // n: survivors (list entries) decided over all centroids
-    uint32_t* nfull;      // their count (zeroed by the histogram pass for the next step)
+    uint32_t* nfull;      // their count
+    int4* mv;             // mvcap moves of the step: point, old cluster, new cluster
+    uint32_t* nmv;        // their count (nsurv, nfull, nmv: zeroed by the centroid-table pass)
+    int32_t mvcap;        // at most this many moves: incremental sums, else full sums
     uint32_t* cs;         // nct * kLgN split rows of the float32 centroids (rows >= k zero)
     float* cn2p;          // nct * kLgN: their float32 squared norms (rows >= k: +inf)
+    float* smin;          // kLgTableSplit x k: column minima of the half-distance table (reduced to s)
     uint2* cand;          // n x nct x 2 x 4: per survivor, centroid tile and half of it, the four
                           // smallest expanded distances (float bits) with their centroids
     int32_t nch;          // chunks per split row

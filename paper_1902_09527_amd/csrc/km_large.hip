@@ -20,8 +20,9 @@
 //   k_chunk_reduce_large  per-cluster sums, counts and the inertia into the
 //                       reduced row read by k_update;
 //   k_centroid_table_tiled  half centroid distances for the next step;
-//   k_split_rows        split operand rows of the new centroids (and, once at
-//                       set-up, of X with its squared norms).
+//   k_split_rows        split operand rows of the new centroids with their
+//                       squared norms and the per-centroid minimum s of the
+//                       table (and, once at set-up, split rows of X).
 // The order of points inside a cluster segment is not fixed, but every sum
 // is an exact integer sum, so results are bitwise reproducible.
 #include <float.h>
@@ -37,6 +38,7 @@ namespace km {
 namespace {
 
 constexpr int kTiTile = 16;   // centroid rows per block of the tiled centroid table
+constexpr int kTiSplit = kLgTableSplit;
 
 // Insert (v, j) into an ascending 4-list ordered by value, then index.
 __device__ inline void top4_insert(float (&L)[4], int (&J)[4], float v, int j) {
@@ -77,6 +79,14 @@ __device__ __forceinline__ void top4_insert_next(float (&L)[4], int (&J)[4], flo
     }
 }
 
+// The step's per-cluster sums come from its moves (added to the running
+// sums kept by k_update) when few points moved; otherwise from the counting
+// sort and exact segment sums.  The first step, and steps that gather the
+// inertia, always take the full sums.
+__device__ __forceinline__ bool large_incremental(const Dev& P, const Large& Lg) {
+    return P.st->t > 0 && !(P.flags & KM_FLAG_STATS) && *Lg.nmv <= (uint32_t)Lg.mvcap;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -91,13 +101,20 @@ __global__ __launch_bounds__(256) void k_bound_large(Dev P, Large Lg) {
     if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 1;
     const bool first = st->t == 0;
     const bool prune = !(P.flags & KM_FLAG_NO_PRUNE);
-    const int lane = threadIdx.x & 63;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __shared__ uint32_t cnt[kLgBoundRounds * 4], base[kLgBoundRounds * 4];
+    // Block b owns points [b kLgBoundSpan, (b + 1) kLgBoundSpan): the flags
+    // of its rounds of 256 stay in a bit mask, the block's survivors take
+    // one atomic on the list counter, then every survivor its place (block
+    // order, then point order).
+    const int64_t lo = (int64_t)blockIdx.x * kLgBoundSpan, hi = min(P.n, lo + kLgBoundSpan);
     uint64_t c1 = 0;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x; i0 < P.n; i0 += stride) {
-        const int64_t i = i0 + threadIdx.x;
+    uint32_t mask = 0;
+#pragma unroll
+    for (int r = 0; r < kLgBoundRounds; ++r) {
+        const int64_t i = lo + 256 * r + tid;
         bool surv = false;
-        if (i < P.n) {
+        if (i < hi) {
             if (first) {
                 surv = true;
             } else {
@@ -111,16 +128,30 @@ __global__ __launch_bounds__(256) void k_bound_large(Dev P, Large Lg) {
                 }
             }
         }
+        mask |= (surv ? 1u : 0u) << r;
         const uint64_t m = __ballot(surv);
-        if (m) {
-            uint32_t b = 0;
-            if (lane == 0) b = atomicAdd(Lg.nsurv, (uint32_t)__popcll(m));
-            b = __shfl(b, 0);
-            if (surv) {
-                const uint32_t pos = b + __popcll(m & ((1ull << lane) - 1ull));
-                Lg.surv[pos] = (int32_t)i;
-                Lg.sx2[pos] = Lg.x2[i];
-            }
+        if (lane == 0) cnt[4 * r + wave] = (uint32_t)__popcll(m);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t tot = 0;
+        for (int q = 0; q < kLgBoundRounds * 4; ++q) {
+            base[q] = tot;
+            tot += cnt[q];
+        }
+        const uint32_t b0 = tot ? atomicAdd(Lg.nsurv, tot) : 0u;
+        for (int q = 0; q < kLgBoundRounds * 4; ++q) base[q] += b0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kLgBoundRounds; ++r) {
+        const bool surv = (mask >> r) & 1u;
+        const uint64_t m = __ballot(surv);
+        if (surv) {
+            const int64_t i = lo + 256 * r + tid;
+            const uint32_t pos = base[4 * r + wave] + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+            Lg.surv[pos] = (int32_t)i;
+            Lg.sx2[pos] = Lg.x2[i];
         }
     }
     c1 = wave_sum_u64(c1);
@@ -155,7 +186,8 @@ __device__ __forceinline__ uint32_t split_lo(float a, float b) {
 
 __global__ __launch_bounds__(256) void k_split_rows(const float* __restrict__ src, int64_t rows, int64_t valid, int d,
                                                     int nch, uint32_t* __restrict__ dst, float* __restrict__ norms,
-                                                    const IterState* st, int force) {
+                                                    const IterState* st, int force, const float* __restrict__ smin,
+                                                    float* __restrict__ s_out) {
     if (st && !force && !st->active) return;
     const int lane = threadIdx.x & 63;
     const int64_t wstride = (int64_t)gridDim.x * (blockDim.x >> 6);
@@ -184,7 +216,14 @@ __global__ __launch_bounds__(256) void k_split_rows(const float* __restrict__ sr
         }
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
-        if (lane == 0) norms[r] = pad ? INFINITY : sq;
+        if (lane == 0) {
+            norms[r] = pad ? INFINITY : sq;
+            if (smin && !pad) {   // min over j != r of the half distances: the table's column minima
+                float m = INFINITY;
+                for (int y = 0; y < kTiSplit; ++y) m = fminf(m, smin[(int64_t)y * valid + r]);
+                s_out[r] = m;
+            }
+        }
     }
 }
 
@@ -558,9 +597,12 @@ __global__ __launch_bounds__(256) void k_refine_large(Dev P, Large Lg) {
     const int part = tid & 1;
     const int hd = (d + 1) / 2, m0 = part * hd, m1 = min(d, m0 + hd);
 
+    const bool rec_moves = !first && !(P.flags & KM_FLAG_STATS);
     for (int64_t c0 = (int64_t)blockIdx.x * 128; c0 < (int64_t)ns; c0 += (int64_t)gridDim.x * 128) {
         const int64_t c = c0 + (tid >> 1);
-        if (c >= (int64_t)ns) continue;   // both threads of a pair
+        int4 mvr = make_int4(0, 0, 0, 0);
+        bool moved = false;
+        if (c < (int64_t)ns) {   // both threads of a pair
         float T[4];
         int TJ[4];
 #pragma unroll
@@ -605,8 +647,7 @@ __global__ __launch_bounds__(256) void k_refine_large(Dev P, Large Lg) {
                 my_comp += (uint64_t)k;
                 my_rc += 1;
             }
-            continue;
-        }
+        } else {
         int nq = 0;
         while (nq < 3 && T[nq] <= thr && TJ[nq] < k) ++nq;   // uniform in the pair
         // Direct-form distance of x to centroid j over this thread's half of
@@ -705,10 +746,25 @@ __global__ __launch_bounds__(256) void k_refine_large(Dev P, Large Lg) {
             if (b != inc) {
                 P.a[i] = b;
                 my_changed += 1;
+                moved = true;
+                mvr = make_int4((int)i, inc, b, 0);
             }
             P.u[i] = ub;
             my_comp += (uint64_t)k;
             my_rc += re ? 1 : 0;
+        }
+        }   // not full
+        }   // c < ns
+        // Moves to the list, one atomic per wave.
+        if (rec_moves) {
+            const uint64_t m = __ballot(moved);
+            if (m) {
+                uint32_t base = 0;
+                if (lane == 0) base = atomicAdd(Lg.nmv, (uint32_t)__popcll(m));
+                base = __shfl(base, 0);
+                const uint32_t q = base + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+                if (moved && q < (uint32_t)Lg.mvcap) Lg.mv[q] = mvr;
+            }
         }
     }
     my_changed = wave_sum_u64(my_changed);
@@ -784,6 +840,10 @@ __global__ __launch_bounds__(256) void k_full_large(Dev P, Large Lg) {
             if (b != inc) {
                 P.a[i] = b;
                 my_changed += 1;
+                if (!first && !(P.flags & KM_FLAG_STATS)) {
+                    const uint32_t qm = atomicAdd(Lg.nmv, 1u);
+                    if (qm < (uint32_t)Lg.mvcap) Lg.mv[qm] = make_int4((int)i, inc, b, 0);
+                }
             }
             P.u[i] = f32_up(sqrt(rD[0]) * (1.0 + 0x1p-40));
         }
@@ -798,14 +858,10 @@ __global__ __launch_bounds__(256) void k_full_large(Dev P, Large Lg) {
 // Counting sort of the points by their new cluster.
 
 __global__ __launch_bounds__(256) void k_hist_large(Dev P, Large Lg) {
-    if (!P.st->active) return;
+    if (!P.st->active || large_incremental(P, Lg)) return;
     extern __shared__ __align__(16) unsigned char smem[];
     uint32_t* h = reinterpret_cast<uint32_t*>(smem);
     const int k = P.k;
-    if (blockIdx.x == 0 && threadIdx.x == 0) {   // for the next step
-        *Lg.nsurv = 0;
-        *Lg.nfull = 0;
-    }
     for (int j = threadIdx.x; j < k; j += blockDim.x) h[j] = 0;
     __syncthreads();
     const int64_t lo = (int64_t)blockIdx.x * Lg.span;
@@ -818,7 +874,7 @@ __global__ __launch_bounds__(256) void k_hist_large(Dev P, Large Lg) {
 // Per cluster j: exclusive prefix of the block counts (write offsets
 // relative to the cluster start) and the cluster size into base[j].
 __global__ __launch_bounds__(256) void k_scan_large_cols(Dev P, Large Lg) {
-    if (!P.st->active) return;
+    if (!P.st->active || large_incremental(P, Lg)) return;
     const int j = blockIdx.x * blockDim.x + threadIdx.x;
     if (j >= P.k) return;
     uint32_t run = 0;
@@ -834,7 +890,7 @@ __global__ __launch_bounds__(256) void k_scan_large_cols(Dev P, Large Lg) {
 // One block: cluster starts (exclusive scan of the sizes) and the first
 // segment chunk of every cluster.  base[k] = n, cbase[k] = chunk count.
 __global__ __launch_bounds__(1024) void k_scan_large_clusters(Dev P, Large Lg) {
-    if (!P.st->active) return;
+    if (!P.st->active || large_incremental(P, Lg)) return;
     const int k = P.k, t = threadIdx.x, T = blockDim.x;
     __shared__ uint32_t ps[1024], pc[1024];
     const int per = (k + T - 1) / T, j0 = t * per, j1 = min(k, j0 + per);
@@ -869,7 +925,7 @@ __global__ __launch_bounds__(1024) void k_scan_large_clusters(Dev P, Large Lg) {
 }
 
 __global__ __launch_bounds__(256) void k_scatter_large(Dev P, Large Lg) {
-    if (!P.st->active) return;
+    if (!P.st->active || large_incremental(P, Lg)) return;
     extern __shared__ __align__(16) unsigned char smem[];
     uint32_t* pos = reinterpret_cast<uint32_t*>(smem);
     const int k = P.k;
@@ -887,7 +943,7 @@ __global__ __launch_bounds__(256) void k_scatter_large(Dev P, Large Lg) {
 // distances to the cluster's current centroid, element by element).
 __global__ __launch_bounds__(256) void k_segsum_large(Dev P_, Large Lg) {
     const Dev P = with_scales(P_);
-    if (!P.st->active) return;
+    if (!P.st->active || large_incremental(P, Lg)) return;
     const int c = blockIdx.x;
     const int k = P.k, d = P.d;
     if (c >= (int)Lg.cbase[k]) return;
@@ -925,17 +981,21 @@ __global__ __launch_bounds__(256) void k_segsum_large(Dev P_, Large Lg) {
 }
 
 // Per-cluster sums (over the cluster's chunks) and counts into the reduced
-// row; block 0 also adds the inertia partials.
+// row, less the running sums that k_update adds back; block 0 also adds the
+// inertia partials.
 __global__ __launch_bounds__(256) void k_chunk_reduce_large(Dev P, Large Lg) {
-    if (!P.st->active) return;
+    if (!P.st->active || large_incremental(P, Lg)) return;
     const int k = P.k, d = P.d;
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e < (int64_t)k * d) {
         const int j = (int)(e / d), m = (int)(e - (int64_t)j * d);
         uint64_t acc = 0;
         for (uint32_t cc = Lg.cbase[j]; cc < Lg.cbase[j + 1]; ++cc) acc += Lg.cpart[(int64_t)cc * d + m];
-        P.total[e] = acc;
-        if (m == 0) P.total[(int64_t)k * d + j] = Lg.base[j + 1] - Lg.base[j];
+        P.total[e] = acc - P.sums[e];
+        if (m == 0) {
+            const int64_t o = (int64_t)k * d + j;
+            P.total[o] = (uint64_t)(Lg.base[j + 1] - Lg.base[j]) - P.sums[o];
+        }
     }
     if (blockIdx.x == 0 && (P.flags & KM_FLAG_STATS)) {
         __shared__ uint64_t rs[4];
@@ -949,14 +1009,46 @@ __global__ __launch_bounds__(256) void k_chunk_reduce_large(Dev P, Large Lg) {
     }
 }
 
+// Incremental sums: every move takes its row's exact fixed-point image out
+// of the old cluster's sum and into the new one's (wrap-around integers, so
+// the result equals the full sum bit for bit); one wave per move.
+__global__ __launch_bounds__(256) void k_moves_large(Dev P_, Large Lg) {
+    const Dev P = with_scales(P_);
+    if (!P.st->active || !large_incremental(P, Lg)) return;
+    const int k = P.k, d = P.d, lane = threadIdx.x & 63;
+    const uint32_t nm = *Lg.nmv;
+    unsigned long long* T = reinterpret_cast<unsigned long long*>(P.total);
+    for (uint32_t q = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); q < nm;
+         q += gridDim.x * (blockDim.x >> 6)) {
+        const int4 mv = Lg.mv[q];
+        const float* xr = P.X + (int64_t)mv.x * d;
+        for (int m = lane; m < d; m += 64) {
+            const uint64_t img = fixed_bits((double)xr[m], P.qscale);
+            atomicAdd(&T[(int64_t)mv.y * d + m], (unsigned long long)(0ull - img));
+            atomicAdd(&T[(int64_t)mv.z * d + m], (unsigned long long)img);
+        }
+        if (lane == 0) {
+            atomicAdd(&T[(int64_t)k * d + mv.y], ~0ull);
+            atomicAdd(&T[(int64_t)k * d + mv.z], 1ull);
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Centroid table for large k*d: a block stages kTiTile float64 rows in LDS
 // and streams every centroid once against them.
 
-__global__ __launch_bounds__(256) void k_centroid_table_tiled(Dev P, int force) {
+__global__ __launch_bounds__(256) void k_centroid_table_tiled(Dev P, Large Lg, int force) {
     if (!force && !P.st->active) return;
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {   // the next step's lists start empty
+        *Lg.nsurv = 0;
+        *Lg.nfull = 0;
+        *Lg.nmv = 0;
+    }
     const int k = P.k, d = P.d;
     const int i0 = blockIdx.x * kTiTile, ni = min(kTiTile, k - i0);
+    // Block column y takes centroids j in [y k / kTiSplit, (y + 1) k / kTiSplit).
+    const int j0 = (int)((int64_t)blockIdx.y * k / kTiSplit), j1 = (int)((int64_t)(blockIdx.y + 1) * k / kTiSplit);
     extern __shared__ __align__(16) unsigned char smem[];
     double* ci = reinterpret_cast<double*>(smem);                  // [kTiTile][d]
     float* mins = reinterpret_cast<float*>(ci + kTiTile * d);      // [kTiTile][256]
@@ -968,7 +1060,7 @@ __global__ __launch_bounds__(256) void k_centroid_table_tiled(Dev P, int force) 
     float mn[kTiTile];
 #pragma unroll
     for (int r = 0; r < kTiTile; ++r) mn[r] = INFINITY;
-    for (int j = threadIdx.x; j < k; j += blockDim.x) {
+    for (int j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
         const double* cj = P.C64 + (int64_t)j * d;
         double acc[kTiTile];
 #pragma unroll
@@ -996,17 +1088,19 @@ __global__ __launch_bounds__(256) void k_centroid_table_tiled(Dev P, int force) 
 #pragma unroll
     for (int r = 0; r < kTiTile; ++r) mins[r * 256 + threadIdx.x] = mn[r];
     __syncthreads();
-    if (threadIdx.x < ni) {
+    if (threadIdx.x < ni) {   // this column's minimum; k_split_rows forms s from the columns
         const int r = threadIdx.x, i = i0 + r;
         float m = INFINITY;
         for (int q = 0; q < (int)blockDim.x; ++q) m = fminf(m, mins[r * 256 + q]);
-        P.s[i] = m;
-        const float* c32 = P.C32 + (int64_t)i * d;
-        double n2 = 0.0;
-        for (int q = 0; q < d; ++q) n2 = fma((double)c32[q], (double)c32[q], n2);
-        P.cn2[i] = (float)n2;
+        Lg.smin[(int64_t)blockIdx.y * k + i] = m;
+        if (blockIdx.y == 0) {
+            const float* c32 = P.C32 + (int64_t)i * d;
+            double n2 = 0.0;
+            for (int q = 0; q < d; ++q) n2 = fma((double)c32[q], (double)c32[q], n2);
+            P.cn2[i] = (float)n2;
+        }
     }
-    if (blockIdx.x == 0) {
+    if (blockIdx.x == 0 && blockIdx.y == 0) {
         float em = 0.f;
         for (int j = threadIdx.x; j < k; j += blockDim.x) em = fmaxf(em, P.ec[j]);
 #pragma unroll
@@ -1036,7 +1130,8 @@ hipError_t launch_large_split_x(const Dev& dv, const Large& lg, int cus, hipStre
     int64_t g = (dv.n + 3) / 4;
     if (g > (int64_t)cus * 16) g = (int64_t)cus * 16;
     hipLaunchKernelGGL(k_split_rows, dim3((unsigned)g), dim3(256), 0, s, dv.X, dv.n, dv.n, dv.d, lg.nch, lg.xs,
-                       lg.x2, static_cast<const IterState*>(nullptr), 1);
+                       lg.x2, static_cast<const IterState*>(nullptr), 1, static_cast<const float*>(nullptr),
+                       static_cast<float*>(nullptr));
     return hipGetLastError();
 }
 
@@ -1049,6 +1144,7 @@ hipError_t launch_large_reduce(const Dev& dv, const Large& lg, hipStream_t s) {
     hipLaunchKernelGGL(k_segsum_large, dim3(lg.NCmax), dim3(256), 0, s, dv, lg);
     const int64_t kd = (int64_t)dv.k * dv.d;
     hipLaunchKernelGGL(k_chunk_reduce_large, dim3((unsigned)((kd + 255) / 256)), dim3(256), 0, s, dv, lg);
+    hipLaunchKernelGGL(k_moves_large, dim3(lg.Gr), dim3(256), 0, s, dv, lg);
     return hipGetLastError();
 }
 
@@ -1069,11 +1165,12 @@ hipError_t large_set_attributes(int k, int d) {
 }
 
 hipError_t launch_large_table(const Dev& dv, const Large& lg, int force, hipStream_t s) {
-    hipLaunchKernelGGL(k_centroid_table_tiled, dim3((dv.k + kTiTile - 1) / kTiTile), dim3(256),
-                       large_table_lds(dv.d), s, dv, force);
+    hipLaunchKernelGGL(k_centroid_table_tiled, dim3((dv.k + kTiTile - 1) / kTiTile, kTiSplit), dim3(256),
+                       large_table_lds(dv.d), s, dv, lg, force);
     const int64_t kp = (int64_t)lg.nct * kLgN;   // padded to whole centroid tiles
     hipLaunchKernelGGL(k_split_rows, dim3((unsigned)((kp + 3) / 4)), dim3(256), 0, s, static_cast<const float*>(dv.C32),
-                       kp, (int64_t)dv.k, dv.d, lg.nch, lg.cs, lg.cn2p, static_cast<const IterState*>(dv.st), force);
+                       kp, (int64_t)dv.k, dv.d, lg.nch, lg.cs, lg.cn2p, static_cast<const IterState*>(dv.st), force,
+                       static_cast<const float*>(lg.smin), dv.s);
     return hipGetLastError();
 }
 
