@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 MFMA_F32_PEAK_TFS = 157.3   # MI355X dense float32 matrix peak
+MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 matrix peak (the global path's split products)
 DEFAULT_WORKLOAD = "aniso-8M-d16-k10"
 METRIC = "k-means iters/sec + effective dist evals/sec; % HBM peak (low d) / % MFMA (big k·d)"
 
@@ -106,13 +107,14 @@ def roofline_entry(kernel: str, workload: str, bytes_per_launch: float, launch_m
 
 
 def mfma_roofline_entry(kernel: str, workload: str, flops_per_launch: float, launch_ms: float,
-                        what: str) -> dict:
-    """Matrix-core roofline of one kernel: algorithmic float32 flops per launch
-    over its mean launch time (HIP events), against the dense float32 peak."""
+                        what: str, peak: float = MFMA_F32_PEAK_TFS, dtype: str = "f32") -> dict:
+    """Matrix-core roofline of one kernel: algorithmic flops per launch over its
+    mean launch time (HIP events), against the dense peak of the products'
+    dtype."""
     achieved = flops_per_launch / (launch_ms / 1e3) / 1e12
     traffic, source = measured_traffic(kernel, workload)
-    return {"kernel": kernel, "bound": "mfma", "achieved": achieved, "peak": MFMA_F32_PEAK_TFS,
-            "unit": "TFLOP/s", "frac": achieved / MFMA_F32_PEAK_TFS, "traffic": traffic,
+    return {"kernel": kernel, "bound": "mfma", "achieved": achieved, "peak": peak,
+            "unit": "TFLOP/s", "frac": achieved / peak, "traffic": traffic, "mfma_dtype": dtype,
             "traffic_source": source, "flops_per_launch": flops_per_launch, "flops_def": what,
             "kernel_us": launch_ms * 1e3}
 
@@ -423,7 +425,9 @@ def main() -> int:
             flops = 2.0 * d * comp / m
         if path == "global-mfma":
             rooflines.append(mfma_roofline_entry(kernel, tag, flops, launch_ms,
-                                                 "steps 1..T-1: 2*d*k per Clause-1 survivor (bound pass included in the time)"))
+                                                 "steps 1..T-1: 2*d*k per Clause-1 survivor (bound pass included "
+                                                 "in the time); the matrix cores run 3 bf16 products per dot "
+                                                 "(3x these flops)", MFMA_BF16_PEAK_TFS, "bf16"))
             rooflines.append(roofline_entry(kernel, tag, bytes_per_launch, launch_ms, what))
         else:
             rooflines.append(roofline_entry(kernel, tag, bytes_per_launch, launch_ms, what))
@@ -447,7 +451,8 @@ def main() -> int:
         first_kernel = "k_first" if path.startswith("stream") else kernel
         if path == "global-mfma":
             rooflines.append(mfma_roofline_entry(first_kernel, tag + "-first-step", 2.0 * d * k * n,
-                                                 first_t["assign_ms"], "first step: 2*d*k per point"))
+                                                 first_t["assign_ms"], "first step: 2*d*k per point (3 bf16 "
+                                                 "products per dot)", MFMA_BF16_PEAK_TFS, "bf16"))
         else:
             rooflines.append(roofline_entry(first_kernel, tag + "-first-step", n * (4.0 * d + 8),
                                             first_t["assign_ms"],
@@ -469,7 +474,7 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16x3+f32" if path == "global-mfma" else "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "method": ("spherical" if args.spherical else "kmeans") +
                    ("+elkan-ti" if args.elkan else ""),

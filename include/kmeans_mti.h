@@ -167,7 +167,10 @@ int kmeans_mti_get_history(km_ctx* ctx, int64_t* changed, int64_t* computed, int
  * HIP events recorded on the context's stream around every launch (needs
  * KM_FLAG_TIMING at init).  ms (HOST, 4 doubles) receives the total
  * milliseconds of the assignment, reduction, update and centroid-table
- * kernels; *iters (nullable) the number of iterations timed.  Synchronizes.
+ * kernels (on the global-memory path the assignment slot holds the Clause-1
+ * pass and the matrix-core distances, and the refinement of their
+ * candidates is timed with the reduction); *iters (nullable) the number of
+ * iterations timed.  Synchronizes.
  * KM_ERR_STATE without KM_FLAG_TIMING.
  */
 int kmeans_mti_get_timing(km_ctx* ctx, double* ms, int64_t* iters);

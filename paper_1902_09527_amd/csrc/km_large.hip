@@ -1118,11 +1118,11 @@ __global__ __launch_bounds__(256) void k_centroid_table_tiled(Dev P, Large Lg, i
 
 const void* large_mfma_symbol() { return reinterpret_cast<const void*>(&k_mfma_large); }
 
+// Assignment group: Clause 1 and the matrix-core candidates.  The candidates'
+// refinement opens the reduction group (its timing slot).
 hipError_t launch_large_assign(const Dev& dv, const Large& lg, int gb, hipStream_t s) {
     hipLaunchKernelGGL(k_bound_large, dim3(gb), dim3(256), 0, s, dv, lg);
     hipLaunchKernelGGL(k_mfma_large, dim3(lg.Gm), dim3(256), large_mfma_lds(), s, dv, lg);
-    hipLaunchKernelGGL(k_refine_large, dim3(lg.Gr), dim3(256), 0, s, dv, lg);
-    hipLaunchKernelGGL(k_full_large, dim3(lg.Gr), dim3(256), 8 * dv.d, s, dv, lg);
     return hipGetLastError();
 }
 
@@ -1136,6 +1136,8 @@ hipError_t launch_large_split_x(const Dev& dv, const Large& lg, int cus, hipStre
 }
 
 hipError_t launch_large_reduce(const Dev& dv, const Large& lg, hipStream_t s) {
+    hipLaunchKernelGGL(k_refine_large, dim3(lg.Gr), dim3(256), 0, s, dv, lg);
+    hipLaunchKernelGGL(k_full_large, dim3(lg.Gr), dim3(256), 8 * dv.d, s, dv, lg);
     const int hl = 4 * dv.k;
     hipLaunchKernelGGL(k_hist_large, dim3(lg.Gs), dim3(256), hl, s, dv, lg);
     hipLaunchKernelGGL(k_scan_large_cols, dim3((dv.k + 255) / 256), dim3(256), 0, s, dv, lg);
