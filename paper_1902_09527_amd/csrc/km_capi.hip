@@ -538,7 +538,9 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
             (rc2 = c->alloc(&L.ciq, (size_t)L.NCmax)) ||
             (rc2 = c->alloc(&L.xs, (size_t)n * L.nch * 16)) || (rc2 = c->alloc(&L.x2, (size_t)n)) ||
             (rc2 = c->alloc(&L.sx2, (size_t)n)) || (rc2 = c->alloc(&L.fq, (size_t)n)) ||
-            (rc2 = c->alloc(&L.nfull, 4)) || (rc2 = c->alloc(&L.nmv, 4)) ||
+            (rc2 = c->alloc(&L.nfull, 4)) || (rc2 = c->alloc(&L.nmv, 4)) || (rc2 = c->alloc(&L.nmq, 4)) ||
+            (rc2 = c->alloc(&L.mq, (size_t)n)) || (rc2 = c->alloc(&L.fpart, (size_t)km::kFullCap * km::kFullSplit)) ||
+            (rc2 = c->alloc(&L.fcnt, (size_t)km::kFullCap)) ||
             (rc2 = c->alloc(&L.mv, (size_t)L.mvcap)) || (rc2 = c->alloc(&v.sums, (size_t)k * d + k)) ||
             (rc2 = c->alloc(&L.cs, (size_t)L.nct * km::kLgN * L.nch * 16)) ||
             (rc2 = c->alloc(&L.cn2p, (size_t)L.nct * km::kLgN)) || (rc2 = c->alloc(&L.smin, (size_t)km::kLgTableSplit * k)) ||
@@ -547,6 +549,8 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         zr.add(L.nsurv, 4 * sizeof(uint32_t));
         zr.add(L.nfull, 4 * sizeof(uint32_t));
         zr.add(L.nmv, 4 * sizeof(uint32_t));
+        zr.add(L.nmq, 4 * sizeof(uint32_t));
+        zr.add(L.fcnt, sizeof(uint32_t) * (size_t)km::kFullCap);
         zr.add(v.sums, sizeof(uint64_t) * ((size_t)k * d + k));
     }
 

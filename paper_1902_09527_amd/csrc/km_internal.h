@@ -107,6 +107,14 @@ constexpr int kLgMaxD = 4096;        // largest d of the global-memory path
 // of 16c + 8 .. +15 (two bf16 per word, the lower dimension in the low half).
 inline int split_chunks(int d) { return (d + kLgK - 1) / kLgK; }
 
+// Best centroid of one range of a survivor decided over all centroids.
+struct FullPart {
+    double D;
+    int32_t j, rk;
+};
+constexpr int kFullCap = 4096;       // survivors per step whose decision is split over blocks
+constexpr int kFullSplit = 8;        // blocks (centroid ranges) per split decision
+
 struct Large {
     int32_t* surv;        // n: survivor point indices of the current step
     uint32_t* nsurv;      // survivor count
@@ -122,8 +130,12 @@ struct Large {
     float* sx2;           // n: x2 of the survivors, in list order
     int32_t* fq;          // n: survivors (list entries) decided over all centroids
     uint32_t* nfull;      // their count
+    FullPart* fpart;      // kFullCap x kFullSplit: the ranges' bests of the split decisions
+    uint32_t* fcnt;       // kFullCap: ranges done per split survivor (reset by the combining block)
+    int4* mq;             // n: survivors with 2-3 candidates (list entry, candidates, -1 for none)
+    uint32_t* nmq;        // their count
     int4* mv;             // mvcap moves of the step: point, old cluster, new cluster
-    uint32_t* nmv;        // their count (nsurv, nfull, nmv: zeroed by the centroid-table pass)
+    uint32_t* nmv;        // their count (nsurv, nfull, nmq, nmv: zeroed by the centroid-table pass)
     int32_t mvcap;        // at most this many moves: incremental sums, else full sums
     uint32_t* cs;         // nct * kLgN split rows of the float32 centroids (rows >= k zero)
     float* cn2p;          // nct * kLgN: their float32 squared norms (rows >= k: +inf)

@@ -10,8 +10,11 @@
 //                       into LDS by direct loads, expanded form): the four
 //                       smallest per survivor and centroid tile;
 //   k_refine_large      per survivor, the candidates within the expanded
-//                       form's error bound refined in the direct form,
-//                       float64 near-tie rule;
+//                       form's error bound; a lone candidate settles it;
+//   k_multi_large,
+//   k_full_large        two or three candidates: direct form and the
+//                       float64 near-tie rule; four or more: float64 over
+//                       all centroids;
 //   k_hist_large        per-block cluster counts of the new assignment;
 //   k_scan_large_cols,
 //   k_scan_large_clusters  cluster starts and per-block write offsets;
@@ -39,6 +42,7 @@ namespace {
 
 constexpr int kTiTile = 16;   // centroid rows per block of the tiled centroid table
 constexpr int kTiSplit = kLgTableSplit;
+constexpr int kRefineFlush = 128;   // LDS entries of the refinement pass that trigger a flush
 
 // Insert (v, j) into an ascending 4-list ordered by value, then index.
 __device__ inline void top4_insert(float (&L)[4], int (&J)[4], float v, int j) {
@@ -49,26 +53,6 @@ __device__ inline void top4_insert(float (&L)[4], int (&J)[4], float v, int j) {
     for (int q = 3; q > 0; --q) {
         const bool sw = L[q] < L[q - 1] || (L[q] == L[q - 1] && J[q] < J[q - 1]);
         if (sw) {
-            const float tv = L[q];
-            L[q] = L[q - 1];
-            L[q - 1] = tv;
-            const int tj = J[q];
-            J[q] = J[q - 1];
-            J[q - 1] = tj;
-        }
-    }
-}
-
-// The same insertion when j is larger than every index in the list (the
-// centroids arrive in increasing index order): a tie keeps the earlier,
-// lower index, so only strict comparisons are needed.
-__device__ __forceinline__ void top4_insert_next(float (&L)[4], int (&J)[4], float v, int j) {
-    if (!(v < L[3])) return;
-    L[3] = v;
-    J[3] = j;
-#pragma unroll
-    for (int q = 3; q > 0; --q) {
-        if (L[q] < L[q - 1]) {
             const float tv = L[q];
             L[q] = L[q - 1];
             L[q - 1] = tv;
@@ -301,7 +285,6 @@ typedef __attribute__((address_space(3))) void* lds_ptr;
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_mfma_large(Dev P, Large Lg) {
     IterState* st = P.st;
     if (!st->active) return;
-    const int k = P.k;
     const int ns = (int)*Lg.nsurv;
     const int nch = Lg.nch, nct = Lg.nct;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, col = lane & 31, half = lane >> 5;
@@ -543,14 +526,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 }
 
 // ---------------------------------------------------------------------------
-// Refinement of every survivor by a thread pair (part 0 and 1, each over half
-// of the dimensions) from its candidate lists (four per centroid tile and
-// half of it): the
-// candidates within twice the expanded form's error bound of the smallest are
-// re-evaluated in the direct form, followed by the float64 near-tie rule; the
-// point's assignment and bound are written.  A survivor whose four smallest
-// all lie inside the bound (more may lie outside the lists) is queued for
-// k_full_large, which decides it in float64 over all centroids.
+// Refinement of every survivor by a thread pair (each merging half of its
+// candidate lists: four per centroid tile and half of it): only centroids
+// within twice the expanded form's error bound of the smallest can be the
+// nearest.  A lone candidate is the assignment, its bound taken from the
+// expanded value; two or three go to k_multi_large (direct form, float64
+// near-tie rule); a survivor whose four smallest all lie inside the bound
+// (more may lie outside the lists) goes to k_full_large, which decides it in
+// float64 over all centroids.
 //
 // Error bound of an expanded value (x and c the float32 row and centroid):
 //   - |x|^2, |c|^2, the float32 roundings: (d + 8) 2^-24 R^2 with
@@ -589,19 +572,47 @@ __global__ __launch_bounds__(256) void k_refine_large(Dev P, Large Lg) {
     __syncthreads();
     const float cnmax = sqrtf(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))) * kUp;
     const float ecm = st->ec_max;
-    const float gamma = P.gamma;
     const float gexp = (float)(d + 8) * 0x1p-24f + 0x1p-15f;
     const float gsp2 = 2.f * (778.f + 6.9f * (float)(16 * Lg.nch)) * 0x1p-24f * (1.f + 0x1p-10f);
-    const bool vec = (d & 3) == 0;
     uint64_t my_changed = 0, my_comp = 0, my_rc = 0;
     const int part = tid & 1;
-    const int hd = (d + 1) / 2, m0 = part * hd, m1 = min(d, m0 + hd);
+    // Queued survivors and moves gather in LDS and go to the global lists
+    // with one atomic per flush of up to 2 kRefineFlush entries (a global
+    // counter per wave would take one atomic per 64 survivors).
+    __shared__ int4 qb[2 * kRefineFlush], mb[2 * kRefineFlush];
+    __shared__ uint32_t nqb, nmb, gq, gm;
+    if (tid == 0) {
+        nqb = 0;
+        nmb = 0;
+    }
+    __syncthreads();
+    auto flush = [&](bool all) __attribute__((always_inline)) {
+        __syncthreads();
+        const uint32_t cq = nqb, cm = nmb;
+        const bool fq = cq >= (all ? 1u : (uint32_t)kRefineFlush), fm = cm >= (all ? 1u : (uint32_t)kRefineFlush);
+        if (tid == 0) {
+            if (fq) gq = atomicAdd(Lg.nmq, cq);
+            if (fm) gm = atomicAdd(Lg.nmv, cm);
+        }
+        __syncthreads();
+        if (fq)
+            for (uint32_t e = tid; e < cq; e += blockDim.x) Lg.mq[gq + e] = qb[e];
+        if (fm)
+            for (uint32_t e = tid; e < cm; e += blockDim.x)
+                if (gm + e < (uint32_t)Lg.mvcap) Lg.mv[gm + e] = mb[e];
+        __syncthreads();
+        if (tid == 0) {
+            if (fq) nqb = 0;
+            if (fm) nmb = 0;
+        }
+        __syncthreads();
+    };
 
     const bool rec_moves = !first && !(P.flags & KM_FLAG_STATS);
     for (int64_t c0 = (int64_t)blockIdx.x * 128; c0 < (int64_t)ns; c0 += (int64_t)gridDim.x * 128) {
         const int64_t c = c0 + (tid >> 1);
-        int4 mvr = make_int4(0, 0, 0, 0);
-        bool moved = false;
+        int4 mvr = make_int4(0, 0, 0, 0), mqr = make_int4(0, 0, 0, 0);
+        bool moved = false, queued = false;
         if (c < (int64_t)ns) {   // both threads of a pair
         float T[4];
         int TJ[4];
@@ -630,7 +641,6 @@ __global__ __launch_bounds__(256) void k_refine_large(Dev P, Large Lg) {
             for (int q = 0; q < 4; ++q) top4_insert(T, TJ, OT[q], OJ[q]);
         }
         const int64_t i = Lg.surv[c];
-        const float* xr = P.X + i * d;
         const int inc = first ? -1 : P.a[i];
         const float x2 = Lg.sx2[c];
         const float xn = sqrtf(fmaxf(x2, 0.f)) * kUp;
@@ -650,123 +660,38 @@ __global__ __launch_bounds__(256) void k_refine_large(Dev P, Large Lg) {
         } else {
         int nq = 0;
         while (nq < 3 && T[nq] <= thr && TJ[nq] < k) ++nq;   // uniform in the pair
-        // Direct-form distance of x to centroid j over this thread's half of
-        // the dimensions, both halves added (equal in the pair).
-        auto dist32 = [&](int j) {
-            const float* cr = P.C32 + (int64_t)j * d;
-            float accd = 0.f;
-            if (vec && (m0 & 3) == 0) {
-                int m = m0;
-                for (; m + 4 <= m1; m += 4) {
-                    const f32x4 xv = *reinterpret_cast<const f32x4*>(xr + m);
-                    const f32x4 cv = *reinterpret_cast<const f32x4*>(cr + m);
-                    const float t0 = xv.x - cv.x, t1 = xv.y - cv.y, t2 = xv.z - cv.z, t3 = xv.w - cv.w;
-                    accd = fmaf(t0, t0, accd);
-                    accd = fmaf(t1, t1, accd);
-                    accd = fmaf(t2, t2, accd);
-                    accd = fmaf(t3, t3, accd);
-                }
-                for (; m < m1; ++m) {
-                    const float t = xr[m] - cr[m];
-                    accd = fmaf(t, t, accd);
-                }
-            } else {
-                for (int m = m0; m < m1; ++m) {
-                    const float t = xr[m] - cr[m];
-                    accd = fmaf(t, t, accd);
-                }
-            }
-            return accd + __shfl_xor(accd, 1);
-        };
-        auto dist64 = [&](int j) {
-            const double* cr = P.C64 + (int64_t)j * d;
-            double accd = 0.0;
-            for (int m = m0; m < m1; ++m) {
-                const double t = (double)xr[m] - cr[m];
-                accd = fma(t, t, accd);
-            }
-            return accd + __shfl_xor(accd, 1);
-        };
-        bool re = false;
-        float d1 = INFINITY, d2 = INFINITY;
-        int rk1 = INT_MAX, j1 = 0;
         // One candidate is the nearest centroid (every other one is certified
         // farther): as on the LDS paths, its bound then comes from its
         // expanded value and the error bound, without the direct form (kept
-        // when statistics are gathered).
-        const bool single = nq == 1 && !(P.flags & KM_FLAG_STATS);
-        if (!single) {
-            for (int q = 0; q < nq; ++q) {
-                const int j = TJ[q];
-                const float Dd = dist32(j);
-                const int rk = j == inc ? -1 : j;
-                if (Dd < d1 || (Dd == d1 && rk < rk1)) {
-                    d2 = d1;
-                    d1 = Dd;
-                    rk1 = rk;
-                    j1 = j;
-                } else if (Dd < d2) {
-                    d2 = Dd;
+        // when statistics are gathered).  Otherwise the survivor and its
+        // candidates go to k_multi_large.
+        if (nq == 1 && !(P.flags & KM_FLAG_STATS)) {
+            const int b = TJ[0];
+            const float ub = __builtin_amdgcn_sqrtf(fmaxf(T[0] + e1, 0.f)) * (1.0f + 0x1p-20f) * kUp;
+            if (part == 0) {
+                if (b != inc) {
+                    P.a[i] = b;
+                    my_changed += 1;
+                    moved = true;
+                    mvr = make_int4((int)i, inc, b, 0);
                 }
+                P.u[i] = ub;
+                my_comp += (uint64_t)k;
             }
-            if (d2 != INFINITY) {
-                const float band =
-                    2.f * gamma * (d1 + d2) + 4.f * (sqrtf(d1) + sqrtf(d2)) * ecm + 8.f * ecm * ecm;
-                if (d2 - d1 <= band) re = true;
-            }
-        }
-        int b = j1;
-        float ub;
-        if (single) {
-            b = TJ[0];
-            ub = __builtin_amdgcn_sqrtf(fmaxf(T[0] + e1, 0.f)) * (1.0f + 0x1p-20f) * kUp;
-        } else {
-            ub = upper_bound(d1, P.ec[j1], gamma);
-        }
-        if (re) {
-            // float64 decision against the master centroids with the oracle's
-            // rule (smaller distance, then the incumbent, then the lower
-            // index) among the candidates inside the bound.
-            double Dbb = INFINITY;
-            int bb = -1, kb = INT_MAX;
-            for (int q = 0; q < nq; ++q) {
-                const int j = TJ[q];
-                const double Dj = dist64(j);
-                const int rk = j == inc ? -1 : j;
-                if (Dj < Dbb || (Dj == Dbb && rk < kb)) {
-                    Dbb = Dj;
-                    bb = j;
-                    kb = rk;
-                }
-            }
-            b = bb < 0 ? 0 : bb;
-            ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
-        }
-        if (part == 0) {
-            if (b != inc) {
-                P.a[i] = b;
-                my_changed += 1;
-                moved = true;
-                mvr = make_int4((int)i, inc, b, 0);
-            }
-            P.u[i] = ub;
+        } else if (part == 0) {
+            queued = true;
+            mqr = make_int4((int)c, TJ[0], nq > 1 ? TJ[1] : -1, nq > 2 ? TJ[2] : -1);
             my_comp += (uint64_t)k;
-            my_rc += re ? 1 : 0;
         }
         }   // not full
         }   // c < ns
-        // Moves to the list, one atomic per wave.
-        if (rec_moves) {
-            const uint64_t m = __ballot(moved);
-            if (m) {
-                uint32_t base = 0;
-                if (lane == 0) base = atomicAdd(Lg.nmv, (uint32_t)__popcll(m));
-                base = __shfl(base, 0);
-                const uint32_t q = base + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
-                if (moved && q < (uint32_t)Lg.mvcap) Lg.mv[q] = mvr;
-            }
-        }
+        // At most 128 entries per round, so a buffer of 2 kRefineFlush holds
+        // a round on top of fewer than kRefineFlush waiting entries.
+        if (queued) qb[atomicAdd(&nqb, 1u)] = mqr;
+        if (moved && rec_moves) mb[atomicAdd(&nmb, 1u)] = mvr;
+        flush(false);
     }
+    flush(true);
     my_changed = wave_sum_u64(my_changed);
     my_comp = wave_sum_u64(my_comp);
     my_rc = wave_sum_u64(my_rc);
@@ -779,33 +704,178 @@ __global__ __launch_bounds__(256) void k_refine_large(Dev P, Large Lg) {
 }
 
 // ---------------------------------------------------------------------------
-// Float64 decision over all centroids for the queued survivors, one block
-// each: the row in LDS as float64, every thread a strided set of centroids
-// (each distance summed over the dimensions in order), then the oracle's
-// rule (smaller distance, then the incumbent, then the lower index) across
-// the block.
+// Survivors with two or three candidates inside the bound, one wave each:
+// the candidates' direct-form float32 distances (lanes over the dimensions,
+// coalesced rows, a fixed butterfly: the float32 error bound holds for any
+// summation order), the nearest with the incumbent winning ties, and when
+// the two smallest lie within the float32 band the float64 decision with
+// the oracle's rule (smaller distance, then the incumbent, then the lower
+// index).  With statistics every survivor comes here (direct-form bounds).
+
+__global__ __launch_bounds__(256) void k_multi_large(Dev P, Large Lg) {
+    IterState* st = P.st;
+    if (!st->active) return;
+    const int k = P.k, d = P.d, lane = threadIdx.x & 63;
+    const bool first = st->t == 0;
+    const bool rec_moves = !first && !(P.flags & KM_FLAG_STATS);
+    const float gamma = P.gamma, ecm = st->ec_max;
+    const uint32_t nq_all = *Lg.nmq;
+    const bool vec = (d & 3) == 0;
+    uint64_t my_changed = 0, my_rc = 0;
+    for (uint32_t q = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); q < nq_all;
+         q += gridDim.x * (blockDim.x >> 6)) {
+        const int4 e = Lg.mq[q];
+        const int js[3] = {e.y, e.z, e.w};
+        const int nq = e.w >= 0 ? 3 : (e.z >= 0 ? 2 : 1);
+        const int64_t i = Lg.surv[e.x];
+        const float* xr = P.X + i * d;
+        const int inc = first ? -1 : P.a[i];
+        auto dist32 = [&](int j) __attribute__((always_inline)) {
+            const float* cr = P.C32 + (int64_t)j * d;
+            float acc = 0.f;
+            if (vec) {
+                for (int m = 4 * lane; m < d; m += 256) {
+                    const f32x4 xv = *reinterpret_cast<const f32x4*>(xr + m);
+                    const f32x4 cv = *reinterpret_cast<const f32x4*>(cr + m);
+                    const float t0 = xv.x - cv.x, t1 = xv.y - cv.y, t2 = xv.z - cv.z, t3 = xv.w - cv.w;
+                    acc = fmaf(t0, t0, acc);
+                    acc = fmaf(t1, t1, acc);
+                    acc = fmaf(t2, t2, acc);
+                    acc = fmaf(t3, t3, acc);
+                }
+            } else {
+                for (int m = lane; m < d; m += 64) {
+                    const float t = xr[m] - cr[m];
+                    acc = fmaf(t, t, acc);
+                }
+            }
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+            return acc;
+        };
+        auto dist64 = [&](int j) __attribute__((always_inline)) {
+            const double* cr = P.C64 + (int64_t)j * d;
+            double acc = 0.0;
+            for (int m = lane; m < d; m += 64) {
+                const double t = (double)xr[m] - cr[m];
+                acc = fma(t, t, acc);
+            }
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+            return acc;
+        };
+        float d1 = INFINITY, d2 = INFINITY;
+        int rk1 = INT_MAX, j1 = 0;
+        for (int t = 0; t < nq; ++t) {
+            const int j = js[t];
+            const float Dd = dist32(j);
+            const int rk = j == inc ? -1 : j;
+            if (Dd < d1 || (Dd == d1 && rk < rk1)) {
+                d2 = d1;
+                d1 = Dd;
+                rk1 = rk;
+                j1 = j;
+            } else if (Dd < d2) {
+                d2 = Dd;
+            }
+        }
+        bool re = false;
+        if (d2 != INFINITY) {
+            const float band = 2.f * gamma * (d1 + d2) + 4.f * (sqrtf(d1) + sqrtf(d2)) * ecm + 8.f * ecm * ecm;
+            re = d2 - d1 <= band;
+        }
+        int b = j1;
+        float ub = upper_bound(d1, P.ec[j1], gamma);
+        if (re) {
+            double Dbb = INFINITY;
+            int bb = -1, kb = INT_MAX;
+            for (int t = 0; t < nq; ++t) {
+                const int j = js[t];
+                const double Dj = dist64(j);
+                const int rk = j == inc ? -1 : j;
+                if (Dj < Dbb || (Dj == Dbb && rk < kb)) {
+                    Dbb = Dj;
+                    bb = j;
+                    kb = rk;
+                }
+            }
+            b = bb < 0 ? 0 : bb;
+            ub = f32_up(sqrt(Dbb) * (1.0 + 0x1p-40));
+        }
+        if (lane == 0) {
+            if (b != inc) {
+                P.a[i] = b;
+                my_changed += 1;
+                if (rec_moves) {
+                    const uint32_t qm = atomicAdd(Lg.nmv, 1u);
+                    if (qm < (uint32_t)Lg.mvcap) Lg.mv[qm] = make_int4((int)i, inc, b, 0);
+                }
+            }
+            P.u[i] = ub;
+            my_rc += re ? 1 : 0;
+        }
+    }
+    my_changed = wave_sum_u64(my_changed);
+    my_rc = wave_sum_u64(my_rc);
+    if (lane == 0) {
+        unsigned long long* sc = reinterpret_cast<unsigned long long*>(P.total + (int64_t)k * d + k);
+        if (my_changed) atomicAdd(&sc[kStChanged], (unsigned long long)my_changed);
+        if (my_rc) atomicAdd(&sc[kStRecheck], (unsigned long long)my_rc);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Float64 decision over all centroids for the queued survivors.  The first
+// kFullCap of them are split over kFullSplit blocks, each taking a range of
+// centroids (the row in LDS as float64, one centroid per thread, its
+// distance summed over the dimensions in order) and writing its best under
+// the oracle's rule (smaller distance, then the incumbent, then the lower
+// index); the block that finishes a survivor last (a counter per survivor
+// behind a fence) combines the ranges and writes the decision.  Survivors
+// past kFullCap take one block over all centroids.
 
 __global__ __launch_bounds__(256) void k_full_large(Dev P, Large Lg) {
     IterState* st = P.st;
     if (!st->active) return;
     const int k = P.k, d = P.d;
     const bool first = st->t == 0;
+    const bool rec_moves = !first && !(P.flags & KM_FLAG_STATS);
     const uint32_t nf = *Lg.nfull;
+    const uint32_t nsplit = min(nf, (uint32_t)kFullCap);
+    const int kr = (k + kFullSplit - 1) / kFullSplit;
     extern __shared__ __align__(16) unsigned char smem[];
     double* xd = reinterpret_cast<double*>(smem);   // [d]
     __shared__ double rD[256];
     __shared__ int rJ[256], rK[256];
+    __shared__ uint32_t last;
     const int tid = threadIdx.x;
     uint64_t my_changed = 0;
-    for (uint32_t q = blockIdx.x; q < nf; q += gridDim.x) {
+    auto decide = [&](int64_t i, int inc, double D, int bj) __attribute__((always_inline)) {
+        const int b = bj < 0 ? 0 : bj;
+        if (b != inc) {
+            P.a[i] = b;
+            my_changed += 1;
+            if (rec_moves) {
+                const uint32_t qm = atomicAdd(Lg.nmv, 1u);
+                if (qm < (uint32_t)Lg.mvcap) Lg.mv[qm] = make_int4((int)i, inc, b, 0);
+            }
+        }
+        P.u[i] = f32_up(sqrt(D) * (1.0 + 0x1p-40));
+    };
+    const uint32_t items = nsplit * kFullSplit + (nf - nsplit);
+    for (uint32_t it = blockIdx.x; it < items; it += gridDim.x) {
+        const bool split = it < nsplit * kFullSplit;
+        const uint32_t q = split ? it / kFullSplit : nsplit + (it - nsplit * kFullSplit);
+        const int part = split ? (int)(it % kFullSplit) : 0;
+        const int j0 = split ? part * kr : 0, j1 = split ? min(k, j0 + kr) : k;
         const int64_t i = Lg.surv[Lg.fq[q]];
-        __syncthreads();   // the previous survivor's row and reduction are consumed
+        __syncthreads();   // the previous item's row and reduction are consumed
         for (int m = tid; m < d; m += blockDim.x) xd[m] = (double)P.X[i * d + m];
         __syncthreads();
         const int inc = first ? -1 : P.a[i];
         double Db = INFINITY;
         int bb = -1, kb = INT_MAX;
-        for (int j = tid; j < k; j += blockDim.x) {
+        for (int j = j0 + tid; j < j1; j += blockDim.x) {
             const double* cr = P.C64 + (int64_t)j * d;
             double acc = 0.0;
             for (int m = 0; m < d; ++m) {
@@ -835,20 +905,36 @@ __global__ __launch_bounds__(256) void k_full_large(Dev P, Large Lg) {
             }
             __syncthreads();
         }
+        if (!split) {
+            if (tid == 0) decide(i, inc, rD[0], rJ[0]);
+            continue;
+        }
         if (tid == 0) {
-            const int b = rJ[0] < 0 ? 0 : rJ[0];
-            if (b != inc) {
-                P.a[i] = b;
-                my_changed += 1;
-                if (!first && !(P.flags & KM_FLAG_STATS)) {
-                    const uint32_t qm = atomicAdd(Lg.nmv, 1u);
-                    if (qm < (uint32_t)Lg.mvcap) Lg.mv[qm] = make_int4((int)i, inc, b, 0);
+            FullPart* fp = Lg.fpart + (int64_t)q * kFullSplit;
+            fp[part] = FullPart{rD[0], rJ[0], rK[0]};
+            __threadfence();
+            last = atomicAdd(&Lg.fcnt[q], 1u);
+        }
+        __syncthreads();
+        if (tid == 0 && last == kFullSplit - 1) {   // every range is in: combine
+            __threadfence();
+            const volatile FullPart* fp = Lg.fpart + (int64_t)q * kFullSplit;
+            double D = INFINITY;
+            int bj = -1, bk = INT_MAX;
+            for (int r = 0; r < kFullSplit; ++r) {
+                const double D2 = fp[r].D;
+                const int k2 = fp[r].rk;
+                if (D2 < D || (D2 == D && k2 < bk)) {
+                    D = D2;
+                    bj = fp[r].j;
+                    bk = k2;
                 }
             }
-            P.u[i] = f32_up(sqrt(rD[0]) * (1.0 + 0x1p-40));
+            Lg.fcnt[q] = 0;   // ready for the next step
+            decide(i, inc, D, bj);
         }
     }
-    if (tid == 0 && my_changed) {
+    if (threadIdx.x == 0 && my_changed) {
         unsigned long long* sc = reinterpret_cast<unsigned long long*>(P.total + (int64_t)k * d + k);
         atomicAdd(&sc[kStChanged], (unsigned long long)my_changed);
     }
@@ -1043,6 +1129,7 @@ __global__ __launch_bounds__(256) void k_centroid_table_tiled(Dev P, Large Lg, i
     if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {   // the next step's lists start empty
         *Lg.nsurv = 0;
         *Lg.nfull = 0;
+        *Lg.nmq = 0;
         *Lg.nmv = 0;
     }
     const int k = P.k, d = P.d;
@@ -1137,6 +1224,7 @@ hipError_t launch_large_split_x(const Dev& dv, const Large& lg, int cus, hipStre
 
 hipError_t launch_large_reduce(const Dev& dv, const Large& lg, hipStream_t s) {
     hipLaunchKernelGGL(k_refine_large, dim3(lg.Gr), dim3(256), 0, s, dv, lg);
+    hipLaunchKernelGGL(k_multi_large, dim3(lg.Gr), dim3(256), 0, s, dv, lg);
     hipLaunchKernelGGL(k_full_large, dim3(lg.Gr), dim3(256), 8 * dv.d, s, dv, lg);
     const int hl = 4 * dv.k;
     hipLaunchKernelGGL(k_hist_large, dim3(lg.Gs), dim3(256), hl, s, dv, lg);
