@@ -95,8 +95,10 @@ constexpr int kLgK = 16;             // dimensions per streamed chunk
 constexpr int kLgStages = 3;         // LDS ring stages (chunks loaded ahead: kLgStages - 1)
 constexpr int kLgStageBytes = (kLgN + kLgM) * 4 * kLgK;   // one chunk of the centroid and survivor tiles
 constexpr int kLgChunkRows = 256;    // rows per segment-sum chunk
-constexpr int kLgBoundRounds = 4;    // rounds of 256 points per block of the bound pass
-constexpr int kLgBoundSpan = 256 * kLgBoundRounds;
+constexpr int kLgBoundThreads = 1024;                 // threads per block of the bound pass
+constexpr int kLgBoundWaves = kLgBoundThreads / 64;
+constexpr int kLgBoundRounds = 4;                     // rounds of kLgBoundThreads points per block
+constexpr int kLgBoundSpan = kLgBoundThreads * kLgBoundRounds;
 constexpr int kLgTableSplit = 4;     // block columns (centroid ranges) of the tiled centroid table
 constexpr int kLgMaxD = 4096;        // largest d of the global-memory path
 

@@ -63,6 +63,26 @@ __device__ inline void top4_insert(float (&L)[4], int (&J)[4], float v, int j) {
     }
 }
 
+// Adds each of n counters (summed over the block) to its slot of the step's
+// statistics, one atomic per counter and block (per-wave atomics on the same
+// words serialize).  Every thread of the block calls it.
+template <int N>
+__device__ __forceinline__ void add_stats_block(uint64_t* total, const int (&slot)[N], uint64_t (&v)[N]) {
+    __shared__ uint64_t part[N][16];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+    for (int c = 0; c < N; ++c) {
+        v[c] = wave_sum_u64(v[c]);
+        if (lane == 0) part[c][wave] = v[c];
+    }
+    __syncthreads();
+    if (threadIdx.x < N) {
+        uint64_t s = 0;
+        for (int w = 0; w < nw; ++w) s += part[threadIdx.x][w];
+        if (s) atomicAdd(reinterpret_cast<unsigned long long*>(total + slot[threadIdx.x]), (unsigned long long)s);
+    }
+}
+
 // The step's per-cluster sums come from its moves (added to the running
 // sums kept by k_update) when few points moved; otherwise from the counting
 // sort and exact segment sums.  The first step, and steps that gather the
@@ -76,7 +96,7 @@ __device__ __forceinline__ bool large_incremental(const Dev& P, const Large& Lg)
 // ---------------------------------------------------------------------------
 // Bound update and Clause 1 for every point; survivors to the global list.
 
-__global__ __launch_bounds__(256) void k_bound_large(Dev P, Large Lg) {
+__global__ __launch_bounds__(kLgBoundThreads) void k_bound_large(Dev P, Large Lg) {
     IterState* st = P.st;
     if (st->done) {
         if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 0;
@@ -86,17 +106,18 @@ __global__ __launch_bounds__(256) void k_bound_large(Dev P, Large Lg) {
     const bool first = st->t == 0;
     const bool prune = !(P.flags & KM_FLAG_NO_PRUNE);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    __shared__ uint32_t cnt[kLgBoundRounds * 4], base[kLgBoundRounds * 4];
+    __shared__ uint32_t cnt[kLgBoundRounds * kLgBoundWaves], base[kLgBoundRounds * kLgBoundWaves];
     // Block b owns points [b kLgBoundSpan, (b + 1) kLgBoundSpan): the flags
-    // of its rounds of 256 stay in a bit mask, the block's survivors take
-    // one atomic on the list counter, then every survivor its place (block
-    // order, then point order).
+    // of its rounds stay in a bit mask, the block's survivors take one atomic
+    // on the list counter (few, large blocks: atomics on one counter are
+    // serialized), then every survivor its place (block order, then point
+    // order).
     const int64_t lo = (int64_t)blockIdx.x * kLgBoundSpan, hi = min(P.n, lo + kLgBoundSpan);
     uint64_t c1 = 0;
     uint32_t mask = 0;
 #pragma unroll
     for (int r = 0; r < kLgBoundRounds; ++r) {
-        const int64_t i = lo + 256 * r + tid;
+        const int64_t i = lo + kLgBoundThreads * r + tid;
         bool surv = false;
         if (i < hi) {
             if (first) {
@@ -114,17 +135,17 @@ __global__ __launch_bounds__(256) void k_bound_large(Dev P, Large Lg) {
         }
         mask |= (surv ? 1u : 0u) << r;
         const uint64_t m = __ballot(surv);
-        if (lane == 0) cnt[4 * r + wave] = (uint32_t)__popcll(m);
+        if (lane == 0) cnt[kLgBoundWaves * r + wave] = (uint32_t)__popcll(m);
     }
     __syncthreads();
     if (tid == 0) {
         uint32_t tot = 0;
-        for (int q = 0; q < kLgBoundRounds * 4; ++q) {
+        for (int q = 0; q < kLgBoundRounds * kLgBoundWaves; ++q) {
             base[q] = tot;
             tot += cnt[q];
         }
         const uint32_t b0 = tot ? atomicAdd(Lg.nsurv, tot) : 0u;
-        for (int q = 0; q < kLgBoundRounds * 4; ++q) base[q] += b0;
+        for (int q = 0; q < kLgBoundRounds * kLgBoundWaves; ++q) base[q] += b0;
     }
     __syncthreads();
 #pragma unroll
@@ -132,16 +153,17 @@ __global__ __launch_bounds__(256) void k_bound_large(Dev P, Large Lg) {
         const bool surv = (mask >> r) & 1u;
         const uint64_t m = __ballot(surv);
         if (surv) {
-            const int64_t i = lo + 256 * r + tid;
-            const uint32_t pos = base[4 * r + wave] + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+            const int64_t i = lo + kLgBoundThreads * r + tid;
+            const uint32_t pos = base[kLgBoundWaves * r + wave] + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
             Lg.surv[pos] = (int32_t)i;
             Lg.sx2[pos] = Lg.x2[i];
         }
     }
-    c1 = wave_sum_u64(c1);
-    if (lane == 0 && c1)
-        atomicAdd(reinterpret_cast<unsigned long long*>(&P.total[(int64_t)P.k * P.d + P.k + kStClause1]),
-                  (unsigned long long)c1);
+    {
+        const int slot[1] = {P.k * P.d + P.k + kStClause1};
+        uint64_t v[1] = {c1};
+        add_stats_block<1>(P.total, slot, v);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -692,14 +714,11 @@ __global__ __launch_bounds__(256) void k_refine_large(Dev P, Large Lg) {
         flush(false);
     }
     flush(true);
-    my_changed = wave_sum_u64(my_changed);
-    my_comp = wave_sum_u64(my_comp);
-    my_rc = wave_sum_u64(my_rc);
-    if (lane == 0) {
-        unsigned long long* sc = reinterpret_cast<unsigned long long*>(P.total + (int64_t)k * d + k);
-        if (my_changed) atomicAdd(&sc[kStChanged], (unsigned long long)my_changed);
-        if (my_comp) atomicAdd(&sc[kStComputed], (unsigned long long)my_comp);
-        if (my_rc) atomicAdd(&sc[kStRecheck], (unsigned long long)my_rc);
+    {
+        const int base = k * d + k;
+        const int slot[3] = {base + kStChanged, base + kStComputed, base + kStRecheck};
+        uint64_t v[3] = {my_changed, my_comp, my_rc};
+        add_stats_block<3>(P.total, slot, v);
     }
 }
 
@@ -815,12 +834,11 @@ __global__ __launch_bounds__(256) void k_multi_large(Dev P, Large Lg) {
             my_rc += re ? 1 : 0;
         }
     }
-    my_changed = wave_sum_u64(my_changed);
-    my_rc = wave_sum_u64(my_rc);
-    if (lane == 0) {
-        unsigned long long* sc = reinterpret_cast<unsigned long long*>(P.total + (int64_t)k * d + k);
-        if (my_changed) atomicAdd(&sc[kStChanged], (unsigned long long)my_changed);
-        if (my_rc) atomicAdd(&sc[kStRecheck], (unsigned long long)my_rc);
+    {
+        const int base = k * d + k;
+        const int slot[2] = {base + kStChanged, base + kStRecheck};
+        uint64_t v[2] = {my_changed, my_rc};
+        add_stats_block<2>(P.total, slot, v);
     }
 }
 
@@ -1208,7 +1226,7 @@ const void* large_mfma_symbol() { return reinterpret_cast<const void*>(&k_mfma_l
 // Assignment group: Clause 1 and the matrix-core candidates.  The candidates'
 // refinement opens the reduction group (its timing slot).
 hipError_t launch_large_assign(const Dev& dv, const Large& lg, int gb, hipStream_t s) {
-    hipLaunchKernelGGL(k_bound_large, dim3(gb), dim3(256), 0, s, dv, lg);
+    hipLaunchKernelGGL(k_bound_large, dim3(gb), dim3(kLgBoundThreads), 0, s, dv, lg);
     hipLaunchKernelGGL(k_mfma_large, dim3(lg.Gm), dim3(256), large_mfma_lds(), s, dv, lg);
     return hipGetLastError();
 }
