@@ -313,7 +313,8 @@ int enqueue_iteration(km_ctx* c) {
         km::Dev dv = c->dv;
         dv.C64 = c->fz.c64 + (size_t)km::slot2(t) * c->k * c->d;   // C^t
         const bool inc = c->inc && t > 0;
-        e = inc                 ? km::launch_inc(dv, c->fz, c->gi, c->lds_inc, t, c->pending ? 1 : 0, c->stream)
+        e = inc                 ? km::launch_inc(dv, c->fz, c->gi, c->lds_inc, t, c->pending ? 1 : 0,
+                                                 t <= km::kIncDenseSteps, c->stream)
             : t == 0 && c->gf ? km::launch_first(dv, c->fz, c->gf, c->lds_first, t, c->stream)
                               : km::launch_small(dv, c->fz, c->lds, t, c->stream);
         if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "streaming step kernel"));
@@ -444,9 +445,13 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
         if (c->inc) {
             c->lds_inc = km::inc_lds_bytes(k);
             if (c->lds_inc > max_lds) return KM_ERR_UNSUPPORTED;
-            const void* isym = km::inc_kernel_symbol(k);
-            int per_cu_i = 0;
-            if ((rcc = kernel_config(c->device, isym, km::kIncThreads, c->lds_inc, &per_cu_i)) != KM_OK) return rcc;
+            int per_cu_i = 0, per_cu_d = 0;
+            if ((rcc = kernel_config(c->device, km::inc_kernel_symbol(k, false), km::kIncThreads, c->lds_inc,
+                                     &per_cu_i)) != KM_OK ||
+                (rcc = kernel_config(c->device, km::inc_kernel_symbol(k, true), km::kIncThreads, c->lds_inc,
+                                     &per_cu_d)) != KM_OK)
+                return rcc;
+            if (per_cu_d < per_cu_i) per_cu_i = per_cu_d;   // one grid for both forms
             if (per_cu_i < 1) return KM_ERR_UNSUPPORTED;
             // Resident blocks (the same count on every CU), at least one wave
             // tile per wave; small inputs still spread over up to one block

@@ -240,6 +240,11 @@ constexpr int kSmallRows = 16;
 // points per lane, four 16-byte state loads issued together), in four
 // sub-tiles of 256.  The state array is padded to whole kIncTile.
 constexpr int kIncWaves = 8;
+// Incremental steps 1 .. kIncDenseSteps stream every row (the dense form)
+// instead of gathering the survivors': right after the first step most
+// points survive Clause 1 and nearly every 128-byte line of X holds a
+// survivor's row.
+constexpr int kIncDenseSteps = 1;
 constexpr int kIncThreads = 64 * kIncWaves;
 constexpr int kIncWaveTile = 1024;
 constexpr int kIncTile = 4 * kIncWaveTile;
@@ -335,7 +340,7 @@ __host__ __device__ inline int finish_lds(int d, int k) { return 8 * k * d + 4 *
 
 bool small_applies(int64_t n, int d, int k, bool aligned);
 const void* small_kernel_symbol(int k);
-const void* inc_kernel_symbol(int k);
+const void* inc_kernel_symbol(int k, bool dense);
 int small_lds_bytes(int k);
 int inc_lds_bytes(int k);
 int small_finish_lds_bytes(int k);
@@ -349,7 +354,8 @@ hipError_t launch_first(const Dev& dv, const Fused& F, int grid, int lds_bytes, 
 // Step t of the incremental kernel.  fused: the end of step t - 1 (an
 // incremental step of the same grid) has not run; every block computes it
 // first and block 0 stores it.  Else dv.C64 = the slot of C^t.
-hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, int fused, hipStream_t s);
+hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, int fused, bool dense,
+                      hipStream_t s);
 // End of step t (one block).  delta: the rows hold the moves of an
 // incremental step (added to the sums of step t - 1), else the full sums of
 // a streaming step (they replace them).

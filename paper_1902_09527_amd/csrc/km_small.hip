@@ -206,9 +206,8 @@ __device__ __forceinline__ Tables table_ptrs(const Dev& P, const SmallLds& lay) 
     return T;
 }
 
-// The tables of step t from memory (the end of step t - 1 has run).
-__device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, const SmallLds& lay, int t) {
-    Tables T = table_ptrs(P, lay);
+// The tables of step t from memory into T (the end of step t - 1 has run).
+__device__ __forceinline__ void fill_tables(const Dev& P, const Fused& F, const Tables& T, int t) {
     const int k = P.k, tid = threadIdx.x;
     const double* dhi = F.dhi + (int64_t)slot2(t) * k;
     const int nt = (int)blockDim.x;
@@ -220,6 +219,12 @@ __device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, cons
         T.ddn[i] = F.ddn[i];
         T.cn[i] = P.cn2[i];
     }
+}
+
+// The tables of step t from memory (the end of step t - 1 has run).
+__device__ __forceinline__ Tables load_tables(const Dev& P, const Fused& F, const SmallLds& lay, int t) {
+    Tables T = table_ptrs(P, lay);
+    fill_tables(P, F, T, t);
     return T;
 }
 
@@ -314,6 +319,26 @@ __device__ __forceinline__ int decide_direct(const Tables& T, const StepFlags& f
 // incumbent (the tightening of the bound) and every c_j that Clause 3 does
 // not skip (the tightened bound at most half the distance from the incumbent
 // to c_j); in the first step, which has no bound, all k.
+// The MTI scan's count of distances for a point with incumbent inc: the
+// incumbent's (which tightens its bound u), then one per other centroid that
+// Clause 3 does not skip (u > half the distance from the incumbent to it).
+// vi: the incumbent's expanded-form value, E its error bound; b, ub: the
+// decision and its bound (u when b is the incumbent).
+template <int KC>
+__device__ __forceinline__ uint32_t mti_count(const float* h, float vi, int k, int inc, int b, float ub, float E) {
+    const float u = b == inc ? ub : sqrt_up(fmaxf(vi + E, 0.f)) * kUp;   // the incumbent's tightened bound
+    uint32_t nc = 1;
+#pragma unroll
+    for (int j = 0; j < KC; j += 4) {
+        const f32x4 hv = *reinterpret_cast<const f32x4*>(h + inc * kSmallMaxK + j);
+        nc += (j < k && j != inc && !(u <= hv.x)) ? 1u : 0u;
+        nc += (j + 1 < k && j + 1 != inc && !(u <= hv.y)) ? 1u : 0u;
+        nc += (j + 2 < k && j + 2 != inc && !(u <= hv.z)) ? 1u : 0u;
+        nc += (j + 3 < k && j + 3 != inc && !(u <= hv.w)) ? 1u : 0u;
+    }
+    return nc;
+}
+
 template <int KC, bool INC_ONLY = false>
 __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, const Tables& T, const StepFlags& fl,
                                        const double* C64, const float (&x)[kD], int64_t p, int inc, int cp,
@@ -359,24 +384,14 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
     } else {
         b = decide_direct(T, fl, C64, x, k, inc, cmask, Db, ub, cn);
     }
-    // The MTI scan's count of distances.
-    uint32_t nc = (uint32_t)k;
     if ((INC_ONLY || inc >= 0) && fl.prune) {
         float vi = INFINITY;
 #pragma unroll
         for (int j = 0; j < KC; ++j) vi = j == inc ? V[j] : vi;
-        const float u = b == inc ? ub : sqrt_up(fmaxf(vi + E, 0.f)) * kUp;   // the incumbent's tightened bound
-        nc = 1;
-#pragma unroll
-        for (int j = 0; j < KC; j += 4) {
-            const f32x4 hv = *reinterpret_cast<const f32x4*>(T.h + inc * kSmallMaxK + j);
-            nc += (j < k && j != inc && !(u <= hv.x)) ? 1u : 0u;
-            nc += (j + 1 < k && j + 1 != inc && !(u <= hv.y)) ? 1u : 0u;
-            nc += (j + 2 < k && j + 2 != inc && !(u <= hv.z)) ? 1u : 0u;
-            nc += (j + 3 < k && j + 3 != inc && !(u <= hv.w)) ? 1u : 0u;
-        }
+        cn.comp += mti_count<KC>(T.h, vi, k, inc, b, ub, E);
+    } else {
+        cn.comp += (uint32_t)k;
     }
-    cn.comp += nc;
     if (fl.want_inertia) cn.iq += fixed_bits((double)Db, P.iscale) - kMagicBits;
     F.w[p] = settle_state(ub, T.ddn[b], b);
     if (b != inc) cn.changed += 1;
@@ -488,7 +503,7 @@ __device__ __forceinline__ EosIn eos_load(const Dev& P, const Fused& F, int t, b
 }
 
 __device__ float eos_finish(const Dev& P, const Fused& F, int t, const EosIn& in, bool writer, unsigned char* scratch,
-                            Tables* T, double* c64n) {
+                            const Tables* T, double* c64n) {
     const int tid = threadIdx.x, j = tid >> 4, m = tid & 15;
     const int k = P.k, kd = k * kD;
     const bool live = j < k;
@@ -991,7 +1006,7 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
 // in its own LDS rows and scans them one per lane.  Only the sums in LDS are
 // shared, through atomics.
 
-template <int KC>
+template <int KC, bool DENSE>
 __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))) void k_inc(Dev P_, Fused F, int t,
                                                                                       int fused) {
     const Dev P = with_scales(P_);
@@ -1041,10 +1056,10 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
     // the gathered rows, and block 0 stores it (and the bookkeeping).  The
     // float64 centroids of near-tie decisions are then the LDS copy.
     double* c64n = reinterpret_cast<double*>(km_smem + lay.off_c64);
-    Tables T;
+    // (T is set once: its pointers stay constants of the code.)
+    const Tables T = table_ptrs(P, lay);
     float ecmax;
     if (fused) {
-        T = table_ptrs(P, lay);
         unsigned char* scr = km_smem + lay.off_qr;
         ecmax = eos_finish(P, F, t - 1, ein, blockIdx.x == 0, scr, &T, c64n);
         if (blockIdx.x == 0 && tid == 0) step_books(P, F, t - 1, ecmax);
@@ -1053,13 +1068,16 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
             return;
         }
     } else {
-        T = load_tables(P, F, lay, t);
+        fill_tables(P, F, T, t);
         ecmax = st->ec_max;
         for (int i = tid; i < P.k * kD; i += kIncThreads) c64n[i] = P.C64[i];
     }
+    // Dense form (DENSE): all rows streamed in order instead of the
+    // survivors' gathered, for a step where most points survive Clause 1.
+    constexpr bool dense = DENSE;
     // The first states are requested once the tables are formed (the end of
     // step holds many registers; the loads arrive during the table staging).
-    if (wt < wt_hi) load_states(wt);
+    if (wt < wt_hi && !dense) load_states(wt);
     if (blockIdx.x == 0 && tid == 0) st->active = 1;
     clear_next_slots(P, F, t);
     StepFlags fl{false, !(P.flags & KM_FLAG_NO_PRUNE), false, P.gamma, ecmax, 0.f};
@@ -1128,6 +1146,190 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
         __builtin_amdgcn_wave_barrier();   // staged rows consumed before the next batch is staged
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
+
+    if constexpr (dense) {
+        // Dense form of an incremental step (all rows streamed): wave w of
+        // the block takes 64-point tiles with a stride of all the grid's
+        // waves, two tiles in flight.  The products are those of the first
+        // step's tiles (16x16x4 matrix-core dot products through a
+        // wave-private LDS tile, one point per lane, certified expanded-form
+        // candidates), with each point's state: a point Clause 1 keeps is
+        // counted and left alone (its state is not rewritten); a survivor with
+        // a single candidate takes it (its state rewritten and, when its
+        // cluster changed, its row moved between the sums by the lanes that
+        // hold its chunks); a survivor with several candidates (or a row that
+        // is not finite) is listed and settled as in the gathered form.
+        const int pl = lane & 15, qd = lane >> 4, k = P.k;
+        // (the tables' fields as plain locals: kept in registers)
+        const float* __restrict__ t_thr = T.thr;
+        const float* __restrict__ t_cn = T.cn;
+        const float* __restrict__ t_h = T.h;
+        const float* __restrict__ t_ddn = T.ddn;
+        uint32_t* __restrict__ t_cnt = T.cnt;
+        uint64_t* __restrict__ t_acc = T.acc;
+        const int t_csu = T.csu, t_kp = T.kp;
+        float* dt = wg;            // the wave's tile: its staged rows
+        int* bt = wq_p;            // its move words: the first 64 queue entries
+        int* rl = wq_p + 64;       // its list: the rest of the queue
+        int* ra = wq_a + 64;
+        constexpr int rcap = kIncWaveQ - 64;
+        float a[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) a[s] = pl < k ? T.C[pl * kCR + 4 * qd + s] : 0.f;
+        const int64_t ntiles = (n + 63) / 64;
+        const int64_t nw = (int64_t)kIncWaves * gridDim.x;
+
+        f32x4 xA[4], xB[4];   // [g]: chunk qd of point 16g + pl of the tile
+        uint32_t sA = 0, sB = 0;   // the state of point `lane` of the tile
+        int nl = 0;   // listed survivors (wave-uniform)
+        // (A tile past the end loads the last tile again, unused: the registers
+        // are then written on every path, so none is held across a drain.)
+        auto prefetch = [&](f32x4 (&xb)[4], uint32_t& sb, int64_t tl) __attribute__((always_inline)) {
+            const int64_t tc = min(tl, ntiles - 1);
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int64_t row = min(tc * 64 + 16 * g + pl, n - 1);
+                xb[g] = __builtin_nontemporal_load(X4 + row * kQD + qd);
+            }
+            sb = F.w[tc * 64 + lane];   // the state array is padded past n
+        };
+        auto wave_sync = []() __attribute__((always_inline)) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        };
+        auto tile_body = [&](const f32x4 (&xb)[4], uint32_t ws, int64_t tl) __attribute__((always_inline)) {
+            const int64_t base = tl * 64;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const f32x4 xv = xb[g];
+                f32x4 dot = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], xv.x, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                dot = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], xv.y, dot, 0, 0, 0);
+                dot = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], xv.z, dot, 0, 0, 0);
+                dot = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], xv.w, dot, 0, 0, 0);
+                float* row = dt + (16 * g + pl) * kCR;
+                *reinterpret_cast<f32x4*>(row + 4 * qd) = dot;
+                row[16 + qd] = fmaf(xv.x, xv.x, fmaf(xv.y, xv.y, fmaf(xv.z, xv.z, xv.w * xv.w)));
+            }
+            wave_sync();
+            const bool valid = base + lane < n;
+            const int inc = state_cluster(ws);
+            const bool surv = valid && !(fl.prune && state_value(ws) <= t_thr[inc]);
+            cn.c1 += valid && !surv ? 1u : 0u;
+            int mv = -1;   // a moved point: new cluster | old cluster << 8
+            bool listed = false;
+            if (surv) {
+                const float* row = dt + lane * kCR;
+                const f32x4 pn = *reinterpret_cast<const f32x4*>(row + 16);
+                const float x2 = ((pn.x + pn.y) + pn.z) + pn.w;
+                // The expanded-form values, formed again from the tile for the
+                // candidate mask (no register array held across the tile).
+                auto vals = [&](int j, float (&v)[4]) __attribute__((always_inline)) {
+                    const f32x4 dv = *reinterpret_cast<const f32x4*>(row + j);
+                    const f32x4 cv = *reinterpret_cast<const f32x4*>(t_cn + j);
+                    v[0] = j < k ? fmaf(-2.f, dv.x, x2 + cv.x) : INFINITY;
+                    v[1] = j + 1 < k ? fmaf(-2.f, dv.y, x2 + cv.y) : INFINITY;
+                    v[2] = j + 2 < k ? fmaf(-2.f, dv.z, x2 + cv.z) : INFINITY;
+                    v[3] = j + 3 < k ? fmaf(-2.f, dv.w, x2 + cv.w) : INFINITY;
+                };
+                float vmin = INFINITY;
+#pragma unroll
+                for (int j = 0; j < KC; j += 4) {
+                    float v[4];
+                    vals(j, v);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (j + r < KC) vmin = fminf(vmin, v[r]);
+                }
+                const float R = sqrtf(x2) * (1.0f + 0x1p-20f) + fl.cnmax;
+                const float E = (kExpGamma * R * R + 4.f * R * fl.ecmax + 2.f * fl.ecmax * fl.ecmax) * kUp;
+                const float lim = vmin + 2.f * E;
+                uint32_t cm = 0;
+#pragma unroll
+                for (int j = 0; j < KC; j += 4) {
+                    float v[4];
+                    vals(j, v);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (j + r < KC) cm |= (v[r] <= lim ? 1u : 0u) << (j + r);
+                }
+                cm &= (1u << k) - 1u;   // (an infinite minimum would admit the slots past k)
+                if (__popc(cm) == 1) {
+                    const int b = __builtin_ctz(cm);
+                    const float ub = sqrt_up(fmaxf(vmin + E, 0.f)) * kUp;
+                    cn.comp += fl.prune ? mti_count<KC>(t_h, fmaf(-2.f, row[inc], x2 + t_cn[inc]), k, inc, b, ub, E)
+                                        : (uint32_t)k;
+                    F.w[base + lane] = settle_state(ub, t_ddn[b], b);
+                    if (b != inc) {
+                        cn.changed += 1;
+                        const int cp = lane & (kCopies - 1);
+                        atomicAdd(&t_cnt[cp * t_kp + b], 1u);
+                        atomicAdd(&t_cnt[cp * t_kp + inc], 0xFFFFFFFFu);
+                        mv = b | (inc << 8);
+                    }
+                } else {
+                    listed = true;
+                }
+            }
+            const uint64_t lm = __ballot(listed);
+            if (listed) {
+                const int e = nl + lanes_below(lm);
+                rl[e] = (int)(base + lane);
+                ra[e] = inc;
+            }
+            nl += __popcll(lm);
+            bt[(lane & 15) * 4 + (lane >> 4)] = mv;
+            wave_sync();
+            // The moved rows out of their old clusters' sums and into the new
+            // ones', by the lanes that hold them.
+            const int4 ms = *reinterpret_cast<const int4*>(bt + pl * 4);
+            const int mm[4] = {ms.x, ms.y, ms.z, ms.w};
+            const int cp = pl & (kCopies - 1);
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                if (mm[g] >= 0) {
+                    const f32x4 xv = xb[g];
+                    const float xs[4] = {xv.x, xv.y, xv.z, xv.w};
+                    unsigned long long* dn = reinterpret_cast<unsigned long long*>(
+                        t_acc + cp * t_csu + (mm[g] & 255) * kSmallAccRow + 4 * qd);
+                    unsigned long long* dp = reinterpret_cast<unsigned long long*>(
+                        t_acc + cp * t_csu + (mm[g] >> 8) * kSmallAccRow + 4 * qd);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const uint64_t v = fixed_bits((double)xs[e], P.qscale);
+                        atomicAdd(dn + e, (unsigned long long)v);
+                        atomicAdd(dp + e, (unsigned long long)(0 - v));
+                    }
+                }
+            }
+            wave_sync();   // the tile is read before the next one is written
+        };
+        // The stream stops (its two tiles in flight discarded) when the next two
+        // tiles could overflow the list; the list is settled with no tile held,
+        // and the stream restarts at the next tile.
+        int64_t tl = (int64_t)kIncWaves * blockIdx.x + w;
+        while (tl < ntiles) {
+            prefetch(xA, sA, tl);
+            prefetch(xB, sB, tl + nw);
+            for (; tl < ntiles;) {
+                tile_body(xA, sA, tl);
+                prefetch(xA, sA, tl + 2 * nw);
+                if (tl + nw < ntiles) {
+                    tile_body(xB, sB, tl + nw);
+                    prefetch(xB, sB, tl + 3 * nw);
+                }
+                tl += 2 * nw;
+                if (nl > rcap - 128) break;
+            }
+            for (int e0 = 0; e0 < nl; e0 += 64) {
+                take_batch(64 + e0, min(nl - e0, 64));
+                scan_batch();
+            }
+            nl = 0;
+        }
+        flush_block(P, F, T, cn, true, t);
+        return;
+    }
 
     int queued = 0;      // wave-uniform
     uint32_t c1w = 0;    // wave-uniform: points Clause 1 kept
@@ -1237,10 +1439,10 @@ const void* small_kernel_symbol(int k) {
     }
 }
 
-const void* inc_kernel_symbol(int k) {
+const void* inc_kernel_symbol(int k, bool dense) {
     switch (small_kc(k)) {
 #define KM_SYM(KC_) \
-    case KC_: return reinterpret_cast<const void*>(&k_inc<KC_>);
+    case KC_: return dense ? reinterpret_cast<const void*>(&k_inc<KC_, true>) : reinterpret_cast<const void*>(&k_inc<KC_, false>);
         KM_SMALL_KCS(KM_SYM)
 #undef KM_SYM
         default: return nullptr;
@@ -1287,10 +1489,16 @@ hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, int t, hip
     return hipGetLastError();
 }
 
-hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, int fused, hipStream_t s) {
+hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, int fused, bool dense,
+                      hipStream_t s) {
     switch (small_kc(dv.k)) {
-#define KM_LAUNCH(KC_)                                                                                \
-    case KC_: hipLaunchKernelGGL((k_inc<KC_>), dim3(grid), dim3(kIncThreads), lds_bytes, s, dv, F, t, fused); break;
+#define KM_LAUNCH(KC_)                                                                                          \
+    case KC_:                                                                                                   \
+        if (dense)                                                                                              \
+            hipLaunchKernelGGL((k_inc<KC_, true>), dim3(grid), dim3(kIncThreads), lds_bytes, s, dv, F, t, fused);  \
+        else                                                                                                    \
+            hipLaunchKernelGGL((k_inc<KC_, false>), dim3(grid), dim3(kIncThreads), lds_bytes, s, dv, F, t, fused); \
+        break;
         KM_SMALL_KCS(KM_LAUNCH)
 #undef KM_LAUNCH
         default: return hipErrorInvalidValue;

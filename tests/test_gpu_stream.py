@@ -208,3 +208,47 @@ def test_incremental_tiling_edges_match_oracle_and_generic_path(n):
     check_centroids(c.cpu().numpy(), ref["C"], X, "final centroids")
     a2, c2, _ = km.run(Xg, Cg, iters, 0.0, generic=True)
     assert torch.equal(a, a2) and torch.equal(c, c2)
+
+
+def test_dense_step_settles_listed_ties_like_the_oracle():
+    # Two fixed centroids (-2, 0, ...) and (2, 0, ...): every cluster's mean is
+    # its initial centroid (rows in +-offset pairs; each tie row x0 = 0 has a
+    # partner at x0 = -4), so the drift is zero and the tie rows (x0 = 0,
+    # equidistant in float32 and float64) survive Clause 1 in every step with
+    # two candidates.  In the streamed first incremental step they are listed
+    # and settled as gathered survivors; 44 % of the rows are ties over about
+    # seven 64-row tiles per wave, so each wave's list fills and is drained
+    # in the middle of its tiles.  The
+    # oracle's lowest index and the incumbent rule both give cluster 0.
+    rng = np.random.default_rng(140)
+    m = 200000
+    y = rng.integers(-3, 4, size=(2 * m, 15))
+    y[:, 0] = np.where(y[:, 0] == 0, 1, y[:, 0])                 # |y| > 0: a bound above s(c0) = 2
+    ties = np.concatenate([np.zeros((2 * m, 1)), np.concatenate([y[:m], -y[:m]])], axis=1)
+    comp = np.concatenate([np.full((2 * m, 1), -4.0), np.concatenate([y[m:], -y[m:]])], axis=1)
+    off = rng.integers(-1, 2, size=(m // 8, 16))
+    base0 = np.concatenate([off, -off]) + np.eye(16)[0] * -2.0
+    off = rng.integers(-1, 2, size=(m // 8, 16))
+    base1 = np.concatenate([off, -off]) + np.eye(16)[0] * 2.0
+    X = np.concatenate([ties, comp, base0, base1]).astype(np.float32)
+    X = X[rng.permutation(len(X))]
+    C0 = np.zeros((2, 16), np.float32)
+    C0[0, 0], C0[1, 0] = -2.0, 2.0
+    n, T = len(X), 3
+    print("n", n, "ties", 2 * m, flush=True)
+    ref = oracle.lloyd(X, C0, T, 0.0)
+    assert (ref["assign"][X[:, 0] == 0.0] == 0).all()
+    outs = []
+    for flags in ({}, {"full_sums": True}):
+        with km.KMeansMTI(_gpu(X), _gpu(C0), **flags) as ctx:
+            for _ in range(T):
+                ctx.iterate()
+            a, _ = ctx.get(centroids=False)
+            outs.append((a.cpu().numpy(), ctx.centroids64(), ctx.history()))
+    a, c64, h = outs[0]
+    np.testing.assert_array_equal(a, ref["assign"])
+    np.testing.assert_allclose(c64, ref["C"], rtol=1e-12, atol=1e-12)
+    np.testing.assert_array_equal(h["changed"], [n, 0, 0])
+    assert (h["rechecks"][1:] >= 2 * m).all()                    # every tie row decided in float64
+    np.testing.assert_array_equal(a, outs[1][0])
+    np.testing.assert_array_equal(c64, outs[1][1])
