@@ -1,7 +1,7 @@
-// Device helpers shared by the kernel translation units (km_kernels.hip,
-// km_large.hip): directed float32 rounding of float64 values, the upper
-// bound of a distance from a float32 squared distance, and the exact
-// fixed-point image of a coordinate.
+// Device helpers shared by the kernel translation units: directed float32
+// rounding of float64 values, the upper bound of a distance from a float32
+// squared distance, the split-bf16 operands of the matrix-core distances,
+// and the exact fixed-point image of a coordinate.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -16,6 +16,26 @@ constexpr float kUp = 1.0f + 0x1p-22f;   // covers one float32 rounding, upward
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));    // native 16-byte vector
 typedef float f32x16 __attribute__((ext_vector_type(16)));  // 32x32 MFMA accumulator slice
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));    // a bf16 matrix-core operand (16 bytes)
+
+// Split operands of two float32 values: hi = bf16(x) (rounded to nearest),
+// returned packed, and the residuals x - hi (exact in float32); split_lo
+// packs bf16 of the two residuals.  x.c is then formed as hi.hi + hi.lo +
+// lo.hi on the bf16 matrix cores.
+__device__ __forceinline__ uint32_t split_hi(float a, float b, float& ra, float& rb) {
+    const f32x2 v = {a, b};
+    const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+    ra = a - __uint_as_float(h << 16);
+    rb = b - __uint_as_float(h & 0xffff0000u);
+    return h;
+}
+
+__device__ __forceinline__ uint32_t split_lo(float a, float b) {
+    const f32x2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
 
 // Largest float <= v and smallest float >= v.
 __device__ inline float f32_down(double v) {

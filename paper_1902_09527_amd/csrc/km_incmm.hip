@@ -1,7 +1,7 @@
 // Incremental MTI step on the matrix cores, d = 16 or 32 and k <= 128: the
 // paper's skipping of the data of the points Clause 1 keeps (section III-C:
 // no row of such a point is read) on the path where the survivors'
-// distances are a dense float32 product X . C^T.
+// distances are a dense product X . C^T.
 //
 // Point state.  One 32-bit word per point: the cluster in bits 6..0 and, in
 // the rest, a float32 value v (rounded up to 128 units in the last place)
@@ -24,11 +24,12 @@
 //     every survivor's bound is at most half the distance from its
 //     incumbent to each centroid of the block (the incumbent's own block is
 //     never skipped, its half-distance to itself being zero);
-//   - the other blocks' distances come from float32 MFMA tiles in the
-//     expanded form |x|^2 - 2 (x.c - |c|^2 / 2), the bracket formed by the
-//     matrix cores with -|c|^2 / 2 as one more dimension; every centroid
-//     within twice the expanded form's error bound of the smallest is a
-//     candidate, a single
+//   - the other blocks' distances come from matrix-core tiles in the
+//     expanded form |x|^2 - 2 (x.c - |c|^2 / 2), x.c as three bf16 products
+//     of split operands (hi = bf16(v), lo = bf16(v - hi): hi.hi + hi.lo +
+//     lo.hi, v_mfma_f32_32x32x16_bf16); every centroid within twice the
+//     expanded form's error bound (the split and accumulation terms
+//     included) of the smallest is a candidate, a single
 //     candidate is the nearest centroid (its bound from the expanded value
 //     plus the error bound), several are decided in the direct form and a
 //     near tie again in float64 against the master centroids;
@@ -80,7 +81,8 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         return;
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) st->active = 1;
-    constexpr int kHalf = D / 2;
+    constexpr int kHalf = D / 2;              // dimensions of a lane's half of a row
+    constexpr int NS = D / 16;                // 16-dimension matrix-core k-steps
     constexpr int XS = D + 4;                // staged row stride (floats): D values, then point and state
     constexpr int CPR = D / 4;               // 16-byte chunks per row
     constexpr int RPL = 64 / CPR;            // rows per wave-wide load
@@ -134,22 +136,38 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     for (int i = tid; i < 4 * k; i += kW * 64) hm[i] = P.hm[i];
     if (tid < kNumStat) bst[tid] = 0;
     if (tid == 0) *tcount = 0;
-    // Matrix-core A operands: lane l feeds centroid row 32*cb + l%32 and
-    // dimension half l/32; k-step q pairs dimension q with dimension D/2 + q.
-    float creg[WIDE ? 1 : KB][WIDE ? 1 : kHalf];
+    // Matrix-core A operands, split (hi, lo): at k-step s lane l feeds
+    // centroid row 32*cb + l%32, dimensions 16 s + 8 (l/32) .. + 7.
+    auto centroid_split = [&](int cb, int s, int l, uint4& hi, uint4& lo) __attribute__((always_inline)) {
+        const int j = cb * 32 + (l & 31);
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = j < k ? P.C32[(int64_t)j * D + 16 * s + 8 * (l >> 5) + i] : 0.f;
+        uint32_t h[4], o[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            float ra, rb;
+            h[p] = split_hi(v[2 * p], v[2 * p + 1], ra, rb);
+            o[p] = split_lo(ra, rb);
+        }
+        hi = make_uint4(h[0], h[1], h[2], h[3]);
+        lo = make_uint4(o[0], o[1], o[2], o[3]);
+    };
+    uint4* cau = reinterpret_cast<uint4*>(ca);   // WIDE: [cb][s][hi, lo][lane]
+    uint4 chi[WIDE ? 1 : KB][WIDE ? 1 : NS], clo[WIDE ? 1 : KB][WIDE ? 1 : NS];
     if constexpr (WIDE) {
-        for (int i = tid; i < KB * kHalf * 64; i += kW * 64) {
-            const int l = i & 63, q = (i >> 6) % kHalf, cb = i / (64 * kHalf);
-            const int j = cb * 32 + (l & 31);
-            ca[i] = j < k ? P.C32[(int64_t)j * D + (l >> 5) * kHalf + q] : 0.f;
+        for (int i = tid; i < KB * NS * 64; i += kW * 64) {
+            const int l = i & 63, s2 = (i >> 6) % NS, cb = i / (64 * NS);
+            uint4 hi, lo;
+            centroid_split(cb, s2, l, hi, lo);
+            cau[((cb * NS + s2) * 2) * 64 + l] = hi;
+            cau[((cb * NS + s2) * 2 + 1) * 64 + l] = lo;
         }
     } else {
 #pragma unroll
-        for (int cb = 0; cb < KB; ++cb) {
-            const int j = cb * 32 + col;
+        for (int cb = 0; cb < KB; ++cb)
 #pragma unroll
-            for (int q = 0; q < kHalf; ++q) creg[cb][q] = j < k ? P.C32[(int64_t)j * D + half * kHalf + q] : 0.f;
-        }
+            for (int s2 = 0; s2 < NS; ++s2) centroid_split(cb, s2, lane, chi[cb][s2], clo[cb][s2]);
     }
     __syncthreads();
     float cnmax;
@@ -158,9 +176,16 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         for (int i = 0; i < k; ++i) m2 = fmaxf(m2, cn2s[i]);
         cnmax = sqrtf(m2) * kUp * kUp;
     }
-    // Error factor of a float32 squared distance in the expanded form,
-    // relative to (|x| + |c|)^2.
+    // Error bound of an expanded value (x and c the float32 row and
+    // centroid): (D + 8) 2^-24 R^2 (R = |x| + max |c|) for the float32 norms
+    // and roundings; for the split product 3.04 2^-16 |x_m| |c_m| per
+    // dimension (the dropped lo.lo and the two roundings' residuals) and, at
+    // most 18 units of 2^-23 relative to |C| + sum |p| per instruction of 16
+    // exact bf16 products, 6.9 D 2^-24 sum |x_m| |c_m| over the 3 D / 16
+    // instructions of a dot (doubled in the squared distance); an absolute
+    // 2^-100 (1 + R) for bf16 values below the normal range.
     constexpr float gexp = (float)(D + 8) * 0x1p-24f;
+    constexpr float gsp2 = 2.f * (778.f + 6.9f * (float)D) * 0x1p-24f * (1.f + 0x1p-10f);
 
     uint32_t my_changed = 0, my_comp = 0, my_rc = 0, c1w = 0;
 
@@ -185,6 +210,7 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         bcnt = c;
     };
 
+    auto dim_of = [&](int q) { return 16 * (q >> 3) + 8 * half + (q & 7); };
     auto scan_batch = [&]() __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < kLoads; ++i)
@@ -198,10 +224,12 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         const int p = park[0];
         const uint32_t wst = (uint32_t)park[1];
         const int inc = first ? -1 : st_cluster(wst);
+        // The lane's half of the row: dimensions 16 s + 8 half .. + 7 of each
+        // k-step s (xh[8 s + i]).
         float xh[kHalf];
 #pragma unroll
         for (int q = 0; q < kHalf; q += 4) {
-            const f32x4 v = *reinterpret_cast<const f32x4*>(xr + half * kHalf + q);
+            const f32x4 v = *reinterpret_cast<const f32x4*>(xr + dim_of(q));
             xh[q] = v.x;
             xh[q + 1] = v.y;
             xh[q + 2] = v.z;
@@ -225,22 +253,45 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
                 if (eval[cb]) nreal += min(32, max(k - 32 * cb, 0));
             }
         }
-        // dot'_j = x.c_j - |c_j|^2 / 2 from the matrix cores: the k-steps of
-        // the dimension pairs, then one step with the extra dimension (1 on
-        // half 0, 0 on half 1).  The squared distance is |x|^2 - 2 dot'_j, so
-        // the nearest centroid has the largest dot'.
+        // dot'_j = x.c_j - |c_j|^2 / 2: x.c_j from the bf16 matrix cores
+        // (hi.hi + hi.lo + lo.hi per k-step), then -|c_j|^2 / 2 added.  The
+        // squared distance is |x|^2 - 2 dot'_j, so the nearest centroid has
+        // the largest dot'.
+        uint4 bhi[NS], blo[NS];
+#pragma unroll
+        for (int s2 = 0; s2 < NS; ++s2) {
+            uint32_t h[4], o[4];
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                float ra, rb;
+                h[p] = split_hi(xh[8 * s2 + 2 * p], xh[8 * s2 + 2 * p + 1], ra, rb);
+                o[p] = split_lo(ra, rb);
+            }
+            bhi[s2] = make_uint4(h[0], h[1], h[2], h[3]);
+            blo[s2] = make_uint4(o[0], o[1], o[2], o[3]);
+        }
+        auto bf = [](uint4 u) { return __builtin_bit_cast(bf16x8, u); };
         f32x16 dot[KB];
-        const float ext = half == 0 ? 1.f : 0.f;
 #pragma unroll
         for (int cb = 0; cb < KB; ++cb) {
             if (eval[cb]) {   // uniform
-                const float aext = half == 0 ? nb[cb * 32 + col] : 0.f;
-                dot[cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(aext, ext, f32x16{}, 0, 0, 0);
+                f32x16 pr = {};
 #pragma unroll
-                for (int q = 0; q < kHalf; ++q)
-                    dot[cb] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                        WIDE ? ca[(cb * kHalf + q) * 64 + lane] : creg[WIDE ? 0 : cb][WIDE ? 0 : q], xh[q], dot[cb],
-                        0, 0, 0);
+                for (int s2 = 0; s2 < NS; ++s2) {
+                    const uint4 ah = WIDE ? cau[((cb * NS + s2) * 2) * 64 + lane] : chi[WIDE ? 0 : cb][WIDE ? 0 : s2];
+                    const uint4 al = WIDE ? cau[((cb * NS + s2) * 2 + 1) * 64 + lane] : clo[WIDE ? 0 : cb][WIDE ? 0 : s2];
+                    pr = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf(ah), bf(bhi[s2]), pr, 0, 0, 0);
+                    pr = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf(ah), bf(blo[s2]), pr, 0, 0, 0);
+                    pr = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf(al), bf(bhi[s2]), pr, 0, 0, 0);
+                }
+#pragma unroll
+                for (int a4 = 0; a4 < 4; ++a4) {
+                    const f32x4 nv = *reinterpret_cast<const f32x4*>(nb + cb * 32 + 8 * a4 + 4 * half);
+                    dot[cb][4 * a4] = pr[4 * a4] + nv.x;
+                    dot[cb][4 * a4 + 1] = pr[4 * a4 + 1] + nv.y;
+                    dot[cb][4 * a4 + 2] = pr[4 * a4 + 2] + nv.z;
+                    dot[cb][4 * a4 + 3] = pr[4 * a4 + 3] + nv.w;
+                }
             } else {
 #pragma unroll
                 for (int e = 0; e < 16; ++e) dot[cb][e] = -INFINITY;
@@ -259,8 +310,10 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
         // 2E of the smallest); every other evaluated centroid is certified
         // farther than the nearest.  A single candidate is counted and found
         // in the same pass.
-        const float R = sqrtf(fmaxf(x2, 0.f)) * (1.0f + 0x1p-20f) + cnmax;
-        const float E = (gexp * R * R + 4.f * R * ecmax + 2.f * ecmax * ecmax) * kUp;
+        const float xn = sqrtf(fmaxf(x2, 0.f)) * (1.0f + 0x1p-20f);
+        const float R = xn + cnmax;
+        const float E = (gexp * R * R + gsp2 * xn * cnmax + 4.f * R * ecmax + 2.f * ecmax * ecmax +
+                         0x1p-100f * (1.f + R)) * kUp;
         const float lim = dmax - E;
         int own = 0, jown = -1;
 #pragma unroll
@@ -372,10 +425,10 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
 #pragma unroll
                 for (int q = 0; q < kHalf; ++q) {
                     const uint64_t v = fixed_bits((double)xh[q], P.qscale);
-                    atomicAdd(reinterpret_cast<unsigned long long*>(acc + b * AR + half * kHalf + q),
+                    atomicAdd(reinterpret_cast<unsigned long long*>(acc + b * AR + dim_of(q)),
                               (unsigned long long)v);
                     if (inc >= 0)
-                        atomicAdd(reinterpret_cast<unsigned long long*>(acc + inc * AR + half * kHalf + q),
+                        atomicAdd(reinterpret_cast<unsigned long long*>(acc + inc * AR + dim_of(q)),
                                   (unsigned long long)(0 - v));
                 }
             }

@@ -173,23 +173,6 @@ __global__ __launch_bounds__(kLgBoundThreads) void k_bound_large(Dev P, Large Lg
 // order, then a fixed butterfly over the wave: deterministic).  Rows from
 // valid to rows are padding: zero operands, norm +inf.  One wave per row.
 
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-
-__device__ __forceinline__ uint32_t split_hi(float a, float b, float& ra, float& rb) {
-    const f32x2 v = {a, b};
-    const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
-    ra = a - __uint_as_float(h << 16);
-    rb = b - __uint_as_float(h & 0xffff0000u);
-    return h;
-}
-
-__device__ __forceinline__ uint32_t split_lo(float a, float b) {
-    const f32x2 v = {a, b};
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
-}
-
 __global__ __launch_bounds__(256) void k_split_rows(const float* __restrict__ src, int64_t rows, int64_t valid, int d,
                                                     int nch, uint32_t* __restrict__ dst, float* __restrict__ norms,
                                                     const IterState* st, int force, const float* __restrict__ smin,
