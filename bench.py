@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 MFMA_F32_PEAK_TFS = 157.3   # MI355X dense float32 matrix peak
-MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 matrix peak (the global path's split products)
+MFMA_BF16_PEAK_TFS = 2500.0  # MI355X dense bf16 matrix peak (the split products of k_mfma_large, k_inc_mm)
 DEFAULT_WORKLOAD = "aniso-8M-d16-k10"
 METRIC = "k-means iters/sec + effective dist evals/sec; % HBM peak (low d) / % MFMA (big k·d)"
 
@@ -437,7 +437,9 @@ def main() -> int:
             if path == "lds-inc":
                 rooflines.append(mfma_roofline_entry(kernel, tag, flops, launch_ms,
                                                      "steps 1..T-1: 2*d per distance of the evaluated "
-                                                     "32-centroid blocks"))
+                                                     "32-centroid blocks; the matrix cores run 3 bf16 "
+                                                     "products per dot (3x these flops)", MFMA_BF16_PEAK_TFS,
+                                                     "bf16"))
         if path == "stream-d16":   # the full-read streaming kernel on the same steps
             _, later_f, h_f = kernel_pass(KS, **dict(base_flags, full_sums=True))
             ch_f = int(h_f["changed"][1:KS].sum())
@@ -474,7 +476,7 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16x3+f32" if path == "global-mfma" else "f32",
+        "dtype": "bf16x3+f32" if path in ("global-mfma", "lds-inc") else "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "method": ("spherical" if args.spherical else "kmeans") +
                    ("+elkan-ti" if args.elkan else ""),
