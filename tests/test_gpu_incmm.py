@@ -97,3 +97,44 @@ def test_determinism_of_the_incremental_path():
             outs.append((a.cpu().numpy(), c.cpu().numpy(), ctx.centroids64()))
     for x, y in zip(outs[0], outs[1]):
         np.testing.assert_array_equal(x, y)
+
+
+@pytest.mark.parametrize("k,flags,path", [
+    (40, {}, "lds-inc"), (100, {}, "lds-inc"), (40, {"large_path": True}, "global-mfma"),
+], ids=["lds-inc-k40", "lds-inc-k100", "global-k40"])
+def test_split_bf16_band_resolves_close_pairs_like_the_oracle(k, flags, path):
+    # Centroids 2000 + U(-50, 50) in every coordinate: |x| |c| is about 1.3e8,
+    # so the split-bf16 error band of the expanded form (about 1.5e4 in
+    # squared distance) is wider than the gap between the two nearest
+    # centroids of most rows (rows placed near the bisector of two centroids:
+    # gaps of about 1e3, well above the 1e-5 relative near-tie mask of the
+    # comparison).  Such rows have several candidates and are decided on
+    # their direct-form distances; a band that dropped the nearest centroid
+    # would change assignments that the oracle fixes.
+    rng = np.random.default_rng(1500 + k)
+    d, n, T = 32, 40000 + 7, 3
+    C0 = (2000.0 + rng.uniform(-50.0, 50.0, size=(k, d))).astype(np.float32)
+    a = rng.integers(0, k, n)
+    b = (a + rng.integers(1, k, n)) % k
+    t = 0.5 + rng.uniform(-0.02, 0.02, n)
+    X = C0[a] + t[:, None] * (C0[b] - C0[a]) + rng.normal(0.0, 0.5, size=(n, d))
+    X = X.astype(np.float32)
+    print("k", k, "path", path, flush=True)
+    ref = oracle.lloyd(X, C0, T, 0.0, history=True)
+    _, best, second, _ = oracle.assign(X, C0)
+    xc = np.linalg.norm(X.astype(np.float64), axis=1) * np.linalg.norm(C0.astype(np.float64), axis=1).max()
+    band = 2.0 * (778.0 + 6.9 * d) * 2.0 ** -24 * xc           # the split terms of the bound
+    assert ((second - best) < band).mean() > 0.9               # most rows have several candidates
+    with km.KMeansMTI(_gpu(X), _gpu(C0), **flags) as ctx:
+        assert ctx.path() == path
+        for _ in range(T):
+            ctx.iterate()
+        got, c = ctx.get()
+        h = ctx.history()
+    info = check_assign(got.cpu().numpy(), ref["assign"], ref["best"], ref["second"], "final assignment")
+    check_centroids(c.cpu().numpy(), ref["C"], X, "final centroids")
+    if info["mismatch"] == 0:
+        np.testing.assert_array_equal(h["changed"], ref["changed"])
+    a_gen, c_gen, _ = km.run(_gpu(X), _gpu(C0), T, 0.0, generic=True)
+    np.testing.assert_array_equal(got.cpu().numpy(), a_gen.cpu().numpy())
+    np.testing.assert_array_equal(c.cpu().numpy(), c_gen.cpu().numpy())
