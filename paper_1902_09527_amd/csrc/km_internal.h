@@ -353,7 +353,8 @@ const void* first_kernel_symbol(int k);
 hipError_t launch_first(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, hipStream_t s);
 // Step t of the incremental kernel.  fused: the end of step t - 1 (an
 // incremental step of the same grid) has not run; every block computes it
-// first and block 0 stores it.  Else dv.C64 = the slot of C^t.
+// first and block 0 stores it.  Else dv.C64 = the slot of C^t.  dense: every
+// row is streamed (the dense form) instead of the survivors' gathered.
 hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, int fused, bool dense,
                       hipStream_t s);
 // End of step t (one block).  delta: the rows hold the moves of an
