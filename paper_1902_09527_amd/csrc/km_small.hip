@@ -181,6 +181,13 @@ struct Tables {
     int csu, kp, copies;
 };
 
+// Place of h(r, j) in the LDS table: rows of kSmallMaxK, the four 16-byte
+// chunks of row r permuted by (r / 4) mod 4 so that rows read at the same
+// chunk by different lanes fall on different banks; entries past k hold +inf.
+__device__ __forceinline__ int hpos(int r, int j) {
+    return r * kSmallMaxK + 4 * ((j >> 2) ^ ((r >> 2) & 3)) + (j & 3);
+}
+
 // Table pointers into LDS, and the block's sums and counters cleared.
 __device__ __forceinline__ Tables table_ptrs(const Dev& P, const SmallLds& lay) {
     Tables T;
@@ -212,7 +219,10 @@ __device__ __forceinline__ void fill_tables(const Dev& P, const Fused& F, const 
     const double* dhi = F.dhi + (int64_t)slot2(t) * k;
     const int nt = (int)blockDim.x;
     for (int i = tid; i < k * kD; i += nt) T.C[(i / kD) * kCR + i % kD] = P.C32[i];
-    for (int i = tid; i < k * k; i += nt) T.h[(i / k) * kSmallMaxK + i % k] = P.h[i];
+    for (int i = tid; i < k * kSmallMaxK; i += nt) {
+        const int r = i / kSmallMaxK, j = i % kSmallMaxK;
+        T.h[hpos(r, j)] = j < k ? P.h[r * k + j] : INFINITY;
+    }
     for (int i = tid; i < k; i += nt) {
         T.thr[i] = clause1_thr(P.s[i], dhi[i]);
         T.ec[i] = P.ec[i];
@@ -323,20 +333,19 @@ __device__ __forceinline__ int decide_direct(const Tables& T, const StepFlags& f
 // incumbent's (which tightens its bound u), then one per other centroid that
 // Clause 3 does not skip (u > half the distance from the incumbent to it).
 // vi: the incumbent's expanded-form value, E its error bound; b, ub: the
-// decision and its bound (u when b is the incumbent).
+// decision and its bound (u when b is the incumbent).  With h(inc, inc) = 0
+// and +inf past k, the count is the number of row entries below u (the
+// incumbent's own included when u > 0), at least one.
 template <int KC>
-__device__ __forceinline__ uint32_t mti_count(const float* h, float vi, int k, int inc, int b, float ub, float E) {
+__device__ __forceinline__ uint32_t mti_count(const float* h, float vi, int inc, int b, float ub, float E) {
     const float u = b == inc ? ub : sqrt_up(fmaxf(vi + E, 0.f)) * kUp;   // the incumbent's tightened bound
-    uint32_t nc = 1;
+    uint32_t nc = 0;
 #pragma unroll
     for (int j = 0; j < KC; j += 4) {
-        const f32x4 hv = *reinterpret_cast<const f32x4*>(h + inc * kSmallMaxK + j);
-        nc += (j < k && j != inc && !(u <= hv.x)) ? 1u : 0u;
-        nc += (j + 1 < k && j + 1 != inc && !(u <= hv.y)) ? 1u : 0u;
-        nc += (j + 2 < k && j + 2 != inc && !(u <= hv.z)) ? 1u : 0u;
-        nc += (j + 3 < k && j + 3 != inc && !(u <= hv.w)) ? 1u : 0u;
+        const f32x4 hv = *reinterpret_cast<const f32x4*>(h + hpos(inc, j));
+        nc += (u > hv.x ? 1u : 0u) + (u > hv.y ? 1u : 0u) + (u > hv.z ? 1u : 0u) + (u > hv.w ? 1u : 0u);
     }
-    return nc;
+    return nc > 1u ? nc : 1u;
 }
 
 template <int KC, bool INC_ONLY = false>
@@ -388,7 +397,7 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
         float vi = INFINITY;
 #pragma unroll
         for (int j = 0; j < KC; ++j) vi = j == inc ? V[j] : vi;
-        cn.comp += mti_count<KC>(T.h, vi, k, inc, b, ub, E);
+        cn.comp += mti_count<KC>(T.h, vi, inc, b, ub, E);
     } else {
         cn.comp += (uint32_t)k;
     }
@@ -587,7 +596,7 @@ __device__ float eos_finish(const Dev& P, const Fused& F, int t, const EosIn& in
 #pragma unroll
         for (int o = 8; o > 0; o >>= 1) sv = fminf(sv, __shfl_xor(sv, o));
         if (m < k && writer) P.h[j * k + m] = hv;
-        if (T) T->h[j * kSmallMaxK + m] = hv;
+        if (T) T->h[hpos(j, m)] = m < k ? hv : INFINITY;
         if (m == 0) {
             if (writer) P.s[j] = sv;
             if (T) T->thr[j] = clause1_thr(sv, hi);
@@ -1257,7 +1266,7 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
                 if (__popc(cm) == 1) {
                     const int b = __builtin_ctz(cm);
                     const float ub = sqrt_up(fmaxf(vmin + E, 0.f)) * kUp;
-                    cn.comp += fl.prune ? mti_count<KC>(t_h, fmaf(-2.f, row[inc], x2 + t_cn[inc]), k, inc, b, ub, E)
+                    cn.comp += fl.prune ? mti_count<KC>(t_h, fmaf(-2.f, row[inc], x2 + t_cn[inc]), inc, b, ub, E)
                                         : (uint32_t)k;
                     F.w[base + lane] = settle_state(ub, t_ddn[b], b);
                     if (b != inc) {
