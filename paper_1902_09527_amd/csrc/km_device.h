@@ -61,6 +61,12 @@ __device__ inline uint64_t fixed_bits(double v, double scale) {
     return (uint64_t)__double_as_longlong(fma(v, scale, kMagic));
 }
 
+// x subtracted from a 64-bit word in LDS, modulo 2^64 (one LDS subtract: no
+// negation of x first).
+__device__ __forceinline__ void lds_sub64(uint64_t* p, uint64_t x) {
+    __hip_atomic_fetch_sub(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
 // The end of step t (one thread): the progress word of a run's host loop, if
 // any, becomes t + 1, negated when the run stops (a system-scope store to
 // pinned host memory).

@@ -428,8 +428,7 @@ __global__ __launch_bounds__(kW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
                     atomicAdd(reinterpret_cast<unsigned long long*>(acc + b * AR + dim_of(q)),
                               (unsigned long long)v);
                     if (inc >= 0)
-                        atomicAdd(reinterpret_cast<unsigned long long*>(acc + inc * AR + dim_of(q)),
-                                  (unsigned long long)(0 - v));
+                        lds_sub64(acc + inc * AR + dim_of(q), v);
                 }
             }
         }

@@ -162,7 +162,10 @@ __device__ __forceinline__ void add_row(uint64_t* dst, const float (&x)[kD], dou
 #pragma unroll
     for (int m = 0; m < kD; ++m) {
         const uint64_t v = fixed_bits((double)x[m], qscale);
-        atomicAdd(reinterpret_cast<unsigned long long*>(dst + m), (unsigned long long)(neg ? 0 - v : v));
+        if (neg)
+            lds_sub64(dst + m, v);
+        else
+            atomicAdd(reinterpret_cast<unsigned long long*>(dst + m), (unsigned long long)v);
     }
 }
 
@@ -1301,13 +1304,12 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
                     const float xs[4] = {xv.x, xv.y, xv.z, xv.w};
                     unsigned long long* dn = reinterpret_cast<unsigned long long*>(
                         t_acc + cp * t_csu + (mm[g] & 255) * kSmallAccRow + 4 * qd);
-                    unsigned long long* dp = reinterpret_cast<unsigned long long*>(
-                        t_acc + cp * t_csu + (mm[g] >> 8) * kSmallAccRow + 4 * qd);
+                    uint64_t* dp = t_acc + cp * t_csu + (mm[g] >> 8) * kSmallAccRow + 4 * qd;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
                         const uint64_t v = fixed_bits((double)xs[e], P.qscale);
                         atomicAdd(dn + e, (unsigned long long)v);
-                        atomicAdd(dp + e, (unsigned long long)(0 - v));
+                        lds_sub64(dp + e, v);
                     }
                 }
             }
