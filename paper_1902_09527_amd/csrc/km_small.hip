@@ -417,6 +417,34 @@ __device__ __forceinline__ void settle_survivor(const Dev& P, const Fused& F, co
     }
 }
 
+// A wave's moved rows out of their old clusters' sums and into the new ones',
+// four lanes per row (chunk lane % 4 of the row) and sixteen rows per pass,
+// so that the LDS atomics run with most lanes active (the dense incremental
+// step, where a tile's 64 points move a few rows each).  Entry e of the list
+// is the row's index among `rows` (stride kCR floats) | new cluster << 6 |
+// old cluster << 10; nmov (at most 64) is uniform.
+__device__ __forceinline__ void move_rows(const Tables& T, const float* rows, const int* list, int nmov, int lane,
+                                          double qscale) {
+    const int c = lane & 3;
+    const int cp = (lane >> 2) & (kCopies - 1);
+    for (int base = 0; base < nmov; base += 16) {
+        const int e = base + (lane >> 2);
+        if (e < nmov) {
+            const int ent = list[e];
+            const f32x4 xv = *reinterpret_cast<const f32x4*>(rows + (ent & 63) * kCR + 4 * c);
+            uint64_t* dn = T.acc + cp * T.csu + ((ent >> 6) & 15) * kSmallAccRow + 4 * c;
+            uint64_t* dp = T.acc + cp * T.csu + ((ent >> 10) & 15) * kSmallAccRow + 4 * c;
+            const float xs[4] = {xv.x, xv.y, xv.z, xv.w};
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const uint64_t v = fixed_bits((double)xs[m], qscale);
+                atomicAdd(reinterpret_cast<unsigned long long*>(dn + m), (unsigned long long)v);
+                lds_sub64(dp + m, v);
+            }
+        }
+    }
+}
+
 // Block counters into the block's counter slot, then the block's sums (copies
 // added) into accumulation row blockIdx % kSmallRows.  skip_zero: only nonzero
 // words are added.
@@ -1178,10 +1206,9 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
         const float* __restrict__ t_h = T.h;
         const float* __restrict__ t_ddn = T.ddn;
         uint32_t* __restrict__ t_cnt = T.cnt;
-        uint64_t* __restrict__ t_acc = T.acc;
-        const int t_csu = T.csu, t_kp = T.kp;
+        const int t_kp = T.kp;
         float* dt = wg;            // the wave's tile: its staged rows
-        int* bt = wq_p;            // its move words: the first 64 queue entries
+        int* bt = wq_p;            // its moved-row list: the first 64 queue entries
         int* rl = wq_p + 64;       // its list: the rest of the queue
         int* ra = wq_a + 64;
         constexpr int rcap = kIncWaveQ - 64;
@@ -1228,7 +1255,7 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
             const int inc = state_cluster(ws);
             const bool surv = valid && !(fl.prune && state_value(ws) <= t_thr[inc]);
             cn.c1 += valid && !surv ? 1u : 0u;
-            int mv = -1;   // a moved point: new cluster | old cluster << 8
+            int mv = -1;   // a moved point: new cluster | old cluster << 4
             bool listed = false;
             if (surv) {
                 const float* row = dt + lane * kCR;
@@ -1277,7 +1304,7 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
                         const int cp = lane & (kCopies - 1);
                         atomicAdd(&t_cnt[cp * t_kp + b], 1u);
                         atomicAdd(&t_cnt[cp * t_kp + inc], 0xFFFFFFFFu);
-                        mv = b | (inc << 8);
+                        mv = b | inc << 4;
                     }
                 } else {
                     listed = true;
@@ -1290,28 +1317,19 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
                 ra[e] = inc;
             }
             nl += __popcll(lm);
-            bt[(lane & 15) * 4 + (lane >> 4)] = mv;
-            wave_sync();
             // The moved rows out of their old clusters' sums and into the new
-            // ones', by the lanes that hold them.
-            const int4 ms = *reinterpret_cast<const int4*>(bt + pl * 4);
-            const int mm[4] = {ms.x, ms.y, ms.z, ms.w};
-            const int cp = pl & (kCopies - 1);
+            // ones': the lanes that hold a moved row's chunks put them in its
+            // row of the tile (its products are spent), then four lanes per row.
+            const uint64_t mm = __ballot(mv >= 0);
+            if (mm) {
+                if (mv >= 0) bt[lanes_below(mm)] = lane | mv << 6;
+                wave_sync();
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                if (mm[g] >= 0) {
-                    const f32x4 xv = xb[g];
-                    const float xs[4] = {xv.x, xv.y, xv.z, xv.w};
-                    unsigned long long* dn = reinterpret_cast<unsigned long long*>(
-                        t_acc + cp * t_csu + (mm[g] & 255) * kSmallAccRow + 4 * qd);
-                    uint64_t* dp = t_acc + cp * t_csu + (mm[g] >> 8) * kSmallAccRow + 4 * qd;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const uint64_t v = fixed_bits((double)xs[e], P.qscale);
-                        atomicAdd(dn + e, (unsigned long long)v);
-                        lds_sub64(dp + e, v);
-                    }
-                }
+                for (int g = 0; g < 4; ++g)
+                    if ((mm >> (16 * g + pl)) & 1ull)
+                        *reinterpret_cast<f32x4*>(dt + (16 * g + pl) * kCR + 4 * qd) = xb[g];
+                wave_sync();
+                move_rows(T, dt, bt, __popcll(mm), lane, P.qscale);
             }
             wave_sync();   // the tile is read before the next one is written
         };
