@@ -189,6 +189,7 @@ struct km_ctx {
     int gim = 0, lds_im = 0;   // its grid and LDS
     int gi = 0, lds_inc = 0;   // grid and LDS of the incremental kernel
     int gf = 0, lds_first = 0;  // grid and LDS of the matrix-core first step (0: k_small runs it)
+    bool fuse_scan = false;     // that first step also finds the largest |x| (no set-up scan of X)
     int64_t enq = 0;      // steps enqueued so far
     km::Fused fz{};
     km::Large lg{};
@@ -318,6 +319,8 @@ int enqueue_iteration(km_ctx* c) {
             : t == 0 && c->gf ? km::launch_first(dv, c->fz, c->gf, c->lds_first, t, c->stream)
                               : km::launch_small(dv, c->fz, c->lds, t, c->stream);
         if (e != hipSuccess) return fail_ctx(c, hip_fail(e, "streaming step kernel"));
+        if (t == 0 && c->gf && c->fuse_scan && (e = km::launch_first_fix(dv, c->fz, c->gf, c->stream)) != hipSuccess)
+            return fail_ctx(c, hip_fail(e, "first step correction kernel"));
         if ((e = mark(1)) != hipSuccess || (e = mark(2)) != hipSuccess)
             return fail_ctx(c, hip_fail(e, "hipEventRecord"));
         if (!inc && (e = km::launch_small_finish(dv, c->fz, t, 0, c->stream)) != hipSuccess)
@@ -628,10 +631,15 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     zr.host = host_word;
     KM_HIP(km::launch_init_buffers(zr, cus, c->stream));
 
-    // Largest magnitude of X and C0 (and non-finite detection) -> fixed-point
-    // scales; with spherical k-means also the unit centroids and whether C0
-    // has a zero row.
-    KM_HIP(km::launch_absmax(X, n * d, C0, (int64_t)k * d, cus, scratch, c->stream));
+    // Largest magnitude of X (and non-finite detection), of C0 and of a fixed
+    // sample of X -> fixed-point scales; with spherical k-means also the unit
+    // centroids and whether C0 has a zero row.  The matrix-core first step of
+    // the stream path reads every row anyway: there it finds the largest |x|
+    // itself and X is not scanned here (not with KM_FLAG_VALIDATE, whose check
+    // needs it before any step, nor with spherical k-means).
+    c->fuse_scan = c->gf && !(c->flags & (KM_FLAG_VALIDATE | KM_FLAG_SPHERICAL));
+    if (c->small) c->fz.amax = c->fuse_scan ? scratch : nullptr;
+    KM_HIP(km::launch_absmax(X, c->fuse_scan ? 0 : n * d, C0, (int64_t)k * d, X, n, d, cus, scratch, c->stream));
     if (c->flags & KM_FLAG_SPHERICAL)
         KM_HIP(km::launch_set_centroids_unit(C0, v.C64, v.C32, v.ec, k, d, reinterpret_cast<int32_t*>(scratch + 4),
                                              c->stream));

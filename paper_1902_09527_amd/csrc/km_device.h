@@ -61,6 +61,52 @@ __device__ inline uint64_t fixed_bits(double v, double scale) {
     return (uint64_t)__double_as_longlong(fma(v, scale, kMagic));
 }
 
+// Set-up magnitude words (uint32 float bits of non-negative values): the
+// largest |x| over all of X (written by the first step itself when that step
+// is the first to read X), whether X or C0 holds a non-finite value, the
+// largest |c| of C0, a zero C0 row (spherical k-means), and the largest |x|
+// over a fixed sample of X.
+constexpr int kAmaxX = 0, kAmaxXBad = 1, kAmaxC = 2, kAmaxCBad = 3, kAmaxZeroRow = 4, kAmaxSample = 5;
+
+// The e with v <= 2^e (frexp's exponent; 0 for v = 0).
+__device__ inline int bound_exp(double v) {
+    int e = 0;
+    if (v > 0.0) (void)frexp(v, &e);
+    return e;
+}
+
+// Exponent of the bound on |x| that the exact sums are scaled for: 16 times
+// the sample's bound, unless X exceeds it.  A fixed sample and margin make
+// it known before X is read in nearly every case.
+__device__ inline int sum_exp(const uint32_t* amax) {
+    const int es = bound_exp((double)__uint_as_float(amax[kAmaxSample])) + 4;
+    const int ex = bound_exp((double)__uint_as_float(amax[kAmaxX]));
+    return ex <= es ? es : ex;
+}
+
+// Shift S of the coordinate sums for |x| <= 2^ex and n points:
+// |x 2^S| <= 2^50 per value and n 2^ex 2^S <= 2^61 overall, so every image
+// is exact and no sum can overflow.
+__device__ inline int sum_shift(int ex, int64_t n) {
+    int lgn = 0;
+    while (lgn < 64 && (1ull << lgn) < (uint64_t)n) ++lgn;
+    const int S = 61 - lgn - ex;
+    return S < 50 - ex ? S : 50 - ex;
+}
+
+// The scales for |x| <= 2^ex and |c| <= cmax: coordinate sums as above,
+// inertia the same for squared distances up to d (2 max(2^ex, cmax))^2.
+__device__ inline void put_scales(IterState* st, int ex, float cmax, int64_t n, int32_t d) {
+    const int S = sum_shift(ex, n);
+    const double xb = ldexp(1.0, ex);
+    const double am = xb > (double)cmax ? xb : (double)cmax;
+    const int SI = sum_shift(bound_exp((double)d * 4.0 * am * am), n);
+    st->qscale = ldexp(1.0, S);
+    st->qinv = ldexp(1.0, -S);
+    st->iscale = ldexp(1.0, SI);
+    st->iinv = ldexp(1.0, -SI);
+}
+
 // x subtracted from a 64-bit word in LDS, modulo 2^64 (one LDS subtract: no
 // negation of x first).
 __device__ __forceinline__ void lds_sub64(uint64_t* p, uint64_t x) {

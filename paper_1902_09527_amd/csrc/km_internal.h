@@ -278,6 +278,9 @@ struct Fused {
     double* dlo;          // 2 slots x k: the same rounded down
     float* dup;           // k: the latest D rounded up to float32
     float* ddn;           // k: the latest D rounded down to float32
+    // Set-up magnitude words when the first step scans X itself (the largest
+    // |x| is written by that step), else null.
+    uint32_t* amax = nullptr;
 };
 
 __host__ __device__ inline int slot3(int t) { return ((t % 3) + 3) % 3; }
@@ -351,6 +354,9 @@ hipError_t launch_small(const Dev& dv, const Fused& F, int lds_bytes, int t, hip
 int first_lds_bytes(int k);
 const void* first_kernel_symbol(int k);
 hipError_t launch_first(const Dev& dv, const Fused& F, int grid, int lds_bytes, int t, hipStream_t s);
+// After a first step that scanned X itself (F.amax set): the correction of
+// its sums when X exceeded the sample's bound (exits at once otherwise).
+hipError_t launch_first_fix(const Dev& dv, const Fused& F, int grid, hipStream_t s);
 // Step t of the incremental kernel.  fused: the end of step t - 1 (an
 // incremental step of the same grid) has not run; every block computes it
 // first and block 0 stores it.  Else dv.C64 = the slot of C^t.  dense: every
@@ -376,11 +382,14 @@ const void* large_mfma_symbol();   // the matrix-core kernel
 hipError_t large_set_attributes(int k, int d);
 
 // Kernel launchers (km_kernels.hip).  Each returns the launch status.
-// Largest |value| of a (na floats) and of b (nb floats) in one launch:
-// out[0], out[2] receive their float bits (atomic max) and out[1], out[3]
-// become nonzero for a non-finite value; out[0..3] must be zero before.
-hipError_t launch_absmax(const float* a, int64_t na, const float* b, int64_t nb, int cus, uint32_t* out,
-                         hipStream_t s);
+// Set-up magnitude words (out[kAmax*], zero before): the largest |value| of a
+// (na floats; na = 0 when the first step scans X itself), of b (nb floats)
+// and of a fixed sample of the n x d rows of x (kAbsSampleChunks chunks of
+// about 1024 values), as float bits (atomic max; NaN ignored, an infinite
+// value counted as the largest float), and whether a or b holds a
+// non-finite value.
+hipError_t launch_absmax(const float* a, int64_t na, const float* b, int64_t nb, const float* x, int64_t n,
+                         int32_t d, int cus, uint32_t* out, hipStream_t s);
 
 // Buffers cleared and the loop state written by one set-up launch.
 struct ZeroRanges {

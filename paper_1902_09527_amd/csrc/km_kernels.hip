@@ -68,18 +68,24 @@ __device__ inline float sqd_lds(const float* x, const float* c, int d) {
 // ---------------------------------------------------------------------------
 // Init helpers
 
-// Largest |value| (as float bits: non-negative floats order as their bits)
-// and whether any value is not finite, over one array: 16-byte loads when it
-// is 16-byte aligned, kAbsLoads in flight per lane, then the scalar tail.
+// Largest |value| (as float bits: non-negative floats order as their bits;
+// NaN ignored, an infinite value counted as the largest float) and whether
+// any value is not finite.
+__device__ __forceinline__ void absmax_take(float v, uint32_t& m, uint32_t& bad) {
+    const uint32_t u = __float_as_uint(v) & 0x7fffffffu;
+    bad |= u >= 0x7f800000u ? 1u : 0u;
+    const uint32_t c = u > 0x7f800000u ? 0u : (u < 0x7f7fffffu ? u : 0x7f7fffffu);
+    m = c > m ? c : m;
+}
+
+// absmax_take over one array: 16-byte loads when it is 16-byte aligned,
+// kAbsLoads in flight per lane, then the scalar tail.
 constexpr int kAbsLoads = 8;
 constexpr int kAbsBlocksPerCU = 1;
+constexpr int kAbsSampleChunks = 256;
 __device__ __forceinline__ void absmax_range(const float* __restrict__ p, int64_t count, int64_t t0,
                                              int64_t stride, uint32_t& m, uint32_t& bad) {
-    auto take = [&](float v) __attribute__((always_inline)) {
-        const uint32_t u = __float_as_uint(v) & 0x7fffffffu;
-        bad |= u >= 0x7f800000u ? 1u : 0u;
-        m = (u < 0x7f800000u && u > m) ? u : m;
-    };
+    auto take = [&](float v) __attribute__((always_inline)) { absmax_take(v, m, bad); };
     const int64_t nq = (reinterpret_cast<uintptr_t>(p) & 15) == 0 ? count / 4 : 0;
     const f32x4* __restrict__ q = reinterpret_cast<const f32x4*>(p);
     int64_t i = t0;
@@ -105,17 +111,29 @@ __device__ __forceinline__ void absmax_range(const float* __restrict__ p, int64_
     for (int64_t j = 4 * nq + t0; j < count; j += stride) take(p[j]);
 }
 
-// Two arrays in one launch: blocks [0, blocks_a) scan a, the others b.
-// out[0] / out[2]: max bits of a / b; out[1] / out[3]: nonzero if a / b
-// holds a non-finite value (all zero before the launch).
+// Three roles in one launch: blocks [0, blocks_a) scan a (out[kAmaxX],
+// out[kAmaxXBad]), the next blocks_b scan b (out[kAmaxC], out[kAmaxCBad]),
+// and the last kAbsSampleChunks blocks one chunk each of the sample of x:
+// rows [c n / 256, c n / 256 + max(1, 1024 / d)) of chunk c, cut at n
+// (out[kAmaxSample]).  All words zero before the launch.
 __global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ a, int64_t na, const float* __restrict__ b,
-                                               int64_t nb, int blocks_a, uint32_t* out) {
-    const bool first = (int)blockIdx.x < blocks_a;
-    const int blk = first ? (int)blockIdx.x : (int)blockIdx.x - blocks_a;
-    const int nblk = first ? blocks_a : (int)gridDim.x - blocks_a;
+                                               int64_t nb, int blocks_a, int blocks_b, const float* __restrict__ x,
+                                               int64_t n, int32_t d, uint32_t* out) {
+    const int bi = (int)blockIdx.x;
+    const int role = bi < blocks_a ? 0 : (bi < blocks_a + blocks_b ? 1 : 2);
     uint32_t m = 0, bad = 0;
-    absmax_range(first ? a : b, first ? na : nb, (int64_t)blk * blockDim.x + threadIdx.x,
-                 (int64_t)nblk * blockDim.x, m, bad);
+    if (role < 2) {
+        const int blk = role == 0 ? bi : bi - blocks_a;
+        const int nblk = role == 0 ? blocks_a : blocks_b;
+        absmax_range(role == 0 ? a : b, role == 0 ? na : nb, (int64_t)blk * blockDim.x + threadIdx.x,
+                     (int64_t)nblk * blockDim.x, m, bad);
+    } else {
+        const int64_t c = bi - blocks_a - blocks_b;
+        const int64_t r0 = c * n / kAbsSampleChunks;
+        const int64_t rows = d >= 1024 ? 1 : 1024 / d;
+        const int64_t r1 = r0 + rows < n ? r0 + rows : n;
+        for (int64_t j = r0 * d + threadIdx.x; j < r1 * d; j += blockDim.x) absmax_take(x[j], m, bad);
+    }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
         const uint32_t o = __shfl_xor(m, off);
@@ -123,8 +141,8 @@ __global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ a, int
     }
     const bool any_bad = __any(bad);
     if ((threadIdx.x & 63) == 0) {
-        atomicMax(out + (first ? 0 : 2), m);
-        if (any_bad) atomicOr(out + (first ? 1 : 3), 1u);
+        atomicMax(out + (role == 0 ? kAmaxX : (role == 1 ? kAmaxC : kAmaxSample)), m);
+        if (any_bad && role < 2) atomicOr(out + (role == 0 ? kAmaxXBad : kAmaxCBad), 1u);
     }
 }
 
@@ -152,30 +170,14 @@ __global__ __launch_bounds__(256) void k_init_buffers(ZeroRanges z) {
     }
 }
 
-// Fixed-point scales from the largest |x| and |c0|.  Coordinate sums:
-// |x * 2^S| <= 2^50 per value and n * max|x| * 2^S <= 2^61 overall, so every
-// image is exact and no sum can overflow.  Inertia: every squared distance
-// is at most d * (2 max(|x|, |c|))^2, with the same two limits.
+// Fixed-point scales (put_scales) from the set-up magnitude words.  When the
+// first step scans X itself, the X word is still zero here: the scales are
+// those of the sample's bound, and the end of the first step sets them again
+// from the word that step wrote (its sums corrected first when X exceeded
+// the bound).
 __global__ void k_set_scales(IterState* st, const uint32_t* absmax, int64_t n, int32_t d, int unit) {
     if (threadIdx.x != 0) return;
-    const float xmax = __uint_as_float(absmax[0]);
-    const float cmax = unit ? 1.0f : __uint_as_float(absmax[2]);
-    int lgn = 0;
-    while (lgn < 64 && (1ull << lgn) < (uint64_t)n) ++lgn;
-    int ex = 0;
-    if (xmax > 0.f) (void)frexp((double)xmax, &ex);   // xmax <= 2^ex
-    int S = 61 - lgn - ex;
-    if (S > 50 - ex) S = 50 - ex;
-    const double amax = xmax > cmax ? (double)xmax : (double)cmax;
-    const double dmax = (double)d * 4.0 * amax * amax;
-    int eD = 0;
-    if (dmax > 0.0) (void)frexp(dmax, &eD);
-    int SI = 61 - lgn - eD;
-    if (SI > 50 - eD) SI = 50 - eD;
-    st->qscale = ldexp(1.0, S);
-    st->qinv = ldexp(1.0, -S);
-    st->iscale = ldexp(1.0, SI);
-    st->iinv = ldexp(1.0, -SI);
+    put_scales(st, sum_exp(absmax), unit ? 1.0f : __uint_as_float(absmax[kAmaxC]), n, d);
 }
 
 __global__ void k_set_centroids(const float* __restrict__ C0, double* C64, float* C32, float* ec,
@@ -1293,16 +1295,18 @@ const void* assign_kernel_symbol(int variant) {
     }
 }
 
-hipError_t launch_absmax(const float* a, int64_t na, const float* b, int64_t nb, int cus, uint32_t* out,
-                         hipStream_t s) {
-    // a (X): up to kAbsBlocksPerCU blocks per CU; b (C0): a few blocks.
+hipError_t launch_absmax(const float* a, int64_t na, const float* b, int64_t nb, const float* x, int64_t n,
+                         int32_t d, int cus, uint32_t* out, hipStream_t s) {
+    if (na < 0 || nb < 1 || n < 1 || d < 1) return hipErrorInvalidValue;
+    // a (X): up to kAbsBlocksPerCU blocks per CU (none when na = 0); b (C0):
+    // a few blocks; then the sample's chunks.
     int64_t ba = (na + 4 * 4 * 256 - 1) / (4 * 4 * 256);
     if (ba > kAbsBlocksPerCU * (int64_t)cus) ba = kAbsBlocksPerCU * (int64_t)cus;
-    if (ba < 1) ba = 1;
     int64_t bb = (nb + 4 * 4 * 256 - 1) / (4 * 4 * 256);
     if (bb > 64) bb = 64;
     if (bb < 1) bb = 1;
-    hipLaunchKernelGGL(k_absmax, dim3((unsigned)(ba + bb)), dim3(256), 0, s, a, na, b, nb, (int)ba, out);
+    hipLaunchKernelGGL(k_absmax, dim3((unsigned)(ba + bb + kAbsSampleChunks)), dim3(256), 0, s, a, na, b, nb,
+                       (int)ba, (int)bb, x, n, d, out);
     return hipGetLastError();
 }
 

@@ -935,12 +935,14 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
 
+    float xm = 0.f;   // largest |x| of the rows this lane reads (NaN ignored)
     auto tile_body = [&](f32x4 (&xb)[4], int64_t tl) __attribute__((always_inline)) {
         const int64_t base = tl * 64;
         // 1. Products and partial norms of the four groups into the tile.
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const f32x4 xv = xb[g];
+            xm = fmaxf(xm, fmaxf(fmaxf(fabsf(xv.x), fabsf(xv.y)), fmaxf(fabsf(xv.z), fabsf(xv.w))));
             f32x4 dot = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], xv.x, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
             dot = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], xv.y, dot, 0, 0, 0);
             dot = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], xv.z, dot, 0, 0, 0);
@@ -1031,7 +1033,39 @@ __global__ __launch_bounds__(kTp) __attribute__((amdgpu_waves_per_eu(4))) void k
             prefetch(xB, tl + 3 * nw);
         }
     }
+    if (F.amax) {   // this step scans X for the set-up: its largest |x| (infinity as the largest float)
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) xm = fmaxf(xm, __shfl_xor(xm, off));
+        if (lane == 0) atomicMax(F.amax + kAmaxX, __float_as_uint(fminf(xm, FLT_MAX)));
+    }
     flush_block(P, F, T, cn, false, t);
+}
+
+// After a first step that scanned X itself: its sums were formed at the scale
+// of the sample's bound.  If X exceeded that bound, every row's image at the
+// final scale minus its image at that scale is added to the step's
+// accumulation rows, which then hold the sums at the final scale (exact
+// modulo 2^64, whatever the first images were); else nothing is done.
+__global__ __launch_bounds__(256) void k_first_fix(Dev P_, Fused F) {
+    const Dev P = with_scales(P_);
+    const int ex = sum_exp(F.amax);
+    if (ex == bound_exp((double)__uint_as_float(F.amax[kAmaxSample])) + 4) return;   // the bound held
+    __shared__ unsigned long long acc[kSmallMaxK * kD];
+    for (int i = threadIdx.x; i < kSmallMaxK * kD; i += blockDim.x) acc[i] = 0;
+    __syncthreads();
+    const double qt = ldexp(1.0, sum_shift(ex, P.n));
+    const int64_t total = P.n * kD;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int b = state_cluster(F.w[i / kD]);
+        const double x = (double)P.X[i];
+        atomicAdd(&acc[b * kD + (int)(i % kD)], (unsigned long long)(fixed_bits(x, qt) - fixed_bits(x, P.qscale)));
+    }
+    __syncthreads();
+    unsigned long long* row = reinterpret_cast<unsigned long long*>(
+        F.rows + ((int64_t)slot3(0) * kSmallRows + blockIdx.x % kSmallRows) * P.L);
+    for (int i = threadIdx.x; i < P.k * kD; i += blockDim.x)
+        if (acc[i]) atomicAdd(row + i, acc[i]);
 }
 
 // ---------------------------------------------------------------------------
@@ -1431,6 +1465,10 @@ __global__ __launch_bounds__(kIncThreads) __attribute__((amdgpu_waves_per_eu(4))
 // after an incremental step whose results are needed before the next step
 // (then the next step starts unfused).
 __global__ __launch_bounds__(kTp) void k_small_finish(Dev P_, Fused F, int t, int delta) {
+    if (t == 0 && F.amax) {   // the first step scanned X: the final scales from its word
+        if (threadIdx.x == 0) put_scales(P_.st, sum_exp(F.amax), __uint_as_float(F.amax[kAmaxC]), P_.n, P_.d);
+        __syncthreads();
+    }
     const Dev P = with_scales(P_);
     if (!P.st->active) return;   // step t did not run (the run had stopped)
     const float em = eos_finish(P, F, t, eos_load(P, F, t, delta != 0), true, km_smem, nullptr, nullptr);
@@ -1535,6 +1573,12 @@ hipError_t launch_inc(const Dev& dv, const Fused& F, int grid, int lds_bytes, in
     return hipGetLastError();
 }
 
+
+hipError_t launch_first_fix(const Dev& dv, const Fused& F, int grid, hipStream_t s) {
+    if (!F.amax || grid < 1 || dv.d != kD || dv.k > kSmallMaxK) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_first_fix, dim3(grid), dim3(256), 0, s, dv, F);
+    return hipGetLastError();
+}
 
 hipError_t launch_small_finish(const Dev& dv, const Fused& F, int t, int delta, hipStream_t s) {
     hipLaunchKernelGGL(k_small_finish, dim3(1), dim3(kTp), finish_lds(dv.d, dv.k), s, dv, F, t, delta);

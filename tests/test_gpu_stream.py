@@ -252,3 +252,48 @@ def test_dense_step_settles_listed_ties_like_the_oracle():
     assert (h["rechecks"][1:] >= 2 * m).all()                    # every tie row decided in float64
     np.testing.assert_array_equal(a, outs[1][0])
     np.testing.assert_array_equal(c64, outs[1][1])
+
+
+def _sample_rows(n, d):
+    # The fixed sample of X the set-up reads: 256 chunks, chunk c from row
+    # c * n // 256, max(1, 1024 // d) rows, cut at n.
+    rows = max(1, 1024 // d)
+    out = np.zeros(n, bool)
+    for c in range(256):
+        r0 = c * n // 256
+        out[r0:min(r0 + rows, n)] = True
+    return out
+
+
+@pytest.mark.parametrize("big", [3.0e3, 1.0e15], ids=["x3e3", "x1e15"])
+def test_first_step_corrects_its_sums_when_x_exceeds_the_sample_bound(big):
+    # The stream path's first step forms its sums at the scale of a bound 16
+    # times the largest |x| of the sample and finds the largest |x| itself; a
+    # row outside the sample beyond that bound makes it correct its sums to
+    # the final scale (for 1e15 the first images are not even exact integers).
+    # The results must be bitwise those of the same path after a full set-up
+    # scan (validate) and of the general kernels, and the oracle's for the
+    # moderate outlier.
+    n, k = 100_000 + 11, 8
+    X, C0 = synth.blobs(n, 16, k, seed=4242, spread=3.0, sigma=1.0)
+    samp = _sample_rows(n, 16)
+    out = np.flatnonzero(~samp)
+    r = int(out[len(out) // 2])
+    X = X.copy()
+    X[r, 3] = big
+    assert np.frexp(np.float32(big))[1] > np.frexp(np.abs(X[samp]).max())[1] + 4   # past the bound
+    print("outlier row", r, big, flush=True)
+    iters = 8
+    Xg, Cg = _gpu(X), _gpu(C0)
+    with km.KMeansMTI(Xg, Cg) as ctx:
+        assert ctx.path() == "stream-d16"
+    a, c, st = km.run(Xg, Cg, iters, 0.0)
+    a1, c1, st1 = km.run(Xg, Cg, iters, 0.0, validate=True)
+    a2, c2, _ = km.run(Xg, Cg, iters, 0.0, generic=True)
+    assert torch.equal(a, a1) and torch.equal(c, c1) and st["iterations"] == st1["iterations"]
+    assert torch.equal(a, a2) and torch.equal(c, c2)
+    if big < 1e6:
+        ref = oracle.lloyd(X, C0, iters, 0.0)
+        assert st["iterations"] == ref["iters"]
+        check_assign(a.cpu().numpy(), ref["assign"], ref["best"], ref["second"], "final assignment")
+        check_centroids(c.cpu().numpy(), ref["C"], X, "final centroids")
