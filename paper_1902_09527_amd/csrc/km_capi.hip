@@ -636,8 +636,10 @@ int init_impl(km_ctx* c, const float* X, int64_t n, int32_t d, int32_t k, const 
     // centroids and whether C0 has a zero row.  The matrix-core first step of
     // the stream path reads every row anyway: there it finds the largest |x|
     // itself and X is not scanned here (not with KM_FLAG_VALIDATE, whose check
-    // needs it before any step, nor with spherical k-means).
-    c->fuse_scan = c->gf && !(c->flags & (KM_FLAG_VALIDATE | KM_FLAG_SPHERICAL));
+    // needs it before any step, nor with spherical k-means; nor below
+    // kFuseScanMin values, where the scan costs less than the correction
+    // kernel's launch).
+    c->fuse_scan = c->gf && n * d >= km::kFuseScanMin && !(c->flags & (KM_FLAG_VALIDATE | KM_FLAG_SPHERICAL));
     if (c->small) c->fz.amax = c->fuse_scan ? scratch : nullptr;
     KM_HIP(km::launch_absmax(X, c->fuse_scan ? 0 : n * d, C0, (int64_t)k * d, X, n, d, cus, scratch, c->stream));
     if (c->flags & KM_FLAG_SPHERICAL)

@@ -245,6 +245,9 @@ constexpr int kIncWaves = 8;
 // points survive Clause 1 and nearly every 128-byte line of X holds a
 // survivor's row.
 constexpr int kIncDenseSteps = 1;
+// The stream path's first step takes the largest |x| itself (no set-up scan
+// of X) from this many values of X on.
+constexpr int64_t kFuseScanMin = int64_t(1) << 20;
 constexpr int kIncThreads = 64 * kIncWaves;
 constexpr int kIncWaveTile = 1024;
 constexpr int kIncTile = 4 * kIncWaveTile;

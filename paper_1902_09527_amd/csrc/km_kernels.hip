@@ -113,12 +113,14 @@ __device__ __forceinline__ void absmax_range(const float* __restrict__ p, int64_
 
 // Three roles in one launch: blocks [0, blocks_a) scan a (out[kAmaxX],
 // out[kAmaxXBad]), the next blocks_b scan b (out[kAmaxC], out[kAmaxCBad]),
-// and the last kAbsSampleChunks blocks one chunk each of the sample of x:
-// rows [c n / 256, c n / 256 + max(1, 1024 / d)) of chunk c, cut at n
-// (out[kAmaxSample]).  All words zero before the launch.
+// and the last blocks one chunk each of the sample of x: rows
+// [c n / 256, c n / 256 + max(1, 1024 / d)) of chunk c < kAbsSampleChunks,
+// cut at n (out[kAmaxSample]).  whole: the sample holds every row (n <= 256
+// rows per chunk) and a is x: no sample blocks, the scan of a writes both
+// words.  All words zero before the launch.
 __global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ a, int64_t na, const float* __restrict__ b,
                                                int64_t nb, int blocks_a, int blocks_b, const float* __restrict__ x,
-                                               int64_t n, int32_t d, uint32_t* out) {
+                                               int64_t n, int32_t d, int whole, uint32_t* out) {
     const int bi = (int)blockIdx.x;
     const int role = bi < blocks_a ? 0 : (bi < blocks_a + blocks_b ? 1 : 2);
     uint32_t m = 0, bad = 0;
@@ -132,7 +134,17 @@ __global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ a, int
         const int64_t r0 = c * n / kAbsSampleChunks;
         const int64_t rows = d >= 1024 ? 1 : 1024 / d;
         const int64_t r1 = r0 + rows < n ? r0 + rows : n;
-        for (int64_t j = r0 * d + threadIdx.x; j < r1 * d; j += blockDim.x) absmax_take(x[j], m, bad);
+        // four loads per lane in flight, then their values
+        for (int64_t j0 = r0 * d; j0 < r1 * d; j0 += 4 * (int64_t)blockDim.x) {
+            float v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t j = j0 + threadIdx.x + (int64_t)u * blockDim.x;
+                v[u] = j < r1 * d ? x[j] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) absmax_take(v[u], m, bad);
+        }
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
@@ -142,6 +154,7 @@ __global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ a, int
     const bool any_bad = __any(bad);
     if ((threadIdx.x & 63) == 0) {
         atomicMax(out + (role == 0 ? kAmaxX : (role == 1 ? kAmaxC : kAmaxSample)), m);
+        if (role == 0 && whole) atomicMax(out + kAmaxSample, m);
         if (any_bad && role < 2) atomicOr(out + (role == 0 ? kAmaxXBad : kAmaxCBad), 1u);
     }
 }
@@ -1305,8 +1318,10 @@ hipError_t launch_absmax(const float* a, int64_t na, const float* b, int64_t nb,
     int64_t bb = (nb + 4 * 4 * 256 - 1) / (4 * 4 * 256);
     if (bb > 64) bb = 64;
     if (bb < 1) bb = 1;
-    hipLaunchKernelGGL(k_absmax, dim3((unsigned)(ba + bb + kAbsSampleChunks)), dim3(256), 0, s, a, na, b, nb,
-                       (int)ba, (int)bb, x, n, d, out);
+    const int64_t rows = d >= 1024 ? 1 : 1024 / d;
+    const int whole = na == n * d && a == x && n <= kAbsSampleChunks * rows ? 1 : 0;
+    hipLaunchKernelGGL(k_absmax, dim3((unsigned)(ba + bb + (whole ? 0 : kAbsSampleChunks))), dim3(256), 0, s, a, na,
+                       b, nb, (int)ba, (int)bb, x, n, d, whole, out);
     return hipGetLastError();
 }
 
