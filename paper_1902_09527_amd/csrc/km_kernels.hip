@@ -82,7 +82,7 @@ __device__ __forceinline__ void absmax_take(float v, uint32_t& m, uint32_t& bad)
 // kAbsLoads in flight per lane, then the scalar tail.
 constexpr int kAbsLoads = 8;
 constexpr int kAbsBlocksPerCU = 1;
-constexpr int kAbsSampleChunks = 256;
+constexpr int kAbsSampleChunks = 16;
 __device__ __forceinline__ void absmax_range(const float* __restrict__ p, int64_t count, int64_t t0,
                                              int64_t stride, uint32_t& m, uint32_t& bad) {
     auto take = [&](float v) __attribute__((always_inline)) { absmax_take(v, m, bad); };
@@ -114,10 +114,10 @@ __device__ __forceinline__ void absmax_range(const float* __restrict__ p, int64_
 // Three roles in one launch: blocks [0, blocks_a) scan a (out[kAmaxX],
 // out[kAmaxXBad]), the next blocks_b scan b (out[kAmaxC], out[kAmaxCBad]),
 // and the last blocks one chunk each of the sample of x: rows
-// [c n / 256, c n / 256 + max(1, 1024 / d)) of chunk c < kAbsSampleChunks,
-// cut at n (out[kAmaxSample]).  whole: the sample holds every row (n <= 256
-// rows per chunk) and a is x: no sample blocks, the scan of a writes both
-// words.  All words zero before the launch.
+// [c n / C, c n / C + max(1, 1024 / d)) of chunk c < C = kAbsSampleChunks,
+// cut at n (out[kAmaxSample]).  whole: the sample holds every row (n <= C
+// times the rows per chunk) and a is x: no sample blocks, the scan of a
+// writes both words.  All words zero before the launch.
 __global__ __launch_bounds__(256) void k_absmax(const float* __restrict__ a, int64_t na, const float* __restrict__ b,
                                                int64_t nb, int blocks_a, int blocks_b, const float* __restrict__ x,
                                                int64_t n, int32_t d, int whole, uint32_t* out) {

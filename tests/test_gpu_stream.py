@@ -255,12 +255,12 @@ def test_dense_step_settles_listed_ties_like_the_oracle():
 
 
 def _sample_rows(n, d):
-    # The fixed sample of X the set-up reads: 256 chunks, chunk c from row
-    # c * n // 256, max(1, 1024 // d) rows, cut at n.
+    # The fixed sample of X the set-up reads: 16 chunks, chunk c from row
+    # c * n // 16, max(1, 1024 // d) rows, cut at n.
     rows = max(1, 1024 // d)
     out = np.zeros(n, bool)
-    for c in range(256):
-        r0 = c * n // 256
+    for c in range(16):
+        r0 = c * n // 16
         out[r0:min(r0 + rows, n)] = True
     return out
 
